@@ -1,0 +1,205 @@
+/*
+ * gevo.h -- C-ABI of libgevo: population-batched fitness evaluation on one
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The method is GEVO-ML (Liou, Forrest, Wu; arXiv 2310.10211).  Its run time is
+ * dominated by fitness evaluation (section 4.3): every individual of the
+ * evolving population is either retrained on the dataset, recording training
+ * time and model error (training workload), or run over the dataset as a
+ * pretrained model, recording inference time and error (prediction workload).
+ * The two objectives are time and error (section 4.3).  The paper's training
+ * model is a two-layer fully-connected net trained by mini-batch SGD whose
+ * output gradient is prediction minus label, reduced over the batch, scaled by
+ * 1/batch, multiplied by the learning rate and subtracted from weights and
+ * biases (section 6.2).  Its discovered mutations act like a changed learning
+ * rate (section 6.2) and like pruned parameters (abstract, section 2), so an
+ * individual here is the original model with its own learning rate and its own
+ * Bernoulli weight-pruning mask.
+ *
+ * Conventions for every entry point
+ *  - Device memory belongs to the caller: datasets, the workspace and the HIP
+ *    stream are passed in; the library never allocates or frees device memory.
+ *    Host arrays passed in or out belong to the caller.
+ *  - Arguments are validated on the host before any HIP call; a bad argument
+ *    returns an error code and launches nothing.
+ *  - Work is enqueued asynchronously on the handle's stream.  Device faults are
+ *    sticky and are reported by the next synchronising call (gevo_pop_scores,
+ *    gevo_pop_export) as GEVO_E_HIP.
+ *  - A handle is not thread-safe; distinct handles are independent.
+ *
+ * Numerics
+ *  - Weights of layer l are d_{l-1} x d_l ("in x out") in every host-visible
+ *    (canonical) array; the device layout is private.
+ *  - GEVO_F32: fp32 operands, fp32 accumulation.  GEVO_BF16: bf16 GEMM operands
+ *    (input rows, weights rounded from the fp32 master each step, hidden
+ *    activations after ReLU, gradients), fp32 accumulation, fp32 master
+ *    weights, fp32 logits/softmax/loss/bias gradients/update.  Rounding to bf16
+ *    is round-to-nearest-even.
+ *  - Random draws use Philox4x32-10 (Salmon et al., SC'11) with key = (seed low
+ *    32 bits, seed high 32 bits) and counter (c0, c1, c2, c3) = (block, layer
+ *    index l-1, variant or epoch, stream); stream 1 learning rate, 2 density,
+ *    3 mask, 4 initial weights, 5 weight noise, 6 data order.  A uniform u24 is
+ *    the top 24 bits of a word.  Weight (k -> n) of layer l has element index
+ *    e = n * d_{l-1} + k.  Learning rate: exp(ln lo + u (ln hi - ln lo)) in
+ *    fp64, rounded to fp32 (block 0, word 0).  Density: list[v mod n] or
+ *    lo + u (hi - lo).  Mask: keep <=> u24 < round_half_away(rho 2^24) (block
+ *    e/4, word e%4).  Xavier init, shared by all variants (the original model):
+ *    (2u - 1) * fl32(sqrt(6 / (d_{l-1} + d_l))) (block e/4, word e%4, variant
+ *    field 0).  Weight noise: eps = sqrt(-2 ln u1) cos(2 pi u2) with
+ *    u1 = (u24 + 1) 2^-24 and u2 = u24 2^-24 from words 2(e%2), 2(e%2)+1 of block
+ *    e/2.  Data order of epoch e: Fisher-Yates from the last index down, swap
+ *    index j = (r * (i + 1)) >> 32 with r word i%4 of block i/4 (variant field =
+ *    epoch, layer field 0); one order shared by all variants.
+ *  - Masked weights are exactly +0.0 and stay so (the update is a select).
+ */
+#ifndef GEVO_H
+#define GEVO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GEVO_ABI_VERSION 1u
+#define GEVO_MAX_LAYERS 3u      /* supported depth of the net (hidden layers + output) */
+#define GEVO_MAX_CLASSES 32u    /* d_L */
+#define GEVO_MAX_BATCH 256u
+#define GEVO_MAX_WIDTH 8192u    /* any d_l */
+
+typedef enum {
+  GEVO_OK = 0,
+  GEVO_E_ARG = -1,          /* NULL pointer, zero size, bad enum */
+  GEVO_E_SHAPE = -2,        /* inconsistent dimensions / sizes */
+  GEVO_E_WORKSPACE = -3,    /* workspace too small or misaligned (256 B) */
+  GEVO_E_ORDER = -4,        /* call out of sequence (epoch order, predict before init) */
+  GEVO_E_HIP = -5,          /* a HIP runtime call failed (sticky device error) */
+  GEVO_E_UNSUPPORTED = -6   /* valid but beyond this build's limits */
+} gevo_status;
+
+typedef enum { GEVO_F32 = 0, GEVO_BF16 = 1 } gevo_dtype;
+typedef enum { GEVO_INIT_XAVIER = 0, GEVO_INIT_BASE_NOISE = 1 } gevo_init;
+
+/*
+ * Population description.  n_layers = L (1..GEVO_MAX_LAYERS); dims[0..L] are
+ * the layer widths d_0 (input) .. d_L (classes).  Learning rates are
+ * log-uniform in [lr_lo, lr_hi) (lr_lo == lr_hi: fixed).  Densities come from
+ * dens_list (host array, cycled by variant index) if n_dens_list > 0, else
+ * uniform in [dens_lo, dens_hi].  init = GEVO_INIT_BASE_NOISE multiplies each
+ * weight of the base model by (1 + noise_rel_std * eps); the base model is
+ * base_params (host array, canonical layout: per layer W_l in x out then b_l)
+ * or, if NULL, the seeded Xavier model.  n_train may be 0 (prediction only).
+ */
+typedef struct {
+  uint32_t abi_version;               /* must be GEVO_ABI_VERSION */
+  uint32_t n_layers;
+  uint32_t dims[GEVO_MAX_LAYERS + 1];
+  uint32_t P;                         /* variants, >= 1 */
+  uint32_t batch;                     /* B, 1..GEVO_MAX_BATCH */
+  gevo_dtype dtype;
+  uint64_t seed;
+  float lr_lo, lr_hi;
+  float dens_lo, dens_hi;
+  const float* dens_list;
+  uint32_t n_dens_list;
+  gevo_init init;
+  const float* base_params;
+  float noise_rel_std;
+  int64_t n_train;                    /* rows of the training split (0 allowed) */
+  int64_t n_test;                     /* rows of the test split (>= 1) */
+} gevo_pop_config;
+
+typedef struct gevo_pop gevo_pop;     /* opaque handle */
+
+/* Bytes of device workspace gevo_pop_init needs for cfg (always a multiple of 256). */
+gevo_status gevo_pop_workspace_bytes(const gevo_pop_config* cfg, size_t* bytes);
+
+/*
+ * Create a population (section 4: copies of the original model carrying random
+ * edits; here a per-variant learning rate and pruning mask).  d_ws: device
+ * workspace of at least gevo_pop_workspace_bytes bytes, 256-byte aligned, owned
+ * by the caller and untouched by it while the handle lives.  Datasets: device
+ * arrays, row-major float32 [n][d_0] features and int32 labels in
+ * [0, d_L); they must outlive the handle (train pointers may be NULL when
+ * n_train == 0).  hip_stream: a hipStream_t (NULL = default stream).
+ * Enqueues mask generation, weight init and dataset conversion.
+ */
+gevo_status gevo_pop_init(const gevo_pop_config* cfg, void* d_ws, size_t ws_bytes,
+                          const float* d_train_x, const int32_t* d_train_y,
+                          const float* d_test_x, const int32_t* d_test_y,
+                          void* hip_stream, gevo_pop** out);
+
+/*
+ * Training workload of section 4.3 / mini-batch SGD of section 6.2: one epoch
+ * over the training split in the epoch's data order, batches of B rows (the
+ * short last batch is kept and scaled by fl32(1/b)).  Epochs must be called as
+ * 0, 1, 2, ... (GEVO_E_ORDER otherwise).  Per variant the epoch's mean
+ * cross-entropy (taken before each step's update) and the wall time of the
+ * call (HIP events) are recorded for gevo_pop_scores.
+ */
+gevo_status gevo_pop_train_epoch(gevo_pop* pop, uint32_t epoch);
+
+/*
+ * Steps [step_begin, step_end) of epoch `epoch`; a sequence of such calls
+ * covering 0..T-1 in order is bit-identical to gevo_pop_train_epoch.  The
+ * first call of an epoch must start at step 0, later calls where the previous
+ * one ended.
+ */
+gevo_status gevo_pop_train_steps(gevo_pop* pop, uint32_t epoch, uint32_t step_begin, uint32_t step_end);
+
+/* Number of SGD steps per epoch, ceil(n_train / B). */
+gevo_status gevo_pop_steps_per_epoch(const gevo_pop* pop, uint32_t* steps);
+
+/*
+ * Prediction workload of section 4.3 (and the held-out check of the fittest
+ * individual): forward pass of every variant over the test split; records
+ * the mean cross-entropy and the accuracy (argmax, lowest index on ties, a
+ * NaN logit counts as a miss) per variant, and the call's wall time.
+ */
+gevo_status gevo_pop_predict(gevo_pop* pop);
+
+/*
+ * Fitness of every variant (section 4.3: error and time).  Synchronises the
+ * stream.  Host arrays of P entries, any may be NULL: mean training CE of the
+ * last trained epoch (NaN if never trained), training accuracy of that epoch,
+ * mean test CE and test accuracy in [0,1] of the last predict (NaN before),
+ * and time_s = wall time of the last train/predict call divided by P
+ * (variants share every kernel, so time is amortised).
+ */
+gevo_status gevo_pop_scores(gevo_pop* pop, float* train_loss, float* train_acc, float* test_loss,
+                            float* test_acc, float* time_s);
+
+/* Wall time in seconds of the last train_epoch / train_steps / predict call. */
+gevo_status gevo_pop_last_time(gevo_pop* pop, double* seconds);
+
+/*
+ * Variant v's state in canonical layout (synchronises the stream):
+ * params_out (host float, per layer W_l in x out then b_l; may be NULL),
+ * mask_out (host uint8 0/1 per weight, same order as the weights; may be NULL),
+ * lr_out, density_out (may be NULL).
+ */
+gevo_status gevo_pop_export(gevo_pop* pop, uint32_t v, float* params_out, uint8_t* mask_out,
+                            float* lr_out, float* density_out);
+
+/* Overwrite variant v's parameters from a host array in canonical layout
+ * (masked weights are forced to +0).  Synchronous. */
+gevo_status gevo_pop_import(gevo_pop* pop, uint32_t v, const float* params);
+
+/* Labels of the current epoch in the order the steps consume them (n_train
+ * entries; synchronises).  Exposes the data order for exactness checks. */
+gevo_status gevo_pop_epoch_labels(gevo_pop* pop, int32_t* labels_out, int64_t n);
+
+/* Host-side data order of epoch `epoch` over n rows (definition above). */
+gevo_status gevo_epoch_permutation(uint64_t seed, uint32_t epoch, uint32_t n, uint32_t* out);
+
+/* Release the handle (does not free the caller's device memory). */
+void gevo_pop_destroy(gevo_pop* pop);
+
+const char* gevo_status_str(gevo_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GEVO_H */

@@ -1,0 +1,261 @@
+"""Python binding of libgevo: population-batched fitness evaluation on MI355X.
+
+Argument marshalling only.  Every step of evaluation runs in the HIP kernels of
+``libgevo.so`` behind the C-ABI declared in ``include/gevo.h``; PyTorch is used
+for device memory (datasets, workspace) and the stream.  There is no CPU
+fallback: without the built library, importing ``Population`` fails loudly.
+
+GEVO-ML (arXiv 2310.10211) evaluates every individual of its population by
+retraining its model on the dataset or by running it over the dataset, scoring
+time and error (section 4.3).  A ``Population`` holds P variants of a small
+fully-connected classifier, each the original model with its own learning rate
+and weight-pruning mask (the effects the paper attributes to its mutations,
+section 6.2 and the abstract).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+__all__ = ["Population", "lib", "epoch_permutation", "GevoError", "config_struct", "workspace_bytes"]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgevo.so")
+
+GEVO_ABI_VERSION = 1
+MAX_LAYERS = 3
+F32, BF16 = 0, 1
+INIT_XAVIER, INIT_BASE_NOISE = 0, 1
+
+EXPORTED = [
+    "gevo_pop_workspace_bytes", "gevo_pop_init", "gevo_pop_train_epoch", "gevo_pop_train_steps",
+    "gevo_pop_steps_per_epoch", "gevo_pop_predict", "gevo_pop_scores", "gevo_pop_last_time",
+    "gevo_pop_export", "gevo_pop_import", "gevo_pop_epoch_labels", "gevo_epoch_permutation",
+    "gevo_pop_destroy", "gevo_status_str",
+]
+
+
+class GevoError(RuntimeError):
+    pass
+
+
+class GevoPopConfig(ctypes.Structure):
+    _fields_ = [
+        ("abi_version", ctypes.c_uint32),
+        ("n_layers", ctypes.c_uint32),
+        ("dims", ctypes.c_uint32 * (MAX_LAYERS + 1)),
+        ("P", ctypes.c_uint32),
+        ("batch", ctypes.c_uint32),
+        ("dtype", ctypes.c_int),
+        ("seed", ctypes.c_uint64),
+        ("lr_lo", ctypes.c_float),
+        ("lr_hi", ctypes.c_float),
+        ("dens_lo", ctypes.c_float),
+        ("dens_hi", ctypes.c_float),
+        ("dens_list", ctypes.POINTER(ctypes.c_float)),
+        ("n_dens_list", ctypes.c_uint32),
+        ("init", ctypes.c_int),
+        ("base_params", ctypes.POINTER(ctypes.c_float)),
+        ("noise_rel_std", ctypes.c_float),
+        ("n_train", ctypes.c_int64),
+        ("n_test", ctypes.c_int64),
+    ]
+
+
+_lib = None
+
+
+def lib():
+    """Load libgevo.so (built by __graft_entry__.build()); raises if missing."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() (hipcc, gfx950)")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, u32, i64 = ctypes.c_void_p, ctypes.c_uint32, ctypes.c_int64
+        f32p = ctypes.POINTER(ctypes.c_float)
+        cfgp = ctypes.POINTER(GevoPopConfig)
+        L.gevo_pop_workspace_bytes.argtypes = [cfgp, ctypes.POINTER(ctypes.c_size_t)]
+        L.gevo_pop_init.argtypes = [cfgp, vp, ctypes.c_size_t, vp, vp, vp, vp, vp, ctypes.POINTER(vp)]
+        L.gevo_pop_train_epoch.argtypes = [vp, u32]
+        L.gevo_pop_train_steps.argtypes = [vp, u32, u32, u32]
+        L.gevo_pop_steps_per_epoch.argtypes = [vp, ctypes.POINTER(u32)]
+        L.gevo_pop_predict.argtypes = [vp]
+        L.gevo_pop_scores.argtypes = [vp, f32p, f32p, f32p, f32p, f32p]
+        L.gevo_pop_last_time.argtypes = [vp, ctypes.POINTER(ctypes.c_double)]
+        L.gevo_pop_export.argtypes = [vp, u32, f32p, ctypes.POINTER(ctypes.c_uint8), f32p, f32p]
+        L.gevo_pop_import.argtypes = [vp, u32, f32p]
+        L.gevo_pop_epoch_labels.argtypes = [vp, ctypes.POINTER(ctypes.c_int32), i64]
+        L.gevo_epoch_permutation.argtypes = [ctypes.c_uint64, u32, u32, ctypes.POINTER(u32)]
+        L.gevo_pop_destroy.argtypes = [vp]
+        L.gevo_pop_destroy.restype = None
+        L.gevo_status_str.argtypes = [ctypes.c_int]
+        L.gevo_status_str.restype = ctypes.c_char_p
+        for name in EXPORTED:
+            if name not in ("gevo_pop_destroy", "gevo_status_str"):
+                getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _check(rc, what):
+    if rc != 0:
+        raise GevoError(f"{what}: {lib().gevo_status_str(rc).decode()} ({rc})")
+
+
+def _fp(a):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+
+
+def config_struct(cfg: dict, n_train: int, n_test: int, keep: list):
+    """GevoPopConfig from a workload dict (keys: dims, P, batch, dtype, seed, lr,
+    dens or dens_list, init, noise_std, base_params)."""
+    c = GevoPopConfig()
+    dims = list(cfg["dims"])
+    c.abi_version = GEVO_ABI_VERSION
+    c.n_layers = len(dims) - 1
+    for i in range(min(len(dims), MAX_LAYERS + 1)):
+        c.dims[i] = dims[i]
+    c.P = cfg["P"]
+    c.batch = cfg.get("batch", 1)
+    c.dtype = BF16 if cfg.get("dtype", "f32") == "bf16" else F32
+    c.seed = cfg["seed"]
+    c.lr_lo, c.lr_hi = cfg.get("lr", (0.0, 0.0))
+    if cfg.get("dens_list"):
+        dl = np.ascontiguousarray(np.asarray(cfg["dens_list"], np.float32))
+        keep.append(dl)
+        c.dens_list = _fp(dl)
+        c.n_dens_list = dl.size
+    else:
+        c.dens_lo, c.dens_hi = cfg.get("dens", (1.0, 1.0))
+    c.init = INIT_BASE_NOISE if cfg.get("init", "xavier") == "base_noise" else INIT_XAVIER
+    if cfg.get("base_params") is not None:
+        bp = np.ascontiguousarray(np.asarray(cfg["base_params"], np.float32))
+        keep.append(bp)
+        c.base_params = _fp(bp)
+    c.noise_rel_std = cfg.get("noise_std", 0.0)
+    c.n_train = n_train
+    c.n_test = n_test
+    return c
+
+
+def workspace_bytes(cfg: dict, n_train: int, n_test: int) -> int:
+    keep = []
+    c = config_struct(cfg, n_train, n_test, keep)
+    out = ctypes.c_size_t()
+    _check(lib().gevo_pop_workspace_bytes(ctypes.byref(c), ctypes.byref(out)), "gevo_pop_workspace_bytes")
+    return out.value
+
+
+def epoch_permutation(seed: int, epoch: int, n: int) -> np.ndarray:
+    out = np.zeros(n, np.uint32)
+    _check(lib().gevo_epoch_permutation(seed, epoch, n, out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32))),
+           "gevo_epoch_permutation")
+    return out
+
+
+def param_count(dims) -> int:
+    return sum(dims[l - 1] * dims[l] + dims[l] for l in range(1, len(dims)))
+
+
+class Population:
+    """P variants on one GPU; all device memory comes from torch."""
+
+    def __init__(self, cfg: dict, x_train, y_train, x_test, y_test, device="cuda", stream=None):
+        import torch
+        self.torch = torch
+        self.cfg = dict(cfg)
+        self.dims = list(cfg["dims"])
+        self.P = cfg["P"]
+        dev = torch.device(device)
+
+        def dt(a, dtype):
+            t = torch.as_tensor(a)
+            return t.to(device=dev, dtype=dtype).contiguous()
+
+        self.x_train = dt(x_train, torch.float32) if x_train is not None and len(x_train) else None
+        self.y_train = dt(y_train, torch.int32) if y_train is not None and len(y_train) else None
+        self.x_test = dt(x_test, torch.float32)
+        self.y_test = dt(y_test, torch.int32)
+        n_train = 0 if self.x_train is None else self.x_train.shape[0]
+        n_test = self.x_test.shape[0]
+        if self.x_train is not None:
+            assert self.x_train.shape == (n_train, self.dims[0]) and self.y_train.shape == (n_train,)
+        assert self.x_test.shape == (n_test, self.dims[0]) and self.y_test.shape == (n_test,)
+        self.n_train, self.n_test = n_train, n_test
+        self._keep = []
+        self._cfg = config_struct(cfg, n_train, n_test, self._keep)
+        nbytes = ctypes.c_size_t()
+        _check(lib().gevo_pop_workspace_bytes(ctypes.byref(self._cfg), ctypes.byref(nbytes)),
+               "gevo_pop_workspace_bytes")
+        self.workspace = torch.empty(max(nbytes.value, 256), dtype=torch.uint8, device=dev)
+        self.stream = stream if stream is not None else torch.cuda.current_stream(dev)
+        h = ctypes.c_void_p()
+        ptr = lambda t: None if t is None else ctypes.c_void_p(t.data_ptr())
+        _check(lib().gevo_pop_init(ctypes.byref(self._cfg), ctypes.c_void_p(self.workspace.data_ptr()),
+                                   nbytes.value, ptr(self.x_train), ptr(self.y_train), ptr(self.x_test),
+                                   ptr(self.y_test), ctypes.c_void_p(self.stream.cuda_stream), ctypes.byref(h)),
+               "gevo_pop_init")
+        self._h = h
+
+    # --------------------------------------------------------------- workloads
+    def train_epoch(self, epoch: int):
+        _check(lib().gevo_pop_train_epoch(self._h, epoch), "gevo_pop_train_epoch")
+
+    def train_steps(self, epoch: int, s0: int, s1: int):
+        _check(lib().gevo_pop_train_steps(self._h, epoch, s0, s1), "gevo_pop_train_steps")
+
+    @property
+    def steps_per_epoch(self) -> int:
+        out = ctypes.c_uint32()
+        _check(lib().gevo_pop_steps_per_epoch(self._h, ctypes.byref(out)), "gevo_pop_steps_per_epoch")
+        return out.value
+
+    def predict(self):
+        _check(lib().gevo_pop_predict(self._h), "gevo_pop_predict")
+
+    def scores(self) -> dict:
+        arrs = {k: np.zeros(self.P, np.float32) for k in ("train_loss", "train_acc", "test_loss", "test_acc", "time_s")}
+        _check(lib().gevo_pop_scores(self._h, *[_fp(arrs[k]) for k in
+                                               ("train_loss", "train_acc", "test_loss", "test_acc", "time_s")]),
+               "gevo_pop_scores")
+        return arrs
+
+    def last_time(self) -> float:
+        s = ctypes.c_double()
+        _check(lib().gevo_pop_last_time(self._h, ctypes.byref(s)), "gevo_pop_last_time")
+        return s.value
+
+    # ------------------------------------------------------------ state access
+    def export(self, v: int):
+        params = np.zeros(param_count(self.dims), np.float32)
+        nw = sum(self.dims[l - 1] * self.dims[l] for l in range(1, len(self.dims)))
+        mask = np.zeros(nw, np.uint8)
+        lr, dens = ctypes.c_float(), ctypes.c_float()
+        _check(lib().gevo_pop_export(self._h, v, _fp(params), mask.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)),
+                                     ctypes.byref(lr), ctypes.byref(dens)), "gevo_pop_export")
+        return dict(params=params, mask=mask, lr=np.float32(lr.value), density=np.float32(dens.value))
+
+    def import_params(self, v: int, params):
+        p = np.ascontiguousarray(np.asarray(params, np.float32))
+        assert p.size == param_count(self.dims)
+        _check(lib().gevo_pop_import(self._h, v, _fp(p)), "gevo_pop_import")
+
+    def epoch_labels(self) -> np.ndarray:
+        out = np.zeros(self.n_train, np.int32)
+        _check(lib().gevo_pop_epoch_labels(self._h, out.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                           self.n_train), "gevo_pop_epoch_labels")
+        return out
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            lib().gevo_pop_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,714 @@
+// Host runtime and C-ABI of libgevo (declared in include/gevo.h): validates
+// configurations, lays out the caller's workspace, draws the per-variant
+// hyper-parameters and the per-epoch data order, and enqueues the kernels of
+// gevo_kernels.hip on the caller's stream.
+#include <math.h>
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+#include "gevo.h"
+#include "gevo_internal.h"
+
+using namespace gevo;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct LayerLay {
+  int K = 0, N = 0, Kp = 0, Np = 0;
+  size_t Wm = 0, bias = 0, mask = 0, Wt = 0, base_w = 0, base_b = 0;
+  size_t arows[2] = {0, 0}, acols[2] = {0, 0};   // training activations (hidden layers)
+  size_t gcols = 0, grows = 0;                     // gradient at this layer's output (hidden)
+  size_t prows = 0;                                // predict activations
+};
+
+struct Layout {
+  int L = 0, P = 0, B = 0, Bp = 0, T = 0;
+  int64_t n_train = 0, n_test = 0;
+  int n_test_pad = 0, n_chunks_test = 0;
+  size_t elt = 4;
+  LayerLay lay[GEVO_MAX_LAYERS];
+  size_t lr = 0, thresh = 0, train_ce = 0, train_corr = 0, test_ce = 0, test_corr = 0, part_ce = 0,
+         part_corr = 0, xrows = 0, xcols = 0, yep = 0, xte = 0, yte = 0, perm = 0;
+  size_t total = 0;
+};
+
+gevo_status validate(const gevo_pop_config* c) {
+  if (!c) return GEVO_E_ARG;
+  if (c->abi_version != GEVO_ABI_VERSION) return GEVO_E_ARG;
+  if (c->n_layers < 1 || c->n_layers > GEVO_MAX_LAYERS) return c->n_layers < 1 ? GEVO_E_ARG : GEVO_E_UNSUPPORTED;
+  if (c->dtype != GEVO_F32 && c->dtype != GEVO_BF16) return GEVO_E_ARG;
+  if (c->init != GEVO_INIT_XAVIER && c->init != GEVO_INIT_BASE_NOISE) return GEVO_E_ARG;
+  if (c->P < 1 || c->batch < 1) return GEVO_E_ARG;
+  if (c->batch > GEVO_MAX_BATCH) return GEVO_E_UNSUPPORTED;
+  for (uint32_t l = 0; l <= c->n_layers; ++l) {
+    if (c->dims[l] < 1) return GEVO_E_SHAPE;
+    if (c->dims[l] > GEVO_MAX_WIDTH) return GEVO_E_UNSUPPORTED;
+  }
+  if (c->dims[c->n_layers] > GEVO_MAX_CLASSES) return GEVO_E_UNSUPPORTED;
+  if (c->n_train < 0 || c->n_test < 1) return GEVO_E_SHAPE;
+  if (c->n_train > 2000000000LL || c->n_test > 2000000000LL) return GEVO_E_UNSUPPORTED;
+  if (!(c->lr_lo >= 0.0f) || !(c->lr_hi >= c->lr_lo) || !isfinite(c->lr_hi)) return GEVO_E_ARG;
+  if (c->lr_lo < c->lr_hi && !(c->lr_lo > 0.0f)) return GEVO_E_ARG;
+  if (c->n_dens_list > 0) {
+    if (!c->dens_list) return GEVO_E_ARG;
+    for (uint32_t i = 0; i < c->n_dens_list; ++i)
+      if (!(c->dens_list[i] >= 0.0f && c->dens_list[i] <= 1.0f)) return GEVO_E_ARG;
+  } else if (!(c->dens_lo >= 0.0f && c->dens_hi >= c->dens_lo && c->dens_hi <= 1.0f)) {
+    return GEVO_E_ARG;
+  }
+  if (!isfinite(c->noise_rel_std)) return GEVO_E_ARG;
+  return GEVO_OK;
+}
+
+// dynamic LDS of the output kernel: operand copy of W_L plus, in training, the gradient rows
+size_t out_lds(int Kp, int Bp, size_t elt, int pad) {
+  return (size_t)32 * (Kp + pad) * elt + (size_t)Bp * (32 + pad) * elt;
+}
+
+gevo_status make_layout(const gevo_pop_config* c, Layout* o) {
+  gevo_status st = validate(c);
+  if (st != GEVO_OK) return st;
+  Layout& y = *o;
+  y = Layout();
+  y.L = (int)c->n_layers;
+  y.P = (int)c->P;
+  y.B = (int)c->batch;
+  y.Bp = round_up(y.B, kTile);
+  y.n_train = c->n_train;
+  y.n_test = c->n_test;
+  y.T = (int)((c->n_train + y.B - 1) / y.B);
+  y.n_test_pad = round_up((int)c->n_test, kOutRows);
+  y.n_chunks_test = y.n_test_pad / kOutRows;
+  y.elt = c->dtype == GEVO_BF16 ? 2 : 4;
+  const int pad = c->dtype == GEVO_BF16 ? 8 : 1;
+  for (int l = 1; l <= y.L; ++l) {
+    LayerLay& q = y.lay[l - 1];
+    q.K = (int)c->dims[l - 1];
+    q.N = (int)c->dims[l];
+    q.Kp = round_up(q.K, kTile);
+    q.Np = (l == y.L) ? kTile : round_up(q.N, kTile);
+  }
+  if (out_lds(y.lay[y.L - 1].Kp, y.Bp, y.elt, pad) > kLdsBudget) return GEVO_E_UNSUPPORTED;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes);
+    return at;
+  };
+  const size_t P = (size_t)y.P, Bp = (size_t)y.Bp, e = y.elt;
+  for (int l = 0; l < y.L; ++l) {
+    LayerLay& q = y.lay[l];
+    const size_t Kp = q.Kp, Np = q.Np;
+    q.Wm = take(P * Np * Kp * 4);
+    q.bias = take(P * Np * 4);
+    q.mask = take(P * Np * (Kp / 32) * 4);
+    q.base_w = take(Np * Kp * 4);
+    q.base_b = take(Np * 4);
+    if (l >= 1 && l < y.L - 1) q.Wt = take(P * Kp * Np * e);         // hidden layer >= 2
+    if (l < y.L - 1) {                                                // hidden layer: activations
+      for (int bsel = 0; bsel < 2; ++bsel) {
+        q.arows[bsel] = take(P * Bp * Np * e);
+        q.acols[bsel] = take(P * Np * Bp * e);
+      }
+      q.gcols = take(P * Np * Bp * e);
+      if (l >= 1) q.grows = take(P * Bp * Np * e);
+      q.prows = take(P * (size_t)kPredictChunk * Np * e);
+    }
+  }
+  y.lr = take(P * 4);
+  y.thresh = take(P * 4);
+  y.train_ce = take(P * 8);
+  y.train_corr = take(P * 8);
+  y.test_ce = take(P * 8);
+  y.test_corr = take(P * 8);
+  y.part_ce = take(P * (size_t)y.n_chunks_test * 8);
+  y.part_corr = take(P * (size_t)y.n_chunks_test * 4);
+  const size_t Kp1 = (size_t)y.lay[0].Kp;
+  const size_t T = (size_t)(y.T > 0 ? y.T : 1);
+  y.xrows = take(T * Bp * Kp1 * e);
+  y.xcols = take(T * Kp1 * Bp * e);
+  y.yep = take(T * Bp * 4);
+  y.xte = take((size_t)y.n_test_pad * Kp1 * e);
+  y.yte = take((size_t)y.n_test_pad * 4);
+  y.perm = take((size_t)(y.n_train > 0 ? y.n_train : 1) * 4);
+  y.total = off;
+  return GEVO_OK;
+}
+
+uint32_t draw_word(uint64_t seed, uint32_t c0, uint32_t c1, uint32_t c2, uint32_t stream, uint32_t word) {
+  const uint32_t ctr[4] = {c0, c1, c2, stream};
+  const uint32_t key[2] = {(uint32_t)(seed & 0xffffffffu), (uint32_t)(seed >> 32)};
+  uint32_t out[4];
+  philox4x32_10_host(ctr, key, out);
+  return out[word];
+}
+
+void fisher_yates(uint64_t seed, uint32_t epoch, uint32_t n, uint32_t* out) {
+  for (uint32_t i = 0; i < n; ++i) out[i] = i;
+  for (uint32_t i = n; i-- > 1;) {
+    const uint32_t r = draw_word(seed, i >> 2, 0, epoch, kStreamPerm, i & 3);
+    const uint32_t j = (uint32_t)(((uint64_t)r * (uint64_t)(i + 1)) >> 32);
+    const uint32_t t = out[i];
+    out[i] = out[j];
+    out[j] = t;
+  }
+}
+
+}  // namespace
+
+namespace gevo {
+void philox4x32_10_host(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]) {
+  uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3], k0 = key[0], k1 = key[1];
+  for (int i = 0; i < 10; ++i) {
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c0, p1 = (uint64_t)0xCD9E8D57u * c2;
+    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0, n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+    c1 = (uint32_t)p1;
+    c3 = (uint32_t)p0;
+    c0 = n0;
+    c2 = n2;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+}  // namespace gevo
+
+struct gevo_pop {
+  gevo_pop_config cfg{};
+  std::vector<float> dens_list;
+  Layout y;
+  char* ws = nullptr;
+  hipStream_t stream = nullptr;
+  const float* trX = nullptr;
+  const int32_t* trY = nullptr;
+  const float* teX = nullptr;
+  const int32_t* teY = nullptr;
+  std::vector<float> lr, dens;
+  std::vector<uint32_t> thresh;
+  int expected_epoch = 0;   // next epoch that may be started
+  int open_epoch = -1;      // epoch in progress (-1: none)
+  int last_epoch = -1;      // epoch whose loss the accumulators hold
+  uint32_t next_step = 0;
+  int64_t rows_done = 0;
+  std::vector<uint32_t> perm_host[2];
+  hipEvent_t perm_ev[2] = {nullptr, nullptr};
+  bool perm_ev_used[2] = {false, false};
+  hipEvent_t ev0 = nullptr, ev1 = nullptr;
+  bool timing_pending = false;
+  double last_s = 0.0;
+  bool predicted = false;
+};
+
+namespace {
+
+template <typename T>
+T* at(gevo_pop* p, size_t off) { return reinterpret_cast<T*>(p->ws + off); }
+
+#define HIP_TRY(x)                              \
+  do {                                          \
+    if ((x) != hipSuccess) return GEVO_E_HIP;   \
+  } while (0)
+
+template <typename S>
+gevo_status forward_hidden(gevo_pop* p, const S* arows0, size_t ar0_vs, int R, int outsel, bool predict) {
+  const Layout& y = p->y;
+  for (int l = 0; l < y.L - 1; ++l) {
+    const LayerLay& q = y.lay[l];
+    LayerArgs<S> a{};
+    a.Kp = q.Kp; a.Np = q.Np; a.Bp = y.Bp;
+    a.Wm = at<float>(p, q.Wm); a.bias = at<float>(p, q.bias); a.mask = at<uint32_t>(p, q.mask);
+    a.lr = at<float>(p, y.lr);
+    a.do_update = 0;
+    a.do_forward = 1;
+    a.R = R;
+    if (l == 0) { a.Arows = arows0; a.ar_vs = ar0_vs; }
+    else if (predict) { a.Arows = at<S>(p, y.lay[l - 1].prows); a.ar_vs = (size_t)kPredictChunk * y.lay[l - 1].Np; }
+    else { a.Arows = at<S>(p, y.lay[l - 1].arows[outsel]); a.ar_vs = (size_t)y.Bp * y.lay[l - 1].Np; }
+    if (predict) {
+      a.Orows = at<S>(p, q.prows); a.or_vs = (size_t)kPredictChunk * q.Np;
+    } else {
+      a.Orows = at<S>(p, q.arows[outsel]); a.or_vs = (size_t)y.Bp * q.Np;
+      a.Ocols = at<S>(p, q.acols[outsel]); a.oc_vs = (size_t)q.Np * y.Bp;
+      if (q.Wt) a.Wt = at<S>(p, q.Wt);
+    }
+    if (a.Kp % kTile || a.Np % kTile || a.R % kTile || a.R <= 0) return GEVO_E_SHAPE;
+    HIP_TRY(launch_layer<S>(a, y.P, p->stream));
+  }
+  return GEVO_OK;
+}
+
+template <typename S>
+gevo_status begin_epoch(gevo_pop* p, int e) {
+  const Layout& y = p->y;
+  const int slot = e & 1;
+  if (p->perm_ev_used[slot]) HIP_TRY(hipEventSynchronize(p->perm_ev[slot]));
+  std::vector<uint32_t>& ph = p->perm_host[slot];
+  ph.resize((size_t)y.n_train);
+  fisher_yates(p->cfg.seed, (uint32_t)e, (uint32_t)y.n_train, ph.data());
+  HIP_TRY(hipMemcpyAsync(at<uint32_t>(p, y.perm), ph.data(), ph.size() * 4, hipMemcpyHostToDevice, p->stream));
+  HIP_TRY(hipEventRecord(p->perm_ev[slot], p->stream));
+  p->perm_ev_used[slot] = true;
+  GatherArgs g{};
+  g.X = p->trX; g.y = p->trY; g.perm = at<uint32_t>(p, y.perm); g.n = y.n_train;
+  g.d0 = y.lay[0].K; g.Kp = y.lay[0].Kp; g.B = y.B; g.Bp = y.Bp; g.T = y.T;
+  g.rows = p->ws + y.xrows; g.labels = at<int32_t>(p, y.yep);
+  HIP_TRY(launch_gather<S>(g, p->stream));
+  TransposeArgs tr{};
+  tr.src = p->ws + y.xrows; tr.dst = p->ws + y.xcols; tr.Kp = y.lay[0].Kp; tr.Bp = y.Bp; tr.T = y.T;
+  HIP_TRY(launch_transpose<S>(tr, p->stream));
+  HIP_TRY(launch_zero_bytes(p->ws + y.train_ce, (size_t)y.P * 8, p->stream));
+  HIP_TRY(launch_zero_bytes(p->ws + y.train_corr, (size_t)y.P * 8, p->stream));
+  // forward of step 0 for the hidden layers
+  if (y.L > 1) {
+    gevo_status st = forward_hidden<S>(p, at<S>(p, y.xrows), 0, y.Bp, 0, false);
+    if (st != GEVO_OK) return st;
+  }
+  p->rows_done = 0;
+  return GEVO_OK;
+}
+
+template <typename S>
+gevo_status train_step(gevo_pop* p, int t) {
+  const Layout& y = p->y;
+  const int L = y.L;
+  const int buf = t & 1, nb = buf ^ 1;
+  const int64_t r0 = (int64_t)t * y.B;
+  const int bt = (int)((y.n_train - r0) < y.B ? (y.n_train - r0) : y.B);
+  const size_t e = y.elt;
+  const size_t xstep_r = (size_t)y.Bp * y.lay[0].Kp, xstep_c = xstep_r;
+  const S* xrows_t = reinterpret_cast<const S*>(p->ws + y.xrows) + (size_t)t * xstep_r;
+  const S* xcols_t = reinterpret_cast<const S*>(p->ws + y.xcols) + (size_t)t * xstep_c;
+  (void)e;
+  // output layer: loss, gradient, W_L update, gradient of the last hidden layer
+  {
+    const LayerLay& q = y.lay[L - 1];
+    OutArgs<S> a{};
+    a.Kp = q.Kp; a.C = q.N; a.Bp = y.Bp;
+    a.Wm = at<float>(p, q.Wm); a.bias = at<float>(p, q.bias); a.mask = at<uint32_t>(p, q.mask);
+    a.lr = at<float>(p, y.lr);
+    a.train = 1;
+    if (L == 1) {
+      a.Arows = xrows_t; a.ar_vs = 0; a.Acols = xcols_t; a.ac_vs = 0;
+    } else {
+      const LayerLay& h = y.lay[L - 2];
+      a.Arows = at<S>(p, h.arows[buf]); a.ar_vs = (size_t)y.Bp * h.Np;
+      a.Acols = at<S>(p, h.acols[buf]); a.ac_vs = (size_t)h.Np * y.Bp;
+      a.Gcols = at<S>(p, h.gcols); a.gc_vs = (size_t)h.Np * y.Bp;
+      if (h.grows) { a.Grows = at<S>(p, h.grows); a.gr_vs = (size_t)y.Bp * h.Np; }
+    }
+    a.labels = at<int32_t>(p, y.yep) + (size_t)t * y.Bp;
+    a.rows = y.Bp;
+    a.scale = (float)(1.0 / (double)bt);
+    a.ce_acc = at<double>(p, y.train_ce);
+    a.correct_acc = at<unsigned long long>(p, y.train_corr);
+    if (a.Kp % kTile || a.Bp % kTile) return GEVO_E_SHAPE;
+    HIP_TRY(launch_out<S>(a, y.P, p->stream));
+  }
+  // hidden backward GEMMs, top down (pre-update weights)
+  for (int l = L - 2; l >= 1; --l) {          // layer index l (0-based) has a hidden layer below
+    const LayerLay& q = y.lay[l];
+    const LayerLay& h = y.lay[l - 1];
+    BwdArgs<S> a{};
+    a.Kp = q.Kp; a.Np = q.Np; a.Bp = y.Bp;
+    a.Wt = at<S>(p, q.Wt);
+    a.Grows = at<S>(p, q.grows); a.gr_vs = (size_t)y.Bp * q.Np;
+    a.Acols = at<S>(p, h.acols[buf]); a.ac_vs = (size_t)h.Np * y.Bp;
+    a.Gcols = at<S>(p, h.gcols); a.gc_vs = (size_t)h.Np * y.Bp;
+    if (h.grows) { a.Grows_out = at<S>(p, h.grows); a.go_vs = (size_t)y.Bp * h.Np; }
+    if (a.Kp % kTile || a.Np % kTile || a.Bp % kTile || a.Kp != h.Np) return GEVO_E_SHAPE;
+    HIP_TRY(launch_bwd<S>(a, y.P, p->stream));
+  }
+  // hidden layers bottom up: update, then the forward of step t+1
+  const bool fwd = t + 1 < y.T;
+  for (int l = 0; l < L - 1; ++l) {
+    const LayerLay& q = y.lay[l];
+    LayerArgs<S> a{};
+    a.Kp = q.Kp; a.Np = q.Np; a.Bp = y.Bp;
+    a.Wm = at<float>(p, q.Wm); a.bias = at<float>(p, q.bias); a.mask = at<uint32_t>(p, q.mask);
+    a.lr = at<float>(p, y.lr);
+    a.do_update = 1;
+    a.Gcols = at<S>(p, q.gcols); a.g_vs = (size_t)q.Np * y.Bp;
+    if (l == 0) { a.Acols = xcols_t; a.ac_vs = 0; }
+    else { a.Acols = at<S>(p, y.lay[l - 1].acols[buf]); a.ac_vs = (size_t)y.lay[l - 1].Np * y.Bp; }
+    a.do_forward = fwd ? 1 : 0;
+    a.R = y.Bp;
+    if (fwd) {
+      if (l == 0) { a.Arows = xrows_t + xstep_r; a.ar_vs = 0; }
+      else { a.Arows = at<S>(p, y.lay[l - 1].arows[nb]); a.ar_vs = (size_t)y.Bp * y.lay[l - 1].Np; }
+      a.Orows = at<S>(p, q.arows[nb]); a.or_vs = (size_t)y.Bp * q.Np;
+      a.Ocols = at<S>(p, q.acols[nb]); a.oc_vs = (size_t)q.Np * y.Bp;
+    }
+    if (q.Wt) a.Wt = at<S>(p, q.Wt);
+    if (a.Kp % kTile || a.Np % kTile || a.Bp % kTile || a.Bp > kPassRows) return GEVO_E_SHAPE;
+    HIP_TRY(launch_layer<S>(a, y.P, p->stream));
+  }
+  p->rows_done += bt;
+  return GEVO_OK;
+}
+
+template <typename S>
+gevo_status do_train_steps(gevo_pop* p, uint32_t epoch, uint32_t s0, uint32_t s1) {
+  const Layout& y = p->y;
+  if (y.n_train == 0 || y.T == 0) return GEVO_E_ORDER;
+  if (s0 > s1 || s1 > (uint32_t)y.T) return GEVO_E_ARG;
+  bool begin = false;
+  if (p->open_epoch < 0) {
+    if (s0 != 0 || (int)epoch != p->expected_epoch) return GEVO_E_ORDER;
+    begin = true;
+  } else if ((int)epoch != p->open_epoch || s0 != p->next_step) {
+    return GEVO_E_ORDER;
+  }
+  HIP_TRY(hipEventRecord(p->ev0, p->stream));
+  if (begin) {
+    gevo_status st = begin_epoch<S>(p, (int)epoch);
+    if (st != GEVO_OK) return st;
+    p->open_epoch = (int)epoch;
+    p->last_epoch = (int)epoch;
+    p->next_step = 0;
+  }
+  for (uint32_t t = s0; t < s1; ++t) {
+    gevo_status st = train_step<S>(p, (int)t);
+    if (st != GEVO_OK) return st;
+  }
+  p->next_step = s1;
+  if (s1 == (uint32_t)y.T) {
+    p->open_epoch = -1;
+    p->expected_epoch = (int)epoch + 1;
+  }
+  HIP_TRY(hipEventRecord(p->ev1, p->stream));
+  p->timing_pending = true;
+  return GEVO_OK;
+}
+
+template <typename S>
+gevo_status do_predict(gevo_pop* p) {
+  const Layout& y = p->y;
+  HIP_TRY(hipEventRecord(p->ev0, p->stream));
+  const size_t Kp1 = (size_t)y.lay[0].Kp;
+  for (int c0 = 0; c0 < y.n_test_pad; c0 += kPredictChunk) {
+    const int R = (y.n_test_pad - c0) < kPredictChunk ? (y.n_test_pad - c0) : kPredictChunk;
+    const S* xr = reinterpret_cast<const S*>(p->ws + y.xte) + (size_t)c0 * Kp1;
+    if (y.L > 1) {
+      gevo_status st = forward_hidden<S>(p, xr, 0, R, 0, true);
+      if (st != GEVO_OK) return st;
+    }
+    const LayerLay& q = y.lay[y.L - 1];
+    OutArgs<S> a{};
+    a.Kp = q.Kp; a.C = q.N; a.Bp = y.Bp;
+    a.Wm = at<float>(p, q.Wm); a.bias = at<float>(p, q.bias); a.mask = at<uint32_t>(p, q.mask);
+    a.lr = at<float>(p, y.lr);
+    a.train = 0;
+    if (y.L == 1) { a.Arows = xr; a.ar_vs = 0; }
+    else { a.Arows = at<S>(p, y.lay[y.L - 2].prows); a.ar_vs = (size_t)kPredictChunk * y.lay[y.L - 2].Np; }
+    a.labels = at<int32_t>(p, y.yte) + c0;
+    a.rows = R;
+    a.chunk0 = c0 / kOutRows;
+    a.n_chunks_total = y.n_chunks_test;
+    a.part_ce = at<double>(p, y.part_ce);
+    a.part_correct = at<unsigned int>(p, y.part_corr);
+    if (a.Kp % kTile || R % kOutRows) return GEVO_E_SHAPE;
+    HIP_TRY(launch_out<S>(a, y.P, p->stream));
+  }
+  HIP_TRY(launch_reduce_partials(at<double>(p, y.part_ce), at<unsigned int>(p, y.part_corr), y.P,
+                                 y.n_chunks_test, at<double>(p, y.test_ce),
+                                 at<unsigned long long>(p, y.test_corr), p->stream));
+  HIP_TRY(hipEventRecord(p->ev1, p->stream));
+  p->timing_pending = true;
+  p->predicted = true;
+  return GEVO_OK;
+}
+
+gevo_status sync_timing(gevo_pop* p) {
+  HIP_TRY(hipStreamSynchronize(p->stream));
+  if (p->timing_pending) {
+    float ms = 0.0f;
+    HIP_TRY(hipEventElapsedTime(&ms, p->ev0, p->ev1));
+    p->last_s = (double)ms * 1e-3;
+    p->timing_pending = false;
+  }
+  return GEVO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+gevo_status gevo_pop_workspace_bytes(const gevo_pop_config* cfg, size_t* bytes) {
+  if (!bytes) return GEVO_E_ARG;
+  Layout y;
+  gevo_status st = make_layout(cfg, &y);
+  if (st != GEVO_OK) return st;
+  *bytes = y.total;
+  return GEVO_OK;
+}
+
+gevo_status gevo_epoch_permutation(uint64_t seed, uint32_t epoch, uint32_t n, uint32_t* out) {
+  if (!out && n > 0) return GEVO_E_ARG;
+  fisher_yates(seed, epoch, n, out);
+  return GEVO_OK;
+}
+
+gevo_status gevo_pop_init(const gevo_pop_config* cfg, void* d_ws, size_t ws_bytes, const float* d_train_x,
+                          const int32_t* d_train_y, const float* d_test_x, const int32_t* d_test_y,
+                          void* hip_stream, gevo_pop** out) {
+  if (!out) return GEVO_E_ARG;
+  *out = nullptr;
+  Layout y;
+  gevo_status st = make_layout(cfg, &y);
+  if (st != GEVO_OK) return st;
+  if (!d_ws || ((uintptr_t)d_ws % kAlign) != 0 || ws_bytes < y.total) return GEVO_E_WORKSPACE;
+  if (!d_test_x || !d_test_y) return GEVO_E_ARG;
+  if (y.n_train > 0 && (!d_train_x || !d_train_y)) return GEVO_E_ARG;
+  gevo_pop* p = new (std::nothrow) gevo_pop();
+  if (!p) return GEVO_E_ARG;
+  p->cfg = *cfg;
+  if (cfg->n_dens_list > 0) p->dens_list.assign(cfg->dens_list, cfg->dens_list + cfg->n_dens_list);
+  p->cfg.dens_list = nullptr;
+  p->cfg.base_params = nullptr;
+  p->y = y;
+  p->ws = reinterpret_cast<char*>(d_ws);
+  p->stream = reinterpret_cast<hipStream_t>(hip_stream);
+  p->trX = d_train_x; p->trY = d_train_y; p->teX = d_test_x; p->teY = d_test_y;
+  auto fail = [&](gevo_status s) { gevo_pop_destroy(p); return s; };
+  if (hipEventCreate(&p->ev0) != hipSuccess || hipEventCreate(&p->ev1) != hipSuccess ||
+      hipEventCreateWithFlags(&p->perm_ev[0], hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&p->perm_ev[1], hipEventDisableTiming) != hipSuccess)
+    return fail(GEVO_E_HIP);
+  // per-variant learning rate, density and mask threshold (host, fp64)
+  const int P = y.P;
+  p->lr.resize(P); p->dens.resize(P); p->thresh.resize(P);
+  for (int v = 0; v < P; ++v) {
+    if (cfg->lr_lo == cfg->lr_hi) {
+      p->lr[v] = cfg->lr_lo;
+    } else {
+      const double u = (double)(draw_word(cfg->seed, 0, 0, (uint32_t)v, kStreamLr, 0) >> 8) * (1.0 / 16777216.0);
+      const double lo = log((double)cfg->lr_lo), hi = log((double)cfg->lr_hi);
+      p->lr[v] = (float)exp(lo + u * (hi - lo));
+    }
+    float rho;
+    if (!p->dens_list.empty()) {
+      rho = p->dens_list[(size_t)v % p->dens_list.size()];
+    } else {
+      const double u = (double)(draw_word(cfg->seed, 0, 0, (uint32_t)v, kStreamDens, 0) >> 8) * (1.0 / 16777216.0);
+      rho = (float)((double)cfg->dens_lo + u * ((double)cfg->dens_hi - (double)cfg->dens_lo));
+    }
+    p->dens[v] = rho;
+    double t = floor((double)rho * 16777216.0 + 0.5);
+    if (t < 0.0) t = 0.0;
+    if (t > 16777216.0) t = 16777216.0;
+    p->thresh[v] = (uint32_t)t;
+  }
+  hipStream_t s = p->stream;
+  if (hipMemcpyAsync(p->ws + y.lr, p->lr.data(), (size_t)P * 4, hipMemcpyHostToDevice, s) != hipSuccess ||
+      hipMemcpyAsync(p->ws + y.thresh, p->thresh.data(), (size_t)P * 4, hipMemcpyHostToDevice, s) != hipSuccess)
+    return fail(GEVO_E_HIP);
+  // optional base model, padded and transposed to the device layout
+  std::vector<std::vector<float>> base_w(y.L), base_b(y.L);
+  if (cfg->init == GEVO_INIT_BASE_NOISE && cfg->base_params) {
+    size_t off = 0;
+    for (int l = 0; l < y.L; ++l) {
+      const LayerLay& q = y.lay[l];
+      base_w[l].assign((size_t)q.Np * q.Kp, 0.0f);
+      base_b[l].assign((size_t)q.Np, 0.0f);
+      for (int k = 0; k < q.K; ++k)
+        for (int n = 0; n < q.N; ++n) base_w[l][(size_t)n * q.Kp + k] = cfg->base_params[off + (size_t)k * q.N + n];
+      off += (size_t)q.K * q.N;
+      for (int n = 0; n < q.N; ++n) base_b[l][n] = cfg->base_params[off + n];
+      off += (size_t)q.N;
+      if (hipMemcpy(p->ws + q.base_w, base_w[l].data(), base_w[l].size() * 4, hipMemcpyHostToDevice) != hipSuccess ||
+          hipMemcpy(p->ws + q.base_b, base_b[l].data(), base_b[l].size() * 4, hipMemcpyHostToDevice) != hipSuccess)
+        return fail(GEVO_E_HIP);
+    }
+  }
+  for (int l = 0; l < y.L; ++l) {
+    const LayerLay& q = y.lay[l];
+    InitArgs a{};
+    a.P = P; a.l_index = l; a.K = q.K; a.N = q.N; a.Kp = q.Kp; a.Np = q.Np;
+    a.seed = cfg->seed;
+    a.init_kind = cfg->init == GEVO_INIT_BASE_NOISE ? 1 : 0;
+    a.xavier_a = (float)sqrt(6.0 / ((double)q.K + (double)q.N));
+    a.noise_std = cfg->noise_rel_std;
+    if (cfg->init == GEVO_INIT_BASE_NOISE && cfg->base_params) {
+      a.base_w = reinterpret_cast<const float*>(p->ws + q.base_w);
+      a.base_b = reinterpret_cast<const float*>(p->ws + q.base_b);
+    }
+    a.thresh = reinterpret_cast<const uint32_t*>(p->ws + y.thresh);
+    a.Wm = reinterpret_cast<float*>(p->ws + q.Wm);
+    a.bias = reinterpret_cast<float*>(p->ws + q.bias);
+    a.mask = reinterpret_cast<uint32_t*>(p->ws + q.mask);
+    if (q.Kp % kTile || q.Np % kTile) return fail(GEVO_E_SHAPE);
+    if (launch_init(a, s) != hipSuccess) return fail(GEVO_E_HIP);
+  }
+  // test split converted once to the operand type, padded to whole chunks
+  GatherArgs g{};
+  g.X = d_test_x; g.y = d_test_y; g.perm = nullptr; g.n = y.n_test;
+  g.d0 = y.lay[0].K; g.Kp = y.lay[0].Kp; g.B = y.n_test_pad; g.Bp = y.n_test_pad; g.T = 1;
+  g.rows = p->ws + y.xte; g.labels = reinterpret_cast<int32_t*>(p->ws + y.yte);
+  hipError_t e = cfg->dtype == GEVO_BF16 ? launch_gather<uint16_t>(g, s) : launch_gather<float>(g, s);
+  if (e != hipSuccess) return fail(GEVO_E_HIP);
+  if (launch_zero_bytes(p->ws + y.train_ce, (size_t)P * 8, s) != hipSuccess ||
+      launch_zero_bytes(p->ws + y.train_corr, (size_t)P * 8, s) != hipSuccess ||
+      launch_zero_bytes(p->ws + y.test_ce, (size_t)P * 8, s) != hipSuccess ||
+      launch_zero_bytes(p->ws + y.test_corr, (size_t)P * 8, s) != hipSuccess)
+    return fail(GEVO_E_HIP);
+  if (cfg->init == GEVO_INIT_BASE_NOISE && cfg->base_params) {
+    if (hipStreamSynchronize(s) != hipSuccess) return fail(GEVO_E_HIP);   // host staging vectors die here
+  }
+  *out = p;
+  return GEVO_OK;
+}
+
+gevo_status gevo_pop_train_steps(gevo_pop* p, uint32_t epoch, uint32_t s0, uint32_t s1) {
+  if (!p) return GEVO_E_ARG;
+  return p->cfg.dtype == GEVO_BF16 ? do_train_steps<uint16_t>(p, epoch, s0, s1)
+                                   : do_train_steps<float>(p, epoch, s0, s1);
+}
+
+gevo_status gevo_pop_train_epoch(gevo_pop* p, uint32_t epoch) {
+  if (!p) return GEVO_E_ARG;
+  if (p->y.n_train == 0) return GEVO_E_ORDER;
+  return gevo_pop_train_steps(p, epoch, 0, (uint32_t)p->y.T);
+}
+
+gevo_status gevo_pop_steps_per_epoch(const gevo_pop* p, uint32_t* steps) {
+  if (!p || !steps) return GEVO_E_ARG;
+  *steps = (uint32_t)p->y.T;
+  return GEVO_OK;
+}
+
+gevo_status gevo_pop_predict(gevo_pop* p) {
+  if (!p) return GEVO_E_ARG;
+  return p->cfg.dtype == GEVO_BF16 ? do_predict<uint16_t>(p) : do_predict<float>(p);
+}
+
+gevo_status gevo_pop_scores(gevo_pop* p, float* train_loss, float* train_acc, float* test_loss, float* test_acc,
+                            float* time_s) {
+  if (!p) return GEVO_E_ARG;
+  gevo_status st = sync_timing(p);
+  if (st != GEVO_OK) return st;
+  const Layout& y = p->y;
+  const int P = y.P;
+  std::vector<double> tce(P), sce(P);
+  std::vector<unsigned long long> tc(P), sc(P);
+  HIP_TRY(hipMemcpy(tce.data(), p->ws + y.train_ce, (size_t)P * 8, hipMemcpyDeviceToHost));
+  HIP_TRY(hipMemcpy(tc.data(), p->ws + y.train_corr, (size_t)P * 8, hipMemcpyDeviceToHost));
+  HIP_TRY(hipMemcpy(sce.data(), p->ws + y.test_ce, (size_t)P * 8, hipMemcpyDeviceToHost));
+  HIP_TRY(hipMemcpy(sc.data(), p->ws + y.test_corr, (size_t)P * 8, hipMemcpyDeviceToHost));
+  const bool trained = p->last_epoch >= 0 && p->rows_done > 0;
+  for (int v = 0; v < P; ++v) {
+    if (train_loss) train_loss[v] = trained ? (float)(tce[v] / (double)p->rows_done) : NAN;
+    if (train_acc) train_acc[v] = trained ? (float)((double)tc[v] / (double)p->rows_done) : NAN;
+    if (test_loss) test_loss[v] = p->predicted ? (float)(sce[v] / (double)y.n_test) : NAN;
+    if (test_acc) test_acc[v] = p->predicted ? (float)((double)sc[v] / (double)y.n_test) : NAN;
+    if (time_s) time_s[v] = (float)(p->last_s / (double)P);
+  }
+  return GEVO_OK;
+}
+
+gevo_status gevo_pop_last_time(gevo_pop* p, double* seconds) {
+  if (!p || !seconds) return GEVO_E_ARG;
+  gevo_status st = sync_timing(p);
+  if (st != GEVO_OK) return st;
+  *seconds = p->last_s;
+  return GEVO_OK;
+}
+
+gevo_status gevo_pop_export(gevo_pop* p, uint32_t v, float* params_out, uint8_t* mask_out, float* lr_out,
+                            float* density_out) {
+  if (!p) return GEVO_E_ARG;
+  const Layout& y = p->y;
+  if (v >= (uint32_t)y.P) return GEVO_E_ARG;
+  HIP_TRY(hipStreamSynchronize(p->stream));
+  size_t off = 0, moff = 0;
+  for (int l = 0; l < y.L; ++l) {
+    const LayerLay& q = y.lay[l];
+    const size_t nw = (size_t)q.Np * q.Kp, words = (size_t)q.Np * (q.Kp / 32);
+    std::vector<float> W(nw), b((size_t)q.Np);
+    std::vector<uint32_t> M(words);
+    HIP_TRY(hipMemcpy(W.data(), p->ws + q.Wm + (size_t)v * nw * 4, nw * 4, hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(b.data(), p->ws + q.bias + (size_t)v * q.Np * 4, (size_t)q.Np * 4, hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(M.data(), p->ws + q.mask + (size_t)v * words * 4, words * 4, hipMemcpyDeviceToHost));
+    for (int k = 0; k < q.K; ++k)
+      for (int n = 0; n < q.N; ++n) {
+        if (params_out) params_out[off + (size_t)k * q.N + n] = W[(size_t)n * q.Kp + k];
+        if (mask_out) mask_out[moff + (size_t)k * q.N + n] = (uint8_t)((M[(size_t)n * (q.Kp / 32) + k / 32] >> (k % 32)) & 1u);
+      }
+    off += (size_t)q.K * q.N;
+    moff += (size_t)q.K * q.N;
+    for (int n = 0; n < q.N; ++n)
+      if (params_out) params_out[off + n] = b[n];
+    off += (size_t)q.N;
+  }
+  if (lr_out) *lr_out = p->lr[v];
+  if (density_out) *density_out = p->dens[v];
+  return GEVO_OK;
+}
+
+gevo_status gevo_pop_import(gevo_pop* p, uint32_t v, const float* params) {
+  if (!p || !params) return GEVO_E_ARG;
+  const Layout& y = p->y;
+  if (v >= (uint32_t)y.P) return GEVO_E_ARG;
+  if (p->open_epoch >= 0) return GEVO_E_ORDER;        // only between epochs
+  HIP_TRY(hipStreamSynchronize(p->stream));
+  size_t off = 0;
+  for (int l = 0; l < y.L; ++l) {
+    const LayerLay& q = y.lay[l];
+    const size_t nw = (size_t)q.Np * q.Kp, words = (size_t)q.Np * (q.Kp / 32);
+    std::vector<uint32_t> M(words);
+    HIP_TRY(hipMemcpy(M.data(), p->ws + q.mask + (size_t)v * words * 4, words * 4, hipMemcpyDeviceToHost));
+    std::vector<float> W(nw, 0.0f), b((size_t)q.Np, 0.0f);
+    for (int k = 0; k < q.K; ++k)
+      for (int n = 0; n < q.N; ++n) {
+        const bool keep = (M[(size_t)n * (q.Kp / 32) + k / 32] >> (k % 32)) & 1u;
+        W[(size_t)n * q.Kp + k] = keep ? params[off + (size_t)k * q.N + n] : 0.0f;
+      }
+    off += (size_t)q.K * q.N;
+    for (int n = 0; n < q.N; ++n) b[n] = params[off + n];
+    off += (size_t)q.N;
+    HIP_TRY(hipMemcpy(p->ws + q.Wm + (size_t)v * nw * 4, W.data(), nw * 4, hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(p->ws + q.bias + (size_t)v * q.Np * 4, b.data(), (size_t)q.Np * 4, hipMemcpyHostToDevice));
+  }
+  return GEVO_OK;
+}
+
+gevo_status gevo_pop_epoch_labels(gevo_pop* p, int32_t* labels_out, int64_t n) {
+  if (!p || !labels_out) return GEVO_E_ARG;
+  const Layout& y = p->y;
+  if (n != y.n_train) return GEVO_E_SHAPE;
+  if (p->last_epoch < 0) return GEVO_E_ORDER;
+  HIP_TRY(hipStreamSynchronize(p->stream));
+  std::vector<int32_t> yep((size_t)y.T * y.Bp);
+  HIP_TRY(hipMemcpy(yep.data(), p->ws + y.yep, yep.size() * 4, hipMemcpyDeviceToHost));
+  for (int64_t r = 0; r < n; ++r) labels_out[r] = yep[(size_t)(r / y.B) * y.Bp + (size_t)(r % y.B)];
+  return GEVO_OK;
+}
+
+void gevo_pop_destroy(gevo_pop* p) {
+  if (!p) return;
+  (void)hipStreamSynchronize(p->stream);   // pending copies may still read host buffers
+  if (p->ev0) (void)hipEventDestroy(p->ev0);
+  if (p->ev1) (void)hipEventDestroy(p->ev1);
+  if (p->perm_ev[0]) (void)hipEventDestroy(p->perm_ev[0]);
+  if (p->perm_ev[1]) (void)hipEventDestroy(p->perm_ev[1]);
+  delete p;
+}
+
+const char* gevo_status_str(gevo_status s) {
+  switch (s) {
+    case GEVO_OK: return "ok";
+    case GEVO_E_ARG: return "invalid argument";
+    case GEVO_E_SHAPE: return "inconsistent shape";
+    case GEVO_E_WORKSPACE: return "workspace too small or misaligned";
+    case GEVO_E_ORDER: return "call out of order";
+    case GEVO_E_HIP: return "HIP runtime error";
+    case GEVO_E_UNSUPPORTED: return "unsupported configuration";
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

@@ -1,0 +1,129 @@
+// Internal declarations shared by the host runtime (gevo_capi.hip) and the
+// kernels (gevo_kernels.hip) of libgevo.  Not part of the C-ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace gevo {
+
+// Tiling constants every launcher checks its shapes against.
+constexpr int kTile = 32;          // MFMA output tile edge; all padded dims are multiples
+constexpr int kThreads = 256;      // 4 wave64 per workgroup
+constexpr int kPassRows = 256;     // forward rows per pass of the layer kernel
+constexpr int kOutRows = 256;      // rows per workgroup of the output kernel (predict)
+constexpr int kPredictChunk = 2048;  // test rows per predict chunk
+constexpr size_t kLdsBudget = 63 * 1024;   // dynamic LDS of the output kernel (static arrays use the rest of 64 KiB)
+
+// Philox stream ids (counter word 3)
+constexpr uint32_t kStreamLr = 1, kStreamDens = 2, kStreamMask = 3, kStreamInit = 4,
+                   kStreamNoise = 5, kStreamPerm = 6;
+
+inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
+
+// ---------------------------------------------------------------- kernels args
+// Storage type S is float (fp32 path) or uint16_t holding bfloat16 bits.
+
+struct InitArgs {
+  int P, l_index, K, N, Kp, Np;  // layer shape (true and padded)
+  uint64_t seed;
+  int init_kind;                 // 0 Xavier, 1 base * (1 + std * eps)
+  float xavier_a;                // fl32(sqrt(6/(K+N)))
+  float noise_std;
+  const float* base_w;           // optional base weights, device, [Np][Kp] padded (layer slice)
+  const float* base_b;           // optional base biases, device, [Np]
+  const uint32_t* thresh;        // [P] mask thresholds
+  float* Wm;                     // [P][Np][Kp]
+  float* bias;                   // [P][Np]
+  uint32_t* mask;                // [P][Np][Kp/32]
+};
+
+template <typename S>
+struct LayerArgs {
+  int Kp, Np;                    // padded input / output width of the layer
+  int Bp;                        // padded batch rows of the update
+  float* Wm;                     // [P][Np][Kp] fp32 master
+  float* bias;                   // [P][Np]
+  const uint32_t* mask;          // [P][Np][Kp/32]
+  const float* lr;               // [P]
+  int do_update;
+  const S* Gcols; size_t g_vs;   // [v][Np][Bp] gradient at this layer's output
+  const S* Acols; size_t ac_vs;  // [v][Kp][Bp] input activations (vs = 0: shared by all variants)
+  int do_forward;
+  int R;                         // forward rows (multiple of kTile)
+  const S* Arows; size_t ar_vs;  // [v][R][Kp] forward input rows
+  S* Orows; size_t or_vs;        // [v][R][Np] relu output rows
+  S* Ocols; size_t oc_vs;        // [v][Np][R] relu output, transposed (nullable)
+  S* Wt;                         // [v][Kp][Np] operand copy of W, transposed (nullable)
+};
+
+template <typename S>
+struct OutArgs {
+  int Kp;                        // padded width of the last hidden layer (input of the output layer)
+  int C;                         // classes (<= 32); padded output width is 32
+  int Bp;                        // padded batch rows (training)
+  float* Wm;                     // [P][32][Kp]
+  float* bias;                   // [P][32]
+  const uint32_t* mask;          // [P][32][Kp/32]
+  const float* lr;               // [P]
+  int train;                     // 1: loss + backward + update on one batch; 0: predict chunk
+  const S* Arows; size_t ar_vs;  // [v][rows][Kp]
+  const S* Acols; size_t ac_vs;  // [v][Kp][Bp] (training)
+  const int32_t* labels;         // [rows]; < 0 marks a padding row
+  int rows;                      // rows covered by the grid (training: Bp)
+  float scale;                   // fl32(1/b_t)
+  double* ce_acc;                // [P] training accumulators
+  unsigned long long* correct_acc;
+  int chunk0;                    // predict: index of the first 256-row chunk
+  int n_chunks_total;            // predict: stride of the partial arrays
+  double* part_ce;               // [P][n_chunks_total]
+  unsigned int* part_correct;
+  S* Gcols; size_t gc_vs;        // [v][Kp][Bp] gradient of the last hidden layer (training)
+  S* Grows; size_t gr_vs;        // [v][Bp][Kp] same, row-major (nullable)
+};
+
+template <typename S>
+struct BwdArgs {
+  int Kp, Np, Bp;                // layer l: input width Kp, output width Np
+  const S* Wt;                   // [v][Kp][Np] pre-update operand weights, transposed
+  const S* Grows; size_t gr_vs;  // [v][Bp][Np] gradient at layer l output
+  const S* Acols; size_t ac_vs;  // [v][Kp][Bp] activations of layer l-1 (for ReLU')
+  S* Gcols; size_t gc_vs;        // [v][Kp][Bp] gradient at layer l-1 output
+  S* Grows_out; size_t go_vs;    // [v][Bp][Kp] (nullable)
+};
+
+struct GatherArgs {
+  const float* X;                // [n][d0] caller's rows
+  const int32_t* y;              // [n]
+  const uint32_t* perm;          // [n] (nullable: identity)
+  int64_t n;
+  int d0, Kp, B, Bp, T;          // T = steps (row blocks)
+  void* rows;                    // [T][Bp][Kp] S
+  int32_t* labels;               // [T][Bp]
+};
+
+struct TransposeArgs {
+  const void* src;               // [T][Bp][Kp] S
+  void* dst;                     // [T][Kp][Bp] S
+  int Kp, Bp, T;
+};
+
+// ---------------------------------------------------------------- launchers
+// Each returns hipSuccess or the launch error.  Shapes are validated by the
+// caller (gevo_capi.hip) before these are reached.
+hipError_t launch_init(const InitArgs& a, hipStream_t s);
+template <typename S> hipError_t launch_layer(const LayerArgs<S>& a, int P, hipStream_t s);
+template <typename S> hipError_t launch_out(const OutArgs<S>& a, int P, hipStream_t s);
+template <typename S> hipError_t launch_bwd(const BwdArgs<S>& a, int P, hipStream_t s);
+template <typename S> hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
+template <typename S> hipError_t launch_transpose(const TransposeArgs& a, hipStream_t s);
+hipError_t launch_zero_bytes(void* p, size_t bytes, hipStream_t s);
+hipError_t launch_reduce_partials(const double* part_ce, const unsigned int* part_corr, int P, int n_chunks,
+                                  double* ce_out, unsigned long long* corr_out, hipStream_t s);
+
+// Philox4x32-10 on the host (the library's own draws: learning rates,
+// densities, data order).
+void philox4x32_10_host(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]);
+
+}  // namespace gevo

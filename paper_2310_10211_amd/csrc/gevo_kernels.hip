@@ -1,0 +1,651 @@
+// HIP kernels of libgevo for CDNA4 (gfx950): population-batched training and
+// prediction of small fully-connected classifiers (fitness evaluation of
+// GEVO-ML, arXiv 2310.10211, section 4.3; SGD update of section 6.2).
+//
+// Device layout (per variant v, layer l with padded input width Kp and padded
+// output width Np, both multiples of 32):
+//   Wm   fp32 master weights, [v][Np][Kp]  ("out x in": k is contiguous)
+//   bias fp32 [v][Np]
+//   mask uint32 bit words, [v][Np][Kp/32] (bit k%32 of word k/32)
+// Activations and gradients come in two orientations: "rows" [v][b][feature]
+// (feature contiguous) and "cols" [v][feature][b] (batch contiguous), so that
+// every MFMA operand is read along its contraction index.
+//
+// GEMMs run on v_mfma_f32_32x32x16_bf16 (bf16 path) or v_mfma_f32_32x32x2_f32
+// (fp32 path).  Fragment layout of a 32x32xK MFMA with E elements per lane
+// (E = 8 for bf16, 1 for fp32): lane l supplies A[l%32][(l/32)*E + i] and
+// B[(l/32)*E + i][l%32]; the 16 accumulators of lane l hold
+// C[8*(r/4) + 4*(l/32) + r%4][l%32], r = 0..15.
+#include "gevo_internal.h"
+
+#include <math.h>
+
+namespace gevo {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ int crow(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// round-to-nearest-even binary32 -> bfloat16; NaN stays a quiet NaN
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x0040u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <typename S> struct Op;
+
+template <> struct Op<uint16_t> {           // bfloat16 operands
+  static constexpr int KM = 16;              // contraction per MFMA
+  static constexpr int KE = 8;               // consecutive elements per lane
+  static constexpr int PAD = 8;              // LDS row padding (elements)
+  typedef uint4 Frag;
+  __device__ __forceinline__ static Frag load(const uint16_t* p) { return *reinterpret_cast<const uint4*>(p); }
+  __device__ __forceinline__ static Frag gather(const uint16_t* p, int stride) {
+    uint4 f;
+    f.x = (uint32_t)p[0] | ((uint32_t)p[stride] << 16);
+    f.y = (uint32_t)p[2 * stride] | ((uint32_t)p[3 * stride] << 16);
+    f.z = (uint32_t)p[4 * stride] | ((uint32_t)p[5 * stride] << 16);
+    f.w = (uint32_t)p[6 * stride] | ((uint32_t)p[7 * stride] << 16);
+    return f;
+  }
+  __device__ __forceinline__ static f32x16_t mma(Frag a, Frag b, f32x16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+  }
+  __device__ __forceinline__ static uint16_t from_f32(float f) { return f32_to_bf16_bits(f); }
+  __device__ __forceinline__ static float to_f32(uint16_t h) { return bf16_bits_to_f32(h); }
+};
+
+template <> struct Op<float> {              // fp32 operands
+  static constexpr int KM = 2;
+  static constexpr int KE = 1;
+  static constexpr int PAD = 1;
+  typedef float Frag;
+  __device__ __forceinline__ static Frag load(const float* p) { return *p; }
+  __device__ __forceinline__ static Frag gather(const float* p, int) { return *p; }
+  __device__ __forceinline__ static f32x16_t mma(Frag a, Frag b, f32x16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+  __device__ __forceinline__ static float from_f32(float f) { return f; }
+  __device__ __forceinline__ static float to_f32(float h) { return h; }
+};
+
+__device__ __forceinline__ f32x16_t zero16() {
+  f32x16_t z;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) z[i] = 0.0f;
+  return z;
+}
+
+// ------------------------------------------------------------------ Philox
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two
+// 32x32->64-bit products; high halves are xored with the other counter words
+// and the round key, which is bumped by the Weyl constants between rounds.
+__device__ __forceinline__ uint4 philox(uint4 c, uint2 k) {
+#pragma unroll
+  for (int i = 0; i < 10; ++i) {
+    const uint32_t hi0 = __umulhi(0xD2511F53u, c.x), lo0 = 0xD2511F53u * c.x;
+    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c.z), lo1 = 0xCD9E8D57u * c.z;
+    c = make_uint4(hi1 ^ c.y ^ k.x, lo1, hi0 ^ c.w ^ k.y, lo0);
+    k.x += 0x9E3779B9u;
+    k.y += 0xBB67AE85u;
+  }
+  return c;
+}
+__device__ __forceinline__ uint32_t pick(uint4 r, uint32_t i) {
+  return i == 0 ? r.x : (i == 1 ? r.y : (i == 2 ? r.z : r.w));
+}
+
+// ------------------------------------------------------------ population init
+// One thread per (variant, padded output row n, 32-wide word of inputs k):
+// draws the 32 mask bits and initial weights of W_l[n][k0..k0+31].
+__global__ __launch_bounds__(256) void k_init(InitArgs a) {
+  const int words = a.Kp / 32;
+  const int64_t total = (int64_t)a.P * a.Np * words;
+  const uint2 key = make_uint2((uint32_t)(a.seed & 0xffffffffu), (uint32_t)(a.seed >> 32));
+  const float two_m24 = 5.9604644775390625e-08f;   // 2^-24
+  for (int64_t it = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; it < total;
+       it += (int64_t)gridDim.x * blockDim.x) {
+    const int kw = (int)(it % words);
+    const int n = (int)((it / words) % a.Np);
+    const int v = (int)(it / ((int64_t)words * a.Np));
+    const uint32_t th = a.thresh[v];
+    float* wrow = a.Wm + ((size_t)v * a.Np + n) * a.Kp + kw * 32;
+    uint32_t bits = 0;
+    uint64_t blk_m = ~0ull, blk_i = ~0ull, blk_n = ~0ull;
+    uint4 rm = make_uint4(0, 0, 0, 0), ri = rm, rn = rm;
+    for (int j = 0; j < 32; ++j) {
+      const int k = kw * 32 + j;
+      float w = 0.0f;
+      if (n < a.N && k < a.K) {
+        const uint64_t e = (uint64_t)n * (uint64_t)a.K + (uint64_t)k;
+        if ((e >> 2) != blk_m) {
+          blk_m = e >> 2;
+          rm = philox(make_uint4((uint32_t)blk_m, (uint32_t)a.l_index, (uint32_t)v, kStreamMask), key);
+        }
+        const bool keep = (pick(rm, (uint32_t)(e & 3)) >> 8) < th;
+        if (a.base_w) {
+          w = a.base_w[(size_t)n * a.Kp + k];
+        } else {
+          if ((e >> 2) != blk_i) {
+            blk_i = e >> 2;
+            ri = philox(make_uint4((uint32_t)blk_i, (uint32_t)a.l_index, 0u, kStreamInit), key);
+          }
+          const float u = (float)(pick(ri, (uint32_t)(e & 3)) >> 8) * two_m24;
+          const float t = __fsub_rn(__fmul_rn(2.0f, u), 1.0f);       // exact
+          w = __fmul_rn(t, a.xavier_a);
+        }
+        if (a.init_kind == 1) {
+          if ((e >> 1) != blk_n) {
+            blk_n = e >> 1;
+            rn = philox(make_uint4((uint32_t)blk_n, (uint32_t)a.l_index, (uint32_t)v, kStreamNoise), key);
+          }
+          const uint32_t w0 = (uint32_t)(e & 1) * 2u;
+          const float u1 = (float)((pick(rn, w0) >> 8) + 1u) * two_m24;   // (0, 1]
+          const float u2 = (float)(pick(rn, w0 + 1) >> 8) * two_m24;
+          const float eps = sqrtf(-2.0f * logf(u1)) * cosf(6.28318530717958647692f * u2);
+          w = __fmul_rn(w, __fadd_rn(1.0f, __fmul_rn(a.noise_std, eps)));
+        }
+        if (!keep) w = 0.0f;
+        bits |= (uint32_t)keep << j;
+      }
+      wrow[j] = w;
+    }
+    a.mask[((size_t)v * a.Np + n) * words + kw] = bits;
+    if (kw == 0) a.bias[(size_t)v * a.Np + n] = (a.base_b && n < a.N) ? a.base_b[n] : 0.0f;
+  }
+}
+
+// ------------------------------------------------------------ hidden layer
+// Workgroup (n-tile of 32 output units, variant v); four waves.
+// Update phase (do_update): for each 32-wide chunk of inputs k,
+//   dW^T[n][k] = sum_b G[n][b] * A[k][b]                  (MFMA, contraction = batch)
+//   W[n][k]    = mask ? fl(W - fl(lr * dW)) : +0           (fp32 master, in place)
+// and b[n] -= lr * sum_b G[n][b].  The updated chunk is kept in LDS as an
+// operand, so the forward pass of the next step runs without re-reading W:
+//   Z[r][n] = sum_k A_next[r][k] * W[n][k] + b[n],  A_out = relu(Z)  (MFMA)
+// Without do_update the chunk is loaded from the master (forward only).
+template <typename S, int BPMAX>
+__global__ __launch_bounds__(256) void k_layer(LayerArgs<S> a) {
+  using O = Op<S>;
+  constexpr int KM = O::KM, KE = O::KE;
+  constexpr int WSTR = 32 + O::PAD;
+  constexpr int NG = BPMAX / KM;
+  __shared__ __align__(16) S wl[4][32][WSTR];
+  __shared__ float bias_l[32];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int l32 = lane & 31, lh = lane >> 5;
+  const int n0 = blockIdx.x * 32, v = blockIdx.y;
+  const int Kp = a.Kp, Np = a.Np, nch = Kp / 32;
+  float* Wm = a.Wm + (size_t)v * Np * Kp;
+  const uint32_t* mk = a.mask + (size_t)v * Np * nch;
+  const float lrv = a.lr[v];
+
+  typename O::Frag gf[NG];
+  const int nsteps = a.Bp / KM;
+  if (a.do_update) {
+    // bias gradient of the 32 units: 8 lanes per unit, fixed-order reduction
+    const S* G = a.Gcols + v * a.g_vs;
+    const int nl = threadIdx.x >> 3, seg = threadIdx.x & 7, per = a.Bp / 8;
+    const S* gr = G + (size_t)(n0 + nl) * a.Bp + seg * per;
+    float s = 0.0f;
+    for (int b = 0; b < per; ++b) s += O::to_f32(gr[b]);
+    s += __shfl_xor(s, 1);
+    s += __shfl_xor(s, 2);
+    s += __shfl_xor(s, 4);
+    if (seg == 0) {
+      const float bo = a.bias[(size_t)v * Np + n0 + nl];
+      const float bn = __fsub_rn(bo, __fmul_rn(lrv, s));
+      a.bias[(size_t)v * Np + n0 + nl] = bn;
+      bias_l[nl] = bn;
+    }
+    const S* gp = G + (size_t)(n0 + l32) * a.Bp + lh * KE;
+#pragma unroll
+    for (int s2 = 0; s2 < NG; ++s2)
+      if (s2 < nsteps) gf[s2] = O::load(gp + s2 * KM);
+  } else if (threadIdx.x < 32) {
+    bias_l[threadIdx.x] = a.bias[(size_t)v * Np + n0 + threadIdx.x];
+  }
+
+  const int R = a.do_forward ? a.R : 0;
+  const int npass = a.do_forward ? (R + kPassRows - 1) / kPassRows : 1;
+  for (int pass = 0; pass < npass; ++pass) {
+    const int row0 = pass * kPassRows;
+    const int prows = a.do_forward ? min(kPassRows, R - row0) : 0;
+    const int ntiles = prows / 32;
+    const bool upd = a.do_update && pass == 0;
+    f32x16_t acc0 = zero16(), acc1 = zero16();
+    for (int round = 0; round * 4 < nch; ++round) {
+      const int c = round * 4 + wave;
+      if (c < nch) {
+        const int k0 = c * 32;
+        if (upd) {
+          float wold[16];
+          uint32_t mw[16];
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int n = n0 + crow(r, lane);
+            wold[r] = Wm[(size_t)n * Kp + k0 + l32];
+            mw[r] = mk[(size_t)n * nch + c];
+          }
+          f32x16_t d = zero16();
+          const S* ap = a.Acols + v * a.ac_vs + (size_t)(k0 + l32) * a.Bp + lh * KE;
+#pragma unroll
+          for (int s2 = 0; s2 < NG; ++s2)
+            if (s2 < nsteps) d = O::mma(gf[s2], O::load(ap + s2 * KM), d);
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int nl = crow(r, lane);
+            const bool keep = (mw[r] >> l32) & 1u;
+            const float wn = keep ? __fsub_rn(wold[r], __fmul_rn(lrv, d[r])) : 0.0f;
+            Wm[(size_t)(n0 + nl) * Kp + k0 + l32] = wn;
+            wl[wave][nl][l32] = O::from_f32(wn);
+          }
+        } else {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int nl = crow(r, lane);
+            wl[wave][nl][l32] = O::from_f32(Wm[(size_t)(n0 + nl) * Kp + k0 + l32]);
+          }
+        }
+      }
+      __syncthreads();
+      if (a.Wt && pass == 0) {
+        // transposed operand copy [k][n] for the backward of the layer above
+        const int j = threadIdx.x >> 6, kl = (threadIdx.x & 63) >> 1, half = threadIdx.x & 1;
+        const int cj = round * 4 + j;
+        if (cj < nch) {
+          S* dst = a.Wt + (size_t)v * Kp * Np + (size_t)(cj * 32 + kl) * Np + n0 + half * 16;
+#pragma unroll
+          for (int i = 0; i < 16; ++i) dst[i] = wl[j][half * 16 + i][kl];
+        }
+      }
+      if (ntiles > 0) {
+        for (int j = 0; j < 4; ++j) {
+          const int cj = round * 4 + j;
+          if (cj >= nch) break;
+          const int kk0 = cj * 32;
+#pragma unroll
+          for (int ti = 0; ti < 2; ++ti) {
+            const int tile = wave + 4 * ti;
+            if (tile < ntiles) {
+              const S* ar = a.Arows + v * a.ar_vs + (size_t)(row0 + tile * 32 + l32) * Kp + kk0 + lh * KE;
+              f32x16_t acc = ti == 0 ? acc0 : acc1;
+#pragma unroll
+              for (int ks = 0; ks < 32 / KM; ++ks)
+                acc = O::mma(O::load(ar + ks * KM), O::load(&wl[j][l32][ks * KM + lh * KE]), acc);
+              if (ti == 0) acc0 = acc; else acc1 = acc;
+            }
+          }
+        }
+      }
+      __syncthreads();
+    }
+    if (!a.do_forward) break;
+    // epilogue: bias + ReLU, rows store, transposed store through LDS
+#pragma unroll
+    for (int ti = 0; ti < 2; ++ti) {
+      const int tile = wave + 4 * ti;
+      const bool valid = tile < ntiles;
+      if (valid) {
+        const f32x16_t acc = ti == 0 ? acc0 : acc1;
+        const float bn = bias_l[l32];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int rl = crow(r, lane);
+          const int row = row0 + tile * 32 + rl;
+          const float z = acc[r] + bn;
+          const S sv = O::from_f32(z > 0.0f ? z : 0.0f);
+          a.Orows[v * a.or_vs + (size_t)row * Np + n0 + l32] = sv;
+          wl[wave][l32][rl] = sv;                       // [n][row] tile for the transposed store
+        }
+      }
+      __syncthreads();
+      if (valid && a.Ocols) {
+        const int nl = lane >> 1, half = lane & 1;
+        S* dst = a.Ocols + v * a.oc_vs + (size_t)(n0 + nl) * R + row0 + tile * 32 + half * 16;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) dst[i] = wl[wave][nl][half * 16 + i];
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// ------------------------------------------------------------ output layer
+// Workgroup = (row chunk, variant).  Logits on MFMA (classes padded to 32),
+// then per row (32 lanes hold the 32 classes of a row): max, NaN flag,
+// sum of exp, log-sum-exp, CE = lse - z_y, argmax with the lowest index on
+// ties (a NaN logit makes the row a miss), and in training the gradient
+// G = (softmax - onehot(y)) * fl(1/b) (section 6.2).  Training continues with
+//   dW_L[c][k] = sum_b G[b][c] A[k][b]  + masked SGD update of W_L, b_L
+//   G_{L-1}[k][b] = (sum_c W_L[c][k] G[b][c]) * [A[k][b] > 0]
+// using the pre-update W_L kept in LDS.
+template <typename S, int BPMAX>
+__global__ __launch_bounds__(256) void k_out(OutArgs<S> a) {
+  using O = Op<S>;
+  constexpr int KM = O::KM, KE = O::KE;
+  constexpr int GSTR = 32 + O::PAD;
+  constexpr int NG = BPMAX / KM;
+  extern __shared__ __align__(16) char smem[];
+  __shared__ double red_ce[4];
+  __shared__ unsigned int red_corr[4];
+  __shared__ float red_db[4][32];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int l32 = lane & 31, lh = lane >> 5;
+  const int v = blockIdx.y, chunk = blockIdx.x;
+  const int Kp = a.Kp, WS = Kp + O::PAD;
+  S* wop = reinterpret_cast<S*>(smem);                  // [32][WS]  W_L as operand, [class][k]
+  S* gs = wop + 32 * WS;                                // [BPMAX][GSTR] gradient rows (training)
+  const float* Wm = a.Wm + (size_t)v * 32 * Kp;
+  for (int i = threadIdx.x; i < 32 * Kp; i += 256) wop[(i / Kp) * WS + (i % Kp)] = O::from_f32(Wm[i]);
+  const float bias_c = a.bias[(size_t)v * 32 + l32];
+  __syncthreads();
+
+  const int row_base = a.train ? 0 : chunk * kOutRows;
+  const int rows = a.train ? a.Bp : min(kOutRows, a.rows - row_base);
+  const int ntiles = rows / 32;
+  const bool cvalid = l32 < a.C;
+  double ce_sum = 0.0;
+  unsigned int corr = 0;
+  float db_part = 0.0f;
+#pragma unroll
+  for (int ti = 0; ti < 2; ++ti) {
+    const int tile = wave + 4 * ti;
+    if (tile >= ntiles) continue;
+    f32x16_t acc = zero16();
+    const S* ar = a.Arows + v * a.ar_vs + (size_t)(row_base + tile * 32 + l32) * Kp + lh * KE;
+    const S* wr = wop + l32 * WS + lh * KE;
+    for (int k = 0; k < Kp; k += KM) acc = O::mma(O::load(ar + k), O::load(wr + k), acc);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rl = tile * 32 + crow(r, lane);
+      const int y = a.labels[row_base + rl];
+      const float z = acc[r] + bias_c;
+      int isn = (cvalid && (z != z)) ? 1 : 0;
+      float m = cvalid ? z : -INFINITY;
+      float bv = (cvalid && !isn) ? z : -INFINITY;
+      int bi = l32;
+#pragma unroll
+      for (int off = 16; off >= 1; off >>= 1) {
+        m = fmaxf(m, __shfl_xor(m, off));
+        isn |= __shfl_xor(isn, off);
+        const float ov = __shfl_xor(bv, off);
+        const int oi = __shfl_xor(bi, off);
+        if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+      }
+      const float e = cvalid ? expf(z - m) : 0.0f;
+      float s = e;
+#pragma unroll
+      for (int off = 16; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+      const float zy = __shfl(z, (lane & 32) | (y & 31));
+      const bool rvalid = y >= 0;
+      float ce = (logf(s) + m) - zy;
+      if (isn) ce = NAN;
+      if (l32 == 0 && rvalid) {
+        ce_sum += (double)ce;
+        corr += (!isn && bi == y) ? 1u : 0u;
+      }
+      if (a.train) {
+        const float p = e / s;
+        const float g = (cvalid && rvalid) ? (p - (l32 == y ? 1.0f : 0.0f)) * a.scale : 0.0f;
+        db_part += g;
+        gs[rl * GSTR + l32] = O::from_f32(g);
+      }
+    }
+  }
+  // reductions in a fixed order
+  ce_sum += __shfl_xor(ce_sum, 32);
+  corr += __shfl_xor(corr, 32);
+  db_part += __shfl_xor(db_part, 32);
+  if (lane == 0) { red_ce[wave] = ce_sum; red_corr[wave] = corr; }
+  if (lh == 0) red_db[wave][l32] = db_part;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const double t = ((red_ce[0] + red_ce[1]) + red_ce[2]) + red_ce[3];
+    const unsigned int cc = red_corr[0] + red_corr[1] + red_corr[2] + red_corr[3];
+    if (a.train) {
+      a.ce_acc[v] += t;
+      a.correct_acc[v] += cc;
+    } else {
+      a.part_ce[(size_t)v * a.n_chunks_total + a.chunk0 + chunk] = t;
+      a.part_correct[(size_t)v * a.n_chunks_total + a.chunk0 + chunk] = cc;
+    }
+  }
+  if (!a.train) return;
+
+  const float lrv = a.lr[v];
+  if (threadIdx.x < 32) {
+    const float db = ((red_db[0][threadIdx.x] + red_db[1][threadIdx.x]) + red_db[2][threadIdx.x]) +
+                     red_db[3][threadIdx.x];
+    const float bo = a.bias[(size_t)v * 32 + threadIdx.x];
+    a.bias[(size_t)v * 32 + threadIdx.x] = __fsub_rn(bo, __fmul_rn(lrv, db));
+  }
+  // dW_L and the masked update of the master (old W_L stays in LDS)
+  const int nsteps = a.Bp / KM;
+  typename O::Frag ga[NG];
+#pragma unroll
+  for (int s2 = 0; s2 < NG; ++s2)
+    if (s2 < nsteps) ga[s2] = O::gather(&gs[(s2 * KM + lh * KE) * GSTR + l32], GSTR);
+  float* Wmv = a.Wm + (size_t)v * 32 * Kp;
+  const uint32_t* mk = a.mask + (size_t)v * 32 * (Kp / 32);
+  const S* Acv = a.Acols + v * a.ac_vs;
+  for (int kt = wave; kt < Kp / 32; kt += 4) {
+    const int k0 = kt * 32;
+    float wold[16];
+    uint32_t mw[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int c = crow(r, lane);
+      wold[r] = Wmv[(size_t)c * Kp + k0 + l32];
+      mw[r] = mk[(size_t)c * (Kp / 32) + kt];
+    }
+    f32x16_t d = zero16();
+    const S* ap = Acv + (size_t)(k0 + l32) * a.Bp + lh * KE;
+#pragma unroll
+    for (int s2 = 0; s2 < NG; ++s2)
+      if (s2 < nsteps) d = O::mma(ga[s2], O::load(ap + s2 * KM), d);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int c = crow(r, lane);
+      const bool keep = (mw[r] >> l32) & 1u;
+      Wmv[(size_t)c * Kp + k0 + l32] = keep ? __fsub_rn(wold[r], __fmul_rn(lrv, d[r])) : 0.0f;
+    }
+  }
+  if (!a.Gcols) return;
+  // gradient of the last hidden layer, batch-contiguous, with ReLU'
+  const int tb = a.Bp / 32, ntot = (Kp / 32) * tb;
+  for (int t = wave; t < ntot; t += 4) {
+    const int kt = t / tb, bt = t % tb;
+    f32x16_t acc = zero16();
+#pragma unroll
+    for (int ks = 0; ks < 32 / KM; ++ks) {
+      const typename O::Frag af = O::gather(&wop[(ks * KM + lh * KE) * WS + kt * 32 + l32], WS);
+      const typename O::Frag bf = O::load(&gs[(bt * 32 + l32) * GSTR + ks * KM + lh * KE]);
+      acc = O::mma(af, bf, acc);
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int k = kt * 32 + crow(r, lane);
+      const int b = bt * 32 + l32;
+      const float av = O::to_f32(Acv[(size_t)k * a.Bp + b]);
+      const S g = O::from_f32(av > 0.0f ? acc[r] : 0.0f);
+      a.Gcols[v * a.gc_vs + (size_t)k * a.Bp + b] = g;
+      if (a.Grows) a.Grows[v * a.gr_vs + (size_t)b * Kp + k] = g;
+    }
+  }
+}
+
+// ------------------------------------------------------- hidden backward GEMM
+// G_{l-1}[k][b] = (sum_n W_l[n][k] G_l[b][n]) * [A_{l-1}[k][b] > 0]; one
+// 32x32 output tile per wave, operands straight from L2.
+template <typename S>
+__global__ __launch_bounds__(256) void k_bwd(BwdArgs<S> a) {
+  using O = Op<S>;
+  constexpr int KM = O::KM, KE = O::KE;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int l32 = lane & 31, lh = lane >> 5;
+  const int v = blockIdx.y;
+  const int tb = a.Bp / 32;
+  const int t = blockIdx.x * 4 + wave;
+  if (t >= (a.Kp / 32) * tb) return;
+  const int kt = t / tb, bt = t % tb;
+  const S* wr = a.Wt + (size_t)v * a.Kp * a.Np + (size_t)(kt * 32 + l32) * a.Np + lh * KE;
+  const S* gr = a.Grows + v * a.gr_vs + (size_t)(bt * 32 + l32) * a.Np + lh * KE;
+  f32x16_t acc = zero16();
+  for (int n = 0; n < a.Np; n += KM) acc = O::mma(O::load(wr + n), O::load(gr + n), acc);
+  const S* acv = a.Acols + v * a.ac_vs;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int k = kt * 32 + crow(r, lane);
+    const int b = bt * 32 + l32;
+    const float av = O::to_f32(acv[(size_t)k * a.Bp + b]);
+    const S g = O::from_f32(av > 0.0f ? acc[r] : 0.0f);
+    a.Gcols[v * a.gc_vs + (size_t)k * a.Bp + b] = g;
+    if (a.Grows_out) a.Grows_out[v * a.go_vs + (size_t)b * a.Kp + k] = g;
+  }
+}
+
+// ------------------------------------------------------------- data movement
+// rows[t][b][k] = X[perm[t*B + b]][k] (zero for k >= d0, b >= b_t, b >= B),
+// labels[t][b] = y[...] or -1.
+template <typename S>
+__global__ __launch_bounds__(256) void k_gather(GatherArgs a) {
+  using O = Op<S>;
+  const int t = blockIdx.y, b = blockIdx.x;
+  const int64_t r = (int64_t)t * a.B + b;
+  const bool valid = b < a.B && r < a.n;
+  const int64_t src = valid ? (a.perm ? (int64_t)a.perm[r] : r) : 0;
+  S* out = reinterpret_cast<S*>(a.rows) + ((size_t)t * a.Bp + b) * a.Kp;
+  const float* x = a.X + src * a.d0;
+  for (int k = threadIdx.x; k < a.Kp; k += blockDim.x) {
+    const float xv = (valid && k < a.d0) ? x[k] : 0.0f;
+    out[k] = O::from_f32(xv);
+  }
+  if (threadIdx.x == 0) a.labels[(size_t)t * a.Bp + b] = valid ? a.y[src] : -1;
+}
+
+template <typename S>
+__global__ __launch_bounds__(256) void k_transpose(TransposeArgs a) {
+  __shared__ S tile[32][33];
+  const int k0 = blockIdx.x * 32, b0 = blockIdx.y * 32, t = blockIdx.z;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  const S* src = reinterpret_cast<const S*>(a.src) + (size_t)t * a.Bp * a.Kp;
+  S* dst = reinterpret_cast<S*>(a.dst) + (size_t)t * a.Kp * a.Bp;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) tile[ty + 8 * i][tx] = src[(size_t)(b0 + ty + 8 * i) * a.Kp + k0 + tx];
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 4; ++i) dst[(size_t)(k0 + ty + 8 * i) * a.Bp + b0 + tx] = tile[tx][ty + 8 * i];
+}
+
+__global__ __launch_bounds__(256) void k_zero(uint32_t* p, size_t words) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < words; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = 0u;
+}
+
+__global__ __launch_bounds__(256) void k_reduce_partials(const double* part_ce, const unsigned int* part_corr,
+                                                         int P, int nch, double* ce_out,
+                                                         unsigned long long* corr_out) {
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= P) return;
+  double s = 0.0;
+  unsigned long long c = 0;
+  for (int i = 0; i < nch; ++i) {
+    s += part_ce[(size_t)v * nch + i];
+    c += part_corr[(size_t)v * nch + i];
+  }
+  ce_out[v] = s;
+  corr_out[v] = c;
+}
+
+// ---------------------------------------------------------------- launchers
+static inline unsigned grid_for(int64_t items, int per_block = 256, int64_t cap = 65536) {
+  int64_t g = (items + per_block - 1) / per_block;
+  if (g < 1) g = 1;
+  if (g > cap) g = cap;
+  return (unsigned)g;
+}
+
+hipError_t launch_init(const InitArgs& a, hipStream_t s) {
+  const int64_t items = (int64_t)a.P * a.Np * (a.Kp / 32);
+  hipLaunchKernelGGL(k_init, dim3(grid_for(items)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <typename S>
+hipError_t launch_layer(const LayerArgs<S>& a, int P, hipStream_t s) {
+  const dim3 grid(a.Np / 32, P);
+  if (a.Bp <= 128)
+    hipLaunchKernelGGL((k_layer<S, 128>), grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_layer<S, 256>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <typename S>
+size_t out_lds_bytes(int Kp, int Bp, int train) {
+  return (size_t)32 * (Kp + Op<S>::PAD) * sizeof(S) + (train ? (size_t)Bp * (32 + Op<S>::PAD) * sizeof(S) : 0);
+}
+
+template <typename S>
+hipError_t launch_out(const OutArgs<S>& a, int P, hipStream_t s) {
+  const size_t lds = out_lds_bytes<S>(a.Kp, a.Bp, a.train);
+  const dim3 grid(a.train ? 1 : (a.rows + kOutRows - 1) / kOutRows, P);
+  if (a.Bp <= 128)
+    hipLaunchKernelGGL((k_out<S, 128>), grid, dim3(256), lds, s, a);
+  else
+    hipLaunchKernelGGL((k_out<S, 256>), grid, dim3(256), lds, s, a);
+  return hipGetLastError();
+}
+
+template <typename S>
+hipError_t launch_bwd(const BwdArgs<S>& a, int P, hipStream_t s) {
+  const int tiles = (a.Kp / 32) * (a.Bp / 32);
+  hipLaunchKernelGGL(k_bwd<S>, dim3((tiles + 3) / 4, P), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <typename S>
+hipError_t launch_gather(const GatherArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_gather<S>, dim3(a.Bp, a.T), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <typename S>
+hipError_t launch_transpose(const TransposeArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_transpose<S>, dim3(a.Kp / 32, a.Bp / 32, a.T), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_bytes(void* p, size_t bytes, hipStream_t s) {
+  const size_t words = bytes / 4;
+  if (words == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_zero, dim3(grid_for((int64_t)words, 256, 4096)), dim3(256), 0, s, (uint32_t*)p, words);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_partials(const double* part_ce, const unsigned int* part_corr, int P, int n_chunks,
+                                  double* ce_out, unsigned long long* corr_out, hipStream_t s) {
+  hipLaunchKernelGGL(k_reduce_partials, dim3((P + 255) / 256), dim3(256), 0, s, part_ce, part_corr, P, n_chunks,
+                     ce_out, corr_out);
+  return hipGetLastError();
+}
+
+template hipError_t launch_layer<float>(const LayerArgs<float>&, int, hipStream_t);
+template hipError_t launch_layer<uint16_t>(const LayerArgs<uint16_t>&, int, hipStream_t);
+template hipError_t launch_out<float>(const OutArgs<float>&, int, hipStream_t);
+template hipError_t launch_out<uint16_t>(const OutArgs<uint16_t>&, int, hipStream_t);
+template hipError_t launch_bwd<float>(const BwdArgs<float>&, int, hipStream_t);
+template hipError_t launch_bwd<uint16_t>(const BwdArgs<uint16_t>&, int, hipStream_t);
+template hipError_t launch_gather<float>(const GatherArgs&, hipStream_t);
+template hipError_t launch_gather<uint16_t>(const GatherArgs&, hipStream_t);
+template hipError_t launch_transpose<float>(const TransposeArgs&, hipStream_t);
+template hipError_t launch_transpose<uint16_t>(const TransposeArgs&, hipStream_t);
+
+}  // namespace gevo
