@@ -1,0 +1,276 @@
+#!/usr/bin/env python3
+"""Benchmark of population-batched fitness evaluation on one MI355X.
+
+One step = one full fitness evaluation of the population (GEVO-ML, arXiv
+2310.10211, section 4.3): create the population from the seed (masks, initial
+weights), retrain every variant for the workload's epochs of mini-batch SGD
+over the training split (section 6.2), predict the test split, read the
+scores.  The default workload is P=256 variants of a 784-256-10 classifier in
+bf16 with fp32 master weights, 60,000 MNIST-shaped synthetic rows, batch 128,
+2 epochs.
+
+Prints one JSON line.  `value` = variant-samples/s of training over the whole
+step (P * n_train * epochs / step time); inputs are resident in HBM before the
+timed region.  `roofline` is for the kernel with the largest share of the
+timed kernel time, from HIP events recorded by each launch's own dispatch.
+`cpu_baseline` times the CPU oracle on a bounded sample of the same workload.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK = {"bf16": 2500.0, "f32": 157.3}        # dense MFMA TFLOP/s, MI355X
+HBM_PEAK_GBS = 8000.0
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2310_10211_amd", "csrc", "gevo_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.json")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", type=int, default=3, help="workload 1..5 (default 3)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU-oracle sample")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-profile", action="store_true", help="time without per-kernel events")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 1 GiB device copy 3 times (reference for HBM counters) and exit")
+    return ap.parse_args()
+
+
+def calibrate_copy():
+    """A plain copy kernel of known size: 1 GiB read + 1 GiB written per launch."""
+    import torch
+    n = 1 << 28                                    # 2^28 float32 = 1 GiB
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read_per_launch": 4 * n, "copy_bytes_written_per_launch": 4 * n, "launches": 3}))
+
+
+# ------------------------------------------------------------ algorithmic cost
+def layer_costs(cfg):
+    """Per-launch algorithmic bytes and flops of each kernel kind (real, unpadded
+    dims; e = operand bytes).  Returns {kind: (bytes, flops)} per launch, averaged
+    over the launches of one SGD step, plus per-step launch counts."""
+    d, P, B = cfg["dims"], cfg["P"], cfg["batch"]
+    e = 2 if cfg["dtype"] == "bf16" else 4
+    L = len(d) - 1
+    out = {}
+    # hidden layers l = 1..L-1: weight gradient + masked update (+ next forward)
+    lb, lf = [], []
+    for l in range(1, L):
+        K, N = d[l - 1], d[l]
+        shared_in = l == 1
+        per_v = N * K * 8 + N * K / 8 + N * B * e + 2 * B * N * e + N * 8   # W rd+wr, mask, G in, A out, bias
+        in_b = (K * B * e) * 2                                             # A cols (dW) + A rows (next forward)
+        byts = P * per_v + (in_b if shared_in else P * in_b)
+        lb.append(byts)
+        lf.append(P * 4.0 * B * K * N)                                      # dW + forward
+    if lb:
+        out["layer_train"] = (sum(lb) / len(lb), sum(lf) / len(lf), len(lb))
+    # output layer
+    K, C = d[L - 1], d[L]
+    byts = P * (C * K * 8 + C * K / 8 + 2 * B * K * e + (K * B * e if L > 1 else 0))
+    fl = P * 2.0 * B * K * C * (3 if L > 1 else 2)
+    out["out_train"] = (byts, fl, 1)
+    # hidden backward GEMMs
+    bb, bf = [], []
+    for l in range(2, L):
+        K, N = d[l - 1], d[l]
+        bb.append(P * (K * N * e + B * N * e + 2 * K * B * e))
+        bf.append(P * 2.0 * B * K * N)
+    if bb:
+        out["bwd"] = (sum(bb) / len(bb), sum(bf) / len(bf), len(bb))
+    return out
+
+
+def train_flops_per_sample(dims):
+    """fwd 2 + weight gradient 2 (+ input gradient 2 above the first layer) per weight."""
+    f = 4 * dims[0] * dims[1]
+    for l in range(2, len(dims)):
+        f += 6 * dims[l - 1] * dims[l]
+    return f
+
+
+def predict_flops_per_sample(dims):
+    return sum(2 * dims[l - 1] * dims[l] for l in range(1, len(dims)))
+
+
+def source_sha():
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def traffic_for(kernel, workload):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or None
+    if absent or taken on a different kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    rec = t.get(workload, {}).get(kernel)
+    if not rec or rec.get("kernel_source_sha") != source_sha():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+# ------------------------------------------------------------------ CPU oracle
+def cpu_baseline(cfg, data, budget_s):
+    import oracle
+    threads = min(8, os.cpu_count() or 1)
+    V = threads
+    variants = list(range(0, cfg["P"], max(1, cfg["P"] // V)))[:V]
+    if cfg["epochs"] == 0:                   # prediction workload
+        rows = 256
+        sub = dict(data, y_test=data["y_test"][:rows], x_test=data["x_test"][:rows])
+        t0 = time.perf_counter()
+        oracle.evaluate(cfg, sub, variants=variants[:1], epochs=0, threads=1)
+        one = time.perf_counter() - t0
+        rows = int(max(256, min(len(data["y_test"]), rows * budget_s / max(one, 1e-3) * 0.8)))
+        sub = dict(data, y_test=data["y_test"][:rows], x_test=data["x_test"][:rows])
+        t0 = time.perf_counter()
+        oracle.evaluate(cfg, sub, variants=variants, epochs=0, threads=threads)
+        wall = time.perf_counter() - t0
+        return dict(value=len(variants) * rows / wall, unit="variant-samples/s", cores=threads, kind="oracle",
+                    sample=f"{len(variants)} variants x {rows} test rows, prediction, {cfg['dtype']} oracle, "
+                           f"{threads} threads, {wall:.1f} s")
+    B = cfg["batch"]
+    t0 = time.perf_counter()
+    oracle.evaluate(cfg, data, variants=variants[:1], epochs=1, steps=1, threads=1, do_predict=False)
+    one = time.perf_counter() - t0
+    steps = int(max(1, min((len(data["y_train"]) + B - 1) // B, budget_s / max(one, 1e-3) * 0.8)))
+    t0 = time.perf_counter()
+    oracle.evaluate(cfg, data, variants=variants, epochs=1, steps=steps, threads=threads, do_predict=False)
+    wall = time.perf_counter() - t0
+    return dict(value=len(variants) * steps * B / wall, unit="variant-samples/s", cores=threads, kind="oracle",
+                sample=f"{len(variants)} variants x {steps} SGD steps of batch {B} (epoch 0), {cfg['dtype']} "
+                       f"oracle, {threads} threads, {wall:.1f} s")
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py: this build evaluates a population on exactly one GPU (asked for {max(args.gpus, world)}); "
+              "variants would shard across GPUs with no exchange of weights.", file=sys.stderr)
+        sys.exit(2)
+
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
+
+    import torch
+    import paper_2310_10211_amd as g
+    import synthetic
+
+    cfg = synthetic.config(args.config)
+    print(f"[bench] workload {cfg['name']}: generating synthetic data", file=sys.stderr, flush=True)
+    data = synthetic.dataset(cfg)
+    dev = torch.device("cuda:0")
+    pop = g.Population(cfg, data["x_train"], data["y_train"], data["x_test"], data["y_test"], device=dev)
+    torch.cuda.synchronize()
+
+    def step(profile):
+        pop.reinit()
+        if profile:
+            pop.set_profiling(True)
+        for ep in range(cfg["epochs"]):
+            pop.train_epoch(ep)
+        pop.predict()
+        s = pop.scores()
+        stats = pop.kernel_stats() if profile else None
+        return s, stats
+
+    for i in range(args.warmup):
+        step(False)
+        print(f"[bench] warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
+
+    profile = not args.no_profile
+    kstats = {}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        s, st = step(profile)
+        if st:
+            for k, (ms, n) in st.items():
+                a = kstats.setdefault(k, [0.0, 0])
+                a[0] += ms
+                a[1] += n
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    print(f"[bench] timed {args.steps} steps", file=sys.stderr, flush=True)
+    ms_step = (t1 - t0) * 1e3 / args.steps
+
+    P, n_tr, n_te, E = cfg["P"], cfg["n_train"], cfg["n_test"], cfg["epochs"]
+    if E > 0:
+        value = P * n_tr * E / (ms_step / 1e3)
+        work_flops = P * n_tr * E * train_flops_per_sample(cfg["dims"]) + P * n_te * predict_flops_per_sample(cfg["dims"])
+    else:
+        value = P * n_te / (ms_step / 1e3)
+        work_flops = P * n_te * predict_flops_per_sample(cfg["dims"])
+    peak = PEAK[cfg["dtype"]]
+
+    roofline = None
+    kernel_ms = {k: round(v[0] / args.steps, 3) for k, v in kstats.items() if v[1]}
+    if kstats:
+        dom = max((k for k in kstats if kstats[k][1] > 0), key=lambda k: kstats[k][0])
+        avg_s = kstats[dom][0] / kstats[dom][1] / 1e3
+        costs = layer_costs(cfg)
+        if dom in costs:
+            byts, fl, _ = costs[dom]
+            ridge = peak * 1e12 / (HBM_PEAK_GBS * 1e9)
+            if fl / byts < ridge:
+                ach = byts / avg_s / 1e9
+                roofline = dict(bound="hbm", achieved=round(ach, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                                frac=round(ach / HBM_PEAK_GBS, 4))
+            else:
+                ach = fl / avg_s / 1e12
+                roofline = dict(bound="mfma", achieved=round(ach, 1), peak=peak, unit="TFLOP/s",
+                                frac=round(ach / peak, 4))
+            roofline.update(kernel=dom, avg_launch_us=round(avg_s * 1e6, 2), launches=kstats[dom][1],
+                            algorithmic_bytes_per_launch=int(byts), algorithmic_flops_per_launch=int(fl),
+                            traffic=traffic_for(dom, cfg["name"]))
+
+    cpu = None
+    if not args.no_cpu:
+        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(cfg, data, args.cpu_seconds)
+
+    out = {
+        "metric": "variant-samples/sec (train fwd+bwd+SGD) at P variants; % bf16 MFMA peak",
+        "value": round(value, 1),
+        "unit": "variant-samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg["dtype"],
+        "data": "synthetic",
+        "config": {"workload": cfg["name"], "P": P, "dims": cfg["dims"], "batch": cfg["batch"], "epochs": E,
+                   "n_train": n_tr, "n_test": n_te, "step": "init + all epochs + test prediction + scores",
+                   "parallelism": "population (one GPU)"},
+        "mfma_frac_of_step": round(work_flops / (ms_step / 1e3) / (peak * 1e12), 4),
+        "kernel_ms_per_step": kernel_ms,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

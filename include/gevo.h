@@ -193,6 +193,28 @@ gevo_status gevo_pop_epoch_labels(gevo_pop* pop, int32_t* labels_out, int64_t n)
 /* Host-side data order of epoch `epoch` over n rows (definition above). */
 gevo_status gevo_epoch_permutation(uint64_t seed, uint32_t epoch, uint32_t n, uint32_t* out);
 
+/*
+ * Kernel-level timing for evidence (fitness time of section 4.3 broken down
+ * by kernel).  With profiling enabled, every kernel enqueued by this handle
+ * carries a HIP event pair recorded by its own dispatch on the handle's
+ * stream; gevo_pop_kernel_stats synchronises and returns, per kind, the summed
+ * kernel time in ms and the launch count since the handle was created.
+ */
+typedef enum {
+  GEVO_KERNEL_INIT = 0,          /* population init (masks, weights) */
+  GEVO_KERNEL_GATHER = 1,        /* per-epoch gather of the data order, transpose */
+  GEVO_KERNEL_LAYER_TRAIN = 2,   /* hidden layer: weight gradient, masked SGD, next forward */
+  GEVO_KERNEL_LAYER_FWD = 3,     /* hidden layer forward only (epoch start, prediction) */
+  GEVO_KERNEL_OUT_TRAIN = 4,     /* output layer: loss, gradients, update */
+  GEVO_KERNEL_OUT_PREDICT = 5,   /* output layer: loss and accuracy on the test split */
+  GEVO_KERNEL_BWD = 6,           /* hidden backward GEMM */
+  GEVO_KERNEL_AUX = 7,           /* zeroing, reductions */
+  GEVO_KERNEL_KINDS = 8
+} gevo_kernel_kind;
+
+gevo_status gevo_pop_set_profiling(gevo_pop* pop, int enable);
+gevo_status gevo_pop_kernel_stats(gevo_pop* pop, int kind, double* total_ms, uint64_t* launches);
+
 /* Release the handle (does not free the caller's device memory). */
 void gevo_pop_destroy(gevo_pop* pop);
 

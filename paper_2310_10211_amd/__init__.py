@@ -33,8 +33,9 @@ EXPORTED = [
     "gevo_pop_workspace_bytes", "gevo_pop_init", "gevo_pop_train_epoch", "gevo_pop_train_steps",
     "gevo_pop_steps_per_epoch", "gevo_pop_predict", "gevo_pop_scores", "gevo_pop_last_time",
     "gevo_pop_export", "gevo_pop_import", "gevo_pop_epoch_labels", "gevo_epoch_permutation",
-    "gevo_pop_destroy", "gevo_status_str",
+    "gevo_pop_set_profiling", "gevo_pop_kernel_stats", "gevo_pop_destroy", "gevo_status_str",
 ]
+KERNEL_KINDS = ["init", "gather", "layer_train", "layer_fwd", "out_train", "out_predict", "bwd", "aux"]
 
 
 class GevoError(RuntimeError):
@@ -89,6 +90,9 @@ def lib():
         L.gevo_pop_import.argtypes = [vp, u32, f32p]
         L.gevo_pop_epoch_labels.argtypes = [vp, ctypes.POINTER(ctypes.c_int32), i64]
         L.gevo_epoch_permutation.argtypes = [ctypes.c_uint64, u32, u32, ctypes.POINTER(u32)]
+        L.gevo_pop_set_profiling.argtypes = [vp, ctypes.c_int]
+        L.gevo_pop_kernel_stats.argtypes = [vp, ctypes.c_int, ctypes.POINTER(ctypes.c_double),
+                                            ctypes.POINTER(ctypes.c_uint64)]
         L.gevo_pop_destroy.argtypes = [vp]
         L.gevo_pop_destroy.restype = None
         L.gevo_status_str.argtypes = [ctypes.c_int]
@@ -248,6 +252,30 @@ class Population:
         _check(lib().gevo_pop_epoch_labels(self._h, out.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
                                            self.n_train), "gevo_pop_epoch_labels")
         return out
+
+    def set_profiling(self, on: bool = True):
+        _check(lib().gevo_pop_set_profiling(self._h, 1 if on else 0), "gevo_pop_set_profiling")
+
+    def kernel_stats(self) -> dict:
+        """{kind: (total_ms, launches)} of kernels enqueued while profiling was on."""
+        out = {}
+        for i, name in enumerate(KERNEL_KINDS):
+            ms, n = ctypes.c_double(), ctypes.c_uint64()
+            _check(lib().gevo_pop_kernel_stats(self._h, i, ctypes.byref(ms), ctypes.byref(n)), "gevo_pop_kernel_stats")
+            out[name] = (ms.value, n.value)
+        return out
+
+    def reinit(self):
+        """Destroy the handle and create a fresh population on the same workspace
+        and datasets (a new fitness evaluation from the seed)."""
+        self.close()
+        h = ctypes.c_void_p()
+        ptr = lambda t: None if t is None else ctypes.c_void_p(t.data_ptr())
+        _check(lib().gevo_pop_init(ctypes.byref(self._cfg), ctypes.c_void_p(self.workspace.data_ptr()),
+                                   self.workspace.numel(), ptr(self.x_train), ptr(self.y_train), ptr(self.x_test),
+                                   ptr(self.y_test), ctypes.c_void_p(self.stream.cuda_stream), ctypes.byref(h)),
+               "gevo_pop_init")
+        self._h = h
 
     def close(self):
         if getattr(self, "_h", None) is not None and self._h.value:

@@ -67,7 +67,7 @@ gevo_status validate(const gevo_pop_config* c) {
 
 // dynamic LDS of the output kernel: operand copy of W_L plus, in training, the gradient rows
 size_t out_lds(int Kp, int Bp, size_t elt, int pad) {
-  return (size_t)32 * (Kp + pad) * elt + (size_t)Bp * (32 + pad) * elt;
+  return (size_t)32 * (Kp + pad) * elt + (size_t)Bp * (32 + pad) * elt + (size_t)4 * 32 * 36 * 4;
 }
 
 gevo_status make_layout(const gevo_pop_config* c, Layout* o) {
@@ -202,12 +202,66 @@ struct gevo_pop {
   bool timing_pending = false;
   double last_s = 0.0;
   bool predicted = false;
+  // kernel-level timing (gevo_pop_set_profiling)
+  bool prof_on = false;
+  struct ProfRec { int kind; hipEvent_t a, b; };
+  std::vector<ProfRec> prof_pending;
+  std::vector<hipEvent_t> ev_free, ev_all;
+  double prof_ms[GEVO_KERNEL_KINDS] = {0};
+  uint64_t prof_n[GEVO_KERNEL_KINDS] = {0};
 };
 
 namespace {
 
 template <typename T>
 T* at(gevo_pop* p, size_t off) { return reinterpret_cast<T*>(p->ws + off); }
+
+constexpr size_t kProfBatch = 4096;   // launches between resolutions of pending timings
+
+hipEvent_t take_event(gevo_pop* p) {
+  if (!p->ev_free.empty()) {
+    hipEvent_t e = p->ev_free.back();
+    p->ev_free.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  p->ev_all.push_back(e);
+  return e;
+}
+
+hipError_t prof_resolve(gevo_pop* p) {
+  if (p->prof_pending.empty()) return hipSuccess;
+  hipError_t err = hipStreamSynchronize(p->stream);
+  if (err != hipSuccess) return err;
+  for (const auto& r : p->prof_pending) {
+    float ms = 0.0f;
+    if (hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
+      p->prof_ms[r.kind] += (double)ms;
+      p->prof_n[r.kind] += 1;
+    }
+    p->ev_free.push_back(r.a);
+    p->ev_free.push_back(r.b);
+  }
+  p->prof_pending.clear();
+  return hipSuccess;
+}
+
+// events recorded by the dispatch of the next launch of this kind (none when profiling is off)
+LaunchEv prof(gevo_pop* p, int kind) {
+  LaunchEv ev;
+  if (!p->prof_on) return ev;
+  if (p->prof_pending.size() >= kProfBatch && prof_resolve(p) != hipSuccess) return ev;
+  ev.start = take_event(p);
+  ev.stop = take_event(p);
+  if (!ev.start || !ev.stop) {
+    if (ev.start) p->ev_free.push_back(ev.start);
+    if (ev.stop) p->ev_free.push_back(ev.stop);
+    return LaunchEv{};
+  }
+  p->prof_pending.push_back({kind, ev.start, ev.stop});
+  return ev;
+}
 
 #define HIP_TRY(x)                              \
   do {                                          \
@@ -237,7 +291,7 @@ gevo_status forward_hidden(gevo_pop* p, const S* arows0, size_t ar0_vs, int R, i
       if (q.Wt) a.Wt = at<S>(p, q.Wt);
     }
     if (a.Kp % kTile || a.Np % kTile || a.R % kTile || a.R <= 0) return GEVO_E_SHAPE;
-    HIP_TRY(launch_layer<S>(a, y.P, p->stream));
+    HIP_TRY(launch_layer<S>(a, y.P, p->stream, prof(p, GEVO_KERNEL_LAYER_FWD)));
   }
   return GEVO_OK;
 }
@@ -257,12 +311,12 @@ gevo_status begin_epoch(gevo_pop* p, int e) {
   g.X = p->trX; g.y = p->trY; g.perm = at<uint32_t>(p, y.perm); g.n = y.n_train;
   g.d0 = y.lay[0].K; g.Kp = y.lay[0].Kp; g.B = y.B; g.Bp = y.Bp; g.T = y.T;
   g.rows = p->ws + y.xrows; g.labels = at<int32_t>(p, y.yep);
-  HIP_TRY(launch_gather<S>(g, p->stream));
+  HIP_TRY(launch_gather<S>(g, p->stream, prof(p, GEVO_KERNEL_GATHER)));
   TransposeArgs tr{};
   tr.src = p->ws + y.xrows; tr.dst = p->ws + y.xcols; tr.Kp = y.lay[0].Kp; tr.Bp = y.Bp; tr.T = y.T;
-  HIP_TRY(launch_transpose<S>(tr, p->stream));
-  HIP_TRY(launch_zero_bytes(p->ws + y.train_ce, (size_t)y.P * 8, p->stream));
-  HIP_TRY(launch_zero_bytes(p->ws + y.train_corr, (size_t)y.P * 8, p->stream));
+  HIP_TRY(launch_transpose<S>(tr, p->stream, prof(p, GEVO_KERNEL_GATHER)));
+  HIP_TRY(launch_zero_bytes(p->ws + y.train_ce, (size_t)y.P * 8, p->stream, prof(p, GEVO_KERNEL_AUX)));
+  HIP_TRY(launch_zero_bytes(p->ws + y.train_corr, (size_t)y.P * 8, p->stream, prof(p, GEVO_KERNEL_AUX)));
   // forward of step 0 for the hidden layers
   if (y.L > 1) {
     gevo_status st = forward_hidden<S>(p, at<S>(p, y.xrows), 0, y.Bp, 0, false);
@@ -307,7 +361,7 @@ gevo_status train_step(gevo_pop* p, int t) {
     a.ce_acc = at<double>(p, y.train_ce);
     a.correct_acc = at<unsigned long long>(p, y.train_corr);
     if (a.Kp % kTile || a.Bp % kTile) return GEVO_E_SHAPE;
-    HIP_TRY(launch_out<S>(a, y.P, p->stream));
+    HIP_TRY(launch_out<S>(a, y.P, p->stream, prof(p, GEVO_KERNEL_OUT_TRAIN)));
   }
   // hidden backward GEMMs, top down (pre-update weights)
   for (int l = L - 2; l >= 1; --l) {          // layer index l (0-based) has a hidden layer below
@@ -321,7 +375,7 @@ gevo_status train_step(gevo_pop* p, int t) {
     a.Gcols = at<S>(p, h.gcols); a.gc_vs = (size_t)h.Np * y.Bp;
     if (h.grows) { a.Grows_out = at<S>(p, h.grows); a.go_vs = (size_t)y.Bp * h.Np; }
     if (a.Kp % kTile || a.Np % kTile || a.Bp % kTile || a.Kp != h.Np) return GEVO_E_SHAPE;
-    HIP_TRY(launch_bwd<S>(a, y.P, p->stream));
+    HIP_TRY(launch_bwd<S>(a, y.P, p->stream, prof(p, GEVO_KERNEL_BWD)));
   }
   // hidden layers bottom up: update, then the forward of step t+1
   const bool fwd = t + 1 < y.T;
@@ -345,7 +399,7 @@ gevo_status train_step(gevo_pop* p, int t) {
     }
     if (q.Wt) a.Wt = at<S>(p, q.Wt);
     if (a.Kp % kTile || a.Np % kTile || a.Bp % kTile || a.Bp > kPassRows) return GEVO_E_SHAPE;
-    HIP_TRY(launch_layer<S>(a, y.P, p->stream));
+    HIP_TRY(launch_layer<S>(a, y.P, p->stream, prof(p, GEVO_KERNEL_LAYER_TRAIN)));
   }
   p->rows_done += bt;
   return GEVO_OK;
@@ -412,11 +466,11 @@ gevo_status do_predict(gevo_pop* p) {
     a.part_ce = at<double>(p, y.part_ce);
     a.part_correct = at<unsigned int>(p, y.part_corr);
     if (a.Kp % kTile || R % kOutRows) return GEVO_E_SHAPE;
-    HIP_TRY(launch_out<S>(a, y.P, p->stream));
+    HIP_TRY(launch_out<S>(a, y.P, p->stream, prof(p, GEVO_KERNEL_OUT_PREDICT)));
   }
   HIP_TRY(launch_reduce_partials(at<double>(p, y.part_ce), at<unsigned int>(p, y.part_corr), y.P,
                                  y.n_chunks_test, at<double>(p, y.test_ce),
-                                 at<unsigned long long>(p, y.test_corr), p->stream));
+                                 at<unsigned long long>(p, y.test_corr), p->stream, prof(p, GEVO_KERNEL_AUX)));
   HIP_TRY(hipEventRecord(p->ev1, p->stream));
   p->timing_pending = true;
   p->predicted = true;
@@ -542,19 +596,19 @@ gevo_status gevo_pop_init(const gevo_pop_config* cfg, void* d_ws, size_t ws_byte
     a.bias = reinterpret_cast<float*>(p->ws + q.bias);
     a.mask = reinterpret_cast<uint32_t*>(p->ws + q.mask);
     if (q.Kp % kTile || q.Np % kTile) return fail(GEVO_E_SHAPE);
-    if (launch_init(a, s) != hipSuccess) return fail(GEVO_E_HIP);
+    if (launch_init(a, s, LaunchEv{}) != hipSuccess) return fail(GEVO_E_HIP);
   }
   // test split converted once to the operand type, padded to whole chunks
   GatherArgs g{};
   g.X = d_test_x; g.y = d_test_y; g.perm = nullptr; g.n = y.n_test;
   g.d0 = y.lay[0].K; g.Kp = y.lay[0].Kp; g.B = y.n_test_pad; g.Bp = y.n_test_pad; g.T = 1;
   g.rows = p->ws + y.xte; g.labels = reinterpret_cast<int32_t*>(p->ws + y.yte);
-  hipError_t e = cfg->dtype == GEVO_BF16 ? launch_gather<uint16_t>(g, s) : launch_gather<float>(g, s);
+  hipError_t e = cfg->dtype == GEVO_BF16 ? launch_gather<uint16_t>(g, s, LaunchEv{}) : launch_gather<float>(g, s, LaunchEv{});
   if (e != hipSuccess) return fail(GEVO_E_HIP);
-  if (launch_zero_bytes(p->ws + y.train_ce, (size_t)P * 8, s) != hipSuccess ||
-      launch_zero_bytes(p->ws + y.train_corr, (size_t)P * 8, s) != hipSuccess ||
-      launch_zero_bytes(p->ws + y.test_ce, (size_t)P * 8, s) != hipSuccess ||
-      launch_zero_bytes(p->ws + y.test_corr, (size_t)P * 8, s) != hipSuccess)
+  if (launch_zero_bytes(p->ws + y.train_ce, (size_t)P * 8, s, LaunchEv{}) != hipSuccess ||
+      launch_zero_bytes(p->ws + y.train_corr, (size_t)P * 8, s, LaunchEv{}) != hipSuccess ||
+      launch_zero_bytes(p->ws + y.test_ce, (size_t)P * 8, s, LaunchEv{}) != hipSuccess ||
+      launch_zero_bytes(p->ws + y.test_corr, (size_t)P * 8, s, LaunchEv{}) != hipSuccess)
     return fail(GEVO_E_HIP);
   if (cfg->init == GEVO_INIT_BASE_NOISE && cfg->base_params) {
     if (hipStreamSynchronize(s) != hipSuccess) return fail(GEVO_E_HIP);   // host staging vectors die here
@@ -688,6 +742,21 @@ gevo_status gevo_pop_epoch_labels(gevo_pop* p, int32_t* labels_out, int64_t n) {
   return GEVO_OK;
 }
 
+gevo_status gevo_pop_set_profiling(gevo_pop* p, int enable) {
+  if (!p) return GEVO_E_ARG;
+  if (!enable && prof_resolve(p) != hipSuccess) return GEVO_E_HIP;
+  p->prof_on = enable != 0;
+  return GEVO_OK;
+}
+
+gevo_status gevo_pop_kernel_stats(gevo_pop* p, int kind, double* total_ms, uint64_t* launches) {
+  if (!p || kind < 0 || kind >= GEVO_KERNEL_KINDS) return GEVO_E_ARG;
+  if (prof_resolve(p) != hipSuccess) return GEVO_E_HIP;
+  if (total_ms) *total_ms = p->prof_ms[kind];
+  if (launches) *launches = p->prof_n[kind];
+  return GEVO_OK;
+}
+
 void gevo_pop_destroy(gevo_pop* p) {
   if (!p) return;
   (void)hipStreamSynchronize(p->stream);   // pending copies may still read host buffers
@@ -695,6 +764,7 @@ void gevo_pop_destroy(gevo_pop* p) {
   if (p->ev1) (void)hipEventDestroy(p->ev1);
   if (p->perm_ev[0]) (void)hipEventDestroy(p->perm_ev[0]);
   if (p->perm_ev[1]) (void)hipEventDestroy(p->perm_ev[1]);
+  for (hipEvent_t e : p->ev_all) (void)hipEventDestroy(e);
   delete p;
 }
 

@@ -14,7 +14,8 @@ constexpr int kThreads = 256;      // 4 wave64 per workgroup
 constexpr int kPassRows = 256;     // forward rows per pass of the layer kernel
 constexpr int kOutRows = 256;      // rows per workgroup of the output kernel (predict)
 constexpr int kPredictChunk = 2048;  // test rows per predict chunk
-constexpr size_t kLdsBudget = 63 * 1024;   // dynamic LDS of the output kernel (static arrays use the rest of 64 KiB)
+constexpr size_t kLdsBudget = 120 * 1024;  // dynamic LDS of the output kernel (one workgroup per variant)
+constexpr size_t kLayerLds = 76 * 1024;   // dynamic LDS per hidden-layer workgroup (two fit in 160 KiB)
 
 // Philox stream ids (counter word 3)
 constexpr uint32_t kStreamLr = 1, kStreamDens = 2, kStreamMask = 3, kStreamInit = 4,
@@ -36,16 +37,17 @@ struct InitArgs {
   const uint32_t* thresh;        // [P] mask thresholds
   float* Wm;                     // [P][Np][Kp]
   float* bias;                   // [P][Np]
-  uint32_t* mask;                // [P][Np][Kp/32]
+  uint32_t* mask;                // [P][Np][Kp/32] row words
 };
 
 template <typename S>
 struct LayerArgs {
   int Kp, Np;                    // padded input / output width of the layer
+  int KB;                        // input columns per LDS block (set by the launcher)
   int Bp;                        // padded batch rows of the update
   float* Wm;                     // [P][Np][Kp] fp32 master
   float* bias;                   // [P][Np]
-  const uint32_t* mask;          // [P][Np][Kp/32]
+  const uint32_t* mask;          // [P][Np][Kp/32] row words: bit k%32 of word [n][k/32]
   const float* lr;               // [P]
   int do_update;
   const S* Gcols; size_t g_vs;   // [v][Np][Bp] gradient at this layer's output
@@ -65,7 +67,7 @@ struct OutArgs {
   int Bp;                        // padded batch rows (training)
   float* Wm;                     // [P][32][Kp]
   float* bias;                   // [P][32]
-  const uint32_t* mask;          // [P][32][Kp/32]
+  const uint32_t* mask;          // [P][32][Kp/32] row words
   const float* lr;               // [P]
   int train;                     // 1: loss + backward + update on one batch; 0: predict chunk
   const S* Arows; size_t ar_vs;  // [v][rows][Kp]
@@ -111,16 +113,20 @@ struct TransposeArgs {
 
 // ---------------------------------------------------------------- launchers
 // Each returns hipSuccess or the launch error.  Shapes are validated by the
-// caller (gevo_capi.hip) before these are reached.
-hipError_t launch_init(const InitArgs& a, hipStream_t s);
-template <typename S> hipError_t launch_layer(const LayerArgs<S>& a, int P, hipStream_t s);
-template <typename S> hipError_t launch_out(const OutArgs<S>& a, int P, hipStream_t s);
-template <typename S> hipError_t launch_bwd(const BwdArgs<S>& a, int P, hipStream_t s);
-template <typename S> hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
-template <typename S> hipError_t launch_transpose(const TransposeArgs& a, hipStream_t s);
-hipError_t launch_zero_bytes(void* p, size_t bytes, hipStream_t s);
+// caller (gevo_capi.hip) before these are reached.  A non-null event pair is
+// recorded by the dispatch itself around the kernel (kernel-level timing).
+struct LaunchEv {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+hipError_t launch_init(const InitArgs& a, hipStream_t s, const LaunchEv& ev);
+template <typename S> hipError_t launch_layer(const LayerArgs<S>& a, int P, hipStream_t s, const LaunchEv& ev);
+template <typename S> hipError_t launch_out(const OutArgs<S>& a, int P, hipStream_t s, const LaunchEv& ev);
+template <typename S> hipError_t launch_bwd(const BwdArgs<S>& a, int P, hipStream_t s, const LaunchEv& ev);
+template <typename S> hipError_t launch_gather(const GatherArgs& a, hipStream_t s, const LaunchEv& ev);
+template <typename S> hipError_t launch_transpose(const TransposeArgs& a, hipStream_t s, const LaunchEv& ev);
+hipError_t launch_zero_bytes(void* p, size_t bytes, hipStream_t s, const LaunchEv& ev);
 hipError_t launch_reduce_partials(const double* part_ce, const unsigned int* part_corr, int P, int n_chunks,
-                                  double* ce_out, unsigned long long* corr_out, hipStream_t s);
+                                  double* ce_out, unsigned long long* corr_out, hipStream_t s, const LaunchEv& ev);
 
 // Philox4x32-10 on the host (the library's own draws: learning rates,
 // densities, data order).

@@ -6,7 +6,7 @@
 // output width Np, both multiples of 32):
 //   Wm   fp32 master weights, [v][Np][Kp]  ("out x in": k is contiguous)
 //   bias fp32 [v][Np]
-//   mask uint32 bit words, [v][Np][Kp/32] (bit k%32 of word k/32)
+//   mask uint32 row words, [v][Np][Kp/32] (bit k%32 of word [n][k/32])
 // Activations and gradients come in two orientations: "rows" [v][b][feature]
 // (feature contiguous) and "cols" [v][feature][b] (batch contiguous), so that
 // every MFMA operand is read along its contraction index.
@@ -18,6 +18,7 @@
 // C[8*(r/4) + 4*(l/32) + r%4][l%32], r = 0..15.
 #include "gevo_internal.h"
 
+#include <hip/hip_ext.h>
 #include <math.h>
 
 namespace gevo {
@@ -114,80 +115,94 @@ __global__ __launch_bounds__(256) void k_init(InitArgs a) {
     const int kw = (int)(it % words);
     const int n = (int)((it / words) % a.Np);
     const int v = (int)(it / ((int64_t)words * a.Np));
-    const uint32_t th = a.thresh[v];
-    float* wrow = a.Wm + ((size_t)v * a.Np + n) * a.Kp + kw * 32;
     uint32_t bits = 0;
-    uint64_t blk_m = ~0ull, blk_i = ~0ull, blk_n = ~0ull;
-    uint4 rm = make_uint4(0, 0, 0, 0), ri = rm, rn = rm;
-    for (int j = 0; j < 32; ++j) {
-      const int k = kw * 32 + j;
-      float w = 0.0f;
-      if (n < a.N && k < a.K) {
-        const uint64_t e = (uint64_t)n * (uint64_t)a.K + (uint64_t)k;
-        if ((e >> 2) != blk_m) {
-          blk_m = e >> 2;
-          rm = philox(make_uint4((uint32_t)blk_m, (uint32_t)a.l_index, (uint32_t)v, kStreamMask), key);
-        }
-        const bool keep = (pick(rm, (uint32_t)(e & 3)) >> 8) < th;
-        if (a.base_w) {
-          w = a.base_w[(size_t)n * a.Kp + k];
-        } else {
-          if ((e >> 2) != blk_i) {
-            blk_i = e >> 2;
-            ri = philox(make_uint4((uint32_t)blk_i, (uint32_t)a.l_index, 0u, kStreamInit), key);
+    {
+      const uint32_t th = a.thresh[v];
+      float* wrow = a.Wm + ((size_t)v * a.Np + n) * a.Kp + kw * 32;
+      uint64_t blk_m = ~0ull, blk_i = ~0ull, blk_n = ~0ull;
+      uint4 rm = make_uint4(0, 0, 0, 0), ri = rm, rn = rm;
+      for (int j = 0; j < 32; ++j) {
+        const int k = kw * 32 + j;
+        float w = 0.0f;
+        if (n < a.N && k < a.K) {
+          const uint64_t e = (uint64_t)n * (uint64_t)a.K + (uint64_t)k;
+          if ((e >> 2) != blk_m) {
+            blk_m = e >> 2;
+            rm = philox(make_uint4((uint32_t)blk_m, (uint32_t)a.l_index, (uint32_t)v, kStreamMask), key);
           }
-          const float u = (float)(pick(ri, (uint32_t)(e & 3)) >> 8) * two_m24;
-          const float t = __fsub_rn(__fmul_rn(2.0f, u), 1.0f);       // exact
-          w = __fmul_rn(t, a.xavier_a);
-        }
-        if (a.init_kind == 1) {
-          if ((e >> 1) != blk_n) {
-            blk_n = e >> 1;
-            rn = philox(make_uint4((uint32_t)blk_n, (uint32_t)a.l_index, (uint32_t)v, kStreamNoise), key);
+          const bool keep = (pick(rm, (uint32_t)(e & 3)) >> 8) < th;
+          if (a.base_w) {
+            w = a.base_w[(size_t)n * a.Kp + k];
+          } else {
+            if ((e >> 2) != blk_i) {
+              blk_i = e >> 2;
+              ri = philox(make_uint4((uint32_t)blk_i, (uint32_t)a.l_index, 0u, kStreamInit), key);
+            }
+            const float u = (float)(pick(ri, (uint32_t)(e & 3)) >> 8) * two_m24;
+            const float t = __fsub_rn(__fmul_rn(2.0f, u), 1.0f);       // exact
+            w = __fmul_rn(t, a.xavier_a);
           }
-          const uint32_t w0 = (uint32_t)(e & 1) * 2u;
-          const float u1 = (float)((pick(rn, w0) >> 8) + 1u) * two_m24;   // (0, 1]
-          const float u2 = (float)(pick(rn, w0 + 1) >> 8) * two_m24;
-          const float eps = sqrtf(-2.0f * logf(u1)) * cosf(6.28318530717958647692f * u2);
-          w = __fmul_rn(w, __fadd_rn(1.0f, __fmul_rn(a.noise_std, eps)));
+          if (a.init_kind == 1) {
+            if ((e >> 1) != blk_n) {
+              blk_n = e >> 1;
+              rn = philox(make_uint4((uint32_t)blk_n, (uint32_t)a.l_index, (uint32_t)v, kStreamNoise), key);
+            }
+            const uint32_t w0 = (uint32_t)(e & 1) * 2u;
+            const float u1 = (float)((pick(rn, w0) >> 8) + 1u) * two_m24;   // (0, 1]
+            const float u2 = (float)(pick(rn, w0 + 1) >> 8) * two_m24;
+            const float eps = sqrtf(-2.0f * logf(u1)) * cosf(6.28318530717958647692f * u2);
+            w = __fmul_rn(w, __fadd_rn(1.0f, __fmul_rn(a.noise_std, eps)));
+          }
+          if (!keep) w = 0.0f;
+          bits |= (uint32_t)keep << j;
         }
-        if (!keep) w = 0.0f;
-        bits |= (uint32_t)keep << j;
+        wrow[j] = w;
       }
-      wrow[j] = w;
+      if (kw == 0) a.bias[(size_t)v * a.Np + n] = (a.base_b && n < a.N) ? a.base_b[n] : 0.0f;
     }
     a.mask[((size_t)v * a.Np + n) * words + kw] = bits;
-    if (kw == 0) a.bias[(size_t)v * a.Np + n] = (a.base_b && n < a.N) ? a.base_b[n] : 0.0f;
   }
 }
 
 // ------------------------------------------------------------ hidden layer
-// Workgroup (n-tile of 32 output units, variant v); four waves.
-// Update phase (do_update): for each 32-wide chunk of inputs k,
-//   dW^T[n][k] = sum_b G[n][b] * A[k][b]                  (MFMA, contraction = batch)
-//   W[n][k]    = mask ? fl(W - fl(lr * dW)) : +0           (fp32 master, in place)
-// and b[n] -= lr * sum_b G[n][b].  The updated chunk is kept in LDS as an
+// Workgroup (n-tile of 32 output units, variant v); four waves.  The inputs
+// k are processed in blocks of KB columns (the block's operand copy of W fits
+// in LDS).  Update (do_update), per 32-wide chunk c of a block, each wave
+// streaming its own chunks with the next chunk's weights already in flight:
+//   dW^T[n][k] = sum_b G[n][b] * A[k][b]          (MFMA, contraction = batch)
+// staged through LDS, then lane (row n, 16 columns) applies
+//   W[n][k]    = mask ? fl(W - fl(lr * dW)) : +0   (fp32 master, float4 in place)
+// and b[n] -= lr * sum_b G[n][b].  The updated block stays in LDS as an
 // operand, so the forward pass of the next step runs without re-reading W:
 //   Z[r][n] = sum_k A_next[r][k] * W[n][k] + b[n],  A_out = relu(Z)  (MFMA)
-// Without do_update the chunk is loaded from the master (forward only).
+// Without do_update a block is loaded from the master (forward only).
 template <typename S, int BPMAX>
-__global__ __launch_bounds__(256) void k_layer(LayerArgs<S> a) {
+__global__ __launch_bounds__(256, 2) void k_layer(LayerArgs<S> a) {
   using O = Op<S>;
+  using F = typename O::Frag;
   constexpr int KM = O::KM, KE = O::KE;
-  constexpr int WSTR = 32 + O::PAD;
   constexpr int NG = BPMAX / KM;
-  __shared__ __align__(16) S wl[4][32][WSTR];
+  constexpr int TPW = BPMAX / 128;                   // row tiles per wave in a forward pass
+  constexpr int PASS = BPMAX;                        // rows per forward pass
+  constexpr int DSTR = 36;                           // fp32 staging row stride (16-byte aligned rows)
+  constexpr int SSTR = 32 + O::PAD;
+  extern __shared__ __align__(16) char smem[];
   __shared__ float bias_l[32];
+  const int KB = a.KB, WS = KB + O::PAD;
+  S* wt = reinterpret_cast<S*>(smem);                                // [32][WS] operand tile
+  float* stage = reinterpret_cast<float*>(smem + (size_t)32 * WS * sizeof(S));   // [4][32][DSTR]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int l32 = lane & 31, lh = lane >> 5;
   const int n0 = blockIdx.x * 32, v = blockIdx.y;
-  const int Kp = a.Kp, Np = a.Np, nch = Kp / 32;
-  float* Wm = a.Wm + (size_t)v * Np * Kp;
-  const uint32_t* mk = a.mask + (size_t)v * Np * nch;
+  const int Kp = a.Kp, Np = a.Np, kwords = Kp / 32;
+  float* Wm = a.Wm + ((size_t)v * Np + n0) * Kp;             // this tile's 32 rows
+  const uint32_t* mk = a.mask + ((size_t)v * Np + n0) * kwords;
   const float lrv = a.lr[v];
-
-  typename O::Frag gf[NG];
   const int nsteps = a.Bp / KM;
+  float* dws = stage + wave * 32 * DSTR;
+  const int rn = lane >> 1, cs = (lane & 1) * 16;            // update ownership: row rn, columns cs..cs+15
+
+  F gf[NG];
   if (a.do_update) {
     // bias gradient of the 32 units: 8 lanes per unit, fixed-order reduction
     const S* G = a.Gcols + v * a.g_vs;
@@ -206,113 +221,197 @@ __global__ __launch_bounds__(256) void k_layer(LayerArgs<S> a) {
     }
     const S* gp = G + (size_t)(n0 + l32) * a.Bp + lh * KE;
 #pragma unroll
-    for (int s2 = 0; s2 < NG; ++s2)
-      if (s2 < nsteps) gf[s2] = O::load(gp + s2 * KM);
+    for (int s2 = 0; s2 < NG; ++s2) gf[s2] = s2 < nsteps ? O::load(gp + s2 * KM) : F{};
   } else if (threadIdx.x < 32) {
     bias_l[threadIdx.x] = a.bias[(size_t)v * Np + n0 + threadIdx.x];
   }
 
+  const int nblk = (Kp + KB - 1) / KB;
   const int R = a.do_forward ? a.R : 0;
-  const int npass = a.do_forward ? (R + kPassRows - 1) / kPassRows : 1;
-  for (int pass = 0; pass < npass; ++pass) {
-    const int row0 = pass * kPassRows;
-    const int prows = a.do_forward ? min(kPassRows, R - row0) : 0;
-    const int ntiles = prows / 32;
-    const bool upd = a.do_update && pass == 0;
-    f32x16_t acc0 = zero16(), acc1 = zero16();
-    for (int round = 0; round * 4 < nch; ++round) {
-      const int c = round * 4 + wave;
-      if (c < nch) {
-        const int k0 = c * 32;
-        if (upd) {
-          float wold[16];
-          uint32_t mw[16];
+  const int npass = a.do_forward ? (R + PASS - 1) / PASS : 0;
+
+  // ---- fill the LDS operand tile with block blk (update or plain load), plus Wt
+  auto fill = [&](int blk, bool upd) {
+    const int kb0 = blk * KB;
+    const int kw = min(KB, Kp - kb0);
+    const int nchb = kw / 32;
+    if (upd) {
+      const float* wrow = Wm + (size_t)rn * Kp + kb0 + cs;
+      const uint32_t* mrow = mk + (size_t)rn * kwords + kb0 / 32;
+      const S* acb = a.Acols + v * a.ac_vs + (size_t)(kb0 + l32) * a.Bp + lh * KE;
+      float4 nx[4];
+      uint32_t nmw = 0;
+      if (wave < nchb) {
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int n = n0 + crow(r, lane);
-            wold[r] = Wm[(size_t)n * Kp + k0 + l32];
-            mw[r] = mk[(size_t)n * nch + c];
-          }
-          f32x16_t d = zero16();
-          const S* ap = a.Acols + v * a.ac_vs + (size_t)(k0 + l32) * a.Bp + lh * KE;
+        for (int u = 0; u < 4; ++u) nx[u] = *reinterpret_cast<const float4*>(wrow + wave * 32 + 4 * u);
+        nmw = mrow[wave];
+      }
+      for (int c = wave; c < nchb; c += 4) {
+        float4 w4[4];
 #pragma unroll
-          for (int s2 = 0; s2 < NG; ++s2)
-            if (s2 < nsteps) d = O::mma(gf[s2], O::load(ap + s2 * KM), d);
+        for (int u = 0; u < 4; ++u) w4[u] = nx[u];
+        const uint32_t mw = nmw;
+        if (c + 4 < nchb) {
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int nl = crow(r, lane);
-            const bool keep = (mw[r] >> l32) & 1u;
-            const float wn = keep ? __fsub_rn(wold[r], __fmul_rn(lrv, d[r])) : 0.0f;
-            Wm[(size_t)(n0 + nl) * Kp + k0 + l32] = wn;
-            wl[wave][nl][l32] = O::from_f32(wn);
-          }
-        } else {
+          for (int u = 0; u < 4; ++u) nx[u] = *reinterpret_cast<const float4*>(wrow + (c + 4) * 32 + 4 * u);
+          nmw = mrow[c + 4];
+        }
+        const S* ap = acb + (size_t)c * 32 * a.Bp;
+        f32x16_t d0 = zero16(), d1 = zero16();
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int nl = crow(r, lane);
-            wl[wave][nl][l32] = O::from_f32(Wm[(size_t)(n0 + nl) * Kp + k0 + l32]);
+        for (int s2 = 0; s2 < NG; s2 += 2) {
+          if (s2 < nsteps) d0 = O::mma(gf[s2], O::load(ap + s2 * KM), d0);
+          if (s2 + 1 < nsteps) d1 = O::mma(gf[s2 + 1], O::load(ap + (s2 + 1) * KM), d1);
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) dws[crow(r, lane) * DSTR + l32] = d0[r] + d1[r];
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+        float dw[16];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float4 t = *reinterpret_cast<const float4*>(dws + rn * DSTR + cs + 4 * u);
+          dw[4 * u] = t.x; dw[4 * u + 1] = t.y; dw[4 * u + 2] = t.z; dw[4 * u + 3] = t.w;
+        }
+        float wn[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float w = (i & 3) == 0 ? w4[i >> 2].x : (i & 3) == 1 ? w4[i >> 2].y : (i & 3) == 2 ? w4[i >> 2].z : w4[i >> 2].w;
+          const bool keep = (mw >> (cs + i)) & 1u;
+          wn[i] = keep ? __fsub_rn(w, __fmul_rn(lrv, dw[i])) : 0.0f;
+        }
+        float* wdst = Wm + (size_t)rn * Kp + kb0 + c * 32 + cs;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          *reinterpret_cast<float4*>(wdst + 4 * u) = make_float4(wn[4 * u], wn[4 * u + 1], wn[4 * u + 2], wn[4 * u + 3]);
+        S* od = wt + rn * WS + c * 32 + cs;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) od[i] = O::from_f32(wn[i]);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+      }
+    } else {
+      const int q = kw / 4;                               // float4 per row
+      for (int i = threadIdx.x; i < 32 * q; i += 256 * 4) {
+        float4 w4[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int j = i + u * 256;
+          w4[u] = j < 32 * q ? *reinterpret_cast<const float4*>(Wm + (size_t)(j / q) * Kp + kb0 + (j % q) * 4)
+                             : make_float4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int j = i + u * 256;
+          if (j < 32 * q) {
+            S* dst = wt + (j / q) * WS + (j % q) * 4;
+            dst[0] = O::from_f32(w4[u].x); dst[1] = O::from_f32(w4[u].y);
+            dst[2] = O::from_f32(w4[u].z); dst[3] = O::from_f32(w4[u].w);
           }
         }
       }
-      __syncthreads();
-      if (a.Wt && pass == 0) {
-        // transposed operand copy [k][n] for the backward of the layer above
-        const int j = threadIdx.x >> 6, kl = (threadIdx.x & 63) >> 1, half = threadIdx.x & 1;
-        const int cj = round * 4 + j;
-        if (cj < nch) {
-          S* dst = a.Wt + (size_t)v * Kp * Np + (size_t)(cj * 32 + kl) * Np + n0 + half * 16;
-#pragma unroll
-          for (int i = 0; i < 16; ++i) dst[i] = wl[j][half * 16 + i][kl];
-        }
-      }
-      if (ntiles > 0) {
-        for (int j = 0; j < 4; ++j) {
-          const int cj = round * 4 + j;
-          if (cj >= nch) break;
-          const int kk0 = cj * 32;
-#pragma unroll
-          for (int ti = 0; ti < 2; ++ti) {
-            const int tile = wave + 4 * ti;
-            if (tile < ntiles) {
-              const S* ar = a.Arows + v * a.ar_vs + (size_t)(row0 + tile * 32 + l32) * Kp + kk0 + lh * KE;
-              f32x16_t acc = ti == 0 ? acc0 : acc1;
-#pragma unroll
-              for (int ks = 0; ks < 32 / KM; ++ks)
-                acc = O::mma(O::load(ar + ks * KM), O::load(&wl[j][l32][ks * KM + lh * KE]), acc);
-              if (ti == 0) acc0 = acc; else acc1 = acc;
-            }
-          }
-        }
-      }
-      __syncthreads();
     }
-    if (!a.do_forward) break;
-    // epilogue: bias + ReLU, rows store, transposed store through LDS
+    __syncthreads();
+    if (a.Wt) {
+      // transposed operand copy [k][n] for the backward of the layer above
+      for (int k = threadIdx.x >> 1; k < kw; k += 128) {
+        const int half = threadIdx.x & 1;
+        S* dst = a.Wt + (size_t)v * Kp * Np + (size_t)(kb0 + k) * Np + n0 + half * 16;
 #pragma unroll
-    for (int ti = 0; ti < 2; ++ti) {
+        for (int i = 0; i < 16; ++i) dst[i] = wt[(half * 16 + i) * WS + k];
+      }
+    }
+  };
+
+  // ---- forward over block blk for rows [row0, row0 + 32*ntiles); two accumulator chains per tile
+  auto forward = [&](int blk, int row0, int ntiles, f32x16_t (&acc)[TPW][2]) {
+    const int kb0 = blk * KB;
+    const int kw = min(KB, Kp - kb0);
+#pragma unroll
+    for (int ti = 0; ti < TPW; ++ti) {
       const int tile = wave + 4 * ti;
-      const bool valid = tile < ntiles;
-      if (valid) {
-        const f32x16_t acc = ti == 0 ? acc0 : acc1;
+      if (tile >= ntiles) continue;
+      const S* ar = a.Arows + v * a.ar_vs + (size_t)(row0 + tile * 32 + l32) * Kp + kb0 + lh * KE;
+      const S* br = wt + l32 * WS + lh * KE;
+      int k = 0;
+      for (; k + 4 * KM <= kw; k += 4 * KM) {
+        F x[4], w[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) { x[u] = O::load(ar + k + u * KM); w[u] = O::load(br + k + u * KM); }
+        acc[ti][0] = O::mma(x[0], w[0], acc[ti][0]);
+        acc[ti][1] = O::mma(x[1], w[1], acc[ti][1]);
+        acc[ti][0] = O::mma(x[2], w[2], acc[ti][0]);
+        acc[ti][1] = O::mma(x[3], w[3], acc[ti][1]);
+      }
+      for (; k < kw; k += KM) acc[ti][0] = O::mma(O::load(ar + k), O::load(br + k), acc[ti][0]);
+    }
+  };
+
+  // ---- epilogue: bias + ReLU, rows store, transposed store staged in LDS
+  auto epilogue = [&](int row0, int ntiles, f32x16_t (&acc)[TPW][2]) {
+    S* sw = reinterpret_cast<S*>(dws);                      // [32][SSTR] per wave
+#pragma unroll
+    for (int ti = 0; ti < TPW; ++ti) {
+      const int tile = wave + 4 * ti;
+      if (tile < ntiles) {                                  // wave-uniform
         const float bn = bias_l[l32];
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int rl = crow(r, lane);
-          const int row = row0 + tile * 32 + rl;
-          const float z = acc[r] + bn;
+          const float z = (acc[ti][0][r] + acc[ti][1][r]) + bn;
           const S sv = O::from_f32(z > 0.0f ? z : 0.0f);
-          a.Orows[v * a.or_vs + (size_t)row * Np + n0 + l32] = sv;
-          wl[wave][l32][rl] = sv;                       // [n][row] tile for the transposed store
+          a.Orows[v * a.or_vs + (size_t)(row0 + tile * 32 + rl) * Np + n0 + l32] = sv;
+          sw[l32 * SSTR + rl] = sv;                        // [n][row]
         }
-      }
-      __syncthreads();
-      if (valid && a.Ocols) {
-        const int nl = lane >> 1, half = lane & 1;
-        S* dst = a.Ocols + v * a.oc_vs + (size_t)(n0 + nl) * R + row0 + tile * 32 + half * 16;
+        if (a.Ocols) {
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+          __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+          const int nl = lane >> 1, half = lane & 1;
+          S* dst = a.Ocols + v * a.oc_vs + (size_t)(n0 + nl) * R + row0 + tile * 32 + half * 16;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) dst[i] = wl[wave][nl][half * 16 + i];
+          for (int i = 0; i < 16; ++i) dst[i] = sw[nl * SSTR + half * 16 + i];
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
       }
+    }
+  };
+
+  if (nblk == 1) {
+    fill(0, a.do_update != 0);
+    __syncthreads();
+    for (int pass = 0; pass < npass; ++pass) {
+      const int row0 = pass * PASS;
+      const int ntiles = min(PASS, R - row0) / 32;
+      f32x16_t acc[TPW][2];
+#pragma unroll
+      for (int ti = 0; ti < TPW; ++ti) { acc[ti][0] = zero16(); acc[ti][1] = zero16(); }
+      forward(0, row0, ntiles, acc);
+      epilogue(row0, ntiles, acc);
+    }
+  } else if (npass == 0) {
+    for (int blk = 0; blk < nblk; ++blk) {
+      fill(blk, a.do_update != 0);
       __syncthreads();
+    }
+  } else {
+    for (int pass = 0; pass < npass; ++pass) {
+      const int row0 = pass * PASS;
+      const int ntiles = min(PASS, R - row0) / 32;
+      f32x16_t acc[TPW][2];
+#pragma unroll
+      for (int ti = 0; ti < TPW; ++ti) { acc[ti][0] = zero16(); acc[ti][1] = zero16(); }
+      for (int blk = 0; blk < nblk; ++blk) {
+        fill(blk, a.do_update != 0 && pass == 0);
+        __syncthreads();
+        forward(blk, row0, ntiles, acc);
+        __syncthreads();
+      }
+      epilogue(row0, ntiles, acc);
     }
   }
 }
@@ -341,9 +440,29 @@ __global__ __launch_bounds__(256) void k_out(OutArgs<S> a) {
   const int v = blockIdx.y, chunk = blockIdx.x;
   const int Kp = a.Kp, WS = Kp + O::PAD;
   S* wop = reinterpret_cast<S*>(smem);                  // [32][WS]  W_L as operand, [class][k]
-  S* gs = wop + 32 * WS;                                // [BPMAX][GSTR] gradient rows (training)
+  S* gs = wop + 32 * WS;                                // [Bp][GSTR] gradient rows (training)
+  float* stg = reinterpret_cast<float*>(gs + (size_t)a.Bp * GSTR);   // [4][32][36] fp32 staging (training)
   const float* Wm = a.Wm + (size_t)v * 32 * Kp;
-  for (int i = threadIdx.x; i < 32 * Kp; i += 256) wop[(i / Kp) * WS + (i % Kp)] = O::from_f32(Wm[i]);
+  {
+    const int q = Kp / 4;                                // float4 per row
+    for (int i = threadIdx.x; i < 32 * q; i += 256 * 4) {
+      float4 w4[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int j = i + u * 256;
+        w4[u] = j < 32 * q ? *reinterpret_cast<const float4*>(Wm + (size_t)j * 4) : make_float4(0, 0, 0, 0);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int j = i + u * 256;
+        if (j < 32 * q) {
+          S* dst = wop + (j / q) * WS + (j % q) * 4;
+          dst[0] = O::from_f32(w4[u].x); dst[1] = O::from_f32(w4[u].y);
+          dst[2] = O::from_f32(w4[u].z); dst[3] = O::from_f32(w4[u].w);
+        }
+      }
+    }
+  }
   const float bias_c = a.bias[(size_t)v * 32 + l32];
   __syncthreads();
 
@@ -426,7 +545,8 @@ __global__ __launch_bounds__(256) void k_out(OutArgs<S> a) {
     const float bo = a.bias[(size_t)v * 32 + threadIdx.x];
     a.bias[(size_t)v * 32 + threadIdx.x] = __fsub_rn(bo, __fmul_rn(lrv, db));
   }
-  // dW_L and the masked update of the master (old W_L stays in LDS)
+  // dW_L and the masked update of the master (old W_L stays in LDS): the dW
+  // tile is staged in LDS, then lane (row rn, 16 columns) updates with float4
   const int nsteps = a.Bp / KM;
   typename O::Frag ga[NG];
 #pragma unroll
@@ -435,27 +555,43 @@ __global__ __launch_bounds__(256) void k_out(OutArgs<S> a) {
   float* Wmv = a.Wm + (size_t)v * 32 * Kp;
   const uint32_t* mk = a.mask + (size_t)v * 32 * (Kp / 32);
   const S* Acv = a.Acols + v * a.ac_vs;
+  float* dws = stg + wave * 32 * 36;
+  const int rn = lane >> 1, cs = (lane & 1) * 16;
   for (int kt = wave; kt < Kp / 32; kt += 4) {
     const int k0 = kt * 32;
-    float wold[16];
-    uint32_t mw[16];
+    float4 w4[4];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int c = crow(r, lane);
-      wold[r] = Wmv[(size_t)c * Kp + k0 + l32];
-      mw[r] = mk[(size_t)c * (Kp / 32) + kt];
-    }
+    for (int u = 0; u < 4; ++u) w4[u] = *reinterpret_cast<const float4*>(Wmv + (size_t)rn * Kp + k0 + cs + 4 * u);
+    const uint32_t mw = mk[(size_t)rn * (Kp / 32) + kt];
     f32x16_t d = zero16();
     const S* ap = Acv + (size_t)(k0 + l32) * a.Bp + lh * KE;
 #pragma unroll
     for (int s2 = 0; s2 < NG; ++s2)
       if (s2 < nsteps) d = O::mma(ga[s2], O::load(ap + s2 * KM), d);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int c = crow(r, lane);
-      const bool keep = (mw[r] >> l32) & 1u;
-      Wmv[(size_t)c * Kp + k0 + l32] = keep ? __fsub_rn(wold[r], __fmul_rn(lrv, d[r])) : 0.0f;
+    for (int r = 0; r < 16; ++r) dws[crow(r, lane) * 36 + l32] = d[r];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    float wn[16];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float4 t = *reinterpret_cast<const float4*>(dws + rn * 36 + cs + 4 * u);
+      const float dv[4] = {t.x, t.y, t.z, t.w};
+      const float wv[4] = {w4[u].x, w4[u].y, w4[u].z, w4[u].w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const bool keep = (mw >> (cs + 4 * u + j)) & 1u;
+        wn[4 * u + j] = keep ? __fsub_rn(wv[j], __fmul_rn(lrv, dv[j])) : 0.0f;
+      }
     }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      *reinterpret_cast<float4*>(Wmv + (size_t)rn * Kp + k0 + cs + 4 * u) =
+          make_float4(wn[4 * u], wn[4 * u + 1], wn[4 * u + 2], wn[4 * u + 3]);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
   }
   if (!a.Gcols) return;
   // gradient of the last hidden layer, batch-contiguous, with ReLU'
@@ -572,80 +708,121 @@ static inline unsigned grid_for(int64_t items, int per_block = 256, int64_t cap 
   return (unsigned)g;
 }
 
-hipError_t launch_init(const InitArgs& a, hipStream_t s) {
+hipError_t launch_init(const InitArgs& a, hipStream_t s, const LaunchEv& ev) {
   const int64_t items = (int64_t)a.P * a.Np * (a.Kp / 32);
-  hipLaunchKernelGGL(k_init, dim3(grid_for(items)), dim3(256), 0, s, a);
+  hipExtLaunchKernelGGL(k_init, dim3(grid_for(items)), dim3(256), 0, s, ev.start, ev.stop, 0, a);
   return hipGetLastError();
 }
 
+size_t layer_stage_bytes() { return (size_t)4 * 32 * 36 * 4; }
+
+int layer_block_cols(int Kp, int elt, int pad) {
+  const size_t stage = layer_stage_bytes();
+  int cap = (int)((kLayerLds - stage) / (32 * (size_t)elt)) - pad;
+  cap = cap / 32 * 32;
+  const int nblk = (Kp + cap - 1) / cap;
+  return round_up((Kp + nblk - 1) / nblk, 32);
+}
+
 template <typename S>
-hipError_t launch_layer(const LayerArgs<S>& a, int P, hipStream_t s) {
+hipError_t launch_layer(const LayerArgs<S>& a0, int P, hipStream_t s, const LaunchEv& ev) {
+  LayerArgs<S> a = a0;
+  a.KB = layer_block_cols(a.Kp, (int)sizeof(S), Op<S>::PAD);
+  const size_t lds = (size_t)32 * (a.KB + Op<S>::PAD) * sizeof(S) + layer_stage_bytes();
   const dim3 grid(a.Np / 32, P);
-  if (a.Bp <= 128)
-    hipLaunchKernelGGL((k_layer<S, 128>), grid, dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL((k_layer<S, 256>), grid, dim3(256), 0, s, a);
+  if (a.Bp <= 128 || !a.do_update) {
+    static bool attr = false;
+    if (!attr) {
+      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_layer<S, 128>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLayerLds);
+      attr = true;
+    }
+    hipExtLaunchKernelGGL((k_layer<S, 128>), grid, dim3(256), lds, s, ev.start, ev.stop, 0, a);
+  } else {
+    static bool attr = false;
+    if (!attr) {
+      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_layer<S, 256>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLayerLds);
+      attr = true;
+    }
+    hipExtLaunchKernelGGL((k_layer<S, 256>), grid, dim3(256), lds, s, ev.start, ev.stop, 0, a);
+  }
   return hipGetLastError();
 }
 
 template <typename S>
 size_t out_lds_bytes(int Kp, int Bp, int train) {
-  return (size_t)32 * (Kp + Op<S>::PAD) * sizeof(S) + (train ? (size_t)Bp * (32 + Op<S>::PAD) * sizeof(S) : 0);
+  return (size_t)32 * (Kp + Op<S>::PAD) * sizeof(S) +
+         (train ? (size_t)Bp * (32 + Op<S>::PAD) * sizeof(S) + (size_t)4 * 32 * 36 * 4 : 0);
 }
 
 template <typename S>
-hipError_t launch_out(const OutArgs<S>& a, int P, hipStream_t s) {
+hipError_t launch_out(const OutArgs<S>& a, int P, hipStream_t s, const LaunchEv& ev) {
   const size_t lds = out_lds_bytes<S>(a.Kp, a.Bp, a.train);
   const dim3 grid(a.train ? 1 : (a.rows + kOutRows - 1) / kOutRows, P);
-  if (a.Bp <= 128)
-    hipLaunchKernelGGL((k_out<S, 128>), grid, dim3(256), lds, s, a);
-  else
-    hipLaunchKernelGGL((k_out<S, 256>), grid, dim3(256), lds, s, a);
+  if (a.Bp <= 128) {
+    static bool attr = false;
+    if (!attr) {
+      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_out<S, 128>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBudget);
+      attr = true;
+    }
+    hipExtLaunchKernelGGL((k_out<S, 128>), grid, dim3(256), lds, s, ev.start, ev.stop, 0, a);
+  } else {
+    static bool attr = false;
+    if (!attr) {
+      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_out<S, 256>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBudget);
+      attr = true;
+    }
+    hipExtLaunchKernelGGL((k_out<S, 256>), grid, dim3(256), lds, s, ev.start, ev.stop, 0, a);
+  }
   return hipGetLastError();
 }
 
 template <typename S>
-hipError_t launch_bwd(const BwdArgs<S>& a, int P, hipStream_t s) {
+hipError_t launch_bwd(const BwdArgs<S>& a, int P, hipStream_t s, const LaunchEv& ev) {
   const int tiles = (a.Kp / 32) * (a.Bp / 32);
-  hipLaunchKernelGGL(k_bwd<S>, dim3((tiles + 3) / 4, P), dim3(256), 0, s, a);
+  hipExtLaunchKernelGGL(k_bwd<S>, dim3((tiles + 3) / 4, P), dim3(256), 0, s, ev.start, ev.stop, 0, a);
   return hipGetLastError();
 }
 
 template <typename S>
-hipError_t launch_gather(const GatherArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_gather<S>, dim3(a.Bp, a.T), dim3(256), 0, s, a);
+hipError_t launch_gather(const GatherArgs& a, hipStream_t s, const LaunchEv& ev) {
+  hipExtLaunchKernelGGL(k_gather<S>, dim3(a.Bp, a.T), dim3(256), 0, s, ev.start, ev.stop, 0, a);
   return hipGetLastError();
 }
 
 template <typename S>
-hipError_t launch_transpose(const TransposeArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_transpose<S>, dim3(a.Kp / 32, a.Bp / 32, a.T), dim3(256), 0, s, a);
+hipError_t launch_transpose(const TransposeArgs& a, hipStream_t s, const LaunchEv& ev) {
+  hipExtLaunchKernelGGL(k_transpose<S>, dim3(a.Kp / 32, a.Bp / 32, a.T), dim3(256), 0, s, ev.start, ev.stop, 0, a);
   return hipGetLastError();
 }
 
-hipError_t launch_zero_bytes(void* p, size_t bytes, hipStream_t s) {
+hipError_t launch_zero_bytes(void* p, size_t bytes, hipStream_t s, const LaunchEv& ev) {
   const size_t words = bytes / 4;
   if (words == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_zero, dim3(grid_for((int64_t)words, 256, 4096)), dim3(256), 0, s, (uint32_t*)p, words);
+  hipExtLaunchKernelGGL(k_zero, dim3(grid_for((int64_t)words, 256, 4096)), dim3(256), 0, s, ev.start, ev.stop, 0,
+                        (uint32_t*)p, words);
   return hipGetLastError();
 }
 
 hipError_t launch_reduce_partials(const double* part_ce, const unsigned int* part_corr, int P, int n_chunks,
-                                  double* ce_out, unsigned long long* corr_out, hipStream_t s) {
-  hipLaunchKernelGGL(k_reduce_partials, dim3((P + 255) / 256), dim3(256), 0, s, part_ce, part_corr, P, n_chunks,
-                     ce_out, corr_out);
+                                  double* ce_out, unsigned long long* corr_out, hipStream_t s, const LaunchEv& ev) {
+  hipExtLaunchKernelGGL(k_reduce_partials, dim3((P + 255) / 256), dim3(256), 0, s, ev.start, ev.stop, 0, part_ce,
+                        part_corr, P, n_chunks, ce_out, corr_out);
   return hipGetLastError();
 }
 
-template hipError_t launch_layer<float>(const LayerArgs<float>&, int, hipStream_t);
-template hipError_t launch_layer<uint16_t>(const LayerArgs<uint16_t>&, int, hipStream_t);
-template hipError_t launch_out<float>(const OutArgs<float>&, int, hipStream_t);
-template hipError_t launch_out<uint16_t>(const OutArgs<uint16_t>&, int, hipStream_t);
-template hipError_t launch_bwd<float>(const BwdArgs<float>&, int, hipStream_t);
-template hipError_t launch_bwd<uint16_t>(const BwdArgs<uint16_t>&, int, hipStream_t);
-template hipError_t launch_gather<float>(const GatherArgs&, hipStream_t);
-template hipError_t launch_gather<uint16_t>(const GatherArgs&, hipStream_t);
-template hipError_t launch_transpose<float>(const TransposeArgs&, hipStream_t);
-template hipError_t launch_transpose<uint16_t>(const TransposeArgs&, hipStream_t);
+template hipError_t launch_layer<float>(const LayerArgs<float>&, int, hipStream_t, const LaunchEv&);
+template hipError_t launch_layer<uint16_t>(const LayerArgs<uint16_t>&, int, hipStream_t, const LaunchEv&);
+template hipError_t launch_out<float>(const OutArgs<float>&, int, hipStream_t, const LaunchEv&);
+template hipError_t launch_out<uint16_t>(const OutArgs<uint16_t>&, int, hipStream_t, const LaunchEv&);
+template hipError_t launch_bwd<float>(const BwdArgs<float>&, int, hipStream_t, const LaunchEv&);
+template hipError_t launch_bwd<uint16_t>(const BwdArgs<uint16_t>&, int, hipStream_t, const LaunchEv&);
+template hipError_t launch_gather<float>(const GatherArgs&, hipStream_t, const LaunchEv&);
+template hipError_t launch_gather<uint16_t>(const GatherArgs&, hipStream_t, const LaunchEv&);
+template hipError_t launch_transpose<float>(const TransposeArgs&, hipStream_t, const LaunchEv&);
+template hipError_t launch_transpose<uint16_t>(const TransposeArgs&, hipStream_t, const LaunchEv&);
 
 }  // namespace gevo
