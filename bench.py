@@ -92,6 +92,13 @@ def layer_costs(cfg):
         bf.append(P * 2.0 * B * K * N)
     if bb:
         out["bwd"] = (sum(bb) / len(bb), sum(bf) / len(bf), len(bb))
+    if L == 2:
+        # fused per-variant kernel: one launch = every SGD step of an epoch
+        K, N = d[0], d[1]
+        T = (cfg["n_train"] + B - 1) // B
+        per_step = P * (N * K * 8 + N * K / 8 + C * N * 8 + C * N / 8 + (N + C) * 8) + 2 * B * K * e + B * 4
+        fl_step = P * B * (4.0 * K * N + 6.0 * N * C)
+        out["fused_train"] = (T * per_step, T * fl_step, 1)
     return out
 
 

@@ -209,7 +209,8 @@ typedef enum {
   GEVO_KERNEL_OUT_PREDICT = 5,   /* output layer: loss and accuracy on the test split */
   GEVO_KERNEL_BWD = 6,           /* hidden backward GEMM */
   GEVO_KERNEL_AUX = 7,           /* zeroing, reductions */
-  GEVO_KERNEL_KINDS = 8
+  GEVO_KERNEL_FUSED_TRAIN = 8,   /* two-layer nets: whole SGD steps, one workgroup per variant */
+  GEVO_KERNEL_KINDS = 9
 } gevo_kernel_kind;
 
 gevo_status gevo_pop_set_profiling(gevo_pop* pop, int enable);

@@ -35,7 +35,8 @@ EXPORTED = [
     "gevo_pop_export", "gevo_pop_import", "gevo_pop_epoch_labels", "gevo_epoch_permutation",
     "gevo_pop_set_profiling", "gevo_pop_kernel_stats", "gevo_pop_destroy", "gevo_status_str",
 ]
-KERNEL_KINDS = ["init", "gather", "layer_train", "layer_fwd", "out_train", "out_predict", "bwd", "aux"]
+KERNEL_KINDS = ["init", "gather", "layer_train", "layer_fwd", "out_train", "out_predict", "bwd", "aux",
+                "fused_train"]
 
 
 class GevoError(RuntimeError):

@@ -28,6 +28,7 @@ struct LayerLay {
 
 struct Layout {
   int L = 0, P = 0, B = 0, Bp = 0, T = 0;
+  bool fused = false;                              // two-layer bf16 nets train in the fused per-variant kernel
   int64_t n_train = 0, n_test = 0;
   int n_test_pad = 0, n_chunks_test = 0;
   size_t elt = 4;
@@ -67,7 +68,7 @@ gevo_status validate(const gevo_pop_config* c) {
 
 // dynamic LDS of the output kernel: operand copy of W_L plus, in training, the gradient rows
 size_t out_lds(int Kp, int Bp, size_t elt, int pad) {
-  return (size_t)32 * (Kp + pad) * elt + (size_t)Bp * (32 + pad) * elt + (size_t)4 * 32 * 36 * 4;
+  return (size_t)32 * (Kp + pad) * elt + (size_t)Bp * (32 + pad) * elt + (size_t)8 * 32 * 36 * 4;
 }
 
 gevo_status make_layout(const gevo_pop_config* c, Layout* o) {
@@ -94,6 +95,7 @@ gevo_status make_layout(const gevo_pop_config* c, Layout* o) {
     q.Np = (l == y.L) ? kTile : round_up(q.N, kTile);
   }
   if (out_lds(y.lay[y.L - 1].Kp, y.Bp, y.elt, pad) > kLdsBudget) return GEVO_E_UNSUPPORTED;
+  y.fused = y.L == 2 && c->dtype == GEVO_BF16 && fused2_lds_bytes(y.lay[0].Np, y.Bp) > 0;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t at = off;
@@ -317,8 +319,8 @@ gevo_status begin_epoch(gevo_pop* p, int e) {
   HIP_TRY(launch_transpose<S>(tr, p->stream, prof(p, GEVO_KERNEL_GATHER)));
   HIP_TRY(launch_zero_bytes(p->ws + y.train_ce, (size_t)y.P * 8, p->stream, prof(p, GEVO_KERNEL_AUX)));
   HIP_TRY(launch_zero_bytes(p->ws + y.train_corr, (size_t)y.P * 8, p->stream, prof(p, GEVO_KERNEL_AUX)));
-  // forward of step 0 for the hidden layers
-  if (y.L > 1) {
+  // forward of step 0 for the hidden layers (the fused kernel does its own)
+  if (y.L > 1 && !y.fused) {
     gevo_status st = forward_hidden<S>(p, at<S>(p, y.xrows), 0, y.Bp, 0, false);
     if (st != GEVO_OK) return st;
   }
@@ -425,9 +427,29 @@ gevo_status do_train_steps(gevo_pop* p, uint32_t epoch, uint32_t s0, uint32_t s1
     p->last_epoch = (int)epoch;
     p->next_step = 0;
   }
-  for (uint32_t t = s0; t < s1; ++t) {
-    gevo_status st = train_step<S>(p, (int)t);
-    if (st != GEVO_OK) return st;
+  if (y.fused && s1 > s0) {
+    Fused2Args f{};
+    const LayerLay& q1 = y.lay[0];
+    const LayerLay& q2 = y.lay[1];
+    f.Kp = q1.Kp; f.Hp = q1.Np; f.C = q2.N; f.B = y.B; f.Bp = y.Bp; f.T = y.T;
+    f.n = y.n_train; f.t0 = (int)s0; f.t1 = (int)s1;
+    f.xrows = at<uint16_t>(p, y.xrows); f.xcols = at<uint16_t>(p, y.xcols); f.labels = at<int32_t>(p, y.yep);
+    f.W1 = at<float>(p, q1.Wm); f.b1 = at<float>(p, q1.bias); f.m1 = at<uint32_t>(p, q1.mask);
+    f.W2 = at<float>(p, q2.Wm); f.b2 = at<float>(p, q2.bias); f.m2 = at<uint32_t>(p, q2.mask);
+    f.lr = at<float>(p, y.lr);
+    f.ce_acc = at<double>(p, y.train_ce);
+    f.correct_acc = at<unsigned long long>(p, y.train_corr);
+    if (q2.Kp != q1.Np || q1.Kp % kTile || fused2_lds_bytes(f.Hp, f.Bp) == 0) return GEVO_E_SHAPE;
+    HIP_TRY(launch_fused2(f, y.P, p->stream, prof(p, GEVO_KERNEL_FUSED_TRAIN)));
+    for (uint32_t t = s0; t < s1; ++t) {
+      const int64_t r0 = (int64_t)t * y.B;
+      p->rows_done += (y.n_train - r0) < y.B ? (y.n_train - r0) : y.B;
+    }
+  } else {
+    for (uint32_t t = s0; t < s1; ++t) {
+      gevo_status st = train_step<S>(p, (int)t);
+      if (st != GEVO_OK) return st;
+    }
   }
   p->next_step = s1;
   if (s1 == (uint32_t)y.T) {
@@ -689,7 +711,7 @@ gevo_status gevo_pop_export(gevo_pop* p, uint32_t v, float* params_out, uint8_t*
     HIP_TRY(hipMemcpy(M.data(), p->ws + q.mask + (size_t)v * words * 4, words * 4, hipMemcpyDeviceToHost));
     for (int k = 0; k < q.K; ++k)
       for (int n = 0; n < q.N; ++n) {
-        if (params_out) params_out[off + (size_t)k * q.N + n] = W[(size_t)n * q.Kp + k];
+        if (params_out) params_out[off + (size_t)k * q.N + n] = W[((size_t)(k / 32) * q.Np + n) * 32 + k % 32];
         if (mask_out) mask_out[moff + (size_t)k * q.N + n] = (uint8_t)((M[(size_t)n * (q.Kp / 32) + k / 32] >> (k % 32)) & 1u);
       }
     off += (size_t)q.K * q.N;
@@ -719,7 +741,7 @@ gevo_status gevo_pop_import(gevo_pop* p, uint32_t v, const float* params) {
     for (int k = 0; k < q.K; ++k)
       for (int n = 0; n < q.N; ++n) {
         const bool keep = (M[(size_t)n * (q.Kp / 32) + k / 32] >> (k % 32)) & 1u;
-        W[(size_t)n * q.Kp + k] = keep ? params[off + (size_t)k * q.N + n] : 0.0f;
+        W[((size_t)(k / 32) * q.Np + n) * 32 + k % 32] = keep ? params[off + (size_t)k * q.N + n] : 0.0f;
       }
     off += (size_t)q.K * q.N;
     for (int n = 0; n < q.N; ++n) b[n] = params[off + n];

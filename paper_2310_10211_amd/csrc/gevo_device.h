@@ -1,0 +1,88 @@
+// Device-side helpers shared by the HIP kernels of libgevo (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gevo {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ int crow(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// round-to-nearest-even binary32 -> bfloat16; NaN stays a quiet NaN
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x0040u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <typename S> struct Op;
+
+template <> struct Op<uint16_t> {           // bfloat16 operands
+  static constexpr int KM = 16;              // contraction per MFMA
+  static constexpr int KE = 8;               // consecutive elements per lane
+  static constexpr int PAD = 8;              // LDS row padding (elements)
+  typedef uint4 Frag;
+  __device__ __forceinline__ static Frag load(const uint16_t* p) { return *reinterpret_cast<const uint4*>(p); }
+  __device__ __forceinline__ static Frag gather(const uint16_t* p, int stride) {
+    uint4 f;
+    f.x = (uint32_t)p[0] | ((uint32_t)p[stride] << 16);
+    f.y = (uint32_t)p[2 * stride] | ((uint32_t)p[3 * stride] << 16);
+    f.z = (uint32_t)p[4 * stride] | ((uint32_t)p[5 * stride] << 16);
+    f.w = (uint32_t)p[6 * stride] | ((uint32_t)p[7 * stride] << 16);
+    return f;
+  }
+  __device__ __forceinline__ static f32x16_t mma(Frag a, Frag b, f32x16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+  }
+  __device__ __forceinline__ static uint16_t from_f32(float f) { return f32_to_bf16_bits(f); }
+  __device__ __forceinline__ static float to_f32(uint16_t h) { return bf16_bits_to_f32(h); }
+};
+
+template <> struct Op<float> {              // fp32 operands
+  static constexpr int KM = 2;
+  static constexpr int KE = 1;
+  static constexpr int PAD = 1;
+  typedef float Frag;
+  __device__ __forceinline__ static Frag load(const float* p) { return *p; }
+  __device__ __forceinline__ static Frag gather(const float* p, int) { return *p; }
+  __device__ __forceinline__ static f32x16_t mma(Frag a, Frag b, f32x16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+  __device__ __forceinline__ static float from_f32(float f) { return f; }
+  __device__ __forceinline__ static float to_f32(float h) { return h; }
+};
+
+__device__ __forceinline__ f32x16_t zero16() {
+  f32x16_t z;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) z[i] = 0.0f;
+  return z;
+}
+
+// ------------------------------------------------------------------ Philox
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two
+// 32x32->64-bit products; high halves are xored with the other counter words
+// and the round key, which is bumped by the Weyl constants between rounds.
+__device__ __forceinline__ uint4 philox(uint4 c, uint2 k) {
+#pragma unroll
+  for (int i = 0; i < 10; ++i) {
+    const uint32_t hi0 = __umulhi(0xD2511F53u, c.x), lo0 = 0xD2511F53u * c.x;
+    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c.z), lo1 = 0xCD9E8D57u * c.z;
+    c = make_uint4(hi1 ^ c.y ^ k.x, lo1, hi0 ^ c.w ^ k.y, lo0);
+    k.x += 0x9E3779B9u;
+    k.y += 0xBB67AE85u;
+  }
+  return c;
+}
+__device__ __forceinline__ uint32_t pick(uint4 r, uint32_t i) {
+  return i == 0 ? r.x : (i == 1 ? r.y : (i == 2 ? r.z : r.w));
+}
+
+}  // namespace gevo

@@ -35,7 +35,7 @@ struct InitArgs {
   const float* base_w;           // optional base weights, device, [Np][Kp] padded (layer slice)
   const float* base_b;           // optional base biases, device, [Np]
   const uint32_t* thresh;        // [P] mask thresholds
-  float* Wm;                     // [P][Np][Kp]
+  float* Wm;                     // [P][Kp/32][Np][32] (k-blocked)
   float* bias;                   // [P][Np]
   uint32_t* mask;                // [P][Np][Kp/32] row words
 };
@@ -45,7 +45,7 @@ struct LayerArgs {
   int Kp, Np;                    // padded input / output width of the layer
   int KB;                        // input columns per LDS block (set by the launcher)
   int Bp;                        // padded batch rows of the update
-  float* Wm;                     // [P][Np][Kp] fp32 master
+  float* Wm;                     // [P][Kp/32][Np][32] fp32 master (k-blocked)
   float* bias;                   // [P][Np]
   const uint32_t* mask;          // [P][Np][Kp/32] row words: bit k%32 of word [n][k/32]
   const float* lr;               // [P]
@@ -65,7 +65,7 @@ struct OutArgs {
   int Kp;                        // padded width of the last hidden layer (input of the output layer)
   int C;                         // classes (<= 32); padded output width is 32
   int Bp;                        // padded batch rows (training)
-  float* Wm;                     // [P][32][Kp]
+  float* Wm;                     // [P][Kp/32][32][32] (k-blocked)
   float* bias;                   // [P][32]
   const uint32_t* mask;          // [P][32][Kp/32] row words
   const float* lr;               // [P]
@@ -93,6 +93,22 @@ struct BwdArgs {
   const S* Acols; size_t ac_vs;  // [v][Kp][Bp] activations of layer l-1 (for ReLU')
   S* Gcols; size_t gc_vs;        // [v][Kp][Bp] gradient at layer l-1 output
   S* Grows_out; size_t go_vs;    // [v][Bp][Kp] (nullable)
+};
+
+// Fused per-variant training of a two-layer net (bf16 operands), one
+// workgroup per variant over steps [t0, t1) of an epoch.
+struct Fused2Args {
+  int Kp, Hp, C, B, Bp, T;       // input width, hidden width (128|256), classes, batch, padded batch, steps/epoch
+  int64_t n;                     // training rows
+  int t0, t1;
+  const uint16_t* xrows;         // [T][Bp][Kp] bf16 bits
+  const uint16_t* xcols;         // [T][Kp][Bp]
+  const int32_t* labels;         // [T][Bp]
+  float* W1; float* b1; const uint32_t* m1;   // [P][Kp/32][Hp][32], [P][Hp], [P][Hp][Kp/32]
+  float* W2; float* b2; const uint32_t* m2;   // [P][Hp/32][32][32], [P][32], [P][32][Hp/32]
+  const float* lr;
+  double* ce_acc;
+  unsigned long long* correct_acc;
 };
 
 struct GatherArgs {
@@ -125,6 +141,8 @@ template <typename S> hipError_t launch_bwd(const BwdArgs<S>& a, int P, hipStrea
 template <typename S> hipError_t launch_gather(const GatherArgs& a, hipStream_t s, const LaunchEv& ev);
 template <typename S> hipError_t launch_transpose(const TransposeArgs& a, hipStream_t s, const LaunchEv& ev);
 hipError_t launch_zero_bytes(void* p, size_t bytes, hipStream_t s, const LaunchEv& ev);
+hipError_t launch_fused2(const Fused2Args& a, int P, hipStream_t s, const LaunchEv& ev);
+size_t fused2_lds_bytes(int hp, int bp);     // 0 when the shape has no fused instantiation
 hipError_t launch_reduce_partials(const double* part_ce, const unsigned int* part_corr, int P, int n_chunks,
                                   double* ce_out, unsigned long long* corr_out, hipStream_t s, const LaunchEv& ev);
 

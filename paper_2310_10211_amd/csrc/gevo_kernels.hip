@@ -4,7 +4,8 @@
 //
 // Device layout (per variant v, layer l with padded input width Kp and padded
 // output width Np, both multiples of 32):
-//   Wm   fp32 master weights, [v][Np][Kp]  ("out x in": k is contiguous)
+//   Wm   fp32 master weights, k-blocked [v][Kp/32][Np][32]: element (n, k) at
+//        ((k/32)*Np + n)*32 + k%32, so every 32-column block is one contiguous run
 //   bias fp32 [v][Np]
 //   mask uint32 row words, [v][Np][Kp/32] (bit k%32 of word [n][k/32])
 // Activations and gradients come in two orientations: "rows" [v][b][feature]
@@ -17,90 +18,12 @@
 // B[(l/32)*E + i][l%32]; the 16 accumulators of lane l hold
 // C[8*(r/4) + 4*(l/32) + r%4][l%32], r = 0..15.
 #include "gevo_internal.h"
+#include "gevo_device.h"
 
 #include <hip/hip_ext.h>
 #include <math.h>
 
 namespace gevo {
-
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
-
-__device__ __forceinline__ int crow(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
-
-__device__ __forceinline__ float bf16_bits_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
-
-// round-to-nearest-even binary32 -> bfloat16; NaN stays a quiet NaN
-__device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x0040u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
-
-template <typename S> struct Op;
-
-template <> struct Op<uint16_t> {           // bfloat16 operands
-  static constexpr int KM = 16;              // contraction per MFMA
-  static constexpr int KE = 8;               // consecutive elements per lane
-  static constexpr int PAD = 8;              // LDS row padding (elements)
-  typedef uint4 Frag;
-  __device__ __forceinline__ static Frag load(const uint16_t* p) { return *reinterpret_cast<const uint4*>(p); }
-  __device__ __forceinline__ static Frag gather(const uint16_t* p, int stride) {
-    uint4 f;
-    f.x = (uint32_t)p[0] | ((uint32_t)p[stride] << 16);
-    f.y = (uint32_t)p[2 * stride] | ((uint32_t)p[3 * stride] << 16);
-    f.z = (uint32_t)p[4 * stride] | ((uint32_t)p[5 * stride] << 16);
-    f.w = (uint32_t)p[6 * stride] | ((uint32_t)p[7 * stride] << 16);
-    return f;
-  }
-  __device__ __forceinline__ static f32x16_t mma(Frag a, Frag b, f32x16_t c) {
-    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
-                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
-  }
-  __device__ __forceinline__ static uint16_t from_f32(float f) { return f32_to_bf16_bits(f); }
-  __device__ __forceinline__ static float to_f32(uint16_t h) { return bf16_bits_to_f32(h); }
-};
-
-template <> struct Op<float> {              // fp32 operands
-  static constexpr int KM = 2;
-  static constexpr int KE = 1;
-  static constexpr int PAD = 1;
-  typedef float Frag;
-  __device__ __forceinline__ static Frag load(const float* p) { return *p; }
-  __device__ __forceinline__ static Frag gather(const float* p, int) { return *p; }
-  __device__ __forceinline__ static f32x16_t mma(Frag a, Frag b, f32x16_t c) {
-    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
-  }
-  __device__ __forceinline__ static float from_f32(float f) { return f; }
-  __device__ __forceinline__ static float to_f32(float h) { return h; }
-};
-
-__device__ __forceinline__ f32x16_t zero16() {
-  f32x16_t z;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) z[i] = 0.0f;
-  return z;
-}
-
-// ------------------------------------------------------------------ Philox
-// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two
-// 32x32->64-bit products; high halves are xored with the other counter words
-// and the round key, which is bumped by the Weyl constants between rounds.
-__device__ __forceinline__ uint4 philox(uint4 c, uint2 k) {
-#pragma unroll
-  for (int i = 0; i < 10; ++i) {
-    const uint32_t hi0 = __umulhi(0xD2511F53u, c.x), lo0 = 0xD2511F53u * c.x;
-    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c.z), lo1 = 0xCD9E8D57u * c.z;
-    c = make_uint4(hi1 ^ c.y ^ k.x, lo1, hi0 ^ c.w ^ k.y, lo0);
-    k.x += 0x9E3779B9u;
-    k.y += 0xBB67AE85u;
-  }
-  return c;
-}
-__device__ __forceinline__ uint32_t pick(uint4 r, uint32_t i) {
-  return i == 0 ? r.x : (i == 1 ? r.y : (i == 2 ? r.z : r.w));
-}
 
 // ------------------------------------------------------------ population init
 // One thread per (variant, padded output row n, 32-wide word of inputs k):
@@ -118,7 +41,7 @@ __global__ __launch_bounds__(256) void k_init(InitArgs a) {
     uint32_t bits = 0;
     {
       const uint32_t th = a.thresh[v];
-      float* wrow = a.Wm + ((size_t)v * a.Np + n) * a.Kp + kw * 32;
+      float* wrow = a.Wm + (size_t)v * a.Np * a.Kp + ((size_t)kw * a.Np + n) * 32;
       uint64_t blk_m = ~0ull, blk_i = ~0ull, blk_n = ~0ull;
       uint4 rm = make_uint4(0, 0, 0, 0), ri = rm, rn = rm;
       for (int j = 0; j < 32; ++j) {
@@ -195,7 +118,7 @@ __global__ __launch_bounds__(256, 2) void k_layer(LayerArgs<S> a) {
   const int l32 = lane & 31, lh = lane >> 5;
   const int n0 = blockIdx.x * 32, v = blockIdx.y;
   const int Kp = a.Kp, Np = a.Np, kwords = Kp / 32;
-  float* Wm = a.Wm + ((size_t)v * Np + n0) * Kp;             // this tile's 32 rows
+  float* Wv = a.Wm + (size_t)v * Np * Kp;                     // this variant, k-blocked
   const uint32_t* mk = a.mask + ((size_t)v * Np + n0) * kwords;
   const float lrv = a.lr[v];
   const int nsteps = a.Bp / KM;
@@ -236,14 +159,15 @@ __global__ __launch_bounds__(256, 2) void k_layer(LayerArgs<S> a) {
     const int kw = min(KB, Kp - kb0);
     const int nchb = kw / 32;
     if (upd) {
-      const float* wrow = Wm + (size_t)rn * Kp + kb0 + cs;
+      // row rn of the tile in 32-column chunk c of this block
+      auto wptr = [&](int c) { return Wv + ((size_t)(kb0 / 32 + c) * Np + n0 + rn) * 32 + cs; };
       const uint32_t* mrow = mk + (size_t)rn * kwords + kb0 / 32;
       const S* acb = a.Acols + v * a.ac_vs + (size_t)(kb0 + l32) * a.Bp + lh * KE;
       float4 nx[4];
       uint32_t nmw = 0;
       if (wave < nchb) {
 #pragma unroll
-        for (int u = 0; u < 4; ++u) nx[u] = *reinterpret_cast<const float4*>(wrow + wave * 32 + 4 * u);
+        for (int u = 0; u < 4; ++u) nx[u] = *reinterpret_cast<const float4*>(wptr(wave) + 4 * u);
         nmw = mrow[wave];
       }
       for (int c = wave; c < nchb; c += 4) {
@@ -253,7 +177,7 @@ __global__ __launch_bounds__(256, 2) void k_layer(LayerArgs<S> a) {
         const uint32_t mw = nmw;
         if (c + 4 < nchb) {
 #pragma unroll
-          for (int u = 0; u < 4; ++u) nx[u] = *reinterpret_cast<const float4*>(wrow + (c + 4) * 32 + 4 * u);
+          for (int u = 0; u < 4; ++u) nx[u] = *reinterpret_cast<const float4*>(wptr(c + 4) + 4 * u);
           nmw = mrow[c + 4];
         }
         const S* ap = acb + (size_t)c * 32 * a.Bp;
@@ -281,7 +205,7 @@ __global__ __launch_bounds__(256, 2) void k_layer(LayerArgs<S> a) {
           const bool keep = (mw >> (cs + i)) & 1u;
           wn[i] = keep ? __fsub_rn(w, __fmul_rn(lrv, dw[i])) : 0.0f;
         }
-        float* wdst = Wm + (size_t)rn * Kp + kb0 + c * 32 + cs;
+        float* wdst = wptr(c);
 #pragma unroll
         for (int u = 0; u < 4; ++u)
           *reinterpret_cast<float4*>(wdst + 4 * u) = make_float4(wn[4 * u], wn[4 * u + 1], wn[4 * u + 2], wn[4 * u + 3]);
@@ -299,14 +223,16 @@ __global__ __launch_bounds__(256, 2) void k_layer(LayerArgs<S> a) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int j = i + u * 256;
-          w4[u] = j < 32 * q ? *reinterpret_cast<const float4*>(Wm + (size_t)(j / q) * Kp + kb0 + (j % q) * 4)
+          // j in memory order: chunk j/256, row (j/8)%32, float4 j%8
+          w4[u] = j < 32 * q ? *reinterpret_cast<const float4*>(
+                                   Wv + ((size_t)(kb0 / 32 + j / 256) * Np + n0 + (j / 8) % 32) * 32 + (j % 8) * 4)
                              : make_float4(0, 0, 0, 0);
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int j = i + u * 256;
           if (j < 32 * q) {
-            S* dst = wt + (j / q) * WS + (j % q) * 4;
+            S* dst = wt + ((j / 8) % 32) * WS + (j / 256) * 32 + (j % 8) * 4;
             dst[0] = O::from_f32(w4[u].x); dst[1] = O::from_f32(w4[u].y);
             dst[2] = O::from_f32(w4[u].z); dst[3] = O::from_f32(w4[u].w);
           }
@@ -425,38 +351,43 @@ __global__ __launch_bounds__(256, 2) void k_layer(LayerArgs<S> a) {
 //   dW_L[c][k] = sum_b G[b][c] A[k][b]  + masked SGD update of W_L, b_L
 //   G_{L-1}[k][b] = (sum_c W_L[c][k] G[b][c]) * [A[k][b] > 0]
 // using the pre-update W_L kept in LDS.
+constexpr int kOutWaves = 8;
+
 template <typename S, int BPMAX>
-__global__ __launch_bounds__(256) void k_out(OutArgs<S> a) {
+__global__ __launch_bounds__(64 * kOutWaves) void k_out(OutArgs<S> a) {
   using O = Op<S>;
+  using F = typename O::Frag;
   constexpr int KM = O::KM, KE = O::KE;
   constexpr int GSTR = 32 + O::PAD;
   constexpr int NG = BPMAX / KM;
+  constexpr int NW = kOutWaves;
+  constexpr int NT = 64 * NW;
   extern __shared__ __align__(16) char smem[];
-  __shared__ double red_ce[4];
-  __shared__ unsigned int red_corr[4];
-  __shared__ float red_db[4][32];
+  __shared__ double red_ce[NW];
+  __shared__ unsigned int red_corr[NW];
+  __shared__ float red_db[NW][32];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int l32 = lane & 31, lh = lane >> 5;
   const int v = blockIdx.y, chunk = blockIdx.x;
   const int Kp = a.Kp, WS = Kp + O::PAD;
   S* wop = reinterpret_cast<S*>(smem);                  // [32][WS]  W_L as operand, [class][k]
   S* gs = wop + 32 * WS;                                // [Bp][GSTR] gradient rows (training)
-  float* stg = reinterpret_cast<float*>(gs + (size_t)a.Bp * GSTR);   // [4][32][36] fp32 staging (training)
+  float* stg = reinterpret_cast<float*>(gs + (size_t)a.Bp * GSTR);   // [NW][32][36] fp32 staging (training)
   const float* Wm = a.Wm + (size_t)v * 32 * Kp;
   {
     const int q = Kp / 4;                                // float4 per row
-    for (int i = threadIdx.x; i < 32 * q; i += 256 * 4) {
+    for (int i = threadIdx.x; i < 32 * q; i += NT * 4) {
       float4 w4[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int j = i + u * 256;
+        const int j = i + u * NT;
         w4[u] = j < 32 * q ? *reinterpret_cast<const float4*>(Wm + (size_t)j * 4) : make_float4(0, 0, 0, 0);
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int j = i + u * 256;
+        const int j = i + u * NT;
         if (j < 32 * q) {
-          S* dst = wop + (j / q) * WS + (j % q) * 4;
+          S* dst = wop + ((j / 8) % 32) * WS + (j / 256) * 32 + (j % 8) * 4;   // row (j/8)%32, chunk j/256
           dst[0] = O::from_f32(w4[u].x); dst[1] = O::from_f32(w4[u].y);
           dst[2] = O::from_f32(w4[u].z); dst[3] = O::from_f32(w4[u].w);
         }
@@ -473,19 +404,29 @@ __global__ __launch_bounds__(256) void k_out(OutArgs<S> a) {
   double ce_sum = 0.0;
   unsigned int corr = 0;
   float db_part = 0.0f;
-#pragma unroll
-  for (int ti = 0; ti < 2; ++ti) {
-    const int tile = wave + 4 * ti;
-    if (tile >= ntiles) continue;
-    f32x16_t acc = zero16();
+  for (int tile = wave; tile < ntiles; tile += NW) {
+    f32x16_t acc0 = zero16(), acc1 = zero16();
     const S* ar = a.Arows + v * a.ar_vs + (size_t)(row_base + tile * 32 + l32) * Kp + lh * KE;
     const S* wr = wop + l32 * WS + lh * KE;
-    for (int k = 0; k < Kp; k += KM) acc = O::mma(O::load(ar + k), O::load(wr + k), acc);
+    int k = 0;
+    for (; k + 4 * KM <= Kp; k += 4 * KM) {
+      F x[4], w[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) { x[u] = O::load(ar + k + u * KM); w[u] = O::load(wr + k + u * KM); }
+      acc0 = O::mma(x[0], w[0], acc0);
+      acc1 = O::mma(x[1], w[1], acc1);
+      acc0 = O::mma(x[2], w[2], acc0);
+      acc1 = O::mma(x[3], w[3], acc1);
+    }
+    for (; k < Kp; k += KM) acc0 = O::mma(O::load(ar + k), O::load(wr + k), acc0);
+    int ylab[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) ylab[r] = a.labels[row_base + tile * 32 + crow(r, lane)];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int rl = tile * 32 + crow(r, lane);
-      const int y = a.labels[row_base + rl];
-      const float z = acc[r] + bias_c;
+      const int y = ylab[r];
+      const float z = (acc0[r] + acc1[r]) + bias_c;
       int isn = (cvalid && (z != z)) ? 1 : 0;
       float m = cvalid ? z : -INFINITY;
       float bv = (cvalid && !isn) ? z : -INFINITY;
@@ -526,8 +467,9 @@ __global__ __launch_bounds__(256) void k_out(OutArgs<S> a) {
   if (lh == 0) red_db[wave][l32] = db_part;
   __syncthreads();
   if (threadIdx.x == 0) {
-    const double t = ((red_ce[0] + red_ce[1]) + red_ce[2]) + red_ce[3];
-    const unsigned int cc = red_corr[0] + red_corr[1] + red_corr[2] + red_corr[3];
+    double t = 0.0;
+    unsigned int cc = 0;
+    for (int w = 0; w < NW; ++w) { t += red_ce[w]; cc += red_corr[w]; }
     if (a.train) {
       a.ce_acc[v] += t;
       a.correct_acc[v] += cc;
@@ -540,8 +482,8 @@ __global__ __launch_bounds__(256) void k_out(OutArgs<S> a) {
 
   const float lrv = a.lr[v];
   if (threadIdx.x < 32) {
-    const float db = ((red_db[0][threadIdx.x] + red_db[1][threadIdx.x]) + red_db[2][threadIdx.x]) +
-                     red_db[3][threadIdx.x];
+    float db = 0.0f;
+    for (int w = 0; w < NW; ++w) db += red_db[w][threadIdx.x];
     const float bo = a.bias[(size_t)v * 32 + threadIdx.x];
     a.bias[(size_t)v * 32 + threadIdx.x] = __fsub_rn(bo, __fmul_rn(lrv, db));
   }
@@ -557,11 +499,11 @@ __global__ __launch_bounds__(256) void k_out(OutArgs<S> a) {
   const S* Acv = a.Acols + v * a.ac_vs;
   float* dws = stg + wave * 32 * 36;
   const int rn = lane >> 1, cs = (lane & 1) * 16;
-  for (int kt = wave; kt < Kp / 32; kt += 4) {
+  for (int kt = wave; kt < Kp / 32; kt += NW) {
     const int k0 = kt * 32;
     float4 w4[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) w4[u] = *reinterpret_cast<const float4*>(Wmv + (size_t)rn * Kp + k0 + cs + 4 * u);
+    for (int u = 0; u < 4; ++u) w4[u] = *reinterpret_cast<const float4*>(Wmv + ((size_t)kt * 32 + rn) * 32 + cs + 4 * u);
     const uint32_t mw = mk[(size_t)rn * (Kp / 32) + kt];
     f32x16_t d = zero16();
     const S* ap = Acv + (size_t)(k0 + l32) * a.Bp + lh * KE;
@@ -587,7 +529,7 @@ __global__ __launch_bounds__(256) void k_out(OutArgs<S> a) {
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u)
-      *reinterpret_cast<float4*>(Wmv + (size_t)rn * Kp + k0 + cs + 4 * u) =
+      *reinterpret_cast<float4*>(Wmv + ((size_t)kt * 32 + rn) * 32 + cs + 4 * u) =
           make_float4(wn[4 * u], wn[4 * u + 1], wn[4 * u + 2], wn[4 * u + 3]);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
     __builtin_amdgcn_wave_barrier();
@@ -596,8 +538,11 @@ __global__ __launch_bounds__(256) void k_out(OutArgs<S> a) {
   if (!a.Gcols) return;
   // gradient of the last hidden layer, batch-contiguous, with ReLU'
   const int tb = a.Bp / 32, ntot = (Kp / 32) * tb;
-  for (int t = wave; t < ntot; t += 4) {
+  for (int t = wave; t < ntot; t += NW) {
     const int kt = t / tb, bt = t % tb;
+    float av[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) av[r] = O::to_f32(Acv[(size_t)(kt * 32 + crow(r, lane)) * a.Bp + bt * 32 + l32]);
     f32x16_t acc = zero16();
 #pragma unroll
     for (int ks = 0; ks < 32 / KM; ++ks) {
@@ -609,8 +554,7 @@ __global__ __launch_bounds__(256) void k_out(OutArgs<S> a) {
     for (int r = 0; r < 16; ++r) {
       const int k = kt * 32 + crow(r, lane);
       const int b = bt * 32 + l32;
-      const float av = O::to_f32(Acv[(size_t)k * a.Bp + b]);
-      const S g = O::from_f32(av > 0.0f ? acc[r] : 0.0f);
+      const S g = O::from_f32(av[r] > 0.0f ? acc[r] : 0.0f);
       a.Gcols[v * a.gc_vs + (size_t)k * a.Bp + b] = g;
       if (a.Grows) a.Grows[v * a.gr_vs + (size_t)b * Kp + k] = g;
     }
@@ -753,7 +697,7 @@ hipError_t launch_layer(const LayerArgs<S>& a0, int P, hipStream_t s, const Laun
 template <typename S>
 size_t out_lds_bytes(int Kp, int Bp, int train) {
   return (size_t)32 * (Kp + Op<S>::PAD) * sizeof(S) +
-         (train ? (size_t)Bp * (32 + Op<S>::PAD) * sizeof(S) + (size_t)4 * 32 * 36 * 4 : 0);
+         (train ? (size_t)Bp * (32 + Op<S>::PAD) * sizeof(S) + (size_t)kOutWaves * 32 * 36 * 4 : 0);
 }
 
 template <typename S>
@@ -767,7 +711,7 @@ hipError_t launch_out(const OutArgs<S>& a, int P, hipStream_t s, const LaunchEv&
                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBudget);
       attr = true;
     }
-    hipExtLaunchKernelGGL((k_out<S, 128>), grid, dim3(256), lds, s, ev.start, ev.stop, 0, a);
+    hipExtLaunchKernelGGL((k_out<S, 128>), grid, dim3(64 * kOutWaves), lds, s, ev.start, ev.stop, 0, a);
   } else {
     static bool attr = false;
     if (!attr) {
@@ -775,7 +719,7 @@ hipError_t launch_out(const OutArgs<S>& a, int P, hipStream_t s, const LaunchEv&
                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBudget);
       attr = true;
     }
-    hipExtLaunchKernelGGL((k_out<S, 256>), grid, dim3(256), lds, s, ev.start, ev.stop, 0, a);
+    hipExtLaunchKernelGGL((k_out<S, 256>), grid, dim3(64 * kOutWaves), lds, s, ev.start, ev.stop, 0, a);
   }
   return hipGetLastError();
 }
