@@ -28,7 +28,17 @@ if ROOT not in sys.path:
 
 PEAK = {"bf16": 2500.0, "f32": 157.3}        # dense MFMA TFLOP/s, MI355X
 HBM_PEAK_GBS = 8000.0
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2310_10211_amd", "csrc", "gevo_kernels.hip")
+CSRC = os.path.join(ROOT, "paper_2310_10211_amd", "csrc")
+KERNEL_SOURCES = ["gevo_device.h", "gevo_internal.h", "gevo_kernels.hip", "gevo_fused.hip"]
+# rocprofv3 kernel-name stem -> kernel kind of gevo_pop_kernel_stats (training kind, predict kind)
+KERNEL_KIND_OF = {"k_fused2": ("fused_train", None), "k_layer": ("layer_train", "layer_fwd"),
+                  "k_out": ("out_train", "out_predict"), "k_bwd": ("bwd", None)}
+
+
+def fused_workload(cfg):
+    """Two-layer bf16 nets train in the fused per-variant kernel; the layer and
+    output kernels then only run for prediction."""
+    return len(cfg["dims"]) == 3 and cfg["dtype"] == "bf16"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.json")
 
 
@@ -43,6 +53,9 @@ def parse():
     ap.add_argument("--no-profile", action="store_true", help="time without per-kernel events")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy 3 times (reference for HBM counters) and exit")
+    ap.add_argument("--traffic-from", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
+                    help="only fold rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs of this workload and of "
+                         "--calibrate-copy into profiles/traffic_counters.json and exit")
     return ap.parse_args()
 
 
@@ -115,8 +128,85 @@ def predict_flops_per_sample(dims):
 
 
 def source_sha():
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def _counter_rows(d, counter):
+    """(kernel name, grid size, value KiB) of every dispatch in a rocprofv3 --pmc csv directory."""
+    import csv
+    import glob
+    rows = []
+    for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                if r["Counter_Name"] == counter:
+                    rows.append((r["Kernel_Name"], int(r["Grid_Size"]), float(r["Counter_Value"])))
+    if not rows:
+        raise SystemExit(f"bench.py: no {counter} rows under {d}")
+    return rows
+
+
+def fold_traffic(cfg, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, command):
+    """HBM bytes per launch of each kernel kind: FETCH_SIZE and WRITE_SIZE (KiB per
+    dispatch) scaled by what the same counters read for a plain 1 GiB copy."""
+    n_copy = 4 << 28
+    scale = {}
+    for counter, d in (("FETCH_SIZE", copy_fetch_dir), ("WRITE_SIZE", copy_write_dir)):
+        big = [v for name, _, v in _counter_rows(d, counter) if "copyBuffer" in name and v > 2 ** 19]
+        if not big:
+            raise SystemExit(f"bench.py: no 1 GiB copy dispatch in {d}")
+        scale[counter] = n_copy / (1024.0 * sum(big) / len(big))
+    per = {}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        groups = {}
+        for name, grid, v in _counter_rows(d, counter):
+            stem = next((k for k in KERNEL_KIND_OF if k in name), None)
+            if stem:
+                groups.setdefault((stem, grid), []).append(v)
+        trains = cfg["epochs"] > 0 and not fused_workload(cfg)
+        # the most frequent launch shape of a layer/output kernel is its training launch
+        top = {}
+        for (stem, grid), vals in groups.items():
+            if stem not in top or len(vals) > len(groups[(stem, top[stem])]):
+                top[stem] = grid
+        for (stem, grid), vals in groups.items():
+            tr_kind, pr_kind = KERNEL_KIND_OF[stem]
+            kind = tr_kind if (stem == "k_fused2" or (trains and grid == top[stem])) else pr_kind
+            if kind is None:
+                continue
+            cur = per.get(kind)
+            # a kernel kind launched with several grids: keep the most frequent launch shape
+            if cur is None or cur["grid"] == grid or len(vals) > cur["n"][counter]:
+                if cur is None or cur["grid"] != grid:
+                    cur = per[kind] = dict(grid=grid, n={"FETCH_SIZE": 0, "WRITE_SIZE": 0}, kib={})
+                cur["n"][counter] = len(vals)
+                cur["kib"][counter] = sum(vals) / len(vals)
+    try:
+        with open(TRAFFIC_FILE) as f:
+            table = json.load(f)
+    except (OSError, ValueError):
+        table = {}
+    rec = table.setdefault(cfg["name"], {})
+    sha = source_sha()
+    for kind, r in per.items():
+        if len(r["kib"]) != 2:
+            continue
+        rec[kind] = dict(kernel_source_sha=sha, grid=r["grid"], dispatches=r["n"],
+                         fetch_kib_per_dispatch=round(r["kib"]["FETCH_SIZE"], 3),
+                         write_kib_per_dispatch=round(r["kib"]["WRITE_SIZE"], 3),
+                         fetch_scale=round(scale["FETCH_SIZE"], 4), write_scale=round(scale["WRITE_SIZE"], 4),
+                         hbm_bytes_per_launch=int(1024 * (r["kib"]["FETCH_SIZE"] * scale["FETCH_SIZE"]
+                                                          + r["kib"]["WRITE_SIZE"] * scale["WRITE_SIZE"])),
+                         command=command)
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(table, f, indent=1, sort_keys=True)
+        f.write("\n")
+    print(json.dumps(rec))
 
 
 def traffic_for(kernel, workload):
@@ -176,6 +266,12 @@ def main():
 
     if args.calibrate_copy:
         calibrate_copy()
+        return
+    if args.traffic_from:
+        import synthetic
+        fold_traffic(synthetic.config(args.config), *args.traffic_from,
+                     command=f"rocprofv3 --pmc FETCH_SIZE|WRITE_SIZE --output-format csv -- python3 bench.py "
+                             f"--config {args.config} --steps 1 --warmup 0 --no-cpu --no-profile")
         return
 
     import torch
