@@ -24,7 +24,26 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
+def check_fused_prefetch() -> dict:
+    """Compile the fused kernel to gfx950 assembly and verify its prefetch
+    register discipline (see check_prefetch.py)."""
+    import tempfile
+
+    from . import check_prefetch
+    with tempfile.TemporaryDirectory() as d:
+        out = os.path.join(d, "gevo_fused.s")
+        cmd = [hipcc(), *[f for f in FLAGS if f not in ("-fPIC", "-shared")], "--cuda-device-only", "-S",
+               "-I", os.path.join(ROOT, "include"), "-I", os.path.join(HERE, "csrc"),
+               "-o", out, os.path.join(HERE, "csrc", "gevo_fused.hip")]
+        res = subprocess.run(cmd, capture_output=True, text=True)
+        if res.returncode != 0:
+            raise RuntimeError("hipcc -S failed: " + res.stderr[-2000:])
+        with open(out) as f:
+            return check_prefetch.check_assembly(f.read())
+
+
 def build(verbose: bool = False) -> str:
+    check_fused_prefetch()
     tmp = LIB + ".tmp"
     cmd = [hipcc(), *FLAGS, "-I", os.path.join(ROOT, "include"), "-I", os.path.join(HERE, "csrc"),
            "-o", tmp, *SOURCES]

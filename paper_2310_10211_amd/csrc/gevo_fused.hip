@@ -5,9 +5,14 @@
 //
 // Per step t, for hidden width HP and batch tile BP
 // (one wave per 32 hidden units, HP/32 waves):
-//   A1 = relu(Z1 + b1) -> LDS (bf16), ReLU' bits kept in registers
-//   logits = A1 W2^T + b2, softmax cross-entropy, argmax, G2 = (p - y) / b
-//   G1 = (G2 W2) * ReLU'   (old W2),   dW2 = G2^T A1,  W2, b2, b1 updated
+//   A1 = relu(Z1 + b1): rows -> LDS (logits operand), bf16 pairs kept in
+//        registers (dW2 operand), ReLU' bits in registers
+//   logits^T = W2 A1^T + b2 (one batch tile per wave, so a lane holds one
+//        row's classes, split over lanes l and l+32); softmax cross-entropy,
+//        argmax and G2 = (p - y) fl(1/b) in the same registers; G2 -> LDS in
+//        both orientations, fp32 G2 -> LDS columns for db2
+//   dW2 = G2^T A1,  G1 = (G2 W2) * ReLU' (pre-update W2),  db1, db2;
+//        W2 (fp32 master in LDS), b2, b1 updated
 //   then, streaming the fp32 master W1 once per 32-column block k:
 //     dW1[k][n] = sum_b X_t[b][k] G1[b][n]           (MFMA, contraction = batch)
 //     W1 = mask ? fl(W1 - fl(lr dW1)) : +0           (float4 in place)
@@ -18,13 +23,22 @@
 // over the rows {16s + 4(l/32) + 0..3, 16s + 8 + 4(l/32) + 0..3}) lets a tile
 // produced as an accumulator feed the next MFMA directly; the other operand is
 // read from LDS with the same row permutation.  This is how G1 (accumulators
-// over b) feeds dW1 and how the updated W1 (accumulators over k) feeds the
-// forward pass without leaving registers.
+// over b) feeds dW1, how A1 feeds dW2, how the lane's own W2 master values
+// feed G1, and how the updated W1 (accumulators over k) feeds the forward pass
+// without leaving registers.
+//
+// The W1 stream is software-pipelined one block ahead and the shared X blocks
+// two blocks ahead; the block loop is unrolled by two with alternating
+// register sets.  The W1 block loads are issued after the block's X loads as
+// explicit instructions with one explicit wait at the top of the next block,
+// so no wait for a compiler-visible load can also drain the W1 prefetch.
 #include "gevo_internal.h"
 #include "gevo_device.h"
 
 #include <hip/hip_ext.h>
 #include <math.h>
+
+#include <type_traits>
 
 namespace gevo {
 
@@ -38,315 +52,459 @@ __device__ __forceinline__ uint4 ld2x8(const uint16_t* p0, const uint16_t* p1) {
 
 __device__ __forceinline__ uint32_t pack2(uint16_t lo, uint16_t hi) { return (uint32_t)lo | ((uint32_t)hi << 16); }
 
+__device__ __forceinline__ uint4 pack8(const uint16_t* u) {
+  return make_uint4(pack2(u[0], u[1]), pack2(u[2], u[3]), pack2(u[4], u[5]), pack2(u[6], u[7]));
+}
+
 __device__ __forceinline__ float f4get(const float4& f, int i) {
   return i == 0 ? f.x : (i == 1 ? f.y : (i == 2 ? f.z : f.w));
 }
+
+typedef float f32x4_t __attribute__((ext_vector_type(4)));   // register-operand form of float4
 
 }  // namespace
 
 template <int HP, int BP>
 struct Fused2Lds {
+  static constexpr int NW = HP / 32;     // waves
+  static constexpr int BT = BP / 32;     // batch tiles
+  static constexpr int NBS = BP / 16;    // contraction steps over the batch
   static constexpr int XR = 32 + 8;      // X row block [BP][32]
   static constexpr int XC = BP + 8;      // X col block [32][BP]
-  static constexpr int AS = HP + 8;      // A1 [BP][HP]
-  static constexpr int W2S = HP + 8;     // W2 operand [32][HP]
-  static constexpr int W2T = 32 + 8;     // W2 operand transposed [HP][32]
-  static constexpr int GS = 32 + 8;      // G2 [BP][32]
+  static constexpr int AS = HP + 8;      // A1 rows [BP][HP]
+  static constexpr int W2S = HP + 8;     // W2 bf16 operand [32][HP]
+  static constexpr int GS = 32 + 8;      // G2 rows [BP][32]
+  static constexpr int GTS = BP + 8;     // G2 columns [32][BP]
+  // region X, block loop: two X row blocks and two X column blocks
   static constexpr size_t xr = 0;
   static constexpr size_t xc = xr + 2ull * BP * XR * 2;
-  static constexpr size_t a1 = xc + 2ull * 32 * XC * 2;
-  static constexpr size_t w2 = a1 + (size_t)BP * AS * 2;
-  static constexpr size_t w2t = w2 + 32ull * W2S * 2;
-  static constexpr size_t g2 = w2t + (size_t)HP * W2T * 2;
-  static constexpr size_t b2 = g2 + (size_t)BP * GS * 2;
-  static constexpr int NW = HP / 32;    // waves
-  static constexpr size_t m2 = b2 + 32 * 4;                  // [32][HP/32] W2 mask words
-  static constexpr size_t rce = m2 + 32 * (HP / 32) * 4;     // [BP] per-row loss
-  static constexpr size_t rco = rce + (size_t)BP * 8;        // [BP] per-row hit
+  static constexpr size_t xend = xc + 2ull * 32 * XC * 2;
+  // region X, output-layer phase
+  static constexpr size_t g2 = 0;
+  static constexpr int ZGS = BP + 1;     // fp32 G2 columns [32][BP]
+  static constexpr size_t g2t = g2 + (size_t)BP * GS * 2;
+  static constexpr size_t zg = g2t + 32ull * GTS * 2;       // [32][ZGS] fp32
+  static constexpr size_t yl = zg + 32ull * ZGS * 4;        // [BP] labels of the step
+  static constexpr size_t send = yl + (size_t)BP * 4;
+  static_assert(send <= xend, "output-layer scratch must fit in the X buffers");
+  // region A: A1 rows in the output-layer phase, G1 operand slots in the block loop
+  static constexpr size_t a1 = (xend + 15) / 16 * 16;
+  static constexpr size_t a1_bytes = (size_t)BP * AS * 2;
+  static_assert((size_t)NW * NBS * 64 * 16 <= a1_bytes, "G1 slots must fit in the A1 region");
+  // persistent: W2 bf16 operand, W2 fp32 master (swizzled rows), b2
+  static constexpr size_t w2 = a1 + a1_bytes;
+  static constexpr size_t w2m = (w2 + 32ull * W2S * 2 + 15) / 16 * 16;
+  static constexpr size_t b2 = w2m + (size_t)HP * 32 * 4;
+  static constexpr int NDP = 2 * NW;     // db2 partial sums per class
+  static constexpr size_t dbp = b2 + 32 * 4;                // [NDP][32] fp32
+  static constexpr size_t rce = dbp + (size_t)NDP * 32 * 4; // [BP] fp64 per-row loss
+  static constexpr size_t rco = rce + (size_t)BP * 8;       // [BP] per-row hit
   static constexpr size_t bytes = rco + (size_t)BP * 4;
-  static_assert((size_t)BP * 33 * 4 + (size_t)NW * 2 * 32 * 4 <= a1, "layer-2 staging must fit in the X buffers");
+  static_assert(rce % 8 == 0, "fp64 row losses must be 8-byte aligned");
 };
 
 template <int HP, int BP>
 __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
   using O = Op<uint16_t>;
-  typedef uint4 F;
   typedef Fused2Lds<HP, BP> Ly;
   constexpr int NW = Ly::NW;                 // waves, one per 32 hidden units
   constexpr int NT = 64 * NW;                // threads
   constexpr int XU = (4 * BP + NT - 1) / NT; // 16-byte X chunks per thread per block
-  constexpr int BT = BP / 32;                // batch tiles
-  constexpr int NBS = BP / 16;               // contraction steps over the batch
-  constexpr int ZS = 33;                     // row stride of the fp32 logit staging
+  constexpr int BT = Ly::BT;
+  constexpr int NBS = Ly::NBS;
   extern __shared__ __align__(16) char smem[];
   uint16_t* xr = reinterpret_cast<uint16_t*>(smem + Ly::xr);
   uint16_t* xc = reinterpret_cast<uint16_t*>(smem + Ly::xc);
-  uint16_t* a1 = reinterpret_cast<uint16_t*>(smem + Ly::a1);
-  uint16_t* w2 = reinterpret_cast<uint16_t*>(smem + Ly::w2);
-  uint16_t* w2t = reinterpret_cast<uint16_t*>(smem + Ly::w2t);
   uint16_t* g2 = reinterpret_cast<uint16_t*>(smem + Ly::g2);
+  uint16_t* g2t = reinterpret_cast<uint16_t*>(smem + Ly::g2t);
+  float* zg = reinterpret_cast<float*>(smem + Ly::zg);
+  int* yl = reinterpret_cast<int*>(smem + Ly::yl);
+  float* dbp = reinterpret_cast<float*>(smem + Ly::dbp);
+  double* rce = reinterpret_cast<double*>(smem + Ly::rce);
+  unsigned int* rco = reinterpret_cast<unsigned int*>(smem + Ly::rco);
+  uint16_t* a1 = reinterpret_cast<uint16_t*>(smem + Ly::a1);
+  uint4* g1s = reinterpret_cast<uint4*>(smem + Ly::a1);
+  uint16_t* w2 = reinterpret_cast<uint16_t*>(smem + Ly::w2);
+  float* w2m = reinterpret_cast<float*>(smem + Ly::w2m);
   float* b2s = reinterpret_cast<float*>(smem + Ly::b2);
-  uint32_t* m2s = reinterpret_cast<uint32_t*>(smem + Ly::m2);
-  double* red_row_ce = reinterpret_cast<double*>(smem + Ly::rce);
-  unsigned int* red_row_co = reinterpret_cast<unsigned int*>(smem + Ly::rco);
-  // layer-2 phase scratch, aliasing the X staging buffers (idle between passes)
-  float* zb = reinterpret_cast<float*>(smem + Ly::xr);                    // [BP][ZS]
-  float* dbpart = zb + BP * ZS;                                           // [NW][32]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, lh = lane >> 5;
   const int v = blockIdx.x;
-  const int Kp = a.Kp, nkb = Kp / 32, kw1 = Kp / 32;
+  const int Kp = a.Kp, nkb = Kp / 32;
   const int n = wave * 32 + l32;             // hidden unit of this lane's column
   float* W1 = a.W1 + (size_t)v * HP * Kp;
-  const uint32_t* m1 = a.m1 + (size_t)v * HP * kw1;
+  const uint32_t* m1 = a.m1 + (size_t)v * HP * nkb;
   float* W2 = a.W2 + (size_t)v * 32 * HP;
   const uint32_t* m2 = a.m2 + (size_t)v * 32 * (HP / 32);
   const float lrv = a.lr[v];
 
-  // resident layer 2: fp32 master of this lane's 16 (class, unit) pairs in
-  // registers, bf16 operand copies in both orientations and the mask in LDS
-  float w2r[16];
+  // Output layer, resident for the whole run: the fp32 master of this lane's
+  // 16 (class, unit) pairs lives in LDS row n (4-float chunk j stored at chunk
+  // j ^ (n & 7), which spreads the lanes of a row read over all banks); the
+  // bf16 operand copy [class][unit] feeds the logits; mask bits in a register.
+  float* w2row = w2m + n * 32;
+  const int sw = n & 7;
+  uint32_t m2bits = 0;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) w2r[r] = W2[((size_t)wave * 32 + crow(r, lane)) * 32 + l32];
-  for (int i = tid; i < 32 * HP; i += NT) {      // W2 k-blocked [HP/32][32][32]
-    const int c = (i >> 5) & 31, nn = (i >> 10) * 32 + (i & 31);
-    const uint16_t u = O::from_f32(W2[i]);
-    w2[c * Ly::W2S + nn] = u;
-    w2t[nn * Ly::W2T + c] = u;
+  for (int q = 0; q < 4; ++q) {
+    float f[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 4 * q + i, c = crow(r, lane);
+      f[i] = W2[((size_t)wave * 32 + c) * 32 + l32];
+      w2[c * Ly::W2S + n] = O::from_f32(f[i]);
+      m2bits |= ((m2[c * (HP / 32) + wave] >> l32) & 1u) << r;
+    }
+    *reinterpret_cast<float4*>(w2row + (((2 * q + lh) ^ sw) << 2)) = make_float4(f[0], f[1], f[2], f[3]);
   }
   if (tid < 32) b2s[tid] = a.b2[(size_t)v * 32 + tid];
-  for (int i = tid; i < 32 * (HP / 32); i += NT) m2s[i] = m2[i];
   float b1v = a.b1[(size_t)v * HP + n];
   double ce_tot = 0.0;
   unsigned long long corr_tot = 0;
-  if (tid == 0) {
+  const int tot_tid = (NW - 1) * 64;          // thread that keeps the loss / hit totals
+  if (tid == tot_tid) {
     ce_tot = a.ce_acc[v];
     corr_tot = a.correct_acc[v];
   }
 
   f32x16_t zacc[BT];
-  F g1p[NBS];
 
-  // ---- head of the next pass over the input columns, loaded into registers
-  //      ahead of time: X blocks 0 and 1, W1 block 0 and its mask words, and
-  //      the labels of the step whose loss the pass prepares
-  uint4 xr0[XU], xc0[XU], xr1[XU], xc1[XU];
-  float4 wn[4];
-  uint32_t mwn = 0;
+  // Prefetch registers of the block loop: two sets of X staging registers
+  // (block kb+1 waiting for its LDS buffer, block kb+2 in flight) and two sets
+  // of W1 master registers (block kb in use, block kb+1 in flight).
+  uint4 xAr[XU], xAc[XU], xBr[XU], xBc[XU];
+  f32x4_t wA[4], wB[4];
+  uint32_t mA = 0, mB = 0;
   int ylab = -1;
-  auto load_x = [&](bool upd, int tu, bool fwd, int tf, int kb, uint4 (&xrn)[XU], uint4 (&xcn)[XU]) {
+  // (registers of a block past the end are left as they are: such a block is never stored)
+  auto load_x = [&](auto updc, int tu, auto fwdc, int tf, int kb, int td, uint4 (&xrn)[XU], uint4 (&xcn)[XU]) {
+    constexpr bool upd = decltype(updc)::value, fwd = decltype(fwdc)::value;
     const uint16_t* xrs = a.xrows + (size_t)tf * BP * Kp;
     const uint16_t* xcs = a.xcols + (size_t)tu * Kp * BP;
 #pragma unroll
     for (int u = 0; u < XU; ++u) {
-      xrn[u] = xcn[u] = make_uint4(0, 0, 0, 0);
-      const int i = tid + NT * u;
-      if (kb < nkb && i < 4 * BP) {
-        if (fwd) {
+      const int i = td + NT * u;
+      const int kc = kb < nkb ? kb : nkb - 1;   // past the end: an in-bounds re-read, never stored
+      if (i < 4 * BP) {
+        if constexpr (fwd) {
           const int b = i >> 2, q = i & 3;
-          xrn[u] = *reinterpret_cast<const uint4*>(xrs + (size_t)b * Kp + kb * 32 + q * 8);
+          xrn[u] = *reinterpret_cast<const uint4*>(xrs + (size_t)b * Kp + kc * 32 + q * 8);
         }
-        if (upd) {
+        if constexpr (upd) {
           const int k = i / (BP / 8), q = i % (BP / 8);
-          xcn[u] = *reinterpret_cast<const uint4*>(xcs + (size_t)(kb * 32 + k) * BP + q * 8);
+          xcn[u] = *reinterpret_cast<const uint4*>(xcs + (size_t)(kc * 32 + k) * BP + q * 8);
         }
       }
     }
   };
-  auto store_x = [&](bool upd, bool fwd, int buf, const uint4 (&xrn)[XU], const uint4 (&xcn)[XU]) {
+  auto store_x = [&](auto updc, auto fwdc, int buf, int td, const uint4 (&xrn)[XU], const uint4 (&xcn)[XU]) {
+    constexpr bool upd = decltype(updc)::value, fwd = decltype(fwdc)::value;
 #pragma unroll
     for (int u = 0; u < XU; ++u) {
-      const int i = tid + NT * u;
+      const int i = td + NT * u;
       if (i < 4 * BP) {
-        if (fwd) {
+        if constexpr (fwd) {
           const int b = i >> 2, q = i & 3;
           *reinterpret_cast<uint4*>(xr + buf * BP * Ly::XR + b * Ly::XR + q * 8) = xrn[u];
         }
-        if (upd) {
+        if constexpr (upd) {
           const int k = i / (BP / 8), q = i % (BP / 8);
           *reinterpret_cast<uint4*>(xc + buf * 32 * Ly::XC + k * Ly::XC + q * 8) = xcn[u];
         }
       }
     }
   };
-  auto issue_head = [&](bool upd, int tu, bool fwd, int tf) {
-    load_x(upd, tu, fwd, tf, 0, xr0, xc0);
-    load_x(upd, tu, fwd, tf, 1, xr1, xc1);
+  // head of the next pass over the input columns: X blocks 0 and 1, W1 block 0
+  // and its mask words, and the labels of the step whose loss the pass prepares
+  auto issue_head = [&](auto updc, int tu, auto fwdc, int tf, int td) {
+    constexpr bool upd = decltype(updc)::value, fwd = decltype(fwdc)::value;
+    const int n = wave * 32 + (td & 31), lh = (td >> 5) & 1;
+    load_x(updc, tu, fwdc, tf, 0, td, xAr, xAc);
+    load_x(updc, tu, fwdc, tf, 1, td, xBr, xBc);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) wn[q] = *reinterpret_cast<const float4*>(W1 + (size_t)n * 32 + 8 * q + 4 * lh);
-    mwn = upd ? m1[(size_t)n * kw1] : 0u;
-    if (fwd && tid < BP) ylab = a.labels[(size_t)tf * BP + tid];
+    for (int q = 0; q < 4; ++q) wA[q] = *reinterpret_cast<const f32x4_t*>(W1 + (size_t)n * 32 + 8 * q + 4 * lh);
+    mA = upd ? m1[(size_t)n * nkb] : 0u;
+    if (fwd && td < BP) ylab = a.labels[(size_t)tf * BP + td];
   };
 
-  // ---- one pass over the input columns (head already issued): optional dW1 +
-  //      update (step tu), optional forward accumulation of step tf into zacc
-  auto kloop = [&](bool upd, int tu, bool fwd, int tf) {
-    if (fwd) {
+  // one 32-column block of a pass: dW1 + update of block kb (step tu) and/or
+  // forward accumulation of step tf; wc/mc hold block kb, wn/mn receive block
+  // kb+1, xl receives X block kb+2, xs holds X block kb+1 for the other buffer
+  auto kblock = [&](auto updc, int tu, auto fwdc, int tf, int kb, int td, f32x4_t (&wc)[4], uint32_t& mc,
+                    f32x4_t (&wn)[4], uint32_t& mn, uint4 (&xlr)[XU], uint4 (&xlc)[XU], uint4 (&xsr)[XU],
+                    uint4 (&xsc)[XU]) {
+    constexpr bool upd = decltype(updc)::value, fwd = decltype(fwdc)::value;
+    const int lane = td & 63, l32 = lane & 31, lh = lane >> 5, n = wave * 32 + l32;
+    const int buf = kb & 1;
+    const bool more = kb + 1 < nkb;
+    // block kb's W1 words (issued one block earlier) and everything older
+    asm volatile("s_waitcnt vmcnt(0)" : "+v"(wc[0]), "+v"(wc[1]), "+v"(wc[2]), "+v"(wc[3]), "+v"(mc) : : "memory");
+    load_x(updc, tu, fwdc, tf, kb + 2, td, xlr, xlc);
+    {
+      // (the last block re-reads itself: the load stays in bounds and its value is unused)
+      const int kn = more ? kb + 1 : kb;
+      const float* wp = W1 + ((size_t)kn * HP + n) * 32 + 4 * lh;
+      if constexpr (upd) {
+        const uint32_t* mp = m1 + (size_t)n * nkb + kn;
+        asm volatile(
+            "global_load_dwordx4 %0, %5, off\n\t"
+            "global_load_dwordx4 %1, %5, off offset:32\n\t"
+            "global_load_dwordx4 %2, %5, off offset:64\n\t"
+            "global_load_dwordx4 %3, %5, off offset:96\n\t"
+            "global_load_dword %4, %6, off"
+            : "=&v"(wn[0]), "=&v"(wn[1]), "=&v"(wn[2]), "=&v"(wn[3]), "=&v"(mn)
+            : "v"(wp), "v"(mp)
+            : "memory");
+      } else {
+        asm volatile(
+            "global_load_dwordx4 %0, %4, off\n\t"
+            "global_load_dwordx4 %1, %4, off offset:32\n\t"
+            "global_load_dwordx4 %2, %4, off offset:64\n\t"
+            "global_load_dwordx4 %3, %4, off offset:96"
+            : "=&v"(wn[0]), "=&v"(wn[1]), "=&v"(wn[2]), "=&v"(wn[3])
+            : "v"(wp)
+            : "memory");
+        mn = 0u;
+      }
+    }
+    const uint16_t* xcb = xc + buf * 32 * Ly::XC;
+    const uint16_t* xrb = xr + buf * BP * Ly::XR;
+    float wnew[16];
+    if constexpr (upd) {
+      f32x16_t dacc = zero16();
+#pragma unroll
+      for (int s = 0; s < NBS; ++s) {
+        const uint16_t* pp = xcb + l32 * Ly::XC + 16 * s + 4 * lh;
+        dacc = O::mma(ld2x8(pp, pp + 8), g1s[(wave * NBS + s) * 64 + lane], dacc);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int kl = 8 * (r >> 2) + 4 * lh + (r & 3);
+        const bool keep = (mc >> kl) & 1u;
+        wnew[r] = keep ? __fsub_rn(wc[r >> 2][r & 3], __fmul_rn(lrv, dacc[r])) : 0.0f;
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<float4*>(W1 + ((size_t)kb * HP + n) * 32 + 8 * q + 4 * lh) =
+            make_float4(wnew[4 * q], wnew[4 * q + 1], wnew[4 * q + 2], wnew[4 * q + 3]);
+    } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) wnew[r] = wc[r >> 2][r & 3];
+    }
+    if constexpr (fwd) {
+      uint4 wb[2];
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        uint16_t u[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) u[i] = O::from_f32(wnew[8 * s2 + i]);
+        wb[s2] = pack8(u);
+      }
+#pragma unroll
+      for (int T = 0; T < BT; ++T)
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) {
+          const uint16_t* pp = xrb + (32 * T + l32) * Ly::XR + 16 * s2 + 4 * lh;
+          zacc[T] = O::mma(ld2x8(pp, pp + 8), wb[s2], zacc[T]);
+        }
+    }
+    if (more) store_x(updc, fwdc, buf ^ 1, td, xsr, xsc);
+    __syncthreads();
+  };
+
+  // one pass over the input columns (head already issued): optional dW1 +
+  // update (step tu), optional forward accumulation of step tf into zacc
+  auto kloop = [&](auto updc, int tu, auto fwdc, int tf, int td) {
+    if constexpr (decltype(fwdc)::value) {
 #pragma unroll
       for (int T = 0; T < BT; ++T) zacc[T] = zero16();
     }
-    store_x(upd, fwd, 0, xr0, xc0);
+    __syncthreads();                           // the output-layer scratch shares the X buffers
+    store_x(updc, fwdc, 0, td, xAr, xAc);
     __syncthreads();
-    for (int kb = 0; kb < nkb; ++kb) {
-      const int buf = kb & 1;
-      const bool more = kb + 1 < nkb;
-      uint4 xr2[XU], xc2[XU];
-      load_x(upd, tu, fwd, tf, kb + 2, xr2, xc2);
-      float4 wc[4];
+    for (int kb = 0; kb < nkb; kb += 2) {
+      kblock(updc, tu, fwdc, tf, kb, td, wA, mA, wB, mB, xAr, xAc, xBr, xBc);
+      if (kb + 1 < nkb) kblock(updc, tu, fwdc, tf, kb + 1, td, wB, mB, wA, mA, xBr, xBc, xAr, xAc);
+    }
+    // the last block's (unused) prefetch must land before its registers are reused
+    asm volatile("s_waitcnt vmcnt(0)"
+                 : "+v"(wA[0]), "+v"(wA[1]), "+v"(wA[2]), "+v"(wA[3]), "+v"(mA), "+v"(wB[0]), "+v"(wB[1]),
+                   "+v"(wB[2]), "+v"(wB[3]), "+v"(mB)
+                 :
+                 : "memory");
+  };
+  const std::true_type on{};
+  const std::false_type off{};
+
+  // output layer, end of a step: b2 -= lr * sum of the db2 partials, and the
+  // per-row losses and hits added to the totals (fixed order)
+  auto finish_out = [&]() {
+    if (tid < 32) {
+      float db = 0.0f;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) wc[q] = wn[q];
-      const uint32_t mw = mwn;
-      if (more) {
+      for (int part = 0; part < Ly::NDP; ++part) db += dbp[part * 32 + tid];
+      b2s[tid] = __fsub_rn(b2s[tid], __fmul_rn(lrv, db));
+    }
+    if (wave == NW - 1) {
+      double sc = 0.0;
+      unsigned int co = 0;
+      for (int r = lane; r < BP; r += 64) { sc += rce[r]; co += rco[r]; }
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          wn[q] = *reinterpret_cast<const float4*>(W1 + ((size_t)(kb + 1) * HP + n) * 32 + 8 * q + 4 * lh);
-        mwn = upd ? m1[(size_t)n * kw1 + kb + 1] : 0u;
-      }
-      const uint16_t* xcb = xc + buf * 32 * Ly::XC;
-      const uint16_t* xrb = xr + buf * BP * Ly::XR;
-      float wnew[16];
-      if (upd) {
-        f32x16_t dacc = zero16();
-#pragma unroll
-        for (int s = 0; s < NBS; ++s) {
-          const uint16_t* pp = xcb + l32 * Ly::XC + 16 * s + 4 * lh;
-          dacc = O::mma(ld2x8(pp, pp + 8), g1p[s], dacc);
-        }
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int kl = 8 * (r >> 2) + 4 * lh + (r & 3);
-          const bool keep = (mw >> kl) & 1u;
-          wnew[r] = keep ? __fsub_rn(f4get(wc[r >> 2], r & 3), __fmul_rn(lrv, dacc[r])) : 0.0f;
-        }
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          *reinterpret_cast<float4*>(W1 + ((size_t)kb * HP + n) * 32 + 8 * q + 4 * lh) =
-              make_float4(wnew[4 * q], wnew[4 * q + 1], wnew[4 * q + 2], wnew[4 * q + 3]);
-      } else {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) wnew[r] = f4get(wc[r >> 2], r & 3);
-      }
-      if (fwd) {
-        F wb[2];
-#pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) {
-          const float* q = &wnew[8 * s2];
-          wb[s2] = make_uint4(pack2(O::from_f32(q[0]), O::from_f32(q[1])), pack2(O::from_f32(q[2]), O::from_f32(q[3])),
-                              pack2(O::from_f32(q[4]), O::from_f32(q[5])), pack2(O::from_f32(q[6]), O::from_f32(q[7])));
-        }
-#pragma unroll
-        for (int T = 0; T < BT; ++T)
-#pragma unroll
-          for (int s2 = 0; s2 < 2; ++s2) {
-            const uint16_t* pp = xrb + (32 * T + l32) * Ly::XR + 16 * s2 + 4 * lh;
-            zacc[T] = O::mma(ld2x8(pp, pp + 8), wb[s2], zacc[T]);
-          }
-      }
-      if (more) store_x(upd, fwd, buf ^ 1, xr1, xc1);
-#pragma unroll
-      for (int u = 0; u < XU; ++u) { xr1[u] = xr2[u]; xc1[u] = xc2[u]; }
-      __syncthreads();
+      for (int off = 32; off >= 1; off >>= 1) { sc += __shfl_xor(sc, off); co += __shfl_xor(co, off); }
+      if (lane == 0) { ce_tot += sc; corr_tot += co; }
     }
   };
 
   // prologue: forward of the first step
-  issue_head(false, 0, true, a.t0);
-  kloop(false, 0, true, a.t0);
+  issue_head(off, 0, on, a.t0, tid);
+  kloop(off, 0, on, a.t0, tid);
 
   for (int t = a.t0; t < a.t1; ++t) {
+    // Lane-dependent indices are recomputed each step from an opaque copy of
+    // the lane id: hoisted out of the loop they would occupy dozens of long-lived
+    // address registers and be spilled to scratch (each reload is a memory round trip).
+    int tid_step;
+    asm volatile("v_mov_b32 %0, %1" : "=v"(tid_step) : "v"(tid));
+    const int lane = tid_step & 63, l32 = lane & 31, lh = lane >> 5, n = wave * 32 + l32;
+    float* w2row = w2m + n * 32;
+    const int sw = n & 7;
     const int64_t r0 = (int64_t)t * a.B;
     const int bt = (int)((a.n - r0) < a.B ? (a.n - r0) : a.B);
     const float scale = __fdiv_rn(1.0f, (float)bt);
-    // ---- A1 = relu(Z1 + b1) -> LDS, ReLU' bits
+    // ---- the previous step's output-layer bias update and loss / hit totals
+    //      (its partial sums waited in LDS during the block loop)
+    if (t > a.t0) finish_out();
+    // ---- A1 = relu(Z1 + b1): rows -> LDS, bf16 operand pairs and ReLU' bits in registers
     uint32_t rb[BT];
+    uint4 a1p[NBS];
 #pragma unroll
     for (int T = 0; T < BT; ++T) {
       uint32_t bits = 0;
+      uint16_t u[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const float z = zacc[T][r] + b1v;
-        const uint16_t u = O::from_f32(z > 0.0f ? z : 0.0f);
-        a1[(32 * T + crow(r, lane)) * Ly::AS + n] = u;
-        bits |= (uint32_t)(u != 0) << r;
+        u[r] = O::from_f32(z > 0.0f ? z : 0.0f);
+        a1[(32 * T + crow(r, lane)) * Ly::AS + n] = u[r];
+        bits |= (uint32_t)(u[r] != 0) << r;
       }
       rb[T] = bits;
+      a1p[2 * T] = pack8(u);
+      a1p[2 * T + 1] = pack8(u + 8);
     }
+    if (tid < BP) yl[tid] = ylab;
     __syncthreads();
-    // ---- logits (MFMA, one batch tile per wave) -> LDS
+    // ---- logits^T (one batch tile per wave): lane = row b, registers = the
+    //      classes crow(r) of the lane's half; softmax cross-entropy, argmax
+    //      (lowest index on ties, a NaN logit is a miss), G2 = (p - onehot(y)) fl(1/b)
     if (wave < BT) {
       f32x16_t c0 = zero16(), c1 = zero16();
-      const uint16_t* ap = a1 + (32 * wave + l32) * Ly::AS + 8 * lh;
-      const uint16_t* bp = w2 + l32 * Ly::W2S + 8 * lh;
+      const uint16_t* ap = w2 + l32 * Ly::W2S + 8 * lh;
+      const uint16_t* bp = a1 + (32 * wave + l32) * Ly::AS + 8 * lh;
 #pragma unroll
       for (int s = 0; s < HP / 16; s += 2) {
         c0 = O::mma(O::load(ap + 16 * s), O::load(bp + 16 * s), c0);
         c1 = O::mma(O::load(ap + 16 * s + 16), O::load(bp + 16 * s + 16), c1);
       }
-      const float bias_c = b2s[l32];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) zb[(32 * wave + crow(r, lane)) * ZS + l32] = (c0[r] + c1[r]) + bias_c;
-    }
-    __syncthreads();
-    // ---- per row (one thread each): softmax cross-entropy, argmax (lowest index
-    //      on ties, a NaN logit is a miss), G2 = (p - onehot(y)) * fl(1/b)
-    if (tid < BP) {
-      const int b = tid, C = a.C, y = ylab;
-      float* zr = zb + b * ZS;
-      float m = zr[0], bv = zr[0];
-      int bi = 0, isn = zr[0] != zr[0];
-      for (int c = 1; c < C; ++c) {
-        const float z = zr[c];
-        if (z != z) isn = 1;
-        else if (z > bv) { bv = z; bi = c; }
-        m = fmaxf(m, z);
-      }
-      float s = 0.0f;
-      for (int c = 0; c < C; ++c) s += expf(zr[c] - m);
+      const int b = 32 * wave + l32, C = a.C, y = yl[b];
       const bool rvalid = y >= 0;
-      float ce = (logf(s) + m) - zr[rvalid ? y : 0];
-      if (isn) ce = NAN;
-      red_row_ce[b] = rvalid ? (double)ce : 0.0;
-      red_row_co[b] = (rvalid && !isn && bi == y) ? 1u : 0u;
-      for (int c = 0; c < 32; ++c) {
-        float g = 0.0f;
-        if (c < C && rvalid) g = (expf(zr[c] - m) / s - (c == y ? 1.0f : 0.0f)) * scale;
-        zr[c] = g;                                                // fp32 gradient for db2
-        g2[b * Ly::GS + c] = O::from_f32(g);
+      float z[16];
+      float ml = -INFINITY, bv = -INFINITY;
+      int bi = 64, nanl = 0;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {                 // r ascending = class ascending within the lane
+        const int c = crow(r, lane);
+        z[r] = (c0[r] + c1[r]) + b2s[c];
+        if (c < C) {
+          ml = fmaxf(ml, z[r]);
+          if (z[r] != z[r]) nanl = 1;
+          else if (z[r] > bv) { bv = z[r]; bi = c; }
+        }
       }
+      const float m = fmaxf(ml, __shfl_xor(ml, 32));
+      const int isn = nanl | __shfl_xor(nanl, 32);
+      {
+        const float ov = __shfl_xor(bv, 32);
+        const int oi = __shfl_xor(bi, 32);
+        if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+      }
+      float e[16], sl = 0.0f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        e[r] = crow(r, lane) < C ? expf(z[r] - m) : 0.0f;
+        sl += e[r];
+      }
+      const float s = sl + __shfl_xor(sl, 32);       // same value in both halves
+      uint16_t gq[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int c = crow(r, lane);
+        const float g = (c < C && rvalid) ? (e[r] / s - (c == y ? 1.0f : 0.0f)) * scale : 0.0f;
+        gq[r] = O::from_f32(g);
+        zg[c * Ly::ZGS + b] = g;
+        g2t[c * Ly::GTS + b] = gq[r];
+        if (c == y) {                                // the label's lane records the row
+          float ce = (logf(s) + m) - z[r];
+          if (isn) ce = NAN;
+          rce[b] = (double)ce;
+          rco[b] = (!isn && bi == y) ? 1u : 0u;
+        }
+      }
+      if (!rvalid && lh == 0) {
+        rce[b] = 0.0;
+        rco[b] = 0u;
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<uint2*>(g2 + b * Ly::GS + 8 * q + 4 * lh) =
+            make_uint2(pack2(gq[4 * q], gq[4 * q + 1]), pack2(gq[4 * q + 2], gq[4 * q + 3]));
     }
     __syncthreads();
-    // ---- reductions in a fixed order: db2 partials over row groups, loss and hits
+    // ---- db2 partial sums over row groups (fixed order); finished after the block loop
     {
-      const int c = tid & 31, part = tid >> 5;                    // NW*2 parts of rows
+      const int c = tid & 31, part = tid >> 5;       // Ly::NDP parts
       float sp = 0.0f;
-      for (int b = part; b < BP; b += 2 * NW) sp += zb[b * ZS + c];
-      dbpart[part * 32 + c] = sp;
+      for (int r = part; r < BP; r += Ly::NDP) sp += zg[c * Ly::ZGS + r];
+      dbp[part * 32 + c] = sp;
     }
-    if (wave == 0) {
-      double sc = 0.0;
-      unsigned int co = 0;
-      for (int b = lane; b < BP; b += 64) { sc += red_row_ce[b]; co += red_row_co[b]; }
+    // the next pass's first blocks, W1 words and labels can load from here on
+    // (the last step's pass also runs a forward, of a valid batch, whose result is unused)
+    const int tf = t + 1 < a.T ? t + 1 : t;
+    issue_head(on, t, on, tf, tid_step);
+    // ---- dW2 = G2^T A1 (classes x hidden), A1 from registers
+    f32x16_t d2 = zero16();
 #pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) { sc += __shfl_xor(sc, off); co += __shfl_xor(co, off); }
-      if (lane == 0) { ce_tot += sc; corr_tot += co; }
+    for (int s = 0; s < NBS; ++s) {
+      const uint16_t* pp = g2t + l32 * Ly::GTS + 16 * s + 4 * lh;
+      d2 = O::mma(ld2x8(pp, pp + 8), a1p[s], d2);
     }
-    __syncthreads();
-    if (tid < 32) {
-      float db = 0.0f;
+    // ---- G1 = (G2 W2) * ReLU' with the pre-update W2, taken from this lane's
+    //      own master values (accumulators reuse zacc)
+    float w2v[16];
 #pragma unroll
-      for (int part = 0; part < 2 * NW; ++part) db += dbpart[part * 32 + tid];
-      b2s[tid] = __fsub_rn(b2s[tid], __fmul_rn(lrv, db));      // read again only next step
+    for (int q = 0; q < 4; ++q) {
+      const float4 f = *reinterpret_cast<const float4*>(w2row + (((2 * q + lh) ^ sw) << 2));
+      w2v[4 * q] = f.x; w2v[4 * q + 1] = f.y; w2v[4 * q + 2] = f.z; w2v[4 * q + 3] = f.w;
     }
-    // ---- G1 = (G2 W2) * ReLU' with the pre-update W2 (accumulators reuse zacc)
+    uint4 w2b[2];
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+      uint16_t u[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) u[i] = O::from_f32(w2v[8 * s2 + i]);
+      w2b[s2] = pack8(u);
+    }
 #pragma unroll
     for (int T = 0; T < BT; ++T) {
       f32x16_t acc = zero16();
 #pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2)
-        acc = O::mma(O::load(g2 + (32 * T + l32) * Ly::GS + 16 * s2 + 8 * lh),
-                     O::load(w2t + n * Ly::W2T + 16 * s2 + 8 * lh), acc);
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const uint16_t* pp = g2 + (32 * T + l32) * Ly::GS + 16 * s2 + 4 * lh;
+        acc = O::mma(ld2x8(pp, pp + 8), w2b[s2], acc);
+      }
       zacc[T] = acc;
     }
+    // ---- G1 operand slots (the A1 rows are no longer read) and db1
     float db1p = 0.0f;
 #pragma unroll
     for (int T = 0; T < BT; ++T) {
@@ -356,42 +514,40 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
         u[r] = O::from_f32(((rb[T] >> r) & 1u) ? zacc[T][r] : 0.0f);
         db1p += O::to_f32(u[r]);
       }
-#pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2)
-        g1p[2 * T + s2] = make_uint4(pack2(u[8 * s2], u[8 * s2 + 1]), pack2(u[8 * s2 + 2], u[8 * s2 + 3]),
-                                     pack2(u[8 * s2 + 4], u[8 * s2 + 5]), pack2(u[8 * s2 + 6], u[8 * s2 + 7]));
+      g1s[(wave * NBS + 2 * T) * 64 + lane] = pack8(u);
+      g1s[(wave * NBS + 2 * T + 1) * 64 + lane] = pack8(u + 8);
     }
     db1p += __shfl_xor(db1p, 32);
     b1v = __fsub_rn(b1v, __fmul_rn(lrv, db1p));
-    // the next pass's first blocks, W1 words and labels can load from here on
-    const bool fwd_next = t + 1 < a.t1;
-    issue_head(true, t, fwd_next, t + 1);
-    // ---- dW2 = G2^T A1 (classes x hidden), reads of LDS only
-    f32x16_t d2 = zero16();
+    // ---- masked SGD on W2 (LDS master) and refresh of its bf16 operand
 #pragma unroll
-    for (int s = 0; s < NBS; ++s)
-      d2 = O::mma(O::gather(g2 + (16 * s + 8 * lh) * Ly::GS + l32, Ly::GS),
-                  O::gather(a1 + (16 * s + 8 * lh) * Ly::AS + n, Ly::AS), d2);
-    __syncthreads();
-    // ---- masked SGD on W2 (register master) and refresh of its LDS operands
+    for (int q = 0; q < 4; ++q) {
+      float f[4];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int c = crow(r, lane);
-      const bool keep = (m2s[c * (HP / 32) + (n >> 5)] >> (n & 31)) & 1u;
-      w2r[r] = keep ? __fsub_rn(w2r[r], __fmul_rn(lrv, d2[r])) : 0.0f;
-      const uint16_t u = O::from_f32(w2r[r]);
-      w2[c * Ly::W2S + n] = u;
-      w2t[n * Ly::W2T + c] = u;
+      for (int i = 0; i < 4; ++i) {
+        const int r = 4 * q + i, c = crow(r, lane);
+        f[i] = ((m2bits >> r) & 1u) ? __fsub_rn(w2v[r], __fmul_rn(lrv, d2[r])) : 0.0f;
+        w2[c * Ly::W2S + n] = O::from_f32(f[i]);
+      }
+      *reinterpret_cast<float4*>(w2row + (((2 * q + lh) ^ sw) << 2)) = make_float4(f[0], f[1], f[2], f[3]);
     }
     // ---- dW1 + masked SGD on W1 + forward of the next step
-    kloop(true, t, fwd_next, t + 1);
+    int tid_pass;
+    asm volatile("v_mov_b32 %0, %1" : "=v"(tid_pass) : "v"(tid));
+    kloop(on, t, on, tf, tid_pass);
   }
+  __syncthreads();                             // the last step's partial sums
+  finish_out();
   // ---- write back the resident state
 #pragma unroll
-  for (int r = 0; r < 16; ++r) W2[((size_t)wave * 32 + crow(r, lane)) * 32 + l32] = w2r[r];
+  for (int q = 0; q < 4; ++q) {
+    const float4 f = *reinterpret_cast<const float4*>(w2row + (((2 * q + lh) ^ sw) << 2));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) W2[((size_t)wave * 32 + crow(4 * q + i, lane)) * 32 + l32] = f4get(f, i);
+  }
   if (lh == 0) a.b1[(size_t)v * HP + n] = b1v;
   if (tid < 32) a.b2[(size_t)v * 32 + tid] = b2s[tid];
-  if (tid == 0) {
+  if (tid == tot_tid) {
     a.ce_acc[v] = ce_tot;
     a.correct_acc[v] = corr_tot;
   }

@@ -1,0 +1,61 @@
+"""The build-time check of the fused kernel's explicit prefetches (register
+discipline between an inline-assembly load and its explicit wait)."""
+import pytest
+
+from paper_2310_10211_amd import check_prefetch
+
+HEAD = "_ZN4gevo8k_fused2ILi256ELi128EEEvNS_10Fused2ArgsE:\n"
+TAIL = ".Lfunc_end0:\n"
+
+
+def _fn(body: str) -> str:
+    return HEAD + body + TAIL
+
+
+CLEAN = _fn("""\
+.LBB0_1:
+\t;;#ASMSTART
+\ts_waitcnt vmcnt(0)
+\t;;#ASMEND
+\tv_add_f32_e32 v20, v8, v9
+\t;;#ASMSTART
+\tglobal_load_dwordx4 v[8:11], v[2:3], off
+\t;;#ASMEND
+\tv_mul_f32_e32 v21, v12, v13
+\ts_cbranch_scc1 .LBB0_1
+\ts_endpgm
+""")
+
+
+def test_clean_function_passes():
+    assert check_prefetch.check_assembly(CLEAN) == {HEAD[:-2]: 1}
+
+
+def test_use_before_wait_on_fallthrough_is_caught():
+    bad = CLEAN.replace("\ts_endpgm\n", "\tv_mov_b32_e32 v30, v9\n\ts_endpgm\n")
+    with pytest.raises(RuntimeError, match="used before its wait"):
+        check_prefetch.check_assembly(bad)
+
+
+def test_use_through_a_branch_target_is_caught():
+    bad = _fn("""\
+\t;;#ASMSTART
+\tglobal_load_dwordx4 v[8:11], v[2:3], off
+\t;;#ASMEND
+\ts_cbranch_execz .LBB0_3
+\tv_mov_b32_e32 v1, 0
+\t;;#ASMSTART
+\ts_waitcnt vmcnt(0)
+\t;;#ASMEND
+\ts_endpgm
+.LBB0_3:
+\tv_mov_b32_e32 v10, 0
+\ts_endpgm
+""")
+    with pytest.raises(RuntimeError, match="used before its wait"):
+        check_prefetch.check_assembly(bad)
+
+
+def test_missing_prefetch_is_reported():
+    with pytest.raises(RuntimeError, match="no prefetch blocks"):
+        check_prefetch.check_assembly(_fn("\ts_endpgm\n"))
