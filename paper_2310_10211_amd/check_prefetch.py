@@ -1,19 +1,25 @@
 """Build-time check of the register discipline of the fused training kernel.
 
 The kernel issues its fp32 master prefetches as explicit load instructions
-(inline assembly) and waits for them with one explicit ``s_waitcnt vmcnt``
-placed where the loaded values are first needed.  The compiler does not track
-such loads, so the generated code is only correct if no instruction reads or
-writes a destination register of a prefetch on any path between the load and
-the next explicit wait.  This module verifies that property on the kernel's
-gfx950 assembly, following the control-flow graph (branches and fall-through),
-and raises if any path violates it.
+(inline assembly) and waits for them with explicit ``s_waitcnt vmcnt(N)``
+instructions placed where the loaded values are first needed.  The compiler
+does not track such loads, so the generated code is only correct if, on every
+path from a prefetch, no instruction reads or writes one of its destination
+registers before a wait that covers the prefetch.  Vector memory operations
+complete in issue order, so ``s_waitcnt vmcnt(N)`` covers a load once at least
+N further vector memory operations have been issued after it on that path.
+This module verifies the property on the kernel's gfx950 assembly, following
+the control-flow graph (branches and fall-through) and counting the vector
+memory operations along each path, and raises if any path violates it.
 """
 from __future__ import annotations
 
 import re
 
 _REG = re.compile(r"\bv\[(\d+):(\d+)\]|\bv(\d+)\b")
+_VMEM = re.compile(r"^(global|buffer|scratch|flat)_(load|store|atomic)")
+_WAIT = re.compile(r"s_waitcnt\b.*\bvmcnt\((\d+)\)")
+_CAP = 64
 
 
 def _regs(text: str) -> set:
@@ -26,8 +32,9 @@ def _regs(text: str) -> set:
     return out
 
 
-def _is_wait(lines, k) -> bool:
-    return lines[k].strip() == ";;#ASMSTART" and k + 1 < len(lines) and "s_waitcnt vmcnt" in lines[k + 1]
+def _instruction(line: str) -> str:
+    t = line.strip()
+    return "" if (not t or t.startswith(";") or t.startswith(".")) else t
 
 
 def check_function(lines: list) -> tuple:
@@ -61,20 +68,24 @@ def check_function(lines: list) -> tuple:
                     dst |= _regs(m.group(1))
                 j += 1
             blocks += 1
-            seen, stack = set(), [j + 1]
+            # state: (line, vector memory operations issued after the prefetch, capped)
+            seen, stack = set(), [(j + 1, 0)]
             while stack:
-                k = stack.pop()
-                if k in seen or k >= len(lines):
+                k, younger = stack.pop()
+                if (k, younger) in seen or k >= len(lines):
                     continue
-                seen.add(k)
-                if _is_wait(lines, k):
-                    continue                       # this path reaches the explicit wait
-                t = lines[k].strip()
-                if t and not t.startswith(";") and not t.startswith("."):
-                    if _regs(t) & dst:
+                seen.add((k, younger))
+                t = _instruction(lines[k])
+                if t:
+                    w = _WAIT.search(t)
+                    if w and younger >= int(w.group(1)):
+                        continue                   # this path waits for the prefetch here
+                    if _VMEM.match(t):
+                        younger = min(younger + 1, _CAP)
+                    if _regs(t) & dst and not w:
                         bad.append((i, k, t))
                         continue
-                stack.extend(successors(k))
+                stack.extend((n, younger) for n in successors(k))
             i = j
         i += 1
     return blocks, bad

@@ -59,3 +59,24 @@ def test_use_through_a_branch_target_is_caught():
 def test_missing_prefetch_is_reported():
     with pytest.raises(RuntimeError, match="no prefetch blocks"):
         check_prefetch.check_assembly(_fn("\ts_endpgm\n"))
+
+
+def test_partial_wait_needs_enough_younger_memory_operations():
+    # vmcnt(2) right after the prefetch leaves it in flight: the later use is a violation
+    early = _fn("""\
+\t;;#ASMSTART
+\tglobal_load_dwordx4 v[8:11], v[2:3], off
+\t;;#ASMEND
+\t;;#ASMSTART
+\ts_waitcnt vmcnt(2)
+\t;;#ASMEND
+\tv_mov_b32_e32 v1, v8
+\ts_endpgm
+""")
+    with pytest.raises(RuntimeError, match="used before its wait"):
+        check_prefetch.check_assembly(early)
+    # two younger stores make vmcnt(2) cover the prefetch
+    ok = early.replace("\t;;#ASMSTART\n\ts_waitcnt vmcnt(2)",
+                       "\tglobal_store_dword v[4:5], v1, off\n\tglobal_store_dword v[4:5], v1, off offset:4\n"
+                       "\t;;#ASMSTART\n\ts_waitcnt vmcnt(2)")
+    assert check_prefetch.check_assembly(ok) == {HEAD[:-2]: 1}
