@@ -175,6 +175,31 @@ def test_bf16_two_layer_ragged_batch():
     pop.close()
 
 
+@pytest.mark.parametrize("dims,batch,n_train", [
+    ([784, 128, 10], 32, 700),      # hidden 128, batch tile 32, ragged tail
+    ([784, 100, 10], 64, 650),      # hidden 100 (padded to 128), batch tile 64
+    ([784, 128, 10], 128, 600),     # hidden 128, batch tile 128
+    ([784, 256, 10], 50, 620),      # hidden 256, batch 50 (tile 64)
+    ([300, 250, 7], 20, 500),       # input 300 (10 column blocks), hidden 250, 7 classes, tile 32
+])
+def test_bf16_two_layer_shapes(dims, batch, n_train):
+    """Two-layer bf16 nets at the other hidden widths and batch tiles of the per-variant training kernel."""
+    cfg, data = _small(3, P=3, n_train=n_train, n_test=300, dims=dims, batch=batch)
+    if dims[0] != 784:
+        data["x_train"] = data["x_train"][:, :dims[0]].copy()
+        data["x_test"] = data["x_test"][:, :dims[0]].copy()
+    if dims[-1] != 10:
+        data["y_train"] = data["y_train"] % dims[-1]
+        data["y_test"] = data["y_test"] % dims[-1]
+    pop = _pop(cfg, data)
+    pop.train_epoch(0)
+    pop.predict()
+    s = pop.scores()
+    ref = oracle.evaluate(cfg, data, epochs=1)
+    _check_losses(s, ref, range(3), BF16_LOSS_RTOL)
+    pop.close()
+
+
 def test_bf16_three_layer():
     """Three weight layers (config 5 structure) at reduced width, batch 256 with a ragged tail."""
     cfg, data = _small(5, P=4, n_train=1300, n_test=600, dims=[3072, 160, 96, 10])
