@@ -35,6 +35,7 @@ struct Layout {
   LayerLay lay[GEVO_MAX_LAYERS];
   size_t lr = 0, thresh = 0, train_ce = 0, train_corr = 0, test_ce = 0, test_corr = 0, part_ce = 0,
          part_corr = 0, xrows = 0, xcols = 0, yep = 0, xte = 0, yte = 0, perm = 0;
+  size_t w1img = 0, m1blk = 0;                    // fused training: W1 register image, block-major W1 mask
   size_t total = 0;
 };
 
@@ -138,6 +139,11 @@ gevo_status make_layout(const gevo_pop_config* c, Layout* o) {
   y.xte = take((size_t)y.n_test_pad * Kp1 * e);
   y.yte = take((size_t)y.n_test_pad * 4);
   y.perm = take((size_t)(y.n_train > 0 ? y.n_train : 1) * 4);
+  if (y.fused) {
+    const size_t Np1 = (size_t)y.lay[0].Np;
+    y.w1img = take(P * Np1 * Kp1 * 4);
+    y.m1blk = take(P * Np1 * (Kp1 / 32) * 4);
+  }
   y.total = off;
   return GEVO_OK;
 }
@@ -204,6 +210,9 @@ struct gevo_pop {
   bool timing_pending = false;
   double last_s = 0.0;
   bool predicted = false;
+  // fused training keeps W1 in its own register image: which copy is current
+  bool img_valid = false;   // the image (and the block-major mask) match the k-blocked master
+  bool blk_stale = false;   // training has advanced the image past the k-blocked master
   // kernel-level timing (gevo_pop_set_profiling)
   bool prof_on = false;
   struct ProfRec { int kind; hipEvent_t a, b; };
@@ -407,6 +416,31 @@ gevo_status train_step(gevo_pop* p, int t) {
   return GEVO_OK;
 }
 
+// The fused training kernel streams W1 in its register image with block-major
+// masks; every other consumer reads the k-blocked master.  These bring the
+// copy that is about to be read up to date.
+gevo_status fused_to_image(gevo_pop* p) {
+  const Layout& y = p->y;
+  if (!y.fused || p->img_valid) return GEVO_OK;
+  const LayerLay& q = y.lay[0];
+  HIP_TRY(launch_w1_image(at<float>(p, q.Wm), at<float>(p, y.w1img), y.P, q.Kp, q.Np, true, p->stream,
+                          prof(p, GEVO_KERNEL_AUX)));
+  HIP_TRY(launch_mask_block_major(at<uint32_t>(p, q.mask), at<uint32_t>(p, y.m1blk), y.P, q.Kp, q.Np, p->stream,
+                                  prof(p, GEVO_KERNEL_AUX)));
+  p->img_valid = true;
+  return GEVO_OK;
+}
+
+gevo_status fused_to_blocked(gevo_pop* p) {
+  const Layout& y = p->y;
+  if (!y.fused || !p->blk_stale) return GEVO_OK;
+  const LayerLay& q = y.lay[0];
+  HIP_TRY(launch_w1_image(at<float>(p, y.w1img), at<float>(p, q.Wm), y.P, q.Kp, q.Np, false, p->stream,
+                          prof(p, GEVO_KERNEL_AUX)));
+  p->blk_stale = false;
+  return GEVO_OK;
+}
+
 template <typename S>
 gevo_status do_train_steps(gevo_pop* p, uint32_t epoch, uint32_t s0, uint32_t s1) {
   const Layout& y = p->y;
@@ -434,13 +468,16 @@ gevo_status do_train_steps(gevo_pop* p, uint32_t epoch, uint32_t s0, uint32_t s1
     f.Kp = q1.Kp; f.Hp = q1.Np; f.C = q2.N; f.B = y.B; f.Bp = y.Bp; f.T = y.T;
     f.n = y.n_train; f.t0 = (int)s0; f.t1 = (int)s1;
     f.xrows = at<uint16_t>(p, y.xrows); f.xcols = at<uint16_t>(p, y.xcols); f.labels = at<int32_t>(p, y.yep);
-    f.W1 = at<float>(p, q1.Wm); f.b1 = at<float>(p, q1.bias); f.m1 = at<uint32_t>(p, q1.mask);
+    gevo_status sti = fused_to_image(p);
+    if (sti != GEVO_OK) return sti;
+    f.W1 = at<float>(p, y.w1img); f.b1 = at<float>(p, q1.bias); f.m1 = at<uint32_t>(p, y.m1blk);
     f.W2 = at<float>(p, q2.Wm); f.b2 = at<float>(p, q2.bias); f.m2 = at<uint32_t>(p, q2.mask);
     f.lr = at<float>(p, y.lr);
     f.ce_acc = at<double>(p, y.train_ce);
     f.correct_acc = at<unsigned long long>(p, y.train_corr);
     if (q2.Kp != q1.Np || q1.Kp % kTile || fused2_lds_bytes(f.Hp, f.Bp) == 0) return GEVO_E_SHAPE;
     HIP_TRY(launch_fused2(f, y.P, p->stream, prof(p, GEVO_KERNEL_FUSED_TRAIN)));
+    p->blk_stale = true;
     for (uint32_t t = s0; t < s1; ++t) {
       const int64_t r0 = (int64_t)t * y.B;
       p->rows_done += (y.n_train - r0) < y.B ? (y.n_train - r0) : y.B;
@@ -465,6 +502,8 @@ template <typename S>
 gevo_status do_predict(gevo_pop* p) {
   const Layout& y = p->y;
   HIP_TRY(hipEventRecord(p->ev0, p->stream));
+  gevo_status stb = fused_to_blocked(p);
+  if (stb != GEVO_OK) return stb;
   const size_t Kp1 = (size_t)y.lay[0].Kp;
   for (int c0 = 0; c0 < y.n_test_pad; c0 += kPredictChunk) {
     const int R = (y.n_test_pad - c0) < kPredictChunk ? (y.n_test_pad - c0) : kPredictChunk;
@@ -699,6 +738,8 @@ gevo_status gevo_pop_export(gevo_pop* p, uint32_t v, float* params_out, uint8_t*
   if (!p) return GEVO_E_ARG;
   const Layout& y = p->y;
   if (v >= (uint32_t)y.P) return GEVO_E_ARG;
+  gevo_status stb = fused_to_blocked(p);
+  if (stb != GEVO_OK) return stb;
   HIP_TRY(hipStreamSynchronize(p->stream));
   size_t off = 0, moff = 0;
   for (int l = 0; l < y.L; ++l) {
@@ -730,7 +771,10 @@ gevo_status gevo_pop_import(gevo_pop* p, uint32_t v, const float* params) {
   const Layout& y = p->y;
   if (v >= (uint32_t)y.P) return GEVO_E_ARG;
   if (p->open_epoch >= 0) return GEVO_E_ORDER;        // only between epochs
+  gevo_status stb = fused_to_blocked(p);
+  if (stb != GEVO_OK) return stb;
   HIP_TRY(hipStreamSynchronize(p->stream));
+  p->img_valid = false;                               // the image is rebuilt from the imported master
   size_t off = 0;
   for (int l = 0; l < y.L; ++l) {
     const LayerLay& q = y.lay[l];

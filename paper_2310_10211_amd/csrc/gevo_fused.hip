@@ -27,6 +27,10 @@
 // feed G1, and how the updated W1 (accumulators over k) feeds the forward pass
 // without leaving registers.
 //
+// W1 is kept in a register image: in block kb, wave w's q-th 16-byte load of
+// every lane reads one contiguous KiB (lane l32 + 32 lh holds inputs
+// 8q + 4lh + 0..3 of unit 32w + l32), and the mask words are block-major, so
+// every W1 load and store instruction covers whole cache lines.
 // The W1 stream is software-pipelined one block ahead and the shared X blocks
 // two blocks ahead; the block loop is unrolled by two with alternating
 // register sets.  The W1 block loads are issued after the block's X loads as
@@ -222,8 +226,9 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
     load_x(updc, tu, fwdc, tf, 0, td, xAr, xAc);
     load_x(updc, tu, fwdc, tf, 1, td, xBr, xBc);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) wA[q] = *reinterpret_cast<const f32x4_t*>(W1 + (size_t)n * 32 + 8 * q + 4 * lh);
-    mA = upd ? m1[(size_t)n * nkb] : 0u;
+    for (int q = 0; q < 4; ++q)
+      wA[q] = *reinterpret_cast<const f32x4_t*>(W1 + (size_t)wave * 1024 + q * 256 + (td & 63) * 4);
+    mA = upd ? m1[n] : 0u;
     if (fwd && td < BP) ylab = a.labels[(size_t)tf * BP + td];
   };
 
@@ -243,14 +248,14 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
     {
       // (the last block re-reads itself: the load stays in bounds and its value is unused)
       const int kn = more ? kb + 1 : kb;
-      const float* wp = W1 + ((size_t)kn * HP + n) * 32 + 4 * lh;
+      const float* wp = W1 + ((size_t)kn * NW + wave) * 1024 + lane * 4;
       if constexpr (upd) {
-        const uint32_t* mp = m1 + (size_t)n * nkb + kn;
+        const uint32_t* mp = m1 + (size_t)kn * HP + n;
         asm volatile(
             "global_load_dwordx4 %0, %5, off\n\t"
-            "global_load_dwordx4 %1, %5, off offset:32\n\t"
-            "global_load_dwordx4 %2, %5, off offset:64\n\t"
-            "global_load_dwordx4 %3, %5, off offset:96\n\t"
+            "global_load_dwordx4 %1, %5, off offset:1024\n\t"
+            "global_load_dwordx4 %2, %5, off offset:2048\n\t"
+            "global_load_dwordx4 %3, %5, off offset:3072\n\t"
             "global_load_dword %4, %6, off"
             : "=&v"(wn[0]), "=&v"(wn[1]), "=&v"(wn[2]), "=&v"(wn[3]), "=&v"(mn)
             : "v"(wp), "v"(mp)
@@ -258,9 +263,9 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
       } else {
         asm volatile(
             "global_load_dwordx4 %0, %4, off\n\t"
-            "global_load_dwordx4 %1, %4, off offset:32\n\t"
-            "global_load_dwordx4 %2, %4, off offset:64\n\t"
-            "global_load_dwordx4 %3, %4, off offset:96"
+            "global_load_dwordx4 %1, %4, off offset:1024\n\t"
+            "global_load_dwordx4 %2, %4, off offset:2048\n\t"
+            "global_load_dwordx4 %3, %4, off offset:3072"
             : "=&v"(wn[0]), "=&v"(wn[1]), "=&v"(wn[2]), "=&v"(wn[3])
             : "v"(wp)
             : "memory");
@@ -285,7 +290,7 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
       }
 #pragma unroll
       for (int q = 0; q < 4; ++q)
-        *reinterpret_cast<float4*>(W1 + ((size_t)kb * HP + n) * 32 + 8 * q + 4 * lh) =
+        *reinterpret_cast<float4*>(W1 + (((size_t)kb * NW + wave) * 4 + q) * 256 + lane * 4) =
             make_float4(wnew[4 * q], wnew[4 * q + 1], wnew[4 * q + 2], wnew[4 * q + 3]);
     } else {
 #pragma unroll

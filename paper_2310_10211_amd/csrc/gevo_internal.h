@@ -104,7 +104,7 @@ struct Fused2Args {
   const uint16_t* xrows;         // [T][Bp][Kp] bf16 bits
   const uint16_t* xcols;         // [T][Kp][Bp]
   const int32_t* labels;         // [T][Bp]
-  float* W1; float* b1; const uint32_t* m1;   // [P][Kp/32][Hp][32], [P][Hp], [P][Hp][Kp/32]
+  float* W1; float* b1; const uint32_t* m1;   // register image (see launch_w1_image), [P][Hp], [P][Kp/32][Hp]
   float* W2; float* b2; const uint32_t* m2;   // [P][Hp/32][32][32], [P][32], [P][32][Hp/32]
   const float* lr;
   double* ce_acc;
@@ -142,6 +142,12 @@ template <typename S> hipError_t launch_gather(const GatherArgs& a, hipStream_t 
 template <typename S> hipError_t launch_transpose(const TransposeArgs& a, hipStream_t s, const LaunchEv& ev);
 hipError_t launch_zero_bytes(void* p, size_t bytes, hipStream_t s, const LaunchEv& ev);
 hipError_t launch_fused2(const Fused2Args& a, int P, hipStream_t s, const LaunchEv& ev);
+// W1 master of a two-layer net: k-blocked layout <-> the fused kernel's register image
+hipError_t launch_w1_image(const float* src, float* dst, int P, int Kp, int Hp, bool to_image, hipStream_t s,
+                           const LaunchEv& ev);
+// W1 mask row words [P][Hp][Kp/32] -> block-major words [P][Kp/32][Hp]
+hipError_t launch_mask_block_major(const uint32_t* src, uint32_t* dst, int P, int Kp, int Hp, hipStream_t s,
+                                   const LaunchEv& ev);
 size_t fused2_lds_bytes(int hp, int bp);     // 0 when the shape has no fused instantiation
 hipError_t launch_reduce_partials(const double* part_ce, const unsigned int* part_corr, int P, int n_chunks,
                                   double* ce_out, unsigned long long* corr_out, hipStream_t s, const LaunchEv& ev);

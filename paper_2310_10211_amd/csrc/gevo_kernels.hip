@@ -624,6 +624,41 @@ __global__ __launch_bounds__(256) void k_transpose(TransposeArgs a) {
   for (int i = 0; i < 4; ++i) dst[(size_t)(k0 + ty + 8 * i) * a.Bp + b0 + tx] = tile[tx][ty + 8 * i];
 }
 
+// W1 master of a two-layer net between the k-blocked layout [P][Kp/32][Hp][32]
+// and the register image the fused training kernel streams: in block kb, wave
+// w (hidden units 32w..32w+31) reads 4 KiB as [q][lane][4], where lane
+// l32 + 32 lh holds inputs 8q + 4lh + 0..3 of unit 32w + l32.  One thread
+// moves one 16-byte group; to_image = 1 converts blocked -> image.
+__global__ __launch_bounds__(256) void k_w1_image(const float* __restrict__ src, float* __restrict__ dst,
+                                                  int64_t groups, int Hp, int to_image) {
+  for (int64_t gi = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; gi < groups;
+       gi += (int64_t)gridDim.x * blockDim.x) {
+    // gi enumerates the image: ((((v * nkb + kb) * NW + w) * 4 + q) * 64 + lane)
+    const int lane = (int)(gi & 63), q = (int)((gi >> 6) & 3);
+    const int64_t blk = gi >> 8;                     // (v * nkb + kb) * NW + w
+    const int NW = Hp / 32, w = (int)(blk % NW);
+    const int64_t vkb = blk / NW;                    // v * nkb + kb
+    const int n = 32 * w + (lane & 31), kl = 8 * q + 4 * (lane >> 5);
+    const int64_t img = gi * 4, kblk = (vkb * Hp + n) * 32 + kl;
+    const float4 val = *reinterpret_cast<const float4*>(src + (to_image ? kblk : img));
+    *reinterpret_cast<float4*>(dst + (to_image ? img : kblk)) = val;
+  }
+}
+
+// W1 mask words of a two-layer net from row words [P][Hp][Kp/32] to
+// block-major words [P][Kp/32][Hp] (the fused kernel's per-block read is contiguous).
+__global__ __launch_bounds__(256) void k_mask_block_major(const uint32_t* __restrict__ src,
+                                                          uint32_t* __restrict__ dst, int64_t words, int Hp,
+                                                          int nkb) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < words;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int n = (int)(i % Hp);
+    const int64_t vkb = i / Hp;                      // v * nkb + kb
+    const int64_t v = vkb / nkb, kb = vkb % nkb;
+    dst[i] = src[(v * Hp + n) * nkb + kb];
+  }
+}
+
 __global__ __launch_bounds__(256) void k_zero(uint32_t* p, size_t words) {
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < words; i += (size_t)gridDim.x * blockDim.x)
     p[i] = 0u;
@@ -748,6 +783,22 @@ hipError_t launch_zero_bytes(void* p, size_t bytes, hipStream_t s, const LaunchE
   if (words == 0) return hipSuccess;
   hipExtLaunchKernelGGL(k_zero, dim3(grid_for((int64_t)words, 256, 4096)), dim3(256), 0, s, ev.start, ev.stop, 0,
                         (uint32_t*)p, words);
+  return hipGetLastError();
+}
+
+hipError_t launch_w1_image(const float* src, float* dst, int P, int Kp, int Hp, bool to_image, hipStream_t s,
+                           const LaunchEv& ev) {
+  const int64_t groups = (int64_t)P * Kp * Hp / 4;
+  hipExtLaunchKernelGGL(k_w1_image, dim3(grid_for(groups, 256, 16384)), dim3(256), 0, s, ev.start, ev.stop, 0, src,
+                        dst, groups, Hp, to_image ? 1 : 0);
+  return hipGetLastError();
+}
+
+hipError_t launch_mask_block_major(const uint32_t* src, uint32_t* dst, int P, int Kp, int Hp, hipStream_t s,
+                                   const LaunchEv& ev) {
+  const int64_t words = (int64_t)P * Hp * (Kp / 32);
+  hipExtLaunchKernelGGL(k_mask_block_major, dim3(grid_for(words, 256, 16384)), dim3(256), 0, s, ev.start, ev.stop,
+                        0, src, dst, words, Hp, Kp / 32);
   return hipGetLastError();
 }
 

@@ -200,6 +200,51 @@ def test_bf16_two_layer_shapes(dims, batch, n_train):
     pop.close()
 
 
+def test_export_import_round_trip_between_epochs_is_exact():
+    """Exporting and re-importing every variant between epochs (the per-variant
+    training kernel's own copy of the hidden layer is rebuilt from the imported
+    master) leaves the run bitwise unchanged."""
+    cfg, data = _small(3, P=3, n_train=700, n_test=256, epochs=2)
+    runs = []
+    for round_trip in (False, True):
+        pop = _pop(cfg, data)
+        pop.train_epoch(0)
+        if round_trip:
+            for v in range(cfg["P"]):
+                pop.import_params(v, pop.export(v)["params"])
+        pop.train_epoch(1)
+        runs.append([pop.export(v)["params"].tobytes() for v in range(cfg["P"])])
+        pop.close()
+    assert runs[0] == runs[1]
+
+
+def test_bf16_one_step_after_import_matches_oracle():
+    """An imported state trains from that state: one bf16 SGD step of the
+    784-256-10 net against the oracle from the same state."""
+    cfg, data = _small(3, P=2, n_train=256, n_test=256)
+    dims = cfg["dims"]
+    pop = _pop(cfg, data)
+    ref = oracle.population(cfg)
+    rng = np.random.default_rng(5)
+    perm = oracle.permutation(cfg["seed"], 0, 256)
+    for v in range(cfg["P"]):
+        st = ref[v]
+        p = st["params"] + 0.01 * rng.standard_normal(st["params"].shape)
+        pop.import_params(v, p.astype(np.float32))             # masked weights are imported as +0
+        st["params"] = pop.export(v)["params"].astype(np.float64)
+    pop.train_steps(0, 0, 1)
+    for v in range(cfg["P"]):
+        st = ref[v]
+        q = st["params"].copy()
+        oracle.train_steps("bf16", dims, q, st["mask"], st["lr"], data["x_train"], data["y_train"], perm,
+                           cfg["batch"], 0, 1)
+        got = pop.export(v)["params"].astype(np.float64)
+        for (Wg, bg), (Wr, br) in zip(oracle.unpack(got, dims), oracle.unpack(q, dims)):
+            assert np.max(np.abs(Wg - Wr)) <= 1e-4 * max(np.max(np.abs(Wr)), 1e-30)
+            assert np.max(np.abs(bg - br)) <= 1e-4 * max(np.max(np.abs(br)), 1e-3)
+    pop.close()
+
+
 def test_bf16_three_layer():
     """Three weight layers (config 5 structure) at reduced width, batch 256 with a ragged tail."""
     cfg, data = _small(5, P=4, n_train=1300, n_test=600, dims=[3072, 160, 96, 10])
