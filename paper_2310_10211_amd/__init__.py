@@ -19,7 +19,8 @@ import os
 
 import numpy as np
 
-__all__ = ["Population", "lib", "epoch_permutation", "GevoError", "config_struct", "workspace_bytes"]
+__all__ = ["Population", "lib", "epoch_permutation", "check_bf16_rounding", "GevoError", "config_struct",
+           "workspace_bytes"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgevo.so")
@@ -34,6 +35,7 @@ EXPORTED = [
     "gevo_pop_steps_per_epoch", "gevo_pop_predict", "gevo_pop_scores", "gevo_pop_last_time",
     "gevo_pop_export", "gevo_pop_import", "gevo_pop_epoch_labels", "gevo_epoch_permutation",
     "gevo_pop_set_profiling", "gevo_pop_kernel_stats", "gevo_pop_destroy", "gevo_status_str",
+    "gevo_check_bf16_rounding",
 ]
 KERNEL_KINDS = ["init", "gather", "layer_train", "layer_fwd", "out_train", "out_predict", "bwd", "aux",
                 "fused_train"]
@@ -94,6 +96,7 @@ def lib():
         L.gevo_pop_set_profiling.argtypes = [vp, ctypes.c_int]
         L.gevo_pop_kernel_stats.argtypes = [vp, ctypes.c_int, ctypes.POINTER(ctypes.c_double),
                                             ctypes.POINTER(ctypes.c_uint64)]
+        L.gevo_check_bf16_rounding.argtypes = [vp, vp]
         L.gevo_pop_destroy.argtypes = [vp]
         L.gevo_pop_destroy.restype = None
         L.gevo_status_str.argtypes = [ctypes.c_int]
@@ -159,6 +162,16 @@ def epoch_permutation(seed: int, epoch: int, n: int) -> np.ndarray:
     _check(lib().gevo_epoch_permutation(seed, epoch, n, out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32))),
            "gevo_epoch_permutation")
     return out
+
+
+def check_bf16_rounding(stream=None) -> list:
+    """Counts of the exhaustive bf16 rounding check (see gevo_check_bf16_rounding)."""
+    import torch
+    counts = torch.zeros(3, dtype=torch.int64, device="cuda")
+    st = stream if stream is not None else torch.cuda.current_stream()
+    _check(lib().gevo_check_bf16_rounding(ctypes.c_void_p(st.cuda_stream), ctypes.c_void_p(counts.data_ptr())),
+           "gevo_check_bf16_rounding")
+    return [int(c) for c in counts.cpu()]
 
 
 def param_count(dims) -> int:

@@ -568,6 +568,15 @@ gevo_status gevo_epoch_permutation(uint64_t seed, uint32_t epoch, uint32_t n, ui
   return GEVO_OK;
 }
 
+gevo_status gevo_check_bf16_rounding(void* hip_stream, uint64_t* d_counts) {
+  if (!d_counts || ((uintptr_t)d_counts % 8) != 0) return GEVO_E_ARG;
+  const hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  HIP_TRY(hipMemsetAsync(d_counts, 0, 3 * sizeof(uint64_t), s));
+  HIP_TRY(launch_bf16_check(reinterpret_cast<unsigned long long*>(d_counts), s));
+  HIP_TRY(hipStreamSynchronize(s));
+  return GEVO_OK;
+}
+
 gevo_status gevo_pop_init(const gevo_pop_config* cfg, void* d_ws, size_t ws_bytes, const float* d_train_x,
                           const int32_t* d_train_y, const float* d_test_x, const int32_t* d_test_y,
                           void* hip_stream, gevo_pop** out) {

@@ -6,7 +6,7 @@
 // Per step t, for hidden width HP and batch tile BP
 // (one wave per 32 hidden units, HP/32 waves):
 //   A1 = relu(Z1 + b1): rows -> LDS (logits operand), bf16 pairs kept in
-//        registers (dW2 operand), ReLU' bits in registers
+//        registers (dW2 operand; a nonzero pair half is also ReLU')
 //   logits^T = W2 A1^T + b2 (one batch tile per wave, so a lane holds one
 //        row's classes, split over lanes l and l+32); softmax cross-entropy,
 //        argmax and G2 = (p - y) fl(1/b) in the same registers; G2 -> LDS in
@@ -59,6 +59,9 @@ __device__ __forceinline__ uint32_t pack2(uint16_t lo, uint16_t hi) { return (ui
 __device__ __forceinline__ uint4 pack8(const uint16_t* u) {
   return make_uint4(pack2(u[0], u[1]), pack2(u[2], u[3]), pack2(u[4], u[5]), pack2(u[6], u[7]));
 }
+
+// bf16 element r of eight packed pairs
+__device__ __forceinline__ uint16_t half_of(const uint32_t* p, int r) { return (uint16_t)(p[r >> 1] >> (16 * (r & 1))); }
 
 __device__ __forceinline__ float f4get(const float4& f, int i) {
   return i == 0 ? f.x : (i == 1 ? f.y : (i == 2 ? f.z : f.w));
@@ -297,14 +300,9 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
       for (int r = 0; r < 16; ++r) wnew[r] = wc[r >> 2][r & 3];
     }
     if constexpr (fwd) {
-      uint4 wb[2];
-#pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) {
-        uint16_t u[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) u[i] = O::from_f32(wnew[8 * s2 + i]);
-        wb[s2] = pack8(u);
-      }
+      uint32_t pw[8];
+      to_bf16x2(wnew, pw);
+      const uint4 wb[2] = {make_uint4(pw[0], pw[1], pw[2], pw[3]), make_uint4(pw[4], pw[5], pw[6], pw[7])};
 #pragma unroll
       for (int T = 0; T < BT; ++T)
 #pragma unroll
@@ -379,23 +377,23 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
     // ---- the previous step's output-layer bias update and loss / hit totals
     //      (its partial sums waited in LDS during the block loop)
     if (t > a.t0) finish_out();
-    // ---- A1 = relu(Z1 + b1): rows -> LDS, bf16 operand pairs and ReLU' bits in registers
-    uint32_t rb[BT];
+    // ---- A1 = relu(Z1 + b1): rows -> LDS, bf16 operand pairs in registers
+    //      (a nonzero bf16 A1 value is also the ReLU' of its element)
     uint4 a1p[NBS];
 #pragma unroll
     for (int T = 0; T < BT; ++T) {
-      uint32_t bits = 0;
-      uint16_t u[16];
+      float f[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const float z = zacc[T][r] + b1v;
-        u[r] = O::from_f32(z > 0.0f ? z : 0.0f);
-        a1[(32 * T + crow(r, lane)) * Ly::AS + n] = u[r];
-        bits |= (uint32_t)(u[r] != 0) << r;
+        f[r] = z > 0.0f ? z : 0.0f;
       }
-      rb[T] = bits;
-      a1p[2 * T] = pack8(u);
-      a1p[2 * T + 1] = pack8(u + 8);
+      uint32_t p[8];
+      to_bf16x2(f, p);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) a1[(32 * T + crow(r, lane)) * Ly::AS + n] = half_of(p, r);
+      a1p[2 * T] = make_uint4(p[0], p[1], p[2], p[3]);
+      a1p[2 * T + 1] = make_uint4(p[4], p[5], p[6], p[7]);
     }
     if (tid < BP) yl[tid] = ylab;
     __syncthreads();
@@ -440,14 +438,19 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
         sl += e[r];
       }
       const float s = sl + __shfl_xor(sl, 32);       // same value in both halves
-      uint16_t gq[16];
+      float gf[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int c = crow(r, lane);
-        const float g = (c < C && rvalid) ? (e[r] / s - (c == y ? 1.0f : 0.0f)) * scale : 0.0f;
-        gq[r] = O::from_f32(g);
-        zg[c * Ly::ZGS + b] = g;
-        g2t[c * Ly::GTS + b] = gq[r];
+        gf[r] = (c < C && rvalid) ? (e[r] / s - (c == y ? 1.0f : 0.0f)) * scale : 0.0f;
+      }
+      uint32_t gq[8];
+      to_bf16x2(gf, gq);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int c = crow(r, lane);
+        zg[c * Ly::ZGS + b] = gf[r];
+        g2t[c * Ly::GTS + b] = half_of(gq, r);
         if (c == y) {                                // the label's lane records the row
           float ce = (logf(s) + m) - z[r];
           if (isn) ce = NAN;
@@ -461,8 +464,7 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
       }
 #pragma unroll
       for (int q = 0; q < 4; ++q)
-        *reinterpret_cast<uint2*>(g2 + b * Ly::GS + 8 * q + 4 * lh) =
-            make_uint2(pack2(gq[4 * q], gq[4 * q + 1]), pack2(gq[4 * q + 2], gq[4 * q + 3]));
+        *reinterpret_cast<uint2*>(g2 + b * Ly::GS + 8 * q + 4 * lh) = make_uint2(gq[2 * q], gq[2 * q + 1]);
     }
     __syncthreads();
     // ---- db2 partial sums over row groups (fixed order); finished after the block loop
@@ -491,14 +493,9 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
       const float4 f = *reinterpret_cast<const float4*>(w2row + (((2 * q + lh) ^ sw) << 2));
       w2v[4 * q] = f.x; w2v[4 * q + 1] = f.y; w2v[4 * q + 2] = f.z; w2v[4 * q + 3] = f.w;
     }
-    uint4 w2b[2];
-#pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2) {
-      uint16_t u[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) u[i] = O::from_f32(w2v[8 * s2 + i]);
-      w2b[s2] = pack8(u);
-    }
+    uint32_t pw2[8];
+    to_bf16x2(w2v, pw2);
+    const uint4 w2b[2] = {make_uint4(pw2[0], pw2[1], pw2[2], pw2[3]), make_uint4(pw2[4], pw2[5], pw2[6], pw2[7])};
 #pragma unroll
     for (int T = 0; T < BT; ++T) {
       f32x16_t acc = zero16();
@@ -513,28 +510,33 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
     float db1p = 0.0f;
 #pragma unroll
     for (int T = 0; T < BT; ++T) {
-      uint16_t u[16];
+      const uint32_t ap[8] = {a1p[2 * T].x, a1p[2 * T].y, a1p[2 * T].z, a1p[2 * T].w,
+                              a1p[2 * T + 1].x, a1p[2 * T + 1].y, a1p[2 * T + 1].z, a1p[2 * T + 1].w};
+      float f[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        u[r] = O::from_f32(((rb[T] >> r) & 1u) ? zacc[T][r] : 0.0f);
-        db1p += O::to_f32(u[r]);
-      }
-      g1s[(wave * NBS + 2 * T) * 64 + lane] = pack8(u);
-      g1s[(wave * NBS + 2 * T + 1) * 64 + lane] = pack8(u + 8);
+      for (int r = 0; r < 16; ++r) f[r] = half_of(ap, r) != 0 ? zacc[T][r] : 0.0f;
+      uint32_t p[8];
+      to_bf16x2(f, p);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) db1p += O::to_f32(half_of(p, r));
+      g1s[(wave * NBS + 2 * T) * 64 + lane] = make_uint4(p[0], p[1], p[2], p[3]);
+      g1s[(wave * NBS + 2 * T + 1) * 64 + lane] = make_uint4(p[4], p[5], p[6], p[7]);
     }
     db1p += __shfl_xor(db1p, 32);
     b1v = __fsub_rn(b1v, __fmul_rn(lrv, db1p));
     // ---- masked SGD on W2 (LDS master) and refresh of its bf16 operand
+    {
+      float f[16];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      float f[4];
+      for (int r = 0; r < 16; ++r) f[r] = ((m2bits >> r) & 1u) ? __fsub_rn(w2v[r], __fmul_rn(lrv, d2[r])) : 0.0f;
+      uint32_t p[8];
+      to_bf16x2(f, p);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = 4 * q + i, c = crow(r, lane);
-        f[i] = ((m2bits >> r) & 1u) ? __fsub_rn(w2v[r], __fmul_rn(lrv, d2[r])) : 0.0f;
-        w2[c * Ly::W2S + n] = O::from_f32(f[i]);
-      }
-      *reinterpret_cast<float4*>(w2row + (((2 * q + lh) ^ sw) << 2)) = make_float4(f[0], f[1], f[2], f[3]);
+      for (int r = 0; r < 16; ++r) w2[crow(r, lane) * Ly::W2S + n] = half_of(p, r);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<float4*>(w2row + (((2 * q + lh) ^ sw) << 2)) =
+            make_float4(f[4 * q], f[4 * q + 1], f[4 * q + 2], f[4 * q + 3]);
     }
     // ---- dW1 + masked SGD on W1 + forward of the next step
     int tid_pass;

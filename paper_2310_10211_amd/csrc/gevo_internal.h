@@ -148,6 +148,7 @@ hipError_t launch_w1_image(const float* src, float* dst, int P, int Kp, int Hp, 
 // W1 mask row words [P][Hp][Kp/32] -> block-major words [P][Kp/32][Hp]
 hipError_t launch_mask_block_major(const uint32_t* src, uint32_t* dst, int P, int Kp, int Hp, hipStream_t s,
                                    const LaunchEv& ev);
+hipError_t launch_bf16_check(unsigned long long* counts, hipStream_t s);   // counts zeroed by the caller
 size_t fused2_lds_bytes(int hp, int bp);     // 0 when the shape has no fused instantiation
 hipError_t launch_reduce_partials(const double* part_ce, const unsigned int* part_corr, int P, int n_chunks,
                                   double* ce_out, unsigned long long* corr_out, hipStream_t s, const LaunchEv& ev);
