@@ -196,16 +196,14 @@ gevo_status gevo_epoch_permutation(uint64_t seed, uint32_t epoch, uint32_t n, ui
 /* Self-check of the binary32 -> bfloat16 rounding that the bf16 kernels use
  * for every operand they round (weights from the master, activations,
  * gradients; round-to-nearest-even, see Numerics).  The kernels convert with
- * gfx950's packed conversion instruction and route groups holding a NaN or a
- * denormal to a bit-level rounding.  This call converts every binary32
- * encoding twice, paired two ways as the packed instruction's operands, on
- * `hip_stream` and writes three counts (over both pairings) to the caller's
- * device array d_counts[3] (8-byte aligned): [0] conversions whose kernel
- * rounding differs from round-to-nearest-even (0 when the kernels are exact),
- * [1] conversions on which the hardware instruction alone differs, [2] those
- * of [1] that the kernels do not route to the bit-level path (must be 0).  Zeroes
- * d_counts first; synchronises the stream.  GEVO_E_ARG for a null or
- * misaligned pointer, GEVO_E_HIP for a runtime error. */
+ * gfx950's packed conversion instruction.  This call converts every binary32
+ * encoding twice, paired two ways as the instruction's two operands, compares
+ * each result with a bit-level round-to-nearest-even (NaN -> quiet NaN) and
+ * writes the number of differing results per pairing to the caller's device
+ * array d_counts[2] (8-byte aligned): both are 0 when the kernels round
+ * exactly.  Zeroes d_counts first; runs on `hip_stream` and synchronises it.
+ * GEVO_E_ARG for a null or misaligned pointer, GEVO_E_HIP for a runtime
+ * error. */
 gevo_status gevo_check_bf16_rounding(void* hip_stream, uint64_t* d_counts);
 
 /*

@@ -165,9 +165,10 @@ def epoch_permutation(seed: int, epoch: int, n: int) -> np.ndarray:
 
 
 def check_bf16_rounding(stream=None) -> list:
-    """Counts of the exhaustive bf16 rounding check (see gevo_check_bf16_rounding)."""
+    """Per operand pairing, the number of binary32 encodings whose kernel bf16
+    rounding differs from round-to-nearest-even (see gevo_check_bf16_rounding)."""
     import torch
-    counts = torch.zeros(3, dtype=torch.int64, device="cuda")
+    counts = torch.zeros(2, dtype=torch.int64, device="cuda")
     st = stream if stream is not None else torch.cuda.current_stream()
     _check(lib().gevo_check_bf16_rounding(ctypes.c_void_p(st.cuda_stream), ctypes.c_void_p(counts.data_ptr())),
            "gevo_check_bf16_rounding")

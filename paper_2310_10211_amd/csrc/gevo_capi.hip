@@ -571,7 +571,7 @@ gevo_status gevo_epoch_permutation(uint64_t seed, uint32_t epoch, uint32_t n, ui
 gevo_status gevo_check_bf16_rounding(void* hip_stream, uint64_t* d_counts) {
   if (!d_counts || ((uintptr_t)d_counts % 8) != 0) return GEVO_E_ARG;
   const hipStream_t s = static_cast<hipStream_t>(hip_stream);
-  HIP_TRY(hipMemsetAsync(d_counts, 0, 3 * sizeof(uint64_t), s));
+  HIP_TRY(hipMemsetAsync(d_counts, 0, 2 * sizeof(uint64_t), s));
   HIP_TRY(launch_bf16_check(reinterpret_cast<unsigned long long*>(d_counts), s));
   HIP_TRY(hipStreamSynchronize(s));
   return GEVO_OK;

@@ -21,37 +21,22 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
   return (uint16_t)(u >> 16);
 }
 
-// gfx950's packed conversion (v_cvt_pk_bf16_f32).  It rounds zero, normal and
-// infinite inputs to nearest even (gevo_check_bf16_rounding compares it with
-// f32_to_bf16_bits over every binary32 encoding); the kernels do not rely on
-// its handling of NaN and denormal inputs.
-__device__ __forceinline__ uint32_t bf16x2_hw(float lo, float hi) {
-  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-  typedef float f32x2 __attribute__((ext_vector_type(2)));
-  const f32x2 x = {lo, hi};
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(x, bf16x2));
+// p[i] = bf16(f[2i]) | bf16(f[2i+1]) << 16 with gfx950's packed conversion
+// (v_cvt_pk_bf16_f32), which rounds to nearest even and keeps NaN a quiet NaN
+// exactly as f32_to_bf16_bits does, denormal inputs included, under the
+// kernels' IEEE denormal mode.  gevo_check_bf16_rounding compares the two over
+// every binary32 encoding.
+__device__ __forceinline__ uint32_t bf16x2(float lo, float hi) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  const f32x2_t x = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(x, bf16x2_t));
 }
 
-// true for the inputs whose rounding is not left to the packed conversion: NaN
-// (signalling or quiet) and denormals of either sign (class mask 0x93)
-__device__ __forceinline__ bool bf16_hw_unsafe(float f) { return __builtin_amdgcn_classf(f, 0x93); }
-
-// p[i] = bf16(f[2i]) | bf16(f[2i+1]) << 16, rounded to nearest even.  The
-// whole group takes the bit-level path when any lane's group holds a NaN or a
-// denormal, so the result never depends on the hardware's handling of them.
 template <int N>
 __device__ __forceinline__ void to_bf16x2(const float (&f)[N], uint32_t (&p)[N / 2]) {
-  bool unsafe = false;
 #pragma unroll
-  for (int i = 0; i < N; ++i) unsafe |= bf16_hw_unsafe(f[i]);
-  if (__builtin_expect(unsafe, 0)) {
-#pragma unroll
-    for (int i = 0; i < N / 2; ++i)
-      p[i] = (uint32_t)f32_to_bf16_bits(f[2 * i]) | ((uint32_t)f32_to_bf16_bits(f[2 * i + 1]) << 16);
-  } else {
-#pragma unroll
-    for (int i = 0; i < N / 2; ++i) p[i] = bf16x2_hw(f[2 * i], f[2 * i + 1]);
-  }
+  for (int i = 0; i < N / 2; ++i) p[i] = bf16x2(f[2 * i], f[2 * i + 1]);
 }
 
 template <typename S> struct Op;

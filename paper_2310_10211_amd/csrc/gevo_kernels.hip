@@ -802,34 +802,23 @@ hipError_t launch_mask_block_major(const uint32_t* src, uint32_t* dst, int P, in
   return hipGetLastError();
 }
 
-// Exhaustive check of the bf16 rounding used by the kernels, over every
-// binary32 encoding in two pairings of the packed conversion's operands:
-// (i, i | 2^31) and (2j, 2j + 1), i, j < 2^31.  Counts over both pairings:
-// counts[0] the kernels' conversion (to_bf16x2) differs from the bit-level
-// rounding; counts[1] the packed hardware conversion alone differs;
-// counts[2] it differs on an input that to_bf16x2 keeps on the hardware path.
+// Exhaustive check of the packed bf16 conversion the kernels use against the
+// bit-level rounding, over every binary32 encoding in two pairings of the
+// instruction's operands: counts[0] for (i, i | 2^31), counts[1] for
+// (2j, 2j + 1), i, j < 2^31, each the number of differing halves.
 __global__ __launch_bounds__(256) void k_bf16_check(unsigned long long* counts) {
   const uint64_t nthreads = (uint64_t)gridDim.x * 256;
-  unsigned long long c0 = 0, c1 = 0, c2 = 0;
+  unsigned long long c[2] = {0, 0};
   for (uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x; i < (1ull << 32); i += nthreads) {
-    const uint32_t j = (uint32_t)(i & 0x7fffffffu);
-    const uint32_t e0 = i >> 31 ? 2u * j : j, e1 = i >> 31 ? 2u * j + 1u : j | 0x80000000u;
+    const uint32_t j = (uint32_t)(i & 0x7fffffffu), pairing = (uint32_t)(i >> 31);
+    const uint32_t e0 = pairing ? 2u * j : j, e1 = pairing ? 2u * j + 1u : j | 0x80000000u;
     const float f[2] = {__uint_as_float(e0), __uint_as_float(e1)};
     uint32_t p[1];
     to_bf16x2(f, p);
-    const uint32_t hw = bf16x2_hw(f[0], f[1]);
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const uint16_t ref = f32_to_bf16_bits(f[h]);
-      const uint16_t got = (uint16_t)(p[0] >> (16 * h)), raw = (uint16_t)(hw >> (16 * h));
-      c0 += got != ref;
-      c1 += raw != ref;
-      c2 += raw != ref && !(bf16_hw_unsafe(f[0]) || bf16_hw_unsafe(f[1]));
-    }
+    c[pairing] += ((uint16_t)p[0] != f32_to_bf16_bits(f[0])) + ((uint16_t)(p[0] >> 16) != f32_to_bf16_bits(f[1]));
   }
-  if (c0) atomicAdd(&counts[0], c0);
-  if (c1) atomicAdd(&counts[1], c1);
-  if (c2) atomicAdd(&counts[2], c2);
+  if (c[0]) atomicAdd(&counts[0], c[0]);
+  if (c[1]) atomicAdd(&counts[1], c[1]);
 }
 
 hipError_t launch_bf16_check(unsigned long long* counts, hipStream_t s) {
