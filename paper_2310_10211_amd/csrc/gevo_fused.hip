@@ -69,6 +69,14 @@ __device__ __forceinline__ float f4get(const float4& f, int i) {
 
 typedef float f32x4_t __attribute__((ext_vector_type(4)));   // register-operand form of float4
 
+// 16x16x32 bf16 MFMA: lane l supplies row (A) / column (B) l%16, contraction
+// elements 8(l/16) .. 8(l/16)+7; the accumulator gives lane l the column l%16
+// and the rows 4(l/16) .. 4(l/16)+3.
+__device__ __forceinline__ f32x4_t mma16(uint4 a, uint4 b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c,
+                                                 0, 0, 0);
+}
+
 }  // namespace
 
 template <int HP, int BP>
@@ -397,10 +405,81 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
     }
     if (tid < BP) yl[tid] = ylab;
     __syncthreads();
-    // ---- logits^T (one batch tile per wave): lane = row b, registers = the
-    //      classes crow(r) of the lane's half; softmax cross-entropy, argmax
-    //      (lowest index on ties, a NaN logit is a miss), G2 = (p - onehot(y)) fl(1/b)
-    if (wave < BT) {
+    // ---- logits^T, softmax cross-entropy, argmax (lowest index on ties, a NaN
+    //      logit is a miss), G2 = (p - onehot(y)) fl(1/b).
+    //      Up to 16 classes: 16-row batch tiles shared by all waves; a lane holds
+    //      four classes of one row and the row's four lanes combine by shuffles.
+    //      Classes 16..31 of G2 are then left unwritten and never read.
+    //      More classes: one 32-row tile per wave; a lane holds the row's
+    //      classes crow(r) of its half, combined with the other half.
+    const bool c16 = a.C <= 16;
+    if (c16) {
+      const int l16 = lane & 15, lq = lane >> 4, C = a.C;
+      for (int tt = wave; tt < BP / 16; tt += NW) {
+        f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+        const uint16_t* ap = w2 + l16 * Ly::W2S + 8 * lq;
+        const uint16_t* bp = a1 + (16 * tt + l16) * Ly::AS + 8 * lq;
+#pragma unroll
+        for (int s = 0; s < HP / 32; ++s) acc = mma16(O::load(ap + 32 * s), O::load(bp + 32 * s), acc);
+        const int b = 16 * tt + l16, y = yl[b];
+        const bool rvalid = y >= 0;
+        float z[4];
+        float ml = -INFINITY, bv = -INFINITY;
+        int bi = 64, nanl = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {                // j ascending = class ascending within the lane
+          const int c = 4 * lq + j;
+          z[j] = acc[j] + b2s[c];
+          if (c < C) {
+            ml = fmaxf(ml, z[j]);
+            if (z[j] != z[j]) nanl = 1;
+            else if (z[j] > bv) { bv = z[j]; bi = c; }
+          }
+        }
+#pragma unroll
+        for (int off = 16; off <= 32; off <<= 1) {
+          ml = fmaxf(ml, __shfl_xor(ml, off));
+          nanl |= __shfl_xor(nanl, off);
+          const float ov = __shfl_xor(bv, off);
+          const int oi = __shfl_xor(bi, off);
+          if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+        }
+        const float m = ml;
+        float e[4], sl = 0.0f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          e[j] = 4 * lq + j < C ? expf(z[j] - m) : 0.0f;
+          sl += e[j];
+        }
+        sl += __shfl_xor(sl, 16);                    // commutative pairings: the row's
+        const float s = sl + __shfl_xor(sl, 32);     // four lanes hold the same sum
+        float gf[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int c = 4 * lq + j;
+          gf[j] = (c < C && rvalid) ? (e[j] / s - (c == y ? 1.0f : 0.0f)) * scale : 0.0f;
+        }
+        uint32_t gq[2];
+        to_bf16x2(gf, gq);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int c = 4 * lq + j;
+          zg[c * Ly::ZGS + b] = gf[j];
+          g2t[c * Ly::GTS + b] = half_of(gq, j);
+          if (c == y) {                              // the label's lane records the row
+            float ce = (logf(s) + m) - z[j];
+            if (nanl) ce = NAN;
+            rce[b] = (double)ce;
+            rco[b] = (!nanl && bi == y) ? 1u : 0u;
+          }
+        }
+        if (!rvalid && lq == 0) {
+          rce[b] = 0.0;
+          rco[b] = 0u;
+        }
+        *reinterpret_cast<uint2*>(g2 + b * Ly::GS + 4 * lq) = make_uint2(gq[0], gq[1]);
+      }
+    } else if (wave < BT) {
       f32x16_t c0 = zero16(), c1 = zero16();
       const uint16_t* ap = w2 + l32 * Ly::W2S + 8 * lh;
       const uint16_t* bp = a1 + (32 * wave + l32) * Ly::AS + 8 * lh;
@@ -471,7 +550,8 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
     {
       const int c = tid & 31, part = tid >> 5;       // Ly::NDP parts
       float sp = 0.0f;
-      for (int r = part; r < BP; r += Ly::NDP) sp += zg[c * Ly::ZGS + r];
+      if (!c16 || c < 16)
+        for (int r = part; r < BP; r += Ly::NDP) sp += zg[c * Ly::ZGS + r];
       dbp[part * 32 + c] = sp;
     }
     // the next pass's first blocks, W1 words and labels can load from here on
@@ -499,10 +579,13 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
 #pragma unroll
     for (int T = 0; T < BT; ++T) {
       f32x16_t acc = zero16();
-#pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) {
-        const uint16_t* pp = g2 + (32 * T + l32) * Ly::GS + 16 * s2 + 4 * lh;
-        acc = O::mma(ld2x8(pp, pp + 8), w2b[s2], acc);
+      {
+        const uint16_t* pp = g2 + (32 * T + l32) * Ly::GS + 4 * lh;
+        acc = O::mma(ld2x8(pp, pp + 8), w2b[0], acc);
+      }
+      if (!c16) {                                    // classes 16..31
+        const uint16_t* pp = g2 + (32 * T + l32) * Ly::GS + 16 + 4 * lh;
+        acc = O::mma(ld2x8(pp, pp + 8), w2b[1], acc);
       }
       zacc[T] = acc;
     }

@@ -191,6 +191,8 @@ def test_bf16_two_layer_ragged_batch():
     ([784, 128, 10], 128, 600),     # hidden 128, batch tile 128
     ([784, 256, 10], 50, 620),      # hidden 256, batch 50 (tile 64)
     ([300, 250, 7], 20, 500),       # input 300 (10 column blocks), hidden 250, 7 classes, tile 32
+    ([784, 256, 16], 128, 600),     # 16 classes: the largest count of the 16-row logits tiles
+    ([784, 128, 24], 64, 600),      # 24 classes: 32-row logits tiles
 ])
 def test_bf16_two_layer_shapes(dims, batch, n_train):
     """Two-layer bf16 nets at the other hidden widths and batch tiles of the per-variant training kernel."""
@@ -198,9 +200,10 @@ def test_bf16_two_layer_shapes(dims, batch, n_train):
     if dims[0] != 784:
         data["x_train"] = data["x_train"][:, :dims[0]].copy()
         data["x_test"] = data["x_test"][:, :dims[0]].copy()
-    if dims[-1] != 10:
-        data["y_train"] = data["y_train"] % dims[-1]
-        data["y_test"] = data["y_test"] % dims[-1]
+    if dims[-1] != 10:                 # spread the ten synthetic classes over all dims[-1] labels
+        for split in ("y_train", "y_test"):
+            y = data[split]
+            data[split] = ((y + 10 * (np.arange(len(y)) % 3)) % dims[-1]).astype(y.dtype)
     pop = _pop(cfg, data)
     pop.train_epoch(0)
     pop.predict()
