@@ -322,9 +322,11 @@ gevo_status begin_epoch(gevo_pop* p, int e) {
   g.X = p->trX; g.y = p->trY; g.perm = at<uint32_t>(p, y.perm); g.n = y.n_train;
   g.d0 = y.lay[0].K; g.Kp = y.lay[0].Kp; g.B = y.B; g.Bp = y.Bp; g.T = y.T;
   g.rows = p->ws + y.xrows; g.labels = at<int32_t>(p, y.yep);
+  g.blocked = y.fused;                             // the fused kernel reads rows one column block at a time
   HIP_TRY(launch_gather<S>(g, p->stream, prof(p, GEVO_KERNEL_GATHER)));
   TransposeArgs tr{};
   tr.src = p->ws + y.xrows; tr.dst = p->ws + y.xcols; tr.Kp = y.lay[0].Kp; tr.Bp = y.Bp; tr.T = y.T;
+  tr.blocked = y.fused;
   HIP_TRY(launch_transpose<S>(tr, p->stream, prof(p, GEVO_KERNEL_GATHER)));
   HIP_TRY(launch_zero_bytes(p->ws + y.train_ce, (size_t)y.P * 8, p->stream, prof(p, GEVO_KERNEL_AUX)));
   HIP_TRY(launch_zero_bytes(p->ws + y.train_corr, (size_t)y.P * 8, p->stream, prof(p, GEVO_KERNEL_AUX)));

@@ -33,9 +33,12 @@
 // every W1 load and store instruction covers whole cache lines.
 // The W1 stream is software-pipelined one block ahead and the shared X blocks
 // two blocks ahead; the block loop is unrolled by two with alternating
-// register sets.  The W1 block loads are issued after the block's X loads as
-// explicit instructions with one explicit wait at the top of the next block,
-// so no wait for a compiler-visible load can also drain the W1 prefetch.
+// register sets.  All these loads are explicit instructions with one explicit
+// wait at the top of the next block, so no wait for a compiler-visible load can
+// also drain the prefetch.  The X rows of a step are stored block-major
+// ([Kp/32][B][32]), so one block's rows are a contiguous 8 KB, and each
+// workgroup starts its passes at a different column block, so the workgroups
+// sharing an L2 do not all request the same X lines at once.
 #include "gevo_internal.h"
 #include "gevo_device.h"
 
@@ -67,7 +70,8 @@ __device__ __forceinline__ float f4get(const float4& f, int i) {
   return i == 0 ? f.x : (i == 1 ? f.y : (i == 2 ? f.z : f.w));
 }
 
-typedef float f32x4_t __attribute__((ext_vector_type(4)));   // register-operand form of float4
+typedef float f32x4_t __attribute__((ext_vector_type(4)));   // register-operand forms of float4
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));   // and uint4
 
 // 16x16x32 bf16 MFMA: lane l supplies row (A) / column (B) l%16, contraction
 // elements 8(l/16) .. 8(l/16)+7; the accumulator gives lane l the column l%16
@@ -152,6 +156,13 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
   float* W2 = a.W2 + (size_t)v * 32 * HP;
   const uint32_t* m2 = a.m2 + (size_t)v * 32 * (HP / 32);
   const float lrv = a.lr[v];
+  // Every pass visits the column blocks in the order rot, rot+1, ... (mod nkb).
+  // All workgroups read the same shared X blocks; workgroup v runs on XCD
+  // v mod 8, and staggering the start block over the workgroups of one XCD
+  // keeps them from requesting the same L2 lines at the same moment.  The
+  // forward's fp32 sum over blocks follows this order.
+  const int rot = (v >> 3) % nkb;
+  auto phys = [&](int j) { return j + rot < nkb ? j + rot : j + rot - nkb; };
 
   // Output layer, resident for the whole run: the fp32 master of this lane's
   // 16 (class, unit) pairs lives in LDS row n (4-float chunk j stored at chunk
@@ -186,33 +197,35 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
 
   // Prefetch registers of the block loop: two sets of X staging registers
   // (block kb+1 waiting for its LDS buffer, block kb+2 in flight) and two sets
-  // of W1 master registers (block kb in use, block kb+1 in flight).
-  uint4 xAr[XU], xAc[XU], xBr[XU], xBc[XU];
+  // of W1 master registers (block kb in use, block kb+1 in flight).  Every load
+  // into them is an explicit instruction with an explicit wait: a load the
+  // compiler tracked into a loop-carried register would make it wait for all
+  // outstanding memory operations at the loop head.
+  u32x4_t xAr[XU], xAc[XU], xBr[XU], xBc[XU];
   f32x4_t wA[4], wB[4];
   uint32_t mA = 0, mB = 0;
   int ylab = -1;
-  // (registers of a block past the end are left as they are: such a block is never stored)
-  auto load_x = [&](auto updc, int tu, auto fwdc, int tf, int kb, int td, uint4 (&xrn)[XU], uint4 (&xcn)[XU]) {
+  // X block of visit j (clamped: past the end an in-bounds re-read whose value
+  // is never stored; threads past the block's chunks re-read its last chunk)
+  auto load_x = [&](auto updc, int tu, auto fwdc, int tf, int j, int td, u32x4_t (&xrn)[XU], u32x4_t (&xcn)[XU]) {
     constexpr bool upd = decltype(updc)::value, fwd = decltype(fwdc)::value;
     const uint16_t* xrs = a.xrows + (size_t)tf * BP * Kp;
     const uint16_t* xcs = a.xcols + (size_t)tu * Kp * BP;
+    const int kc = phys(j < nkb ? j : nkb - 1);
 #pragma unroll
     for (int u = 0; u < XU; ++u) {
-      const int i = td + NT * u;
-      const int kc = kb < nkb ? kb : nkb - 1;   // past the end: an in-bounds re-read, never stored
-      if (i < 4 * BP) {
-        if constexpr (fwd) {
-          const int b = i >> 2, q = i & 3;
-          xrn[u] = *reinterpret_cast<const uint4*>(xrs + (size_t)b * Kp + kc * 32 + q * 8);
-        }
-        if constexpr (upd) {
-          const int k = i / (BP / 8), q = i % (BP / 8);
-          xcn[u] = *reinterpret_cast<const uint4*>(xcs + (size_t)(kc * 32 + k) * BP + q * 8);
-        }
+      const int i = td + NT * u < 4 * BP ? td + NT * u : 4 * BP - 1;
+      if constexpr (fwd) {                         // rows block-major: block kc is BP x 32 contiguous
+        const uint16_t* p = xrs + (size_t)kc * BP * 32 + (size_t)i * 8;
+        asm volatile("global_load_dwordx4 %0, %1, off" : "=&v"(xrn[u]) : "v"(p) : "memory");
+      }
+      if constexpr (upd) {
+        const uint16_t* p = xcs + (size_t)(kc * 32 + i / (BP / 8)) * BP + (i % (BP / 8)) * 8;
+        asm volatile("global_load_dwordx4 %0, %1, off" : "=&v"(xcn[u]) : "v"(p) : "memory");
       }
     }
   };
-  auto store_x = [&](auto updc, auto fwdc, int buf, int td, const uint4 (&xrn)[XU], const uint4 (&xcn)[XU]) {
+  auto store_x = [&](auto updc, auto fwdc, int buf, int td, const u32x4_t (&xrn)[XU], const u32x4_t (&xcn)[XU]) {
     constexpr bool upd = decltype(updc)::value, fwd = decltype(fwdc)::value;
 #pragma unroll
     for (int u = 0; u < XU; ++u) {
@@ -220,69 +233,78 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
       if (i < 4 * BP) {
         if constexpr (fwd) {
           const int b = i >> 2, q = i & 3;
-          *reinterpret_cast<uint4*>(xr + buf * BP * Ly::XR + b * Ly::XR + q * 8) = xrn[u];
+          *reinterpret_cast<u32x4_t*>(xr + buf * BP * Ly::XR + b * Ly::XR + q * 8) = xrn[u];
         }
         if constexpr (upd) {
           const int k = i / (BP / 8), q = i % (BP / 8);
-          *reinterpret_cast<uint4*>(xc + buf * 32 * Ly::XC + k * Ly::XC + q * 8) = xcn[u];
+          *reinterpret_cast<u32x4_t*>(xc + buf * 32 * Ly::XC + k * Ly::XC + q * 8) = xcn[u];
         }
       }
+    }
+  };
+  // W1 block of visit j for this wave (and its mask words when updating)
+  auto load_w = [&](auto updc, int j, int td, f32x4_t (&wn)[4], uint32_t& mn) {
+    constexpr bool upd = decltype(updc)::value;
+    const int kb = phys(j);
+    const float* wp = W1 + ((size_t)kb * NW + wave) * 1024 + (td & 63) * 4;
+    if constexpr (upd) {
+      const uint32_t* mp = m1 + (size_t)kb * HP + wave * 32 + (td & 31);
+      asm volatile(
+          "global_load_dwordx4 %0, %5, off\n\t"
+          "global_load_dwordx4 %1, %5, off offset:1024\n\t"
+          "global_load_dwordx4 %2, %5, off offset:2048\n\t"
+          "global_load_dwordx4 %3, %5, off offset:3072\n\t"
+          "global_load_dword %4, %6, off"
+          : "=&v"(wn[0]), "=&v"(wn[1]), "=&v"(wn[2]), "=&v"(wn[3]), "=&v"(mn)
+          : "v"(wp), "v"(mp)
+          : "memory");
+    } else {
+      asm volatile(
+          "global_load_dwordx4 %0, %4, off\n\t"
+          "global_load_dwordx4 %1, %4, off offset:1024\n\t"
+          "global_load_dwordx4 %2, %4, off offset:2048\n\t"
+          "global_load_dwordx4 %3, %4, off offset:3072"
+          : "=&v"(wn[0]), "=&v"(wn[1]), "=&v"(wn[2]), "=&v"(wn[3])
+          : "v"(wp)
+          : "memory");
+      mn = 0u;
     }
   };
   // head of the next pass over the input columns: X blocks 0 and 1, W1 block 0
-  // and its mask words, and the labels of the step whose loss the pass prepares
+  // and its mask words (in this order), then the labels of the step whose loss
+  // the pass prepares
   auto issue_head = [&](auto updc, int tu, auto fwdc, int tf, int td) {
-    constexpr bool upd = decltype(updc)::value, fwd = decltype(fwdc)::value;
-    const int n = wave * 32 + (td & 31), lh = (td >> 5) & 1;
+    constexpr bool fwd = decltype(fwdc)::value;
     load_x(updc, tu, fwdc, tf, 0, td, xAr, xAc);
     load_x(updc, tu, fwdc, tf, 1, td, xBr, xBc);
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      wA[q] = *reinterpret_cast<const f32x4_t*>(W1 + (size_t)wave * 1024 + q * 256 + (td & 63) * 4);
-    mA = upd ? m1[n] : 0u;
+    load_w(updc, 0, td, wA, mA);
     if (fwd && td < BP) ylab = a.labels[(size_t)tf * BP + td];
   };
 
-  // one 32-column block of a pass: dW1 + update of block kb (step tu) and/or
-  // forward accumulation of step tf; wc/mc hold block kb, wn/mn receive block
-  // kb+1, xl receives X block kb+2, xs holds X block kb+1 for the other buffer
-  auto kblock = [&](auto updc, int tu, auto fwdc, int tf, int kb, int td, f32x4_t (&wc)[4], uint32_t& mc,
-                    f32x4_t (&wn)[4], uint32_t& mn, uint4 (&xlr)[XU], uint4 (&xlc)[XU], uint4 (&xsr)[XU],
-                    uint4 (&xsc)[XU]) {
+  // visit kb of a pass (column block phys(kb)): dW1 + update (step tu) and/or
+  // forward accumulation of step tf; wc/mc hold visit kb's W1 block, wn/mn
+  // receive visit kb+1's, xl receives X of visit kb+2, xs holds X of visit kb+1
+  // for the other buffer
+  auto kblock = [&](auto firstc, auto updc, int tu, auto fwdc, int tf, int kb, int td, f32x4_t (&wc)[4],
+                    uint32_t& mc, f32x4_t (&wn)[4], uint32_t& mn, u32x4_t (&xlr)[XU], u32x4_t (&xlc)[XU],
+                    u32x4_t (&xsr)[XU], u32x4_t (&xsc)[XU]) {
     constexpr bool upd = decltype(updc)::value, fwd = decltype(fwdc)::value;
     const int lane = td & 63, l32 = lane & 31, lh = lane >> 5, n = wave * 32 + l32;
     const int buf = kb & 1;
     const bool more = kb + 1 < nkb;
-    // block kb's W1 words (issued one block earlier) and everything older
-    asm volatile("s_waitcnt vmcnt(0)" : "+v"(wc[0]), "+v"(wc[1]), "+v"(wc[2]), "+v"(wc[3]), "+v"(mc) : : "memory");
+    // Block kb's W1 words and X block kb+1 were issued one block earlier, and
+    // vector memory operations retire in issue order.  After them that block
+    // issued only its four W1 stores (when updating), which may stay in
+    // flight; block 0 follows the head and waits for everything.
+    constexpr int NS = (decltype(firstc)::value || !upd) ? 0 : 4;
+    asm volatile("s_waitcnt vmcnt(%5)"
+                 : "+v"(wc[0]), "+v"(wc[1]), "+v"(wc[2]), "+v"(wc[3]), "+v"(mc)
+                 : "n"(NS)
+                 : "memory");
+#pragma unroll
+    for (int u = 0; u < XU; ++u) asm volatile("" : "+v"(xsr[u]), "+v"(xsc[u]));
     load_x(updc, tu, fwdc, tf, kb + 2, td, xlr, xlc);
-    {
-      // (the last block re-reads itself: the load stays in bounds and its value is unused)
-      const int kn = more ? kb + 1 : kb;
-      const float* wp = W1 + ((size_t)kn * NW + wave) * 1024 + lane * 4;
-      if constexpr (upd) {
-        const uint32_t* mp = m1 + (size_t)kn * HP + n;
-        asm volatile(
-            "global_load_dwordx4 %0, %5, off\n\t"
-            "global_load_dwordx4 %1, %5, off offset:1024\n\t"
-            "global_load_dwordx4 %2, %5, off offset:2048\n\t"
-            "global_load_dwordx4 %3, %5, off offset:3072\n\t"
-            "global_load_dword %4, %6, off"
-            : "=&v"(wn[0]), "=&v"(wn[1]), "=&v"(wn[2]), "=&v"(wn[3]), "=&v"(mn)
-            : "v"(wp), "v"(mp)
-            : "memory");
-      } else {
-        asm volatile(
-            "global_load_dwordx4 %0, %4, off\n\t"
-            "global_load_dwordx4 %1, %4, off offset:1024\n\t"
-            "global_load_dwordx4 %2, %4, off offset:2048\n\t"
-            "global_load_dwordx4 %3, %4, off offset:3072"
-            : "=&v"(wn[0]), "=&v"(wn[1]), "=&v"(wn[2]), "=&v"(wn[3])
-            : "v"(wp)
-            : "memory");
-        mn = 0u;
-      }
-    }
+    load_w(updc, more ? kb + 1 : kb, td, wn, mn);   // the last block re-reads itself (in bounds, unused)
     const uint16_t* xcb = xc + buf * 32 * Ly::XC;
     const uint16_t* xrb = xr + buf * BP * Ly::XR;
     float wnew[16];
@@ -301,7 +323,7 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
       }
 #pragma unroll
       for (int q = 0; q < 4; ++q)
-        *reinterpret_cast<float4*>(W1 + (((size_t)kb * NW + wave) * 4 + q) * 256 + lane * 4) =
+        *reinterpret_cast<float4*>(W1 + (((size_t)phys(kb) * NW + wave) * 4 + q) * 256 + lane * 4) =
             make_float4(wnew[4 * q], wnew[4 * q + 1], wnew[4 * q + 2], wnew[4 * q + 3]);
     } else {
 #pragma unroll
@@ -326,23 +348,39 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
   // one pass over the input columns (head already issued): optional dW1 +
   // update (step tu), optional forward accumulation of step tf into zacc
   auto kloop = [&](auto updc, int tu, auto fwdc, int tf, int td) {
+    const std::true_type first{};
+    const std::false_type later{};
     if constexpr (decltype(fwdc)::value) {
 #pragma unroll
       for (int T = 0; T < BT; ++T) zacc[T] = zero16();
     }
     __syncthreads();                           // the output-layer scratch shares the X buffers
+    // X block 0 is the oldest operation of the head; X block 1 and W1 block 0
+    // (NX + NL operations) may stay in flight
+    constexpr int NX = (decltype(fwdc)::value ? XU : 0) + (decltype(updc)::value ? XU : 0);
+    constexpr int NL = decltype(updc)::value ? 5 : 4;
+    asm volatile("s_waitcnt vmcnt(%0)" : : "n"(NX + NL) : "memory");
+#pragma unroll
+    for (int u = 0; u < XU; ++u) asm volatile("" : "+v"(xAr[u]), "+v"(xAc[u]));
     store_x(updc, fwdc, 0, td, xAr, xAc);
     __syncthreads();
-    for (int kb = 0; kb < nkb; kb += 2) {
-      kblock(updc, tu, fwdc, tf, kb, td, wA, mA, wB, mB, xAr, xAc, xBr, xBc);
-      if (kb + 1 < nkb) kblock(updc, tu, fwdc, tf, kb + 1, td, wB, mB, wA, mA, xBr, xBc, xAr, xAc);
+    // block 0, then whole pairs of blocks (alternating register sets), then an
+    // odd last block: no branch inside the loop body skips a block
+    kblock(first, updc, tu, fwdc, tf, 0, td, wA, mA, wB, mB, xAr, xAc, xBr, xBc);
+    int kb = 1;
+    for (; kb + 1 < nkb; kb += 2) {
+      kblock(later, updc, tu, fwdc, tf, kb, td, wB, mB, wA, mA, xBr, xBc, xAr, xAc);
+      kblock(later, updc, tu, fwdc, tf, kb + 1, td, wA, mA, wB, mB, xAr, xAc, xBr, xBc);
     }
-    // the last block's (unused) prefetch must land before its registers are reused
+    if (kb < nkb) kblock(later, updc, tu, fwdc, tf, kb, td, wB, mB, wA, mA, xBr, xBc, xAr, xAc);
+    // the last blocks' (unused) prefetches and stores land before their registers are reused
     asm volatile("s_waitcnt vmcnt(0)"
                  : "+v"(wA[0]), "+v"(wA[1]), "+v"(wA[2]), "+v"(wA[3]), "+v"(mA), "+v"(wB[0]), "+v"(wB[1]),
                    "+v"(wB[2]), "+v"(wB[3]), "+v"(mB)
                  :
                  : "memory");
+#pragma unroll
+    for (int u = 0; u < XU; ++u) asm volatile("" : "+v"(xAr[u]), "+v"(xAc[u]), "+v"(xBr[u]), "+v"(xBc[u]));
   };
   const std::true_type on{};
   const std::false_type off{};

@@ -101,7 +101,7 @@ struct Fused2Args {
   int Kp, Hp, C, B, Bp, T;       // input width, hidden width (128|256), classes, batch, padded batch, steps/epoch
   int64_t n;                     // training rows
   int t0, t1;
-  const uint16_t* xrows;         // [T][Bp][Kp] bf16 bits
+  const uint16_t* xrows;         // [T][Kp/32][Bp][32] bf16 bits (block-major rows)
   const uint16_t* xcols;         // [T][Kp][Bp]
   const int32_t* labels;         // [T][Bp]
   float* W1; float* b1; const uint32_t* m1;   // register image (see launch_w1_image), [P][Hp], [P][Kp/32][Hp]
@@ -117,14 +117,16 @@ struct GatherArgs {
   const uint32_t* perm;          // [n] (nullable: identity)
   int64_t n;
   int d0, Kp, B, Bp, T;          // T = steps (row blocks)
+  int blocked;                   // rows block-major, [T][Kp/32][Bp][32], instead of [T][Bp][Kp]
   void* rows;                    // [T][Bp][Kp] S
   int32_t* labels;               // [T][Bp]
 };
 
 struct TransposeArgs {
-  const void* src;               // [T][Bp][Kp] S
+  const void* src;               // [T][Bp][Kp] S, or [T][Kp/32][Bp][32] when blocked
   void* dst;                     // [T][Kp][Bp] S
   int Kp, Bp, T;
+  int blocked;
 };
 
 // ---------------------------------------------------------------- launchers

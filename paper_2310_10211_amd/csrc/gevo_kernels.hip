@@ -601,11 +601,12 @@ __global__ __launch_bounds__(256) void k_gather(GatherArgs a) {
   const int64_t r = (int64_t)t * a.B + b;
   const bool valid = b < a.B && r < a.n;
   const int64_t src = valid ? (a.perm ? (int64_t)a.perm[r] : r) : 0;
-  S* out = reinterpret_cast<S*>(a.rows) + ((size_t)t * a.Bp + b) * a.Kp;
+  S* rows = reinterpret_cast<S*>(a.rows) + (size_t)t * a.Bp * a.Kp;
   const float* x = a.X + src * a.d0;
   for (int k = threadIdx.x; k < a.Kp; k += blockDim.x) {
     const float xv = (valid && k < a.d0) ? x[k] : 0.0f;
-    out[k] = O::from_f32(xv);
+    const size_t at = a.blocked ? ((size_t)(k >> 5) * a.Bp + b) * 32 + (k & 31) : (size_t)b * a.Kp + k;
+    rows[at] = O::from_f32(xv);
   }
   if (threadIdx.x == 0) a.labels[(size_t)t * a.Bp + b] = valid ? a.y[src] : -1;
 }
@@ -618,7 +619,10 @@ __global__ __launch_bounds__(256) void k_transpose(TransposeArgs a) {
   const S* src = reinterpret_cast<const S*>(a.src) + (size_t)t * a.Bp * a.Kp;
   S* dst = reinterpret_cast<S*>(a.dst) + (size_t)t * a.Kp * a.Bp;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) tile[ty + 8 * i][tx] = src[(size_t)(b0 + ty + 8 * i) * a.Kp + k0 + tx];
+  for (int i = 0; i < 4; ++i) {
+    const int b = b0 + ty + 8 * i;
+    tile[ty + 8 * i][tx] = src[a.blocked ? ((size_t)blockIdx.x * a.Bp + b) * 32 + tx : (size_t)b * a.Kp + k0 + tx];
+  }
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < 4; ++i) dst[(size_t)(k0 + ty + 8 * i) * a.Bp + b0 + tx] = tile[tx][ty + 8 * i];
