@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <new>
+#include <type_traits>
 #include <vector>
 
 #include "gevo.h"
@@ -302,6 +303,15 @@ gevo_status forward_hidden(gevo_pop* p, const S* arows0, size_t ar0_vs, int R, i
       if (q.Wt) a.Wt = at<S>(p, q.Wt);
     }
     if (a.Kp % kTile || a.Np % kTile || a.R % kTile || a.R <= 0) return GEVO_E_SHAPE;
+    if constexpr (std::is_same<S, uint16_t>::value) {
+      if (predict && fwd_gemm_supported(a.Kp, a.Np, a.R)) {      // plain per-variant GEMM, no update
+        FwdGemmArgs g{};
+        g.A = a.Arows; g.a_vs = a.ar_vs; g.Wm = a.Wm; g.bias = a.bias; g.O = a.Orows; g.o_vs = a.or_vs;
+        g.Kp = a.Kp; g.Np = a.Np; g.R = a.R; g.P = y.P;
+        HIP_TRY(launch_fwd_gemm(g, p->stream, prof(p, GEVO_KERNEL_LAYER_FWD)));
+        continue;
+      }
+    }
     HIP_TRY(launch_layer<S>(a, y.P, p->stream, prof(p, GEVO_KERNEL_LAYER_FWD)));
   }
   return GEVO_OK;

@@ -60,6 +60,15 @@ struct LayerArgs {
   S* Wt;                         // [v][Kp][Np] operand copy of W, transposed (nullable)
 };
 
+// bf16 forward of a hidden layer over prediction rows (no update)
+struct FwdGemmArgs {
+  const uint16_t* A; size_t a_vs;   // [v][R][Kp] input rows (a_vs = 0: shared by all variants)
+  const float* Wm;                  // [P][Kp/32][Np][32] fp32 master (k-blocked)
+  const float* bias;                // [P][Np]
+  uint16_t* O; size_t o_vs;         // [v][R][Np] relu output rows
+  int Kp, Np, R, P;
+};
+
 template <typename S>
 struct OutArgs {
   int Kp;                        // padded width of the last hidden layer (input of the output layer)
@@ -151,6 +160,8 @@ hipError_t launch_w1_image(const float* src, float* dst, int P, int Kp, int Hp, 
 hipError_t launch_mask_block_major(const uint32_t* src, uint32_t* dst, int P, int Kp, int Hp, hipStream_t s,
                                    const LaunchEv& ev);
 hipError_t launch_bf16_check(unsigned long long* counts, hipStream_t s);   // counts zeroed by the caller
+bool fwd_gemm_supported(int Kp, int Np, int R);   // Kp % 32, Np % 128, R % 256
+hipError_t launch_fwd_gemm(const FwdGemmArgs& a, hipStream_t s, const LaunchEv& ev);
 size_t fused2_lds_bytes(int hp, int bp);     // 0 when the shape has no fused instantiation
 hipError_t launch_reduce_partials(const double* part_ce, const unsigned int* part_corr, int P, int n_chunks,
                                   double* ce_out, unsigned long long* corr_out, hipStream_t s, const LaunchEv& ev);
