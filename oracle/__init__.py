@@ -85,6 +85,7 @@ def lib():
                                              f32p, f32p, u32p]
             L.or_variant_init.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int, u32p, ctypes.c_uint32,
                                           ctypes.c_int, f64p, ctypes.c_float, f64p, u8p]
+            L.or_genome_mask.argtypes = [ctypes.c_uint64, ctypes.c_int, u32p, ctypes.c_uint32, u32p, u32p, u8p]
             L.or_permutation.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32, u32p]
             L.or_permutation.restype = None
             L.or_batch_grad.argtypes = [ctypes.c_int, ctypes.c_int, u32p, f64p, f32p, i32p, ctypes.c_uint32,
@@ -189,6 +190,20 @@ def variant_init(seed, v, dims, thresh, init_kind=0, base=None, noise_std=0.0):
                                _p(mask, ctypes.c_uint8))
     assert rc == 0
     return params, mask
+
+
+def genome_mask(seed, dims, edit_ids, thresholds):
+    """Mask (uint8 over weights, canonical order) of an individual whose pruning
+    edits are (edit_ids[i], thresholds[i]): a weight is kept when every edit keeps it."""
+    d = _dims(dims)
+    ids = np.ascontiguousarray(np.asarray(edit_ids, dtype=np.uint32))
+    th = np.ascontiguousarray(np.asarray(thresholds, dtype=np.uint32))
+    assert ids.shape == th.shape
+    mask = np.zeros(weight_count(dims), dtype=np.uint8)
+    rc = lib().or_genome_mask(ctypes.c_uint64(seed), len(d) - 1, _p(d, ctypes.c_uint32), len(ids),
+                              _p(ids, ctypes.c_uint32), _p(th, ctypes.c_uint32), _p(mask, ctypes.c_uint8))
+    assert rc == 0
+    return mask
 
 
 def permutation(seed, epoch, n):

@@ -233,6 +233,36 @@ int or_variant_init(uint64_t seed, uint32_t v, int L, const uint32_t* dims,
   return 0;
 }
 
+/* Mask of an individual whose pruning edits are (edit_id[i], thresh[i]),
+ * i < n_edits.  An edit keeps weight (layer l, flat index e = n*din + k) when
+ * the top 24 bits of its mask draw, taken with the edit id where the initial
+ * population uses the variant index, fall below its threshold; a weight is
+ * kept when every edit keeps it (the edits of an individual apply in sequence
+ * to the original program, section 4.2; their effect is pruning, abstract).
+ * No edit keeps everything.  A single edit (v, T_v) gives the initial mask of
+ * variant v (or_variant_init). */
+int or_genome_mask(uint64_t seed, int L, const uint32_t* dims, uint32_t n_edits, const uint32_t* edit_id,
+                   const uint32_t* thresh, uint8_t* mask) {
+  if (L < 1 || L > OR_MAX_LAYERS) return -1;
+  for (int l = 1; l <= L; ++l) {
+    uint32_t din = dims[l - 1], dout = dims[l];
+    uint8_t* M = mask + m_off(dims, l);
+    for (uint32_t k = 0; k < din; ++k) {
+      for (uint32_t n = 0; n < dout; ++n) {
+        uint64_t e = (uint64_t)n * din + k;
+        int keep = 1;
+        for (uint32_t i = 0; i < n_edits; ++i) {
+          uint32_t rm = draw_word(seed, (uint32_t)(e >> 2), (uint32_t)(l - 1), edit_id[i], OR_STREAM_MASK,
+                                  (uint32_t)(e & 3));
+          if ((rm >> 8) >= thresh[i]) keep = 0;
+        }
+        M[(size_t)k * dout + n] = (uint8_t)keep;
+      }
+    }
+  }
+  return 0;
+}
+
 /* Per-epoch data order, shared by all variants: Fisher-Yates from the end,
  * swap index j = floor(r * (i+1) / 2^32) with r a 32-bit Philox word
  * (multiply-shift, no rejection). */
