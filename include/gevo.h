@@ -193,6 +193,95 @@ gevo_status gevo_pop_epoch_labels(gevo_pop* pop, int32_t* labels_out, int64_t n)
 /* Host-side data order of epoch `epoch` over n rows (definition above). */
 gevo_status gevo_epoch_permutation(uint64_t seed, uint32_t epoch, uint32_t n, uint32_t* out);
 
+/*
+ * Search step (paper section 4).  GEVO-ML evolves individuals that are lists
+ * of edits to the original program (patch representation, section 4.2):
+ * each initial individual gets three random mutations (section 4), crossover
+ * is one-point messy crossover (section 4.2), and selection keeps the best 16
+ * unchanged and fills the rest by tournament selection among NSGA-II ranked
+ * individuals (section 4.4).  Here an edit is one of the two effects the
+ * paper attributes to its evolved edits: a changed learning rate (section 6.2)
+ * or pruned weights (abstract).
+ *
+ * Every random choice is a Philox4x32-10 draw (key = seed as above), word w of
+ * Philox((c0, c1, c2, stream)):
+ *   tournament j of generation g:       (j, g, 0, 7), words 0 and 1 pick the two
+ *                                       contestants (multiply-shift onto [0, n))
+ *   crossover of children 2i, 2i+1:     (0, g, 2i, 8) word 0 decides (u24 < cxpb),
+ *                                       word 1 the cut; (1 + t/4, g, 2i, 8) word
+ *                                       t%4 the Fisher-Yates draw for position t
+ *   mutation of child i, generation g:  (0, g, i, 9) word 0 decides (u24 < mutpb);
+ *                                       the edit from words 1 and 2 of (1, g, i, 9)
+ *   edit j of initial individual i:     words 1 and 2 of (j, 0, i, 9)
+ * where u24 = (word >> 8) * 2^-24.  A drawn edit is, with equal odds (word 1
+ * u24 < 1/2), a learning-rate factor exp(ln(1/2) + u ln 4) (u from word 2,
+ * computed in binary64, rounded to binary32) or pruning at density
+ * rho = rho_lo + u (1 - rho_lo), threshold round-half-even(rho 2^24).
+ */
+typedef enum { GEVO_EDIT_LR = 0, GEVO_EDIT_PRUNE = 1 } gevo_edit_kind;
+typedef struct {
+  uint32_t kind;    /* gevo_edit_kind */
+  uint32_t id;      /* pruning: the draw id of its mask (see gevo_pop_set_genomes) */
+  uint32_t value;   /* GEVO_EDIT_LR: bits of the binary32 factor; GEVO_EDIT_PRUNE: keep threshold (<= 2^24) */
+} gevo_edit;
+
+/* NSGA-II ranking (Deb et al., IEEE TEC 2002) of n points with m objectives,
+ * all minimised, objs row-major [n][m], no NaN.  rank[i] = front index (0 =
+ * non-dominated; a dominates b when no objective is larger and one is
+ * smaller); crowding[i] = sum over objectives k of (f_k of the next point -
+ * f_k of the previous point) / (max - min of f_k) over i's front, neighbours
+ * ordered by f_k then by index, the first and last point of every objective
+ * getting +infinity, terms added in objective order in binary64.  Host
+ * arrays; GEVO_E_ARG for a null pointer, m == 0 or a NaN objective. */
+gevo_status gevo_nsga2_rank(uint32_t n, uint32_t m, const double* objs, uint32_t* rank, double* crowding);
+
+/* Selection of generation gen (section 4.4): out[0 .. n_elite) are the
+ * n_elite best points by the crowded comparison (lower rank, then larger
+ * crowding, then lower index), best first; out[n_elite .. n_select) are
+ * binary-tournament winners under the same comparison (draws above).  Host
+ * arrays; GEVO_E_ARG unless n_elite <= n_select, n_elite <= n and n > 0 (when
+ * n_select > 0). */
+gevo_status gevo_nsga2_select(uint32_t n, const uint32_t* rank, const double* crowding, uint32_t n_elite,
+                              uint32_t n_select, uint64_t seed, uint32_t gen, uint32_t* out);
+
+/* Initial population (section 4): individual i gets n_mut drawn edits, edit j
+ * with id id_base + n_mut i + j, written to out[n_mut i + j] (host array of
+ * n * n_mut edits).  GEVO_E_ARG for a null pointer or rho_lo outside [0, 1]. */
+gevo_status gevo_genomes_initial(uint32_t n, uint32_t n_mut, uint64_t seed, double rho_lo, uint32_t id_base,
+                                 gevo_edit* out);
+
+/* Children of generation gen >= 1 from n parents (the tournament winners);
+ * parent i's edits are edits[offsets[i] .. offsets[i+1]).  Pairs (2i, 2i+1)
+ * are recombined with probability cxpb by one-point messy crossover:
+ * concatenate both lists, shuffle (Fisher-Yates from the last position), cut
+ * at a drawn point in [0, length], each child keeping at most max_edits; an
+ * odd last parent is copied.  Then child i gets one drawn edit with id
+ * id_base + i, with probability mutpb, when it holds fewer than max_edits.
+ * Writes out_offsets[n + 1] and the edits (host arrays); GEVO_E_ARG for bad
+ * offsets, gen == 0, probabilities outside [0, 1] or out_capacity below
+ * offsets[n] + n. */
+gevo_status gevo_genomes_breed(uint32_t n, const uint32_t* offsets, const gevo_edit* edits, uint64_t seed,
+                               uint32_t gen, double cxpb, double mutpb, double rho_lo, uint32_t id_base,
+                               uint32_t max_edits, uint32_t* out_offsets, gevo_edit* out_edits,
+                               size_t out_capacity);
+
+/* Rebuild the population from genomes, variant v from edits[offsets[v] ..
+ * offsets[v+1]) (host arrays, offsets[P] entries after the first).  Learning
+ * rate: lr_base times the GEVO_EDIT_LR factors in order, each product rounded
+ * to binary32.  Mask: a weight is kept when every GEVO_EDIT_PRUNE edit keeps
+ * it, edit (id, threshold) keeping weight (layer l, index e = n d_{l-1} + k)
+ * when the top 24 bits of the mask draw of initialisation, taken with id in
+ * place of the variant index, are below the threshold (one edit (v, T_v)
+ * reproduces variant v of gevo_pop_init).  Weights are the initial weights of
+ * gevo_pop_init under the new mask, biases as initialised; the next training
+ * epoch is epoch 0 again.  Writes lr_out[P] and density_out[P] (the product
+ * of the edits' keep fractions threshold / 2^24, binary64, in order) when not
+ * null.  At most 64 pruning edits per variant.  Synchronous; GEVO_E_ARG for
+ * bad offsets, kinds, thresholds above 2^24, a non-finite or non-positive
+ * learning rate or too many pruning edits, GEVO_E_ORDER during an epoch. */
+gevo_status gevo_pop_set_genomes(gevo_pop* pop, float lr_base, const uint32_t* offsets, const gevo_edit* edits,
+                                 float* lr_out, double* density_out);
+
 /* Self-check of the binary32 -> bfloat16 rounding that the bf16 kernels use
  * for every operand they round (weights from the master, activations,
  * gradients; round-to-nearest-even, see Numerics).  The kernels convert with

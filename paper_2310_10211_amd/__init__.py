@@ -20,7 +20,8 @@ import os
 import numpy as np
 
 __all__ = ["Population", "lib", "epoch_permutation", "check_bf16_rounding", "GevoError", "config_struct",
-           "workspace_bytes"]
+           "workspace_bytes", "nsga2_rank", "nsga2_select", "genomes_initial", "genomes_breed", "EDIT_LR",
+           "EDIT_PRUNE"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgevo.so")
@@ -35,7 +36,8 @@ EXPORTED = [
     "gevo_pop_steps_per_epoch", "gevo_pop_predict", "gevo_pop_scores", "gevo_pop_last_time",
     "gevo_pop_export", "gevo_pop_import", "gevo_pop_epoch_labels", "gevo_epoch_permutation",
     "gevo_pop_set_profiling", "gevo_pop_kernel_stats", "gevo_pop_destroy", "gevo_status_str",
-    "gevo_check_bf16_rounding",
+    "gevo_check_bf16_rounding", "gevo_nsga2_rank", "gevo_nsga2_select", "gevo_genomes_initial",
+    "gevo_genomes_breed", "gevo_pop_set_genomes",
 ]
 KERNEL_KINDS = ["init", "gather", "layer_train", "layer_fwd", "out_train", "out_predict", "bwd", "aux",
                 "fused_train"]
@@ -43,6 +45,13 @@ KERNEL_KINDS = ["init", "gather", "layer_train", "layer_fwd", "out_train", "out_
 
 class GevoError(RuntimeError):
     pass
+
+
+class GevoEdit(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_uint32), ("id", ctypes.c_uint32), ("value", ctypes.c_uint32)]
+
+
+EDIT_LR, EDIT_PRUNE = 0, 1
 
 
 class GevoPopConfig(ctypes.Structure):
@@ -97,6 +106,14 @@ def lib():
         L.gevo_pop_kernel_stats.argtypes = [vp, ctypes.c_int, ctypes.POINTER(ctypes.c_double),
                                             ctypes.POINTER(ctypes.c_uint64)]
         L.gevo_check_bf16_rounding.argtypes = [vp, vp]
+        u32p, f64p = ctypes.POINTER(u32), ctypes.POINTER(ctypes.c_double)
+        editp = ctypes.POINTER(GevoEdit)
+        L.gevo_nsga2_rank.argtypes = [u32, u32, f64p, u32p, f64p]
+        L.gevo_nsga2_select.argtypes = [u32, u32p, f64p, u32, u32, ctypes.c_uint64, u32, u32p]
+        L.gevo_genomes_initial.argtypes = [u32, u32, ctypes.c_uint64, ctypes.c_double, u32, editp]
+        L.gevo_genomes_breed.argtypes = [u32, u32p, editp, ctypes.c_uint64, u32, ctypes.c_double, ctypes.c_double,
+                                         ctypes.c_double, u32, u32, u32p, editp, ctypes.c_size_t]
+        L.gevo_pop_set_genomes.argtypes = [vp, ctypes.c_float, u32p, editp, f32p, f64p]
         L.gevo_pop_destroy.argtypes = [vp]
         L.gevo_pop_destroy.restype = None
         L.gevo_status_str.argtypes = [ctypes.c_int]
@@ -173,6 +190,69 @@ def check_bf16_rounding(stream=None) -> list:
     _check(lib().gevo_check_bf16_rounding(ctypes.c_void_p(st.cuda_stream), ctypes.c_void_p(counts.data_ptr())),
            "gevo_check_bf16_rounding")
     return [int(c) for c in counts.cpu()]
+
+
+def _u32p(a):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32))
+
+
+def _f64p(a):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def _pack_genomes(genomes):
+    """Flat (offsets, edits) of a list of edit lists [(kind, id, value), ...]."""
+    offsets = np.zeros(len(genomes) + 1, np.uint32)
+    flat = [e for g in genomes for e in g]
+    edits = (GevoEdit * max(len(flat), 1))()
+    for i, (kind, eid, value) in enumerate(flat):
+        edits[i].kind, edits[i].id, edits[i].value = kind, eid, value
+    offsets[1:] = np.cumsum([len(g) for g in genomes], dtype=np.uint64).astype(np.uint32)
+    return offsets, edits
+
+
+def _unpack_genomes(offsets, edits):
+    return [[(edits[i].kind, edits[i].id, edits[i].value) for i in range(int(offsets[v]), int(offsets[v + 1]))]
+            for v in range(len(offsets) - 1)]
+
+
+def nsga2_rank(objs):
+    """NSGA-II front index and crowding distance of each row of objs [n][m] (minimised)."""
+    o = np.ascontiguousarray(np.asarray(objs, np.float64))
+    n, m = o.shape
+    rank = np.zeros(n, np.uint32)
+    crowd = np.zeros(n, np.float64)
+    _check(lib().gevo_nsga2_rank(n, m, _f64p(o), _u32p(rank), _f64p(crowd)), "gevo_nsga2_rank")
+    return rank, crowd
+
+
+def nsga2_select(rank, crowding, n_elite, n_select, seed, gen):
+    """Elites (best first) followed by binary-tournament winners."""
+    r = np.ascontiguousarray(np.asarray(rank, np.uint32))
+    c = np.ascontiguousarray(np.asarray(crowding, np.float64))
+    out = np.zeros(n_select, np.uint32)
+    _check(lib().gevo_nsga2_select(len(r), _u32p(r), _f64p(c), n_elite, n_select, seed, gen, _u32p(out)),
+           "gevo_nsga2_select")
+    return [int(i) for i in out]
+
+
+def genomes_initial(n, seed, rho_lo, n_mut=3, id_base=0):
+    """n individuals with n_mut drawn edits each."""
+    edits = (GevoEdit * max(n * n_mut, 1))()
+    _check(lib().gevo_genomes_initial(n, n_mut, seed, rho_lo, id_base, edits), "gevo_genomes_initial")
+    return [[(edits[n_mut * i + j].kind, edits[n_mut * i + j].id, edits[n_mut * i + j].value) for j in range(n_mut)]
+            for i in range(n)]
+
+
+def genomes_breed(parents, seed, gen, cxpb, mutpb, rho_lo, id_base, max_edits):
+    """Children of the tournament winners (messy one-point crossover, mutation)."""
+    off, edits = _pack_genomes(parents)
+    cap = int(off[-1]) + len(parents)
+    out_off = np.zeros(len(parents) + 1, np.uint32)
+    out = (GevoEdit * max(cap, 1))()
+    _check(lib().gevo_genomes_breed(len(parents), _u32p(off), edits, seed, gen, cxpb, mutpb, rho_lo, id_base,
+                                    max_edits, _u32p(out_off), out, cap), "gevo_genomes_breed")
+    return _unpack_genomes(out_off, out)
 
 
 def param_count(dims) -> int:
@@ -279,6 +359,17 @@ class Population:
             _check(lib().gevo_pop_kernel_stats(self._h, i, ctypes.byref(ms), ctypes.byref(n)), "gevo_pop_kernel_stats")
             out[name] = (ms.value, n.value)
         return out
+
+    def set_genomes(self, genomes, lr_base):
+        """Rebuild every variant from its edit list; returns (learning rates,
+        expected kept fractions).  Training restarts at epoch 0."""
+        assert len(genomes) == self.P
+        off, edits = _pack_genomes(genomes)
+        lr = np.zeros(self.P, np.float32)
+        dens = np.zeros(self.P, np.float64)
+        _check(lib().gevo_pop_set_genomes(self._h, lr_base, _u32p(off), edits, _fp(lr), _f64p(dens)),
+               "gevo_pop_set_genomes")
+        return lr, dens
 
     def reinit(self):
         """Destroy the handle and create a fresh population on the same workspace

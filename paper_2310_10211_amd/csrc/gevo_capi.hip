@@ -5,6 +5,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <cmath>
 #include <new>
 #include <type_traits>
 #include <vector>
@@ -34,6 +35,7 @@ struct Layout {
   int n_test_pad = 0, n_chunks_test = 0;
   size_t elt = 4;
   LayerLay lay[GEVO_MAX_LAYERS];
+  size_t prune_off = 0, prune_id = 0, prune_th = 0;   // genome pruning edits (gevo_pop_set_genomes)
   size_t lr = 0, thresh = 0, train_ce = 0, train_corr = 0, test_ce = 0, test_corr = 0, part_ce = 0,
          part_corr = 0, xrows = 0, xcols = 0, yep = 0, xte = 0, yte = 0, perm = 0;
   size_t w1img = 0, m1blk = 0;                    // fused training: W1 register image, block-major W1 mask
@@ -126,6 +128,9 @@ gevo_status make_layout(const gevo_pop_config* c, Layout* o) {
   }
   y.lr = take(P * 4);
   y.thresh = take(P * 4);
+  y.prune_off = take((P + 1) * 4);
+  y.prune_id = take(P * (size_t)kMaxGenomePrunes * 4);
+  y.prune_th = take(P * (size_t)kMaxGenomePrunes * 4);
   y.train_ce = take(P * 8);
   y.train_corr = take(P * 8);
   y.test_ce = take(P * 8);
@@ -211,6 +216,7 @@ struct gevo_pop {
   bool timing_pending = false;
   double last_s = 0.0;
   bool predicted = false;
+  bool has_base = false;    // initial weights come from the caller's base model
   // fused training keeps W1 in its own register image: which copy is current
   bool img_valid = false;   // the image (and the block-major mask) match the k-blocked master
   bool blk_stale = false;   // training has advanced the image past the k-blocked master
@@ -589,6 +595,38 @@ gevo_status gevo_check_bf16_rounding(void* hip_stream, uint64_t* d_counts) {
   return GEVO_OK;
 }
 
+// weights, biases and masks of every layer from the seed (and the caller's
+// base model, when given); genomes: masks from the pruning-edit lists
+static gevo_status init_layers(gevo_pop* p, bool genomes) {
+  const Layout& y = p->y;
+  const gevo_pop_config* cfg = &p->cfg;
+  for (int l = 0; l < y.L; ++l) {
+    const LayerLay& q = y.lay[l];
+    InitArgs a{};
+    a.P = y.P; a.l_index = l; a.K = q.K; a.N = q.N; a.Kp = q.Kp; a.Np = q.Np;
+    a.seed = cfg->seed;
+    a.init_kind = cfg->init == GEVO_INIT_BASE_NOISE ? 1 : 0;
+    a.xavier_a = (float)sqrt(6.0 / ((double)q.K + (double)q.N));
+    a.noise_std = cfg->noise_rel_std;
+    if (p->has_base) {
+      a.base_w = reinterpret_cast<const float*>(p->ws + q.base_w);
+      a.base_b = reinterpret_cast<const float*>(p->ws + q.base_b);
+    }
+    a.thresh = reinterpret_cast<const uint32_t*>(p->ws + y.thresh);
+    if (genomes) {
+      a.prune_off = reinterpret_cast<const uint32_t*>(p->ws + y.prune_off);
+      a.prune_id = reinterpret_cast<const uint32_t*>(p->ws + y.prune_id);
+      a.prune_th = reinterpret_cast<const uint32_t*>(p->ws + y.prune_th);
+    }
+    a.Wm = reinterpret_cast<float*>(p->ws + q.Wm);
+    a.bias = reinterpret_cast<float*>(p->ws + q.bias);
+    a.mask = reinterpret_cast<uint32_t*>(p->ws + q.mask);
+    if (q.Kp % kTile || q.Np % kTile) return GEVO_E_SHAPE;
+    if (launch_init(a, p->stream, LaunchEv{}) != hipSuccess) return GEVO_E_HIP;
+  }
+  return GEVO_OK;
+}
+
 gevo_status gevo_pop_init(const gevo_pop_config* cfg, void* d_ws, size_t ws_bytes, const float* d_train_x,
                           const int32_t* d_train_y, const float* d_test_x, const int32_t* d_test_y,
                           void* hip_stream, gevo_pop** out) {
@@ -661,24 +699,10 @@ gevo_status gevo_pop_init(const gevo_pop_config* cfg, void* d_ws, size_t ws_byte
         return fail(GEVO_E_HIP);
     }
   }
-  for (int l = 0; l < y.L; ++l) {
-    const LayerLay& q = y.lay[l];
-    InitArgs a{};
-    a.P = P; a.l_index = l; a.K = q.K; a.N = q.N; a.Kp = q.Kp; a.Np = q.Np;
-    a.seed = cfg->seed;
-    a.init_kind = cfg->init == GEVO_INIT_BASE_NOISE ? 1 : 0;
-    a.xavier_a = (float)sqrt(6.0 / ((double)q.K + (double)q.N));
-    a.noise_std = cfg->noise_rel_std;
-    if (cfg->init == GEVO_INIT_BASE_NOISE && cfg->base_params) {
-      a.base_w = reinterpret_cast<const float*>(p->ws + q.base_w);
-      a.base_b = reinterpret_cast<const float*>(p->ws + q.base_b);
-    }
-    a.thresh = reinterpret_cast<const uint32_t*>(p->ws + y.thresh);
-    a.Wm = reinterpret_cast<float*>(p->ws + q.Wm);
-    a.bias = reinterpret_cast<float*>(p->ws + q.bias);
-    a.mask = reinterpret_cast<uint32_t*>(p->ws + q.mask);
-    if (q.Kp % kTile || q.Np % kTile) return fail(GEVO_E_SHAPE);
-    if (launch_init(a, s, LaunchEv{}) != hipSuccess) return fail(GEVO_E_HIP);
+  p->has_base = cfg->init == GEVO_INIT_BASE_NOISE && cfg->base_params;
+  {
+    const gevo_status st = init_layers(p, false);
+    if (st != GEVO_OK) return fail(st);
   }
   // test split converted once to the operand type, padded to whole chunks
   GatherArgs g{};
@@ -696,6 +720,76 @@ gevo_status gevo_pop_init(const gevo_pop_config* cfg, void* d_ws, size_t ws_byte
     if (hipStreamSynchronize(s) != hipSuccess) return fail(GEVO_E_HIP);   // host staging vectors die here
   }
   *out = p;
+  return GEVO_OK;
+}
+
+gevo_status gevo_pop_set_genomes(gevo_pop* p, float lr_base, const uint32_t* offsets, const gevo_edit* edits,
+                                 float* lr_out, double* density_out) {
+  if (!p || !offsets || offsets[0] != 0) return GEVO_E_ARG;
+  if (p->open_epoch >= 0) return GEVO_E_ORDER;
+  const Layout& y = p->y;
+  const int P = y.P;
+  for (int v = 0; v < P; ++v)
+    if (offsets[v + 1] < offsets[v]) return GEVO_E_ARG;
+  if (offsets[P] > 0 && !edits) return GEVO_E_ARG;
+  std::vector<float> lr(P);
+  std::vector<double> dens(P);
+  std::vector<uint32_t> off(P + 1, 0), ids, th;
+  for (int v = 0; v < P; ++v) {
+    float r = lr_base;
+    double d = 1.0;
+    uint32_t np = 0;
+    for (uint32_t i = offsets[v]; i < offsets[v + 1]; ++i) {
+      const gevo_edit& e = edits[i];
+      if (e.kind == GEVO_EDIT_LR) {
+        float f;
+        memcpy(&f, &e.value, 4);
+        r = r * f;                               // binary32 product, in order
+      } else if (e.kind == GEVO_EDIT_PRUNE) {
+        if (e.value > (1u << 24) || ++np > kMaxGenomePrunes) return GEVO_E_ARG;
+        ids.push_back(e.id);
+        th.push_back(e.value);
+        d = d * ((double)e.value / 16777216.0);
+      } else {
+        return GEVO_E_ARG;
+      }
+    }
+    if (!(r > 0.0f) || !std::isfinite(r)) return GEVO_E_ARG;
+    lr[v] = r;
+    dens[v] = d;
+    off[v + 1] = (uint32_t)ids.size();
+  }
+  hipStream_t s = p->stream;
+  HIP_TRY(hipStreamSynchronize(s));              // nothing may still read the state being replaced
+  HIP_TRY(hipMemcpy(p->ws + y.lr, lr.data(), (size_t)P * 4, hipMemcpyHostToDevice));
+  HIP_TRY(hipMemcpy(p->ws + y.prune_off, off.data(), off.size() * 4, hipMemcpyHostToDevice));
+  if (!ids.empty()) {
+    HIP_TRY(hipMemcpy(p->ws + y.prune_id, ids.data(), ids.size() * 4, hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(p->ws + y.prune_th, th.data(), th.size() * 4, hipMemcpyHostToDevice));
+  }
+  const gevo_status st = init_layers(p, true);
+  if (st != GEVO_OK) return st;
+  HIP_TRY(launch_zero_bytes(p->ws + y.train_ce, (size_t)P * 8, s, LaunchEv{}));
+  HIP_TRY(launch_zero_bytes(p->ws + y.train_corr, (size_t)P * 8, s, LaunchEv{}));
+  HIP_TRY(launch_zero_bytes(p->ws + y.test_ce, (size_t)P * 8, s, LaunchEv{}));
+  HIP_TRY(launch_zero_bytes(p->ws + y.test_corr, (size_t)P * 8, s, LaunchEv{}));
+  HIP_TRY(hipStreamSynchronize(s));
+  for (int v = 0; v < P; ++v) {
+    p->lr[v] = lr[v];
+    p->dens[v] = (float)dens[v];
+    p->thresh[v] = 0;
+    if (lr_out) lr_out[v] = lr[v];
+    if (density_out) density_out[v] = dens[v];
+  }
+  p->expected_epoch = 0;
+  p->open_epoch = -1;
+  p->last_epoch = -1;
+  p->next_step = 0;
+  p->rows_done = 0;
+  p->predicted = false;
+  p->timing_pending = false;
+  p->img_valid = false;                          // the fused kernel's copy of the hidden layer is stale
+  p->blk_stale = false;
   return GEVO_OK;
 }
 

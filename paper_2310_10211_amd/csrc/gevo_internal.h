@@ -19,7 +19,9 @@ constexpr size_t kLayerLds = 76 * 1024;   // dynamic LDS per hidden-layer workgr
 
 // Philox stream ids (counter word 3)
 constexpr uint32_t kStreamLr = 1, kStreamDens = 2, kStreamMask = 3, kStreamInit = 4,
-                   kStreamNoise = 5, kStreamPerm = 6;
+                   kStreamNoise = 5, kStreamPerm = 6, kStreamSelect = 7, kStreamCross = 8,
+                   kStreamMut = 9;
+constexpr uint32_t kMaxGenomePrunes = 64;   // pruning edits per variant held on the device
 
 inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
 
@@ -35,6 +37,12 @@ struct InitArgs {
   const float* base_w;           // optional base weights, device, [Np][Kp] padded (layer slice)
   const float* base_b;           // optional base biases, device, [Np]
   const uint32_t* thresh;        // [P] mask thresholds
+  // optional genomes: variant v keeps a weight only when each of its pruning
+  // edits i in [prune_off[v], prune_off[v+1]) keeps it, drawing with
+  // prune_id[i] where the initial population draws with v, against prune_th[i]
+  const uint32_t* prune_off;     // [P+1] (null: one edit per variant, (v, thresh[v]))
+  const uint32_t* prune_id;
+  const uint32_t* prune_th;
   float* Wm;                     // [P][Kp/32][Np][32] (k-blocked)
   float* bias;                   // [P][Np]
   uint32_t* mask;                // [P][Np][Kp/32] row words

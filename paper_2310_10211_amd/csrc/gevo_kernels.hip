@@ -49,11 +49,20 @@ __global__ __launch_bounds__(256) void k_init(InitArgs a) {
         float w = 0.0f;
         if (n < a.N && k < a.K) {
           const uint64_t e = (uint64_t)n * (uint64_t)a.K + (uint64_t)k;
-          if ((e >> 2) != blk_m) {
-            blk_m = e >> 2;
-            rm = philox(make_uint4((uint32_t)blk_m, (uint32_t)a.l_index, (uint32_t)v, kStreamMask), key);
+          bool keep;
+          if (a.prune_off) {
+            keep = true;
+            for (uint32_t q = a.prune_off[v]; q < a.prune_off[v + 1]; ++q) {
+              const uint4 r = philox(make_uint4((uint32_t)(e >> 2), (uint32_t)a.l_index, a.prune_id[q], kStreamMask), key);
+              if ((pick(r, (uint32_t)(e & 3)) >> 8) >= a.prune_th[q]) keep = false;
+            }
+          } else {
+            if ((e >> 2) != blk_m) {
+              blk_m = e >> 2;
+              rm = philox(make_uint4((uint32_t)blk_m, (uint32_t)a.l_index, (uint32_t)v, kStreamMask), key);
+            }
+            keep = (pick(rm, (uint32_t)(e & 3)) >> 8) < th;
           }
-          const bool keep = (pick(rm, (uint32_t)(e & 3)) >> 8) < th;
           if (a.base_w) {
             w = a.base_w[(size_t)n * a.Kp + k];
           } else {
