@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU-oracle sample")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="time without per-kernel events")
+    ap.add_argument("--search", type=int, default=0, metavar="G",
+                    help="time G generations of the search loop on this workload instead")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy 3 times (reference for HBM counters) and exit")
     ap.add_argument("--traffic-from", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
@@ -285,6 +287,10 @@ def main():
     pop = g.Population(cfg, data["x_train"], data["y_train"], data["x_test"], data["y_test"], device=dev)
     torch.cuda.synchronize()
 
+    if args.search:
+        search_bench(pop, cfg, args.search)
+        return
+
     def step(profile):
         pop.reinit()
         if profile:
@@ -371,6 +377,52 @@ def main():
         "kernel_ms_per_step": kernel_ms,
         "roofline": roofline,
         "cpu_baseline": cpu,
+    }
+    print(json.dumps(out))
+
+
+def search_bench(pop, cfg, generations):
+    """Generations of the GEVO-ML search on one population: each generation is
+    a genome rebuild, a full fitness evaluation (all epochs, prediction,
+    scores) and the host's ranking, selection and breeding."""
+    import torch
+    import paper_2310_10211_amd as g
+    from paper_2310_10211_amd.search import Search
+    lr_base = 0.05
+    s = Search(pop, lr_base=lr_base, seed=cfg["seed"], epochs=cfg["epochs"], n_elite=min(16, pop.P))
+    s.start()                                                  # generation 0 (untimed)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(generations):
+        s.step()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    cur = s.history[-1]
+    h0 = time.perf_counter()
+    reps = 10
+    for r in range(reps):                                      # the host part of one step, alone
+        rank, crowd = g.nsga2_rank(cur.objectives)
+        chosen = g.nsga2_select(rank, crowd, s.n_elite, pop.P, s.seed, 1 + r)
+        g.genomes_breed([cur.genomes[i] for i in chosen[s.n_elite:]], s.seed, 1 + r, s.cxpb, s.mutpb, s.rho_lo,
+                        10**6, s.max_edits)
+    host_ms = (time.perf_counter() - h0) / reps * 1e3
+    front = Search.front(cur)
+    out = {
+        "metric": "search generations/s (genome rebuild + fitness evaluation + NSGA-II step)",
+        "value": round(generations / dt, 4),
+        "unit": "generations/s",
+        "n_gpus": 1,
+        "generations": generations,
+        "ms_per_generation": round(dt / generations * 1e3, 3),
+        "host_select_breed_ms": round(host_ms, 3),
+        "higher_is_better": True,
+        "data": "synthetic",
+        "config": {"workload": cfg["name"], "P": pop.P, "dims": cfg["dims"], "batch": cfg["batch"],
+                   "epochs": cfg["epochs"], "lr_base": lr_base, "n_elite": s.n_elite, "cxpb": s.cxpb,
+                   "mutpb": s.mutpb, "rho_lo": s.rho_lo},
+        "front": [{"train_error": round(float(cur.objectives[i][0]), 5),
+                   "kept_fraction": round(float(cur.objectives[i][1]), 5),
+                   "test_error": round(float(cur.test_error[i]), 5), "lr": float(cur.lr[i])} for i in front[:8]],
     }
     print(json.dumps(out))
 
