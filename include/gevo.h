@@ -282,6 +282,16 @@ gevo_status gevo_genomes_breed(uint32_t n, const uint32_t* offsets, const gevo_e
 gevo_status gevo_pop_set_genomes(gevo_pop* pop, float lr_base, const uint32_t* offsets, const gevo_edit* edits,
                                  float* lr_out, double* density_out);
 
+/* Per-element output-gradient scale (section 6.2: the mutation that improved
+ * 2fcNet replaced the scalar 1/32 multiplying the output gradient by a tensor
+ * of the gradient's shape, mostly ones).  scale is a host array [P][batch][C]
+ * (C = classes): from the next training step on, row i of every batch of
+ * variant v has G_L[i][c] = (p - onehot(y))[i][c] * scale[v][i][c] in
+ * binary32, in place of (p - onehot(y)) * fl(1/b_t); rows past a short last
+ * batch are not used.  scale == NULL restores the scalar.  Synchronous;
+ * GEVO_E_ARG for a non-finite entry, GEVO_E_ORDER during an epoch. */
+gevo_status gevo_pop_set_grad_scale(gevo_pop* pop, const float* scale);
+
 /* Self-check of the binary32 -> bfloat16 rounding that the bf16 kernels use
  * for every operand they round (weights from the master, activations,
  * gradients; round-to-nearest-even, see Numerics).  The kernels convert with

@@ -89,10 +89,10 @@ def lib():
             L.or_permutation.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32, u32p]
             L.or_permutation.restype = None
             L.or_batch_grad.argtypes = [ctypes.c_int, ctypes.c_int, u32p, f64p, f32p, i32p, ctypes.c_uint32,
-                                        ctypes.c_double, f64p, f64p, f64p, f64p]
+                                        ctypes.c_double, f32p, f64p, f64p, f64p, f64p]
             L.or_train_steps.argtypes = [ctypes.c_int, ctypes.c_int, u32p, f64p, u8p, ctypes.c_float, f32p, i32p,
                                          ctypes.c_uint32, u32p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
-                                         f64p, u64p]
+                                         f32p, f64p, u64p]
             L.or_predict.argtypes = [ctypes.c_int, ctypes.c_int, u32p, f64p, f32p, i32p, ctypes.c_uint32,
                                      f64p, u64p]
             _lib = L
@@ -213,8 +213,17 @@ def permutation(seed, epoch, n):
 
 
 # ------------------------------------------------------------------ train / eval
-def batch_grad(mode, dims, params, X, y, scale=0.0):
-    """Loss sum, gradients (canonical layout), logits and probabilities of one batch."""
+def _gscale(gscale, rows, C):
+    if gscale is None:
+        return None, None
+    g = np.ascontiguousarray(np.asarray(gscale, dtype=np.float32))
+    assert g.shape == (rows, C), g.shape
+    return g, _p(g, ctypes.c_float)
+
+
+def batch_grad(mode, dims, params, X, y, scale=0.0, gscale=None):
+    """Loss sum, gradients (canonical layout), logits and probabilities of one
+    batch; gscale ([b][C], optional) replaces the scalar gradient scale."""
     d = _dims(dims)
     X = np.ascontiguousarray(np.asarray(X, dtype=np.float32))
     y = np.ascontiguousarray(np.asarray(y, dtype=np.int32))
@@ -224,16 +233,19 @@ def batch_grad(mode, dims, params, X, y, scale=0.0):
     ce = ctypes.c_double()
     logits = np.zeros((b, int(d[-1])), dtype=np.float64)
     probs = np.zeros((b, int(d[-1])), dtype=np.float64)
+    gs, gsp = _gscale(gscale, b, int(d[-1]))
     rc = lib().or_batch_grad(_mode(mode), len(d) - 1, _p(d, ctypes.c_uint32), _p(params, ctypes.c_double),
-                             _p(X, ctypes.c_float), _p(y, ctypes.c_int32), b, float(scale),
+                             _p(X, ctypes.c_float), _p(y, ctypes.c_int32), b, float(scale), gsp,
                              _p(grads, ctypes.c_double), ctypes.byref(ce), _p(logits, ctypes.c_double),
                              _p(probs, ctypes.c_double))
     assert rc == 0, rc
     return ce.value, grads, logits, probs
 
 
-def train_steps(mode, dims, params, mask, lr, X, y, perm, batch, t0, t1):
-    """In-place SGD steps [t0, t1) on ``params``; returns (ce_sum, correct)."""
+def train_steps(mode, dims, params, mask, lr, X, y, perm, batch, t0, t1, gscale=None):
+    """In-place SGD steps [t0, t1) on ``params``; returns (ce_sum, correct).
+    gscale ([batch][C], optional): row i scales the output gradient of row i of
+    every batch in place of fl(1/b_t)."""
     d = _dims(dims)
     assert params.dtype == np.float64 and params.flags.c_contiguous
     mask = np.ascontiguousarray(mask, dtype=np.uint8)
@@ -242,9 +254,10 @@ def train_steps(mode, dims, params, mask, lr, X, y, perm, batch, t0, t1):
     perm = np.ascontiguousarray(perm, dtype=np.uint32)
     ce = ctypes.c_double(0.0)
     corr = ctypes.c_uint64(0)
+    gs, gsp = _gscale(gscale, batch, int(d[-1]))
     rc = lib().or_train_steps(_mode(mode), len(d) - 1, _p(d, ctypes.c_uint32), _p(params, ctypes.c_double),
                               _p(mask, ctypes.c_uint8), float(lr), _p(X, ctypes.c_float), _p(y, ctypes.c_int32),
-                              y.shape[0], _p(perm, ctypes.c_uint32), batch, t0, t1,
+                              y.shape[0], _p(perm, ctypes.c_uint32), batch, t0, t1, gsp,
                               ctypes.byref(ce), ctypes.byref(corr))
     assert rc == 0, rc
     return ce.value, corr.value

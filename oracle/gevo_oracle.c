@@ -323,9 +323,12 @@ static void forward(int mode, work_t* w, const double* params, uint32_t b) {
 }
 
 /* Softmax cross-entropy of one logit row; optionally the gradient
- * (p - onehot(y)) * scale.  Returns CE = log sum exp(z - m) + m - z_y. */
+ * (p - onehot(y)) * scale, or (p - onehot(y))[c] * srow[c] when a row of a
+ * gradient-scale tensor is given (the 2fcNet mutation replaces the scalar
+ * 1/32 by a tensor of the gradient's shape, section 6.2).
+ * Returns CE = log sum exp(z - m) + m - z_y. */
 static double softmax_ce(int mode, const double* z, uint32_t C, int32_t y, double scale,
-                         double* g, double* probs) {
+                         const float* srow, double* g, double* probs) {
   double m = z[0];
   for (uint32_t c = 1; c < C; ++c) if (z[c] > m) m = z[c];
   double s = 0.0;
@@ -336,7 +339,7 @@ static double softmax_ce(int mode, const double* z, uint32_t C, int32_t y, doubl
   for (uint32_t c = 0; c < C; ++c) {
     double p = rw(mode, e[c] / s);
     if (probs) probs[c] = p;
-    if (g) g[c] = rw(mode, rw(mode, p - (c == (uint32_t)y ? 1.0 : 0.0)) * scale);
+    if (g) g[c] = rw(mode, rw(mode, p - (c == (uint32_t)y ? 1.0 : 0.0)) * (srow ? (double)srow[c] : scale));
   }
   return ce;
 }
@@ -348,14 +351,16 @@ static double softmax_ce(int mode, const double* z, uint32_t C, int32_t y, doubl
  * ReLU'(z) is taken as [stored activation > 0], so ReLU'(0) = 0.
  */
 static void backward(int mode, work_t* w, const double* params, const int32_t* y, uint32_t b,
-                     double scale, double* grads, double* ce_sum, uint64_t* correct, double* probs) {
+                     double scale, const float* gscale, double* grads, double* ce_sum, uint64_t* correct,
+                     double* probs) {
   int L = w->L;
   const uint32_t* d = w->dims;
   uint32_t C = d[L];
   double* G = w->G;                 /* b x d_l, working precision (unrounded) */
   for (uint32_t i = 0; i < b; ++i) {
     const double* z = w->logits + (size_t)i * C;
-    double ce = softmax_ce(mode, z, C, y[i], scale, G + (size_t)i * C, probs ? probs + (size_t)i * C : NULL);
+    double ce = softmax_ce(mode, z, C, y[i], scale, gscale ? gscale + (size_t)i * C : NULL, G + (size_t)i * C,
+                           probs ? probs + (size_t)i * C : NULL);
     if (ce_sum) *ce_sum += ce;
     if (correct) *correct += (uint64_t)argmax_correct(z, C, y[i]);
   }
@@ -430,11 +435,12 @@ static int check_dims(int L, const uint32_t* dims) {
 
 /*
  * Loss and gradients of one batch (rows already gathered; b x d0 binary32
- * inputs).  scale <= 0 selects the default fl(1/b).  Used by the pins
+ * inputs).  scale <= 0 selects the default fl(1/b); a gradient-scale tensor
+ * gscale (b x dL binary32, nullable) replaces the scalar.  Used by the pins
  * (finite differences, hand-computed example).  probs (b x dL) optional.
  */
 int or_batch_grad(int mode, int L, const uint32_t* dims, const double* params,
-                  const float* X, const int32_t* y, uint32_t b, double scale,
+                  const float* X, const int32_t* y, uint32_t b, double scale, const float* gscale,
                   double* grads, double* ce_sum, double* logits_out, double* probs_out) {
   if (check_dims(L, dims)) return -1;
   if (b == 0) return -2;
@@ -445,7 +451,7 @@ int or_batch_grad(int mode, int L, const uint32_t* dims, const double* params,
   forward(mode, &w, params, b);
   if (logits_out) memcpy(logits_out, w.logits, sizeof(double) * (size_t)b * dims[L]);
   double ce = 0.0;
-  backward(mode, &w, params, y, b, scale, grads, &ce, NULL, probs_out);
+  backward(mode, &w, params, y, b, scale, gscale, grads, &ce, NULL, probs_out);
   if (ce_sum) *ce_sum = ce;
   work_free(&w);
   return 0;
@@ -454,14 +460,17 @@ int or_batch_grad(int mode, int L, const uint32_t* dims, const double* params,
 /*
  * Steps [t0, t1) of one epoch of mini-batch SGD for one variant.
  * Step t uses rows perm[t*B .. min(n, (t+1)*B)); the short last batch is kept
- * and scaled by fl(1/b_t).  Update (section 6.2: the mean gradient times the
+ * and scaled by fl(1/b_t), or, when the gradient-scale tensor gscale (batch x
+ * dL binary32) is given, row i of every batch by its row i (section 6.2's
+ * mutation).  Update (section 6.2: the mean gradient times the
  * learning rate is subtracted from weights and biases):
  *   W <- mask ? fl(W - fl(lr * dW)) : +0,   b <- fl(b - fl(lr * db)).
  * The loss of step t is taken before its update; ce_sum and correct accumulate.
  */
 int or_train_steps(int mode, int L, const uint32_t* dims, double* params, const uint8_t* mask,
                    float lr, const float* X, const int32_t* y, uint32_t n, const uint32_t* perm,
-                   uint32_t batch, uint32_t t0, uint32_t t1, double* ce_sum, uint64_t* correct) {
+                   uint32_t batch, uint32_t t0, uint32_t t1, const float* gscale, double* ce_sum,
+                   uint64_t* correct) {
   if (check_dims(L, dims)) return -1;
   if (batch == 0) return -2;
   uint32_t T = (n + batch - 1) / batch;
@@ -483,7 +492,7 @@ int or_train_steps(int mode, int L, const uint32_t* dims, double* params, const 
     }
     double scale = (mode == OR_F64) ? 1.0 / (double)b : f32(1.0 / (double)b);
     forward(mode, &w, params, b);
-    backward(mode, &w, params, yb, b, scale, grads, ce_sum, correct, NULL);
+    backward(mode, &w, params, yb, b, scale, gscale, grads, ce_sum, correct, NULL);
     double lrd = (double)lr;
     for (int l = 1; l <= L; ++l) {
       uint32_t din = dims[l - 1], dout = dims[l];
@@ -523,7 +532,7 @@ int or_predict(int mode, int L, const uint32_t* dims, const double* params,
     forward(mode, &w, params, b);
     for (uint32_t i = 0; i < b; ++i) {
       const double* z = w.logits + (size_t)i * C;
-      if (ce_sum) *ce_sum += softmax_ce(mode, z, C, y[r0 + i], 1.0, NULL, NULL);
+      if (ce_sum) *ce_sum += softmax_ce(mode, z, C, y[r0 + i], 1.0, NULL, NULL, NULL);
       if (correct) *correct += (uint64_t)argmax_correct(z, C, y[r0 + i]);
     }
   }

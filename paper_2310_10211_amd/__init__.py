@@ -37,7 +37,7 @@ EXPORTED = [
     "gevo_pop_export", "gevo_pop_import", "gevo_pop_epoch_labels", "gevo_epoch_permutation",
     "gevo_pop_set_profiling", "gevo_pop_kernel_stats", "gevo_pop_destroy", "gevo_status_str",
     "gevo_check_bf16_rounding", "gevo_nsga2_rank", "gevo_nsga2_select", "gevo_genomes_initial",
-    "gevo_genomes_breed", "gevo_pop_set_genomes",
+    "gevo_genomes_breed", "gevo_pop_set_genomes", "gevo_pop_set_grad_scale",
 ]
 KERNEL_KINDS = ["init", "gather", "layer_train", "layer_fwd", "out_train", "out_predict", "bwd", "aux",
                 "fused_train"]
@@ -114,6 +114,7 @@ def lib():
         L.gevo_genomes_breed.argtypes = [u32, u32p, editp, ctypes.c_uint64, u32, ctypes.c_double, ctypes.c_double,
                                          ctypes.c_double, u32, u32, u32p, editp, ctypes.c_size_t]
         L.gevo_pop_set_genomes.argtypes = [vp, ctypes.c_float, u32p, editp, f32p, f64p]
+        L.gevo_pop_set_grad_scale.argtypes = [vp, f32p]
         L.gevo_pop_destroy.argtypes = [vp]
         L.gevo_pop_destroy.restype = None
         L.gevo_status_str.argtypes = [ctypes.c_int]
@@ -370,6 +371,15 @@ class Population:
         _check(lib().gevo_pop_set_genomes(self._h, lr_base, _u32p(off), edits, _fp(lr), _f64p(dens)),
                "gevo_pop_set_genomes")
         return lr, dens
+
+    def set_grad_scale(self, scale):
+        """Per-element output-gradient scale [P][batch][classes] (None: the scalar 1/b)."""
+        if scale is None:
+            _check(lib().gevo_pop_set_grad_scale(self._h, None), "gevo_pop_set_grad_scale")
+            return
+        s = np.ascontiguousarray(np.asarray(scale, np.float32))
+        assert s.shape == (self.P, self.cfg["batch"], self.dims[-1]), s.shape
+        _check(lib().gevo_pop_set_grad_scale(self._h, _fp(s)), "gevo_pop_set_grad_scale")
 
     def reinit(self):
         """Destroy the handle and create a fresh population on the same workspace

@@ -36,6 +36,7 @@ struct Layout {
   size_t elt = 4;
   LayerLay lay[GEVO_MAX_LAYERS];
   size_t prune_off = 0, prune_id = 0, prune_th = 0;   // genome pruning edits (gevo_pop_set_genomes)
+  size_t gscale = 0;                               // [P][Bp][32] output-gradient scales (gevo_pop_set_grad_scale)
   size_t lr = 0, thresh = 0, train_ce = 0, train_corr = 0, test_ce = 0, test_corr = 0, part_ce = 0,
          part_corr = 0, xrows = 0, xcols = 0, yep = 0, xte = 0, yte = 0, perm = 0;
   size_t w1img = 0, m1blk = 0;                    // fused training: W1 register image, block-major W1 mask
@@ -129,6 +130,7 @@ gevo_status make_layout(const gevo_pop_config* c, Layout* o) {
   y.lr = take(P * 4);
   y.thresh = take(P * 4);
   y.prune_off = take((P + 1) * 4);
+  y.gscale = take(P * Bp * 32 * 4);
   y.prune_id = take(P * (size_t)kMaxGenomePrunes * 4);
   y.prune_th = take(P * (size_t)kMaxGenomePrunes * 4);
   y.train_ce = take(P * 8);
@@ -217,6 +219,7 @@ struct gevo_pop {
   double last_s = 0.0;
   bool predicted = false;
   bool has_base = false;    // initial weights come from the caller's base model
+  bool gscale_on = false;   // output gradients scaled per element (gevo_pop_set_grad_scale)
   // fused training keeps W1 in its own register image: which copy is current
   bool img_valid = false;   // the image (and the block-major mask) match the k-blocked master
   bool blk_stale = false;   // training has advanced the image past the k-blocked master
@@ -387,6 +390,7 @@ gevo_status train_step(gevo_pop* p, int t) {
     a.labels = at<int32_t>(p, y.yep) + (size_t)t * y.Bp;
     a.rows = y.Bp;
     a.scale = (float)(1.0 / (double)bt);
+    a.gscale = p->gscale_on ? at<float>(p, y.gscale) : nullptr;
     a.ce_acc = at<double>(p, y.train_ce);
     a.correct_acc = at<unsigned long long>(p, y.train_corr);
     if (a.Kp % kTile || a.Bp % kTile) return GEVO_E_SHAPE;
@@ -491,6 +495,7 @@ gevo_status do_train_steps(gevo_pop* p, uint32_t epoch, uint32_t s0, uint32_t s1
     f.W1 = at<float>(p, y.w1img); f.b1 = at<float>(p, q1.bias); f.m1 = at<uint32_t>(p, y.m1blk);
     f.W2 = at<float>(p, q2.Wm); f.b2 = at<float>(p, q2.bias); f.m2 = at<uint32_t>(p, q2.mask);
     f.lr = at<float>(p, y.lr);
+    f.gscale = p->gscale_on ? at<float>(p, y.gscale) : nullptr;
     f.ce_acc = at<double>(p, y.train_ce);
     f.correct_acc = at<unsigned long long>(p, y.train_corr);
     if (q2.Kp != q1.Np || q1.Kp % kTile || fused2_lds_bytes(f.Hp, f.Bp) == 0) return GEVO_E_SHAPE;
@@ -790,6 +795,29 @@ gevo_status gevo_pop_set_genomes(gevo_pop* p, float lr_base, const uint32_t* off
   p->timing_pending = false;
   p->img_valid = false;                          // the fused kernel's copy of the hidden layer is stale
   p->blk_stale = false;
+  return GEVO_OK;
+}
+
+gevo_status gevo_pop_set_grad_scale(gevo_pop* p, const float* scale) {
+  if (!p) return GEVO_E_ARG;
+  if (p->open_epoch >= 0) return GEVO_E_ORDER;
+  if (!scale) {
+    p->gscale_on = false;
+    return GEVO_OK;
+  }
+  const Layout& y = p->y;
+  const int C = y.lay[y.L - 1].N;
+  const size_t n = (size_t)y.P * y.B * C;
+  for (size_t i = 0; i < n; ++i)
+    if (!std::isfinite(scale[i])) return GEVO_E_ARG;
+  std::vector<float> dev((size_t)y.P * y.Bp * 32, 0.0f);
+  for (int v = 0; v < y.P; ++v)
+    for (int b = 0; b < y.B; ++b)
+      for (int c = 0; c < C; ++c)
+        dev[((size_t)v * y.Bp + b) * 32 + c] = scale[((size_t)v * y.B + b) * C + c];
+  HIP_TRY(hipStreamSynchronize(p->stream));      // no step in flight may read the old scales
+  HIP_TRY(hipMemcpy(p->ws + y.gscale, dev.data(), dev.size() * 4, hipMemcpyHostToDevice));
+  p->gscale_on = true;
   return GEVO_OK;
 }
 

@@ -444,7 +444,8 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
     if (tid < BP) yl[tid] = ylab;
     __syncthreads();
     // ---- logits^T, softmax cross-entropy, argmax (lowest index on ties, a NaN
-    //      logit is a miss), G2 = (p - onehot(y)) fl(1/b).
+    //      logit is a miss), G2 = (p - onehot(y)) fl(1/b), or times the
+    //      variant's per-element scale tensor when one is set.
     //      Up to 16 classes: 16-row batch tiles shared by all waves; a lane holds
     //      four classes of one row and the row's four lanes combine by shuffles.
     //      Classes 16..31 of G2 are then left unwritten and never read.
@@ -454,6 +455,8 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
     if (c16) {
       const int l16 = lane & 15, lq = lane >> 4, C = a.C;
       for (int tt = wave; tt < BP / 16; tt += NW) {
+        f32x4_t gsv = {scale, scale, scale, scale};   // the row's output-gradient scales (issued early)
+        if (a.gscale) gsv = *reinterpret_cast<const f32x4_t*>(a.gscale + ((size_t)v * BP + 16 * tt + l16) * 32 + 4 * lq);
         f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
         const uint16_t* ap = w2 + l16 * Ly::W2S + 8 * lq;
         const uint16_t* bp = a1 + (16 * tt + l16) * Ly::AS + 8 * lq;
@@ -495,7 +498,7 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int c = 4 * lq + j;
-          gf[j] = (c < C && rvalid) ? (e[j] / s - (c == y ? 1.0f : 0.0f)) * scale : 0.0f;
+          gf[j] = (c < C && rvalid) ? (e[j] / s - (c == y ? 1.0f : 0.0f)) * gsv[j] : 0.0f;
         }
         uint32_t gq[2];
         to_bf16x2(gf, gq);
@@ -518,6 +521,12 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
         *reinterpret_cast<uint2*>(g2 + b * Ly::GS + 4 * lq) = make_uint2(gq[0], gq[1]);
       }
     } else if (wave < BT) {
+      f32x4_t gsv[4] = {{scale, scale, scale, scale}, {scale, scale, scale, scale}, {scale, scale, scale, scale},
+                        {scale, scale, scale, scale}};   // classes 8q + 4lh + 0..3 of the row (issued early)
+      if (a.gscale)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          gsv[q] = *reinterpret_cast<const f32x4_t*>(a.gscale + ((size_t)v * BP + 32 * wave + l32) * 32 + 8 * q + 4 * lh);
       f32x16_t c0 = zero16(), c1 = zero16();
       const uint16_t* ap = w2 + l32 * Ly::W2S + 8 * lh;
       const uint16_t* bp = a1 + (32 * wave + l32) * Ly::AS + 8 * lh;
@@ -559,7 +568,7 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int c = crow(r, lane);
-        gf[r] = (c < C && rvalid) ? (e[r] / s - (c == y ? 1.0f : 0.0f)) * scale : 0.0f;
+        gf[r] = (c < C && rvalid) ? (e[r] / s - (c == y ? 1.0f : 0.0f)) * gsv[r >> 2][r & 3] : 0.0f;
       }
       uint32_t gq[8];
       to_bf16x2(gf, gq);

@@ -92,6 +92,7 @@ struct OutArgs {
   const int32_t* labels;         // [rows]; < 0 marks a padding row
   int rows;                      // rows covered by the grid (training: Bp)
   float scale;                   // fl32(1/b_t)
+  const float* gscale;           // [P][Bp][32] per-element output-gradient scale (nullable: scale)
   double* ce_acc;                // [P] training accumulators
   unsigned long long* correct_acc;
   int chunk0;                    // predict: index of the first 256-row chunk
@@ -126,6 +127,7 @@ struct Fused2Args {
   const float* lr;
   double* ce_acc;
   unsigned long long* correct_acc;
+  const float* gscale;           // [P][Bp][32] per-element output-gradient scale (nullable: fl32(1/b_t))
 };
 
 struct GatherArgs {

@@ -462,7 +462,8 @@ __global__ __launch_bounds__(64 * kOutWaves) void k_out(OutArgs<S> a) {
       }
       if (a.train) {
         const float p = e / s;
-        const float g = (cvalid && rvalid) ? (p - (l32 == y ? 1.0f : 0.0f)) * a.scale : 0.0f;
+        const float sc = a.gscale ? a.gscale[((size_t)v * a.Bp + rl) * 32 + l32] : a.scale;
+        const float g = (cvalid && rvalid) ? (p - (l32 == y ? 1.0f : 0.0f)) * sc : 0.0f;
         db_part += g;
         gs[rl * GSTR + l32] = O::from_f32(g);
       }
