@@ -213,16 +213,25 @@ gevo_status gevo_epoch_permutation(uint64_t seed, uint32_t epoch, uint32_t n, ui
  *   mutation of child i, generation g:  (0, g, i, 9) word 0 decides (u24 < mutpb);
  *                                       the edit from words 1 and 2 of (1, g, i, 9)
  *   edit j of initial individual i:     words 1 and 2 of (j, 0, i, 9)
- * where u24 = (word >> 8) * 2^-24.  A drawn edit is, with equal odds (word 1
- * u24 < 1/2), a learning-rate factor exp(ln(1/2) + u ln 4) (u from word 2,
- * computed in binary64, rounded to binary32) or pruning at density
- * rho = rho_lo + u (1 - rho_lo), threshold round-half-even(rho 2^24).
+ * where u24 = (word >> 8) * 2^-24.  A drawn edit is structural when word 1's
+ * u24 < struct_p: bias removal of layer 1 + (word 0 onto [0, L)) when word 3's
+ * u24 < 1/2 or the net has no hidden layer, otherwise width 1 + (word 2 onto
+ * [0, d_l)) of hidden layer l = 1 + (word 0 onto [0, L-1)).  Otherwise it is a
+ * learning-rate factor exp(ln(1/2) + u ln 4) (u from word 2, binary64, rounded
+ * to binary32) when word 1's u24 < struct_p + (1 - struct_p)/2, else pruning
+ * at density rho = rho_lo + u (1 - rho_lo), threshold round-half-even(rho 2^24).
+ * struct_p = 0 draws no structural edit (dims may then be null).
  */
-typedef enum { GEVO_EDIT_LR = 0, GEVO_EDIT_PRUNE = 1 } gevo_edit_kind;
+typedef enum {
+  GEVO_EDIT_LR = 0,        /* value = bits of a binary32 learning-rate factor */
+  GEVO_EDIT_PRUNE = 1,     /* id = mask draw id, value = keep threshold (<= 2^24) */
+  GEVO_EDIT_WIDTH = 2,     /* id = hidden layer l (1 .. L-1), value = units kept (>= 1) */
+  GEVO_EDIT_BIAS_OFF = 3   /* id = layer l (1 .. L): its biases are removed */
+} gevo_edit_kind;
 typedef struct {
   uint32_t kind;    /* gevo_edit_kind */
-  uint32_t id;      /* pruning: the draw id of its mask (see gevo_pop_set_genomes) */
-  uint32_t value;   /* GEVO_EDIT_LR: bits of the binary32 factor; GEVO_EDIT_PRUNE: keep threshold (<= 2^24) */
+  uint32_t id;
+  uint32_t value;
 } gevo_edit;
 
 /* NSGA-II ranking (Deb et al., IEEE TEC 2002) of n points with m objectives,
@@ -246,9 +255,10 @@ gevo_status gevo_nsga2_select(uint32_t n, const uint32_t* rank, const double* cr
 
 /* Initial population (section 4): individual i gets n_mut drawn edits, edit j
  * with id id_base + n_mut i + j, written to out[n_mut i + j] (host array of
- * n * n_mut edits).  GEVO_E_ARG for a null pointer or rho_lo outside [0, 1]. */
+ * n * n_mut edits).  dims[n_layers + 1]: the net's widths (for structural
+ * edits).  GEVO_E_ARG for a null pointer, rho_lo or struct_p outside [0, 1]. */
 gevo_status gevo_genomes_initial(uint32_t n, uint32_t n_mut, uint64_t seed, double rho_lo, uint32_t id_base,
-                                 gevo_edit* out);
+                                 double struct_p, uint32_t n_layers, const uint32_t* dims, gevo_edit* out);
 
 /* Children of generation gen >= 1 from n parents (the tournament winners);
  * parent i's edits are edits[offsets[i] .. offsets[i+1]).  Pairs (2i, 2i+1)
@@ -256,14 +266,14 @@ gevo_status gevo_genomes_initial(uint32_t n, uint32_t n_mut, uint64_t seed, doub
  * concatenate both lists, shuffle (Fisher-Yates from the last position), cut
  * at a drawn point in [0, length], each child keeping at most max_edits; an
  * odd last parent is copied.  Then child i gets one drawn edit with id
- * id_base + i, with probability mutpb, when it holds fewer than max_edits.
- * Writes out_offsets[n + 1] and the edits (host arrays); GEVO_E_ARG for bad
- * offsets, gen == 0, probabilities outside [0, 1] or out_capacity below
- * offsets[n] + n. */
+ * id_base + i, with probability mutpb, when it holds fewer than max_edits
+ * (structural with probability struct_p, see above).  Writes
+ * out_offsets[n + 1] and the edits (host arrays); GEVO_E_ARG for bad offsets,
+ * gen == 0, probabilities outside [0, 1] or out_capacity below offsets[n] + n. */
 gevo_status gevo_genomes_breed(uint32_t n, const uint32_t* offsets, const gevo_edit* edits, uint64_t seed,
                                uint32_t gen, double cxpb, double mutpb, double rho_lo, uint32_t id_base,
-                               uint32_t max_edits, uint32_t* out_offsets, gevo_edit* out_edits,
-                               size_t out_capacity);
+                               uint32_t max_edits, double struct_p, uint32_t n_layers, const uint32_t* dims,
+                               uint32_t* out_offsets, gevo_edit* out_edits, size_t out_capacity);
 
 /* Rebuild the population from genomes, variant v from edits[offsets[v] ..
  * offsets[v+1]) (host arrays, offsets[P] entries after the first).  Learning
@@ -272,13 +282,22 @@ gevo_status gevo_genomes_breed(uint32_t n, const uint32_t* offsets, const gevo_e
  * it, edit (id, threshold) keeping weight (layer l, index e = n d_{l-1} + k)
  * when the top 24 bits of the mask draw of initialisation, taken with id in
  * place of the variant index, are below the threshold (one edit (v, T_v)
- * reproduces variant v of gevo_pop_init).  Weights are the initial weights of
- * gevo_pop_init under the new mask, biases as initialised; the next training
- * epoch is epoch 0 again.  Writes lr_out[P] and density_out[P] (the product
- * of the edits' keep fractions threshold / 2^24, binary64, in order) when not
- * null.  At most 64 pruning edits per variant.  Synchronous; GEVO_E_ARG for
- * bad offsets, kinds, thresholds above 2^24, a non-finite or non-positive
- * learning rate or too many pruning edits, GEVO_E_ORDER during an epoch. */
+ * reproduces variant v of gevo_pop_init).  Structural edits (removing the
+ * bias term, section 6.1; shrinking a tensor, the repair of section 4.1):
+ * GEVO_EDIT_WIDTH keeps the first `value` units of hidden layer `id` (several
+ * on one layer: the smallest), removing every weight into and out of the
+ * other units and their biases; GEVO_EDIT_BIAS_OFF removes the biases of
+ * layer `id`.  Removed biases are +0 and stay +0 in training; a variant whose
+ * units are removed computes exactly what the narrower network computes.
+ * Weights are the initial weights of gevo_pop_init under the new mask,
+ * biases as initialised; the next training epoch is epoch 0 again.  Writes
+ * lr_out[P] and density_out[P] when not null: the product of the pruning
+ * edits' keep fractions threshold / 2^24 in order, times the fraction of
+ * weights the structural edits keep (sum over layers of kept inputs times
+ * kept units over sum of d_{l-1} d_l), in binary64.  At most 64 pruning edits
+ * per variant.  Synchronous; GEVO_E_ARG for bad offsets, kinds, layers,
+ * widths of 0, thresholds above 2^24, a non-finite or non-positive learning
+ * rate or too many pruning edits, GEVO_E_ORDER during an epoch. */
 gevo_status gevo_pop_set_genomes(gevo_pop* pop, float lr_base, const uint32_t* offsets, const gevo_edit* edits,
                                  float* lr_out, double* density_out);
 

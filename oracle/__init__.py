@@ -90,7 +90,8 @@ def lib():
             L.or_permutation.restype = None
             L.or_batch_grad.argtypes = [ctypes.c_int, ctypes.c_int, u32p, f64p, f32p, i32p, ctypes.c_uint32,
                                         ctypes.c_double, f32p, f64p, f64p, f64p, f64p]
-            L.or_train_steps.argtypes = [ctypes.c_int, ctypes.c_int, u32p, f64p, u8p, ctypes.c_float, f32p, i32p,
+            L.or_structure_masks.argtypes = [ctypes.c_int, u32p, u32p, u8p, u8p, u8p]
+            L.or_train_steps.argtypes = [ctypes.c_int, ctypes.c_int, u32p, f64p, u8p, u8p, ctypes.c_float, f32p, i32p,
                                          ctypes.c_uint32, u32p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
                                          f32p, f64p, u64p]
             L.or_predict.argtypes = [ctypes.c_int, ctypes.c_int, u32p, f64p, f32p, i32p, ctypes.c_uint32,
@@ -242,10 +243,28 @@ def batch_grad(mode, dims, params, X, y, scale=0.0, gscale=None):
     return ce.value, grads, logits, probs
 
 
-def train_steps(mode, dims, params, mask, lr, X, y, perm, batch, t0, t1, gscale=None):
+def structure_masks(dims, widths, bias_keep, mask=None):
+    """(weight mask, bias mask) of structural edits: layer l keeps its first
+    widths[l] units and its bias when bias_keep[l-1]; mask (optional) is the
+    weight mask to narrow."""
+    d = _dims(dims)
+    L = len(d) - 1
+    w = np.ascontiguousarray(np.asarray(widths, dtype=np.uint32))
+    bk = np.ascontiguousarray(np.asarray(bias_keep, dtype=np.uint8))
+    assert w.size == L + 1 and bk.size == L
+    m = np.ones(weight_count(dims), np.uint8) if mask is None else np.array(mask, dtype=np.uint8, copy=True)
+    bm = np.zeros(int(sum(d[1:])), np.uint8)
+    rc = lib().or_structure_masks(L, _p(d, ctypes.c_uint32), _p(w, ctypes.c_uint32), _p(bk, ctypes.c_uint8),
+                                  _p(m, ctypes.c_uint8), _p(bm, ctypes.c_uint8))
+    assert rc == 0
+    return m, bm
+
+
+def train_steps(mode, dims, params, mask, lr, X, y, perm, batch, t0, t1, gscale=None, bmask=None):
     """In-place SGD steps [t0, t1) on ``params``; returns (ce_sum, correct).
     gscale ([batch][C], optional): row i scales the output gradient of row i of
-    every batch in place of fl(1/b_t)."""
+    every batch in place of fl(1/b_t).  bmask (over all biases, optional):
+    biases with 0 stay +0."""
     d = _dims(dims)
     assert params.dtype == np.float64 and params.flags.c_contiguous
     mask = np.ascontiguousarray(mask, dtype=np.uint8)
@@ -255,8 +274,9 @@ def train_steps(mode, dims, params, mask, lr, X, y, perm, batch, t0, t1, gscale=
     ce = ctypes.c_double(0.0)
     corr = ctypes.c_uint64(0)
     gs, gsp = _gscale(gscale, batch, int(d[-1]))
+    bm = None if bmask is None else np.ascontiguousarray(bmask, dtype=np.uint8)
     rc = lib().or_train_steps(_mode(mode), len(d) - 1, _p(d, ctypes.c_uint32), _p(params, ctypes.c_double),
-                              _p(mask, ctypes.c_uint8), float(lr), _p(X, ctypes.c_float), _p(y, ctypes.c_int32),
+                              _p(mask, ctypes.c_uint8), None if bm is None else _p(bm, ctypes.c_uint8), float(lr), _p(X, ctypes.c_float), _p(y, ctypes.c_int32),
                               y.shape[0], _p(perm, ctypes.c_uint32), batch, t0, t1, gsp,
                               ctypes.byref(ce), ctypes.byref(corr))
     assert rc == 0, rc

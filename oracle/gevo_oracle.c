@@ -263,6 +263,30 @@ int or_genome_mask(uint64_t seed, int L, const uint32_t* dims, uint32_t n_edits,
   return 0;
 }
 
+/* Structural edits of an individual: layer l keeps its first width[l] units
+ * (width[0] = d0 and width[L] = dL: inputs and classes are never removed) and
+ * its bias unless bias_keep[l-1] is 0 (removing the bias term, section 6.1;
+ * shrinking a tensor, the repair of section 4.1).  Clears the weights into
+ * and out of removed units in the weight mask (canonical order) and writes
+ * the bias mask (bmask, over all biases, 1 = trained).  A network whose
+ * removed units have no weights and no bias computes exactly what the
+ * narrower network computes. */
+int or_structure_masks(int L, const uint32_t* dims, const uint32_t* width, const uint8_t* bias_keep,
+                       uint8_t* mask, uint8_t* bmask) {
+  if (L < 1 || L > OR_MAX_LAYERS) return -1;
+  size_t bo = 0;
+  for (int l = 1; l <= L; ++l) {
+    uint32_t din = dims[l - 1], dout = dims[l];
+    uint8_t* M = mask + m_off(dims, l);
+    for (uint32_t k = 0; k < din; ++k)
+      for (uint32_t n = 0; n < dout; ++n)
+        if (k >= width[l - 1] || n >= width[l]) M[(size_t)k * dout + n] = 0;
+    for (uint32_t n = 0; n < dout; ++n) bmask[bo + n] = (uint8_t)(n < width[l] && bias_keep[l - 1]);
+    bo += dout;
+  }
+  return 0;
+}
+
 /* Per-epoch data order, shared by all variants: Fisher-Yates from the end,
  * swap index j = floor(r * (i+1) / 2^32) with r a 32-bit Philox word
  * (multiply-shift, no rejection). */
@@ -464,13 +488,14 @@ int or_batch_grad(int mode, int L, const uint32_t* dims, const double* params,
  * dL binary32) is given, row i of every batch by its row i (section 6.2's
  * mutation).  Update (section 6.2: the mean gradient times the
  * learning rate is subtracted from weights and biases):
- *   W <- mask ? fl(W - fl(lr * dW)) : +0,   b <- fl(b - fl(lr * db)).
+ *   W <- mask ? fl(W - fl(lr * dW)) : +0,   b <- bmask ? fl(b - fl(lr * db)) : +0
+ * (bmask over all biases, nullable: every bias is trained).
  * The loss of step t is taken before its update; ce_sum and correct accumulate.
  */
 int or_train_steps(int mode, int L, const uint32_t* dims, double* params, const uint8_t* mask,
-                   float lr, const float* X, const int32_t* y, uint32_t n, const uint32_t* perm,
-                   uint32_t batch, uint32_t t0, uint32_t t1, const float* gscale, double* ce_sum,
-                   uint64_t* correct) {
+                   const uint8_t* bmask, float lr, const float* X, const int32_t* y, uint32_t n,
+                   const uint32_t* perm, uint32_t batch, uint32_t t0, uint32_t t1, const float* gscale,
+                   double* ce_sum, uint64_t* correct) {
   if (check_dims(L, dims)) return -1;
   if (batch == 0) return -2;
   uint32_t T = (n + batch - 1) / batch;
@@ -494,6 +519,7 @@ int or_train_steps(int mode, int L, const uint32_t* dims, double* params, const 
     forward(mode, &w, params, b);
     backward(mode, &w, params, yb, b, scale, gscale, grads, ce_sum, correct, NULL);
     double lrd = (double)lr;
+    size_t bo = 0;
     for (int l = 1; l <= L; ++l) {
       uint32_t din = dims[l - 1], dout = dims[l];
       double* W = params + w_off(dims, l);
@@ -503,7 +529,9 @@ int or_train_steps(int mode, int L, const uint32_t* dims, double* params, const 
         W[i] = M[i] ? rw(mode, W[i] - rw(mode, lrd * dW[i])) : 0.0;
       double* bias = W + (size_t)din * dout;
       double* db = dW + (size_t)din * dout;
-      for (uint32_t j = 0; j < dout; ++j) bias[j] = rw(mode, bias[j] - rw(mode, lrd * db[j]));
+      for (uint32_t j = 0; j < dout; ++j)
+        bias[j] = (!bmask || bmask[bo + j]) ? rw(mode, bias[j] - rw(mode, lrd * db[j])) : 0.0;
+      bo += dout;
     }
   }
   free(grads); free(yb);

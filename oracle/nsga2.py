@@ -19,10 +19,14 @@ Definitions:
     to the next generation and the rest is chosen by tournament selection
     (section 4.4).
   * Edits here are the effects the paper attributes to its evolved edits: a
-    changed learning rate (section 6.2) and pruned weights (abstract).  Edit
-    (kind 0, id, value): multiply the learning rate by the binary32 factor
-    whose bits are ``value``; edit (kind 1, id, value): keep a weight only when
-    the top 24 bits of its mask draw under edit ``id`` fall below ``value``.
+    changed learning rate (section 6.2) and pruned weights (abstract), and the
+    structural ones of its MobileNet analysis and repair: removed biases
+    (section 6.1) and shrunk tensors (section 4.1).  Edit (kind 0, id, value):
+    multiply the learning rate by the binary32 factor whose bits are
+    ``value``; (kind 1, id, value): keep a weight only when the top 24 bits of
+    its mask draw under edit ``id`` fall below ``value``; (kind 2, l, w): keep
+    the first w units of hidden layer l; (kind 3, l, 0): remove the biases of
+    layer l.
 
 Counter layout of the draws (key = seed), word w of Philox((c0, c1, c2, stream)):
   tournament j of generation g:     (j, g, 0, 7), words 0 and 1 = contestants
@@ -31,6 +35,10 @@ Counter layout of the draws (key = seed), word w of Philox((c0, c1, c2, stream))
   mutation of child i, generation g >= 1: (0, g, i, 9) word 0 = decision;
                                     the new edit from words 1 (kind) and 2 (value) of (1, g, i, 9)
   edit j of initial individual i:   words 1 (kind) and 2 (value) of (j, 0, i, 9)
+  a drawn edit is structural when word 1's u24 < struct_p: word 3 picks bias
+  removal (u24 < 1/2, or no hidden layer) or a width, word 0 the layer, word 2
+  the width (1 + multiply-shift onto [0, d_l)); otherwise a learning-rate edit
+  when u24 < struct_p + (1 - struct_p) / 2, else pruning
 Objectives must not be NaN (a NaN compares false and would never be dominated).
 
 Parity status:
@@ -52,7 +60,7 @@ import numpy as np
 from . import philox
 
 STREAM_SELECT, STREAM_CROSS, STREAM_MUT = 7, 8, 9
-LR_EDIT, PRUNE_EDIT = 0, 1
+LR_EDIT, PRUNE_EDIT, WIDTH_EDIT, BIAS_EDIT = 0, 1, 2, 3
 INF = float("inf")
 
 
@@ -156,25 +164,35 @@ def select(rank, dist, n_elite, n_select, seed, gen):
     return out
 
 
-def random_edit(seed, gen, i, j, edit_id, rho_lo):
-    """The edit drawn from (j, gen, i, 9): with equal odds a learning-rate
-    factor log-uniform on [1/2, 2] or pruning at a density uniform on [rho_lo, 1]."""
+def random_edit(seed, gen, i, j, edit_id, rho_lo, struct_p=0.0, dims=None):
+    """The edit drawn from (j, gen, i, 9): with probability struct_p a
+    structural edit (bias removal or a hidden width), otherwise with equal
+    odds a learning-rate factor log-uniform on [1/2, 2] or pruning at a
+    density uniform on [rho_lo, 1]."""
     w = _draw(seed, j, gen, i, STREAM_MUT)
     u = _u24(w[2])
-    if _u24(w[1]) < 0.5:
+    uk = _u24(w[1])
+    if uk < struct_p:
+        L = len(dims) - 1
+        if _u24(w[3]) < 0.5 or L < 2:
+            return (BIAS_EDIT, 1 + _below(w[0], L), 0)
+        layer = 1 + _below(w[0], L - 1)
+        return (WIDTH_EDIT, layer, 1 + _below(w[2], int(dims[layer])))
+    if uk < struct_p + (1.0 - struct_p) * 0.5:
         factor = _f32(math.exp(math.log(0.5) + u * math.log(4.0)))
         return (LR_EDIT, edit_id, _f32_bits(factor))
     rho = rho_lo + u * (1.0 - rho_lo)
     return (PRUNE_EDIT, edit_id, int(round(rho * 16777216.0)))
 
 
-def initial(n, seed, rho_lo, n_mut=3, id_base=0):
+def initial(n, seed, rho_lo, n_mut=3, id_base=0, struct_p=0.0, dims=None):
     """Initial population: n individuals, each with n_mut random edits
     (edit ids id_base + n_mut * i + j)."""
-    return [[random_edit(seed, 0, i, j, id_base + n_mut * i + j, rho_lo) for j in range(n_mut)] for i in range(n)]
+    return [[random_edit(seed, 0, i, j, id_base + n_mut * i + j, rho_lo, struct_p, dims) for j in range(n_mut)]
+            for i in range(n)]
 
 
-def breed(parents, seed, gen, cxpb, mutpb, rho_lo, id_base, max_edits):
+def breed(parents, seed, gen, cxpb, mutpb, rho_lo, id_base, max_edits, struct_p=0.0, dims=None):
     """Children of the tournament winners, in pairs (0,1), (2,3), ...: with
     probability cxpb a pair is recombined by messy one-point crossover
     (concatenate, shuffle, cut; each child keeps at most max_edits), then each
@@ -195,7 +213,7 @@ def breed(parents, seed, gen, cxpb, mutpb, rho_lo, id_base, max_edits):
     for i in range(len(children)):
         w = _draw(seed, 0, gen, i, STREAM_MUT)
         if _u24(w[0]) < mutpb and len(children[i]) < max_edits:
-            children[i].append(random_edit(seed, gen, i, 1, id_base + i, rho_lo))
+            children[i].append(random_edit(seed, gen, i, 1, id_base + i, rho_lo, struct_p, dims))
     return children
 
 
@@ -208,8 +226,34 @@ def apply(edits, lr_base):
     for kind, eid, value in edits:
         if kind == LR_EDIT:
             lr = _f32(lr * _bits_f32(value))
-        else:
+        elif kind == PRUNE_EDIT:
             ids.append(eid)
             th.append(value)
             dens = dens * (value / 16777216.0)
     return lr, ids, th, dens
+
+
+def structure(edits, dims):
+    """(widths [L+1], bias_keep [L]) of an individual: a hidden layer keeps the
+    smallest width any of its edits asks for, inputs and classes are kept."""
+    L = len(dims) - 1
+    widths = [int(d) for d in dims]
+    keep = [1] * L
+    for kind, eid, value in edits:
+        if kind == WIDTH_EDIT:
+            assert 1 <= eid <= L - 1 and value >= 1
+            widths[eid] = min(widths[eid], int(value))
+        elif kind == BIAS_EDIT:
+            assert 1 <= eid <= L
+            keep[eid - 1] = 0
+    return widths, keep
+
+
+def density(edits, dims):
+    """Expected kept fraction of the weights: the pruning edits' keep
+    fractions in order, times the fraction the structural edits keep."""
+    dens = apply(edits, 1.0)[3]
+    widths, _ = structure(edits, dims)
+    kept = sum(widths[l - 1] * widths[l] for l in range(1, len(dims)))
+    total = sum(int(dims[l - 1]) * int(dims[l]) for l in range(1, len(dims)))
+    return dens * (kept / total)

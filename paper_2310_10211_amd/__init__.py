@@ -21,7 +21,7 @@ import numpy as np
 
 __all__ = ["Population", "lib", "epoch_permutation", "check_bf16_rounding", "GevoError", "config_struct",
            "workspace_bytes", "nsga2_rank", "nsga2_select", "genomes_initial", "genomes_breed", "EDIT_LR",
-           "EDIT_PRUNE"]
+           "EDIT_PRUNE", "EDIT_WIDTH", "EDIT_BIAS_OFF"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgevo.so")
@@ -51,7 +51,7 @@ class GevoEdit(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_uint32), ("id", ctypes.c_uint32), ("value", ctypes.c_uint32)]
 
 
-EDIT_LR, EDIT_PRUNE = 0, 1
+EDIT_LR, EDIT_PRUNE, EDIT_WIDTH, EDIT_BIAS_OFF = 0, 1, 2, 3
 
 
 class GevoPopConfig(ctypes.Structure):
@@ -110,9 +110,11 @@ def lib():
         editp = ctypes.POINTER(GevoEdit)
         L.gevo_nsga2_rank.argtypes = [u32, u32, f64p, u32p, f64p]
         L.gevo_nsga2_select.argtypes = [u32, u32p, f64p, u32, u32, ctypes.c_uint64, u32, u32p]
-        L.gevo_genomes_initial.argtypes = [u32, u32, ctypes.c_uint64, ctypes.c_double, u32, editp]
+        L.gevo_genomes_initial.argtypes = [u32, u32, ctypes.c_uint64, ctypes.c_double, u32, ctypes.c_double, u32,
+                                           u32p, editp]
         L.gevo_genomes_breed.argtypes = [u32, u32p, editp, ctypes.c_uint64, u32, ctypes.c_double, ctypes.c_double,
-                                         ctypes.c_double, u32, u32, u32p, editp, ctypes.c_size_t]
+                                         ctypes.c_double, u32, u32, ctypes.c_double, u32, u32p, u32p, editp,
+                                         ctypes.c_size_t]
         L.gevo_pop_set_genomes.argtypes = [vp, ctypes.c_float, u32p, editp, f32p, f64p]
         L.gevo_pop_set_grad_scale.argtypes = [vp, f32p]
         L.gevo_pop_destroy.argtypes = [vp]
@@ -237,22 +239,32 @@ def nsga2_select(rank, crowding, n_elite, n_select, seed, gen):
     return [int(i) for i in out]
 
 
-def genomes_initial(n, seed, rho_lo, n_mut=3, id_base=0):
-    """n individuals with n_mut drawn edits each."""
+def _dims_arg(dims):
+    if dims is None:
+        return 0, None, None
+    d = np.ascontiguousarray(np.asarray(dims, np.uint32))
+    return len(d) - 1, d, _u32p(d)
+
+
+def genomes_initial(n, seed, rho_lo, n_mut=3, id_base=0, struct_p=0.0, dims=None):
+    """n individuals with n_mut drawn edits each (structural with probability struct_p)."""
     edits = (GevoEdit * max(n * n_mut, 1))()
-    _check(lib().gevo_genomes_initial(n, n_mut, seed, rho_lo, id_base, edits), "gevo_genomes_initial")
+    nl, keep, dp = _dims_arg(dims)
+    _check(lib().gevo_genomes_initial(n, n_mut, seed, rho_lo, id_base, struct_p, nl, dp, edits),
+           "gevo_genomes_initial")
     return [[(edits[n_mut * i + j].kind, edits[n_mut * i + j].id, edits[n_mut * i + j].value) for j in range(n_mut)]
             for i in range(n)]
 
 
-def genomes_breed(parents, seed, gen, cxpb, mutpb, rho_lo, id_base, max_edits):
+def genomes_breed(parents, seed, gen, cxpb, mutpb, rho_lo, id_base, max_edits, struct_p=0.0, dims=None):
     """Children of the tournament winners (messy one-point crossover, mutation)."""
     off, edits = _pack_genomes(parents)
     cap = int(off[-1]) + len(parents)
     out_off = np.zeros(len(parents) + 1, np.uint32)
     out = (GevoEdit * max(cap, 1))()
+    nl, keep, dp = _dims_arg(dims)
     _check(lib().gevo_genomes_breed(len(parents), _u32p(off), edits, seed, gen, cxpb, mutpb, rho_lo, id_base,
-                                    max_edits, _u32p(out_off), out, cap), "gevo_genomes_breed")
+                                    max_edits, struct_p, nl, dp, _u32p(out_off), out, cap), "gevo_genomes_breed")
     return _unpack_genomes(out_off, out)
 
 

@@ -5,6 +5,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <algorithm>
 #include <cmath>
 #include <new>
 #include <type_traits>
@@ -23,6 +24,8 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 struct LayerLay {
   int K = 0, N = 0, Kp = 0, Np = 0;
   size_t Wm = 0, bias = 0, mask = 0, Wt = 0, base_w = 0, base_b = 0;
+  size_t bmask = 0;                                // [P][Np/32] bias-trained bits
+  size_t win = 0, wout = 0, bkeep = 0;             // [P] structural edits (gevo_pop_set_genomes)
   size_t arows[2] = {0, 0}, acols[2] = {0, 0};   // training activations (hidden layers)
   size_t gcols = 0, grows = 0;                     // gradient at this layer's output (hidden)
   size_t prows = 0;                                // predict activations
@@ -114,6 +117,10 @@ gevo_status make_layout(const gevo_pop_config* c, Layout* o) {
     q.Wm = take(P * Np * Kp * 4);
     q.bias = take(P * Np * 4);
     q.mask = take(P * Np * (Kp / 32) * 4);
+    q.bmask = take(P * (Np / 32) * 4);
+    q.win = take(P * 4);
+    q.wout = take(P * 4);
+    q.bkeep = take(P * 4);
     q.base_w = take(Np * Kp * 4);
     q.base_b = take(Np * 4);
     if (l >= 1 && l < y.L - 1) q.Wt = take(P * Kp * Np * e);         // hidden layer >= 2
@@ -296,7 +303,7 @@ gevo_status forward_hidden(gevo_pop* p, const S* arows0, size_t ar0_vs, int R, i
     const LayerLay& q = y.lay[l];
     LayerArgs<S> a{};
     a.Kp = q.Kp; a.Np = q.Np; a.Bp = y.Bp;
-    a.Wm = at<float>(p, q.Wm); a.bias = at<float>(p, q.bias); a.mask = at<uint32_t>(p, q.mask);
+    a.Wm = at<float>(p, q.Wm); a.bias = at<float>(p, q.bias); a.mask = at<uint32_t>(p, q.mask); a.bmask = at<uint32_t>(p, q.bmask);
     a.lr = at<float>(p, y.lr);
     a.do_update = 0;
     a.do_forward = 1;
@@ -375,7 +382,7 @@ gevo_status train_step(gevo_pop* p, int t) {
     const LayerLay& q = y.lay[L - 1];
     OutArgs<S> a{};
     a.Kp = q.Kp; a.C = q.N; a.Bp = y.Bp;
-    a.Wm = at<float>(p, q.Wm); a.bias = at<float>(p, q.bias); a.mask = at<uint32_t>(p, q.mask);
+    a.Wm = at<float>(p, q.Wm); a.bias = at<float>(p, q.bias); a.mask = at<uint32_t>(p, q.mask); a.bmask = at<uint32_t>(p, q.bmask);
     a.lr = at<float>(p, y.lr);
     a.train = 1;
     if (L == 1) {
@@ -416,7 +423,7 @@ gevo_status train_step(gevo_pop* p, int t) {
     const LayerLay& q = y.lay[l];
     LayerArgs<S> a{};
     a.Kp = q.Kp; a.Np = q.Np; a.Bp = y.Bp;
-    a.Wm = at<float>(p, q.Wm); a.bias = at<float>(p, q.bias); a.mask = at<uint32_t>(p, q.mask);
+    a.Wm = at<float>(p, q.Wm); a.bias = at<float>(p, q.bias); a.mask = at<uint32_t>(p, q.mask); a.bmask = at<uint32_t>(p, q.bmask);
     a.lr = at<float>(p, y.lr);
     a.do_update = 1;
     a.Gcols = at<S>(p, q.gcols); a.g_vs = (size_t)q.Np * y.Bp;
@@ -494,6 +501,7 @@ gevo_status do_train_steps(gevo_pop* p, uint32_t epoch, uint32_t s0, uint32_t s1
     if (sti != GEVO_OK) return sti;
     f.W1 = at<float>(p, y.w1img); f.b1 = at<float>(p, q1.bias); f.m1 = at<uint32_t>(p, y.m1blk);
     f.W2 = at<float>(p, q2.Wm); f.b2 = at<float>(p, q2.bias); f.m2 = at<uint32_t>(p, q2.mask);
+    f.bm1 = at<uint32_t>(p, q1.bmask); f.bm2 = at<uint32_t>(p, q2.bmask);
     f.lr = at<float>(p, y.lr);
     f.gscale = p->gscale_on ? at<float>(p, y.gscale) : nullptr;
     f.ce_acc = at<double>(p, y.train_ce);
@@ -538,7 +546,7 @@ gevo_status do_predict(gevo_pop* p) {
     const LayerLay& q = y.lay[y.L - 1];
     OutArgs<S> a{};
     a.Kp = q.Kp; a.C = q.N; a.Bp = y.Bp;
-    a.Wm = at<float>(p, q.Wm); a.bias = at<float>(p, q.bias); a.mask = at<uint32_t>(p, q.mask);
+    a.Wm = at<float>(p, q.Wm); a.bias = at<float>(p, q.bias); a.mask = at<uint32_t>(p, q.mask); a.bmask = at<uint32_t>(p, q.bmask);
     a.lr = at<float>(p, y.lr);
     a.train = 0;
     if (y.L == 1) { a.Arows = xr; a.ar_vs = 0; }
@@ -602,6 +610,27 @@ gevo_status gevo_check_bf16_rounding(void* hip_stream, uint64_t* d_counts) {
 
 // weights, biases and masks of every layer from the seed (and the caller's
 // base model, when given); genomes: masks from the pruning-edit lists
+// bias masks of every layer: unit n of variant v trains its bias when n < N
+// and, with structural edits (width[v][l], bias_keep[v][l-1]), n < the
+// layer's width and its bias is kept.  Synchronous upload.
+static gevo_status upload_bias_masks(gevo_pop* p, const std::vector<uint32_t>* width,
+                                     const std::vector<uint32_t>* bias_keep) {
+  const Layout& y = p->y;
+  for (int l = 0; l < y.L; ++l) {
+    const LayerLay& q = y.lay[l];
+    const int words = q.Np / 32;
+    std::vector<uint32_t> bits((size_t)y.P * words, 0u);
+    for (int v = 0; v < y.P; ++v) {
+      int keep_n = q.N;
+      if (width) keep_n = std::min<int>(keep_n, (int)(*width)[(size_t)v * (y.L + 1) + l + 1]);
+      if (bias_keep && !(*bias_keep)[(size_t)v * y.L + l]) keep_n = 0;
+      for (int n = 0; n < keep_n; ++n) bits[(size_t)v * words + n / 32] |= 1u << (n % 32);
+    }
+    HIP_TRY(hipMemcpy(p->ws + q.bmask, bits.data(), bits.size() * 4, hipMemcpyHostToDevice));
+  }
+  return GEVO_OK;
+}
+
 static gevo_status init_layers(gevo_pop* p, bool genomes) {
   const Layout& y = p->y;
   const gevo_pop_config* cfg = &p->cfg;
@@ -622,6 +651,9 @@ static gevo_status init_layers(gevo_pop* p, bool genomes) {
       a.prune_off = reinterpret_cast<const uint32_t*>(p->ws + y.prune_off);
       a.prune_id = reinterpret_cast<const uint32_t*>(p->ws + y.prune_id);
       a.prune_th = reinterpret_cast<const uint32_t*>(p->ws + y.prune_th);
+      a.width_in = reinterpret_cast<const uint32_t*>(p->ws + q.win);
+      a.width_out = reinterpret_cast<const uint32_t*>(p->ws + q.wout);
+      a.bias_keep = reinterpret_cast<const uint32_t*>(p->ws + q.bkeep);
     }
     a.Wm = reinterpret_cast<float*>(p->ws + q.Wm);
     a.bias = reinterpret_cast<float*>(p->ws + q.bias);
@@ -706,7 +738,8 @@ gevo_status gevo_pop_init(const gevo_pop_config* cfg, void* d_ws, size_t ws_byte
   }
   p->has_base = cfg->init == GEVO_INIT_BASE_NOISE && cfg->base_params;
   {
-    const gevo_status st = init_layers(p, false);
+    gevo_status st = upload_bias_masks(p, nullptr, nullptr);
+    if (st == GEVO_OK) st = init_layers(p, false);
     if (st != GEVO_OK) return fail(st);
   }
   // test split converted once to the operand type, padded to whole chunks
@@ -737,13 +770,20 @@ gevo_status gevo_pop_set_genomes(gevo_pop* p, float lr_base, const uint32_t* off
   for (int v = 0; v < P; ++v)
     if (offsets[v + 1] < offsets[v]) return GEVO_E_ARG;
   if (offsets[P] > 0 && !edits) return GEVO_E_ARG;
+  const int L = y.L;
   std::vector<float> lr(P);
   std::vector<double> dens(P);
   std::vector<uint32_t> off(P + 1, 0), ids, th;
+  std::vector<uint32_t> width((size_t)P * (L + 1)), bkeep((size_t)P * L, 1u);
+  double total_w = 0.0;
+  for (int l = 1; l <= L; ++l) total_w += (double)y.lay[l - 1].K * (double)y.lay[l - 1].N;
   for (int v = 0; v < P; ++v) {
     float r = lr_base;
     double d = 1.0;
     uint32_t np = 0;
+    uint32_t* wv = width.data() + (size_t)v * (L + 1);
+    wv[0] = (uint32_t)y.lay[0].K;
+    for (int l = 1; l <= L; ++l) wv[l] = (uint32_t)y.lay[l - 1].N;
     for (uint32_t i = offsets[v]; i < offsets[v + 1]; ++i) {
       const gevo_edit& e = edits[i];
       if (e.kind == GEVO_EDIT_LR) {
@@ -755,10 +795,19 @@ gevo_status gevo_pop_set_genomes(gevo_pop* p, float lr_base, const uint32_t* off
         ids.push_back(e.id);
         th.push_back(e.value);
         d = d * ((double)e.value / 16777216.0);
+      } else if (e.kind == GEVO_EDIT_WIDTH) {
+        if (e.id < 1 || (int)e.id > L - 1 || e.value == 0) return GEVO_E_ARG;
+        wv[e.id] = std::min(wv[e.id], e.value);
+      } else if (e.kind == GEVO_EDIT_BIAS_OFF) {
+        if (e.id < 1 || (int)e.id > L) return GEVO_E_ARG;
+        bkeep[(size_t)v * L + e.id - 1] = 0u;
       } else {
         return GEVO_E_ARG;
       }
     }
+    double kept_w = 0.0;
+    for (int l = 1; l <= L; ++l) kept_w += (double)wv[l - 1] * (double)wv[l];
+    d = d * (kept_w / total_w);
     if (!(r > 0.0f) || !std::isfinite(r)) return GEVO_E_ARG;
     lr[v] = r;
     dens[v] = d;
@@ -771,6 +820,21 @@ gevo_status gevo_pop_set_genomes(gevo_pop* p, float lr_base, const uint32_t* off
   if (!ids.empty()) {
     HIP_TRY(hipMemcpy(p->ws + y.prune_id, ids.data(), ids.size() * 4, hipMemcpyHostToDevice));
     HIP_TRY(hipMemcpy(p->ws + y.prune_th, th.data(), th.size() * 4, hipMemcpyHostToDevice));
+  }
+  for (int l = 0; l < L; ++l) {                  // per-layer structural arrays of the init kernel
+    std::vector<uint32_t> win(P), wout(P), bk(P);
+    for (int v = 0; v < P; ++v) {
+      win[v] = width[(size_t)v * (L + 1) + l];
+      wout[v] = width[(size_t)v * (L + 1) + l + 1];
+      bk[v] = bkeep[(size_t)v * L + l];
+    }
+    HIP_TRY(hipMemcpy(p->ws + y.lay[l].win, win.data(), (size_t)P * 4, hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(p->ws + y.lay[l].wout, wout.data(), (size_t)P * 4, hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(p->ws + y.lay[l].bkeep, bk.data(), (size_t)P * 4, hipMemcpyHostToDevice));
+  }
+  {
+    const gevo_status sb = upload_bias_masks(p, &width, &bkeep);
+    if (sb != GEVO_OK) return sb;
   }
   const gevo_status st = init_layers(p, true);
   if (st != GEVO_OK) return st;

@@ -185,6 +185,8 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
   }
   if (tid < 32) b2s[tid] = a.b2[(size_t)v * 32 + tid];
   float b1v = a.b1[(size_t)v * HP + n];
+  const bool b1k = (a.bm1[(size_t)v * (HP / 32) + wave] >> l32) & 1u;   // this unit's bias is trained
+  const bool b2k = tid < 32 && ((a.bm2[v] >> (tid & 31)) & 1u);          // class tid's bias is trained
   double ce_tot = 0.0;
   unsigned long long corr_tot = 0;
   const int tot_tid = (NW - 1) * 64;          // thread that keeps the loss / hit totals
@@ -392,7 +394,7 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
       float db = 0.0f;
 #pragma unroll
       for (int part = 0; part < Ly::NDP; ++part) db += dbp[part * 32 + tid];
-      b2s[tid] = __fsub_rn(b2s[tid], __fmul_rn(lrv, db));
+      b2s[tid] = b2k ? __fsub_rn(b2s[tid], __fmul_rn(lrv, db)) : 0.0f;
     }
     if (wave == NW - 1) {
       double sc = 0.0;
@@ -653,7 +655,7 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
       g1s[(wave * NBS + 2 * T + 1) * 64 + lane] = make_uint4(p[4], p[5], p[6], p[7]);
     }
     db1p += __shfl_xor(db1p, 32);
-    b1v = __fsub_rn(b1v, __fmul_rn(lrv, db1p));
+    b1v = b1k ? __fsub_rn(b1v, __fmul_rn(lrv, db1p)) : 0.0f;
     // ---- masked SGD on W2 (LDS master) and refresh of its bf16 operand
     {
       float f[16];

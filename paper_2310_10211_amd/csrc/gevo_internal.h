@@ -43,6 +43,11 @@ struct InitArgs {
   const uint32_t* prune_off;     // [P+1] (null: one edit per variant, (v, thresh[v]))
   const uint32_t* prune_id;
   const uint32_t* prune_th;
+  // optional structural edits: variant v keeps inputs k < width_in[v], units
+  // n < width_out[v] and, when bias_keep[v], their biases (null: everything)
+  const uint32_t* width_in;      // [P]
+  const uint32_t* width_out;     // [P]
+  const uint32_t* bias_keep;     // [P]
   float* Wm;                     // [P][Kp/32][Np][32] (k-blocked)
   float* bias;                   // [P][Np]
   uint32_t* mask;                // [P][Np][Kp/32] row words
@@ -56,6 +61,7 @@ struct LayerArgs {
   float* Wm;                     // [P][Kp/32][Np][32] fp32 master (k-blocked)
   float* bias;                   // [P][Np]
   const uint32_t* mask;          // [P][Np][Kp/32] row words: bit k%32 of word [n][k/32]
+  const uint32_t* bmask;         // [P][Np/32]: bit n%32 of word n/32 = bias n is trained
   const float* lr;               // [P]
   int do_update;
   const S* Gcols; size_t g_vs;   // [v][Np][Bp] gradient at this layer's output
@@ -85,6 +91,7 @@ struct OutArgs {
   float* Wm;                     // [P][Kp/32][32][32] (k-blocked)
   float* bias;                   // [P][32]
   const uint32_t* mask;          // [P][32][Kp/32] row words
+  const uint32_t* bmask;         // [P]: bit c = bias of class c is trained
   const float* lr;               // [P]
   int train;                     // 1: loss + backward + update on one batch; 0: predict chunk
   const S* Arows; size_t ar_vs;  // [v][rows][Kp]
@@ -124,6 +131,7 @@ struct Fused2Args {
   const int32_t* labels;         // [T][Bp]
   float* W1; float* b1; const uint32_t* m1;   // register image (see launch_w1_image), [P][Hp], [P][Kp/32][Hp]
   float* W2; float* b2; const uint32_t* m2;   // [P][Hp/32][32][32], [P][32], [P][32][Hp/32]
+  const uint32_t* bm1; const uint32_t* bm2;   // bias masks [P][Hp/32], [P] (bit = bias trained)
   const float* lr;
   double* ce_acc;
   unsigned long long* correct_acc;

@@ -47,6 +47,7 @@ __global__ __launch_bounds__(256) void k_init(InitArgs a) {
       for (int j = 0; j < 32; ++j) {
         const int k = kw * 32 + j;
         float w = 0.0f;
+        const bool kept_unit = !a.width_out || (n < (int)a.width_out[v] && k < (int)a.width_in[v]);
         if (n < a.N && k < a.K) {
           const uint64_t e = (uint64_t)n * (uint64_t)a.K + (uint64_t)k;
           bool keep;
@@ -85,12 +86,16 @@ __global__ __launch_bounds__(256) void k_init(InitArgs a) {
             const float eps = sqrtf(-2.0f * logf(u1)) * cosf(6.28318530717958647692f * u2);
             w = __fmul_rn(w, __fadd_rn(1.0f, __fmul_rn(a.noise_std, eps)));
           }
+          keep = keep && kept_unit;
           if (!keep) w = 0.0f;
           bits |= (uint32_t)keep << j;
         }
         wrow[j] = w;
       }
-      if (kw == 0) a.bias[(size_t)v * a.Np + n] = (a.base_b && n < a.N) ? a.base_b[n] : 0.0f;
+      if (kw == 0) {
+        const bool bk = n < a.N && (!a.width_out || (n < (int)a.width_out[v] && a.bias_keep[v]));
+        a.bias[(size_t)v * a.Np + n] = (a.base_b && bk) ? a.base_b[n] : 0.0f;
+      }
     }
     a.mask[((size_t)v * a.Np + n) * words + kw] = bits;
   }
@@ -147,7 +152,8 @@ __global__ __launch_bounds__(256, 2) void k_layer(LayerArgs<S> a) {
     s += __shfl_xor(s, 4);
     if (seg == 0) {
       const float bo = a.bias[(size_t)v * Np + n0 + nl];
-      const float bn = __fsub_rn(bo, __fmul_rn(lrv, s));
+      const bool bk = (a.bmask[(size_t)v * (Np / 32) + blockIdx.x] >> nl) & 1u;   // n0 = 32 blockIdx.x
+      const float bn = bk ? __fsub_rn(bo, __fmul_rn(lrv, s)) : 0.0f;
       a.bias[(size_t)v * Np + n0 + nl] = bn;
       bias_l[nl] = bn;
     }
@@ -495,7 +501,8 @@ __global__ __launch_bounds__(64 * kOutWaves) void k_out(OutArgs<S> a) {
     float db = 0.0f;
     for (int w = 0; w < NW; ++w) db += red_db[w][threadIdx.x];
     const float bo = a.bias[(size_t)v * 32 + threadIdx.x];
-    a.bias[(size_t)v * 32 + threadIdx.x] = __fsub_rn(bo, __fmul_rn(lrv, db));
+    const bool bk = (a.bmask[v] >> threadIdx.x) & 1u;
+    a.bias[(size_t)v * 32 + threadIdx.x] = bk ? __fsub_rn(bo, __fmul_rn(lrv, db)) : 0.0f;
   }
   // dW_L and the masked update of the master (old W_L stays in LDS): the dW
   // tile is staged in LDS, then lane (row rn, 16 columns) updates with float4

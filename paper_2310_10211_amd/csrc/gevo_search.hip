@@ -46,15 +46,36 @@ bool dominates(const double* a, const double* b, uint32_t m) {
   return smaller;
 }
 
-// the edit drawn from (j, gen, i, mutation stream): a learning-rate factor
-// log-uniform on [1/2, 2] or pruning at a density uniform on [rho_lo, 1]
-gevo_edit random_edit(uint64_t seed, uint32_t gen, uint32_t i, uint32_t j, uint32_t id, double rho_lo) {
+// shape of the nets a drawn structural edit applies to
+struct NetShape {
+  uint32_t L = 0;
+  const uint32_t* dims = nullptr;
+};
+
+// the edit drawn from (j, gen, i, mutation stream): with probability struct_p
+// a structural edit (bias removal, or a width of a hidden layer), otherwise a
+// learning-rate factor log-uniform on [1/2, 2] or pruning at a density
+// uniform on [rho_lo, 1], with equal odds
+gevo_edit random_edit(uint64_t seed, uint32_t gen, uint32_t i, uint32_t j, uint32_t id, double rho_lo,
+                      double struct_p, const NetShape& net) {
   uint32_t w[4];
   draw4(seed, j, gen, i, kStreamMut, w);
-  const double u = u24(w[2]);
+  const double u = u24(w[2]), uk = u24(w[1]);
   gevo_edit e{};
+  if (uk < struct_p) {
+    if (u24(w[3]) < 0.5 || net.L < 2) {
+      e.kind = GEVO_EDIT_BIAS_OFF;
+      e.id = 1 + below(w[0], net.L);
+      e.value = 0;
+    } else {
+      e.kind = GEVO_EDIT_WIDTH;
+      e.id = 1 + below(w[0], net.L - 1);
+      e.value = 1 + below(w[2], net.dims[e.id]);
+    }
+    return e;
+  }
   e.id = id;
-  if (u24(w[1]) < 0.5) {
+  if (uk < struct_p + (1.0 - struct_p) * 0.5) {
     e.kind = GEVO_EDIT_LR;
     e.value = float_bits((float)exp(log(0.5) + u * log(4.0)));
   } else {
@@ -62,6 +83,17 @@ gevo_edit random_edit(uint64_t seed, uint32_t gen, uint32_t i, uint32_t j, uint3
     e.value = (uint32_t)nearbyint((rho_lo + u * (1.0 - rho_lo)) * 16777216.0);   // round half to even
   }
   return e;
+}
+
+bool valid_shape(double struct_p, uint32_t n_layers, const uint32_t* dims, NetShape* net) {
+  if (!(struct_p >= 0.0 && struct_p <= 1.0)) return false;
+  if (struct_p == 0.0) return true;
+  if (n_layers < 1 || !dims) return false;
+  for (uint32_t l = 0; l <= n_layers; ++l)
+    if (dims[l] == 0) return false;
+  net->L = n_layers;
+  net->dims = dims;
+  return true;
 }
 
 bool valid_offsets(uint32_t n, const uint32_t* off) {
@@ -150,20 +182,24 @@ gevo_status gevo_nsga2_select(uint32_t n, const uint32_t* rank, const double* cr
 }
 
 gevo_status gevo_genomes_initial(uint32_t n, uint32_t n_mut, uint64_t seed, double rho_lo, uint32_t id_base,
-                                 gevo_edit* out) {
-  if (!(rho_lo >= 0.0 && rho_lo <= 1.0)) return GEVO_E_ARG;
+                                 double struct_p, uint32_t n_layers, const uint32_t* dims, gevo_edit* out) {
+  NetShape net;
+  if (!(rho_lo >= 0.0 && rho_lo <= 1.0) || !valid_shape(struct_p, n_layers, dims, &net)) return GEVO_E_ARG;
   if ((size_t)n * n_mut == 0) return GEVO_OK;
   if (!out) return GEVO_E_ARG;
   for (uint32_t i = 0; i < n; ++i)
-    for (uint32_t j = 0; j < n_mut; ++j) out[(size_t)n_mut * i + j] = random_edit(seed, 0, i, j, id_base + n_mut * i + j, rho_lo);
+    for (uint32_t j = 0; j < n_mut; ++j)
+      out[(size_t)n_mut * i + j] = random_edit(seed, 0, i, j, id_base + n_mut * i + j, rho_lo, struct_p, net);
   return GEVO_OK;
 }
 
 gevo_status gevo_genomes_breed(uint32_t n, const uint32_t* offsets, const gevo_edit* edits, uint64_t seed,
                                uint32_t gen, double cxpb, double mutpb, double rho_lo, uint32_t id_base,
-                               uint32_t max_edits, uint32_t* out_offsets, gevo_edit* out_edits,
-                               size_t out_capacity) {
-  if (gen == 0 || !valid_offsets(n, offsets) || !out_offsets) return GEVO_E_ARG;
+                               uint32_t max_edits, double struct_p, uint32_t n_layers, const uint32_t* dims,
+                               uint32_t* out_offsets, gevo_edit* out_edits, size_t out_capacity) {
+  NetShape net;
+  if (gen == 0 || !valid_offsets(n, offsets) || !out_offsets || !valid_shape(struct_p, n_layers, dims, &net))
+    return GEVO_E_ARG;
   if (!(cxpb >= 0.0 && cxpb <= 1.0) || !(mutpb >= 0.0 && mutpb <= 1.0) || !(rho_lo >= 0.0 && rho_lo <= 1.0))
     return GEVO_E_ARG;
   if (offsets[n] > 0 && !edits) return GEVO_E_ARG;
@@ -189,7 +225,8 @@ gevo_status gevo_genomes_breed(uint32_t n, const uint32_t* offsets, const gevo_e
   for (uint32_t i = 0; i < n; ++i) {
     uint32_t w[4];
     draw4(seed, 0, gen, i, kStreamMut, w);
-    if (u24(w[0]) < mutpb && kids[i].size() < max_edits) kids[i].push_back(random_edit(seed, gen, i, 1, id_base + i, rho_lo));
+    if (u24(w[0]) < mutpb && kids[i].size() < max_edits)
+      kids[i].push_back(random_edit(seed, gen, i, 1, id_base + i, rho_lo, struct_p, net));
   }
   size_t off = 0;
   out_offsets[0] = 0;

@@ -4,11 +4,14 @@ GPU, then ranked, selected and bred by the library's host code.
 
 An individual is a list of edits (patch representation, section 4.2) whose
 effects are a changed learning rate (section 6.2) and pruned weights
-(abstract).  Fitness (section 4.3) is minimised over two objectives:
+(abstract), optionally also removed biases (section 6.1) and narrowed
+hidden layers (the tensor-shrinking repair, section 4.1) with probability
+struct_p per drawn edit.  Fitness (section 4.3) is minimised over two objectives:
   * model error: the training-split error of the last epoch (the paper
     computes accuracy on the training split during the search and keeps the
     test split for checking the result afterwards, section 5);
-  * cost: the expected kept fraction of the weights.  The paper's second
+  * cost: the expected kept fraction of the weights (pruning densities times
+    the fraction the structural edits keep).  The paper's second
     objective is run time; here every variant runs the same dense kernels, so
     each individual's time is the same share of one launch, and the kept
     fraction stands for the time a pruned model saves.
@@ -40,12 +43,13 @@ class Generation:
 
 class Search:
     def __init__(self, pop: Population, lr_base: float, seed: int, epochs: int = 1, rho_lo: float = 0.3,
-                 n_elite: int = 16, cxpb: float = 0.8, mutpb: float = 0.5, max_edits: int = 16, n_mut: int = 3):
+                 n_elite: int = 16, cxpb: float = 0.8, mutpb: float = 0.5, max_edits: int = 16, n_mut: int = 3,
+                 struct_p: float = 0.0):
         if not 0 <= n_elite <= pop.P:
             raise ValueError("n_elite must be in [0, P]")
         self.pop, self.lr_base, self.seed, self.epochs = pop, float(lr_base), int(seed), int(epochs)
         self.rho_lo, self.n_elite, self.cxpb, self.mutpb = float(rho_lo), int(n_elite), float(cxpb), float(mutpb)
-        self.max_edits, self.n_mut = int(max_edits), int(n_mut)
+        self.max_edits, self.n_mut, self.struct_p = int(max_edits), int(n_mut), float(struct_p)
         self.history: list[Generation] = []
 
     def evaluate(self, genomes, carried=None) -> Generation:
@@ -70,7 +74,8 @@ class Search:
 
     def start(self) -> Generation:
         """Generation 0: n_mut drawn edits per individual (section 4)."""
-        genomes = genomes_initial(self.pop.P, self.seed, self.rho_lo, self.n_mut, id_base=0)
+        genomes = genomes_initial(self.pop.P, self.seed, self.rho_lo, self.n_mut, id_base=0, struct_p=self.struct_p,
+                                  dims=self.pop.dims)
         self.history = [self.evaluate(genomes)]
         return self.history[-1]
 
@@ -85,7 +90,8 @@ class Search:
         elites = [cur.genomes[i] for i in chosen[:self.n_elite]]
         parents = [cur.genomes[i] for i in chosen[self.n_elite:]]
         id_base = self.n_mut * P + (g - 1) * P            # fresh edit ids every generation
-        kids = genomes_breed(parents, self.seed, g, self.cxpb, self.mutpb, self.rho_lo, id_base, self.max_edits)
+        kids = genomes_breed(parents, self.seed, g, self.cxpb, self.mutpb, self.rho_lo, id_base, self.max_edits,
+                             self.struct_p, self.pop.dims)
         keep = list(chosen[:self.n_elite])
         self.history.append(self.evaluate(elites + kids, (cur.objectives[keep], cur.test_error[keep])))
         return self.history[-1]

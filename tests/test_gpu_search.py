@@ -137,3 +137,71 @@ def test_search_generations_are_deterministic_and_keep_elites():
         pop.close()
     for (ga, oa, ta), (gb, ob, tb) in zip(*runs):
         assert ga == gb and np.array_equal(oa, ob) and np.array_equal(ta, tb)
+
+
+def _struct_genomes(P, dims, seed):
+    gs = ns.initial(P, seed, 0.4, 3, 0, 0.6, dims)
+    L = len(dims) - 1
+    gs[0] = [(ns.BIAS_EDIT, L, 0)]                              # output biases removed
+    if L > 1:
+        gs[1] = [(ns.WIDTH_EDIT, 1, max(1, dims[1] // 3)), (ns.BIAS_EDIT, 1, 0)]
+        gs[2] = gs[2] + [(ns.WIDTH_EDIT, 1, dims[1] - 5), (ns.WIDTH_EDIT, 1, dims[1] - 9)]
+    return gs
+
+
+def _struct_reference(cfg, genome, lr_base):
+    dims = cfg["dims"]
+    lr, ids, th, _ = ns.apply(genome, lr_base)
+    widths, keep = ns.structure(genome, dims)
+    mask, bmask = oracle.structure_masks(dims, widths, keep, oracle.genome_mask(cfg["seed"], dims, ids, th))
+    full, _ = oracle.variant_init(cfg["seed"], 0, dims, 1 << 24)
+    params = full.copy()
+    off, moff, boff = 0, 0, 0
+    for l in range(1, len(dims)):
+        k = dims[l - 1] * dims[l]
+        params[off:off + k] *= mask[moff:moff + k]
+        params[off + k:off + k + dims[l]] *= bmask[boff:boff + dims[l]]
+        off += k + dims[l]
+        moff += k
+        boff += dims[l]
+    return lr, mask, bmask, params
+
+
+@pytest.mark.parametrize("i,dims", [(1, None), (3, None), (3, [200, 96, 64, 10])])
+def test_structural_genomes_rebuild_and_train_like_the_oracle(i, dims):
+    cfg, data = _small(i, P=4, n_train=640, n_test=256)
+    if dims:
+        cfg["dims"] = dims
+        for k in ("x_train", "x_test"):
+            data[k] = np.ascontiguousarray(data[k][:, :dims[0]])
+    mode = "bf16" if cfg["dtype"] == "bf16" else "f32"
+    rtol = 2e-2 if mode == "bf16" else 1e-4
+    pop = _pop(cfg, data)
+    genomes = _struct_genomes(4, cfg["dims"], 61)
+    lr, dens = pop.set_genomes(genomes, 0.05)
+    refs = [_struct_reference(cfg, genomes[v], 0.05) for v in range(4)]
+    for v in range(4):
+        e = pop.export(v)
+        r_lr, r_mask, r_bmask, r_params = refs[v]
+        assert np.array_equal(e["mask"], r_mask), v
+        assert np.array_equal(e["params"].astype(np.float64), r_params), v
+        assert lr[v] == np.float32(r_lr) and dens[v] == ns.density(genomes[v], cfg["dims"])
+    pop.train_epoch(0)
+    s = pop.scores()
+    n = len(data["y_train"])
+    perm = oracle.permutation(cfg["seed"], 0, n)
+    for v in range(4):
+        r_lr, r_mask, r_bmask, r_params = refs[v]
+        params = r_params.copy()
+        ce, _ = oracle.train_steps(mode, cfg["dims"], params, r_mask, float(r_lr), data["x_train"], data["y_train"],
+                                   perm, cfg["batch"], 0, -(-n // cfg["batch"]), bmask=r_bmask)
+        assert abs(float(s["train_loss"][v]) - ce / n) <= rtol * abs(ce / n), (v, s["train_loss"][v], ce / n)
+        e = pop.export(v)
+        off, boff = 0, 0
+        for l in range(1, len(cfg["dims"])):                   # removed biases are still +0
+            k = cfg["dims"][l - 1] * cfg["dims"][l]
+            b = e["params"][off + k:off + k + cfg["dims"][l]]
+            assert np.all(b[r_bmask[boff:boff + cfg["dims"][l]] == 0] == 0.0), (v, l)
+            off += k + cfg["dims"][l]
+            boff += cfg["dims"][l]
+    pop.close()

@@ -86,6 +86,28 @@ def test_search_entry_points_reject_bad_arguments():
     off = np.array([0, 2, 1], np.uint32)                                                     # decreasing offsets
     edits = (g.GevoEdit * 2)()
     oo = np.zeros(3, np.uint32)
-    assert L.gevo_genomes_breed(2, u32p(off), edits, 1, 1, 0.5, 0.5, 0.4, 0, 8, u32p(oo), edits, 8) == -1
+    assert L.gevo_genomes_breed(2, u32p(off), edits, 1, 1, 0.5, 0.5, 0.4, 0, 8, 0.0, 0, None, u32p(oo), edits,
+                                8) == -1
     good = np.array([0, 1, 2], np.uint32)
-    assert L.gevo_genomes_breed(2, u32p(good), edits, 1, 1, 0.5, 0.5, 0.4, 0, 8, u32p(oo), edits, 3) == -1
+    assert L.gevo_genomes_breed(2, u32p(good), edits, 1, 1, 0.5, 0.5, 0.4, 0, 8, 0.0, 0, None, u32p(oo), edits,
+                                3) == -1                                              # capacity below n + edits
+    with pytest.raises(g.GevoError):
+        g.genomes_initial(3, 1, 0.4, struct_p=0.5)                                   # structural draws need dims
+
+
+@pytest.mark.parametrize("dims,struct_p,seed", [([784, 256, 10], 0.3, 21), ([200, 96, 64, 10], 0.5, 22),
+                                                ([50, 10], 1.0, 23)])
+def test_structural_draws_match_the_oracle(dims, struct_p, seed):
+    _lib()
+    init = g.genomes_initial(40, seed, 0.4, 3, 0, struct_p, dims)
+    assert init == ns.initial(40, seed, 0.4, 3, 0, struct_p, dims)
+    kinds = {e[0] for ind in init for e in ind}
+    assert ns.BIAS_EDIT in kinds
+    if len(dims) > 2:
+        assert ns.WIDTH_EDIT in kinds
+        for ind in init:
+            for kind, l, w in ind:
+                if kind == ns.WIDTH_EDIT:
+                    assert 1 <= l <= len(dims) - 2 and 1 <= w <= dims[l]
+    kids = g.genomes_breed(init, seed, 2, 0.8, 1.0, 0.4, 500, 16, struct_p, dims)
+    assert kids == ns.breed(init, seed, 2, 0.8, 1.0, 0.4, 500, 16, struct_p, dims)

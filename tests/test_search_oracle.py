@@ -154,3 +154,74 @@ def test_genome_mask_extends_the_initial_masks():
     assert oracle.genome_mask(21, dims, [], []).all()          # no edit keeps everything
     n = both.size                                              # kept fraction near 1/2 * 3/4
     assert abs(both.mean() - 0.375) < 5 * math.sqrt(0.375 * 0.625 / n)
+
+
+def _narrow(params, dims, widths):
+    """Parameters of the network whose hidden layers keep their first widths[l] units."""
+    out, off = [], 0
+    for l in range(1, len(dims)):
+        din, dout = dims[l - 1], dims[l]
+        W = params[off:off + din * dout].reshape(din, dout)
+        b = params[off + din * dout:off + din * dout + dout]
+        out += [W[:widths[l - 1], :widths[l]].ravel(), b[:widths[l]]]
+        off += din * dout + dout
+    return np.concatenate(out)
+
+
+@pytest.mark.parametrize("mode", ["f64", "f32", "bf16"])
+def test_a_narrowed_net_computes_what_the_narrow_net_computes(mode):
+    """Structural width edits clear the weights into and out of the removed
+    units and their biases; training the wide net then equals training the
+    narrow net exactly (the removed units contribute exact zeros)."""
+    dims = [20, 12, 9, 4]
+    widths = [20, 7, 5, 4]
+    rng = np.random.default_rng(8)
+    params = rng.normal(0, 0.4, oracle.param_count(dims))
+    prune = (rng.random(oracle.weight_count(dims)) < 0.8).astype(np.uint8)
+    mask, bmask = oracle.structure_masks(dims, widths, [1, 1, 1], prune)
+    bias_off = 0
+    for l in range(1, len(dims)):                               # the wide net starts masked
+        off = sum(dims[j - 1] * dims[j] + dims[j] for j in range(1, l))
+        moff = sum(dims[j - 1] * dims[j] for j in range(1, l))
+        n = dims[l - 1] * dims[l]
+        params[off:off + n] *= mask[moff:moff + n]
+        params[off + n:off + n + dims[l]] *= bmask[bias_off:bias_off + dims[l]]
+        bias_off += dims[l]
+    X = rng.random((64, 20), dtype=np.float32)
+    y = rng.integers(0, 4, 64).astype(np.int32)
+    perm = np.arange(64, dtype=np.uint32)
+    wide = params.copy()
+    narrow = _narrow(params, dims, widths)
+    nmask = _narrow(np.concatenate([np.concatenate([mask[sum(dims[j - 1] * dims[j] for j in range(1, l)):][:dims[l - 1] * dims[l]],
+                                                    np.ones(dims[l])]) for l in range(1, len(dims))]).astype(np.float64),
+                    dims, widths)
+    nmask = np.concatenate([nmask[sum(widths[j - 1] * widths[j] + widths[j] for j in range(1, l)):][:widths[l - 1] * widths[l]]
+                            for l in range(1, len(dims))]).astype(np.uint8)
+    rw = oracle.train_steps(mode, dims, wide, mask, 0.1, X, y, perm, 16, 0, 4, bmask=bmask)
+    rn = oracle.train_steps(mode, widths, narrow, nmask, 0.1, X, y, perm, 16, 0, 4)
+    assert rw == rn
+    assert np.array_equal(_narrow(wide, dims, widths), narrow)
+
+
+def test_removed_biases_stay_zero_and_the_rest_trains():
+    dims = [10, 6, 3]
+    rng = np.random.default_rng(9)
+    params = rng.normal(0, 0.4, oracle.param_count(dims))
+    mask, bmask = oracle.structure_masks(dims, dims, [0, 1])
+    params[60:66] = 0.0                                         # layer-1 biases removed from the start
+    X = rng.random((32, 10), dtype=np.float32)
+    y = rng.integers(0, 3, 32).astype(np.int32)
+    before = params.copy()
+    oracle.train_steps("f64", dims, params, mask, 0.2, X, y, np.arange(32, dtype=np.uint32), 8, 0, 4, bmask=bmask)
+    assert np.all(params[60:66] == 0.0) and not np.array_equal(params[84:87], before[84:87])
+    assert list(bmask) == [0] * 6 + [1] * 3
+
+
+def test_structure_and_density_of_edit_lists():
+    dims = [100, 40, 20, 10]
+    edits = [(ns.WIDTH_EDIT, 1, 30), (ns.PRUNE_EDIT, 5, 2**23), (ns.WIDTH_EDIT, 1, 35), (ns.BIAS_EDIT, 3, 0),
+             (ns.WIDTH_EDIT, 2, 25)]
+    widths, keep = ns.structure(edits, dims)
+    assert widths == [100, 30, 20, 10] and keep == [1, 1, 0]
+    total = 100 * 40 + 40 * 20 + 20 * 10
+    assert ns.density(edits, dims) == 0.5 * ((100 * 30 + 30 * 20 + 20 * 10) / total)
