@@ -9,7 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libgevo.so")
 SOURCES = [os.path.join(HERE, "csrc", n)
-           for n in ("gevo_kernels.hip", "gevo_fused.hip", "gevo_gemm.hip", "gevo_search.hip", "gevo_capi.hip")]
+           for n in ("gevo_kernels.hip", "gevo_fused.hip", "gevo_gemm.hip", "gevo_stream.hip", "gevo_search.hip", "gevo_capi.hip")]
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
     "-ffp-contract=off",                                   # elementwise fp32 ops round one at a time
@@ -25,22 +25,29 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
+# kernels whose master prefetches are explicit loads with explicit waits
+PREFETCH_CHECKED = (("gevo_fused.hip", "_ZN4gevo8k_fused2"), ("gevo_stream.hip", "_ZN4gevo14k_stream_layer"))
+
+
 def check_fused_prefetch() -> dict:
-    """Compile the fused kernel to gfx950 assembly and verify its prefetch
-    register discipline (see check_prefetch.py)."""
+    """Compile the kernels with explicit prefetches to gfx950 assembly and
+    verify their prefetch register discipline (see check_prefetch.py)."""
     import tempfile
 
     from . import check_prefetch
+    found = {}
     with tempfile.TemporaryDirectory() as d:
-        out = os.path.join(d, "gevo_fused.s")
-        cmd = [hipcc(), *[f for f in FLAGS if f not in ("-fPIC", "-shared")], "--cuda-device-only", "-S",
-               "-I", os.path.join(ROOT, "include"), "-I", os.path.join(HERE, "csrc"),
-               "-o", out, os.path.join(HERE, "csrc", "gevo_fused.hip")]
-        res = subprocess.run(cmd, capture_output=True, text=True)
-        if res.returncode != 0:
-            raise RuntimeError("hipcc -S failed: " + res.stderr[-2000:])
-        with open(out) as f:
-            return check_prefetch.check_assembly(f.read())
+        for src, prefix in PREFETCH_CHECKED:
+            out = os.path.join(d, src[:-4] + ".s")
+            cmd = [hipcc(), *[f for f in FLAGS if f not in ("-fPIC", "-shared")], "--cuda-device-only", "-S",
+                   "-I", os.path.join(ROOT, "include"), "-I", os.path.join(HERE, "csrc"),
+                   "-o", out, os.path.join(HERE, "csrc", src)]
+            res = subprocess.run(cmd, capture_output=True, text=True)
+            if res.returncode != 0:
+                raise RuntimeError("hipcc -S failed: " + res.stderr[-2000:])
+            with open(out) as f:
+                found.update(check_prefetch.check_assembly(f.read(), prefix))
+    return found
 
 
 def build(verbose: bool = False) -> str:

@@ -1,6 +1,7 @@
-"""Build-time check of the register discipline of the fused training kernel.
+"""Build-time check of the register discipline of the streaming kernels (the
+fused two-layer training kernel and the hidden-layer kernel).
 
-The kernel issues its fp32 master prefetches as explicit load instructions
+The kernels issue their fp32 master prefetches as explicit load instructions
 (inline assembly) and waits for them with explicit ``s_waitcnt vmcnt(N)``
 instructions placed where the loaded values are first needed.  The compiler
 does not track such loads, so the generated code is only correct if, on every
@@ -8,7 +9,7 @@ path from a prefetch, no instruction reads or writes one of its destination
 registers before a wait that covers the prefetch.  Vector memory operations
 complete in issue order, so ``s_waitcnt vmcnt(N)`` covers a load once at least
 N further vector memory operations have been issued after it on that path.
-This module verifies the property on the kernel's gfx950 assembly, following
+This module verifies the property on the kernels' gfx950 assembly, following
 the control-flow graph (branches and fall-through) and counting the vector
 memory operations along each path, and raises if any path violates it.
 """
@@ -106,5 +107,5 @@ def check_assembly(asm: str, kernel_prefix: str = "_ZN4gevo8k_fused2") -> dict:
             raise RuntimeError(f"{name}: no prefetch blocks found; the check no longer matches the kernel")
         found[name] = blocks
     if not found:
-        raise RuntimeError("no instantiation of the fused kernel in the assembly")
+        raise RuntimeError(f"no instantiation of {kernel_prefix} in the assembly")
     return found

@@ -327,6 +327,10 @@ gevo_status forward_hidden(gevo_pop* p, const S* arows0, size_t ar0_vs, int R, i
         HIP_TRY(launch_fwd_gemm(g, p->stream, prof(p, GEVO_KERNEL_LAYER_FWD)));
         continue;
       }
+      if (!predict && stream_layer_supported(a.Kp, a.Np, a.Bp, a.R)) {
+        HIP_TRY(launch_stream_layer(a, y.P, p->stream, prof(p, GEVO_KERNEL_LAYER_FWD)));
+        continue;
+      }
     }
     HIP_TRY(launch_layer<S>(a, y.P, p->stream, prof(p, GEVO_KERNEL_LAYER_FWD)));
   }
@@ -439,6 +443,12 @@ gevo_status train_step(gevo_pop* p, int t) {
     }
     if (q.Wt) a.Wt = at<S>(p, q.Wt);
     if (a.Kp % kTile || a.Np % kTile || a.Bp % kTile || a.Bp > kPassRows) return GEVO_E_SHAPE;
+    if constexpr (std::is_same<S, uint16_t>::value) {
+      if (stream_layer_supported(a.Kp, a.Np, a.Bp, a.R)) {
+        HIP_TRY(launch_stream_layer(a, y.P, p->stream, prof(p, GEVO_KERNEL_LAYER_TRAIN)));
+        continue;
+      }
+    }
     HIP_TRY(launch_layer<S>(a, y.P, p->stream, prof(p, GEVO_KERNEL_LAYER_TRAIN)));
   }
   p->rows_done += bt;

@@ -180,6 +180,10 @@ hipError_t launch_mask_block_major(const uint32_t* src, uint32_t* dst, int P, in
 hipError_t launch_bf16_check(unsigned long long* counts, hipStream_t s);   // counts zeroed by the caller
 bool fwd_gemm_supported(int Kp, int Np, int R);   // Kp % 32, Np % 128, R % 256
 hipError_t launch_fwd_gemm(const FwdGemmArgs& a, hipStream_t s, const LaunchEv& ev);
+// bf16 hidden layer over one training batch (update and/or forward of the
+// next batch) streaming the fp32 master once; shapes outside these use k_layer
+bool stream_layer_supported(int Kp, int Np, int Bp, int R);
+hipError_t launch_stream_layer(const LayerArgs<uint16_t>& a, int P, hipStream_t s, const LaunchEv& ev);
 size_t fused2_lds_bytes(int hp, int bp);     // 0 when the shape has no fused instantiation
 hipError_t launch_reduce_partials(const double* part_ce, const unsigned int* part_corr, int P, int n_chunks,
                                   double* ce_out, unsigned long long* corr_out, hipStream_t s, const LaunchEv& ev);

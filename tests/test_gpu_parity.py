@@ -271,6 +271,31 @@ def test_bf16_three_layer():
     pop.close()
 
 
+@pytest.mark.parametrize("dims,batch,n_train", [
+    ([3072, 256, 128, 10], 256, 1300),    # both hidden layers on the streaming kernel, ragged tail of 20
+    ([512, 128, 256, 10], 100, 730),      # batch tile 128
+    ([3072, 192, 128, 10], 256, 800),     # first hidden layer on the blocked kernel (192 units), second streamed
+    ([3072, 256, 160, 10], 256, 700),     # second layer's 256 inputs streamed, 160 units on the blocked kernel
+    ([1024, 384, 256, 10], 128, 700),     # three 128-unit tiles per variant, batch tile 128
+])
+def test_bf16_deep_nets_on_the_streaming_layer_kernel(dims, batch, n_train):
+    """Hidden layers whose widths are multiples of 128 and whose inputs are
+    multiples of 64, at batch tiles 128 and 256, train through the streaming
+    hidden-layer kernel; the other layers of the same nets through the
+    blocked one."""
+    cfg, data = _small(5, P=3, n_train=n_train, n_test=400, dims=dims, batch=batch)
+    if dims[0] != 3072:
+        data["x_train"] = data["x_train"][:, :dims[0]].copy()
+        data["x_test"] = data["x_test"][:, :dims[0]].copy()
+    pop = _pop(cfg, data)
+    pop.train_epoch(0)
+    pop.predict()
+    s = pop.scores()
+    ref = oracle.evaluate(cfg, data, epochs=1)
+    _check_losses(s, ref, range(3), BF16_LOSS_RTOL)
+    pop.close()
+
+
 def test_fp32_three_layer():
     cfg, data = _small(2, P=3, n_train=700, n_test=300, dims=[784, 96, 64, 10], batch=64)
     pop = _pop(cfg, data)
