@@ -419,6 +419,12 @@ gevo_status train_step(gevo_pop* p, int t) {
     a.Gcols = at<S>(p, h.gcols); a.gc_vs = (size_t)h.Np * y.Bp;
     if (h.grows) { a.Grows_out = at<S>(p, h.grows); a.go_vs = (size_t)y.Bp * h.Np; }
     if (a.Kp % kTile || a.Np % kTile || a.Bp % kTile || a.Kp != h.Np) return GEVO_E_SHAPE;
+    if constexpr (std::is_same<S, uint16_t>::value) {
+      if (bwd_gemm_supported(a.Kp, a.Np, a.Bp)) {
+        HIP_TRY(launch_bwd_gemm(a, y.P, p->stream, prof(p, GEVO_KERNEL_BWD)));
+        continue;
+      }
+    }
     HIP_TRY(launch_bwd<S>(a, y.P, p->stream, prof(p, GEVO_KERNEL_BWD)));
   }
   // hidden layers bottom up: update, then the forward of step t+1

@@ -183,6 +183,9 @@ hipError_t launch_fwd_gemm(const FwdGemmArgs& a, hipStream_t s, const LaunchEv& 
 // bf16 hidden layer over one training batch (update and/or forward of the
 // next batch) streaming the fp32 master once; shapes outside these use k_layer
 bool stream_layer_supported(int Kp, int Np, int Bp, int R);
+// bf16 backward GEMM of a hidden layer (per variant, LDS-tiled); other shapes use k_bwd
+bool bwd_gemm_supported(int Kp, int Np, int Bp);
+hipError_t launch_bwd_gemm(const BwdArgs<uint16_t>& a, int P, hipStream_t s, const LaunchEv& ev);
 hipError_t launch_stream_layer(const LayerArgs<uint16_t>& a, int P, hipStream_t s, const LaunchEv& ev);
 size_t fused2_lds_bytes(int hp, int bp);     // 0 when the shape has no fused instantiation
 hipError_t launch_reduce_partials(const double* part_ce, const unsigned int* part_corr, int P, int n_chunks,
