@@ -85,6 +85,9 @@ def lib():
                                              f32p, f32p, u32p]
             L.or_variant_init.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int, u32p, ctypes.c_uint32,
                                           ctypes.c_int, f64p, ctypes.c_float, f64p, u8p]
+            L.or_tensor_init.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
+                                         ctypes.c_uint32, ctypes.c_uint32, ctypes.c_int, f64p, f64p, ctypes.c_float,
+                                         f64p, f64p, u8p]
             L.or_genome_mask.argtypes = [ctypes.c_uint64, ctypes.c_int, u32p, ctypes.c_uint32, u32p, u32p, u8p]
             L.or_permutation.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32, u32p]
             L.or_permutation.restype = None

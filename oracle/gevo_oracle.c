@@ -188,6 +188,47 @@ int or_variant_hparams(uint64_t seed, uint32_t v, float lr_lo, float lr_hi,
  *              Box-Muller, then the mask; biases are copied unperturbed.
  * Masked weights are exactly +0.
  */
+/* One weight tensor of variant v, viewed as din x dout with layer index li
+ * (the third Philox counter word), as section 4 builds the initial
+ * population: mask bit keep <=> u24 < thresh; W = Xavier draw (init_kind 0)
+ * or base * fl(1 + fl(std * eps)) (init_kind 1, eps by Box-Muller); W = +0
+ * where the mask drops it; biases 0 or the base's.  W is [din][dout]
+ * row-major, bias [dout], M [din][dout]; base_w/base_b may be NULL. */
+int or_tensor_init(uint64_t seed, uint32_t v, uint32_t li, uint32_t din, uint32_t dout, uint32_t thresh,
+                   int init_kind, const double* base_w, const double* base_b, float noise_std, double* W,
+                   double* bias, uint8_t* M) {
+  float a = (float)sqrt(6.0 / ((double)din + (double)dout));
+  for (uint32_t k = 0; k < din; ++k) {
+    for (uint32_t n = 0; n < dout; ++n) {
+      uint64_t e = (uint64_t)n * din + k;
+      uint32_t rm = draw_word(seed, (uint32_t)(e >> 2), li, v, OR_STREAM_MASK, (uint32_t)(e & 3));
+      int keep = (rm >> 8) < thresh;
+      double w;
+      if (init_kind == 1 && base_w != NULL) {
+        w = base_w[(size_t)k * dout + n];
+      } else {
+        uint32_t ri = draw_word(seed, (uint32_t)(e >> 2), li, 0, OR_STREAM_INIT, (uint32_t)(e & 3));
+        double t = 2.0 * u24_of(ri) - 1.0;      /* exact in binary32 */
+        w = f32(t * (double)a);
+      }
+      if (init_kind == 1) {
+        uint32_t c0 = (uint32_t)(e >> 1), w0 = (uint32_t)((e & 1) * 2);
+        uint32_t ra = draw_word(seed, c0, li, v, OR_STREAM_NOISE, w0);
+        uint32_t rb = draw_word(seed, c0, li, v, OR_STREAM_NOISE, w0 + 1);
+        double u1 = (double)((ra >> 8) + 1u) * (1.0 / 16777216.0);  /* (0,1] */
+        double u2 = u24_of(rb);
+        double eps = sqrt(-2.0 * log(u1)) * cos(2.0 * OR_PI * u2);
+        double s = f32(1.0 + f32((double)noise_std * f32(eps)));
+        w = f32(w * s);
+      }
+      W[(size_t)k * dout + n] = keep ? w : 0.0;
+      M[(size_t)k * dout + n] = (uint8_t)keep;
+    }
+  }
+  for (uint32_t n = 0; n < dout; ++n) bias[n] = (init_kind == 1 && base_b != NULL) ? base_b[n] : 0.0;
+  return 0;
+}
+
 int or_variant_init(uint64_t seed, uint32_t v, int L, const uint32_t* dims,
                     uint32_t thresh, int init_kind, const double* base, float noise_std,
                     double* params, uint8_t* mask) {
@@ -195,40 +236,9 @@ int or_variant_init(uint64_t seed, uint32_t v, int L, const uint32_t* dims,
   for (int l = 1; l <= L; ++l) {
     uint32_t din = dims[l - 1], dout = dims[l];
     double* W = params + w_off(dims, l);
-    double* bias = W + (size_t)din * dout;
-    uint8_t* M = mask + m_off(dims, l);
-    float a = (float)sqrt(6.0 / ((double)din + (double)dout));
-    for (uint32_t k = 0; k < din; ++k) {
-      for (uint32_t n = 0; n < dout; ++n) {
-        uint64_t e = (uint64_t)n * din + k;
-        uint32_t li = (uint32_t)(l - 1);
-        uint32_t rm = draw_word(seed, (uint32_t)(e >> 2), li, v, OR_STREAM_MASK, (uint32_t)(e & 3));
-        int keep = (rm >> 8) < thresh;
-        double w;
-        if (init_kind == 1 && base != NULL) {
-          w = base[w_off(dims, l) + (size_t)k * dout + n];
-        } else {
-          uint32_t ri = draw_word(seed, (uint32_t)(e >> 2), li, 0, OR_STREAM_INIT, (uint32_t)(e & 3));
-          double t = 2.0 * u24_of(ri) - 1.0;      /* exact in binary32 */
-          w = f32(t * (double)a);
-        }
-        if (init_kind == 1) {
-          uint32_t c0 = (uint32_t)(e >> 1), w0 = (uint32_t)((e & 1) * 2);
-          uint32_t ra = draw_word(seed, c0, li, v, OR_STREAM_NOISE, w0);
-          uint32_t rb = draw_word(seed, c0, li, v, OR_STREAM_NOISE, w0 + 1);
-          double u1 = (double)((ra >> 8) + 1u) * (1.0 / 16777216.0);  /* (0,1] */
-          double u2 = u24_of(rb);
-          double eps = sqrt(-2.0 * log(u1)) * cos(2.0 * OR_PI * u2);
-          double s = f32(1.0 + f32((double)noise_std * f32(eps)));
-          w = f32(w * s);
-        }
-        W[(size_t)k * dout + n] = keep ? w : 0.0;
-        M[(size_t)k * dout + n] = (uint8_t)keep;
-      }
-    }
-    for (uint32_t n = 0; n < dout; ++n) {
-      bias[n] = (init_kind == 1 && base != NULL) ? base[w_off(dims, l) + (size_t)din * dout + n] : 0.0;
-    }
+    const double* bw = base ? base + w_off(dims, l) : NULL;
+    or_tensor_init(seed, v, (uint32_t)(l - 1), din, dout, thresh, init_kind, bw, bw ? bw + (size_t)din * dout : NULL,
+                   noise_std, W, W + (size_t)din * dout, mask + m_off(dims, l));
   }
   return 0;
 }
