@@ -352,6 +352,82 @@ void gevo_pop_destroy(gevo_pop* pop);
 
 const char* gevo_status_str(gevo_status s);
 
+/* ------------------------------------------------------------------------
+ * Convolutional prediction workload (section 4.3: the prediction workload
+ * runs a model over a dataset and records its error; Table 1 lists
+ * MobileNet, a depthwise-separable convolutional net).  P variants of a
+ * CIFAR-shaped, MobileNet-like net are evaluated over a test set:
+ *   stem   3x3 convolution (stride 1, zero padding 1) C -> stem_channels,
+ *          bias, ReLU
+ *   block  3x3 depthwise convolution (stride 1 or 2, zero padding 1), bias,
+ *          ReLU; then 1x1 pointwise convolution -> block_channels[i], bias,
+ *          ReLU
+ *   head   global average pooling, fully connected -> classes, softmax
+ *          cross-entropy and argmax (lowest index on ties)
+ * Variant v is the caller's base model with every weight multiplied by
+ * fl(1 + fl(noise_rel_std * eps)) (eps standard normal, Box-Muller) and kept
+ * with probability rho_v ~ U[dens_lo, dens_hi] (a pruning edit, section
+ * 4.2); biases are the base's.  bf16 operands and activations, fp32
+ * accumulation and master weights.
+ *
+ * Canonical parameter layout (base_params, gevo_cnn_export): the tensors in
+ * order stem, (depthwise i, pointwise i) for each block, head; each as a
+ * K x N row-major matrix followed by its N biases:
+ *   stem        K = 9 C, row (3 dy + dx) C + c, N = stem_channels
+ *   depthwise   K = 9, row 3 dy + dx, N = the block's input channels
+ *   pointwise   K = input channels, N = block_channels[i]
+ *   head        K = last block_channels, N = classes
+ * Images are fp32 [n][height][width][channels] (NHWC), labels int32 in
+ * [0, classes).
+ * ------------------------------------------------------------------------ */
+#define GEVO_CNN_MAX_BLOCKS 4u
+
+typedef struct {
+  uint32_t abi_version;               /* must be GEVO_ABI_VERSION */
+  uint32_t P;                         /* variants, 1..65535 */
+  uint32_t height, width, channels;   /* input images; channels 1..4, sides 1..1024 */
+  uint32_t stem_channels;             /* multiple of 32, <= 512 */
+  uint32_t n_blocks;                  /* 1..GEVO_CNN_MAX_BLOCKS */
+  uint32_t block_stride[GEVO_CNN_MAX_BLOCKS];    /* 1 or 2 */
+  uint32_t block_channels[GEVO_CNN_MAX_BLOCKS];  /* multiples of 128, <= 1024 */
+  uint32_t classes;                   /* 2..32 */
+  uint64_t seed;                      /* counter-based draws of densities, masks, noise */
+  float dens_lo, dens_hi;             /* 0 <= lo <= hi <= 1 */
+  float noise_rel_std;                /* >= 0 */
+} gevo_cnn_config;
+
+typedef struct gevo_cnn gevo_cnn;     /* opaque handle */
+
+/* Number of floats of the canonical parameter vector.  GEVO_E_UNSUPPORTED
+ * for shapes outside the limits above or whose pointwise layers would see a
+ * row count (64 images x pixels) that is not a multiple of 256. */
+gevo_status gevo_cnn_param_count(const gevo_cnn_config* cfg, size_t* count);
+
+/* Device workspace for n_test test images (caller-owned, 256-byte aligned). */
+gevo_status gevo_cnn_workspace_bytes(const gevo_cnn_config* cfg, int64_t n_test, size_t* bytes);
+
+/* Builds the population on the device.  base_params: host array of
+ * gevo_cnn_param_count floats (read during the call).  d_test_x, d_test_y:
+ * device arrays that must outlive the handle.  Synchronous; labels outside
+ * [0, classes) give GEVO_E_SHAPE.  The library allocates no device memory. */
+gevo_status gevo_cnn_init(const gevo_cnn_config* cfg, void* d_ws, size_t ws_bytes, const float* base_params,
+                          const float* d_test_x, const int32_t* d_test_y, int64_t n_test, void* hip_stream,
+                          gevo_cnn** out);
+
+/* Runs every variant over the test set (asynchronous on the stream). */
+gevo_status gevo_cnn_predict(gevo_cnn* h);
+
+/* Mean test CE and accuracy per variant (host arrays of P, any may be NULL)
+ * and time_s = wall time of the last predict divided by P.  Synchronises;
+ * GEVO_E_ORDER before the first predict. */
+gevo_status gevo_cnn_scores(gevo_cnn* h, float* test_loss, float* test_acc, float* time_s);
+
+/* Variant v's parameters (canonical layout), mask (uint8 0/1 over the
+ * weights, same order) and density rho_v; any output may be NULL. */
+gevo_status gevo_cnn_export(gevo_cnn* h, uint32_t v, float* params_out, uint8_t* mask_out, float* density_out);
+
+void gevo_cnn_destroy(gevo_cnn* h);
+
 #ifdef __cplusplus
 }
 #endif

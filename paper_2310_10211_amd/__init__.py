@@ -38,7 +38,10 @@ EXPORTED = [
     "gevo_pop_set_profiling", "gevo_pop_kernel_stats", "gevo_pop_destroy", "gevo_status_str",
     "gevo_check_bf16_rounding", "gevo_nsga2_rank", "gevo_nsga2_select", "gevo_genomes_initial",
     "gevo_genomes_breed", "gevo_pop_set_genomes", "gevo_pop_set_grad_scale",
+    "gevo_cnn_param_count", "gevo_cnn_workspace_bytes", "gevo_cnn_init", "gevo_cnn_predict", "gevo_cnn_scores",
+    "gevo_cnn_export", "gevo_cnn_destroy",
 ]
+CNN_MAX_BLOCKS = 4
 KERNEL_KINDS = ["init", "gather", "layer_train", "layer_fwd", "out_train", "out_predict", "bwd", "aux",
                 "fused_train"]
 
@@ -52,6 +55,35 @@ class GevoEdit(ctypes.Structure):
 
 
 EDIT_LR, EDIT_PRUNE, EDIT_WIDTH, EDIT_BIAS_OFF = 0, 1, 2, 3
+
+
+class GevoCnnConfig(ctypes.Structure):
+    _fields_ = [
+        ("abi_version", ctypes.c_uint32), ("P", ctypes.c_uint32),
+        ("height", ctypes.c_uint32), ("width", ctypes.c_uint32), ("channels", ctypes.c_uint32),
+        ("stem_channels", ctypes.c_uint32), ("n_blocks", ctypes.c_uint32),
+        ("block_stride", ctypes.c_uint32 * CNN_MAX_BLOCKS), ("block_channels", ctypes.c_uint32 * CNN_MAX_BLOCKS),
+        ("classes", ctypes.c_uint32), ("seed", ctypes.c_uint64),
+        ("dens_lo", ctypes.c_float), ("dens_hi", ctypes.c_float), ("noise_rel_std", ctypes.c_float),
+    ]
+
+
+def cnn_config_struct(cfg: dict) -> GevoCnnConfig:
+    """cfg keys: P, H, W, C, stem, blocks [(stride, channels)], classes, seed,
+    dens (lo, hi), noise_std."""
+    c = GevoCnnConfig()
+    c.abi_version = 1
+    c.P = cfg["P"]
+    c.height, c.width, c.channels = cfg["H"], cfg["W"], cfg["C"]
+    c.stem_channels = cfg["stem"]
+    c.n_blocks = len(cfg["blocks"])
+    for i, (st, ch) in enumerate(cfg["blocks"][:CNN_MAX_BLOCKS]):
+        c.block_stride[i], c.block_channels[i] = st, ch
+    c.classes = cfg["classes"]
+    c.seed = cfg["seed"]
+    c.dens_lo, c.dens_hi = cfg.get("dens", (1.0, 1.0))
+    c.noise_rel_std = cfg.get("noise_std", 0.0)
+    return c
 
 
 class GevoPopConfig(ctypes.Structure):
@@ -117,6 +149,15 @@ def lib():
                                          ctypes.c_size_t]
         L.gevo_pop_set_genomes.argtypes = [vp, ctypes.c_float, u32p, editp, f32p, f64p]
         L.gevo_pop_set_grad_scale.argtypes = [vp, f32p]
+        ccfgp = ctypes.POINTER(GevoCnnConfig)
+        L.gevo_cnn_param_count.argtypes = [ccfgp, ctypes.POINTER(ctypes.c_size_t)]
+        L.gevo_cnn_workspace_bytes.argtypes = [ccfgp, i64, ctypes.POINTER(ctypes.c_size_t)]
+        L.gevo_cnn_init.argtypes = [ccfgp, vp, ctypes.c_size_t, f32p, vp, vp, i64, vp, ctypes.POINTER(vp)]
+        L.gevo_cnn_predict.argtypes = [vp]
+        L.gevo_cnn_scores.argtypes = [vp, f32p, f32p, f32p]
+        L.gevo_cnn_export.argtypes = [vp, u32, f32p, ctypes.POINTER(ctypes.c_uint8), f32p]
+        L.gevo_cnn_destroy.argtypes = [vp]
+        L.gevo_cnn_destroy.restype = None
         L.gevo_pop_destroy.argtypes = [vp]
         L.gevo_pop_destroy.restype = None
         L.gevo_status_str.argtypes = [ctypes.c_int]
@@ -415,3 +456,81 @@ class Population:
             self.close()
         except Exception:
             pass
+
+
+def cnn_param_count(cfg: dict) -> int:
+    n = ctypes.c_size_t()
+    c = cnn_config_struct(cfg)
+    _check(lib().gevo_cnn_param_count(ctypes.byref(c), ctypes.byref(n)), "gevo_cnn_param_count")
+    return n.value
+
+
+class CnnPopulation:
+    """P variants of the convolutional prediction workload on one GPU; all
+    device memory comes from torch."""
+
+    def __init__(self, cfg: dict, base_params, x_test, y_test, device="cuda", stream=None):
+        import torch
+        self.torch = torch
+        self.cfg = dict(cfg)
+        self.P = cfg["P"]
+        dev = torch.device(device)
+        self.x_test = torch.as_tensor(x_test).to(device=dev, dtype=torch.float32).contiguous()
+        self.y_test = torch.as_tensor(y_test).to(device=dev, dtype=torch.int32).contiguous()
+        n = self.x_test.shape[0]
+        assert self.x_test.shape == (n, cfg["H"], cfg["W"], cfg["C"]) and self.y_test.shape == (n,)
+        self.n_test = n
+        self._cfg = cnn_config_struct(cfg)
+        base = np.ascontiguousarray(np.asarray(base_params, dtype=np.float32))
+        assert base.size == cnn_param_count(cfg)
+        nbytes = ctypes.c_size_t()
+        _check(lib().gevo_cnn_workspace_bytes(ctypes.byref(self._cfg), n, ctypes.byref(nbytes)),
+               "gevo_cnn_workspace_bytes")
+        self.workspace = torch.empty(max(nbytes.value, 256), dtype=torch.uint8, device=dev)
+        self.stream = stream if stream is not None else torch.cuda.current_stream(dev)
+        h = ctypes.c_void_p()
+        _check(lib().gevo_cnn_init(ctypes.byref(self._cfg), ctypes.c_void_p(self.workspace.data_ptr()), nbytes.value,
+                                   _fp(base), ctypes.c_void_p(self.x_test.data_ptr()),
+                                   ctypes.c_void_p(self.y_test.data_ptr()), n,
+                                   ctypes.c_void_p(self.stream.cuda_stream), ctypes.byref(h)), "gevo_cnn_init")
+        self._h = h
+
+    def predict(self):
+        _check(lib().gevo_cnn_predict(self._h), "gevo_cnn_predict")
+
+    def scores(self) -> dict:
+        loss = np.zeros(self.P, np.float32)
+        acc = np.zeros(self.P, np.float32)
+        t = np.zeros(self.P, np.float32)
+        _check(lib().gevo_cnn_scores(self._h, _fp(loss), _fp(acc), _fp(t)), "gevo_cnn_scores")
+        return {"test_loss": loss, "test_acc": acc, "time_s": t}
+
+    def export(self, v: int) -> dict:
+        n = cnn_param_count(self.cfg)
+        params = np.zeros(n, np.float32)
+        nw = n - _cnn_bias_count(self.cfg)
+        mask = np.zeros(nw, np.uint8)
+        dens = np.zeros(1, np.float32)
+        _check(lib().gevo_cnn_export(self._h, v, _fp(params), mask.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)),
+                                     _fp(dens)), "gevo_cnn_export")
+        return {"params": params, "mask": mask, "density": float(dens[0])}
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            lib().gevo_cnn_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _cnn_bias_count(cfg: dict) -> int:
+    n = cfg["stem"]
+    c = cfg["stem"]
+    for _, co in cfg["blocks"]:
+        n += c + co
+        c = co
+    return n + cfg["classes"]

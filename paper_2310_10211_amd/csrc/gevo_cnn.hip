@@ -1,0 +1,526 @@
+// Convolutional prediction workload (section 4.3: the prediction workload
+// runs a model over a dataset and records its error; Table 1 lists MobileNet,
+// a depthwise-separable convolutional net, among the models): P variants of a
+// CIFAR-shaped MobileNet-like net, each the caller's base weights times
+// fl(1 + fl(std eps)) under its own Bernoulli(rho_v) mask (section 4.2's
+// pruning edits, as in the fully connected workload 4), evaluated over a test
+// set.  Per 64-image chunk and for all variants at once:
+//   stem   3x3 convolution, stride 1, zero padding 1, bias, ReLU  (k_cnn_stem)
+//   block  3x3 depthwise convolution, stride 1|2, bias, ReLU      (k_cnn_dw)
+//          1x1 pointwise convolution = a per-variant GEMM over the
+//          chunk's pixels, bias, ReLU                             (k_fwd_gemm)
+//   head   global average pooling                                 (k_cnn_pool)
+//          fully connected layer, softmax cross-entropy, argmax   (k_out)
+// bf16 operands and activations, fp32 accumulation, fp32 master weights.
+#include "gevo_internal.h"
+#include "gevo_device.h"
+#include "gevo.h"
+
+#include <hip/hip_ext.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <vector>
+
+namespace gevo {
+
+namespace {
+
+constexpr int kCnnChunk = 64;            // images per prediction chunk
+constexpr int kCnnRows = kOutRows;       // pooled rows per chunk handed to the output kernel (padded)
+
+struct CnnStemArgs {
+  const float* x; int64_t n_test; int img0;   // test images [n][H][W][C] fp32, first image of the chunk
+  int H, W, C;
+  int K, Kp, Np;                              // stem tensor: K = 9C inputs, Np output channels
+  const float* Wm; const float* bias;         // [P][Kp/32][Np][32], [P][Np]
+  uint16_t* out; size_t out_vs;               // [v][chunk][H][W][Np] bf16
+};
+
+struct CnnDwArgs {
+  const uint16_t* in; size_t in_vs;           // [v][chunk][H][W][C]
+  uint16_t* out; size_t out_vs;               // [v][chunk][Ho][Wo][C]
+  int H, W, C, Ho, Wo, stride;
+  const float* Wm; const float* bias;         // filter taps of channel c at [v][c][32] (first 9), [P][C]
+};
+
+struct CnnPoolArgs {
+  const uint16_t* in; size_t in_vs;           // [v][chunk][HW][C]
+  int HW, C;
+  uint16_t* out; size_t out_vs;               // [v][kCnnRows][C]; rows past the chunk are zero
+};
+
+__device__ __forceinline__ float bf16r(float f) { return bf16_bits_to_f32(f32_to_bf16_bits(f)); }
+
+}  // namespace
+
+// stem: one thread per output pixel of one variant, all output channels;
+// the variant's weights, rounded to bf16, sit in LDS as [k][Np]
+__global__ __launch_bounds__(256) void k_cnn_stem(CnnStemArgs a) {
+  extern __shared__ float wl[];
+  const int v = blockIdx.y, Np = a.Np, K = a.K;
+  const float* Wv = a.Wm + (size_t)v * Np * a.Kp;
+  for (int i = threadIdx.x; i < K * Np; i += blockDim.x) {
+    const int k = i / Np, n = i % Np;
+    wl[i] = bf16r(Wv[((size_t)(k / 32) * Np + n) * 32 + k % 32]);
+  }
+  __syncthreads();
+  const int HW = a.H * a.W;
+  const int p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= kCnnChunk * HW) return;
+  const int img = p / HW, y = (p % HW) / a.W, x = p % a.W;
+  const int64_t g = (int64_t)a.img0 + img;
+  const bool valid = g < a.n_test;
+  float patch[36];                                     // 9 C <= 36 inputs, k = (3 dy + dx) C + c
+#pragma unroll
+  for (int k = 0; k < 36; ++k) patch[k] = 0.0f;
+  for (int dy = 0; dy < 3; ++dy)
+    for (int dx = 0; dx < 3; ++dx) {
+      const int yy = y + dy - 1, xx = x + dx - 1;
+      if (valid && yy >= 0 && yy < a.H && xx >= 0 && xx < a.W)
+        for (int c = 0; c < a.C; ++c)
+          patch[(3 * dy + dx) * a.C + c] = bf16r(a.x[((g * a.H + yy) * a.W + xx) * a.C + c]);
+    }
+  const float* bv = a.bias + (size_t)v * Np;
+  uint16_t* o = a.out + a.out_vs * v + (size_t)p * Np;
+  for (int n0 = 0; n0 < Np; n0 += 8) {
+    float acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = 0.0f;
+    for (int k = 0; k < K; ++k) {
+      const float pk = patch[k];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[j] = __fmaf_rn(pk, wl[k * Np + n0 + j], acc[j]);
+    }
+    float f[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float z = acc[j] + bv[n0 + j];
+      f[j] = z > 0.0f ? z : 0.0f;
+    }
+    uint32_t pk[4];
+    to_bf16x2(f, pk);
+    *reinterpret_cast<uint4*>(o + n0) = make_uint4(pk[0], pk[1], pk[2], pk[3]);
+  }
+}
+
+// depthwise 3x3: one thread per output pixel and 8 channels of one variant
+__global__ __launch_bounds__(256) void k_cnn_dw(CnnDwArgs a) {
+  extern __shared__ float dl[];                        // taps [9][C], then bias [C]
+  const int v = blockIdx.y, C = a.C;
+  for (int i = threadIdx.x; i < 9 * C; i += blockDim.x) {
+    const int t = i / C, c = i % C;
+    dl[i] = bf16r(a.Wm[((size_t)v * C + c) * 32 + t]);
+  }
+  for (int c = threadIdx.x; c < C; c += blockDim.x) dl[9 * C + c] = a.bias[(size_t)v * C + c];
+  __syncthreads();
+  const int C8 = C / 8, HWo = a.Ho * a.Wo;
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= kCnnChunk * HWo * C8) return;
+  const int c0 = (i % C8) * 8, pix = i / C8;
+  const int img = pix / HWo, yo = (pix % HWo) / a.Wo, xo = pix % a.Wo;
+  const uint16_t* src = a.in + a.in_vs * v + (size_t)img * a.H * a.W * C;
+  float acc[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) acc[j] = 0.0f;
+  for (int dy = 0; dy < 3; ++dy)
+    for (int dx = 0; dx < 3; ++dx) {
+      const int yy = a.stride * yo + dy - 1, xx = a.stride * xo + dx - 1;
+      if (yy < 0 || yy >= a.H || xx < 0 || xx >= a.W) continue;
+      const uint4 q = *reinterpret_cast<const uint4*>(src + ((size_t)yy * a.W + xx) * C + c0);
+      const uint32_t w4[4] = {q.x, q.y, q.z, q.w};
+      const float* tw = dl + (3 * dy + dx) * C + c0;
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        acc[j] = __fmaf_rn(bf16_bits_to_f32((uint16_t)(w4[j >> 1] >> (16 * (j & 1)))), tw[j], acc[j]);
+    }
+  float f[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const float z = acc[j] + dl[9 * C + c0 + j];
+    f[j] = z > 0.0f ? z : 0.0f;
+  }
+  uint32_t pk[4];
+  to_bf16x2(f, pk);
+  *reinterpret_cast<uint4*>(a.out + a.out_vs * v + (size_t)pix * C + c0) = make_uint4(pk[0], pk[1], pk[2], pk[3]);
+}
+
+// global average pooling: one thread per pooled row (image) and 8 channels
+__global__ __launch_bounds__(256) void k_cnn_pool(CnnPoolArgs a) {
+  const int v = blockIdx.y, C8 = a.C / 8;
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= kCnnRows * C8) return;
+  const int row = i / C8, c0 = (i % C8) * 8;
+  float f[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) f[j] = 0.0f;
+  if (row < kCnnChunk) {
+    const uint16_t* src = a.in + a.in_vs * v + (size_t)row * a.HW * a.C + c0;
+    for (int p = 0; p < a.HW; ++p) {
+      const uint4 q = *reinterpret_cast<const uint4*>(src + (size_t)p * a.C);
+      const uint32_t w4[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+      for (int j = 0; j < 8; ++j) f[j] += bf16_bits_to_f32((uint16_t)(w4[j >> 1] >> (16 * (j & 1))));
+    }
+    const float inv = 1.0f / (float)a.HW;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) f[j] *= inv;
+  }
+  uint32_t pk[4];
+  to_bf16x2(f, pk);
+  *reinterpret_cast<uint4*>(a.out + a.out_vs * v + (size_t)row * a.C + c0) = make_uint4(pk[0], pk[1], pk[2], pk[3]);
+}
+
+namespace {
+
+int round_up32(int x) { return (x + 31) / 32 * 32; }
+
+// word `word` of the Philox4x32-10 block at counter (c0, c1, c2, stream), key seed
+uint32_t draw_word(uint64_t seed, uint32_t c0, uint32_t c1, uint32_t c2, uint32_t stream, uint32_t word) {
+  const uint32_t ctr[4] = {c0, c1, c2, stream};
+  const uint32_t key[2] = {(uint32_t)(seed & 0xffffffffu), (uint32_t)(seed >> 32)};
+  uint32_t out[4];
+  philox4x32_10_host(ctr, key, out);
+  return out[word];
+}
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct CnnTensor {
+  int K = 0, N = 0, Kp = 0, Np = 0;
+  size_t Wm = 0, bias = 0, mask = 0, base_w = 0, base_b = 0;
+};
+
+struct CnnLayout {
+  int P = 0, nb = 0, H = 0, W = 0, C = 0, classes = 0, n_chunks = 0;
+  int64_t n_test = 0;
+  int stem = 0, ch[GEVO_CNN_MAX_BLOCKS] = {0}, stride[GEVO_CNN_MAX_BLOCKS] = {0};
+  int hin[GEVO_CNN_MAX_BLOCKS + 1] = {0}, win[GEVO_CNN_MAX_BLOCKS + 1] = {0};   // spatial size entering block i (last: the head)
+  int nt = 0;
+  CnnTensor t[2 * GEVO_CNN_MAX_BLOCKS + 2];  // stem, (dw, pw) per block, fc
+  size_t act_vs = 0;                          // elements per variant of an activation buffer
+  size_t thresh = 0, aux = 0, actA = 0, actB = 0, pooled = 0, labels = 0, part_ce = 0, part_corr = 0;
+  size_t test_ce = 0, test_corr = 0, total = 0;
+};
+
+gevo_status cnn_layout(const gevo_cnn_config* c, int64_t n_test, CnnLayout& y) {
+  if (!c || c->abi_version != GEVO_ABI_VERSION) return GEVO_E_ARG;
+  if (c->P < 1 || c->height < 1 || c->width < 1 || c->channels < 1 || n_test < 1) return GEVO_E_ARG;
+  if (c->n_blocks < 1 || c->n_blocks > GEVO_CNN_MAX_BLOCKS) return GEVO_E_UNSUPPORTED;
+  if (c->channels > 4 || c->stem_channels % 32 || c->stem_channels == 0 || c->stem_channels > 512)
+    return GEVO_E_UNSUPPORTED;
+  if (c->classes < 2 || c->classes > 32) return GEVO_E_UNSUPPORTED;
+  if (c->height > 1024 || c->width > 1024 || c->P > 65535) return GEVO_E_UNSUPPORTED;
+  if (!(c->dens_lo >= 0.0f && c->dens_hi <= 1.0f && c->dens_lo <= c->dens_hi)) return GEVO_E_ARG;
+  if (!(c->noise_rel_std >= 0.0f)) return GEVO_E_ARG;
+  y.P = (int)c->P; y.nb = (int)c->n_blocks; y.H = (int)c->height; y.W = (int)c->width; y.C = (int)c->channels;
+  y.classes = (int)c->classes; y.n_test = n_test; y.stem = (int)c->stem_channels;
+  y.n_chunks = (int)((n_test + kCnnChunk - 1) / kCnnChunk);
+  int h = y.H, w = y.W, ch = y.stem;
+  size_t act = (size_t)kCnnChunk * h * w * ch;
+  y.nt = 0;
+  auto add = [&](int K, int N, int Np) {
+    CnnTensor& t = y.t[y.nt++];
+    t.K = K; t.N = N; t.Kp = round_up32(K); t.Np = Np;
+  };
+  add(9 * y.C, y.stem, y.stem);
+  for (int i = 0; i < y.nb; ++i) {
+    const int s = (int)c->block_stride[i], co = (int)c->block_channels[i];
+    if ((s != 1 && s != 2) || co % 128 || co == 0 || co > 1024) return GEVO_E_UNSUPPORTED;
+    y.hin[i] = h; y.win[i] = w; y.stride[i] = s; y.ch[i] = co;
+    h = (h - 1) / s + 1;
+    w = (w - 1) / s + 1;
+    if (((size_t)kCnnChunk * h * w) % 256) return GEVO_E_UNSUPPORTED;   // pointwise GEMM rows
+    add(9, ch, ch);                                   // depthwise taps of each channel
+    add(ch, co, co);                                  // pointwise
+    act = std::max(act, (size_t)kCnnChunk * h * w * std::max(ch, co));
+    ch = co;
+  }
+  y.hin[y.nb] = h; y.win[y.nb] = w;
+  add(ch, y.classes, 32);                             // head, in the output kernel's 32-class layout
+  if ((size_t)9 * y.C * y.stem * 4 > 65536) return GEVO_E_UNSUPPORTED;
+  y.act_vs = act;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { const size_t at = off; off = align256(off + bytes); return at; };
+  const size_t P = (size_t)y.P;
+  for (int i = 0; i < y.nt; ++i) {
+    CnnTensor& t = y.t[i];
+    t.Wm = take(P * t.Np * t.Kp * 4);
+    t.bias = take(P * t.Np * 4);
+    t.mask = take(P * t.Np * (t.Kp / 32) * 4);
+    t.base_w = take((size_t)t.Np * t.Kp * 4);
+    t.base_b = take((size_t)t.Np * 4);
+  }
+  y.thresh = take(P * 4);
+  y.aux = take(P * 4);                                // learning rates and bias bits the output kernel reads
+  y.actA = take(P * y.act_vs * 2);
+  y.actB = take(P * y.act_vs * 2);
+  y.pooled = take(P * kCnnRows * ch * 2);
+  y.labels = take((size_t)y.n_chunks * kCnnRows * 4);
+  y.part_ce = take(P * y.n_chunks * 8);
+  y.part_corr = take(P * y.n_chunks * 4);
+  y.test_ce = take(P * 8);
+  y.test_corr = take(P * 8);
+  y.total = off;
+  return GEVO_OK;
+}
+
+template <typename T>
+T* at(char* ws, size_t off) { return reinterpret_cast<T*>(ws + off); }
+
+}  // namespace
+
+}  // namespace gevo
+
+using namespace gevo;
+
+struct gevo_cnn {
+  gevo_cnn_config cfg{};
+  CnnLayout y;
+  char* ws = nullptr;
+  hipStream_t stream = nullptr;
+  const float* teX = nullptr;
+  hipEvent_t ev0 = nullptr, ev1 = nullptr;
+  bool predicted = false, timing_pending = false;
+  double last_s = 0.0;
+  std::vector<float> dens;
+};
+
+#define CNN_HIP(x)                              \
+  do {                                          \
+    if ((x) != hipSuccess) return GEVO_E_HIP;   \
+  } while (0)
+
+extern "C" {
+
+gevo_status gevo_cnn_param_count(const gevo_cnn_config* cfg, size_t* count) {
+  if (!count) return GEVO_E_ARG;
+  CnnLayout y;
+  const gevo_status st = cnn_layout(cfg, 1, y);
+  if (st != GEVO_OK) return st;
+  size_t n = 0;
+  for (int i = 0; i < y.nt; ++i) n += (size_t)y.t[i].K * y.t[i].N + y.t[i].N;
+  *count = n;
+  return GEVO_OK;
+}
+
+gevo_status gevo_cnn_workspace_bytes(const gevo_cnn_config* cfg, int64_t n_test, size_t* bytes) {
+  if (!bytes) return GEVO_E_ARG;
+  CnnLayout y;
+  const gevo_status st = cnn_layout(cfg, n_test, y);
+  if (st != GEVO_OK) return st;
+  *bytes = y.total;
+  return GEVO_OK;
+}
+
+void gevo_cnn_destroy(gevo_cnn* h) {
+  if (!h) return;
+  if (h->ev0) (void)hipEventDestroy(h->ev0);
+  if (h->ev1) (void)hipEventDestroy(h->ev1);
+  delete h;
+}
+
+gevo_status gevo_cnn_init(const gevo_cnn_config* cfg, void* d_ws, size_t ws_bytes, const float* base_params,
+                          const float* d_test_x, const int32_t* d_test_y, int64_t n_test, void* hip_stream,
+                          gevo_cnn** out) {
+  if (!out) return GEVO_E_ARG;
+  *out = nullptr;
+  CnnLayout y;
+  gevo_status st = cnn_layout(cfg, n_test, y);
+  if (st != GEVO_OK) return st;
+  if (!d_ws || !base_params || !d_test_x || !d_test_y) return GEVO_E_ARG;
+  if (ws_bytes < y.total || (reinterpret_cast<uintptr_t>(d_ws) & 255)) return GEVO_E_WORKSPACE;
+  gevo_cnn* h = new (std::nothrow) gevo_cnn;
+  if (!h) return GEVO_E_ARG;
+  h->cfg = *cfg;
+  h->y = y;
+  h->ws = reinterpret_cast<char*>(d_ws);
+  h->stream = reinterpret_cast<hipStream_t>(hip_stream);
+  h->teX = d_test_x;
+  auto fail = [&](gevo_status s) { gevo_cnn_destroy(h); return s; };
+  if (hipEventCreate(&h->ev0) != hipSuccess || hipEventCreate(&h->ev1) != hipSuccess) return fail(GEVO_E_HIP);
+  const int P = y.P;
+  // per-variant density and mask threshold (host, fp64), drawn as for the
+  // fully connected populations (stream kStreamDens)
+  std::vector<uint32_t> thresh(P), ones(P, 0xffffffffu);
+  std::vector<float> zeros(P, 0.0f);
+  h->dens.resize(P);
+  for (int v = 0; v < P; ++v) {
+    const double u = (double)(draw_word(cfg->seed, 0, 0, (uint32_t)v, kStreamDens, 0) >> 8) * (1.0 / 16777216.0);
+    const float rho = (float)((double)cfg->dens_lo + u * ((double)cfg->dens_hi - (double)cfg->dens_lo));
+    h->dens[v] = rho;
+    double t = floor((double)rho * 16777216.0 + 0.5);
+    t = t < 0.0 ? 0.0 : (t > 16777216.0 ? 16777216.0 : t);
+    thresh[v] = (uint32_t)t;
+  }
+  char* ws = h->ws;
+  if (hipMemcpy(ws + y.thresh, thresh.data(), (size_t)P * 4, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(ws + y.aux, zeros.data(), (size_t)P * 4, hipMemcpyHostToDevice) != hipSuccess)
+    return fail(GEVO_E_HIP);
+  // base tensors, padded and transposed to [Np][Kp], then the variants
+  size_t off = 0;
+  for (int i = 0; i < y.nt; ++i) {
+    const CnnTensor& t = y.t[i];
+    std::vector<float> bw((size_t)t.Np * t.Kp, 0.0f), bb((size_t)t.Np, 0.0f);
+    for (int k = 0; k < t.K; ++k)
+      for (int n = 0; n < t.N; ++n) bw[(size_t)n * t.Kp + k] = base_params[off + (size_t)k * t.N + n];
+    off += (size_t)t.K * t.N;
+    for (int n = 0; n < t.N; ++n) bb[n] = base_params[off + n];
+    off += (size_t)t.N;
+    if (hipMemcpy(ws + t.base_w, bw.data(), bw.size() * 4, hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemcpy(ws + t.base_b, bb.data(), bb.size() * 4, hipMemcpyHostToDevice) != hipSuccess)
+      return fail(GEVO_E_HIP);
+    InitArgs a{};
+    a.P = P; a.l_index = i; a.K = t.K; a.N = t.N; a.Kp = t.Kp; a.Np = t.Np;
+    a.seed = cfg->seed;
+    a.init_kind = 1;
+    a.xavier_a = (float)sqrt(6.0 / ((double)t.K + (double)t.N));
+    a.noise_std = cfg->noise_rel_std;
+    a.base_w = at<const float>(ws, t.base_w);
+    a.base_b = at<const float>(ws, t.base_b);
+    a.thresh = at<const uint32_t>(ws, y.thresh);
+    a.Wm = at<float>(ws, t.Wm);
+    a.bias = at<float>(ws, t.bias);
+    a.mask = at<uint32_t>(ws, t.mask);
+    if (launch_init(a, h->stream, LaunchEv{}) != hipSuccess) return fail(GEVO_E_HIP);
+  }
+  // test labels in 256-row tiles per chunk, padding rows marked -1
+  std::vector<int32_t> ylab((size_t)n_test), tiles((size_t)y.n_chunks * kCnnRows, -1);
+  if (hipMemcpy(ylab.data(), d_test_y, (size_t)n_test * 4, hipMemcpyDeviceToHost) != hipSuccess) return fail(GEVO_E_HIP);
+  for (int64_t r = 0; r < n_test; ++r) {
+    if (ylab[r] < 0 || ylab[r] >= y.classes) return fail(GEVO_E_SHAPE);
+    tiles[(size_t)(r / kCnnChunk) * kCnnRows + r % kCnnChunk] = ylab[r];
+  }
+  if (hipMemcpy(ws + y.labels, tiles.data(), tiles.size() * 4, hipMemcpyHostToDevice) != hipSuccess)
+    return fail(GEVO_E_HIP);
+  if (hipDeviceSynchronize() != hipSuccess) return fail(GEVO_E_HIP);
+  *out = h;
+  return GEVO_OK;
+}
+
+gevo_status gevo_cnn_predict(gevo_cnn* h) {
+  if (!h) return GEVO_E_ARG;
+  const CnnLayout& y = h->y;
+  char* ws = h->ws;
+  hipStream_t s = h->stream;
+  const int P = y.P;
+  CNN_HIP(hipEventRecord(h->ev0, s));
+  for (int c = 0; c < y.n_chunks; ++c) {
+    // stem: test images -> A
+    const CnnTensor& ts = y.t[0];
+    CnnStemArgs sa{};
+    sa.x = h->teX; sa.n_test = y.n_test; sa.img0 = c * kCnnChunk;
+    sa.H = y.H; sa.W = y.W; sa.C = y.C;
+    sa.K = ts.K; sa.Kp = ts.Kp; sa.Np = ts.Np;
+    sa.Wm = at<const float>(ws, ts.Wm); sa.bias = at<const float>(ws, ts.bias);
+    sa.out = at<uint16_t>(ws, y.actA); sa.out_vs = y.act_vs;
+    const int stem_px = kCnnChunk * y.H * y.W;
+    hipExtLaunchKernelGGL(k_cnn_stem, dim3((stem_px + 255) / 256, P), dim3(256), (size_t)ts.K * ts.Np * 4, s, nullptr,
+                          nullptr, 0, sa);
+    CNN_HIP(hipGetLastError());
+    int ch = y.stem;
+    for (int i = 0; i < y.nb; ++i) {
+      const CnnTensor& td = y.t[1 + 2 * i];
+      const CnnTensor& tp = y.t[2 + 2 * i];
+      CnnDwArgs da{};
+      da.in = at<const uint16_t>(ws, y.actA); da.in_vs = y.act_vs;
+      da.out = at<uint16_t>(ws, y.actB); da.out_vs = y.act_vs;
+      da.H = y.hin[i]; da.W = y.win[i]; da.C = ch; da.Ho = y.hin[i + 1]; da.Wo = y.win[i + 1]; da.stride = y.stride[i];
+      da.Wm = at<const float>(ws, td.Wm); da.bias = at<const float>(ws, td.bias);
+      const int dw_threads = kCnnChunk * da.Ho * da.Wo * (ch / 8);
+      hipExtLaunchKernelGGL(k_cnn_dw, dim3((dw_threads + 255) / 256, P), dim3(256), (size_t)10 * ch * 4, s, nullptr,
+                            nullptr, 0, da);
+      CNN_HIP(hipGetLastError());
+      FwdGemmArgs g{};
+      g.A = at<const uint16_t>(ws, y.actB); g.a_vs = y.act_vs;
+      g.Wm = at<const float>(ws, tp.Wm); g.bias = at<const float>(ws, tp.bias);
+      g.O = at<uint16_t>(ws, y.actA); g.o_vs = y.act_vs;
+      g.Kp = tp.Kp; g.Np = tp.Np; g.R = kCnnChunk * da.Ho * da.Wo; g.P = P;
+      if (!fwd_gemm_supported(g.Kp, g.Np, g.R)) return GEVO_E_SHAPE;
+      CNN_HIP(launch_fwd_gemm(g, s, LaunchEv{}));
+      ch = y.ch[i];
+    }
+    CnnPoolArgs pa{};
+    pa.in = at<const uint16_t>(ws, y.actA); pa.in_vs = y.act_vs;
+    pa.HW = y.hin[y.nb] * y.win[y.nb]; pa.C = ch;
+    pa.out = at<uint16_t>(ws, y.pooled); pa.out_vs = (size_t)kCnnRows * ch;
+    hipExtLaunchKernelGGL(k_cnn_pool, dim3((kCnnRows * (ch / 8) + 255) / 256, P), dim3(256), 0, s, nullptr, nullptr,
+                          0, pa);
+    CNN_HIP(hipGetLastError());
+    const CnnTensor& tf = y.t[y.nt - 1];
+    OutArgs<uint16_t> o{};
+    o.Kp = tf.Kp; o.C = y.classes; o.Bp = kCnnRows;
+    o.Wm = at<float>(ws, tf.Wm); o.bias = at<float>(ws, tf.bias); o.mask = at<const uint32_t>(ws, tf.mask);
+    o.bmask = at<const uint32_t>(ws, y.aux); o.lr = at<const float>(ws, y.aux);
+    o.train = 0;
+    o.Arows = at<const uint16_t>(ws, y.pooled); o.ar_vs = (size_t)kCnnRows * ch;
+    o.labels = at<const int32_t>(ws, y.labels) + (size_t)c * kCnnRows;
+    o.rows = kCnnRows;
+    o.chunk0 = c;
+    o.n_chunks_total = y.n_chunks;
+    o.part_ce = at<double>(ws, y.part_ce);
+    o.part_correct = at<unsigned int>(ws, y.part_corr);
+    CNN_HIP(launch_out<uint16_t>(o, P, s, LaunchEv{}));
+  }
+  CNN_HIP(launch_reduce_partials(at<double>(ws, y.part_ce), at<unsigned int>(ws, y.part_corr), P, y.n_chunks,
+                                 at<double>(ws, y.test_ce), at<unsigned long long>(ws, y.test_corr), s, LaunchEv{}));
+  CNN_HIP(hipEventRecord(h->ev1, s));
+  h->timing_pending = true;
+  h->predicted = true;
+  return GEVO_OK;
+}
+
+gevo_status gevo_cnn_scores(gevo_cnn* h, float* test_loss, float* test_acc, float* time_s) {
+  if (!h) return GEVO_E_ARG;
+  if (!h->predicted) return GEVO_E_ORDER;
+  CNN_HIP(hipStreamSynchronize(h->stream));
+  if (h->timing_pending) {
+    float ms = 0.0f;
+    CNN_HIP(hipEventElapsedTime(&ms, h->ev0, h->ev1));
+    h->last_s = (double)ms * 1e-3;
+    h->timing_pending = false;
+  }
+  const int P = h->y.P;
+  std::vector<double> ce(P);
+  std::vector<unsigned long long> corr(P);
+  CNN_HIP(hipMemcpy(ce.data(), h->ws + h->y.test_ce, (size_t)P * 8, hipMemcpyDeviceToHost));
+  CNN_HIP(hipMemcpy(corr.data(), h->ws + h->y.test_corr, (size_t)P * 8, hipMemcpyDeviceToHost));
+  for (int v = 0; v < P; ++v) {
+    if (test_loss) test_loss[v] = (float)(ce[v] / (double)h->y.n_test);
+    if (test_acc) test_acc[v] = (float)((double)corr[v] / (double)h->y.n_test);
+    if (time_s) time_s[v] = (float)(h->last_s / P);
+  }
+  return GEVO_OK;
+}
+
+gevo_status gevo_cnn_export(gevo_cnn* h, uint32_t v, float* params_out, uint8_t* mask_out, float* density_out) {
+  if (!h) return GEVO_E_ARG;
+  const CnnLayout& y = h->y;
+  if (v >= (uint32_t)y.P) return GEVO_E_ARG;
+  CNN_HIP(hipStreamSynchronize(h->stream));
+  size_t off = 0, moff = 0;
+  for (int i = 0; i < y.nt; ++i) {
+    const CnnTensor& t = y.t[i];
+    const size_t nw = (size_t)t.Np * t.Kp, words = (size_t)t.Np * (t.Kp / 32);
+    std::vector<float> W(nw), b((size_t)t.Np);
+    std::vector<uint32_t> M(words);
+    CNN_HIP(hipMemcpy(W.data(), h->ws + t.Wm + (size_t)v * nw * 4, nw * 4, hipMemcpyDeviceToHost));
+    CNN_HIP(hipMemcpy(b.data(), h->ws + t.bias + (size_t)v * t.Np * 4, (size_t)t.Np * 4, hipMemcpyDeviceToHost));
+    CNN_HIP(hipMemcpy(M.data(), h->ws + t.mask + (size_t)v * words * 4, words * 4, hipMemcpyDeviceToHost));
+    for (int k = 0; k < t.K; ++k)
+      for (int n = 0; n < t.N; ++n) {
+        if (params_out) params_out[off + (size_t)k * t.N + n] = W[((size_t)(k / 32) * t.Np + n) * 32 + k % 32];
+        if (mask_out) mask_out[moff + (size_t)k * t.N + n] = (uint8_t)((M[(size_t)n * (t.Kp / 32) + k / 32] >> (k % 32)) & 1u);
+      }
+    off += (size_t)t.K * t.N;
+    moff += (size_t)t.K * t.N;
+    for (int n = 0; n < t.N; ++n)
+      if (params_out) params_out[off + n] = b[n];
+    off += (size_t)t.N;
+  }
+  if (density_out) *density_out = h->dens[v];
+  return GEVO_OK;
+}
+
+}  // extern "C"

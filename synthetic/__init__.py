@@ -156,3 +156,60 @@ def dataset(cfg: dict, n_train: int | None = None, n_test: int | None = None, se
     gen = cifar_like if cfg["data"] == "cifar" else mnist_like
     xtr, ytr, xte, yte = gen(n_train, n_test, seed)
     return dict(x_train=xtr, y_train=ytr, x_test=xte, y_test=yte)
+
+
+# The convolutional prediction workload: P variants of a depthwise-separable
+# (MobileNet-like) net, each run over a CIFAR-shaped test split (section 4.3's
+# prediction fitness; Table 1's MobileNet is the paper's convolutional case).
+CNN_CONFIGS = {
+    "full": dict(name="p64-dwsep-cnn32x32x3-32-128-128-256-512-10-bf16", P=64, H=32, W=32, C=3, stem=32,
+                 blocks=[(1, 128), (2, 128), (2, 256), (2, 512)], classes=10, n_test=10000,
+                 dens=(0.5, 1.0), noise_std=0.01, seed=POP_SEED_BASE + 6),
+    "small": dict(name="p6-dwsep-cnn8x8x3-32-128-128-10-bf16", P=6, H=8, W=8, C=3, stem=32,
+                  blocks=[(1, 128), (2, 128)], classes=10, n_test=150,
+                  dens=(0.5, 1.0), noise_std=0.01, seed=POP_SEED_BASE + 7),
+}
+
+
+def cnn_config(key: str, **overrides) -> dict:
+    c = dict(CNN_CONFIGS[key])
+    c.update(overrides)
+    return c
+
+
+def cnn_tensor_shapes(cfg: dict):
+    """[(K, N)] of the net's weight tensors in canonical order: stem (9 C x
+    stem), then per block depthwise (9 x C_in) and pointwise (C_in x C_out),
+    then the head (C_last x classes)."""
+    out = [(9 * cfg["C"], cfg["stem"])]
+    c = cfg["stem"]
+    for _, co in cfg["blocks"]:
+        out += [(9, c), (c, co)]
+        c = co
+    return out + [(c, cfg["classes"])]
+
+
+def cnn_inputs(cfg: dict, n_test: int | None = None, seed: int = DATA_SEED):
+    """(base parameters float32 canonical, images float32 [n][H][W][C],
+    labels int32 [n]).
+
+    The base model stands in for a pretrained one: weights are normal with
+    variance 2 / fan_in (fan_in = 9 C for the stem, 9 for a depthwise filter,
+    C_in for a pointwise layer and the head), biases normal with s.d. 0.05.
+    Images are the CIFAR-shaped stand-in, cropped (top-left) to H x W when
+    smaller than 32 x 32, with C of its 3 channels (C <= 3) or the first
+    channel repeated (C = 4).  Labels are the stand-in's ten classes taken
+    modulo the net's class count."""
+    n = cfg["n_test"] if n_test is None else n_test
+    r = np.random.default_rng([seed + 5, cfg["seed"]])
+    parts = []
+    for K, N in cnn_tensor_shapes(cfg):
+        parts.append(r.normal(0.0, np.sqrt(2.0 / K), size=K * N))     # fan_in = K
+        parts.append(r.normal(0.0, 0.05, size=N))
+    base = np.concatenate(parts).astype(np.float32)
+    H, W, C = cfg["H"], cfg["W"], cfg["C"]
+    assert H <= 32 and W <= 32 and 1 <= C <= 4
+    _, _, x, y = cifar_like(0, n, seed)
+    img = x.reshape(n, 32, 32, 3)[:, :H, :W, :]
+    img = img[..., :C] if C <= 3 else np.concatenate([img, img[..., :1]], axis=3)
+    return base, np.ascontiguousarray(img, np.float32), (y % cfg["classes"]).astype(np.int32)
