@@ -51,6 +51,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU-oracle sample")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="time without per-kernel events")
+    ap.add_argument("--cnn", action="store_true",
+                    help="time the convolutional prediction workload (P=64 depthwise-separable nets on "
+                         "32x32x3 images) instead")
     ap.add_argument("--search", type=int, default=0, metavar="G",
                     help="time G generations of the search loop on this workload instead")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -276,6 +279,10 @@ def main():
                              f"--config {args.config} --steps 1 --warmup 0 --no-cpu --no-profile")
         return
 
+    if args.cnn:
+        cnn_bench(args)
+        return
+
     import torch
     import paper_2310_10211_amd as g
     import synthetic
@@ -375,6 +382,138 @@ def main():
                    "parallelism": "population (one GPU)"},
         "mfma_frac_of_step": round(work_flops / (ms_step / 1e3) / (peak * 1e12), 4),
         "kernel_ms_per_step": kernel_ms,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out))
+
+
+# ------------------------------------------------------- convolutional workload
+def cnn_costs(cfg, n):
+    """{kernel kind: (algorithmic HBM bytes, flops)} of one prediction pass over
+    n test images for all P variants.  Per image and variant every activation
+    map is written once by its producer and read once by its consumer (bf16);
+    the input image is read once for all variants (fp32); every launch reads
+    its variants' fp32 weights and biases once per 64-image chunk."""
+    P, H, W, C, cls = cfg["P"], cfg["H"], cfg["W"], cfg["C"], cfg["classes"]
+    chunks = (n + 63) // 64
+    stem = cfg["stem"]
+    out = {"stem": [n * H * W * C * 4 + P * n * H * W * stem * 2 + P * chunks * (9 * C * stem + stem) * 4,
+                    2.0 * P * n * H * W * 9 * C * stem]}
+    dw, pw = [0.0, 0.0], [0.0, 0.0]
+    h, w, ch = H, W, stem
+    for s_, co in cfg["blocks"]:
+        ho, wo = (h - 1) // s_ + 1, (w - 1) // s_ + 1
+        dw[0] += P * n * (h * w * ch + ho * wo * ch) * 2 + P * chunks * 10 * ch * 4
+        dw[1] += 2.0 * P * n * ho * wo * ch * 9
+        pw[0] += P * n * ho * wo * (ch + co) * 2 + P * chunks * (ch * co + co) * 4
+        pw[1] += 2.0 * P * n * ho * wo * ch * co
+        h, w, ch = ho, wo, co
+    out["depthwise"], out["pointwise"] = dw, pw
+    out["pool"] = [P * n * (h * w * ch + ch) * 2, float(P * n * h * w * ch)]
+    out["head"] = [P * n * ch * 2 + P * chunks * (ch * cls + cls) * 4, 2.0 * P * n * ch * cls]
+    return {k: tuple(v) for k, v in out.items()}
+
+
+def cnn_cpu_baseline(cfg, base, x, y, budget_s):
+    from oracle import cnn
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = 1
+    n0 = 64
+    t0 = time.perf_counter()
+    cnn.evaluate(cfg, base, x[:n0], y[:n0], [0], mode="bf16")
+    one = time.perf_counter() - t0
+    n = int(max(n0, min(len(y), n0 * budget_s / max(one, 1e-3) * 0.8)))
+    t0 = time.perf_counter()
+    cnn.evaluate(cfg, base, x[:n], y[:n], [0], mode="bf16")
+    wall = time.perf_counter() - t0
+    return dict(value=n / wall, unit="variant-images/s", cores=cores, kind="oracle",
+                sample=f"variant 0 x {n} test images, prediction, bf16-rounding fp64 oracle (numpy, {cores} BLAS "
+                       f"threads), {wall:.1f} s")
+
+
+def cnn_bench(args):
+    import numpy as np
+    import torch
+    import paper_2310_10211_amd as g
+    import synthetic
+
+    cfg = synthetic.cnn_config("full")
+    print(f"[bench] workload {cfg['name']}: generating synthetic inputs", file=sys.stderr, flush=True)
+    base, x, y = synthetic.cnn_inputs(cfg)
+    dev = torch.device("cuda:0")
+    t0 = time.perf_counter()
+    pop = g.CnnPopulation(cfg, base, x, y, device=dev)
+    torch.cuda.synchronize()
+    init_ms = (time.perf_counter() - t0) * 1e3
+
+    def step():
+        pop.predict()
+        return pop.scores()
+
+    for i in range(args.warmup):
+        step()
+        print(f"[bench] warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
+    profile = not args.no_profile
+    if profile:
+        before = pop.kernel_stats()
+        pop.set_profiling(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        s = step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    print(f"[bench] timed {args.steps} steps", file=sys.stderr, flush=True)
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    P, n = cfg["P"], len(y)
+    value = P * n / (ms_step / 1e3)
+    costs = cnn_costs(cfg, n)
+    roofline, kernel_ms = None, {}
+    if profile:
+        after = pop.kernel_stats()
+        pop.set_profiling(False)
+        kst = {k: (after[k][0] - before[k][0], after[k][1] - before[k][1]) for k in after}
+        kernel_ms = {k: round(v[0] / args.steps, 3) for k, v in kst.items() if v[1]}
+        dom = max((k for k in kst if kst[k][1] and k in costs), key=lambda k: kst[k][0])
+        byts, fl = costs[dom]
+        tot_s = kst[dom][0] / 1e3 / args.steps
+        launches = kst[dom][1] // args.steps
+        ach = byts / tot_s / 1e9
+        roofline = dict(bound="hbm", achieved=round(ach, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                        frac=round(ach / HBM_PEAK_GBS, 4), kernel=dom,
+                        avg_launch_us=round(tot_s / launches * 1e6, 2), launches=launches,
+                        algorithmic_bytes_per_launch=int(byts / launches),
+                        algorithmic_flops_per_launch=int(fl / launches),
+                        traffic=traffic_for("cnn_" + dom, cfg["name"]))
+    cpu = None
+    if not args.no_cpu:
+        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        cpu = cnn_cpu_baseline(cfg, base.astype(np.float64), x, y, args.cpu_seconds)
+    total_flops = sum(v[1] for v in costs.values())
+    out = {
+        "metric": "variant-images/sec (prediction fitness) at P variants",
+        "value": round(value, 1),
+        "unit": "variant-images/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": cfg["name"], "P": P, "image": [cfg["H"], cfg["W"], cfg["C"]], "stem": cfg["stem"],
+                   "blocks": cfg["blocks"], "classes": cfg["classes"], "n_test": n,
+                   "step": "test prediction of every variant + scores (variants built once, outside)",
+                   "init_ms": round(init_ms, 1), "parallelism": "population (one GPU)"},
+        "mfma_frac_of_step": round(total_flops / (ms_step / 1e3) / (PEAK["bf16"] * 1e12), 4),
+        "kernel_ms_per_step": kernel_ms,
+        "mean_test_loss": round(float(np.mean(s["test_loss"])), 4),
         "roofline": roofline,
         "cpu_baseline": cpu,
     }

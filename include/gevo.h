@@ -386,7 +386,7 @@ typedef struct {
   uint32_t abi_version;               /* must be GEVO_ABI_VERSION */
   uint32_t P;                         /* variants, 1..65535 */
   uint32_t height, width, channels;   /* input images; channels 1..4, sides 1..1024 */
-  uint32_t stem_channels;             /* multiple of 32, <= 512 */
+  uint32_t stem_channels;             /* multiple of 32, <= 512, 36 x channels x stem_channels <= 65536 */
   uint32_t n_blocks;                  /* 1..GEVO_CNN_MAX_BLOCKS */
   uint32_t block_stride[GEVO_CNN_MAX_BLOCKS];    /* 1 or 2 */
   uint32_t block_channels[GEVO_CNN_MAX_BLOCKS];  /* multiples of 128, <= 1024 */
@@ -425,6 +425,25 @@ gevo_status gevo_cnn_scores(gevo_cnn* h, float* test_loss, float* test_acc, floa
 /* Variant v's parameters (canonical layout), mask (uint8 0/1 over the
  * weights, same order) and density rho_v; any output may be NULL. */
 gevo_status gevo_cnn_export(gevo_cnn* h, uint32_t v, float* params_out, uint8_t* mask_out, float* density_out);
+
+/* Kernel-level timing, as for gevo_pop_set_profiling: with profiling enabled
+ * every kernel that gevo_cnn_predict enqueues carries a HIP event pair
+ * recorded by its own dispatch on the handle's stream; gevo_cnn_kernel_stats
+ * synchronises and returns, per kind, the summed kernel time in ms and the
+ * launch count since the handle was created.  GEVO_E_ARG for a null handle
+ * or a kind outside the enum. */
+typedef enum {
+  GEVO_CNN_KERNEL_STEM = 0,        /* 3x3 stem convolution */
+  GEVO_CNN_KERNEL_DEPTHWISE = 1,   /* 3x3 depthwise convolutions */
+  GEVO_CNN_KERNEL_POINTWISE = 2,   /* 1x1 pointwise convolutions (per-variant GEMMs) */
+  GEVO_CNN_KERNEL_POOL = 3,        /* global average pooling */
+  GEVO_CNN_KERNEL_HEAD = 4,        /* fully connected head, loss and argmax */
+  GEVO_CNN_KERNEL_REDUCE = 5,      /* per-variant sums of the chunks' partial scores */
+  GEVO_CNN_KERNEL_KINDS = 6
+} gevo_cnn_kernel_kind;
+
+gevo_status gevo_cnn_set_profiling(gevo_cnn* h, int enable);
+gevo_status gevo_cnn_kernel_stats(gevo_cnn* h, int kind, double* total_ms, uint64_t* launches);
 
 void gevo_cnn_destroy(gevo_cnn* h);
 

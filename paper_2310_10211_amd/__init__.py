@@ -39,9 +39,10 @@ EXPORTED = [
     "gevo_check_bf16_rounding", "gevo_nsga2_rank", "gevo_nsga2_select", "gevo_genomes_initial",
     "gevo_genomes_breed", "gevo_pop_set_genomes", "gevo_pop_set_grad_scale",
     "gevo_cnn_param_count", "gevo_cnn_workspace_bytes", "gevo_cnn_init", "gevo_cnn_predict", "gevo_cnn_scores",
-    "gevo_cnn_export", "gevo_cnn_destroy",
+    "gevo_cnn_export", "gevo_cnn_destroy", "gevo_cnn_set_profiling", "gevo_cnn_kernel_stats",
 ]
 CNN_MAX_BLOCKS = 4
+CNN_KERNEL_KINDS = ["stem", "depthwise", "pointwise", "pool", "head", "reduce"]
 KERNEL_KINDS = ["init", "gather", "layer_train", "layer_fwd", "out_train", "out_predict", "bwd", "aux",
                 "fused_train"]
 
@@ -156,6 +157,9 @@ def lib():
         L.gevo_cnn_predict.argtypes = [vp]
         L.gevo_cnn_scores.argtypes = [vp, f32p, f32p, f32p]
         L.gevo_cnn_export.argtypes = [vp, u32, f32p, ctypes.POINTER(ctypes.c_uint8), f32p]
+        L.gevo_cnn_set_profiling.argtypes = [vp, ctypes.c_int]
+        L.gevo_cnn_kernel_stats.argtypes = [vp, ctypes.c_int, ctypes.POINTER(ctypes.c_double),
+                                            ctypes.POINTER(ctypes.c_uint64)]
         L.gevo_cnn_destroy.argtypes = [vp]
         L.gevo_cnn_destroy.restype = None
         L.gevo_pop_destroy.argtypes = [vp]
@@ -504,6 +508,18 @@ class CnnPopulation:
         t = np.zeros(self.P, np.float32)
         _check(lib().gevo_cnn_scores(self._h, _fp(loss), _fp(acc), _fp(t)), "gevo_cnn_scores")
         return {"test_loss": loss, "test_acc": acc, "time_s": t}
+
+    def set_profiling(self, on: bool):
+        _check(lib().gevo_cnn_set_profiling(self._h, 1 if on else 0), "gevo_cnn_set_profiling")
+
+    def kernel_stats(self) -> dict:
+        """{kind: (total ms, launches)} of the kernels timed so far."""
+        out = {}
+        for i, k in enumerate(CNN_KERNEL_KINDS):
+            ms, n = ctypes.c_double(), ctypes.c_uint64()
+            _check(lib().gevo_cnn_kernel_stats(self._h, i, ctypes.byref(ms), ctypes.byref(n)), "gevo_cnn_kernel_stats")
+            out[k] = (ms.value, n.value)
+        return out
 
     def export(self, v: int) -> dict:
         n = cnn_param_count(self.cfg)

@@ -33,9 +33,10 @@ constexpr int kCnnRows = kOutRows;       // pooled rows per chunk handed to the 
 
 struct CnnStemArgs {
   const float* x; int64_t n_test; int img0;   // test images [n][H][W][C] fp32, first image of the chunk
-  int H, W, C;
-  int K, Kp, Np;                              // stem tensor: K = 9C inputs, Np output channels
-  const float* Wm; const float* bias;         // [P][Kp/32][Np][32], [P][Np]
+  int H, W;
+  int Np;                                     // output channels
+  const float* wp; const float* bias;         // bf16-valued taps [P][9C][Np] (fp32 storage), biases [P][Np]
+                                              // (9C x Np x 4 bytes <= 64 KiB: they are staged in LDS)
   uint16_t* out; size_t out_vs;               // [v][chunk][H][W][Np] bf16
 };
 
@@ -43,7 +44,7 @@ struct CnnDwArgs {
   const uint16_t* in; size_t in_vs;           // [v][chunk][H][W][C]
   uint16_t* out; size_t out_vs;               // [v][chunk][Ho][Wo][C]
   int H, W, C, Ho, Wo, stride;
-  const float* Wm; const float* bias;         // filter taps of channel c at [v][c][32] (first 9), [P][C]
+  const float* wp; const float* bias;         // bf16-valued taps [P][9][C] (fp32 storage), biases [P][C]
 };
 
 struct CnnPoolArgs {
@@ -56,16 +57,28 @@ __device__ __forceinline__ float bf16r(float f) { return bf16_bits_to_f32(f32_to
 
 }  // namespace
 
-// stem: one thread per output pixel of one variant, all output channels;
-// the variant's weights, rounded to bf16, sit in LDS as [k][Np]
+// Prediction copy of one weight tensor: out[v][k][n] = bf16(W_v[k][n]) held in
+// fp32, read from the k-blocked master [v][Kp/32][Np][32].  The handle never
+// changes its masters, so this runs once, at init.
+__global__ __launch_bounds__(256) void k_cnn_pack(const float* __restrict__ Wm, int Kp, int Np, int K, int N, int P,
+                                                  float* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)P * K * N) return;
+  const int n = (int)(i % N), k = (int)((i / N) % K), v = (int)(i / ((int64_t)K * N));
+  out[i] = bf16r(Wm[(size_t)v * Np * Kp + ((size_t)(k / 32) * Np + n) * 32 + k % 32]);
+}
+
+// stem: one thread per output pixel of one variant, all output channels.  The
+// 9C inputs of the pixel sit in registers (C is a template parameter, so every
+// index is static); the variant's taps sit in LDS as [k][Np], each read a
+// broadcast to the whole wave.
+template <int C>
 __global__ __launch_bounds__(256) void k_cnn_stem(CnnStemArgs a) {
+  constexpr int K = 9 * C;
   extern __shared__ float wl[];
-  const int v = blockIdx.y, Np = a.Np, K = a.K;
-  const float* Wv = a.Wm + (size_t)v * Np * a.Kp;
-  for (int i = threadIdx.x; i < K * Np; i += blockDim.x) {
-    const int k = i / Np, n = i % Np;
-    wl[i] = bf16r(Wv[((size_t)(k / 32) * Np + n) * 32 + k % 32]);
-  }
+  const int v = blockIdx.y, Np = a.Np;
+  const float* wv = a.wp + (size_t)v * K * Np;
+  for (int i = threadIdx.x; i < K * Np; i += blockDim.x) wl[i] = wv[i];
   __syncthreads();
   const int HW = a.H * a.W;
   const int p = blockIdx.x * blockDim.x + threadIdx.x;
@@ -73,15 +86,16 @@ __global__ __launch_bounds__(256) void k_cnn_stem(CnnStemArgs a) {
   const int img = p / HW, y = (p % HW) / a.W, x = p % a.W;
   const int64_t g = (int64_t)a.img0 + img;
   const bool valid = g < a.n_test;
-  float patch[36];                                     // 9 C <= 36 inputs, k = (3 dy + dx) C + c
+  float patch[K];                                      // k = (3 dy + dx) C + c
 #pragma unroll
-  for (int k = 0; k < 36; ++k) patch[k] = 0.0f;
   for (int dy = 0; dy < 3; ++dy)
+#pragma unroll
     for (int dx = 0; dx < 3; ++dx) {
       const int yy = y + dy - 1, xx = x + dx - 1;
-      if (valid && yy >= 0 && yy < a.H && xx >= 0 && xx < a.W)
-        for (int c = 0; c < a.C; ++c)
-          patch[(3 * dy + dx) * a.C + c] = bf16r(a.x[((g * a.H + yy) * a.W + xx) * a.C + c]);
+      const bool in = valid && yy >= 0 && yy < a.H && xx >= 0 && xx < a.W;
+      const float* src = a.x + (in ? ((g * a.H + yy) * a.W + xx) * C : 0);
+#pragma unroll
+      for (int c = 0; c < C; ++c) patch[(3 * dy + dx) * C + c] = in ? bf16r(src[c]) : 0.0f;
     }
   const float* bv = a.bias + (size_t)v * Np;
   uint16_t* o = a.out + a.out_vs * v + (size_t)p * Np;
@@ -89,10 +103,13 @@ __global__ __launch_bounds__(256) void k_cnn_stem(CnnStemArgs a) {
     float acc[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[j] = 0.0f;
-    for (int k = 0; k < K; ++k) {
-      const float pk = patch[k];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) acc[j] = __fmaf_rn(pk, wl[k * Np + n0 + j], acc[j]);
+    for (int k = 0; k < K; ++k) {
+      const float4 w0 = *reinterpret_cast<const float4*>(wl + k * Np + n0);
+      const float4 w1 = *reinterpret_cast<const float4*>(wl + k * Np + n0 + 4);
+      const float w[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[j] = __fmaf_rn(patch[k], w[j], acc[j]);
     }
     float f[8];
 #pragma unroll
@@ -110,10 +127,8 @@ __global__ __launch_bounds__(256) void k_cnn_stem(CnnStemArgs a) {
 __global__ __launch_bounds__(256) void k_cnn_dw(CnnDwArgs a) {
   extern __shared__ float dl[];                        // taps [9][C], then bias [C]
   const int v = blockIdx.y, C = a.C;
-  for (int i = threadIdx.x; i < 9 * C; i += blockDim.x) {
-    const int t = i / C, c = i % C;
-    dl[i] = bf16r(a.Wm[((size_t)v * C + c) * 32 + t]);
-  }
+  const float* wv = a.wp + (size_t)v * 9 * C;
+  for (int i = threadIdx.x; i < 9 * C; i += blockDim.x) dl[i] = wv[i];
   for (int c = threadIdx.x; c < C; c += blockDim.x) dl[9 * C + c] = a.bias[(size_t)v * C + c];
   __syncthreads();
   const int C8 = C / 8, HWo = a.Ho * a.Wo;
@@ -125,7 +140,9 @@ __global__ __launch_bounds__(256) void k_cnn_dw(CnnDwArgs a) {
   float acc[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) acc[j] = 0.0f;
+#pragma unroll
   for (int dy = 0; dy < 3; ++dy)
+#pragma unroll
     for (int dx = 0; dx < 3; ++dx) {
       const int yy = a.stride * yo + dy - 1, xx = a.stride * xo + dx - 1;
       if (yy < 0 || yy >= a.H || xx < 0 || xx >= a.W) continue;
@@ -190,6 +207,8 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 struct CnnTensor {
   int K = 0, N = 0, Kp = 0, Np = 0;
   size_t Wm = 0, bias = 0, mask = 0, base_w = 0, base_b = 0;
+  size_t pack = 0;                            // prediction copy [P][K][N] (stem and depthwise tensors)
+  bool packed = false;
 };
 
 struct CnnLayout {
@@ -225,6 +244,7 @@ gevo_status cnn_layout(const gevo_cnn_config* c, int64_t n_test, CnnLayout& y) {
     t.K = K; t.N = N; t.Kp = round_up32(K); t.Np = Np;
   };
   add(9 * y.C, y.stem, y.stem);
+  y.t[0].packed = true;
   for (int i = 0; i < y.nb; ++i) {
     const int s = (int)c->block_stride[i], co = (int)c->block_channels[i];
     if ((s != 1 && s != 2) || co % 128 || co == 0 || co > 1024) return GEVO_E_UNSUPPORTED;
@@ -233,13 +253,14 @@ gevo_status cnn_layout(const gevo_cnn_config* c, int64_t n_test, CnnLayout& y) {
     w = (w - 1) / s + 1;
     if (((size_t)kCnnChunk * h * w) % 256) return GEVO_E_UNSUPPORTED;   // pointwise GEMM rows
     add(9, ch, ch);                                   // depthwise taps of each channel
+    y.t[y.nt - 1].packed = true;
     add(ch, co, co);                                  // pointwise
     act = std::max(act, (size_t)kCnnChunk * h * w * std::max(ch, co));
     ch = co;
   }
   y.hin[y.nb] = h; y.win[y.nb] = w;
+  if ((size_t)9 * y.C * y.stem * 4 > 65536) return GEVO_E_UNSUPPORTED;   // stem taps staged in LDS
   add(ch, y.classes, 32);                             // head, in the output kernel's 32-class layout
-  if ((size_t)9 * y.C * y.stem * 4 > 65536) return GEVO_E_UNSUPPORTED;
   y.act_vs = act;
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t at = off; off = align256(off + bytes); return at; };
@@ -251,6 +272,7 @@ gevo_status cnn_layout(const gevo_cnn_config* c, int64_t n_test, CnnLayout& y) {
     t.mask = take(P * t.Np * (t.Kp / 32) * 4);
     t.base_w = take((size_t)t.Np * t.Kp * 4);
     t.base_b = take((size_t)t.Np * 4);
+    if (t.packed) t.pack = take(P * t.K * t.N * 4);
   }
   y.thresh = take(P * 4);
   y.aux = take(P * 4);                                // learning rates and bias bits the output kernel reads
@@ -285,7 +307,65 @@ struct gevo_cnn {
   bool predicted = false, timing_pending = false;
   double last_s = 0.0;
   std::vector<float> dens;
+  // kernel-level timing (gevo_cnn_set_profiling)
+  bool prof_on = false;
+  struct ProfRec { int kind; hipEvent_t a, b; };
+  std::vector<ProfRec> prof_pending;
+  std::vector<hipEvent_t> ev_free, ev_all;
+  double prof_ms[GEVO_CNN_KERNEL_KINDS] = {0};
+  uint64_t prof_n[GEVO_CNN_KERNEL_KINDS] = {0};
 };
+
+namespace {
+
+constexpr size_t kCnnProfBatch = 8192;   // launches between resolutions of pending timings
+
+hipError_t cnn_prof_resolve(gevo_cnn* h) {
+  if (h->prof_pending.empty()) return hipSuccess;
+  const hipError_t err = hipStreamSynchronize(h->stream);
+  if (err != hipSuccess) return err;
+  for (const auto& r : h->prof_pending) {
+    float ms = 0.0f;
+    if (hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
+      h->prof_ms[r.kind] += (double)ms;
+      h->prof_n[r.kind] += 1;
+    }
+    h->ev_free.push_back(r.a);
+    h->ev_free.push_back(r.b);
+  }
+  h->prof_pending.clear();
+  return hipSuccess;
+}
+
+hipEvent_t cnn_take_event(gevo_cnn* h) {
+  if (!h->ev_free.empty()) {
+    hipEvent_t e = h->ev_free.back();
+    h->ev_free.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  h->ev_all.push_back(e);
+  return e;
+}
+
+// events recorded by the dispatch of the next launch of this kind (none when profiling is off)
+LaunchEv cnn_prof(gevo_cnn* h, int kind) {
+  LaunchEv ev;
+  if (!h->prof_on) return ev;
+  if (h->prof_pending.size() >= kCnnProfBatch && cnn_prof_resolve(h) != hipSuccess) return ev;
+  ev.start = cnn_take_event(h);
+  ev.stop = cnn_take_event(h);
+  if (!ev.start || !ev.stop) {
+    if (ev.start) h->ev_free.push_back(ev.start);
+    if (ev.stop) h->ev_free.push_back(ev.stop);
+    return LaunchEv{};
+  }
+  h->prof_pending.push_back({kind, ev.start, ev.stop});
+  return ev;
+}
+
+}  // namespace
 
 #define CNN_HIP(x)                              \
   do {                                          \
@@ -314,10 +394,27 @@ gevo_status gevo_cnn_workspace_bytes(const gevo_cnn_config* cfg, int64_t n_test,
   return GEVO_OK;
 }
 
+gevo_status gevo_cnn_set_profiling(gevo_cnn* h, int enable) {
+  if (!h) return GEVO_E_ARG;
+  if (!enable && cnn_prof_resolve(h) != hipSuccess) return GEVO_E_HIP;
+  h->prof_on = enable != 0;
+  return GEVO_OK;
+}
+
+gevo_status gevo_cnn_kernel_stats(gevo_cnn* h, int kind, double* total_ms, uint64_t* launches) {
+  if (!h || kind < 0 || kind >= GEVO_CNN_KERNEL_KINDS) return GEVO_E_ARG;
+  if (cnn_prof_resolve(h) != hipSuccess) return GEVO_E_HIP;
+  if (total_ms) *total_ms = h->prof_ms[kind];
+  if (launches) *launches = h->prof_n[kind];
+  return GEVO_OK;
+}
+
 void gevo_cnn_destroy(gevo_cnn* h) {
   if (!h) return;
   if (h->ev0) (void)hipEventDestroy(h->ev0);
   if (h->ev1) (void)hipEventDestroy(h->ev1);
+  if (!h->ev_all.empty()) (void)hipStreamSynchronize(h->stream);
+  for (hipEvent_t e : h->ev_all) (void)hipEventDestroy(e);
   delete h;
 }
 
@@ -384,6 +481,12 @@ gevo_status gevo_cnn_init(const gevo_cnn_config* cfg, void* d_ws, size_t ws_byte
     a.bias = at<float>(ws, t.bias);
     a.mask = at<uint32_t>(ws, t.mask);
     if (launch_init(a, h->stream, LaunchEv{}) != hipSuccess) return fail(GEVO_E_HIP);
+    if (t.packed) {
+      const int64_t n = (int64_t)P * t.K * t.N;
+      hipLaunchKernelGGL(k_cnn_pack, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, h->stream,
+                         at<const float>(ws, t.Wm), t.Kp, t.Np, t.K, t.N, P, at<float>(ws, t.pack));
+      if (hipGetLastError() != hipSuccess) return fail(GEVO_E_HIP);
+    }
   }
   // test labels in 256-row tiles per chunk, padding rows marked -1
   std::vector<int32_t> ylab((size_t)n_test), tiles((size_t)y.n_chunks * kCnnRows, -1);
@@ -411,13 +514,19 @@ gevo_status gevo_cnn_predict(gevo_cnn* h) {
     const CnnTensor& ts = y.t[0];
     CnnStemArgs sa{};
     sa.x = h->teX; sa.n_test = y.n_test; sa.img0 = c * kCnnChunk;
-    sa.H = y.H; sa.W = y.W; sa.C = y.C;
-    sa.K = ts.K; sa.Kp = ts.Kp; sa.Np = ts.Np;
-    sa.Wm = at<const float>(ws, ts.Wm); sa.bias = at<const float>(ws, ts.bias);
+    sa.H = y.H; sa.W = y.W; sa.Np = ts.Np;
+    sa.wp = at<const float>(ws, ts.pack); sa.bias = at<const float>(ws, ts.bias);
     sa.out = at<uint16_t>(ws, y.actA); sa.out_vs = y.act_vs;
     const int stem_px = kCnnChunk * y.H * y.W;
-    hipExtLaunchKernelGGL(k_cnn_stem, dim3((stem_px + 255) / 256, P), dim3(256), (size_t)ts.K * ts.Np * 4, s, nullptr,
-                          nullptr, 0, sa);
+    LaunchEv ev = cnn_prof(h, GEVO_CNN_KERNEL_STEM);
+    const dim3 sg((stem_px + 255) / 256, P);
+    const size_t lds = (size_t)ts.K * ts.Np * 4;
+    switch (y.C) {
+      case 1: hipExtLaunchKernelGGL(k_cnn_stem<1>, sg, dim3(256), lds, s, ev.start, ev.stop, 0, sa); break;
+      case 2: hipExtLaunchKernelGGL(k_cnn_stem<2>, sg, dim3(256), lds, s, ev.start, ev.stop, 0, sa); break;
+      case 3: hipExtLaunchKernelGGL(k_cnn_stem<3>, sg, dim3(256), lds, s, ev.start, ev.stop, 0, sa); break;
+      default: hipExtLaunchKernelGGL(k_cnn_stem<4>, sg, dim3(256), lds, s, ev.start, ev.stop, 0, sa); break;
+    }
     CNN_HIP(hipGetLastError());
     int ch = y.stem;
     for (int i = 0; i < y.nb; ++i) {
@@ -427,10 +536,11 @@ gevo_status gevo_cnn_predict(gevo_cnn* h) {
       da.in = at<const uint16_t>(ws, y.actA); da.in_vs = y.act_vs;
       da.out = at<uint16_t>(ws, y.actB); da.out_vs = y.act_vs;
       da.H = y.hin[i]; da.W = y.win[i]; da.C = ch; da.Ho = y.hin[i + 1]; da.Wo = y.win[i + 1]; da.stride = y.stride[i];
-      da.Wm = at<const float>(ws, td.Wm); da.bias = at<const float>(ws, td.bias);
+      da.wp = at<const float>(ws, td.pack); da.bias = at<const float>(ws, td.bias);
       const int dw_threads = kCnnChunk * da.Ho * da.Wo * (ch / 8);
-      hipExtLaunchKernelGGL(k_cnn_dw, dim3((dw_threads + 255) / 256, P), dim3(256), (size_t)10 * ch * 4, s, nullptr,
-                            nullptr, 0, da);
+      ev = cnn_prof(h, GEVO_CNN_KERNEL_DEPTHWISE);
+      hipExtLaunchKernelGGL(k_cnn_dw, dim3((dw_threads + 255) / 256, P), dim3(256), (size_t)10 * ch * 4, s, ev.start,
+                            ev.stop, 0, da);
       CNN_HIP(hipGetLastError());
       FwdGemmArgs g{};
       g.A = at<const uint16_t>(ws, y.actB); g.a_vs = y.act_vs;
@@ -438,14 +548,15 @@ gevo_status gevo_cnn_predict(gevo_cnn* h) {
       g.O = at<uint16_t>(ws, y.actA); g.o_vs = y.act_vs;
       g.Kp = tp.Kp; g.Np = tp.Np; g.R = kCnnChunk * da.Ho * da.Wo; g.P = P;
       if (!fwd_gemm_supported(g.Kp, g.Np, g.R)) return GEVO_E_SHAPE;
-      CNN_HIP(launch_fwd_gemm(g, s, LaunchEv{}));
+      CNN_HIP(launch_fwd_gemm(g, s, cnn_prof(h, GEVO_CNN_KERNEL_POINTWISE)));
       ch = y.ch[i];
     }
     CnnPoolArgs pa{};
     pa.in = at<const uint16_t>(ws, y.actA); pa.in_vs = y.act_vs;
     pa.HW = y.hin[y.nb] * y.win[y.nb]; pa.C = ch;
     pa.out = at<uint16_t>(ws, y.pooled); pa.out_vs = (size_t)kCnnRows * ch;
-    hipExtLaunchKernelGGL(k_cnn_pool, dim3((kCnnRows * (ch / 8) + 255) / 256, P), dim3(256), 0, s, nullptr, nullptr,
+    ev = cnn_prof(h, GEVO_CNN_KERNEL_POOL);
+    hipExtLaunchKernelGGL(k_cnn_pool, dim3((kCnnRows * (ch / 8) + 255) / 256, P), dim3(256), 0, s, ev.start, ev.stop,
                           0, pa);
     CNN_HIP(hipGetLastError());
     const CnnTensor& tf = y.t[y.nt - 1];
@@ -461,10 +572,11 @@ gevo_status gevo_cnn_predict(gevo_cnn* h) {
     o.n_chunks_total = y.n_chunks;
     o.part_ce = at<double>(ws, y.part_ce);
     o.part_correct = at<unsigned int>(ws, y.part_corr);
-    CNN_HIP(launch_out<uint16_t>(o, P, s, LaunchEv{}));
+    CNN_HIP(launch_out<uint16_t>(o, P, s, cnn_prof(h, GEVO_CNN_KERNEL_HEAD)));
   }
   CNN_HIP(launch_reduce_partials(at<double>(ws, y.part_ce), at<unsigned int>(ws, y.part_corr), P, y.n_chunks,
-                                 at<double>(ws, y.test_ce), at<unsigned long long>(ws, y.test_corr), s, LaunchEv{}));
+                                 at<double>(ws, y.test_ce), at<unsigned long long>(ws, y.test_corr), s,
+                                 cnn_prof(h, GEVO_CNN_KERNEL_REDUCE)));
   CNN_HIP(hipEventRecord(h->ev1, s));
   h->timing_pending = true;
   h->predicted = true;
