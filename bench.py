@@ -132,9 +132,15 @@ def predict_flops_per_sample(dims):
     return sum(2 * dims[l - 1] * dims[l] for l in range(1, len(dims)))
 
 
-def source_sha():
+CNN_KERNEL_SOURCES = ["gevo_device.h", "gevo_internal.h", "gevo_kernels.hip", "gevo_gemm.hip", "gevo_cnn.hip"]
+# rocprofv3 kernel-name stem -> kernel kind of the convolutional workload
+CNN_KIND_OF = {"k_cnn_stem": "stem", "k_cnn_dw": "depthwise", "k_fwd_gemm": "pointwise", "k_cnn_pool": "pool",
+               "k_out": "head"}
+
+
+def source_sha(sources=None):
     h = hashlib.sha256()
-    for name in KERNEL_SOURCES:
+    for name in sources or KERNEL_SOURCES:
         with open(os.path.join(CSRC, name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -158,13 +164,7 @@ def _counter_rows(d, counter):
 def fold_traffic(cfg, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, command):
     """HBM bytes per launch of each kernel kind: FETCH_SIZE and WRITE_SIZE (KiB per
     dispatch) scaled by what the same counters read for a plain 1 GiB copy."""
-    n_copy = 4 << 28
-    scale = {}
-    for counter, d in (("FETCH_SIZE", copy_fetch_dir), ("WRITE_SIZE", copy_write_dir)):
-        big = [v for name, _, v in _counter_rows(d, counter) if "copyBuffer" in name and v > 2 ** 19]
-        if not big:
-            raise SystemExit(f"bench.py: no 1 GiB copy dispatch in {d}")
-        scale[counter] = n_copy / (1024.0 * sum(big) / len(big))
+    scale = copy_scales(copy_fetch_dir, copy_write_dir)
     per = {}
     for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         groups = {}
@@ -214,7 +214,56 @@ def fold_traffic(cfg, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, comm
     print(json.dumps(rec))
 
 
-def traffic_for(kernel, workload):
+def copy_scales(copy_fetch_dir, copy_write_dir):
+    """Bytes per counter unit: a plain 1 GiB copy's known bytes over its FETCH_SIZE
+    and WRITE_SIZE readings."""
+    n_copy = 4 << 28
+    scale = {}
+    for counter, d in (("FETCH_SIZE", copy_fetch_dir), ("WRITE_SIZE", copy_write_dir)):
+        big = [v for name, _, v in _counter_rows(d, counter) if "copyBuffer" in name and v > 2 ** 19]
+        if not big:
+            raise SystemExit(f"bench.py: no 1 GiB copy dispatch in {d}")
+        scale[counter] = n_copy / (1024.0 * sum(big) / len(big))
+    return scale
+
+
+def fold_traffic_cnn(cfg, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, command):
+    """Convolutional workload: mean HBM bytes per launch of each kernel kind over
+    all its launches (the kinds launch with several shapes, one per layer)."""
+    scale = copy_scales(copy_fetch_dir, copy_write_dir)
+    per = {}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        for name, _, v in _counter_rows(d, counter):
+            stem = next((k for k in CNN_KIND_OF if k in name), None)
+            if stem:
+                r = per.setdefault(CNN_KIND_OF[stem], {}).setdefault(counter, [0.0, 0])
+                r[0] += v
+                r[1] += 1
+    try:
+        with open(TRAFFIC_FILE) as f:
+            table = json.load(f)
+    except (OSError, ValueError):
+        table = {}
+    rec = table.setdefault(cfg["name"], {})
+    sha = source_sha(CNN_KERNEL_SOURCES)
+    for kind, r in per.items():
+        if len(r) != 2:
+            continue
+        kib = {c: r[c][0] / r[c][1] for c in r}
+        rec["cnn_" + kind] = dict(kernel_source_sha=sha, dispatches={c: r[c][1] for c in r},
+                                  fetch_kib_per_dispatch=round(kib["FETCH_SIZE"], 3),
+                                  write_kib_per_dispatch=round(kib["WRITE_SIZE"], 3),
+                                  fetch_scale=round(scale["FETCH_SIZE"], 4), write_scale=round(scale["WRITE_SIZE"], 4),
+                                  hbm_bytes_per_launch=int(1024 * (kib["FETCH_SIZE"] * scale["FETCH_SIZE"]
+                                                                   + kib["WRITE_SIZE"] * scale["WRITE_SIZE"])),
+                                  command=command)
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(table, f, indent=1, sort_keys=True)
+        f.write("\n")
+    print(json.dumps(rec))
+
+
+def traffic_for(kernel, workload, sources=None):
     """HBM bytes per launch from the committed rocprofv3 counter summary, or None
     if absent or taken on a different kernel source."""
     try:
@@ -223,7 +272,7 @@ def traffic_for(kernel, workload):
     except (OSError, ValueError):
         return None
     rec = t.get(workload, {}).get(kernel)
-    if not rec or rec.get("kernel_source_sha") != source_sha():
+    if not rec or rec.get("kernel_source_sha") != source_sha(sources):
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -271,6 +320,12 @@ def main():
 
     if args.calibrate_copy:
         calibrate_copy()
+        return
+    if args.traffic_from and args.cnn:
+        import synthetic
+        fold_traffic_cnn(synthetic.cnn_config("full"), *args.traffic_from,
+                         command="rocprofv3 --pmc FETCH_SIZE|WRITE_SIZE --output-format csv -- python3 bench.py "
+                                 "--cnn --steps 1 --warmup 0 --no-cpu --no-profile")
         return
     if args.traffic_from:
         import synthetic
@@ -488,7 +543,7 @@ def cnn_bench(args):
                         avg_launch_us=round(tot_s / launches * 1e6, 2), launches=launches,
                         algorithmic_bytes_per_launch=int(byts / launches),
                         algorithmic_flops_per_launch=int(fl / launches),
-                        traffic=traffic_for("cnn_" + dom, cfg["name"]))
+                        traffic=traffic_for("cnn_" + dom, cfg["name"], CNN_KERNEL_SOURCES))
     cpu = None
     if not args.no_cpu:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)

@@ -385,8 +385,9 @@ const char* gevo_status_str(gevo_status s);
 typedef struct {
   uint32_t abi_version;               /* must be GEVO_ABI_VERSION */
   uint32_t P;                         /* variants, 1..65535 */
-  uint32_t height, width, channels;   /* input images; channels 1..4, sides 1..1024 */
-  uint32_t stem_channels;             /* multiple of 32, <= 512, 36 x channels x stem_channels <= 65536 */
+  uint32_t height, width, channels;   /* input images; channels 1..4, (height + 2) (width + 2) channels
+                                         <= 28672 */
+  uint32_t stem_channels;             /* multiple of 32, <= 512 */
   uint32_t n_blocks;                  /* 1..GEVO_CNN_MAX_BLOCKS */
   uint32_t block_stride[GEVO_CNN_MAX_BLOCKS];    /* 1 or 2 */
   uint32_t block_channels[GEVO_CNN_MAX_BLOCKS];  /* multiples of 128, <= 1024 */

@@ -36,7 +36,6 @@ struct CnnStemArgs {
   int H, W;
   int Np;                                     // output channels
   const float* wp; const float* bias;         // bf16-valued taps [P][9C][Np] (fp32 storage), biases [P][Np]
-                                              // (9C x Np x 4 bytes <= 64 KiB: they are staged in LDS)
   uint16_t* out; size_t out_vs;               // [v][chunk][H][W][Np] bf16
 };
 
@@ -68,100 +67,190 @@ __global__ __launch_bounds__(256) void k_cnn_pack(const float* __restrict__ Wm, 
   out[i] = bf16r(Wm[(size_t)v * Np * Kp + ((size_t)(k / 32) * Np + n) * 32 + k % 32]);
 }
 
-// stem: one thread per output pixel of one variant, all output channels.  The
-// 9C inputs of the pixel sit in registers (C is a template parameter, so every
-// index is static); the variant's taps sit in LDS as [k][Np], each read a
-// broadcast to the whole wave.
+// Workgroup slot -> (variant, tile): slot i runs on XCD i % 8, and each XCD
+// takes a contiguous range of the variants' tiles in order, so neighbouring
+// tiles (which share input rows) meet in the same L2.
+__device__ __forceinline__ void cnn_slot(int& v, int& tile) {
+  const int gx = gridDim.x, total = gx * gridDim.y, i = blockIdx.y * gx + blockIdx.x;
+  const int j = total % 8 == 0 ? (i % 8) * (total / 8) + i / 8 : i;
+  v = j / gx;
+  tile = j % gx;
+}
+
+typedef uint32_t cnn_u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x16_t cnn_mma(cnn_u32x4 a, cnn_u32x4 b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c,
+                                                 0, 0, 0);
+}
+
+// stem as a GEMM on the matrix cores: per 32-pixel tile and 32 output
+// channels, out^T[n][p] = sum_k W[k][n] patch_p[k] with the taps k = (3 dy + dx)
+// C + c padded with zeros to a multiple of 16 (32x32x16 bf16 MFMAs, fp32
+// accumulation).  Lane l gives column (pixel) l % 32 and k slots 8 (l / 32)
+// + 0..7 of each 16-k step in both operands; the accumulator holds channels
+// crow(r, l) of pixel l % 32.  One workgroup per (variant, image): the image,
+// rounded to bf16 and zero-padded by one pixel, sits in LDS; each wave stages
+// its 32 x 32 results in LDS and stores them as whole 64-byte pixel rows.
 template <int C>
 __global__ __launch_bounds__(256) void k_cnn_stem(CnnStemArgs a) {
-  constexpr int K = 9 * C;
-  extern __shared__ float wl[];
-  const int v = blockIdx.y, Np = a.Np;
-  const float* wv = a.wp + (size_t)v * K * Np;
-  for (int i = threadIdx.x; i < K * Np; i += blockDim.x) wl[i] = wv[i];
-  __syncthreads();
-  const int HW = a.H * a.W;
-  const int p = blockIdx.x * blockDim.x + threadIdx.x;
-  if (p >= kCnnChunk * HW) return;
-  const int img = p / HW, y = (p % HW) / a.W, x = p % a.W;
+  constexpr int K = 9 * C, KS = (K + 15) / 16;
+  __shared__ __align__(16) uint32_t stage[4][32 * 16];         // per wave: 32 pixels x 32 channels bf16
+  extern __shared__ __align__(16) uint16_t im[];                // [H + 2][W + 2][C]
+  int v, img;
+  cnn_slot(v, img);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l32 = lane & 31, lh = lane >> 5;
+  const int H = a.H, W = a.W, W2 = W + 2, HW = H * W, Np = a.Np;
   const int64_t g = (int64_t)a.img0 + img;
   const bool valid = g < a.n_test;
-  float patch[K];                                      // k = (3 dy + dx) C + c
-#pragma unroll
-  for (int dy = 0; dy < 3; ++dy)
-#pragma unroll
-    for (int dx = 0; dx < 3; ++dx) {
-      const int yy = y + dy - 1, xx = x + dx - 1;
-      const bool in = valid && yy >= 0 && yy < a.H && xx >= 0 && xx < a.W;
-      const float* src = a.x + (in ? ((g * a.H + yy) * a.W + xx) * C : 0);
-#pragma unroll
-      for (int c = 0; c < C; ++c) patch[(3 * dy + dx) * C + c] = in ? bf16r(src[c]) : 0.0f;
-    }
+  for (int i = threadIdx.x; i < (H + 2) * W2 * C; i += blockDim.x) {
+    const int c = i % C, pix = i / C, yy = pix / W2 - 1, xx = pix % W2 - 1;
+    const bool in = valid && yy >= 0 && yy < H && xx >= 0 && xx < W;
+    const int64_t at = in ? ((g * H + yy) * W + xx) * C + c : 0;   // in-bounds even when unused
+    im[i] = in ? f32_to_bf16_bits(a.x[at]) : (uint16_t)0;
+  }
+  const float* wv = a.wp + (size_t)v * K * Np;
   const float* bv = a.bias + (size_t)v * Np;
-  uint16_t* o = a.out + a.out_vs * v + (size_t)p * Np;
-  for (int n0 = 0; n0 < Np; n0 += 8) {
-    float acc[8];
+  uint16_t* ov = a.out + a.out_vs * v + (size_t)img * HW * Np;
+  uint32_t* st = stage[wave];
+  __syncthreads();
+  // tap k of this lane half: LDS offset relative to the pixel's top-left neighbour
+  int toff[KS][8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[j] = 0.0f;
-#pragma unroll
-    for (int k = 0; k < K; ++k) {
-      const float4 w0 = *reinterpret_cast<const float4*>(wl + k * Np + n0);
-      const float4 w1 = *reinterpret_cast<const float4*>(wl + k * Np + n0 + 4);
-      const float w[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-#pragma unroll
-      for (int j = 0; j < 8; ++j) acc[j] = __fmaf_rn(patch[k], w[j], acc[j]);
-    }
-    float f[8];
+  for (int s = 0; s < KS; ++s)
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const float z = acc[j] + bv[n0 + j];
-      f[j] = z > 0.0f ? z : 0.0f;
+      const int k0 = 16 * s + j, k1 = k0 + 8;
+      const int t0 = k0 < K ? ((k0 / C) / 3 * W2 + (k0 / C) % 3) * C + k0 % C : -1;
+      const int t1 = k1 < K ? ((k1 / C) / 3 * W2 + (k1 / C) % 3) * C + k1 % C : -1;
+      toff[s][j] = lh ? t1 : t0;
     }
-    uint32_t pk[4];
-    to_bf16x2(f, pk);
-    *reinterpret_cast<uint4*>(o + n0) = make_uint4(pk[0], pk[1], pk[2], pk[3]);
+  const int ntiles = (HW + 31) / 32;
+  for (int n0 = 0; n0 < Np; n0 += 32) {
+    // A operand (taps of channels n0 + l32) and the biases of this lane's accumulator rows
+    cnn_u32x4 aq[KS];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      uint32_t hw[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int k = 16 * s + 8 * lh + j;
+        hw[j] = k < K ? f32_to_bf16_bits(wv[(size_t)k * Np + n0 + l32]) : 0u;
+      }
+      aq[s] = cnn_u32x4{hw[0] | hw[1] << 16, hw[2] | hw[3] << 16, hw[4] | hw[5] << 16, hw[6] | hw[7] << 16};
+    }
+    float bias[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) bias[r] = bv[n0 + crow(r, lane)];
+    for (int t = wave; t < ntiles; t += 4) {
+      const int p = min(t * 32 + l32, HW - 1);           // pixels past the image: computed, never stored
+      const int base = ((p / W) * W2 + p % W) * C;
+      f32x16_t acc = zero16();
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        uint32_t hv[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) hv[j] = toff[s][j] >= 0 ? (uint32_t)im[base + toff[s][j]] : 0u;
+        const cnn_u32x4 bq{hv[0] | hv[1] << 16, hv[2] | hv[3] << 16, hv[4] | hv[5] << 16, hv[6] | hv[7] << 16};
+        acc = cnn_mma(aq[s], bq, acc);
+      }
+      float f[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float z = acc[r] + bias[r];
+        f[r] = z > 0.0f ? z : 0.0f;
+      }
+      uint32_t pk[8];
+      to_bf16x2(f, pk);                                  // pk[i]: channels crow(2i), crow(2i) + 1
+#pragma unroll
+      for (int i = 0; i < 8; ++i) st[(l32 * 32 + crow(2 * i, lane)) / 2] = pk[i];
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {                      // 16 pixels x 64 bytes per pass
+        const int px = 16 * h + (lane >> 2), q = lane & 3;
+        const cnn_u32x4 val = *reinterpret_cast<const cnn_u32x4*>(st + px * 16 + q * 4);
+        if (t * 32 + px < HW) *reinterpret_cast<cnn_u32x4*>(ov + (size_t)(t * 32 + px) * Np + n0 + q * 8) = val;
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
   }
 }
 
-// depthwise 3x3: one thread per output pixel and 8 channels of one variant
+// depthwise 3x3 with stride S: one thread per (image, output column, 8
+// channels) of one variant, walking down the output rows with the 3 x 3 input
+// window in registers (a new output row loads S new input rows of three
+// pixels).  A wave's loads and stores cover 8 whole 16-byte channel groups of
+// consecutive pixels.
+template <int S>
 __global__ __launch_bounds__(256) void k_cnn_dw(CnnDwArgs a) {
   extern __shared__ float dl[];                        // taps [9][C], then bias [C]
-  const int v = blockIdx.y, C = a.C;
+  int v, w;
+  cnn_slot(v, w);
+  const int C = a.C, H = a.H, W = a.W;
   const float* wv = a.wp + (size_t)v * 9 * C;
   for (int i = threadIdx.x; i < 9 * C; i += blockDim.x) dl[i] = wv[i];
   for (int c = threadIdx.x; c < C; c += blockDim.x) dl[9 * C + c] = a.bias[(size_t)v * C + c];
   __syncthreads();
-  const int C8 = C / 8, HWo = a.Ho * a.Wo;
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= kCnnChunk * HWo * C8) return;
-  const int c0 = (i % C8) * 8, pix = i / C8;
-  const int img = pix / HWo, yo = (pix % HWo) / a.Wo, xo = pix % a.Wo;
-  const uint16_t* src = a.in + a.in_vs * v + (size_t)img * a.H * a.W * C;
-  float acc[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) acc[j] = 0.0f;
-#pragma unroll
-  for (int dy = 0; dy < 3; ++dy)
+  const int C8 = C / 8;
+  const int i = w * 256 + threadIdx.x;
+  if (i >= kCnnChunk * a.Wo * C8) return;
+  const int c0 = (i % C8) * 8, xo = (i / C8) % a.Wo, img = i / (C8 * a.Wo);
+  const uint16_t* src = a.in + a.in_vs * v + (size_t)img * H * W * C + c0;
+  uint16_t* dst = a.out + a.out_vs * v + (size_t)img * a.Ho * a.Wo * C + (size_t)xo * C + c0;
+  const int x0 = S * xo - 1;
+  uint4 win[3][3];                                     // [input row of the window][column]
+  auto load_row = [&](int r, uint4 (&row)[3]) {
 #pragma unroll
     for (int dx = 0; dx < 3; ++dx) {
-      const int yy = a.stride * yo + dy - 1, xx = a.stride * xo + dx - 1;
-      if (yy < 0 || yy >= a.H || xx < 0 || xx >= a.W) continue;
-      const uint4 q = *reinterpret_cast<const uint4*>(src + ((size_t)yy * a.W + xx) * C + c0);
-      const uint32_t w4[4] = {q.x, q.y, q.z, q.w};
-      const float* tw = dl + (3 * dy + dx) * C + c0;
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        acc[j] = __fmaf_rn(bf16_bits_to_f32((uint16_t)(w4[j >> 1] >> (16 * (j & 1)))), tw[j], acc[j]);
+      const int xx = x0 + dx;
+      const bool in = r >= 0 && r < H && xx >= 0 && xx < W;
+      row[dx] = in ? *reinterpret_cast<const uint4*>(src + ((size_t)r * W + xx) * C) : make_uint4(0, 0, 0, 0);
     }
-  float f[8];
+  };
+  load_row(-1, win[0]);
+  load_row(0, win[1]);
+  load_row(1, win[2]);
+  const float* bias = dl + 9 * C + c0;
+  for (int yo = 0; yo < a.Ho; ++yo) {
+    float acc[8];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const float z = acc[j] + dl[9 * C + c0 + j];
-    f[j] = z > 0.0f ? z : 0.0f;
+    for (int j = 0; j < 8; ++j) acc[j] = 0.0f;
+#pragma unroll
+    for (int dy = 0; dy < 3; ++dy)
+#pragma unroll
+      for (int dx = 0; dx < 3; ++dx) {
+        const uint4 q = win[dy][dx];
+        const uint32_t w4[4] = {q.x, q.y, q.z, q.w};
+        const float* tw = dl + (3 * dy + dx) * C + c0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          acc[j] = __fmaf_rn(bf16_bits_to_f32((uint16_t)(w4[j >> 1] >> (16 * (j & 1)))), tw[j], acc[j]);
+      }
+    float f[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float z = acc[j] + bias[j];
+      f[j] = z > 0.0f ? z : 0.0f;
+    }
+    uint32_t pk[4];
+    to_bf16x2(f, pk);
+    *reinterpret_cast<uint4*>(dst + (size_t)yo * a.Wo * C) = make_uint4(pk[0], pk[1], pk[2], pk[3]);
+    // window of output row yo + 1: input rows S (yo + 1) - 1 .. + 2
+    const int r0 = S * (yo + 1) - 1;
+    if (S == 1) {
+#pragma unroll
+      for (int dx = 0; dx < 3; ++dx) {
+        win[0][dx] = win[1][dx];
+        win[1][dx] = win[2][dx];
+      }
+      load_row(r0 + 2, win[2]);
+    } else {
+#pragma unroll
+      for (int dx = 0; dx < 3; ++dx) win[0][dx] = win[2][dx];
+      load_row(r0 + 1, win[1]);
+      load_row(r0 + 2, win[2]);
+    }
   }
-  uint32_t pk[4];
-  to_bf16x2(f, pk);
-  *reinterpret_cast<uint4*>(a.out + a.out_vs * v + (size_t)pix * C + c0) = make_uint4(pk[0], pk[1], pk[2], pk[3]);
 }
 
 // global average pooling: one thread per pooled row (image) and 8 channels
@@ -193,6 +282,9 @@ __global__ __launch_bounds__(256) void k_cnn_pool(CnnPoolArgs a) {
 namespace {
 
 int round_up32(int x) { return (x + 31) / 32 * 32; }
+
+// LDS bytes of the stem's zero-padded bf16 image
+size_t cnn_stem_lds(int H, int W, int C) { return ((size_t)(H + 2) * (W + 2) * C * 2 + 15) / 16 * 16; }
 
 // word `word` of the Philox4x32-10 block at counter (c0, c1, c2, stream), key seed
 uint32_t draw_word(uint64_t seed, uint32_t c0, uint32_t c1, uint32_t c2, uint32_t stream, uint32_t word) {
@@ -259,7 +351,7 @@ gevo_status cnn_layout(const gevo_cnn_config* c, int64_t n_test, CnnLayout& y) {
     ch = co;
   }
   y.hin[y.nb] = h; y.win[y.nb] = w;
-  if ((size_t)9 * y.C * y.stem * 4 > 65536) return GEVO_E_UNSUPPORTED;   // stem taps staged in LDS
+  if (cnn_stem_lds(y.H, y.W, y.C) > 56 * 1024) return GEVO_E_UNSUPPORTED;   // the stem stages one image in LDS
   add(ch, y.classes, 32);                             // head, in the output kernel's 32-class layout
   y.act_vs = act;
   size_t off = 0;
@@ -517,10 +609,9 @@ gevo_status gevo_cnn_predict(gevo_cnn* h) {
     sa.H = y.H; sa.W = y.W; sa.Np = ts.Np;
     sa.wp = at<const float>(ws, ts.pack); sa.bias = at<const float>(ws, ts.bias);
     sa.out = at<uint16_t>(ws, y.actA); sa.out_vs = y.act_vs;
-    const int stem_px = kCnnChunk * y.H * y.W;
     LaunchEv ev = cnn_prof(h, GEVO_CNN_KERNEL_STEM);
-    const dim3 sg((stem_px + 255) / 256, P);
-    const size_t lds = (size_t)ts.K * ts.Np * 4;
+    const dim3 sg(kCnnChunk, P);                                 // one workgroup per (variant, image)
+    const size_t lds = cnn_stem_lds(y.H, y.W, y.C);
     switch (y.C) {
       case 1: hipExtLaunchKernelGGL(k_cnn_stem<1>, sg, dim3(256), lds, s, ev.start, ev.stop, 0, sa); break;
       case 2: hipExtLaunchKernelGGL(k_cnn_stem<2>, sg, dim3(256), lds, s, ev.start, ev.stop, 0, sa); break;
@@ -537,10 +628,13 @@ gevo_status gevo_cnn_predict(gevo_cnn* h) {
       da.out = at<uint16_t>(ws, y.actB); da.out_vs = y.act_vs;
       da.H = y.hin[i]; da.W = y.win[i]; da.C = ch; da.Ho = y.hin[i + 1]; da.Wo = y.win[i + 1]; da.stride = y.stride[i];
       da.wp = at<const float>(ws, td.pack); da.bias = at<const float>(ws, td.bias);
-      const int dw_threads = kCnnChunk * da.Ho * da.Wo * (ch / 8);
+      const int dw_threads = kCnnChunk * da.Wo * (ch / 8);      // (image, column, 8 channels)
       ev = cnn_prof(h, GEVO_CNN_KERNEL_DEPTHWISE);
-      hipExtLaunchKernelGGL(k_cnn_dw, dim3((dw_threads + 255) / 256, P), dim3(256), (size_t)10 * ch * 4, s, ev.start,
-                            ev.stop, 0, da);
+      const dim3 dg((dw_threads + 255) / 256, P);
+      if (da.stride == 1)
+        hipExtLaunchKernelGGL(k_cnn_dw<1>, dg, dim3(256), (size_t)10 * ch * 4, s, ev.start, ev.stop, 0, da);
+      else
+        hipExtLaunchKernelGGL(k_cnn_dw<2>, dg, dim3(256), (size_t)10 * ch * 4, s, ev.start, ev.stop, 0, da);
       CNN_HIP(hipGetLastError());
       FwdGemmArgs g{};
       g.A = at<const uint16_t>(ws, y.actB); g.a_vs = y.act_vs;

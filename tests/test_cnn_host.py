@@ -49,6 +49,8 @@ def test_param_count_matches_the_oracle(key):
     (dict(classes=33), E_UNSUPPORTED),
     (dict(C=5), E_UNSUPPORTED),
     (dict(C=4), OK),
+    (dict(H=96, W=96), E_UNSUPPORTED),                     # padded image over the stem's 56 KiB of LDS
+    (dict(H=64, W=64), OK),
     (dict(P=0), E_ARG),
     (dict(dens=(0.8, 0.7)), E_ARG),
     (dict(dens=(0.5, 1.5)), E_ARG),
