@@ -135,7 +135,7 @@ def predict_flops_per_sample(dims):
 CNN_KERNEL_SOURCES = ["gevo_device.h", "gevo_internal.h", "gevo_kernels.hip", "gevo_gemm.hip", "gevo_cnn.hip"]
 # rocprofv3 kernel-name stem -> kernel kind of the convolutional workload
 CNN_KIND_OF = {"k_cnn_stem": "stem", "k_cnn_dw": "depthwise", "k_fwd_gemm": "pointwise", "k_cnn_pool": "pool",
-               "k_out": "head"}
+               "k_out": "head", "k_cnn_pwdw": "pw_dw"}
 
 
 def source_sha(sources=None):
@@ -444,27 +444,73 @@ def main():
 
 
 # ------------------------------------------------------- convolutional workload
+def cnn_fuse_rows(cin, cout, w, s, ho):
+    """Strip rows of the fused pointwise + depthwise kernel for one block pair,
+    or 0 when the library runs the pair unfused (the library's rule: Cin <= 128, Cout <= 256;
+    a strip's S (R - 1) + 3 rows of inputs, outputs and the taps within 64 KiB
+    of LDS, its inputs within 2,048 pieces of 16 bytes)."""
+    if cin % 32 or cin > 128 or cout % 32 or cout > 256:
+        return 0
+    best = 0
+    for r in range(1, ho + 1):
+        px = (s * (r - 1) + 3) * w
+        lds = (px * (cin + 8) + 7) // 8 * 8 * 2 + (px * (cout + 8) + 7) // 8 * 8 * 2 + 40 * cout
+        if lds <= 64 * 1024 and px * cin // 8 <= 2048:
+            best = r
+    return best
+
+
 def cnn_costs(cfg, n):
     """{kernel kind: (algorithmic HBM bytes, flops)} of one prediction pass over
     n test images for all P variants.  Per image and variant every activation
-    map is written once by its producer and read once by its consumer (bf16);
-    the input image is read once for all variants (fp32); every launch reads
-    its variants' fp32 weights and biases once per 64-image chunk."""
+    map that goes through memory is written once by its producer and read once
+    by its consumer (bf16); a fused pointwise + depthwise pair keeps the
+    pointwise map on chip.  The input image is read once for all variants
+    (fp32); every launch reads its variants' fp32 weights and biases once per
+    64-image chunk."""
     P, H, W, C, cls = cfg["P"], cfg["H"], cfg["W"], cfg["C"], cfg["classes"]
     chunks = (n + 63) // 64
     stem = cfg["stem"]
     out = {"stem": [n * H * W * C * 4 + P * n * H * W * stem * 2 + P * chunks * (9 * C * stem + stem) * 4,
                     2.0 * P * n * H * W * 9 * C * stem]}
-    dw, pw = [0.0, 0.0], [0.0, 0.0]
-    h, w, ch = H, W, stem
-    for s_, co in cfg["blocks"]:
-        ho, wo = (h - 1) // s_ + 1, (w - 1) // s_ + 1
-        dw[0] += P * n * (h * w * ch + ho * wo * ch) * 2 + P * chunks * 10 * ch * 4
-        dw[1] += 2.0 * P * n * ho * wo * ch * 9
-        pw[0] += P * n * ho * wo * (ch + co) * 2 + P * chunks * (ch * co + co) * 4
-        pw[1] += 2.0 * P * n * ho * wo * ch * co
-        h, w, ch = ho, wo, co
-    out["depthwise"], out["pointwise"] = dw, pw
+    blocks = cfg["blocks"]
+    sizes = [(H, W)]
+    for s_, _ in blocks:
+        h, w = sizes[-1]
+        sizes.append(((h - 1) // s_ + 1, (w - 1) // s_ + 1))
+    chans = [stem] + [co for _, co in blocks]          # input channels of block i = chans[i]
+    dw, pw, fu = [0.0, 0.0], [0.0, 0.0], [0.0, 0.0]
+
+    def dw_cost(i):
+        (h, w), (ho, wo), c = sizes[i], sizes[i + 1], chans[i]
+        return P * n * (h * w + ho * wo) * c * 2 + P * chunks * 10 * c * 4, 2.0 * P * n * ho * wo * c * 9
+
+    b0, f0 = dw_cost(0)
+    dw[0] += b0
+    dw[1] += f0
+    i = 0
+    while i < len(blocks):
+        (h, w), ci, co = sizes[i + 1], chans[i], chans[i + 1]
+        pw_fl = 2.0 * P * n * h * w * ci * co
+        if i + 1 < len(blocks) and cnn_fuse_rows(ci, co, w, blocks[i + 1][0], sizes[i + 2][0]):
+            (ho, wo) = sizes[i + 2]
+            fu[0] += P * n * (h * w * ci + ho * wo * co) * 2 + P * chunks * (ci * co + co + 10 * co) * 4
+            fu[1] += pw_fl + 2.0 * P * n * ho * wo * co * 9
+        else:
+            pw[0] += P * n * h * w * (ci + co) * 2 + P * chunks * (ci * co + co) * 4
+            pw[1] += pw_fl
+            if i + 1 < len(blocks):
+                b, f = dw_cost(i + 1)
+                dw[0] += b
+                dw[1] += f
+        i += 1
+    out["depthwise"] = dw
+    if pw[0]:
+        out["pointwise"] = pw
+    if fu[0]:
+        out["pw_dw"] = fu
+    h, w = sizes[-1]
+    ch = chans[-1]
     out["pool"] = [P * n * (h * w * ch + ch) * 2, float(P * n * h * w * ch)]
     out["head"] = [P * n * ch * 2 + P * chunks * (ch * cls + cls) * 4, 2.0 * P * n * ch * cls]
     return {k: tuple(v) for k, v in out.items()}

@@ -440,7 +440,8 @@ typedef enum {
   GEVO_CNN_KERNEL_POOL = 3,        /* global average pooling */
   GEVO_CNN_KERNEL_HEAD = 4,        /* fully connected head, loss and argmax */
   GEVO_CNN_KERNEL_REDUCE = 5,      /* per-variant sums of the chunks' partial scores */
-  GEVO_CNN_KERNEL_KINDS = 6
+  GEVO_CNN_KERNEL_POINTWISE_DEPTHWISE = 6,   /* a pointwise layer fused with the next depthwise layer */
+  GEVO_CNN_KERNEL_KINDS = 7
 } gevo_cnn_kernel_kind;
 
 gevo_status gevo_cnn_set_profiling(gevo_cnn* h, int enable);

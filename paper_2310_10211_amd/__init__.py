@@ -42,7 +42,7 @@ EXPORTED = [
     "gevo_cnn_export", "gevo_cnn_destroy", "gevo_cnn_set_profiling", "gevo_cnn_kernel_stats",
 ]
 CNN_MAX_BLOCKS = 4
-CNN_KERNEL_KINDS = ["stem", "depthwise", "pointwise", "pool", "head", "reduce"]
+CNN_KERNEL_KINDS = ["stem", "depthwise", "pointwise", "pool", "head", "reduce", "pw_dw"]
 KERNEL_KINDS = ["init", "gather", "layer_train", "layer_fwd", "out_train", "out_predict", "bwd", "aux",
                 "fused_train"]
 

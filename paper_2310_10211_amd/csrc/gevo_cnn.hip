@@ -46,6 +46,15 @@ struct CnnDwArgs {
   const float* wp; const float* bias;         // bf16-valued taps [P][9][C] (fp32 storage), biases [P][C]
 };
 
+struct CnnPwDwArgs {
+  const uint16_t* in; size_t in_vs;           // pointwise input [v][chunk][H][W][Cin]
+  const float* Wm; const float* pbias;        // pointwise master [P][Cin/32][Cout][32], biases [P][Cout]
+  const float* dwp; const float* dbias;       // depthwise taps [P][9][Cout] (bf16-valued fp32), biases [P][Cout]
+  uint16_t* out; size_t out_vs;               // depthwise output [v][chunk][Ho][Wo][Cout]
+  int H, W, Cin, Cout, Ho, Wo, R;             // R: depthwise output rows per strip
+  int ipw;                                    // images per workgroup (divides the chunk)
+};
+
 struct CnnPoolArgs {
   const uint16_t* in; size_t in_vs;           // [v][chunk][HW][C]
   int HW, C;
@@ -95,7 +104,7 @@ __device__ __forceinline__ f32x16_t cnn_mma(cnn_u32x4 a, cnn_u32x4 b, f32x16_t c
 template <int C>
 __global__ __launch_bounds__(256) void k_cnn_stem(CnnStemArgs a) {
   constexpr int K = 9 * C, KS = (K + 15) / 16;
-  __shared__ __align__(16) uint32_t stage[4][32 * 16];         // per wave: 32 pixels x 32 channels bf16
+  __shared__ __align__(16) uint32_t stage[4][32 * 20];         // per wave: 32 pixels x 32 channels bf16 (+8 pad)
   extern __shared__ __align__(16) uint16_t im[];                // [H + 2][W + 2][C]
   int v, img;
   cnn_slot(v, img);
@@ -163,12 +172,12 @@ __global__ __launch_bounds__(256) void k_cnn_stem(CnnStemArgs a) {
       uint32_t pk[8];
       to_bf16x2(f, pk);                                  // pk[i]: channels crow(2i), crow(2i) + 1
 #pragma unroll
-      for (int i = 0; i < 8; ++i) st[(l32 * 32 + crow(2 * i, lane)) / 2] = pk[i];
+      for (int i = 0; i < 8; ++i) st[l32 * 20 + crow(2 * i, lane) / 2] = pk[i];
       __builtin_amdgcn_wave_barrier();
 #pragma unroll
       for (int h = 0; h < 2; ++h) {                      // 16 pixels x 64 bytes per pass
         const int px = 16 * h + (lane >> 2), q = lane & 3;
-        const cnn_u32x4 val = *reinterpret_cast<const cnn_u32x4*>(st + px * 16 + q * 4);
+        const cnn_u32x4 val = *reinterpret_cast<const cnn_u32x4*>(st + px * 20 + q * 4);
         if (t * 32 + px < HW) *reinterpret_cast<cnn_u32x4*>(ov + (size_t)(t * 32 + px) * Np + n0 + q * 8) = val;
       }
       __builtin_amdgcn_wave_barrier();
@@ -253,6 +262,174 @@ __global__ __launch_bounds__(256) void k_cnn_dw(CnnDwArgs a) {
   }
 }
 
+// A pointwise convolution fused with the depthwise convolution after it
+// (stride S): one workgroup per (variant, ipw images) walks each image's
+// depthwise output rows in strips of R (several images per workgroup share
+// one load of the variant's pointwise weights).  A strip needs the pointwise outputs of S (R - 1) + 3
+// input rows (those inside the image):
+//   1. their pointwise inputs are staged in LDS (rows of the image are
+//      contiguous, so these are whole 16-byte pieces of one contiguous span;
+//      the next strip's pieces are loaded into registers while the current
+//      strip is computed);
+//   2. the pointwise outputs go to LDS as bf16 from 32x32x16 bf16 MFMAs with
+//      fp32 accumulation: per 32-pixel x 32-channel tile out^T[n][p] =
+//      sum_k W[k][n] A[p][k]; lane l gives channel / pixel l % 32 and k slots
+//      8 (l / 32) + 0..7 of each 16-k step in both operands, and its
+//      accumulator holds channels crow(r, l) of pixel l % 32; wave w takes
+//      the channel tiles w, w + 4, ...;
+//   3. the depthwise convolution reads them from LDS, one thread per (output
+//      pixel, 8 channels), and writes its output.
+// The pointwise output never goes to global memory.  Cin <= 128, Cout <= 256,
+// and a
+// strip's inputs are at most kPwDwPieces x 256 pieces of 16 bytes.
+constexpr int kPwDwPieces = 8;
+
+template <int S>
+__global__ __launch_bounds__(256) void k_cnn_pwdw(CnnPwDwArgs a) {
+  extern __shared__ __align__(16) char smem[];
+  int v, w;
+  cnn_slot(v, w);
+  const int Cin = a.Cin, Cout = a.Cout, H = a.H, W = a.W, KS = Cin / 16, AS = Cin + 8, PS = Cout + 8;
+  const int rows_in = S * (a.R - 1) + 3;
+  uint16_t* al = reinterpret_cast<uint16_t*>(smem);                                // [rows_in W][Cin + 8]
+  uint16_t* pl = al + (((size_t)rows_in * W * AS + 7) & ~(size_t)7);                 // [rows_in][W][Cout + 8]
+  float* dt = reinterpret_cast<float*>(pl + (((size_t)rows_in * W * PS + 7) & ~(size_t)7));     // [10][Cout]
+  for (int i = threadIdx.x; i < 9 * Cout; i += blockDim.x) dt[i] = a.dwp[(size_t)v * 9 * Cout + i];
+  for (int c = threadIdx.x; c < Cout; c += blockDim.x) dt[9 * Cout + c] = a.dbias[(size_t)v * Cout + c];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l32 = lane & 31, lh = lane >> 5;
+  const float* Wv = a.Wm + (size_t)v * Cin * Cout;
+  const float* pb = a.pbias + (size_t)v * Cout;
+  const int C8in = Cin / 8;
+  // jobs: (image, strip) pairs of this workgroup's images, in order
+  const int nstrips = (a.Ho + a.R - 1) / a.R, njobs = a.ipw * nstrips;
+  auto job_image = [&](int j) { return w * a.ipw + j / nstrips; };
+  auto job_row = [&](int j) { return (j % nstrips) * a.R; };
+  // rows [rv0, rv1) of the strip starting at depthwise output row yo0
+  auto strip_rows = [&](int yo0, int& rv0, int& rv1) {
+    rv0 = max(0, S * yo0 - 1);
+    rv1 = min(H, S * yo0 - 1 + rows_in);
+  };
+  cnn_u32x4 pre[kPwDwPieces];
+  auto fetch = [&](int j) {
+    int rv0, rv1;
+    strip_rows(job_row(j), rv0, rv1);
+    const int n = (rv1 - rv0) * W * C8in;
+    const uint16_t* src = a.in + a.in_vs * v + ((size_t)job_image(j) * H + rv0) * W * Cin;
+#pragma unroll
+    for (int q = 0; q < kPwDwPieces; ++q) {
+      const int p = threadIdx.x + 256 * q;
+      if (p < n) pre[q] = *reinterpret_cast<const cnn_u32x4*>(src + (size_t)p * 8);
+    }
+  };
+  auto commit = [&](int j) {
+    int rv0, rv1;
+    strip_rows(job_row(j), rv0, rv1);
+    const int n = (rv1 - rv0) * W * C8in;
+#pragma unroll
+    for (int q = 0; q < kPwDwPieces; ++q) {
+      const int p = threadIdx.x + 256 * q;
+      if (p < n) *reinterpret_cast<cnn_u32x4*>(al + (size_t)(p / C8in) * AS + (p % C8in) * 8) = pre[q];
+    }
+  };
+  // this wave's channel tiles (wave, wave + 4; Cout <= 256): weights as bf16 A
+  // operands and the biases of the accumulator rows, loaded once
+  cnn_u32x4 awt[2][8];
+  float biast[2][16];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int n0 = min(wave + 4 * u, Cout / 32 - 1) * 32;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      if (s < KS) {
+        const int k = 16 * s + 8 * lh;
+        const float* src = Wv + ((size_t)(k / 32) * Cout + n0 + l32) * 32 + k % 32;
+        const float4 w0 = *reinterpret_cast<const float4*>(src);
+        const float4 w1 = *reinterpret_cast<const float4*>(src + 4);
+        awt[u][s] = cnn_u32x4{f32_to_bf16_bits(w0.x) | (uint32_t)f32_to_bf16_bits(w0.y) << 16,
+                              f32_to_bf16_bits(w0.z) | (uint32_t)f32_to_bf16_bits(w0.w) << 16,
+                              f32_to_bf16_bits(w1.x) | (uint32_t)f32_to_bf16_bits(w1.y) << 16,
+                              f32_to_bf16_bits(w1.z) | (uint32_t)f32_to_bf16_bits(w1.w) << 16};
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) biast[u][r] = pb[n0 + crow(r, lane)];
+  }
+  fetch(0);
+  commit(0);
+  __syncthreads();
+  for (int j = 0; j < njobs; ++j) {
+    const bool more = j + 1 < njobs;
+    if (more) fetch(j + 1);                                  // in flight through this strip's work
+    const int yo0 = job_row(j);
+    uint16_t* ov = a.out + a.out_vs * v + (size_t)job_image(j) * a.Ho * a.Wo * Cout;
+    const int rbase = S * yo0 - 1;
+    int rv0, rv1;
+    strip_rows(yo0, rv0, rv1);
+    const int M = (rv1 - rv0) * W, mt = (M + 31) / 32;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int nt = wave + 4 * u;
+      if (nt >= Cout / 32) break;
+      const int n0 = nt * 32;
+      const cnn_u32x4* aw = awt[u];
+      const float* bias = biast[u];
+      for (int m = 0; m < mt; ++m) {
+        const int pm = min(m * 32 + l32, M - 1);            // pixels past the strip: computed, never stored
+        const uint16_t* ap = al + (size_t)pm * AS + 8 * lh;
+        f32x16_t acc = zero16();
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+          if (s < KS) acc = cnn_mma(aw[s], *reinterpret_cast<const cnn_u32x4*>(ap + 16 * s), acc);
+        float f[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float z = acc[r] + bias[r];
+          f[r] = z > 0.0f ? z : 0.0f;
+        }
+        uint32_t pk[8];
+        to_bf16x2(f, pk);                                    // pk[i]: channels crow(2i), crow(2i) + 1
+        if (m * 32 + l32 < M) {
+          uint16_t* dst = pl + ((size_t)(rv0 - rbase) * W + m * 32 + l32) * PS + n0 + 4 * lh;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) *reinterpret_cast<uint2*>(dst + 8 * q) = make_uint2(pk[2 * q], pk[2 * q + 1]);
+        }
+      }
+    }
+    __syncthreads();                                         // pointwise strip complete; its inputs are free
+    const int R = min(a.R, a.Ho - yo0), C8 = Cout / 8, items = R * a.Wo * C8;
+    for (int it = threadIdx.x; it < items; it += blockDim.x) {
+      const int c0 = (it % C8) * 8, xo = (it / C8) % a.Wo, yo = yo0 + it / (C8 * a.Wo);
+      float acc[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[j] = 0.0f;
+#pragma unroll
+      for (int dy = 0; dy < 3; ++dy)
+#pragma unroll
+        for (int dx = 0; dx < 3; ++dx) {
+          const int r = S * yo + dy - 1, xx = S * xo + dx - 1;
+          if (r < 0 || r >= H || xx < 0 || xx >= W) continue;
+          const uint4 q = *reinterpret_cast<const uint4*>(pl + ((size_t)(r - rbase) * W + xx) * PS + c0);
+          const uint32_t w4[4] = {q.x, q.y, q.z, q.w};
+          const float* tw = dt + (3 * dy + dx) * Cout + c0;
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            acc[j] = __fmaf_rn(bf16_bits_to_f32((uint16_t)(w4[j >> 1] >> (16 * (j & 1)))), tw[j], acc[j]);
+        }
+      float f[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float z = acc[j] + dt[9 * Cout + c0 + j];
+        f[j] = z > 0.0f ? z : 0.0f;
+      }
+      uint32_t pk[4];
+      to_bf16x2(f, pk);
+      *reinterpret_cast<uint4*>(ov + ((size_t)yo * a.Wo + xo) * Cout + c0) = make_uint4(pk[0], pk[1], pk[2], pk[3]);
+    }
+    if (more) commit(j + 1);
+    __syncthreads();                                         // next inputs staged; this strip's outputs read
+  }
+}
+
 // global average pooling: one thread per pooled row (image) and 8 channels
 __global__ __launch_bounds__(256) void k_cnn_pool(CnnPoolArgs a) {
   const int v = blockIdx.y, C8 = a.C / 8;
@@ -286,6 +463,28 @@ int round_up32(int x) { return (x + 31) / 32 * 32; }
 // LDS bytes of the stem's zero-padded bf16 image
 size_t cnn_stem_lds(int H, int W, int C) { return ((size_t)(H + 2) * (W + 2) * C * 2 + 15) / 16 * 16; }
 
+// LDS bytes of the fused pointwise + depthwise kernel for strips of R output
+// rows: the pointwise inputs (S (R - 1) + 3 rows of W pixels x (Cin + 8) bf16),
+// the pointwise outputs (the same rows x (Cout + 8) bf16), the depthwise taps and
+// biases (fp32)
+size_t cnn_pwdw_lds(int S, int R, int W, int Cin, int Cout) {
+  const size_t px = (size_t)(S * (R - 1) + 3) * W;
+  return ((px * (Cin + 8) + 7) & ~(size_t)7) * 2 + ((px * (Cout + 8) + 7) & ~(size_t)7) * 2 + (size_t)10 * Cout * 4;
+}
+
+// Strip rows of the fused kernel for pointwise Cin -> Cout on H x W followed
+// by a depthwise stride S to Ho rows: the most rows whose LDS fits 64 KiB and
+// whose inputs fit the staging registers, or 0 when the pair runs unfused.
+int cnn_fuse_rows(int Cin, int Cout, int W, int S, int Ho) {
+  if (Cin % 32 || Cin > 128 || Cout % 32 || Cout > 256) return 0;
+  int R = 0;
+  for (int r = 1; r <= Ho; ++r) {
+    const size_t pieces = (size_t)(S * (r - 1) + 3) * W * Cin / 8;
+    if (cnn_pwdw_lds(S, r, W, Cin, Cout) <= 64 * 1024 && pieces <= (size_t)kPwDwPieces * 256) R = r;
+  }
+  return R;
+}
+
 // word `word` of the Philox4x32-10 block at counter (c0, c1, c2, stream), key seed
 uint32_t draw_word(uint64_t seed, uint32_t c0, uint32_t c1, uint32_t c2, uint32_t stream, uint32_t word) {
   const uint32_t ctr[4] = {c0, c1, c2, stream};
@@ -307,6 +506,7 @@ struct CnnLayout {
   int P = 0, nb = 0, H = 0, W = 0, C = 0, classes = 0, n_chunks = 0;
   int64_t n_test = 0;
   int stem = 0, ch[GEVO_CNN_MAX_BLOCKS] = {0}, stride[GEVO_CNN_MAX_BLOCKS] = {0};
+  int fuse_R[GEVO_CNN_MAX_BLOCKS] = {0};      // > 0: pointwise i runs fused with depthwise i + 1, R rows per strip
   int hin[GEVO_CNN_MAX_BLOCKS + 1] = {0}, win[GEVO_CNN_MAX_BLOCKS + 1] = {0};   // spatial size entering block i (last: the head)
   int nt = 0;
   CnnTensor t[2 * GEVO_CNN_MAX_BLOCKS + 2];  // stem, (dw, pw) per block, fc
@@ -351,6 +551,13 @@ gevo_status cnn_layout(const gevo_cnn_config* c, int64_t n_test, CnnLayout& y) {
     ch = co;
   }
   y.hin[y.nb] = h; y.win[y.nb] = w;
+  {
+    int cin = y.stem;
+    for (int i = 0; i + 1 < y.nb; ++i) {
+      y.fuse_R[i] = cnn_fuse_rows(cin, y.ch[i], y.win[i + 1], y.stride[i + 1], y.hin[i + 2]);
+      cin = y.ch[i];
+    }
+  }
   if (cnn_stem_lds(y.H, y.W, y.C) > 56 * 1024) return GEVO_E_UNSUPPORTED;   // the stem stages one image in LDS
   add(ch, y.classes, 32);                             // head, in the output kernel's 32-class layout
   y.act_vs = act;
@@ -619,34 +826,67 @@ gevo_status gevo_cnn_predict(gevo_cnn* h) {
       default: hipExtLaunchKernelGGL(k_cnn_stem<4>, sg, dim3(256), lds, s, ev.start, ev.stop, 0, sa); break;
     }
     CNN_HIP(hipGetLastError());
-    int ch = y.stem;
-    for (int i = 0; i < y.nb; ++i) {
+    // activations ping-pong between the two buffers; `cur` holds the latest map
+    uint16_t* cur = at<uint16_t>(ws, y.actA);
+    uint16_t* other = at<uint16_t>(ws, y.actB);
+    auto depthwise = [&](int i, int C) -> hipError_t {      // depthwise of block i: cur -> other
       const CnnTensor& td = y.t[1 + 2 * i];
-      const CnnTensor& tp = y.t[2 + 2 * i];
       CnnDwArgs da{};
-      da.in = at<const uint16_t>(ws, y.actA); da.in_vs = y.act_vs;
-      da.out = at<uint16_t>(ws, y.actB); da.out_vs = y.act_vs;
-      da.H = y.hin[i]; da.W = y.win[i]; da.C = ch; da.Ho = y.hin[i + 1]; da.Wo = y.win[i + 1]; da.stride = y.stride[i];
+      da.in = cur; da.in_vs = y.act_vs;
+      da.out = other; da.out_vs = y.act_vs;
+      da.H = y.hin[i]; da.W = y.win[i]; da.C = C; da.Ho = y.hin[i + 1]; da.Wo = y.win[i + 1]; da.stride = y.stride[i];
       da.wp = at<const float>(ws, td.pack); da.bias = at<const float>(ws, td.bias);
-      const int dw_threads = kCnnChunk * da.Wo * (ch / 8);      // (image, column, 8 channels)
-      ev = cnn_prof(h, GEVO_CNN_KERNEL_DEPTHWISE);
+      const int dw_threads = kCnnChunk * da.Wo * (C / 8);        // (image, column, 8 channels)
+      const LaunchEv e = cnn_prof(h, GEVO_CNN_KERNEL_DEPTHWISE);
       const dim3 dg((dw_threads + 255) / 256, P);
       if (da.stride == 1)
-        hipExtLaunchKernelGGL(k_cnn_dw<1>, dg, dim3(256), (size_t)10 * ch * 4, s, ev.start, ev.stop, 0, da);
+        hipExtLaunchKernelGGL(k_cnn_dw<1>, dg, dim3(256), (size_t)10 * C * 4, s, e.start, e.stop, 0, da);
       else
-        hipExtLaunchKernelGGL(k_cnn_dw<2>, dg, dim3(256), (size_t)10 * ch * 4, s, ev.start, ev.stop, 0, da);
-      CNN_HIP(hipGetLastError());
-      FwdGemmArgs g{};
-      g.A = at<const uint16_t>(ws, y.actB); g.a_vs = y.act_vs;
-      g.Wm = at<const float>(ws, tp.Wm); g.bias = at<const float>(ws, tp.bias);
-      g.O = at<uint16_t>(ws, y.actA); g.o_vs = y.act_vs;
-      g.Kp = tp.Kp; g.Np = tp.Np; g.R = kCnnChunk * da.Ho * da.Wo; g.P = P;
-      if (!fwd_gemm_supported(g.Kp, g.Np, g.R)) return GEVO_E_SHAPE;
-      CNN_HIP(launch_fwd_gemm(g, s, cnn_prof(h, GEVO_CNN_KERNEL_POINTWISE)));
-      ch = y.ch[i];
+        hipExtLaunchKernelGGL(k_cnn_dw<2>, dg, dim3(256), (size_t)10 * C * 4, s, e.start, e.stop, 0, da);
+      std::swap(cur, other);
+      return hipGetLastError();
+    };
+    CNN_HIP(depthwise(0, y.stem));
+    int ch = y.stem;
+    for (int i = 0; i < y.nb; ++i) {
+      const CnnTensor& tp = y.t[2 + 2 * i];
+      const int Hp = y.hin[i + 1], Wp = y.win[i + 1];          // the pointwise layer's spatial size
+      if (i + 1 < y.nb && y.fuse_R[i] > 0) {
+        // pointwise i and depthwise i + 1 in one kernel: cur -> other
+        const CnnTensor& td = y.t[1 + 2 * (i + 1)];
+        CnnPwDwArgs fa{};
+        fa.in = cur; fa.in_vs = y.act_vs;
+        fa.Wm = at<const float>(ws, tp.Wm); fa.pbias = at<const float>(ws, tp.bias);
+        fa.dwp = at<const float>(ws, td.pack); fa.dbias = at<const float>(ws, td.bias);
+        fa.out = other; fa.out_vs = y.act_vs;
+        fa.H = Hp; fa.W = Wp; fa.Cin = ch; fa.Cout = y.ch[i];
+        fa.Ho = y.hin[i + 2]; fa.Wo = y.win[i + 2]; fa.R = y.fuse_R[i];
+        fa.ipw = Hp * Wp >= 1024 ? 1 : (Hp * Wp >= 256 ? 4 : 8);   // images per workgroup
+        const int S = y.stride[i + 1];
+        const size_t lds = cnn_pwdw_lds(S, fa.R, fa.W, fa.Cin, fa.Cout);
+        const LaunchEv e = cnn_prof(h, GEVO_CNN_KERNEL_POINTWISE_DEPTHWISE);
+        if (S == 1)
+          hipExtLaunchKernelGGL(k_cnn_pwdw<1>, dim3(kCnnChunk / fa.ipw, P), dim3(256), lds, s, e.start, e.stop, 0, fa);
+        else
+          hipExtLaunchKernelGGL(k_cnn_pwdw<2>, dim3(kCnnChunk / fa.ipw, P), dim3(256), lds, s, e.start, e.stop, 0, fa);
+        CNN_HIP(hipGetLastError());
+        std::swap(cur, other);                                     // cur: depthwise i + 1 output
+        ch = y.ch[i];
+      } else {
+        FwdGemmArgs g{};
+        g.A = cur; g.a_vs = y.act_vs;
+        g.Wm = at<const float>(ws, tp.Wm); g.bias = at<const float>(ws, tp.bias);
+        g.O = other; g.o_vs = y.act_vs;
+        g.Kp = tp.Kp; g.Np = tp.Np; g.R = kCnnChunk * Hp * Wp; g.P = P;
+        if (!fwd_gemm_supported(g.Kp, g.Np, g.R)) return GEVO_E_SHAPE;
+        CNN_HIP(launch_fwd_gemm(g, s, cnn_prof(h, GEVO_CNN_KERNEL_POINTWISE)));
+        std::swap(cur, other);
+        ch = y.ch[i];
+        if (i + 1 < y.nb) CNN_HIP(depthwise(i + 1, ch));
+      }
     }
     CnnPoolArgs pa{};
-    pa.in = at<const uint16_t>(ws, y.actA); pa.in_vs = y.act_vs;
+    pa.in = cur; pa.in_vs = y.act_vs;
     pa.HW = y.hin[y.nb] * y.win[y.nb]; pa.C = ch;
     pa.out = at<uint16_t>(ws, y.pooled); pa.out_vs = (size_t)kCnnRows * ch;
     ev = cnn_prof(h, GEVO_CNN_KERNEL_POOL);

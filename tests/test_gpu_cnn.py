@@ -59,6 +59,12 @@ SMALL_SHAPES = [
          n_test=70, seed=33, noise_std=0.0),
     dict(name="p3-dwsep-cnn8x8x1-32-128-256-32", P=3, C=1, blocks=[(1, 128), (2, 256)], classes=32,
          n_test=64, seed=34, dens=(0.2, 0.9), noise_std=0.05),
+    # stride-1 depthwise layers after pointwise ones (the fused kernel with S = 1)
+    dict(name="p2-dwsep-cnn8x8x3-32-128-128-256-10", P=2, blocks=[(2, 128), (1, 128), (1, 256)], n_test=100,
+         seed=35),
+    # a 256-channel pointwise input: that pair runs unfused, the first pair fused in two strips
+    dict(name="p2-dwsep-cnn8x8x3-32-256-128-128-10", P=2, blocks=[(1, 256), (1, 128), (2, 128)], n_test=100,
+         seed=36),
 ]
 
 
