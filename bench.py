@@ -446,15 +446,16 @@ def main():
 # ------------------------------------------------------- convolutional workload
 def cnn_fuse_rows(cin, cout, w, s, ho):
     """Strip rows of the fused pointwise + depthwise kernel for one block pair,
-    or 0 when the library runs the pair unfused (the library's rule: Cin <= 128, Cout <= 256;
-    a strip's S (R - 1) + 3 rows of inputs, outputs and the taps within 64 KiB
-    of LDS, its inputs within 2,048 pieces of 16 bytes)."""
-    if cin % 32 or cin > 128 or cout % 32 or cout > 256:
+    or 0 when the library runs the pair unfused (the library's rule: Cin <= 128
+    and Cout 128 or 256; a strip's S (R - 1) + 3 rows of inputs and outputs
+    and the tap pairs within 64 KiB of LDS, its inputs within 2,048 pieces of
+    16 bytes)."""
+    if cin % 32 or cin > 128 or cout not in (128, 256):
         return 0
     best = 0
     for r in range(1, ho + 1):
         px = (s * (r - 1) + 3) * w
-        lds = (px * (cin + 8) + 7) // 8 * 8 * 2 + (px * (cout + 8) + 7) // 8 * 8 * 2 + 40 * cout
+        lds = (px * (cin + 8) + 7) // 8 * 8 * 2 + (px * (cout + 8) + 7) // 8 * 8 * 2 + 24 * cout
         if lds <= 64 * 1024 and px * cin // 8 <= 2048:
             best = r
     return best

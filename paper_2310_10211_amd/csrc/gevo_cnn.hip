@@ -43,13 +43,13 @@ struct CnnDwArgs {
   const uint16_t* in; size_t in_vs;           // [v][chunk][H][W][C]
   uint16_t* out; size_t out_vs;               // [v][chunk][Ho][Wo][C]
   int H, W, C, Ho, Wo, stride;
-  const float* wp; const float* bias;         // bf16-valued taps [P][9][C] (fp32 storage), biases [P][C]
+  const uint32_t* wp; const float* bias;      // tap pairs [P][5][C] (bf16 x 2), biases [P][C]
 };
 
 struct CnnPwDwArgs {
   const uint16_t* in; size_t in_vs;           // pointwise input [v][chunk][H][W][Cin]
   const float* Wm; const float* pbias;        // pointwise master [P][Cin/32][Cout][32], biases [P][Cout]
-  const float* dwp; const float* dbias;       // depthwise taps [P][9][Cout] (bf16-valued fp32), biases [P][Cout]
+  const uint32_t* dwp; const float* dbias;    // depthwise tap pairs [P][5][Cout] (bf16 x 2), biases [P][Cout]
   uint16_t* out; size_t out_vs;               // depthwise output [v][chunk][Ho][Wo][Cout]
   int H, W, Cin, Cout, Ho, Wo, R;             // R: depthwise output rows per strip
   int ipw;                                    // images per workgroup (divides the chunk)
@@ -91,6 +91,53 @@ typedef uint32_t cnn_u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ f32x16_t cnn_mma(cnn_u32x4 a, cnn_u32x4 b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c,
                                                  0, 0, 0);
+}
+
+// Depthwise taps of the prediction copy as bf16 pairs: out[v][p][c] holds taps
+// 2p (low half) and 2p + 1 (high half) of channel c, tap 9 being zero, read
+// from the k-blocked master [v][1][C][32] (taps k < 9 of channel c).
+__global__ __launch_bounds__(256) void k_cnn_pack_pairs(const float* __restrict__ Wm, int C, int P,
+                                                        uint32_t* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)P * 5 * C) return;
+  const int c = (int)(i % C), p = (int)((i / C) % 5), v = (int)(i / ((int64_t)5 * C));
+  const float* w = Wm + ((size_t)v * C + c) * 32;
+  const uint32_t lo = f32_to_bf16_bits(w[2 * p]);
+  const uint32_t hi = 2 * p + 1 < 9 ? f32_to_bf16_bits(w[2 * p + 1]) : 0u;
+  out[i] = lo | hi << 16;
+}
+
+typedef __bf16 cnn_bf16x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float cnn_dot2(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(cnn_bf16x2, a), __builtin_bit_cast(cnn_bf16x2, b), c,
+                                         false);
+}
+
+// One depthwise output for 8 channels: acc[j] += sum_t in[t][j] w[t][j] over
+// the 9 taps (in[t]: 8 bf16 channels of tap t = 3 dy + dx, zero outside the
+// image).  Taps
+// go in pairs (2p, 2p + 1) through the bf16 dot2 instruction (two products
+// summed into the fp32 accumulator), the inputs re-paired by channel.
+// tap(t) gives in[t]; wp: tap pairs [5][C] at this thread's first channel.
+template <typename Tap>
+__device__ __forceinline__ void cnn_dw_dot(Tap tap, const uint32_t* wp, int C, float (&acc)[8]) {
+#pragma unroll
+  for (int p = 0; p < 5; ++p) {
+    const uint4 wa = *reinterpret_cast<const uint4*>(wp + p * C);
+    const uint4 wb = *reinterpret_cast<const uint4*>(wp + p * C + 4);
+    const uint32_t w[8] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
+    const uint4 q0 = tap(2 * p);
+    const uint4 q1 = p < 4 ? tap(2 * p + 1) : make_uint4(0, 0, 0, 0);
+    const uint32_t a0[4] = {q0.x, q0.y, q0.z, q0.w}, a1[4] = {q1.x, q1.y, q1.z, q1.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {                       // channels 2i, 2i + 1
+      const uint32_t lo = (a0[i] & 0xffffu) | (a1[i] << 16);
+      const uint32_t hi = (a0[i] >> 16) | (a1[i] & 0xffff0000u);
+      acc[2 * i] = cnn_dot2(lo, w[2 * i], acc[2 * i]);
+      acc[2 * i + 1] = cnn_dot2(hi, w[2 * i + 1], acc[2 * i + 1]);
+    }
+  }
 }
 
 // stem as a GEMM on the matrix cores: per 32-pixel tile and 32 output
@@ -192,13 +239,14 @@ __global__ __launch_bounds__(256) void k_cnn_stem(CnnStemArgs a) {
 // consecutive pixels.
 template <int S>
 __global__ __launch_bounds__(256) void k_cnn_dw(CnnDwArgs a) {
-  extern __shared__ float dl[];                        // taps [9][C], then bias [C]
+  extern __shared__ uint32_t dl[];                     // tap pairs [5][C], then bias [C] (fp32)
   int v, w;
   cnn_slot(v, w);
   const int C = a.C, H = a.H, W = a.W;
-  const float* wv = a.wp + (size_t)v * 9 * C;
-  for (int i = threadIdx.x; i < 9 * C; i += blockDim.x) dl[i] = wv[i];
-  for (int c = threadIdx.x; c < C; c += blockDim.x) dl[9 * C + c] = a.bias[(size_t)v * C + c];
+  const uint32_t* wv = a.wp + (size_t)v * 5 * C;
+  for (int i = threadIdx.x; i < 5 * C; i += blockDim.x) dl[i] = wv[i];
+  float* dbias = reinterpret_cast<float*>(dl + 5 * C);
+  for (int c = threadIdx.x; c < C; c += blockDim.x) dbias[c] = a.bias[(size_t)v * C + c];
   __syncthreads();
   const int C8 = C / 8;
   const int i = w * 256 + threadIdx.x;
@@ -219,22 +267,12 @@ __global__ __launch_bounds__(256) void k_cnn_dw(CnnDwArgs a) {
   load_row(-1, win[0]);
   load_row(0, win[1]);
   load_row(1, win[2]);
-  const float* bias = dl + 9 * C + c0;
+  const float* bias = dbias + c0;
   for (int yo = 0; yo < a.Ho; ++yo) {
     float acc[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[j] = 0.0f;
-#pragma unroll
-    for (int dy = 0; dy < 3; ++dy)
-#pragma unroll
-      for (int dx = 0; dx < 3; ++dx) {
-        const uint4 q = win[dy][dx];
-        const uint32_t w4[4] = {q.x, q.y, q.z, q.w};
-        const float* tw = dl + (3 * dy + dx) * C + c0;
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-          acc[j] = __fmaf_rn(bf16_bits_to_f32((uint16_t)(w4[j >> 1] >> (16 * (j & 1)))), tw[j], acc[j]);
-      }
+    cnn_dw_dot([&](int t) { return win[t / 3][t % 3]; }, dl + c0, C, acc);
     float f[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
@@ -279,12 +317,12 @@ __global__ __launch_bounds__(256) void k_cnn_dw(CnnDwArgs a) {
 //      the channel tiles w, w + 4, ...;
 //   3. the depthwise convolution reads them from LDS, one thread per (output
 //      pixel, 8 channels), and writes its output.
-// The pointwise output never goes to global memory.  Cin <= 128, Cout <= 256,
+// The pointwise output never goes to global memory.  Cin <= 128, Cout = 128 NT,
 // and a
 // strip's inputs are at most kPwDwPieces x 256 pieces of 16 bytes.
 constexpr int kPwDwPieces = 8;
 
-template <int S>
+template <int S, int NT>
 __global__ __launch_bounds__(256) void k_cnn_pwdw(CnnPwDwArgs a) {
   extern __shared__ __align__(16) char smem[];
   int v, w;
@@ -293,9 +331,10 @@ __global__ __launch_bounds__(256) void k_cnn_pwdw(CnnPwDwArgs a) {
   const int rows_in = S * (a.R - 1) + 3;
   uint16_t* al = reinterpret_cast<uint16_t*>(smem);                                // [rows_in W][Cin + 8]
   uint16_t* pl = al + (((size_t)rows_in * W * AS + 7) & ~(size_t)7);                 // [rows_in][W][Cout + 8]
-  float* dt = reinterpret_cast<float*>(pl + (((size_t)rows_in * W * PS + 7) & ~(size_t)7));     // [10][Cout]
-  for (int i = threadIdx.x; i < 9 * Cout; i += blockDim.x) dt[i] = a.dwp[(size_t)v * 9 * Cout + i];
-  for (int c = threadIdx.x; c < Cout; c += blockDim.x) dt[9 * Cout + c] = a.dbias[(size_t)v * Cout + c];
+  uint32_t* dt = reinterpret_cast<uint32_t*>(pl + (((size_t)rows_in * W * PS + 7) & ~(size_t)7));  // [5][Cout] pairs
+  float* dbias = reinterpret_cast<float*>(dt + 5 * Cout);                                             // [Cout]
+  for (int i = threadIdx.x; i < 5 * Cout; i += blockDim.x) dt[i] = a.dwp[(size_t)v * 5 * Cout + i];
+  for (int c = threadIdx.x; c < Cout; c += blockDim.x) dbias[c] = a.dbias[(size_t)v * Cout + c];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l32 = lane & 31, lh = lane >> 5;
   const float* Wv = a.Wm + (size_t)v * Cin * Cout;
   const float* pb = a.pbias + (size_t)v * Cout;
@@ -331,12 +370,12 @@ __global__ __launch_bounds__(256) void k_cnn_pwdw(CnnPwDwArgs a) {
       if (p < n) *reinterpret_cast<cnn_u32x4*>(al + (size_t)(p / C8in) * AS + (p % C8in) * 8) = pre[q];
     }
   };
-  // this wave's channel tiles (wave, wave + 4; Cout <= 256): weights as bf16 A
-  // operands and the biases of the accumulator rows, loaded once
-  cnn_u32x4 awt[2][8];
-  float biast[2][16];
+  // this wave's NT channel tiles (wave, wave + 4; Cout = 128 NT): weights as
+  // bf16 A operands and the biases of the accumulator rows, loaded once
+  cnn_u32x4 awt[NT][8];
+  float biast[NT][16];
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
+  for (int u = 0; u < NT; ++u) {
     const int n0 = min(wave + 4 * u, Cout / 32 - 1) * 32;
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
@@ -367,9 +406,8 @@ __global__ __launch_bounds__(256) void k_cnn_pwdw(CnnPwDwArgs a) {
     strip_rows(yo0, rv0, rv1);
     const int M = (rv1 - rv0) * W, mt = (M + 31) / 32;
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < NT; ++u) {
       const int nt = wave + 4 * u;
-      if (nt >= Cout / 32) break;
       const int n0 = nt * 32;
       const cnn_u32x4* aw = awt[u];
       const float* bias = biast[u];
@@ -399,26 +437,20 @@ __global__ __launch_bounds__(256) void k_cnn_pwdw(CnnPwDwArgs a) {
     const int R = min(a.R, a.Ho - yo0), C8 = Cout / 8, items = R * a.Wo * C8;
     for (int it = threadIdx.x; it < items; it += blockDim.x) {
       const int c0 = (it % C8) * 8, xo = (it / C8) % a.Wo, yo = yo0 + it / (C8 * a.Wo);
+      auto tap = [&](int t) {
+        const int r = S * yo + t / 3 - 1, xx = S * xo + t % 3 - 1;
+        const bool in = r >= 0 && r < H && xx >= 0 && xx < W;
+        return in ? *reinterpret_cast<const uint4*>(pl + ((size_t)(r - rbase) * W + xx) * PS + c0)
+                  : make_uint4(0, 0, 0, 0);
+      };
       float acc[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) acc[j] = 0.0f;
-#pragma unroll
-      for (int dy = 0; dy < 3; ++dy)
-#pragma unroll
-        for (int dx = 0; dx < 3; ++dx) {
-          const int r = S * yo + dy - 1, xx = S * xo + dx - 1;
-          if (r < 0 || r >= H || xx < 0 || xx >= W) continue;
-          const uint4 q = *reinterpret_cast<const uint4*>(pl + ((size_t)(r - rbase) * W + xx) * PS + c0);
-          const uint32_t w4[4] = {q.x, q.y, q.z, q.w};
-          const float* tw = dt + (3 * dy + dx) * Cout + c0;
-#pragma unroll
-          for (int j = 0; j < 8; ++j)
-            acc[j] = __fmaf_rn(bf16_bits_to_f32((uint16_t)(w4[j >> 1] >> (16 * (j & 1)))), tw[j], acc[j]);
-        }
+      cnn_dw_dot(tap, dt + c0, Cout, acc);
       float f[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const float z = acc[j] + dt[9 * Cout + c0 + j];
+        const float z = acc[j] + dbias[c0 + j];
         f[j] = z > 0.0f ? z : 0.0f;
       }
       uint32_t pk[4];
@@ -465,18 +497,18 @@ size_t cnn_stem_lds(int H, int W, int C) { return ((size_t)(H + 2) * (W + 2) * C
 
 // LDS bytes of the fused pointwise + depthwise kernel for strips of R output
 // rows: the pointwise inputs (S (R - 1) + 3 rows of W pixels x (Cin + 8) bf16),
-// the pointwise outputs (the same rows x (Cout + 8) bf16), the depthwise taps and
-// biases (fp32)
+// the pointwise outputs (the same rows x (Cout + 8) bf16), the depthwise tap
+// pairs and biases
 size_t cnn_pwdw_lds(int S, int R, int W, int Cin, int Cout) {
   const size_t px = (size_t)(S * (R - 1) + 3) * W;
-  return ((px * (Cin + 8) + 7) & ~(size_t)7) * 2 + ((px * (Cout + 8) + 7) & ~(size_t)7) * 2 + (size_t)10 * Cout * 4;
+  return ((px * (Cin + 8) + 7) & ~(size_t)7) * 2 + ((px * (Cout + 8) + 7) & ~(size_t)7) * 2 + (size_t)6 * Cout * 4;
 }
 
 // Strip rows of the fused kernel for pointwise Cin -> Cout on H x W followed
 // by a depthwise stride S to Ho rows: the most rows whose LDS fits 64 KiB and
 // whose inputs fit the staging registers, or 0 when the pair runs unfused.
 int cnn_fuse_rows(int Cin, int Cout, int W, int S, int Ho) {
-  if (Cin % 32 || Cin > 128 || Cout % 32 || Cout > 256) return 0;
+  if (Cin % 32 || Cin > 128 || (Cout != 128 && Cout != 256)) return 0;
   int R = 0;
   for (int r = 1; r <= Ho; ++r) {
     const size_t pieces = (size_t)(S * (r - 1) + 3) * W * Cin / 8;
@@ -498,8 +530,8 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 struct CnnTensor {
   int K = 0, N = 0, Kp = 0, Np = 0;
   size_t Wm = 0, bias = 0, mask = 0, base_w = 0, base_b = 0;
-  size_t pack = 0;                            // prediction copy [P][K][N] (stem and depthwise tensors)
-  bool packed = false;
+  size_t pack = 0;                            // prediction copy: [P][K][N] fp32 (stem), [P][5][N] tap pairs (depthwise)
+  bool packed = false, pairs = false;
 };
 
 struct CnnLayout {
@@ -546,6 +578,7 @@ gevo_status cnn_layout(const gevo_cnn_config* c, int64_t n_test, CnnLayout& y) {
     if (((size_t)kCnnChunk * h * w) % 256) return GEVO_E_UNSUPPORTED;   // pointwise GEMM rows
     add(9, ch, ch);                                   // depthwise taps of each channel
     y.t[y.nt - 1].packed = true;
+    y.t[y.nt - 1].pairs = true;
     add(ch, co, co);                                  // pointwise
     act = std::max(act, (size_t)kCnnChunk * h * w * std::max(ch, co));
     ch = co;
@@ -571,7 +604,7 @@ gevo_status cnn_layout(const gevo_cnn_config* c, int64_t n_test, CnnLayout& y) {
     t.mask = take(P * t.Np * (t.Kp / 32) * 4);
     t.base_w = take((size_t)t.Np * t.Kp * 4);
     t.base_b = take((size_t)t.Np * 4);
-    if (t.packed) t.pack = take(P * t.K * t.N * 4);
+    if (t.packed) t.pack = take(P * (t.pairs ? 5 : t.K) * t.N * 4);
   }
   y.thresh = take(P * 4);
   y.aux = take(P * 4);                                // learning rates and bias bits the output kernel reads
@@ -780,7 +813,12 @@ gevo_status gevo_cnn_init(const gevo_cnn_config* cfg, void* d_ws, size_t ws_byte
     a.bias = at<float>(ws, t.bias);
     a.mask = at<uint32_t>(ws, t.mask);
     if (launch_init(a, h->stream, LaunchEv{}) != hipSuccess) return fail(GEVO_E_HIP);
-    if (t.packed) {
+    if (t.packed && t.pairs) {
+      const int64_t n = (int64_t)P * 5 * t.N;
+      hipLaunchKernelGGL(k_cnn_pack_pairs, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, h->stream,
+                         at<const float>(ws, t.Wm), t.N, P, at<uint32_t>(ws, t.pack));
+      if (hipGetLastError() != hipSuccess) return fail(GEVO_E_HIP);
+    } else if (t.packed) {
       const int64_t n = (int64_t)P * t.K * t.N;
       hipLaunchKernelGGL(k_cnn_pack, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, h->stream,
                          at<const float>(ws, t.Wm), t.Kp, t.Np, t.K, t.N, P, at<float>(ws, t.pack));
@@ -835,14 +873,14 @@ gevo_status gevo_cnn_predict(gevo_cnn* h) {
       da.in = cur; da.in_vs = y.act_vs;
       da.out = other; da.out_vs = y.act_vs;
       da.H = y.hin[i]; da.W = y.win[i]; da.C = C; da.Ho = y.hin[i + 1]; da.Wo = y.win[i + 1]; da.stride = y.stride[i];
-      da.wp = at<const float>(ws, td.pack); da.bias = at<const float>(ws, td.bias);
+      da.wp = at<const uint32_t>(ws, td.pack); da.bias = at<const float>(ws, td.bias);
       const int dw_threads = kCnnChunk * da.Wo * (C / 8);        // (image, column, 8 channels)
       const LaunchEv e = cnn_prof(h, GEVO_CNN_KERNEL_DEPTHWISE);
       const dim3 dg((dw_threads + 255) / 256, P);
       if (da.stride == 1)
-        hipExtLaunchKernelGGL(k_cnn_dw<1>, dg, dim3(256), (size_t)10 * C * 4, s, e.start, e.stop, 0, da);
+        hipExtLaunchKernelGGL(k_cnn_dw<1>, dg, dim3(256), (size_t)6 * C * 4, s, e.start, e.stop, 0, da);
       else
-        hipExtLaunchKernelGGL(k_cnn_dw<2>, dg, dim3(256), (size_t)10 * C * 4, s, e.start, e.stop, 0, da);
+        hipExtLaunchKernelGGL(k_cnn_dw<2>, dg, dim3(256), (size_t)6 * C * 4, s, e.start, e.stop, 0, da);
       std::swap(cur, other);
       return hipGetLastError();
     };
@@ -857,7 +895,7 @@ gevo_status gevo_cnn_predict(gevo_cnn* h) {
         CnnPwDwArgs fa{};
         fa.in = cur; fa.in_vs = y.act_vs;
         fa.Wm = at<const float>(ws, tp.Wm); fa.pbias = at<const float>(ws, tp.bias);
-        fa.dwp = at<const float>(ws, td.pack); fa.dbias = at<const float>(ws, td.bias);
+        fa.dwp = at<const uint32_t>(ws, td.pack); fa.dbias = at<const float>(ws, td.bias);
         fa.out = other; fa.out_vs = y.act_vs;
         fa.H = Hp; fa.W = Wp; fa.Cin = ch; fa.Cout = y.ch[i];
         fa.Ho = y.hin[i + 2]; fa.Wo = y.win[i + 2]; fa.R = y.fuse_R[i];
@@ -865,10 +903,15 @@ gevo_status gevo_cnn_predict(gevo_cnn* h) {
         const int S = y.stride[i + 1];
         const size_t lds = cnn_pwdw_lds(S, fa.R, fa.W, fa.Cin, fa.Cout);
         const LaunchEv e = cnn_prof(h, GEVO_CNN_KERNEL_POINTWISE_DEPTHWISE);
-        if (S == 1)
-          hipExtLaunchKernelGGL(k_cnn_pwdw<1>, dim3(kCnnChunk / fa.ipw, P), dim3(256), lds, s, e.start, e.stop, 0, fa);
+        const dim3 fg(kCnnChunk / fa.ipw, P);
+        if (S == 1 && fa.Cout == 128)
+          hipExtLaunchKernelGGL((k_cnn_pwdw<1, 1>), fg, dim3(256), lds, s, e.start, e.stop, 0, fa);
+        else if (S == 1)
+          hipExtLaunchKernelGGL((k_cnn_pwdw<1, 2>), fg, dim3(256), lds, s, e.start, e.stop, 0, fa);
+        else if (fa.Cout == 128)
+          hipExtLaunchKernelGGL((k_cnn_pwdw<2, 1>), fg, dim3(256), lds, s, e.start, e.stop, 0, fa);
         else
-          hipExtLaunchKernelGGL(k_cnn_pwdw<2>, dim3(kCnnChunk / fa.ipw, P), dim3(256), lds, s, e.start, e.stop, 0, fa);
+          hipExtLaunchKernelGGL((k_cnn_pwdw<2, 2>), fg, dim3(256), lds, s, e.start, e.stop, 0, fa);
         CNN_HIP(hipGetLastError());
         std::swap(cur, other);                                     // cur: depthwise i + 1 output
         ch = y.ch[i];
