@@ -53,6 +53,7 @@ struct CnnPwDwArgs {
   uint16_t* out; size_t out_vs;               // depthwise output [v][chunk][Ho][Wo][Cout]
   int H, W, Cin, Cout, Ho, Wo, R;             // R: depthwise output rows per strip
   int ipw;                                    // images per workgroup (divides the chunk)
+  uint32_t wo_magic, c8in_magic;              // ceil(2^32 / Wo), ceil(2^32 / (Cin / 8)): exact quotients below 2^16
 };
 
 struct CnnPoolArgs {
@@ -307,8 +308,9 @@ __global__ __launch_bounds__(256) void k_cnn_dw(CnnDwArgs a) {
 // input rows (those inside the image):
 //   1. their pointwise inputs are staged in LDS (rows of the image are
 //      contiguous, so these are whole 16-byte pieces of one contiguous span;
-//      the next strip's pieces are loaded into registers while the current
-//      strip is computed);
+//      the next strip's pieces are loaded into registers during the current
+//      strip's pointwise phase and stored to LDS before its depthwise phase,
+//      whose global stores would otherwise join the wait);
 //   2. the pointwise outputs go to LDS as bf16 from 32x32x16 bf16 MFMAs with
 //      fp32 accumulation: per 32-pixel x 32-channel tile out^T[n][p] =
 //      sum_k W[k][n] A[p][k]; lane l gives channel / pixel l % 32 and k slots
@@ -323,7 +325,7 @@ __global__ __launch_bounds__(256) void k_cnn_dw(CnnDwArgs a) {
 constexpr int kPwDwPieces = 8;
 
 template <int S, int NT>
-__global__ __launch_bounds__(256) void k_cnn_pwdw(CnnPwDwArgs a) {
+__global__ __launch_bounds__(256, NT == 1 ? 2 : 1) void k_cnn_pwdw(CnnPwDwArgs a) {
   extern __shared__ __align__(16) char smem[];
   int v, w;
   cnn_slot(v, w);
@@ -367,7 +369,10 @@ __global__ __launch_bounds__(256) void k_cnn_pwdw(CnnPwDwArgs a) {
 #pragma unroll
     for (int q = 0; q < kPwDwPieces; ++q) {
       const int p = threadIdx.x + 256 * q;
-      if (p < n) *reinterpret_cast<cnn_u32x4*>(al + (size_t)(p / C8in) * AS + (p % C8in) * 8) = pre[q];
+      if (p < n) {
+        const int px = (int)__umulhi((uint32_t)p, a.c8in_magic);   // p / C8in
+        *reinterpret_cast<cnn_u32x4*>(al + (size_t)px * AS + (p - px * C8in) * 8) = pre[q];
+      }
     }
   };
   // this wave's NT channel tiles (wave, wave + 4; Cout = 128 NT): weights as
@@ -434,9 +439,15 @@ __global__ __launch_bounds__(256) void k_cnn_pwdw(CnnPwDwArgs a) {
       }
     }
     __syncthreads();                                         // pointwise strip complete; its inputs are free
-    const int R = min(a.R, a.Ho - yo0), C8 = Cout / 8, items = R * a.Wo * C8;
-    for (int it = threadIdx.x; it < items; it += blockDim.x) {
-      const int c0 = (it % C8) * 8, xo = (it / C8) % a.Wo, yo = yo0 + it / (C8 * a.Wo);
+    if (more) commit(j + 1);                                 // before this strip's stores join the wait
+    // depthwise items (output pixel, 8 channels): a thread keeps its channels
+    // (256 is a multiple of Cout / 8) and steps through the strip's pixels
+    constexpr int C8 = 16 * NT;
+    const int R = min(a.R, a.Ho - yo0), npix = R * a.Wo;
+    const int c0 = (threadIdx.x % C8) * 8;
+    for (int pix = threadIdx.x / C8; pix < npix; pix += 256 / C8) {
+      const int yr = (int)__umulhi((uint32_t)pix, a.wo_magic);     // pix / Wo
+      const int xo = pix - yr * a.Wo, yo = yo0 + yr;
       auto tap = [&](int t) {
         const int r = S * yo + t / 3 - 1, xx = S * xo + t % 3 - 1;
         const bool in = r >= 0 && r < H && xx >= 0 && xx < W;
@@ -457,7 +468,6 @@ __global__ __launch_bounds__(256) void k_cnn_pwdw(CnnPwDwArgs a) {
       to_bf16x2(f, pk);
       *reinterpret_cast<uint4*>(ov + ((size_t)yo * a.Wo + xo) * Cout + c0) = make_uint4(pk[0], pk[1], pk[2], pk[3]);
     }
-    if (more) commit(j + 1);
     __syncthreads();                                         // next inputs staged; this strip's outputs read
   }
 }
@@ -491,6 +501,9 @@ __global__ __launch_bounds__(256) void k_cnn_pool(CnnPoolArgs a) {
 namespace {
 
 int round_up32(int x) { return (x + 31) / 32 * 32; }
+
+// ceil(2^32 / d): for n, d < 2^16, (n * m) >> 32 is exactly n / d
+uint32_t cnn_magic(int d) { return (uint32_t)((((uint64_t)1 << 32) + (uint64_t)d - 1) / (uint64_t)d); }
 
 // LDS bytes of the stem's zero-padded bf16 image
 size_t cnn_stem_lds(int H, int W, int C) { return ((size_t)(H + 2) * (W + 2) * C * 2 + 15) / 16 * 16; }
@@ -900,6 +913,8 @@ gevo_status gevo_cnn_predict(gevo_cnn* h) {
         fa.H = Hp; fa.W = Wp; fa.Cin = ch; fa.Cout = y.ch[i];
         fa.Ho = y.hin[i + 2]; fa.Wo = y.win[i + 2]; fa.R = y.fuse_R[i];
         fa.ipw = Hp * Wp >= 1024 ? 1 : (Hp * Wp >= 256 ? 4 : 8);   // images per workgroup
+        fa.wo_magic = cnn_magic(fa.Wo);
+        fa.c8in_magic = cnn_magic(fa.Cin / 8);
         const int S = y.stride[i + 1];
         const size_t lds = cnn_pwdw_lds(S, fa.R, fa.W, fa.Cin, fa.Cout);
         const LaunchEv e = cnn_prof(h, GEVO_CNN_KERNEL_POINTWISE_DEPTHWISE);
