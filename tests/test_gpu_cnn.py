@@ -65,6 +65,8 @@ SMALL_SHAPES = [
     # a 256-channel pointwise input: that pair runs unfused, the first pair fused in two strips
     dict(name="p2-dwsep-cnn8x8x3-32-256-128-128-10", P=2, blocks=[(1, 256), (1, 128), (2, 128)], n_test=100,
          seed=36),
+    # a stem map too large to stay in LDS: the stem and the first depthwise layer run unfused
+    dict(name="p2-dwsep-cnn32x32x3-64-128-10", P=2, H=32, W=32, stem=64, blocks=[(2, 128)], n_test=70, seed=37),
 ]
 
 
