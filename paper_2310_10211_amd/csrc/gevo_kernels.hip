@@ -567,13 +567,27 @@ __global__ __launch_bounds__(64 * kOutWaves) void k_out(OutArgs<S> a) {
       const typename O::Frag bf = O::load(&gs[(bt * 32 + l32) * GSTR + ks * KM + lh * KE]);
       acc = O::mma(af, bf, acc);
     }
+    const int b = bt * 32 + l32;
+    S g[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int k = kt * 32 + crow(r, lane);
-      const int b = bt * 32 + l32;
-      const S g = O::from_f32(av[r] > 0.0f ? acc[r] : 0.0f);
-      a.Gcols[v * a.gc_vs + (size_t)k * a.Bp + b] = g;
-      if (a.Grows) a.Grows[v * a.gr_vs + (size_t)b * Kp + k] = g;
+      g[r] = O::from_f32(av[r] > 0.0f ? acc[r] : 0.0f);
+      a.Gcols[v * a.gc_vs + (size_t)(kt * 32 + crow(r, lane)) * a.Bp + b] = g[r];
+    }
+    if (a.Grows) {
+      // rows [b][k]: accumulator rows 4q..4q+3 are the consecutive inputs
+      // kt 32 + 8q + 4 (l / 32) + 0..3, one 4-element store each
+      S* gr = a.Grows + v * a.gr_vs + (size_t)b * Kp + kt * 32 + 4 * lh;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if constexpr (sizeof(S) == 2) {
+          const uint32_t lo = (uint32_t)g[4 * q] | (uint32_t)g[4 * q + 1] << 16;
+          const uint32_t hi = (uint32_t)g[4 * q + 2] | (uint32_t)g[4 * q + 3] << 16;
+          *reinterpret_cast<uint2*>(gr + 8 * q) = make_uint2(lo, hi);
+        } else {
+          *reinterpret_cast<float4*>(gr + 8 * q) = make_float4(g[4 * q], g[4 * q + 1], g[4 * q + 2], g[4 * q + 3]);
+        }
+      }
     }
   }
 }
