@@ -29,7 +29,6 @@ namespace gevo {
 namespace {
 
 constexpr int kCnnChunk = 64;            // images per prediction chunk
-constexpr int kCnnRows = kOutRows;       // pooled rows per chunk handed to the output kernel (padded)
 
 struct CnnStemArgs {
   const float* x; int64_t n_test; int img0;   // test images [n][H][W][C] fp32, first image of the chunk
@@ -59,7 +58,7 @@ struct CnnPwDwArgs {
 struct CnnPoolArgs {
   const uint16_t* in; size_t in_vs;           // [v][chunk][HW][C]
   int HW, C;
-  uint16_t* out; size_t out_vs;               // [v][kCnnRows][C]; rows past the chunk are zero
+  uint16_t* out; size_t out_vs;               // [v][chunk][C]
 };
 
 __device__ __forceinline__ float bf16r(float f) { return bf16_bits_to_f32(f32_to_bf16_bits(f)); }
@@ -476,23 +475,21 @@ __global__ __launch_bounds__(256, NT == 1 ? 2 : 1) void k_cnn_pwdw(CnnPwDwArgs a
 __global__ __launch_bounds__(256) void k_cnn_pool(CnnPoolArgs a) {
   const int v = blockIdx.y, C8 = a.C / 8;
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= kCnnRows * C8) return;
+  if (i >= kCnnChunk * C8) return;
   const int row = i / C8, c0 = (i % C8) * 8;
   float f[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) f[j] = 0.0f;
-  if (row < kCnnChunk) {
-    const uint16_t* src = a.in + a.in_vs * v + (size_t)row * a.HW * a.C + c0;
-    for (int p = 0; p < a.HW; ++p) {
-      const uint4 q = *reinterpret_cast<const uint4*>(src + (size_t)p * a.C);
-      const uint32_t w4[4] = {q.x, q.y, q.z, q.w};
+  const uint16_t* src = a.in + a.in_vs * v + (size_t)row * a.HW * a.C + c0;
+  for (int p = 0; p < a.HW; ++p) {
+    const uint4 q = *reinterpret_cast<const uint4*>(src + (size_t)p * a.C);
+    const uint32_t w4[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
-      for (int j = 0; j < 8; ++j) f[j] += bf16_bits_to_f32((uint16_t)(w4[j >> 1] >> (16 * (j & 1))));
-    }
-    const float inv = 1.0f / (float)a.HW;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) f[j] *= inv;
+    for (int j = 0; j < 8; ++j) f[j] += bf16_bits_to_f32((uint16_t)(w4[j >> 1] >> (16 * (j & 1))));
   }
+  const float inv = 1.0f / (float)a.HW;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) f[j] *= inv;
   uint32_t pk[4];
   to_bf16x2(f, pk);
   *reinterpret_cast<uint4*>(a.out + a.out_vs * v + (size_t)row * a.C + c0) = make_uint4(pk[0], pk[1], pk[2], pk[3]);
@@ -623,8 +620,8 @@ gevo_status cnn_layout(const gevo_cnn_config* c, int64_t n_test, CnnLayout& y) {
   y.aux = take(P * 4);                                // learning rates and bias bits the output kernel reads
   y.actA = take(P * y.act_vs * 2);
   y.actB = take(P * y.act_vs * 2);
-  y.pooled = take(P * kCnnRows * ch * 2);
-  y.labels = take((size_t)y.n_chunks * kCnnRows * 4);
+  y.pooled = take(P * kCnnChunk * ch * 2);
+  y.labels = take((size_t)y.n_chunks * kCnnChunk * 4);
   y.part_ce = take(P * y.n_chunks * 8);
   y.part_corr = take(P * y.n_chunks * 4);
   y.test_ce = take(P * 8);
@@ -838,12 +835,12 @@ gevo_status gevo_cnn_init(const gevo_cnn_config* cfg, void* d_ws, size_t ws_byte
       if (hipGetLastError() != hipSuccess) return fail(GEVO_E_HIP);
     }
   }
-  // test labels in 256-row tiles per chunk, padding rows marked -1
-  std::vector<int32_t> ylab((size_t)n_test), tiles((size_t)y.n_chunks * kCnnRows, -1);
+  // test labels per 64-image chunk, the last chunk's padding images marked -1
+  std::vector<int32_t> ylab((size_t)n_test), tiles((size_t)y.n_chunks * kCnnChunk, -1);
   if (hipMemcpy(ylab.data(), d_test_y, (size_t)n_test * 4, hipMemcpyDeviceToHost) != hipSuccess) return fail(GEVO_E_HIP);
   for (int64_t r = 0; r < n_test; ++r) {
     if (ylab[r] < 0 || ylab[r] >= y.classes) return fail(GEVO_E_SHAPE);
-    tiles[(size_t)(r / kCnnChunk) * kCnnRows + r % kCnnChunk] = ylab[r];
+    tiles[(size_t)r] = ylab[r];
   }
   if (hipMemcpy(ws + y.labels, tiles.data(), tiles.size() * 4, hipMemcpyHostToDevice) != hipSuccess)
     return fail(GEVO_E_HIP);
@@ -946,20 +943,20 @@ gevo_status gevo_cnn_predict(gevo_cnn* h) {
     CnnPoolArgs pa{};
     pa.in = cur; pa.in_vs = y.act_vs;
     pa.HW = y.hin[y.nb] * y.win[y.nb]; pa.C = ch;
-    pa.out = at<uint16_t>(ws, y.pooled); pa.out_vs = (size_t)kCnnRows * ch;
+    pa.out = at<uint16_t>(ws, y.pooled); pa.out_vs = (size_t)kCnnChunk * ch;
     ev = cnn_prof(h, GEVO_CNN_KERNEL_POOL);
-    hipExtLaunchKernelGGL(k_cnn_pool, dim3((kCnnRows * (ch / 8) + 255) / 256, P), dim3(256), 0, s, ev.start, ev.stop,
+    hipExtLaunchKernelGGL(k_cnn_pool, dim3((kCnnChunk * (ch / 8) + 255) / 256, P), dim3(256), 0, s, ev.start, ev.stop,
                           0, pa);
     CNN_HIP(hipGetLastError());
     const CnnTensor& tf = y.t[y.nt - 1];
     OutArgs<uint16_t> o{};
-    o.Kp = tf.Kp; o.C = y.classes; o.Bp = kCnnRows;
+    o.Kp = tf.Kp; o.C = y.classes; o.Bp = kOutRows;
     o.Wm = at<float>(ws, tf.Wm); o.bias = at<float>(ws, tf.bias); o.mask = at<const uint32_t>(ws, tf.mask);
     o.bmask = at<const uint32_t>(ws, y.aux); o.lr = at<const float>(ws, y.aux);
     o.train = 0;
-    o.Arows = at<const uint16_t>(ws, y.pooled); o.ar_vs = (size_t)kCnnRows * ch;
-    o.labels = at<const int32_t>(ws, y.labels) + (size_t)c * kCnnRows;
-    o.rows = kCnnRows;
+    o.Arows = at<const uint16_t>(ws, y.pooled); o.ar_vs = (size_t)kCnnChunk * ch;
+    o.labels = at<const int32_t>(ws, y.labels) + (size_t)c * kCnnChunk;
+    o.rows = kCnnChunk;                                          // padding images of the last chunk carry label -1
     o.chunk0 = c;
     o.n_chunks_total = y.n_chunks;
     o.part_ce = at<double>(ws, y.part_ce);
