@@ -9,6 +9,8 @@
 //   block  3x3 depthwise convolution, stride 1|2, bias, ReLU      (k_cnn_dw)
 //          1x1 pointwise convolution = a per-variant GEMM over the
 //          chunk's pixels, bias, ReLU                             (k_fwd_gemm)
+//          (a pointwise layer and the next block's depthwise layer
+//          run as one kernel when its map fits LDS strips)        (k_cnn_pwdw)
 //   head   global average pooling                                 (k_cnn_pool)
 //          fully connected layer, softmax cross-entropy, argmax   (k_out)
 // bf16 operands and activations, fp32 accumulation, fp32 master weights.
@@ -94,8 +96,9 @@ __device__ __forceinline__ f32x16_t cnn_mma(cnn_u32x4 a, cnn_u32x4 b, f32x16_t c
 }
 
 // Depthwise taps of the prediction copy as bf16 pairs: out[v][p][c] holds taps
-// 2p (low half) and 2p + 1 (high half) of channel c, tap 9 being zero, read
-// from the k-blocked master [v][1][C][32] (taps k < 9 of channel c).
+// 2p (low half) and 2p + 1 (high half) of channel c, the high half of pair 4
+// being zero, read from the k-blocked master [v][1][C][32] (taps k < 9 of
+// channel c).
 __global__ __launch_bounds__(256) void k_cnn_pack_pairs(const float* __restrict__ Wm, int C, int P,
                                                         uint32_t* __restrict__ out) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -116,10 +119,10 @@ __device__ __forceinline__ float cnn_dot2(uint32_t a, uint32_t b, float c) {
 
 // One depthwise output for 8 channels: acc[j] += sum_t in[t][j] w[t][j] over
 // the 9 taps (in[t]: 8 bf16 channels of tap t = 3 dy + dx, zero outside the
-// image).  Taps
-// go in pairs (2p, 2p + 1) through the bf16 dot2 instruction (two products
-// summed into the fp32 accumulator), the inputs re-paired by channel.
-// tap(t) gives in[t]; wp: tap pairs [5][C] at this thread's first channel.
+// image).  Taps go in pairs (2p, 2p + 1) through the bf16 dot2 instruction
+// (two products summed into the fp32 accumulator), the inputs re-paired by
+// channel.  tap(t) gives in[t]; wp: tap pairs [5][C] at this thread's first
+// channel.
 template <typename Tap>
 __device__ __forceinline__ void cnn_dw_dot(Tap tap, const uint32_t* wp, int C, float (&acc)[8]) {
 #pragma unroll
@@ -782,7 +785,7 @@ gevo_status gevo_cnn_init(const gevo_cnn_config* cfg, void* d_ws, size_t ws_byte
   const int P = y.P;
   // per-variant density and mask threshold (host, fp64), drawn as for the
   // fully connected populations (stream kStreamDens)
-  std::vector<uint32_t> thresh(P), ones(P, 0xffffffffu);
+  std::vector<uint32_t> thresh(P);
   std::vector<float> zeros(P, 0.0f);
   h->dens.resize(P);
   for (int v = 0; v < P; ++v) {
