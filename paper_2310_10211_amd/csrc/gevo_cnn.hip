@@ -135,8 +135,10 @@ __device__ __forceinline__ void cnn_dw_dot(Tap tap, const uint32_t* wp, int C, f
     const uint32_t a0[4] = {q0.x, q0.y, q0.z, q0.w}, a1[4] = {q1.x, q1.y, q1.z, q1.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {                       // channels 2i, 2i + 1
-      const uint32_t lo = (a0[i] & 0xffffu) | (a1[i] << 16);
-      const uint32_t hi = (a0[i] >> 16) | (a1[i] & 0xffff0000u);
+      // byte permutes of {a1 (bytes 4-7), a0 (bytes 0-3)}: lo = channel 2i of
+      // taps 2p, 2p + 1; hi = channel 2i + 1 of both
+      const uint32_t lo = __builtin_amdgcn_perm(a1[i], a0[i], 0x05040100u);
+      const uint32_t hi = __builtin_amdgcn_perm(a1[i], a0[i], 0x07060302u);
       acc[2 * i] = cnn_dot2(lo, w[2 * i], acc[2 * i]);
       acc[2 * i + 1] = cnn_dot2(hi, w[2 * i + 1], acc[2 * i + 1]);
     }
