@@ -174,3 +174,37 @@ def test_labels_outside_the_classes_are_rejected():
     import paper_2310_10211_amd as g
     with pytest.raises(g.GevoError, match="shape"):
         _pop(cfg, base, x, y)
+
+
+@pytest.mark.parametrize("over", [dict(), SMALL_SHAPES[3], SMALL_SHAPES[4], SMALL_SHAPES[5]])
+def test_launch_plan_matches_the_benchmark_cost_model(over):
+    """The benchmark's roofline prices each kernel kind from its own copy of
+    the library's fusion rules; the kinds and launch counts the library
+    reports must be the ones it prices."""
+    import bench
+    cfg = synthetic.cnn_config("full", **over) if not over else synthetic.cnn_config("small", **over)
+    base, x, y = synthetic.cnn_inputs(cfg, n_test=min(cfg["n_test"], 200))
+    pop = _pop(cfg, base, x, y)
+    pop.set_profiling(True)
+    pop.predict()
+    st = pop.kernel_stats()
+    costs = bench.cnn_costs(cfg, len(y))
+    chunks = (len(y) + 63) // 64
+    nb = len(cfg["blocks"])
+    fused = sum(1 for i in range(nb - 1) if bench.cnn_fuse_rows(
+        ([cfg["stem"]] + [c for _, c in cfg["blocks"]])[i], cfg["blocks"][i][1],
+        _sizes(cfg)[i + 1][1], cfg["blocks"][i + 1][0], _sizes(cfg)[i + 2][0]))
+    assert {k for k, (_, n) in st.items() if n and k != "reduce"} == set(costs)
+    assert st["pw_dw"][1] == chunks * fused
+    assert st["pointwise"][1] == chunks * (nb - fused)
+    assert st["depthwise"][1] == chunks * (nb - fused)
+    assert st["stem"][1] == st["pool"][1] == st["head"][1] == chunks
+    pop.close()
+
+
+def _sizes(cfg):
+    out = [(cfg["H"], cfg["W"])]
+    for s, _ in cfg["blocks"]:
+        h, w = out[-1]
+        out.append(((h - 1) // s + 1, (w - 1) // s + 1))
+    return out
