@@ -36,6 +36,7 @@ struct CnnStemArgs {
   const float* x; int64_t n_test; int img0;   // test images [n][H][W][C] fp32, first image of the chunk
   int H, W;
   int Np;                                     // output channels
+  uint32_t w_magic, w2_magic;                 // ceil(2^32 / W), ceil(2^32 / (W + 2)): exact quotients below 2^16
   const float* wp; const float* bias;         // bf16-valued taps [P][9C][Np] (fp32 storage), biases [P][Np]
   uint16_t* out; size_t out_vs;               // [v][chunk][H][W][Np] bf16
 };
@@ -165,7 +166,8 @@ __global__ __launch_bounds__(256) void k_cnn_stem(CnnStemArgs a) {
   const int64_t g = (int64_t)a.img0 + img;
   const bool valid = g < a.n_test;
   for (int i = threadIdx.x; i < (H + 2) * W2 * C; i += blockDim.x) {
-    const int c = i % C, pix = i / C, yy = pix / W2 - 1, xx = pix % W2 - 1;
+    const int c = i % C, pix = i / C, py = (int)__umulhi((uint32_t)pix, a.w2_magic);
+    const int yy = py - 1, xx = pix - py * W2 - 1;
     const bool in = valid && yy >= 0 && yy < H && xx >= 0 && xx < W;
     const int64_t at = in ? ((g * H + yy) * W + xx) * C + c : 0;   // in-bounds even when unused
     im[i] = in ? f32_to_bf16_bits(a.x[at]) : (uint16_t)0;
@@ -205,7 +207,8 @@ __global__ __launch_bounds__(256) void k_cnn_stem(CnnStemArgs a) {
     for (int r = 0; r < 16; ++r) bias[r] = bv[n0 + crow(r, lane)];
     for (int t = wave; t < ntiles; t += 4) {
       const int p = min(t * 32 + l32, HW - 1);           // pixels past the image: computed, never stored
-      const int base = ((p / W) * W2 + p % W) * C;
+      const int py = (int)__umulhi((uint32_t)p, a.w_magic);    // p / W
+      const int base = (py * W2 + (p - py * W)) * C;
       f32x16_t acc = zero16();
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
@@ -867,6 +870,7 @@ gevo_status gevo_cnn_predict(gevo_cnn* h) {
     CnnStemArgs sa{};
     sa.x = h->teX; sa.n_test = y.n_test; sa.img0 = c * kCnnChunk;
     sa.H = y.H; sa.W = y.W; sa.Np = ts.Np;
+    sa.w_magic = cnn_magic(y.W); sa.w2_magic = cnn_magic(y.W + 2);
     sa.wp = at<const float>(ws, ts.pack); sa.bias = at<const float>(ws, ts.bias);
     sa.out = at<uint16_t>(ws, y.actA); sa.out_vs = y.act_vs;
     LaunchEv ev = cnn_prof(h, GEVO_CNN_KERNEL_STEM);
