@@ -34,7 +34,9 @@ Parity status: conv3x3 pinned against scipy.signal.correlate2d and an
 identity filter; the stem against brute-force loops; pooling and the
 pointwise layer by their definitions; the whole forward against a
 brute-force per-pixel implementation on a tiny net; tensor_init against the
-chain initialisation of the fully connected nets.
+chain initialisation of the fully connected nets; removed layers (skip plus
+repair) against the same layers with identity weights (the centre tap, or
+the truncated identity matrix, and zero biases).
 """
 from __future__ import annotations
 
@@ -151,31 +153,58 @@ def conv3x3_full(a, w):
     return out
 
 
-def forward_logits(cfg, params, x, mode="bf16"):
-    """Logits [n][classes] of images x [n][H][W][C] (values as given, fp32)."""
+def removed_depthwise(a, stride):
+    """A removed depthwise layer (section 6.1 removes a convolution layer of
+    MobileNet): its output is its input, repaired to the shape the next layer
+    expects (section 4.1 shrinks or pads tensors) -- at stride s, the pixels
+    (s yo, s xo), the centres of the windows the layer would have read."""
+    return a[:, ::stride, ::stride, :]
+
+
+def removed_pointwise(a, c_out):
+    """A removed pointwise layer: its output is its input, repaired to c_out
+    channels -- the first c_out channels kept, or zero channels appended."""
+    n, H, Wd, C = a.shape
+    if C >= c_out:
+        return a[..., :c_out]
+    return np.concatenate([a, np.zeros((n, H, Wd, c_out - C), a.dtype)], axis=3)
+
+
+def forward_logits(cfg, params, x, mode="bf16", removed=()):
+    """Logits [n][classes] of images x [n][H][W][C] (values as given, fp32).
+    removed: names ("dw<i>", "pw<i>") of the block layers taken out of the
+    net (their parameters are then ignored)."""
     p = unpack(np.asarray(params, np.float64), cfg)
     a = _r(x.astype(np.float32), mode)
     W, b = p["stem"]
     a = _r(np.maximum(conv3x3_full(a, _r(W, mode)) + b, 0.0), mode)
     for i, (s, co) in enumerate(cfg["blocks"]):
-        W, b = p[f"dw{i}"]
-        a = _r(np.maximum(conv3x3_depthwise(a, _r(W, mode), s) + b, 0.0), mode)
-        W, b = p[f"pw{i}"]
-        a = _r(np.maximum(a @ _r(W, mode) + b, 0.0), mode)
+        if f"dw{i}" in removed:
+            a = removed_depthwise(a, s)
+        else:
+            W, b = p[f"dw{i}"]
+            a = _r(np.maximum(conv3x3_depthwise(a, _r(W, mode), s) + b, 0.0), mode)
+        if f"pw{i}" in removed:
+            a = removed_pointwise(a, co)
+        else:
+            W, b = p[f"pw{i}"]
+            a = _r(np.maximum(a @ _r(W, mode) + b, 0.0), mode)
     h = _r(a.mean(axis=(1, 2)), mode)
     W, b = p["fc"]
     return h @ _r(W, mode) + b
 
 
-def evaluate(cfg, base, x, y, variants, mode="bf16", chunk=256):
-    """{v: (test CE sum, correct count)} over images x [n][H][W][C], labels y."""
+def evaluate(cfg, base, x, y, variants, mode="bf16", chunk=256, removed=None):
+    """{v: (test CE sum, correct count)} over images x [n][H][W][C], labels y.
+    removed: optional {v: names of the block layers variant v has removed}."""
     out = {}
     for v in variants:
         th = thresholds(cfg, [v])[0]
         params, _ = variant_params(cfg, base, v, th)
+        gone = (removed or {}).get(v, ())
         ce, corr = 0.0, 0
         for c0 in range(0, len(y), chunk):
-            z = forward_logits(cfg, params, x[c0:c0 + chunk], mode)
+            z = forward_logits(cfg, params, x[c0:c0 + chunk], mode, gone)
             c, k = softmax_stats(z, y[c0:c0 + chunk])
             ce += c
             corr += k

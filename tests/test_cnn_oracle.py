@@ -160,3 +160,66 @@ def test_variant_params_apply_noise_and_mask_to_the_base():
         assert np.all(np.abs(W[M] / Wb[M] - 1.0) < 0.1)       # 1 + 0.01 eps
         assert np.array_equal(b, bb)                           # biases are not perturbed
     assert 0.35 < mask.mean() < 0.65
+
+
+# A removed block layer (section 6.1 takes a convolution layer out of MobileNet)
+# is the identity map plus the shape repair of section 4.1.  On non-negative
+# inputs (every block layer reads a ReLU output) that equals the same layer with
+# identity weights: the depthwise centre tap 1 (at stride 2 it reads exactly the
+# pixels (2 yo, 2 xo)), or the pointwise matrix with ones on its diagonal (zero
+# channels appended when it widens, the first channels kept when it narrows),
+# and zero biases.  These pins compare the skip code against those layers
+# computed by the convolution code pinned above.
+REMOVAL = dict(C=3, stem=4, blocks=[(1, 3), (2, 5), (2, 2)], classes=3, seed=12, dens=(1.0, 1.0),
+               noise_std=0.0)
+
+
+def _with_identity(cfg, params, name):
+    out = np.array(params, np.float64)
+    off = 0
+    for tname, K, N in cnn.tensors(cfg):
+        if tname == name:
+            W = np.zeros((K, N))
+            if name.startswith("dw"):
+                W[4, :] = 1.0                                     # centre tap (dy, dx) = (1, 1)
+            else:
+                for k in range(min(K, N)):
+                    W[k, k] = 1.0
+            out[off:off + K * N] = W.ravel()
+            out[off + K * N:off + K * N + N] = 0.0
+            return out
+        off += K * N + N
+    raise KeyError(name)
+
+
+@pytest.mark.parametrize("mode", ["f64", "bf16"])
+@pytest.mark.parametrize("gone", [("dw0",), ("dw1",), ("pw1",), ("pw2",), ("pw0",), ("dw1", "pw1", "dw2")])
+def test_removed_layers_equal_identity_layers(mode, gone):
+    rng = np.random.default_rng(21)
+    params = np.abs(rng.normal(0, 0.5, cnn.param_count(REMOVAL)))      # every unit stays active
+    x = rng.random((2, 5, 7, 3)).astype(np.float32)
+    ident = params
+    for name in gone:
+        ident = _with_identity(REMOVAL, ident, name)
+    got = cnn.forward_logits(REMOVAL, params, x, mode=mode, removed=gone)
+    want = cnn.forward_logits(REMOVAL, ident, x, mode=mode)
+    assert np.array_equal(got, want)
+    assert not np.array_equal(got, cnn.forward_logits(REMOVAL, params, x, mode=mode))
+
+
+def test_removed_layer_ignores_its_parameters_and_repairs_shapes():
+    rng = np.random.default_rng(22)
+    a = rng.random((1, 5, 7, 3))
+    d = cnn.removed_depthwise(a, 2)
+    assert d.shape == (1, 3, 4, 3) and np.array_equal(d[0, 1, 2], a[0, 2, 4])
+    assert d.shape[1:3] == cnn.conv3x3_depthwise(a, np.ones((9, 3)), 2).shape[1:3]
+    assert np.array_equal(cnn.removed_depthwise(a, 1), a)
+    wide = cnn.removed_pointwise(a, 5)
+    assert np.array_equal(wide[..., :3], a) and not np.any(wide[..., 3:])
+    assert np.array_equal(cnn.removed_pointwise(a, 2), a[..., :2])
+    params = np.abs(rng.normal(0, 0.5, cnn.param_count(REMOVAL)))
+    x = rng.random((1, 5, 7, 3)).astype(np.float32)
+    other = params + (_with_identity(REMOVAL, params, "pw1") != params) * 7.0   # pw1 changed, nothing else
+    assert not np.array_equal(other, params)
+    assert np.array_equal(cnn.forward_logits(REMOVAL, params, x, mode="f64", removed=("pw1",)),
+                          cnn.forward_logits(REMOVAL, other, x, mode="f64", removed=("pw1",)))
