@@ -423,6 +423,25 @@ gevo_status gevo_cnn_predict(gevo_cnn* h);
  * GEVO_E_ORDER before the first predict. */
 gevo_status gevo_cnn_scores(gevo_cnn* h, float* test_loss, float* test_acc, float* time_s);
 
+/* Structural edit: variant v loses block layer `layer` (its index in the
+ * canonical tensor order: 2 i + 1 the depthwise layer of block i, 2 i + 2
+ * its pointwise layer).  Section 6.1 removes a convolution layer of
+ * MobileNet; section 4.1 repairs the shapes that an edit breaks by
+ * shrinking or padding tensors.  The removed layer passes its input on,
+ * repaired to the shape the next layer reads: a depthwise layer of stride 2
+ * keeps the pixels (2 yo, 2 xo); a pointwise layer keeps its first
+ * block_channels[i] channels or appends zero channels.  The variant's
+ * master of that layer is overwritten by the layer's identity form (the
+ * depthwise centre tap 1, or ones on the pointwise diagonal; every other
+ * weight and every bias +0; the mask marks the ones), which computes
+ * exactly that on the layer's non-negative (ReLU) inputs, so later predict
+ * calls see the edit and gevo_cnn_export returns that form.  The edit
+ * cannot be undone short of a new gevo_cnn_init.  Asynchronous on the
+ * handle's stream; allocates nothing.  GEVO_E_ARG for v >= P or a layer
+ * past the head, GEVO_E_UNSUPPORTED for the stem (0) and the head
+ * (2 n_blocks + 1). */
+gevo_status gevo_cnn_remove_layer(gevo_cnn* h, uint32_t v, uint32_t layer);
+
 /* Variant v's parameters (canonical layout), mask (uint8 0/1 over the
  * weights, same order) and density rho_v; any output may be NULL. */
 gevo_status gevo_cnn_export(gevo_cnn* h, uint32_t v, float* params_out, uint8_t* mask_out, float* density_out);

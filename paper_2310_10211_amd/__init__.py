@@ -39,7 +39,7 @@ EXPORTED = [
     "gevo_check_bf16_rounding", "gevo_nsga2_rank", "gevo_nsga2_select", "gevo_genomes_initial",
     "gevo_genomes_breed", "gevo_pop_set_genomes", "gevo_pop_set_grad_scale",
     "gevo_cnn_param_count", "gevo_cnn_workspace_bytes", "gevo_cnn_init", "gevo_cnn_predict", "gevo_cnn_scores",
-    "gevo_cnn_export", "gevo_cnn_destroy", "gevo_cnn_set_profiling", "gevo_cnn_kernel_stats",
+    "gevo_cnn_export", "gevo_cnn_remove_layer", "gevo_cnn_destroy", "gevo_cnn_set_profiling", "gevo_cnn_kernel_stats",
 ]
 CNN_MAX_BLOCKS = 4
 CNN_KERNEL_KINDS = ["stem", "depthwise", "pointwise", "pool", "head", "reduce", "pw_dw"]
@@ -157,6 +157,7 @@ def lib():
         L.gevo_cnn_predict.argtypes = [vp]
         L.gevo_cnn_scores.argtypes = [vp, f32p, f32p, f32p]
         L.gevo_cnn_export.argtypes = [vp, u32, f32p, ctypes.POINTER(ctypes.c_uint8), f32p]
+        L.gevo_cnn_remove_layer.argtypes = [vp, u32, u32]
         L.gevo_cnn_set_profiling.argtypes = [vp, ctypes.c_int]
         L.gevo_cnn_kernel_stats.argtypes = [vp, ctypes.c_int, ctypes.POINTER(ctypes.c_double),
                                             ctypes.POINTER(ctypes.c_uint64)]
@@ -520,6 +521,14 @@ class CnnPopulation:
             _check(lib().gevo_cnn_kernel_stats(self._h, i, ctypes.byref(ms), ctypes.byref(n)), "gevo_cnn_kernel_stats")
             out[k] = (ms.value, n.value)
         return out
+
+    def remove_layer(self, v: int, layer):
+        """Variant v loses a block layer: its canonical tensor index, or its
+        name "dw<i>" / "pw<i>" (the depthwise or pointwise layer of block i)."""
+        if isinstance(layer, str):
+            i = int(layer[2:])
+            layer = 2 * i + (1 if layer.startswith("dw") else 2)
+        _check(lib().gevo_cnn_remove_layer(self._h, v, layer), "gevo_cnn_remove_layer")
 
     def export(self, v: int) -> dict:
         n = cnn_param_count(self.cfg)

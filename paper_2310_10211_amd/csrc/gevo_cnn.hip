@@ -111,6 +111,32 @@ __global__ __launch_bounds__(256) void k_cnn_pack_pairs(const float* __restrict_
   out[i] = lo | hi << 16;
 }
 
+// A removed block layer in its identity form, written over one variant's
+// master (k-blocked [Kp/32][Np][32]), biases [Np] and mask bits ([Np][Kp/32],
+// bit k % 32 of word k / 32): W[k][n] = 1 where k == centre (a depthwise
+// layer's centre tap, for every channel) or, with centre < 0, where k == n (a
+// pointwise layer: channels passed on, zero channels appended or the first N
+// kept); every other weight, the padding and every bias +0.  Every block
+// layer reads a ReLU output, so relu(x 1 + 0) = x exactly and the layer
+// passes its input on.
+__global__ __launch_bounds__(256) void k_cnn_identity(float* __restrict__ Wm, float* __restrict__ bias,
+                                                      uint32_t* __restrict__ mask, int Kp, int Np, int K, int N,
+                                                      int centre) {
+  const int stride = gridDim.x * blockDim.x, t0 = blockIdx.x * blockDim.x + threadIdx.x;
+  auto one = [&](int k, int n) { return k < K && n < N && (centre >= 0 ? k == centre : k == n); };
+  for (int i = t0; i < Kp * Np; i += stride) {
+    const int kb = i / (Np * 32), r = i - kb * Np * 32, n = r / 32, k = kb * 32 + r % 32;
+    Wm[i] = one(k, n) ? 1.0f : 0.0f;
+  }
+  for (int i = t0; i < Np * (Kp / 32); i += stride) {
+    const int n = i / (Kp / 32), kw = i - n * (Kp / 32);
+    uint32_t bits = 0;
+    for (int b = 0; b < 32; ++b) bits |= one(32 * kw + b, n) ? 1u << b : 0u;
+    mask[i] = bits;
+  }
+  for (int n = t0; n < Np; n += stride) bias[n] = 0.0f;
+}
+
 typedef __bf16 cnn_bf16x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ float cnn_dot2(uint32_t a, uint32_t b, float c) {
@@ -1000,6 +1026,28 @@ gevo_status gevo_cnn_scores(gevo_cnn* h, float* test_loss, float* test_acc, floa
     if (test_loss) test_loss[v] = (float)(ce[v] / (double)h->y.n_test);
     if (test_acc) test_acc[v] = (float)((double)corr[v] / (double)h->y.n_test);
     if (time_s) time_s[v] = (float)(h->last_s / P);
+  }
+  return GEVO_OK;
+}
+
+gevo_status gevo_cnn_remove_layer(gevo_cnn* h, uint32_t v, uint32_t layer) {
+  if (!h) return GEVO_E_ARG;
+  const CnnLayout& y = h->y;
+  if (v >= (uint32_t)y.P || layer >= (uint32_t)y.nt) return GEVO_E_ARG;
+  if (layer == 0 || layer + 1 == (uint32_t)y.nt) return GEVO_E_UNSUPPORTED;   // the stem and the head stay
+  const CnnTensor& t = y.t[layer];
+  const bool depthwise = layer % 2 == 1;                                      // stem, (dw, pw) per block, head
+  char* ws = h->ws;
+  hipLaunchKernelGGL(k_cnn_identity, dim3(std::max(1, std::min(256, (t.Kp * t.Np + 255) / 256))), dim3(256), 0,
+                     h->stream, at<float>(ws, t.Wm) + (size_t)v * t.Np * t.Kp, at<float>(ws, t.bias) + (size_t)v * t.Np,
+                     at<uint32_t>(ws, t.mask) + (size_t)v * t.Np * (t.Kp / 32), t.Kp, t.Np, t.K, t.N,
+                     depthwise ? 4 : -1);
+  CNN_HIP(hipGetLastError());
+  if (t.packed && t.pairs) {                                                  // the prediction copy of the taps
+    const int64_t n = (int64_t)y.P * 5 * t.N;
+    hipLaunchKernelGGL(k_cnn_pack_pairs, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, h->stream,
+                       at<const float>(ws, t.Wm), t.N, y.P, at<uint32_t>(ws, t.pack));
+    CNN_HIP(hipGetLastError());
   }
   return GEVO_OK;
 }

@@ -208,3 +208,81 @@ def _sizes(cfg):
         h, w = out[-1]
         out.append(((h - 1) // s + 1, (w - 1) // s + 1))
     return out
+
+
+# Removed block layers (a structural edit: section 6.1 removes a convolution
+# layer, section 4.1 repairs the shapes).  Per variant the names it loses;
+# the kinds covered: a stride-1 depthwise layer on the stem output, a
+# stride-2 depthwise layer inside the fused pointwise + depthwise kernel, a
+# widening pointwise layer (32 -> 128 channels, zero channels appended), a
+# narrowing one (256 -> 128, the first kept), a square one, and variant 0
+# left whole.
+REMOVAL_CASES = [
+    (dict(P=4, n_test=100, seed=41), {1: ("dw0",), 2: ("pw0", "dw1"), 3: ("pw1",)}),
+    (dict(name="p4-dwsep-cnn8x8x3-32-256-128-128-10", P=4, blocks=[(1, 256), (1, 128), (2, 128)], n_test=100,
+          seed=42), {1: ("pw1",), 2: ("dw2", "pw2"), 3: ("dw0", "pw0", "dw1")}),
+]
+
+
+def _tensor_slices(cfg):
+    off = moff = 0
+    out = {}
+    for name, K, N in cnn.tensors(cfg):
+        out[name] = (off, moff, K, N)
+        off += K * N + N
+        moff += K * N
+    return out
+
+
+@pytest.mark.parametrize("over,gone", REMOVAL_CASES)
+def test_removed_layers_match_the_oracle(over, gone):
+    cfg = synthetic.cnn_config("small", **over)
+    base, x, y = synthetic.cnn_inputs(cfg)
+    pop = _pop(cfg, base, x, y)
+    for v, names in gone.items():
+        for name in names:
+            print(f"[gpu] remove {name} from variant {v}", flush=True)
+            pop.remove_layer(v, name)
+    pop.predict()
+    s = pop.scores()
+    ref = cnn.evaluate(cfg, base.astype(np.float64), x, y, range(cfg["P"]), mode="bf16", removed=gone)
+    _check(s, ref, range(cfg["P"]), len(y))
+    whole = cnn.evaluate(cfg, base.astype(np.float64), x, y, list(gone), mode="bf16")
+    assert any(abs(whole[v][0] - ref[v][0]) > 1e-2 * abs(ref[v][0]) for v in gone)   # the edits matter
+    # exported: the removed layers in identity form, every other tensor the variant's own
+    ths = cnn.thresholds(cfg, range(cfg["P"]))
+    sl = _tensor_slices(cfg)
+    for v in range(cfg["P"]):
+        e = pop.export(v)
+        params, mask = cnn.variant_params(cfg, base.astype(np.float64), v, ths[v])
+        for name, (off, moff, K, N) in sl.items():
+            W = e["params"][off:off + K * N].reshape(K, N)
+            b = e["params"][off + K * N:off + K * N + N]
+            if name in gone.get(v, ()):
+                ident = np.zeros((K, N), np.float32)
+                if name.startswith("dw"):
+                    ident[4, :] = 1.0
+                else:
+                    ident[np.arange(min(K, N)), np.arange(min(K, N))] = 1.0
+                assert W.tobytes() == ident.tobytes() and b.tobytes() == np.zeros(N, np.float32).tobytes(), name
+                assert np.array_equal(e["mask"][moff:moff + K * N], (ident != 0).ravel().astype(np.uint8))
+            else:
+                assert np.array_equal(e["mask"][moff:moff + K * N], mask[moff:moff + K * N]), (v, name)
+                np.testing.assert_allclose(W.ravel(), params[off:off + K * N], rtol=2e-6, atol=0)
+                assert b.tobytes() == params[off + K * N:off + K * N + N].astype(np.float32).tobytes()
+    pop.close()
+
+
+def test_remove_layer_rejects_the_stem_the_head_and_bad_indexes():
+    cfg = synthetic.cnn_config("small", P=2, n_test=64, seed=43)
+    base, x, y = synthetic.cnn_inputs(cfg)
+    pop = _pop(cfg, base, x, y)
+    n_t = len(cnn.tensors(cfg))
+    for v, layer in [(0, 0), (0, n_t - 1), (0, n_t), (2, 1)]:
+        with pytest.raises(Exception):
+            pop.remove_layer(v, layer)
+    pop.predict()                                   # the handle still works, no variant edited
+    s = pop.scores()
+    ref = cnn.evaluate(cfg, base.astype(np.float64), x, y, range(cfg["P"]), mode="bf16")
+    _check(s, ref, range(cfg["P"]), len(y))
+    pop.close()
