@@ -117,6 +117,7 @@ def test_null_handles_rejected():
     assert L.gevo_cnn_predict(None) == E_ARG
     assert L.gevo_cnn_scores(None, None, None, None) == E_ARG
     assert L.gevo_cnn_export(None, 0, None, None, None) == E_ARG
+    assert L.gevo_cnn_remove_layer(None, 0, 1) == E_ARG
     assert L.gevo_cnn_set_profiling(None, 1) == E_ARG
     assert L.gevo_cnn_kernel_stats(None, 0, None, None) == E_ARG
     L.gevo_cnn_destroy(None)
