@@ -27,6 +27,12 @@ Parity status per function:
                         argmax ties
   bf16 emulation        pinned by exhaustive/edge-value checks against the
                         definition of round-to-nearest-even
+  bf16 rounding points  one hand-built net per point (X, W in the forward and
+                        in G_l W_l^T, A after ReLU, G_l as an operand, hidden
+                        bias gradient from the rounded G_l), each with only
+                        that value off the bf16 grid; a mutation test rebuilds
+                        the oracle with each point removed and checks that a
+                        pin fails (tests/test_oracle_bf16_points.py)
 """
 from __future__ import annotations
 
