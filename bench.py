@@ -27,6 +27,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK = {"bf16": 2500.0, "f32": 157.3}        # dense MFMA TFLOP/s, MI355X
+PREDICT_CHUNK = 2048                          # test rows per prediction launch (the library's chunk)
+PREDICT_WEIGHT_BYTES = 4                      # bytes per weight the prediction GEMM reads (fp32 master)
 HBM_PEAK_GBS = 8000.0
 CSRC = os.path.join(ROOT, "paper_2310_10211_amd", "csrc")
 KERNEL_SOURCES = ["gevo_device.h", "gevo_internal.h", "gevo_kernels.hip", "gevo_fused.hip"]
@@ -110,6 +112,27 @@ def layer_costs(cfg):
         bf.append(P * 2.0 * B * K * N)
     if bb:
         out["bwd"] = (sum(bb) / len(bb), sum(bf) / len(bf), len(bb))
+    if cfg["epochs"] == 0:
+        # prediction workloads: hidden layers over row chunks (every layer_fwd /
+        # out_predict launch is a prediction launch), averaged over the launches
+        # of one pass over the test split
+        n, R = cfg["n_test"], PREDICT_CHUNK
+        chunks = [min(R, n - c) for c in range(0, n, R)]
+        fb, ff, fl_n = 0.0, 0.0, 0
+        for rows in chunks:
+            for l in range(1, L):
+                K, N = d[l - 1], d[l]
+                w = P * (K * N * PREDICT_WEIGHT_BYTES + N * 4)                 # weights (operand copy) + bias
+                a_in = rows * K * e if l == 1 else P * rows * K * e        # layer 1 input shared by all variants
+                fb += w + a_in + P * rows * N * e
+                ff += P * 2.0 * rows * K * N
+                fl_n += 1
+        if fl_n:
+            out["layer_fwd"] = (fb / fl_n, ff / fl_n, fl_n)
+        K = d[L - 1]
+        ob = sum(P * (C * K * 4 + C * 4) + (rows * K * e if L == 1 else P * rows * K * e) for rows in chunks)
+        of = sum(P * 2.0 * rows * K * C for rows in chunks)
+        out["out_predict"] = (ob / len(chunks), of / len(chunks), len(chunks))
     if L == 2:
         # fused per-variant kernel: one launch = every SGD step of an epoch
         K, N = d[0], d[1]
@@ -278,9 +301,20 @@ def traffic_for(kernel, workload, sources=None):
 
 
 # ------------------------------------------------------------------ CPU oracle
+def host_threads():
+    """(threads to use, CPUs this process may run on): the machine's CPU share
+    (OMP_NUM_THREADS where the environment sets it) within the affinity mask."""
+    avail = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    try:
+        share = int(os.environ.get("OMP_NUM_THREADS", "0"))
+    except ValueError:
+        share = 0
+    return (min(share, avail) if share > 0 else avail), avail
+
+
 def cpu_baseline(cfg, data, budget_s):
     import oracle
-    threads = min(8, os.cpu_count() or 1)
+    threads, nproc = host_threads()
     V = threads
     variants = list(range(0, cfg["P"], max(1, cfg["P"] // V)))[:V]
     if cfg["epochs"] == 0:                   # prediction workload
@@ -294,9 +328,10 @@ def cpu_baseline(cfg, data, budget_s):
         t0 = time.perf_counter()
         oracle.evaluate(cfg, sub, variants=variants, epochs=0, threads=threads)
         wall = time.perf_counter() - t0
-        return dict(value=len(variants) * rows / wall, unit="variant-samples/s", cores=threads, kind="oracle",
+        return dict(value=len(variants) * rows / wall, unit="variant-samples/s", cores=threads, nproc=nproc,
+                    kind="oracle",
                     sample=f"{len(variants)} variants x {rows} test rows, prediction, {cfg['dtype']} oracle, "
-                           f"{threads} threads, {wall:.1f} s")
+                           f"one variant per thread, {threads} threads of {nproc} CPUs, {wall:.1f} s")
     B = cfg["batch"]
     t0 = time.perf_counter()
     oracle.evaluate(cfg, data, variants=variants[:1], epochs=1, steps=1, threads=1, do_predict=False)
@@ -305,9 +340,10 @@ def cpu_baseline(cfg, data, budget_s):
     t0 = time.perf_counter()
     oracle.evaluate(cfg, data, variants=variants, epochs=1, steps=steps, threads=threads, do_predict=False)
     wall = time.perf_counter() - t0
-    return dict(value=len(variants) * steps * B / wall, unit="variant-samples/s", cores=threads, kind="oracle",
+    return dict(value=len(variants) * steps * B / wall, unit="variant-samples/s", cores=threads, nproc=nproc,
+                kind="oracle",
                 sample=f"{len(variants)} variants x {steps} SGD steps of batch {B} (epoch 0), {cfg['dtype']} "
-                       f"oracle, {threads} threads, {wall:.1f} s")
+                       f"oracle, one variant per thread, {threads} threads of {nproc} CPUs, {wall:.1f} s")
 
 
 def main():

@@ -29,11 +29,14 @@ struct LayerLay {
   size_t arows[2] = {0, 0}, acols[2] = {0, 0};   // training activations (hidden layers)
   size_t gcols = 0, grows = 0;                     // gradient at this layer's output (hidden)
   size_t prows = 0;                                // predict activations
+  bool streamed = false;                           // bf16 hidden layer trained by the streaming kernel
+  size_t wimg = 0, mblk = 0;                       // its master as a register image, block-major mask words
 };
 
 struct Layout {
   int L = 0, P = 0, B = 0, Bp = 0, T = 0;
   bool fused = false;                              // two-layer bf16 nets train in the fused per-variant kernel
+  bool images = false;                             // some layer trains on a register-image copy of its master
   int64_t n_train = 0, n_test = 0;
   int n_test_pad = 0, n_chunks_test = 0;
   size_t elt = 4;
@@ -104,6 +107,12 @@ gevo_status make_layout(const gevo_pop_config* c, Layout* o) {
   }
   if (out_lds(y.lay[y.L - 1].Kp, y.Bp, y.elt, pad) > kLdsBudget) return GEVO_E_UNSUPPORTED;
   y.fused = y.L == 2 && c->dtype == GEVO_BF16 && fused2_lds_bytes(y.lay[0].Np, y.Bp) > 0;
+  for (int l = 0; l + 1 < y.L; ++l) {
+    LayerLay& q = y.lay[l];
+    q.streamed = c->dtype == GEVO_BF16 && !y.fused && stream_layer_supported(q.Kp, q.Np, y.Bp, y.Bp);
+    y.images = y.images || q.streamed;
+  }
+  y.images = y.images || y.fused;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t at = off;
@@ -132,6 +141,10 @@ gevo_status make_layout(const gevo_pop_config* c, Layout* o) {
       q.gcols = take(P * Np * Bp * e);
       if (l >= 1) q.grows = take(P * Bp * Np * e);
       q.prows = take(P * (size_t)kPredictChunk * Np * e);
+    }
+    if (q.streamed) {
+      q.wimg = take(P * Np * Kp * 4);
+      q.mblk = take(P * Np * (Kp / 32) * 4);
     }
   }
   y.lr = take(P * 4);
@@ -327,7 +340,8 @@ gevo_status forward_hidden(gevo_pop* p, const S* arows0, size_t ar0_vs, int R, i
         HIP_TRY(launch_fwd_gemm(g, p->stream, prof(p, GEVO_KERNEL_LAYER_FWD)));
         continue;
       }
-      if (!predict && stream_layer_supported(a.Kp, a.Np, a.Bp, a.R)) {
+      if (!predict && q.streamed) {
+        a.Wimg = at<float>(p, q.wimg); a.mblk = at<uint32_t>(p, q.mblk);
         HIP_TRY(launch_stream_layer(a, y.P, p->stream, prof(p, GEVO_KERNEL_LAYER_FWD)));
         continue;
       }
@@ -450,7 +464,8 @@ gevo_status train_step(gevo_pop* p, int t) {
     if (q.Wt) a.Wt = at<S>(p, q.Wt);
     if (a.Kp % kTile || a.Np % kTile || a.Bp % kTile || a.Bp > kPassRows) return GEVO_E_SHAPE;
     if constexpr (std::is_same<S, uint16_t>::value) {
-      if (stream_layer_supported(a.Kp, a.Np, a.Bp, a.R)) {
+      if (q.streamed) {
+        a.Wimg = at<float>(p, q.wimg); a.mblk = at<uint32_t>(p, q.mblk);
         HIP_TRY(launch_stream_layer(a, y.P, p->stream, prof(p, GEVO_KERNEL_LAYER_TRAIN)));
         continue;
       }
@@ -461,27 +476,46 @@ gevo_status train_step(gevo_pop* p, int t) {
   return GEVO_OK;
 }
 
-// The fused training kernel streams W1 in its register image with block-major
-// masks; every other consumer reads the k-blocked master.  These bring the
-// copy that is about to be read up to date.
-gevo_status fused_to_image(gevo_pop* p) {
+// The fused training kernel and the streaming hidden-layer kernel read and
+// write register-image copies of their masters (with block-major mask words);
+// every other consumer reads the k-blocked master.  These bring the copy that
+// is about to be read up to date.
+gevo_status sync_images(gevo_pop* p) {
   const Layout& y = p->y;
-  if (!y.fused || p->img_valid) return GEVO_OK;
-  const LayerLay& q = y.lay[0];
-  HIP_TRY(launch_w1_image(at<float>(p, q.Wm), at<float>(p, y.w1img), y.P, q.Kp, q.Np, true, p->stream,
-                          prof(p, GEVO_KERNEL_AUX)));
-  HIP_TRY(launch_mask_block_major(at<uint32_t>(p, q.mask), at<uint32_t>(p, y.m1blk), y.P, q.Kp, q.Np, p->stream,
-                                  prof(p, GEVO_KERNEL_AUX)));
+  if (!y.images || p->img_valid) return GEVO_OK;
+  if (y.fused) {
+    const LayerLay& q = y.lay[0];
+    HIP_TRY(launch_w1_image(at<float>(p, q.Wm), at<float>(p, y.w1img), y.P, q.Kp, q.Np, true, p->stream,
+                            prof(p, GEVO_KERNEL_AUX)));
+    HIP_TRY(launch_mask_block_major(at<uint32_t>(p, q.mask), at<uint32_t>(p, y.m1blk), y.P, q.Kp, q.Np, p->stream,
+                                    prof(p, GEVO_KERNEL_AUX)));
+  }
+  for (int l = 0; l + 1 < y.L; ++l) {
+    const LayerLay& q = y.lay[l];
+    if (!q.streamed) continue;
+    HIP_TRY(launch_w1_image(at<float>(p, q.Wm), at<float>(p, q.wimg), y.P, q.Kp, q.Np, true, p->stream,
+                            prof(p, GEVO_KERNEL_AUX)));
+    HIP_TRY(launch_mask_block_major(at<uint32_t>(p, q.mask), at<uint32_t>(p, q.mblk), y.P, q.Kp, q.Np, p->stream,
+                                    prof(p, GEVO_KERNEL_AUX)));
+  }
   p->img_valid = true;
   return GEVO_OK;
 }
 
-gevo_status fused_to_blocked(gevo_pop* p) {
+gevo_status sync_masters(gevo_pop* p) {
   const Layout& y = p->y;
-  if (!y.fused || !p->blk_stale) return GEVO_OK;
-  const LayerLay& q = y.lay[0];
-  HIP_TRY(launch_w1_image(at<float>(p, y.w1img), at<float>(p, q.Wm), y.P, q.Kp, q.Np, false, p->stream,
-                          prof(p, GEVO_KERNEL_AUX)));
+  if (!y.images || !p->blk_stale) return GEVO_OK;
+  if (y.fused) {
+    const LayerLay& q = y.lay[0];
+    HIP_TRY(launch_w1_image(at<float>(p, y.w1img), at<float>(p, q.Wm), y.P, q.Kp, q.Np, false, p->stream,
+                            prof(p, GEVO_KERNEL_AUX)));
+  }
+  for (int l = 0; l + 1 < y.L; ++l) {
+    const LayerLay& q = y.lay[l];
+    if (!q.streamed) continue;
+    HIP_TRY(launch_w1_image(at<float>(p, q.wimg), at<float>(p, q.Wm), y.P, q.Kp, q.Np, false, p->stream,
+                            prof(p, GEVO_KERNEL_AUX)));
+  }
   p->blk_stale = false;
   return GEVO_OK;
 }
@@ -499,6 +533,10 @@ gevo_status do_train_steps(gevo_pop* p, uint32_t epoch, uint32_t s0, uint32_t s1
     return GEVO_E_ORDER;
   }
   HIP_TRY(hipEventRecord(p->ev0, p->stream));
+  {
+    gevo_status sti = sync_images(p);               // before the first forward of an epoch
+    if (sti != GEVO_OK) return sti;
+  }
   if (begin) {
     gevo_status st = begin_epoch<S>(p, (int)epoch);
     if (st != GEVO_OK) return st;
@@ -513,8 +551,6 @@ gevo_status do_train_steps(gevo_pop* p, uint32_t epoch, uint32_t s0, uint32_t s1
     f.Kp = q1.Kp; f.Hp = q1.Np; f.C = q2.N; f.B = y.B; f.Bp = y.Bp; f.T = y.T;
     f.n = y.n_train; f.t0 = (int)s0; f.t1 = (int)s1;
     f.xrows = at<uint16_t>(p, y.xrows); f.xcols = at<uint16_t>(p, y.xcols); f.labels = at<int32_t>(p, y.yep);
-    gevo_status sti = fused_to_image(p);
-    if (sti != GEVO_OK) return sti;
     f.W1 = at<float>(p, y.w1img); f.b1 = at<float>(p, q1.bias); f.m1 = at<uint32_t>(p, y.m1blk);
     f.W2 = at<float>(p, q2.Wm); f.b2 = at<float>(p, q2.bias); f.m2 = at<uint32_t>(p, q2.mask);
     f.bm1 = at<uint32_t>(p, q1.bmask); f.bm2 = at<uint32_t>(p, q2.bmask);
@@ -534,6 +570,7 @@ gevo_status do_train_steps(gevo_pop* p, uint32_t epoch, uint32_t s0, uint32_t s1
       gevo_status st = train_step<S>(p, (int)t);
       if (st != GEVO_OK) return st;
     }
+    if (y.images && (begin || s1 > s0)) p->blk_stale = true;   // streamed layers moved on in their images
   }
   p->next_step = s1;
   if (s1 == (uint32_t)y.T) {
@@ -549,7 +586,7 @@ template <typename S>
 gevo_status do_predict(gevo_pop* p) {
   const Layout& y = p->y;
   HIP_TRY(hipEventRecord(p->ev0, p->stream));
-  gevo_status stb = fused_to_blocked(p);
+  gevo_status stb = sync_masters(p);
   if (stb != GEVO_OK) return stb;
   const size_t Kp1 = (size_t)y.lay[0].Kp;
   for (int c0 = 0; c0 < y.n_test_pad; c0 += kPredictChunk) {
@@ -873,7 +910,7 @@ gevo_status gevo_pop_set_genomes(gevo_pop* p, float lr_base, const uint32_t* off
   p->rows_done = 0;
   p->predicted = false;
   p->timing_pending = false;
-  p->img_valid = false;                          // the fused kernel's copy of the hidden layer is stale
+  p->img_valid = false;                          // the register-image copies are stale
   p->blk_stale = false;
   return GEVO_OK;
 }
@@ -961,7 +998,7 @@ gevo_status gevo_pop_export(gevo_pop* p, uint32_t v, float* params_out, uint8_t*
   if (!p) return GEVO_E_ARG;
   const Layout& y = p->y;
   if (v >= (uint32_t)y.P) return GEVO_E_ARG;
-  gevo_status stb = fused_to_blocked(p);
+  gevo_status stb = sync_masters(p);
   if (stb != GEVO_OK) return stb;
   HIP_TRY(hipStreamSynchronize(p->stream));
   size_t off = 0, moff = 0;
@@ -994,7 +1031,7 @@ gevo_status gevo_pop_import(gevo_pop* p, uint32_t v, const float* params) {
   const Layout& y = p->y;
   if (v >= (uint32_t)y.P) return GEVO_E_ARG;
   if (p->open_epoch >= 0) return GEVO_E_ORDER;        // only between epochs
-  gevo_status stb = fused_to_blocked(p);
+  gevo_status stb = sync_masters(p);
   if (stb != GEVO_OK) return stb;
   HIP_TRY(hipStreamSynchronize(p->stream));
   p->img_valid = false;                               // the image is rebuilt from the imported master

@@ -72,6 +72,10 @@ struct LayerArgs {
   S* Orows; size_t or_vs;        // [v][R][Np] relu output rows
   S* Ocols; size_t oc_vs;        // [v][Np][R] relu output, transposed (nullable)
   S* Wt;                         // [v][Kp][Np] operand copy of W, transposed (nullable)
+  // bf16 streaming kernel only: the master as a register image and its mask
+  // words block-major (see launch_w1_image / launch_mask_block_major)
+  float* Wimg;                   // [P][Kp/32][Np/32][4][64][4]
+  const uint32_t* mblk;          // [P][Kp/32][Np]
 };
 
 // bf16 forward of a hidden layer over prediction rows (no update)

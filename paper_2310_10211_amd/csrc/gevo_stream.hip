@@ -8,7 +8,10 @@
 //   Z[b][n]  = sum_k A_{t+1}[b][k] bf16(W)[k][n] + b,  O = bf16(relu(Z))
 //
 // The fp32 master streams once per step, 32 inputs (one k-block) at a time,
-// through registers.  Four waves, one per SIMD with the whole register file:
+// through registers, in the register-image layout (each load or store of a
+// wave moves one contiguous KiB; the launcher keeps that copy of the master
+// and its block-major mask words current).  Four waves, one per SIMD with the
+// whole register file:
 // wave w owns units 32w..32w+31.  For a block, the weight gradient comes out
 // of 32x32x16 MFMAs in the accumulator layout (lane l: unit l%32, inputs
 // k = 8(r/4) + 4(l/32) + r%4 of register r), is applied in place, rounded to
@@ -85,8 +88,13 @@ __global__ __launch_bounds__(kST, 1) void k_stream_layer(LayerArgs<uint16_t> a) 
   const int rot = (v * (int)gridDim.x + tile) % nkb;
   auto phys = [&](int j) { return j + rot < nkb ? j + rot : j + rot - nkb; };
   const int n = tile * kSU + wave * 32 + l32;          // this lane's unit
-  float* Wv = a.Wm + (size_t)v * Np * Kp;              // k-blocked: ((kb Np + n) 32 + k%32)
   const float lrv = a.lr[v];
+  // Scalar bases of the master image and mask words (see below).  Declared
+  // here, before the gradient loads, the compiler keeps them in scalar
+  // registers; the build rejects a base in vector registers (the assembler)
+  // or one moved there from vector registers (check_prefetch.sgpr_hazards).
+  float* wimg = a.Wimg + (size_t)v * Np * Kp;
+  const uint32_t* mblk = a.mblk + (size_t)v * nkb * Np;
 
   // the gradient at this layer's output for the whole pass: gs[s] holds
   // G[n][16s + 8lh .. +7], the B operand of contraction step s
@@ -114,7 +122,14 @@ __global__ __launch_bounds__(kST, 1) void k_stream_layer(LayerArgs<uint16_t> a) 
   // loop-invariant 32-bit lane offset in bytes.
   const uint16_t* acol = UPD ? a.Acols + a.ac_vs * v : nullptr;   // [Kp][BP]
   const uint16_t* arow = FWD ? a.Arows + a.ar_vs * v : nullptr;   // [BP][Kp]
-  const uint32_t* mrow = a.mask + (size_t)v * Np * nkb;           // [Np][nkb]
+  // master image of this variant: block kb, unit group g (32 units) holds
+  // 4 KiB as [q][lane][4], lane l32 + 32lh holding inputs 8q + 4lh + 0..3 of
+  // unit 32g + l32; mask words block-major [kb][n].  The scalar base of a
+  // block depends on the variant and the block only; the unit group goes
+  // into the 32-bit lane offset, so no base is ever moved from a vector
+  // register (a VALU write of an SGPR that a memory instruction reads needs
+  // five wait states, which the compiler does not insert before inline
+  // assembly).
   uint32_t oc[XU], orr[XU];
 #pragma unroll
   for (int q = 0; q < XU; ++q) {
@@ -122,7 +137,8 @@ __global__ __launch_bounds__(kST, 1) void k_stream_layer(LayerArgs<uint16_t> a) 
     oc[q] = (uint32_t)(((i / (BP / 8)) * BP + (i % (BP / 8)) * 8) * 2);
     orr[q] = (uint32_t)(((i >> 2) * Kp + (i & 3) * 8) * 2);
   }
-  const uint32_t ow = (uint32_t)((n * 32 + 4 * lh) * 4), om = (uint32_t)(n * nkb * 4);
+  const int grp = tile * (kSU / 32) + wave;            // this wave's 32-unit group
+  const uint32_t ow = (uint32_t)((grp * 1024 + lane * 4) * 4), om = (uint32_t)(n * 4);
   u32x4_t st[2 * XU];                                  // input staging: columns [0, XU), rows [XU, 2XU)
   auto load_xc = [&](int j) {
     if constexpr (UPD) {
@@ -161,17 +177,18 @@ __global__ __launch_bounds__(kST, 1) void k_stream_layer(LayerArgs<uint16_t> a) 
     }
   };
   // this lane's master values of block kb: k = 32kb + 8q + 4lh + 0..3
-  // (q = 0..3, 32 bytes apart), and the unit's mask word
+  // (q = 0..3: one contiguous KiB of the wave's image per load), and the
+  // unit's mask word
   auto load_w = [&](int j, f32x4_t (&w)[4], uint32_t& m) {
     const int kb = phys(j);
-    const float* bw = Wv + (size_t)kb * Np * 32;
+    const float* bw = wimg + (size_t)kb * Np * 32;     // the block's image: Np/32 groups of 1024 floats
     if constexpr (UPD) {
-      const uint32_t* bm = mrow + kb;
+      const uint32_t* bm = mblk + (size_t)kb * Np;
       asm volatile(
           "global_load_dwordx4 %0, %5, %6\n\t"
-          "global_load_dwordx4 %1, %5, %6 offset:32\n\t"
-          "global_load_dwordx4 %2, %5, %6 offset:64\n\t"
-          "global_load_dwordx4 %3, %5, %6 offset:96\n\t"
+          "global_load_dwordx4 %1, %5, %6 offset:1024\n\t"
+          "global_load_dwordx4 %2, %5, %6 offset:2048\n\t"
+          "global_load_dwordx4 %3, %5, %6 offset:3072\n\t"
           "global_load_dword %4, %7, %8"
           : "=&v"(w[0]), "=&v"(w[1]), "=&v"(w[2]), "=&v"(w[3]), "=&v"(m)
           : "v"(ow), "s"(bw), "v"(om), "s"(bm)
@@ -179,9 +196,9 @@ __global__ __launch_bounds__(kST, 1) void k_stream_layer(LayerArgs<uint16_t> a) 
     } else {
       asm volatile(
           "global_load_dwordx4 %0, %4, %5\n\t"
-          "global_load_dwordx4 %1, %4, %5 offset:32\n\t"
-          "global_load_dwordx4 %2, %4, %5 offset:64\n\t"
-          "global_load_dwordx4 %3, %4, %5 offset:96"
+          "global_load_dwordx4 %1, %4, %5 offset:1024\n\t"
+          "global_load_dwordx4 %2, %4, %5 offset:2048\n\t"
+          "global_load_dwordx4 %3, %4, %5 offset:3072"
           : "=&v"(w[0]), "=&v"(w[1]), "=&v"(w[2]), "=&v"(w[3])
           : "v"(ow), "s"(bw)
           : "memory");
@@ -247,10 +264,10 @@ __global__ __launch_bounds__(kST, 1) void k_stream_layer(LayerArgs<uint16_t> a) 
         const uint32_t keep = (uint32_t)(((int)(m << (31 - kl))) >> 31);
         wn[r] = __uint_as_float(__float_as_uint(__fsub_rn(w[r >> 2][r & 3], __fmul_rn(lrv, d[r]))) & keep);
       }
-      float* wp = Wv + ((size_t)kb * Np + n) * 32 + 4 * lh;
+      float* wp = wimg + ((size_t)kb * (Np / 32) + grp) * 1024 + lane * 4;
 #pragma unroll
       for (int q = 0; q < 4; ++q)
-        *reinterpret_cast<float4*>(wp + 8 * q) = make_float4(wn[4 * q], wn[4 * q + 1], wn[4 * q + 2], wn[4 * q + 3]);
+        *reinterpret_cast<float4*>(wp + 256 * q) = make_float4(wn[4 * q], wn[4 * q + 1], wn[4 * q + 2], wn[4 * q + 3]);
     } else {
       if constexpr (FWD && !first) forward((j - 1) & 1);
 #pragma unroll

@@ -80,3 +80,58 @@ def test_partial_wait_needs_enough_younger_memory_operations():
                        "\tglobal_store_dword v[4:5], v1, off\n\tglobal_store_dword v[4:5], v1, off offset:4\n"
                        "\t;;#ASMSTART\n\ts_waitcnt vmcnt(2)")
     assert check_prefetch.check_assembly(ok) == {HEAD[:-2]: 1}
+
+
+# ------------------------------------------------- VALU -> SGPR -> memory hazard
+def _hz(body: str) -> str:
+    return _fn(body)
+
+
+HAZARD = _hz("""\
+\tv_readfirstlane_b32 s0, v130
+\tv_readfirstlane_b32 s1, v131
+\t;;#ASMSTART
+\tglobal_load_dwordx4 v[8:11], v150, s[0:1]
+\t;;#ASMEND
+\t;;#ASMSTART
+\ts_waitcnt vmcnt(0)
+\t;;#ASMEND
+\tv_add_f32_e32 v20, v8, v9
+\ts_endpgm
+""")
+
+
+def test_sgpr_base_written_by_valu_just_before_an_asm_load_is_caught():
+    with pytest.raises(RuntimeError, match="reads an SGPR fewer than 5 wait states"):
+        check_prefetch.check_assembly(HAZARD)
+
+
+def test_five_wait_states_clear_the_sgpr_hazard():
+    ok = HAZARD.replace("\tv_readfirstlane_b32 s1, v131\n", "\tv_readfirstlane_b32 s1, v131\n\ts_nop 4\n")
+    assert check_prefetch.check_assembly(ok) == {HEAD[:-2]: 1}
+
+
+def test_scalar_alu_base_is_not_a_hazard():
+    ok = HAZARD.replace("v_readfirstlane_b32 s0, v130", "s_add_u32 s0, s20, s2").replace(
+        "v_readfirstlane_b32 s1, v131", "s_addc_u32 s1, s21, 0")
+    assert check_prefetch.check_assembly(ok) == {HEAD[:-2]: 1}
+
+
+def test_sgpr_hazard_through_a_loop_back_edge_is_caught():
+    bad = _hz("""\
+.LBB0_1:
+\t;;#ASMSTART
+\tglobal_load_dwordx4 v[8:11], v150, s[4:5]
+\t;;#ASMEND
+\t;;#ASMSTART
+\ts_waitcnt vmcnt(0)
+\t;;#ASMEND
+\tv_add_f32_e32 v20, v8, v9
+\tv_add_co_u32_e64 v40, s[4:5], v41, v42
+\ts_cbranch_scc1 .LBB0_1
+\ts_endpgm
+""")
+    with pytest.raises(RuntimeError, match="reads an SGPR"):
+        check_prefetch.check_assembly(bad)
+    hz = check_prefetch.sgpr_hazards(bad.split("\n"))
+    assert len(hz) == 1 and "s[4:5]" in hz[0][2]
