@@ -28,13 +28,16 @@ if ROOT not in sys.path:
 
 PEAK = {"bf16": 2500.0, "f32": 157.3}        # dense MFMA TFLOP/s, MI355X
 PREDICT_CHUNK = 2048                          # test rows per prediction launch (the library's chunk)
-PREDICT_WEIGHT_BYTES = 4                      # bytes per weight the prediction GEMM reads (fp32 master)
 HBM_PEAK_GBS = 8000.0
 CSRC = os.path.join(ROOT, "paper_2310_10211_amd", "csrc")
-KERNEL_SOURCES = ["gevo_device.h", "gevo_internal.h", "gevo_kernels.hip", "gevo_fused.hip"]
+KERNEL_SOURCES = ["gevo_device.h", "gevo_internal.h", "gevo_kernels.hip", "gevo_fused.hip", "gevo_stream.hip",
+                  "gevo_bwd.hip", "gevo_gemm.hip", "gevo_predict.hip"]
 # rocprofv3 kernel-name stem -> kernel kind of gevo_pop_kernel_stats (training kind, predict kind)
-KERNEL_KIND_OF = {"k_fused2": ("fused_train", None), "k_layer": ("layer_train", "layer_fwd"),
-                  "k_out": ("out_train", "out_predict"), "k_bwd": ("bwd", None)}
+KERNEL_KIND_OF = {"k_fused2": ("fused_train", None), "k_stream_layer": ("layer_train", "layer_fwd"),
+                  "k_layer": ("layer_train", "layer_fwd"), "k_out": ("out_train", "out_predict"),
+                  "k_bwd_gemm": ("bwd", None), "k_bwd": ("bwd", None), "k_pred_gemmILb1": (None, "fwd_out"),
+                  "k_pred_gemmILb0": (None, "layer_fwd"), "k_wt_bf16": (None, "weight_copy"),
+                  "k_fwd_gemm": (None, "layer_fwd")}
 
 
 def fused_workload(cfg):
@@ -113,26 +116,7 @@ def layer_costs(cfg):
     if bb:
         out["bwd"] = (sum(bb) / len(bb), sum(bf) / len(bf), len(bb))
     if cfg["epochs"] == 0:
-        # prediction workloads: hidden layers over row chunks (every layer_fwd /
-        # out_predict launch is a prediction launch), averaged over the launches
-        # of one pass over the test split
-        n, R = cfg["n_test"], PREDICT_CHUNK
-        chunks = [min(R, n - c) for c in range(0, n, R)]
-        fb, ff, fl_n = 0.0, 0.0, 0
-        for rows in chunks:
-            for l in range(1, L):
-                K, N = d[l - 1], d[l]
-                w = P * (K * N * PREDICT_WEIGHT_BYTES + N * 4)                 # weights (operand copy) + bias
-                a_in = rows * K * e if l == 1 else P * rows * K * e        # layer 1 input shared by all variants
-                fb += w + a_in + P * rows * N * e
-                ff += P * 2.0 * rows * K * N
-                fl_n += 1
-        if fl_n:
-            out["layer_fwd"] = (fb / fl_n, ff / fl_n, fl_n)
-        K = d[L - 1]
-        ob = sum(P * (C * K * 4 + C * 4) + (rows * K * e if L == 1 else P * rows * K * e) for rows in chunks)
-        of = sum(P * 2.0 * rows * K * C for rows in chunks)
-        out["out_predict"] = (ob / len(chunks), of / len(chunks), len(chunks))
+        out.update(predict_costs(cfg))
     if L == 2:
         # fused per-variant kernel: one launch = every SGD step of an epoch
         K, N = d[0], d[1]
@@ -141,6 +125,76 @@ def layer_costs(cfg):
         fl_step = P * B * (4.0 * K * N + 6.0 * N * C)
         out["fused_train"] = (T * per_step, T * fl_step, 1)
     return out
+
+
+def _pad(x, m=32):
+    return (x + m - 1) // m * m
+
+
+def predict_plan(cfg):
+    """The library's prediction plan for bf16 nets: hidden layer l runs on the
+    prediction GEMM when its padded width is a multiple of 256 (reading a bf16
+    weight copy), and a last hidden layer exactly 256 wide also runs the output
+    layer ('fwd_out'); other hidden layers run the older forward kernels
+    ('layer_fwd' with fp32 weights) and the output layer on its own
+    ('out_predict').  Returns [(kind, weight bytes per weight)] per hidden layer
+    and whether the output layer is fused."""
+    d = cfg["dims"]
+    L = len(d) - 1
+    plan, fused = [], False
+    for l in range(1, L):
+        pred = cfg["dtype"] == "bf16" and _pad(d[l]) % 256 == 0
+        if pred and l == L - 1 and _pad(d[l]) == 256:
+            plan.append(("fwd_out", 2))
+            fused = True
+        else:
+            plan.append(("layer_fwd", 2 if pred else 4))
+    return plan, fused
+
+
+def predict_costs(cfg):
+    """{kind: (bytes, flops, launches)} per launch of one pass over the test
+    split, averaged over the kind's launches.  Per launch (one chunk of rows,
+    all P variants): weights once (the bf16 copy or the fp32 master) plus
+    biases; the layer's input rows (layer 1: shared by all variants); its
+    output rows unless the output layer is fused; a fused launch adds the
+    output layer's fp32 weights and the chunk's labels.  The weight copy
+    reads the fp32 master and writes bf16."""
+    d, P = cfg["dims"], cfg["P"]
+    e = 2 if cfg["dtype"] == "bf16" else 4
+    L = len(d) - 1
+    C = d[L]
+    n, R = cfg["n_test"], PREDICT_CHUNK
+    chunks = [min(R, n - c) for c in range(0, n, R)]
+    plan, fused = predict_plan(cfg)
+    acc = {}
+
+    def add(kind, b, f):
+        a = acc.setdefault(kind, [0.0, 0.0, 0])
+        a[0] += b
+        a[1] += f
+        a[2] += 1
+
+    for l, (kind, wb) in enumerate(plan, start=1):
+        K, N = d[l - 1], d[l]
+        if wb == 2:
+            add("weight_copy", P * K * N * (4 + 2), 0.0)
+        for rows in chunks:
+            a_in = rows * K * e if l == 1 else P * rows * K * e
+            b = P * (K * N * wb + N * 4) + a_in
+            f = P * 2.0 * rows * K * N
+            if kind == "fwd_out":
+                b += P * (C * N * 4 + C * 4) + rows * 4
+                f += P * 2.0 * rows * N * C
+            else:
+                b += P * rows * N * e
+            add(kind, b, f)
+    if not fused:
+        K = d[L - 1]
+        for rows in chunks:
+            add("out_predict", P * (C * K * 4 + C * 4) + (rows * K * e if L == 1 else P * rows * K * e) + rows * 4,
+                P * 2.0 * rows * K * C)
+    return {k: (v[0] / v[2], v[1] / v[2], v[2]) for k, v in acc.items()}
 
 
 def train_flops_per_sample(dims):

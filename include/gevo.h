@@ -341,7 +341,9 @@ typedef enum {
   GEVO_KERNEL_BWD = 6,           /* hidden backward GEMM */
   GEVO_KERNEL_AUX = 7,           /* zeroing, reductions */
   GEVO_KERNEL_FUSED_TRAIN = 8,   /* two-layer nets: whole SGD steps, one workgroup per variant */
-  GEVO_KERNEL_KINDS = 9
+  GEVO_KERNEL_WEIGHT_COPY = 9,   /* bf16 weight copies read by the prediction GEMM */
+  GEVO_KERNEL_FWD_OUT = 10,      /* prediction: last hidden layer GEMM with the output layer fused */
+  GEVO_KERNEL_KINDS = 11
 } gevo_kernel_kind;
 
 gevo_status gevo_pop_set_profiling(gevo_pop* pop, int enable);

@@ -44,7 +44,7 @@ EXPORTED = [
 CNN_MAX_BLOCKS = 4
 CNN_KERNEL_KINDS = ["stem", "depthwise", "pointwise", "pool", "head", "reduce", "pw_dw"]
 KERNEL_KINDS = ["init", "gather", "layer_train", "layer_fwd", "out_train", "out_predict", "bwd", "aux",
-                "fused_train"]
+                "fused_train", "weight_copy", "fwd_out"]
 
 
 class GevoError(RuntimeError):

@@ -29,6 +29,8 @@ struct LayerLay {
   size_t arows[2] = {0, 0}, acols[2] = {0, 0};   // training activations (hidden layers)
   size_t gcols = 0, grows = 0;                     // gradient at this layer's output (hidden)
   size_t prows = 0;                                // predict activations
+  bool pred = false;                               // bf16 hidden layer predicted by k_pred_gemm
+  size_t wbf = 0;                                  // its bf16 weight copy [P][Np][Kp]
   bool streamed = false;                           // bf16 hidden layer trained by the streaming kernel
   size_t wimg = 0, mblk = 0;                       // its master as a register image, block-major mask words
 };
@@ -109,6 +111,7 @@ gevo_status make_layout(const gevo_pop_config* c, Layout* o) {
   y.fused = y.L == 2 && c->dtype == GEVO_BF16 && fused2_lds_bytes(y.lay[0].Np, y.Bp) > 0;
   for (int l = 0; l + 1 < y.L; ++l) {
     LayerLay& q = y.lay[l];
+    q.pred = c->dtype == GEVO_BF16 && pred_gemm_supported(q.Kp, q.Np, kOutRows);
     q.streamed = c->dtype == GEVO_BF16 && !y.fused && stream_layer_supported(q.Kp, q.Np, y.Bp, y.Bp);
     y.images = y.images || q.streamed;
   }
@@ -142,6 +145,7 @@ gevo_status make_layout(const gevo_pop_config* c, Layout* o) {
       if (l >= 1) q.grows = take(P * Bp * Np * e);
       q.prows = take(P * (size_t)kPredictChunk * Np * e);
     }
+    if (q.pred) q.wbf = take(P * Np * Kp * 2);
     if (q.streamed) {
       q.wimg = take(P * Np * Kp * 4);
       q.mblk = take(P * Np * (Kp / 32) * 4);
@@ -243,6 +247,7 @@ struct gevo_pop {
   // fused training keeps W1 in its own register image: which copy is current
   bool img_valid = false;   // the image (and the block-major mask) match the k-blocked master
   bool blk_stale = false;   // training has advanced the image past the k-blocked master
+  bool wbf_valid = false;   // the bf16 weight copies of the prediction GEMM match the masters
   // kernel-level timing (gevo_pop_set_profiling)
   bool prof_on = false;
   struct ProfRec { int kind; hipEvent_t a, b; };
@@ -309,44 +314,54 @@ LaunchEv prof(gevo_pop* p, int kind) {
     if ((x) != hipSuccess) return GEVO_E_HIP;   \
   } while (0)
 
+// forward of hidden layer l over R rows (layer 0 reads arows0; deeper layers
+// the previous layer's activations), training (outsel: activation buffer) or
+// prediction (the chunk buffers)
+template <typename S>
+gevo_status forward_layer(gevo_pop* p, int l, const S* arows0, size_t ar0_vs, int R, int outsel, bool predict) {
+  const Layout& y = p->y;
+  const LayerLay& q = y.lay[l];
+  LayerArgs<S> a{};
+  a.Kp = q.Kp; a.Np = q.Np; a.Bp = y.Bp;
+  a.Wm = at<float>(p, q.Wm); a.bias = at<float>(p, q.bias); a.mask = at<uint32_t>(p, q.mask); a.bmask = at<uint32_t>(p, q.bmask);
+  a.lr = at<float>(p, y.lr);
+  a.do_update = 0;
+  a.do_forward = 1;
+  a.R = R;
+  if (l == 0) { a.Arows = arows0; a.ar_vs = ar0_vs; }
+  else if (predict) { a.Arows = at<S>(p, y.lay[l - 1].prows); a.ar_vs = (size_t)kPredictChunk * y.lay[l - 1].Np; }
+  else { a.Arows = at<S>(p, y.lay[l - 1].arows[outsel]); a.ar_vs = (size_t)y.Bp * y.lay[l - 1].Np; }
+  if (predict) {
+    a.Orows = at<S>(p, q.prows); a.or_vs = (size_t)kPredictChunk * q.Np;
+  } else {
+    a.Orows = at<S>(p, q.arows[outsel]); a.or_vs = (size_t)y.Bp * q.Np;
+    a.Ocols = at<S>(p, q.acols[outsel]); a.oc_vs = (size_t)q.Np * y.Bp;
+    if (q.Wt) a.Wt = at<S>(p, q.Wt);
+  }
+  if (a.Kp % kTile || a.Np % kTile || a.R % kTile || a.R <= 0) return GEVO_E_SHAPE;
+  if constexpr (std::is_same<S, uint16_t>::value) {
+    if (predict && fwd_gemm_supported(a.Kp, a.Np, a.R)) {      // plain per-variant GEMM, no update
+      FwdGemmArgs g{};
+      g.A = a.Arows; g.a_vs = a.ar_vs; g.Wm = a.Wm; g.bias = a.bias; g.O = a.Orows; g.o_vs = a.or_vs;
+      g.Kp = a.Kp; g.Np = a.Np; g.R = a.R; g.P = y.P;
+      HIP_TRY(launch_fwd_gemm(g, p->stream, prof(p, GEVO_KERNEL_LAYER_FWD)));
+      return GEVO_OK;
+    }
+    if (!predict && q.streamed) {
+      a.Wimg = at<float>(p, q.wimg); a.mblk = at<uint32_t>(p, q.mblk);
+      HIP_TRY(launch_stream_layer(a, y.P, p->stream, prof(p, GEVO_KERNEL_LAYER_FWD)));
+      return GEVO_OK;
+    }
+  }
+  HIP_TRY(launch_layer<S>(a, y.P, p->stream, prof(p, GEVO_KERNEL_LAYER_FWD)));
+  return GEVO_OK;
+}
+
 template <typename S>
 gevo_status forward_hidden(gevo_pop* p, const S* arows0, size_t ar0_vs, int R, int outsel, bool predict) {
-  const Layout& y = p->y;
-  for (int l = 0; l < y.L - 1; ++l) {
-    const LayerLay& q = y.lay[l];
-    LayerArgs<S> a{};
-    a.Kp = q.Kp; a.Np = q.Np; a.Bp = y.Bp;
-    a.Wm = at<float>(p, q.Wm); a.bias = at<float>(p, q.bias); a.mask = at<uint32_t>(p, q.mask); a.bmask = at<uint32_t>(p, q.bmask);
-    a.lr = at<float>(p, y.lr);
-    a.do_update = 0;
-    a.do_forward = 1;
-    a.R = R;
-    if (l == 0) { a.Arows = arows0; a.ar_vs = ar0_vs; }
-    else if (predict) { a.Arows = at<S>(p, y.lay[l - 1].prows); a.ar_vs = (size_t)kPredictChunk * y.lay[l - 1].Np; }
-    else { a.Arows = at<S>(p, y.lay[l - 1].arows[outsel]); a.ar_vs = (size_t)y.Bp * y.lay[l - 1].Np; }
-    if (predict) {
-      a.Orows = at<S>(p, q.prows); a.or_vs = (size_t)kPredictChunk * q.Np;
-    } else {
-      a.Orows = at<S>(p, q.arows[outsel]); a.or_vs = (size_t)y.Bp * q.Np;
-      a.Ocols = at<S>(p, q.acols[outsel]); a.oc_vs = (size_t)q.Np * y.Bp;
-      if (q.Wt) a.Wt = at<S>(p, q.Wt);
-    }
-    if (a.Kp % kTile || a.Np % kTile || a.R % kTile || a.R <= 0) return GEVO_E_SHAPE;
-    if constexpr (std::is_same<S, uint16_t>::value) {
-      if (predict && fwd_gemm_supported(a.Kp, a.Np, a.R)) {      // plain per-variant GEMM, no update
-        FwdGemmArgs g{};
-        g.A = a.Arows; g.a_vs = a.ar_vs; g.Wm = a.Wm; g.bias = a.bias; g.O = a.Orows; g.o_vs = a.or_vs;
-        g.Kp = a.Kp; g.Np = a.Np; g.R = a.R; g.P = y.P;
-        HIP_TRY(launch_fwd_gemm(g, p->stream, prof(p, GEVO_KERNEL_LAYER_FWD)));
-        continue;
-      }
-      if (!predict && q.streamed) {
-        a.Wimg = at<float>(p, q.wimg); a.mblk = at<uint32_t>(p, q.mblk);
-        HIP_TRY(launch_stream_layer(a, y.P, p->stream, prof(p, GEVO_KERNEL_LAYER_FWD)));
-        continue;
-      }
-    }
-    HIP_TRY(launch_layer<S>(a, y.P, p->stream, prof(p, GEVO_KERNEL_LAYER_FWD)));
+  for (int l = 0; l < p->y.L - 1; ++l) {
+    gevo_status st = forward_layer<S>(p, l, arows0, ar0_vs, R, outsel, predict);
+    if (st != GEVO_OK) return st;
   }
   return GEVO_OK;
 }
@@ -533,6 +548,7 @@ gevo_status do_train_steps(gevo_pop* p, uint32_t epoch, uint32_t s0, uint32_t s1
     return GEVO_E_ORDER;
   }
   HIP_TRY(hipEventRecord(p->ev0, p->stream));
+  p->wbf_valid = false;                             // the masters move on
   {
     gevo_status sti = sync_images(p);               // before the first forward of an epoch
     if (sti != GEVO_OK) return sti;
@@ -582,17 +598,73 @@ gevo_status do_train_steps(gevo_pop* p, uint32_t epoch, uint32_t s0, uint32_t s1
   return GEVO_OK;
 }
 
+// bf16 prediction of one chunk through k_pred_gemm: every hidden layer with
+// a bf16 weight copy runs as a plain GEMM (other shapes as in forward_hidden);
+// a last hidden layer of exactly one column tile also runs the output layer.
+// Returns whether the output layer was fused (the caller then skips k_out).
+gevo_status predict_chunk_gemm(gevo_pop* p, const uint16_t* xr, int c0, int R, bool* out_done) {
+  const Layout& y = p->y;
+  *out_done = false;
+  for (int l = 0; l < y.L - 1; ++l) {
+    const LayerLay& q = y.lay[l];
+    const uint16_t* ain = l == 0 ? xr : at<uint16_t>(p, y.lay[l - 1].prows);
+    const size_t a_vs = l == 0 ? 0 : (size_t)kPredictChunk * y.lay[l - 1].Np;
+    if (!q.pred || !pred_gemm_supported(q.Kp, q.Np, R)) {
+      gevo_status st = forward_layer<uint16_t>(p, l, xr, 0, R, 0, true);
+      if (st != GEVO_OK) return st;
+      continue;
+    }
+    PredGemmArgs g{};
+    g.A = ain; g.a_vs = a_vs; g.W = at<uint16_t>(p, q.wbf); g.bias = at<float>(p, q.bias);
+    g.Kp = q.Kp; g.Np = q.Np; g.R = R; g.P = y.P;
+    const LayerLay& o = y.lay[y.L - 1];
+    if (l == y.L - 2 && q.Np == 256 && o.Kp == 256) {          // last hidden layer, one tile wide
+      g.WL = at<float>(p, o.Wm); g.bL = at<float>(p, o.bias); g.C = o.N;
+      g.labels = at<int32_t>(p, y.yte) + c0;
+      g.chunk0 = c0 / kOutRows; g.n_chunks_total = y.n_chunks_test;
+      g.part_ce = at<double>(p, y.part_ce); g.part_correct = at<unsigned int>(p, y.part_corr);
+      HIP_TRY(launch_pred_gemm(g, p->stream, prof(p, GEVO_KERNEL_FWD_OUT)));
+      *out_done = true;
+    } else {
+      g.O = at<uint16_t>(p, q.prows); g.o_vs = (size_t)kPredictChunk * q.Np;
+      HIP_TRY(launch_pred_gemm(g, p->stream, prof(p, GEVO_KERNEL_LAYER_FWD)));
+    }
+  }
+  return GEVO_OK;
+}
+
 template <typename S>
 gevo_status do_predict(gevo_pop* p) {
   const Layout& y = p->y;
   HIP_TRY(hipEventRecord(p->ev0, p->stream));
   gevo_status stb = sync_masters(p);
   if (stb != GEVO_OK) return stb;
+  bool gemm = false;
+  if constexpr (std::is_same<S, uint16_t>::value) {
+    for (int l = 0; l + 1 < y.L; ++l) gemm = gemm || y.lay[l].pred;
+    if (gemm && !p->wbf_valid) {                      // bf16 weight copies, once per change of the masters
+      for (int l = 0; l + 1 < y.L; ++l) {
+        const LayerLay& q = y.lay[l];
+        if (q.pred)
+          HIP_TRY(launch_wt_bf16(at<float>(p, q.Wm), at<uint16_t>(p, q.wbf), y.P, q.Kp, q.Np, p->stream,
+                                 prof(p, GEVO_KERNEL_WEIGHT_COPY)));
+      }
+      p->wbf_valid = true;
+    }
+  }
   const size_t Kp1 = (size_t)y.lay[0].Kp;
   for (int c0 = 0; c0 < y.n_test_pad; c0 += kPredictChunk) {
     const int R = (y.n_test_pad - c0) < kPredictChunk ? (y.n_test_pad - c0) : kPredictChunk;
     const S* xr = reinterpret_cast<const S*>(p->ws + y.xte) + (size_t)c0 * Kp1;
-    if (y.L > 1) {
+    if constexpr (std::is_same<S, uint16_t>::value) {
+      if (gemm) {
+        bool out_done = false;
+        gevo_status st = predict_chunk_gemm(p, xr, c0, R, &out_done);
+        if (st != GEVO_OK) return st;
+        if (out_done) continue;
+      }
+    }
+    if (y.L > 1 && !gemm) {
       gevo_status st = forward_hidden<S>(p, xr, 0, R, 0, true);
       if (st != GEVO_OK) return st;
     }
@@ -911,6 +983,7 @@ gevo_status gevo_pop_set_genomes(gevo_pop* p, float lr_base, const uint32_t* off
   p->predicted = false;
   p->timing_pending = false;
   p->img_valid = false;                          // the register-image copies are stale
+  p->wbf_valid = false;
   p->blk_stale = false;
   return GEVO_OK;
 }
@@ -1035,6 +1108,7 @@ gevo_status gevo_pop_import(gevo_pop* p, uint32_t v, const float* params) {
   if (stb != GEVO_OK) return stb;
   HIP_TRY(hipStreamSynchronize(p->stream));
   p->img_valid = false;                               // the image is rebuilt from the imported master
+  p->wbf_valid = false;
   size_t off = 0;
   for (int l = 0; l < y.L; ++l) {
     const LayerLay& q = y.lay[l];

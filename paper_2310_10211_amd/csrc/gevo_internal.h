@@ -87,6 +87,25 @@ struct FwdGemmArgs {
   int Kp, Np, R, P;
 };
 
+// bf16 prediction GEMM of a hidden layer (gevo_predict.hip): per variant
+// O = bf16(relu(A W + b)) over R rows, W the bf16 operand copy; with WL set,
+// the layer (Np == 256) is the last hidden one and its tile also runs the
+// output layer, writing per-tile loss sums and hit counts instead of O
+struct PredGemmArgs {
+  const uint16_t* A; size_t a_vs;   // [v][R][Kp] input rows (a_vs = 0: shared by all variants)
+  const uint16_t* W;                // [P][Np][Kp] bf16 weights
+  const float* bias;                // [P][Np]
+  uint16_t* O; size_t o_vs;         // [v][R][Np] relu output rows (unused with WL)
+  int Kp, Np, R, P;
+  const float* WL;                  // output layer master [P][Np/32][32][32] (k-blocked), or null
+  const float* bL;                  // [P][32]
+  int C;                            // classes
+  const int32_t* labels;            // [R] labels of the chunk's rows, < 0 for padding rows
+  int chunk0, n_chunks_total;       // partial sums at [v][chunk0 + row tile]
+  double* part_ce;
+  unsigned int* part_correct;
+};
+
 template <typename S>
 struct OutArgs {
   int Kp;                        // padded width of the last hidden layer (input of the output layer)
@@ -184,6 +203,10 @@ hipError_t launch_mask_block_major(const uint32_t* src, uint32_t* dst, int P, in
 hipError_t launch_bf16_check(unsigned long long* counts, hipStream_t s);   // counts zeroed by the caller
 bool fwd_gemm_supported(int Kp, int Np, int R);   // Kp % 32, Np % 128, R % 256
 hipError_t launch_fwd_gemm(const FwdGemmArgs& a, hipStream_t s, const LaunchEv& ev);
+bool pred_gemm_supported(int Kp, int Np, int R);  // Kp % 32, Np % 256, R % 256
+hipError_t launch_pred_gemm(const PredGemmArgs& a, hipStream_t s, const LaunchEv& ev);
+// k-blocked fp32 master [P][Kp/32][Np][32] -> bf16 [P][Np][Kp] (Np % 256 == 0)
+hipError_t launch_wt_bf16(const float* Wm, uint16_t* Wb, int P, int Kp, int Np, hipStream_t s, const LaunchEv& ev);
 // bf16 hidden layer over one training batch (update and/or forward of the
 // next batch) streaming the fp32 master once; shapes outside these use k_layer
 bool stream_layer_supported(int Kp, int Np, int Bp, int R);

@@ -1,0 +1,346 @@
+// Prediction workload (paper section 4.3: a model is run over the dataset and
+// its error recorded) for bf16 nets: every hidden layer of every variant is a
+// plain GEMM over a chunk of test rows,
+//   O_v = bf16(relu(A_v W_v + b_v)),
+// with W_v a bf16 copy of the fp32 master rounded once per prediction call.
+// When the last hidden layer is exactly one column tile wide, its GEMM also
+// runs the output layer: logits, softmax cross-entropy, argmax (lowest index
+// on ties, a NaN logit is a miss) and the tile's loss and hit sums, so the
+// last hidden activations never leave the chip.
+//
+// One workgroup (four waves, one per SIMD) computes a 256-row x 256-unit tile
+// of one variant; the waves form a 2 x 2 grid of 128 x 128 tiles of 32x32x16
+// MFMAs (sixteen accumulator tiles, 256 accumulator registers per lane).  The
+// contraction runs over 64-wide blocks (zero-filled past the input width),
+// double-buffered in LDS; the next block's
+// loads are issued right after the barrier and land in registers while the
+// current block is multiplied.  Input rows and weights are both stored with
+// the contraction index contiguous ([row][k] and [unit][k]), so both operand
+// tiles load and read alike.  Workgroups that share a weight tile (same
+// variant, all row tiles) get consecutive dispatch slots on one XCD
+// (workgroup i runs on XCD i mod 8).
+#include "gevo_internal.h"
+#include "gevo_device.h"
+
+#include <hip/hip_ext.h>
+#include <math.h>
+
+#include <type_traits>
+
+namespace gevo {
+
+namespace {
+
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kPM = 256;                 // rows per tile
+constexpr int kPN = 256;                 // units per tile
+constexpr int kPK = 64;                  // contraction per block
+constexpr int kPS = kPK + 8;             // LDS row stride (bf16) of both operand tiles: 144 B
+constexpr int kPT = 256;                 // threads
+constexpr size_t kTileBytes = (size_t)kPM * kPS * 2;
+constexpr size_t kGemmLds = 4 * kTileBytes;            // A and W tiles, two buffers each
+// output-layer epilogue: hidden tile [256][kHS] bf16, W_L operand [32][kHS] bf16, biases
+constexpr int kHS = kPN + 8;
+constexpr size_t kOutH = 0;
+constexpr size_t kOutW = kOutH + (size_t)kPM * kHS * 2;
+constexpr size_t kOutB = kOutW + (size_t)32 * kHS * 2;
+constexpr size_t kOutRed = kOutB + 32 * 4;             // [4] fp64 loss sums, [4] hit counts
+constexpr size_t kOutEnd = kOutRed + 4 * 8 + 4 * 4;
+// the output epilogue reuses (and extends) the operand buffers
+constexpr size_t kGemmOutLds = kOutEnd > kGemmLds ? kOutEnd : kGemmLds;
+static_assert(kGemmOutLds <= 160 * 1024, "LDS of one CU");
+
+__device__ __forceinline__ f32x16_t mma32(u32x4_t a, u32x4_t b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c,
+                                                 0, 0, 0);
+}
+
+}  // namespace
+
+template <bool OUT>
+__global__ __launch_bounds__(kPT, 1) void k_pred_gemm(PredGemmArgs a) {
+  extern __shared__ __align__(16) char smem[];
+  const int nr = a.R / kPM, nn = a.Np / kPN;
+  const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3;
+  const int p = (j / nr) * 8 + xcd, rt = j % nr;
+  if (p >= a.P * nn) return;
+  const int v = p / nn, n0 = (p % nn) * kPN, r0 = rt * kPM;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, lh = lane >> 5;
+  const int wm = wave & 1, wn = wave >> 1;           // 128-row band, 128-unit band
+  const int Kp = a.Kp;
+  const int nblk = (Kp + kPK - 1) / kPK;
+  const uint16_t* A = a.A + a.a_vs * v + (size_t)r0 * Kp;
+  const uint16_t* W = a.W + ((size_t)v * a.Np + n0) * Kp;
+
+  // staging: thread chunk c = tid + 256 u covers row c / 8, 16 bytes c % 8 of
+  // the block; chunks past the input width (the second half of a 32-wide last
+  // block) are zeros, so every block runs the same four contraction steps
+  u32x4_t sa[8], sw[8];
+  auto load = [&](int kb) {
+    const int k = kb * kPK + (tid & 7) * 8;
+    const bool in = k < Kp;
+    const int kc = in ? k : 0;                       // past the width: an in-bounds read, replaced by zeros
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const size_t off = (size_t)((tid >> 3) + 32 * u) * Kp + kc;
+      sa[u] = *reinterpret_cast<const u32x4_t*>(A + off);
+      sw[u] = *reinterpret_cast<const u32x4_t*>(W + off);
+    }
+    if (!in) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) sa[u] = sw[u] = u32x4_t{0u, 0u, 0u, 0u};
+    }
+  };
+  auto store = [&](int buf) {
+    uint16_t* as = reinterpret_cast<uint16_t*>(smem + (size_t)buf * 2 * kTileBytes);
+    uint16_t* ws = reinterpret_cast<uint16_t*>(smem + (size_t)buf * 2 * kTileBytes + kTileBytes);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int row = (tid >> 3) + 32 * u, q = tid & 7;
+      *reinterpret_cast<u32x4_t*>(as + row * kPS + q * 8) = sa[u];
+      *reinterpret_cast<u32x4_t*>(ws + row * kPS + q * 8) = sw[u];
+    }
+  };
+
+  f32x16_t acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[i][t] = zero16();
+
+  auto compute = [&](int buf) {
+    const uint16_t* as = reinterpret_cast<const uint16_t*>(smem + (size_t)buf * 2 * kTileBytes);
+    const uint16_t* ws = reinterpret_cast<const uint16_t*>(smem + (size_t)buf * 2 * kTileBytes + kTileBytes);
+#pragma unroll
+    for (int s = 0; s < kPK / 16; ++s) {
+      u32x4_t af[4], bf[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        af[i] = *reinterpret_cast<const u32x4_t*>(as + (wm * 128 + i * 32 + l32) * kPS + 16 * s + 8 * lh);
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        bf[t] = *reinterpret_cast<const u32x4_t*>(ws + (wn * 128 + t * 32 + l32) * kPS + 16 * s + 8 * lh);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) acc[i][t] = mma32(af[i], bf[t], acc[i][t]);
+    }
+  };
+
+  // block kb is staged from registers into buffer kb & 1 after block kb - 1 is
+  // multiplied; one barrier per block both publishes it and retires the reads
+  // of the buffer the next staging overwrites
+  load(0);
+  store(0);
+  __syncthreads();
+  if (nblk > 1) load(1);
+  for (int kb = 0; kb < nblk; ++kb) {
+    compute(kb & 1);
+    if (kb + 1 < nblk) {
+      store((kb + 1) & 1);
+      __syncthreads();
+      if (kb + 2 < nblk) load(kb + 2);
+    }
+  }
+
+  if constexpr (!OUT) {
+    // bias, ReLU, bf16; lane holds unit l32 of a 32-unit tile and rows crow(r) of a 32-row tile
+    uint16_t* Out = a.O + a.o_vs * v;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int n = n0 + wn * 128 + t * 32 + l32;
+      const float bn = a.bias[(size_t)v * a.Np + n];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float f[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float z = acc[i][t][r] + bn;
+          f[r] = z > 0.0f ? z : 0.0f;
+        }
+        uint32_t pk[8];
+        to_bf16x2(f, pk);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = r0 + wm * 128 + i * 32 + crow(r, lane);
+          Out[(size_t)row * a.Np + n] = (uint16_t)(pk[r >> 1] >> (16 * (r & 1)));
+        }
+      }
+    }
+  } else {
+    // The layer is one tile wide (Np == 256): the tile holds whole rows of
+    // the last hidden activation.  H = bf16(relu(Z + b)) goes to LDS as
+    // [row][unit]; the output layer's weights as the bf16 operand [class][unit].
+    __syncthreads();                                   // every wave is done with the operand buffers
+    uint16_t* H = reinterpret_cast<uint16_t*>(smem + kOutH);
+    uint16_t* WL = reinterpret_cast<uint16_t*>(smem + kOutW);
+    float* bL = reinterpret_cast<float*>(smem + kOutB);
+    double* red_ce = reinterpret_cast<double*>(smem + kOutRed);
+    unsigned int* red_hit = reinterpret_cast<unsigned int*>(smem + kOutRed + 4 * 8);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int n = wn * 128 + t * 32 + l32;
+      const float bn = a.bias[(size_t)v * a.Np + n];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float f[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float z = acc[i][t][r] + bn;
+          f[r] = z > 0.0f ? z : 0.0f;
+        }
+        uint32_t pk[8];
+        to_bf16x2(f, pk);
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          H[(wm * 128 + i * 32 + crow(r, lane)) * kHS + n] = (uint16_t)(pk[r >> 1] >> (16 * (r & 1)));
+      }
+    }
+    // output layer master, k-blocked [Np/32][32 classes][32 inputs]: thread tid
+    // converts class tid / 8, inputs 32 (tid % 8) .. +31
+    {
+      const float* WLm = a.WL + (size_t)v * 32 * kPN;
+      const int c = tid >> 3, kb = tid & 7;
+      const float* src = WLm + ((size_t)kb * 32 + c) * 32;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 f0 = *reinterpret_cast<const float4*>(src + 8 * q);
+        const float4 f1 = *reinterpret_cast<const float4*>(src + 8 * q + 4);
+        const float f[8] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w};
+        uint32_t pk[4];
+        to_bf16x2(f, pk);
+        *reinterpret_cast<u32x4_t*>(WL + c * kHS + kb * 32 + 8 * q) = u32x4_t{pk[0], pk[1], pk[2], pk[3]};
+      }
+      if (tid < 32) bL[tid] = a.bL[(size_t)v * 32 + tid];
+    }
+    __syncthreads();
+    // logits^T of 32 rows per tile: lane holds row l32 and classes crow(r) of
+    // its half; the row's other half is in lane ^ 32
+    const int C = a.C;
+    double ce_sum = 0.0;
+    unsigned int hits = 0;
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) {
+      const int rl = wave * 64 + tt * 32;            // first row of the tile (in the workgroup)
+      f32x16_t z0 = zero16(), z1 = zero16();
+#pragma unroll
+      for (int s = 0; s < kPN / 16; s += 2) {
+        z0 = mma32(*reinterpret_cast<const u32x4_t*>(WL + l32 * kHS + 16 * s + 8 * lh),
+                   *reinterpret_cast<const u32x4_t*>(H + (rl + l32) * kHS + 16 * s + 8 * lh), z0);
+        z1 = mma32(*reinterpret_cast<const u32x4_t*>(WL + l32 * kHS + 16 * s + 16 + 8 * lh),
+                   *reinterpret_cast<const u32x4_t*>(H + (rl + l32) * kHS + 16 * s + 16 + 8 * lh), z1);
+      }
+      const int y = a.labels[r0 + rl + l32];
+      float z[16];
+      float m = -INFINITY, bv = -INFINITY;
+      int bi = 64, nanl = 0;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {                 // r ascending = class ascending within the lane
+        const int c = crow(r, lane);
+        z[r] = (z0[r] + z1[r]) + bL[c];
+        if (c < C) {
+          m = fmaxf(m, z[r]);
+          if (z[r] != z[r]) nanl = 1;
+          else if (z[r] > bv) { bv = z[r]; bi = c; }
+        }
+      }
+      m = fmaxf(m, __shfl_xor(m, 32));
+      nanl |= __shfl_xor(nanl, 32);
+      {
+        const float ov = __shfl_xor(bv, 32);
+        const int oi = __shfl_xor(bi, 32);
+        if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+      }
+      float sl = 0.0f, zy = 0.0f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int c = crow(r, lane);
+        if (c < C) sl += expf(z[r] - m);
+        if (c == y) zy = z[r];
+      }
+      const float s = sl + __shfl_xor(sl, 32);
+      zy += __shfl_xor(zy, 32);                      // exactly one lane of the pair holds class y
+      float ce = (logf(s) + m) - zy;
+      if (nanl) ce = NAN;
+      if (lh == 0 && y >= 0) {
+        ce_sum += (double)ce;
+        hits += (!nanl && bi == y) ? 1u : 0u;
+      }
+    }
+#pragma unroll
+    for (int off = 16; off >= 1; off >>= 1) {        // lanes 0..31 hold the rows; fixed order
+      ce_sum += __shfl_xor(ce_sum, off);
+      hits += __shfl_xor(hits, off);
+    }
+    if (lane == 0) { red_ce[wave] = ce_sum; red_hit[wave] = hits; }
+    __syncthreads();
+    if (tid == 0) {
+      double t = 0.0;
+      unsigned int h = 0;
+      for (int w = 0; w < 4; ++w) { t += red_ce[w]; h += red_hit[w]; }
+      a.part_ce[(size_t)v * a.n_chunks_total + a.chunk0 + rt] = t;
+      a.part_correct[(size_t)v * a.n_chunks_total + a.chunk0 + rt] = h;
+    }
+  }
+}
+
+// bf16 operand copy of a hidden layer's master: from the k-blocked fp32
+// master [P][Kp/32][Np][32] to [P][Np][Kp], one workgroup per (variant,
+// 32-input block, 256 units); thread t converts unit t's 32 inputs.
+__global__ __launch_bounds__(256) void k_wt_bf16(const float* __restrict__ Wm, uint16_t* __restrict__ Wb, int Kp,
+                                                 int Np) {
+  const int nkb = Kp / 32, ntile = Np / 256;
+  const int64_t b = blockIdx.x;
+  const int v = (int)(b / ((int64_t)nkb * ntile)), rem = (int)(b % ((int64_t)nkb * ntile));
+  const int kb = rem / ntile, n = (rem % ntile) * 256 + threadIdx.x;
+  const float* src = Wm + (((size_t)v * nkb + kb) * Np + n) * 32;
+  uint16_t* dst = Wb + ((size_t)v * Np + n) * Kp + kb * 32;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float4 f0 = *reinterpret_cast<const float4*>(src + 8 * q);
+    const float4 f1 = *reinterpret_cast<const float4*>(src + 8 * q + 4);
+    const float f[8] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w};
+    uint32_t pk[4];
+    to_bf16x2(f, pk);
+    *reinterpret_cast<u32x4_t*>(dst + 8 * q) = u32x4_t{pk[0], pk[1], pk[2], pk[3]};
+  }
+}
+
+bool pred_gemm_supported(int Kp, int Np, int R) {
+  return Kp % 32 == 0 && Kp > 0 && Np % kPN == 0 && R % kPM == 0 && R > 0;
+}
+
+hipError_t launch_wt_bf16(const float* Wm, uint16_t* Wb, int P, int Kp, int Np, hipStream_t s, const LaunchEv& ev) {
+  if (Kp % 32 || Np % 256 || P <= 0) return hipErrorInvalidValue;
+  const int64_t blocks = (int64_t)P * (Kp / 32) * (Np / 256);
+  hipExtLaunchKernelGGL(k_wt_bf16, dim3((unsigned)blocks), dim3(256), 0, s, ev.start, ev.stop, 0, Wm, Wb, Kp, Np);
+  return hipGetLastError();
+}
+
+template <bool OUT>
+static hipError_t launch_pg(const PredGemmArgs& a, hipStream_t s, const LaunchEv& ev) {
+  constexpr size_t lds = OUT ? kGemmOutLds : kGemmLds;
+  static bool attr = false;
+  if (!attr) {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pred_gemm<OUT>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    attr = true;
+  }
+  const int64_t pairs = (int64_t)a.P * (a.Np / kPN);
+  const int64_t slots = (pairs + 7) / 8 * 8 * (a.R / kPM);
+  hipExtLaunchKernelGGL((k_pred_gemm<OUT>), dim3((unsigned)slots), dim3(kPT), lds, s, ev.start, ev.stop, 0, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_pred_gemm(const PredGemmArgs& a, hipStream_t s, const LaunchEv& ev) {
+  if (!pred_gemm_supported(a.Kp, a.Np, a.R)) return hipErrorInvalidValue;
+  if (a.WL) {
+    if (a.Np != kPN || a.C < 1 || a.C > 32 || !a.bL || !a.labels || !a.part_ce || !a.part_correct)
+      return hipErrorInvalidValue;
+    return launch_pg<true>(a, s, ev);
+  }
+  return launch_pg<false>(a, s, ev);
+}
+
+}  // namespace gevo

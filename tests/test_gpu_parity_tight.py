@@ -1,8 +1,8 @@
 """Tighter GPU parity: element-wise single steps of every training kernel,
 per-sample prediction, and the argmax tie and NaN-logit rules on the GPU.
 
-* One SGD step from an imported state, weights and biases element by element
-  against the oracle in bf16 mode, for nets whose hidden layers train in the
+* One SGD step from an imported state, weight and bias updates element by
+  element against the oracle in bf16 mode (bounds derived in _check_update), for nets whose hidden layers train in the
   streaming kernel (with the backward GEMM and the output kernel), including
   the full 3072-1024-512-10 width, and for the fused two-layer kernel at
   variants whose column blocks are visited in rotated order.
@@ -48,20 +48,37 @@ def _data(i, n_train, n_test, dims):
     return d
 
 
+def _check_update(dg, dr, what):
+    """One step's update (GPU dg, oracle dr), element by element.
+
+    Both sides round the same operands to bf16; the GPU sums them in fp32 in
+    its own order, the oracle exactly, so an operand whose two sums straddle a
+    bf16 rounding boundary rounds one ulp apart (2^-8 to 2^-7 of it).  Such a
+    flip moves one row or column of the update by one term's ulp, so:
+      * median relative error over the elements above 1% of the largest
+        update <= 2e-4 (a rounding point missing or misplaced on either side
+        gives about 1e-3 on most elements; fp32 summation gives about 1e-7);
+      * every element within 1e-2 of the largest update (about 2.5 bf16 ulps
+        of the largest term)."""
+    scale = max(float(np.max(np.abs(dr))), 1e-30)
+    diff = np.abs(dg - dr)
+    big = np.abs(dr) > 1e-2 * scale
+    med = float(np.median(diff[big] / np.abs(dr[big]))) if np.any(big) else 0.0
+    info = (what, "max", float(np.max(diff)) / scale, "median rel", med, "elements over 1e-3 of max",
+            int(np.sum(diff > 1e-3 * scale)), "of", diff.size)
+    assert med <= 2e-4, info
+    assert float(np.max(diff)) <= 1e-2 * scale, info
+
+
 def _compare_step(got, want, before, dims, what):
-    """Weights and biases after one step: the update W_after - W_before element
-    by element within 2e-3 of the layer's largest update (plus the
-    parameters themselves within 1e-5 of the largest weight)."""
+    """Weights and biases after one step from the same imported state: the
+    updates W_after - W_before (see _check_update), and the parameters
+    themselves within 1e-5 of the layer's largest weight."""
     for l, ((Wg, bg), (Wr, br), (W0, b0)) in enumerate(zip(oracle.unpack(got, dims), oracle.unpack(want, dims),
                                                           oracle.unpack(before, dims))):
-        dg, dr = Wg - W0, Wr - W0
-        scale = max(np.max(np.abs(dr)), 1e-30)
-        err = np.max(np.abs(dg - dr))
-        assert err <= 2e-3 * scale, (what, "layer", l + 1, "weight update", err, scale)
+        _check_update(Wg - W0, Wr - W0, f"{what} layer {l + 1} weights")
+        _check_update(bg - b0, br - b0, f"{what} layer {l + 1} biases")
         assert np.max(np.abs(Wg - Wr)) <= 1e-5 * max(np.max(np.abs(Wr)), 1e-30), (what, l + 1)
-        dbg, dbr = bg - b0, br - b0
-        bscale = max(np.max(np.abs(dbr)), 1e-30)
-        assert np.max(np.abs(dbg - dbr)) <= 2e-3 * bscale, (what, "layer", l + 1, "bias update")
 
 
 def _one_step_case(cfg, data, variants, seed=5):
