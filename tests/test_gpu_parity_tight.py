@@ -72,13 +72,13 @@ def _check_update(dg, dr, what):
 
 def _compare_step(got, want, before, dims, what):
     """Weights and biases after one step from the same imported state: the
-    updates W_after - W_before (see _check_update), and the parameters
-    themselves within 1e-5 of the layer's largest weight."""
+    updates W_after - W_before (see _check_update); the state before the step
+    is identical on both sides, so the parameters differ exactly by the
+    difference of the updates."""
     for l, ((Wg, bg), (Wr, br), (W0, b0)) in enumerate(zip(oracle.unpack(got, dims), oracle.unpack(want, dims),
                                                           oracle.unpack(before, dims))):
         _check_update(Wg - W0, Wr - W0, f"{what} layer {l + 1} weights")
         _check_update(bg - b0, br - b0, f"{what} layer {l + 1} biases")
-        assert np.max(np.abs(Wg - Wr)) <= 1e-5 * max(np.max(np.abs(Wr)), 1e-30), (what, l + 1)
 
 
 def _one_step_case(cfg, data, variants, seed=5):
