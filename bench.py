@@ -63,6 +63,9 @@ def parse():
                     help="time G generations of the search loop on this workload instead")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy 3 times (reference for HBM counters) and exit")
+    ap.add_argument("--mfma-from", metavar="DIR",
+                    help="only summarise a rocprofv3 --pmc run of the MFMA counters (SQ_VALU_MFMA_BUSY_CYCLES, "
+                         "SQ_INSTS_VALU_MFMA_MOPS_BF16/_F32, GRBM_GUI_ACTIVE, ...) as a markdown table and exit")
     ap.add_argument("--traffic-from", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
                     help="only fold rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs of this workload and of "
                          "--calibrate-copy into profiles/traffic_counters.json and exit")
@@ -354,6 +357,51 @@ def traffic_for(kernel, workload, sources=None):
     return rec.get("hbm_bytes_per_launch")
 
 
+N_SIMD = 1024                                 # 256 CUs x 4 SIMDs
+N_XCD = 8
+MOP_FLOPS = 512                                # flops per MFMA "MOP" (SQ_INSTS_VALU_MFMA_MOPS_*)
+
+
+def mfma_summary(d):
+    """Per kernel of a rocprofv3 --pmc run: dispatches, cycles per dispatch
+    (the dispatch timestamps), GPU clock (GRBM_GUI_ACTIVE, summed over the 8
+    XCDs, over that time), MFMA busy fraction
+    (SQ_VALU_MFMA_BUSY_CYCLES over all SIMD-cycles), MFMA flops per dispatch
+    (MOPS x 512, padding included) and their rate at the measured cycles."""
+    import collections
+    import csv
+    import glob
+    acc = collections.defaultdict(lambda: collections.defaultdict(float))
+    n = collections.Counter()
+    dur = collections.defaultdict(float)
+    for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                k = r["Kernel_Name"].split("(")[0].replace("void ", "").replace("gevo::", "")
+                acc[k][r["Counter_Name"]] += float(r["Counter_Value"])
+                if r["Counter_Name"] == "GRBM_GUI_ACTIVE":
+                    n[k] += 1
+                    dur[k] += (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9
+    lines = ["| Kernel | Dispatches | us per dispatch | GPU clock (GHz) | MFMA busy | MFMA TFLOP/s (bf16) | "
+             "MFMA TFLOP/s (fp32) | LDS bank conflicts per LDS instruction |",
+             "|---|---:|---:|---:|---:|---:|---:|---:|"]
+    for k, v in sorted(acc.items(), key=lambda kv: -kv[1].get("GRBM_GUI_ACTIVE", 0.0)):
+        if not n[k] or v.get("GRBM_GUI_ACTIVE", 0) <= 0 or dur[k] <= 0:
+            continue
+        cyc = v["GRBM_GUI_ACTIVE"] / N_XCD / n[k]
+        t = dur[k] / n[k]
+        busy = v.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / n[k] / (N_SIMD * cyc)
+        bf = v.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) * MOP_FLOPS / n[k] / t / 1e12
+        f32 = v.get("SQ_INSTS_VALU_MFMA_MOPS_F32", 0.0) * MOP_FLOPS / n[k] / t / 1e12
+        lds = v.get("SQ_INSTS_LDS", 0.0)
+        conf = v.get("SQ_LDS_BANK_CONFLICT", 0.0) / lds if lds else 0.0
+        if busy < 1e-4 and cyc < 1e5:
+            continue
+        lines.append(f"| {k} | {n[k]} | {t * 1e6:,.1f} | {cyc / t / 1e9:.2f} | {100 * busy:.1f}% | {bf:,.1f} | "
+                     f"{f32:,.1f} | {conf:.3f} |")
+    return "\n".join(lines)
+
+
 # ------------------------------------------------------------------ CPU oracle
 def host_threads():
     """(threads to use, CPUs this process may run on): the machine's CPU share
@@ -410,6 +458,9 @@ def main():
 
     if args.calibrate_copy:
         calibrate_copy()
+        return
+    if args.mfma_from:
+        print(mfma_summary(args.mfma_from))
         return
     if args.traffic_from and args.cnn:
         import synthetic
