@@ -314,11 +314,11 @@ LaunchEv prof(gevo_pop* p, int kind) {
     if ((x) != hipSuccess) return GEVO_E_HIP;   \
   } while (0)
 
-// forward of hidden layer l over R rows (layer 0 reads arows0; deeper layers
-// the previous layer's activations), training (outsel: activation buffer) or
-// prediction (the chunk buffers)
+// forward of hidden layer l over the R rows of a training batch (layer 0
+// reads arows0; deeper layers the previous layer's activations of buffer
+// outsel), writing the activations of buffer outsel in both orientations
 template <typename S>
-gevo_status forward_layer(gevo_pop* p, int l, const S* arows0, size_t ar0_vs, int R, int outsel, bool predict) {
+gevo_status forward_layer(gevo_pop* p, int l, const S* arows0, size_t ar0_vs, int R, int outsel) {
   const Layout& y = p->y;
   const LayerLay& q = y.lay[l];
   LayerArgs<S> a{};
@@ -329,25 +329,13 @@ gevo_status forward_layer(gevo_pop* p, int l, const S* arows0, size_t ar0_vs, in
   a.do_forward = 1;
   a.R = R;
   if (l == 0) { a.Arows = arows0; a.ar_vs = ar0_vs; }
-  else if (predict) { a.Arows = at<S>(p, y.lay[l - 1].prows); a.ar_vs = (size_t)kPredictChunk * y.lay[l - 1].Np; }
   else { a.Arows = at<S>(p, y.lay[l - 1].arows[outsel]); a.ar_vs = (size_t)y.Bp * y.lay[l - 1].Np; }
-  if (predict) {
-    a.Orows = at<S>(p, q.prows); a.or_vs = (size_t)kPredictChunk * q.Np;
-  } else {
-    a.Orows = at<S>(p, q.arows[outsel]); a.or_vs = (size_t)y.Bp * q.Np;
-    a.Ocols = at<S>(p, q.acols[outsel]); a.oc_vs = (size_t)q.Np * y.Bp;
-    if (q.Wt) a.Wt = at<S>(p, q.Wt);
-  }
+  a.Orows = at<S>(p, q.arows[outsel]); a.or_vs = (size_t)y.Bp * q.Np;
+  a.Ocols = at<S>(p, q.acols[outsel]); a.oc_vs = (size_t)q.Np * y.Bp;
+  if (q.Wt) a.Wt = at<S>(p, q.Wt);
   if (a.Kp % kTile || a.Np % kTile || a.R % kTile || a.R <= 0) return GEVO_E_SHAPE;
   if constexpr (std::is_same<S, uint16_t>::value) {
-    if (predict && fwd_gemm_supported(a.Kp, a.Np, a.R)) {      // plain per-variant GEMM, no update
-      FwdGemmArgs g{};
-      g.A = a.Arows; g.a_vs = a.ar_vs; g.Wm = a.Wm; g.bias = a.bias; g.O = a.Orows; g.o_vs = a.or_vs;
-      g.Kp = a.Kp; g.Np = a.Np; g.R = a.R; g.P = y.P;
-      HIP_TRY(launch_fwd_gemm(g, p->stream, prof(p, GEVO_KERNEL_LAYER_FWD)));
-      return GEVO_OK;
-    }
-    if (!predict && q.streamed) {
+    if (q.streamed) {
       a.Wimg = at<float>(p, q.wimg); a.mblk = at<uint32_t>(p, q.mblk);
       HIP_TRY(launch_stream_layer(a, y.P, p->stream, prof(p, GEVO_KERNEL_LAYER_FWD)));
       return GEVO_OK;
@@ -358,9 +346,9 @@ gevo_status forward_layer(gevo_pop* p, int l, const S* arows0, size_t ar0_vs, in
 }
 
 template <typename S>
-gevo_status forward_hidden(gevo_pop* p, const S* arows0, size_t ar0_vs, int R, int outsel, bool predict) {
+gevo_status forward_hidden(gevo_pop* p, const S* arows0, size_t ar0_vs, int R, int outsel) {
   for (int l = 0; l < p->y.L - 1; ++l) {
-    gevo_status st = forward_layer<S>(p, l, arows0, ar0_vs, R, outsel, predict);
+    gevo_status st = forward_layer<S>(p, l, arows0, ar0_vs, R, outsel);
     if (st != GEVO_OK) return st;
   }
   return GEVO_OK;
@@ -391,7 +379,7 @@ gevo_status begin_epoch(gevo_pop* p, int e) {
   HIP_TRY(launch_zero_bytes(p->ws + y.train_corr, (size_t)y.P * 8, p->stream, prof(p, GEVO_KERNEL_AUX)));
   // forward of step 0 for the hidden layers (the fused kernel does its own)
   if (y.L > 1 && !y.fused) {
-    gevo_status st = forward_hidden<S>(p, at<S>(p, y.xrows), 0, y.Bp, 0, false);
+    gevo_status st = forward_hidden<S>(p, at<S>(p, y.xrows), 0, y.Bp, 0);
     if (st != GEVO_OK) return st;
   }
   p->rows_done = 0;
@@ -517,19 +505,19 @@ gevo_status sync_images(gevo_pop* p) {
   return GEVO_OK;
 }
 
-gevo_status sync_masters(gevo_pop* p) {
+gevo_status sync_masters(gevo_pop* p, bool profile = true) {
   const Layout& y = p->y;
   if (!y.images || !p->blk_stale) return GEVO_OK;
   if (y.fused) {
     const LayerLay& q = y.lay[0];
     HIP_TRY(launch_w1_image(at<float>(p, y.w1img), at<float>(p, q.Wm), y.P, q.Kp, q.Np, false, p->stream,
-                            prof(p, GEVO_KERNEL_AUX)));
+                            profile ? prof(p, GEVO_KERNEL_AUX) : LaunchEv{}));
   }
   for (int l = 0; l + 1 < y.L; ++l) {
     const LayerLay& q = y.lay[l];
     if (!q.streamed) continue;
     HIP_TRY(launch_w1_image(at<float>(p, q.wimg), at<float>(p, q.Wm), y.P, q.Kp, q.Np, false, p->stream,
-                            prof(p, GEVO_KERNEL_AUX)));
+                            profile ? prof(p, GEVO_KERNEL_AUX) : LaunchEv{}));
   }
   p->blk_stale = false;
   return GEVO_OK;
@@ -598,38 +586,125 @@ gevo_status do_train_steps(gevo_pop* p, uint32_t epoch, uint32_t s0, uint32_t s1
   return GEVO_OK;
 }
 
-// bf16 prediction of one chunk through k_pred_gemm: every hidden layer with
-// a bf16 weight copy runs as a plain GEMM (other shapes as in forward_hidden);
-// a last hidden layer of exactly one column tile also runs the output layer.
-// Returns whether the output layer was fused (the caller then skips k_out).
-gevo_status predict_chunk_gemm(gevo_pop* p, const uint16_t* xr, int c0, int R, bool* out_done) {
+// Scratch and variant range of one prediction pass: variants [v0, v0 + G);
+// per hidden layer the chunk activations act[l] ([G][kPredictChunk][Np]
+// operands) and the bf16 weight copy wbf[l] ([G][Np][Kp], null when the layer
+// does not run on the prediction GEMM); the partial sums [G][n_chunks_test].
+// gevo_pop_predict takes them from the workspace.
+struct PredictBufs {
+  int v0 = 0, G = 0;
+  void* act[GEVO_MAX_LAYERS] = {};
+  uint16_t* wbf[GEVO_MAX_LAYERS] = {};
+  bool convert = true;             // write the bf16 weight copies first
+  double* part_ce = nullptr;
+  unsigned int* part_corr = nullptr;
+  bool profile = true;             // per-kernel timing events (they may be created on first use)
+};
+
+LaunchEv pev(gevo_pop* p, const PredictBufs& b, int kind) { return b.profile ? prof(p, kind) : LaunchEv{}; }
+
+// forward of hidden layer l of variants [v0, v0 + G) over R prediction rows
+template <typename S>
+gevo_status predict_layer(gevo_pop* p, const PredictBufs& b, int l, const S* arows, size_t ar_vs, int R) {
   const Layout& y = p->y;
-  *out_done = false;
-  for (int l = 0; l < y.L - 1; ++l) {
-    const LayerLay& q = y.lay[l];
-    const uint16_t* ain = l == 0 ? xr : at<uint16_t>(p, y.lay[l - 1].prows);
-    const size_t a_vs = l == 0 ? 0 : (size_t)kPredictChunk * y.lay[l - 1].Np;
-    if (!q.pred || !pred_gemm_supported(q.Kp, q.Np, R)) {
-      gevo_status st = forward_layer<uint16_t>(p, l, xr, 0, R, 0, true);
-      if (st != GEVO_OK) return st;
-      continue;
+  const LayerLay& q = y.lay[l];
+  const size_t v0 = (size_t)b.v0;
+  LayerArgs<S> a{};
+  a.Kp = q.Kp; a.Np = q.Np; a.Bp = y.Bp;
+  a.Wm = at<float>(p, q.Wm) + v0 * q.Np * q.Kp; a.bias = at<float>(p, q.bias) + v0 * q.Np;
+  a.mask = at<uint32_t>(p, q.mask) + v0 * q.Np * (q.Kp / 32); a.bmask = at<uint32_t>(p, q.bmask) + v0 * (q.Np / 32);
+  a.lr = at<float>(p, y.lr) + v0;
+  a.do_update = 0;
+  a.do_forward = 1;
+  a.R = R;
+  a.Arows = arows; a.ar_vs = ar_vs;
+  a.Orows = static_cast<S*>(b.act[l]); a.or_vs = (size_t)kPredictChunk * q.Np;
+  if (a.Kp % kTile || a.Np % kTile || a.R % kTile || a.R <= 0) return GEVO_E_SHAPE;
+  if constexpr (std::is_same<S, uint16_t>::value) {
+    if (b.wbf[l] && pred_gemm_supported(q.Kp, q.Np, R)) {
+      PredGemmArgs g{};
+      g.A = arows; g.a_vs = ar_vs; g.W = b.wbf[l]; g.bias = a.bias; g.O = a.Orows; g.o_vs = a.or_vs;
+      g.Kp = q.Kp; g.Np = q.Np; g.R = R; g.P = b.G;
+      HIP_TRY(launch_pred_gemm(g, p->stream, pev(p, b, GEVO_KERNEL_LAYER_FWD)));
+      return GEVO_OK;
     }
-    PredGemmArgs g{};
-    g.A = ain; g.a_vs = a_vs; g.W = at<uint16_t>(p, q.wbf); g.bias = at<float>(p, q.bias);
-    g.Kp = q.Kp; g.Np = q.Np; g.R = R; g.P = y.P;
-    const LayerLay& o = y.lay[y.L - 1];
-    if (l == y.L - 2 && q.Np == 256 && o.Kp == 256) {          // last hidden layer, one tile wide
-      g.WL = at<float>(p, o.Wm); g.bL = at<float>(p, o.bias); g.C = o.N;
-      g.labels = at<int32_t>(p, y.yte) + c0;
-      g.chunk0 = c0 / kOutRows; g.n_chunks_total = y.n_chunks_test;
-      g.part_ce = at<double>(p, y.part_ce); g.part_correct = at<unsigned int>(p, y.part_corr);
-      HIP_TRY(launch_pred_gemm(g, p->stream, prof(p, GEVO_KERNEL_FWD_OUT)));
-      *out_done = true;
-    } else {
-      g.O = at<uint16_t>(p, q.prows); g.o_vs = (size_t)kPredictChunk * q.Np;
-      HIP_TRY(launch_pred_gemm(g, p->stream, prof(p, GEVO_KERNEL_LAYER_FWD)));
+    if (fwd_gemm_supported(a.Kp, a.Np, a.R)) {                 // plain per-variant GEMM, fp32 weights
+      FwdGemmArgs g{};
+      g.A = arows; g.a_vs = ar_vs; g.Wm = a.Wm; g.bias = a.bias; g.O = a.Orows; g.o_vs = a.or_vs;
+      g.Kp = a.Kp; g.Np = a.Np; g.R = a.R; g.P = b.G;
+      HIP_TRY(launch_fwd_gemm(g, p->stream, pev(p, b, GEVO_KERNEL_LAYER_FWD)));
+      return GEVO_OK;
     }
   }
+  HIP_TRY(launch_layer<S>(a, b.G, p->stream, pev(p, b, GEVO_KERNEL_LAYER_FWD)));
+  return GEVO_OK;
+}
+
+// One pass over the test split for variants [v0, v0 + G): hidden layers per
+// chunk (a last hidden layer of exactly one 256-unit tile on the prediction
+// GEMM also runs the output layer), the output layer otherwise, then the
+// per-variant sums of the chunks' partial sums into test_ce / test_corr.
+template <typename S>
+gevo_status predict_pass(gevo_pop* p, const PredictBufs& b) {
+  const Layout& y = p->y;
+  const size_t v0 = (size_t)b.v0;
+  if constexpr (std::is_same<S, uint16_t>::value) {
+    if (b.convert)
+      for (int l = 0; l + 1 < y.L; ++l) {
+        const LayerLay& q = y.lay[l];
+        if (b.wbf[l])
+          HIP_TRY(launch_wt_bf16(at<float>(p, q.Wm) + v0 * q.Np * q.Kp, b.wbf[l], b.G, q.Kp, q.Np, p->stream,
+                                 pev(p, b, GEVO_KERNEL_WEIGHT_COPY)));
+      }
+  }
+  const LayerLay& o = y.lay[y.L - 1];
+  const size_t Kp1 = (size_t)y.lay[0].Kp;
+  for (int c0 = 0; c0 < y.n_test_pad; c0 += kPredictChunk) {
+    const int R = (y.n_test_pad - c0) < kPredictChunk ? (y.n_test_pad - c0) : kPredictChunk;
+    const S* xr = reinterpret_cast<const S*>(p->ws + y.xte) + (size_t)c0 * Kp1;
+    bool fused = false;
+    for (int l = 0; l < y.L - 1; ++l) {
+      const LayerLay& q = y.lay[l];
+      const S* ain = l == 0 ? xr : static_cast<const S*>(b.act[l - 1]);
+      const size_t a_vs = l == 0 ? 0 : (size_t)kPredictChunk * y.lay[l - 1].Np;
+      if constexpr (std::is_same<S, uint16_t>::value) {
+        if (b.wbf[l] && l == y.L - 2 && q.Np == 256 && o.Kp == 256 && pred_gemm_supported(q.Kp, q.Np, R)) {
+          PredGemmArgs g{};                                      // last hidden layer, one tile wide
+          g.A = ain; g.a_vs = a_vs; g.W = b.wbf[l]; g.bias = at<float>(p, q.bias) + v0 * q.Np;
+          g.Kp = q.Kp; g.Np = q.Np; g.R = R; g.P = b.G;
+          g.WL = at<float>(p, o.Wm) + v0 * 32 * o.Kp; g.bL = at<float>(p, o.bias) + v0 * 32; g.C = o.N;
+          g.labels = at<int32_t>(p, y.yte) + c0;
+          g.chunk0 = c0 / kOutRows; g.n_chunks_total = y.n_chunks_test;
+          g.part_ce = b.part_ce; g.part_correct = b.part_corr;
+          HIP_TRY(launch_pred_gemm(g, p->stream, pev(p, b, GEVO_KERNEL_FWD_OUT)));
+          fused = true;
+          continue;
+        }
+      }
+      gevo_status st = predict_layer<S>(p, b, l, ain, a_vs, R);
+      if (st != GEVO_OK) return st;
+    }
+    if (fused) continue;
+    OutArgs<S> a{};
+    a.Kp = o.Kp; a.C = o.N; a.Bp = y.Bp;
+    a.Wm = at<float>(p, o.Wm) + v0 * 32 * o.Kp; a.bias = at<float>(p, o.bias) + v0 * 32;
+    a.mask = at<uint32_t>(p, o.mask) + v0 * 32 * (o.Kp / 32); a.bmask = at<uint32_t>(p, o.bmask) + v0;
+    a.lr = at<float>(p, y.lr) + v0;
+    a.train = 0;
+    if (y.L == 1) { a.Arows = xr; a.ar_vs = 0; }
+    else { a.Arows = static_cast<const S*>(b.act[y.L - 2]); a.ar_vs = (size_t)kPredictChunk * y.lay[y.L - 2].Np; }
+    a.labels = at<int32_t>(p, y.yte) + c0;
+    a.rows = R;
+    a.chunk0 = c0 / kOutRows;
+    a.n_chunks_total = y.n_chunks_test;
+    a.part_ce = b.part_ce;
+    a.part_correct = b.part_corr;
+    if (a.Kp % kTile || R % kOutRows) return GEVO_E_SHAPE;
+    HIP_TRY(launch_out<S>(a, b.G, p->stream, pev(p, b, GEVO_KERNEL_OUT_PREDICT)));
+  }
+  HIP_TRY(launch_reduce_partials(b.part_ce, b.part_corr, b.G, y.n_chunks_test, at<double>(p, y.test_ce) + v0,
+                                 at<unsigned long long>(p, y.test_corr) + v0, p->stream,
+                                 pev(p, b, GEVO_KERNEL_AUX)));
   return GEVO_OK;
 }
 
@@ -639,55 +714,23 @@ gevo_status do_predict(gevo_pop* p) {
   HIP_TRY(hipEventRecord(p->ev0, p->stream));
   gevo_status stb = sync_masters(p);
   if (stb != GEVO_OK) return stb;
-  bool gemm = false;
-  if constexpr (std::is_same<S, uint16_t>::value) {
-    for (int l = 0; l + 1 < y.L; ++l) gemm = gemm || y.lay[l].pred;
-    if (gemm && !p->wbf_valid) {                      // bf16 weight copies, once per change of the masters
-      for (int l = 0; l + 1 < y.L; ++l) {
-        const LayerLay& q = y.lay[l];
-        if (q.pred)
-          HIP_TRY(launch_wt_bf16(at<float>(p, q.Wm), at<uint16_t>(p, q.wbf), y.P, q.Kp, q.Np, p->stream,
-                                 prof(p, GEVO_KERNEL_WEIGHT_COPY)));
-      }
-      p->wbf_valid = true;
+  PredictBufs b;
+  b.v0 = 0;
+  b.G = y.P;
+  bool any_copy = false;
+  for (int l = 0; l + 1 < y.L; ++l) {
+    b.act[l] = p->ws + y.lay[l].prows;
+    if (y.lay[l].pred) {
+      b.wbf[l] = at<uint16_t>(p, y.lay[l].wbf);
+      any_copy = true;
     }
   }
-  const size_t Kp1 = (size_t)y.lay[0].Kp;
-  for (int c0 = 0; c0 < y.n_test_pad; c0 += kPredictChunk) {
-    const int R = (y.n_test_pad - c0) < kPredictChunk ? (y.n_test_pad - c0) : kPredictChunk;
-    const S* xr = reinterpret_cast<const S*>(p->ws + y.xte) + (size_t)c0 * Kp1;
-    if constexpr (std::is_same<S, uint16_t>::value) {
-      if (gemm) {
-        bool out_done = false;
-        gevo_status st = predict_chunk_gemm(p, xr, c0, R, &out_done);
-        if (st != GEVO_OK) return st;
-        if (out_done) continue;
-      }
-    }
-    if (y.L > 1 && !gemm) {
-      gevo_status st = forward_hidden<S>(p, xr, 0, R, 0, true);
-      if (st != GEVO_OK) return st;
-    }
-    const LayerLay& q = y.lay[y.L - 1];
-    OutArgs<S> a{};
-    a.Kp = q.Kp; a.C = q.N; a.Bp = y.Bp;
-    a.Wm = at<float>(p, q.Wm); a.bias = at<float>(p, q.bias); a.mask = at<uint32_t>(p, q.mask); a.bmask = at<uint32_t>(p, q.bmask);
-    a.lr = at<float>(p, y.lr);
-    a.train = 0;
-    if (y.L == 1) { a.Arows = xr; a.ar_vs = 0; }
-    else { a.Arows = at<S>(p, y.lay[y.L - 2].prows); a.ar_vs = (size_t)kPredictChunk * y.lay[y.L - 2].Np; }
-    a.labels = at<int32_t>(p, y.yte) + c0;
-    a.rows = R;
-    a.chunk0 = c0 / kOutRows;
-    a.n_chunks_total = y.n_chunks_test;
-    a.part_ce = at<double>(p, y.part_ce);
-    a.part_correct = at<unsigned int>(p, y.part_corr);
-    if (a.Kp % kTile || R % kOutRows) return GEVO_E_SHAPE;
-    HIP_TRY(launch_out<S>(a, y.P, p->stream, prof(p, GEVO_KERNEL_OUT_PREDICT)));
-  }
-  HIP_TRY(launch_reduce_partials(at<double>(p, y.part_ce), at<unsigned int>(p, y.part_corr), y.P,
-                                 y.n_chunks_test, at<double>(p, y.test_ce),
-                                 at<unsigned long long>(p, y.test_corr), p->stream, prof(p, GEVO_KERNEL_AUX)));
+  b.convert = any_copy && !p->wbf_valid;               // bf16 weight copies, once per change of the masters
+  b.part_ce = at<double>(p, y.part_ce);
+  b.part_corr = at<unsigned int>(p, y.part_corr);
+  gevo_status st = predict_pass<S>(p, b);
+  if (st != GEVO_OK) return st;
+  if (any_copy) p->wbf_valid = true;
   HIP_TRY(hipEventRecord(p->ev1, p->stream));
   p->timing_pending = true;
   p->predicted = true;
