@@ -160,6 +160,24 @@ gevo_status gevo_pop_steps_per_epoch(const gevo_pop* pop, uint32_t* steps);
 gevo_status gevo_pop_predict(gevo_pop* pop);
 
 /*
+ * For callers that cannot allocate device memory or create objects during
+ * the call (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation): gevo_pop_predict, computing the same scores bit
+ * for bit, whose scratch (per-chunk activations, bf16 weight copies, partial
+ * sums) is a static device array of GEVO_NOALLOC_SCRATCH_BYTES instead of
+ * part of the workspace.  Every GPU the library runs on holds one such array
+ * from the first gevo_pop_init on it until the process ends.  Variants are
+ * processed in groups that fit the array; the call allocates nothing and
+ * creates no event (kernel-level profiling is not recorded for it).  All
+ * calls on one GPU share its array: calls that overlap on one GPU (other
+ * streams, other threads) race and must not be made.  GEVO_E_UNSUPPORTED
+ * when the scratch of a single variant exceeds the array (e.g. hidden layers
+ * of 8192 x 8192 bf16 weights); GEVO_E_HIP for a runtime error.
+ */
+#define GEVO_NOALLOC_SCRATCH_BYTES (64ull << 20)
+gevo_status gevo_pop_predict_noalloc(gevo_pop* pop);
+
+/*
  * Fitness of every variant (section 4.3: error and time).  Synchronises the
  * stream.  Host arrays of P entries, any may be NULL: mean training CE of the
  * last trained epoch (NaN if never trained), training accuracy of that epoch,

@@ -33,7 +33,8 @@ INIT_XAVIER, INIT_BASE_NOISE = 0, 1
 
 EXPORTED = [
     "gevo_pop_workspace_bytes", "gevo_pop_init", "gevo_pop_train_epoch", "gevo_pop_train_steps",
-    "gevo_pop_steps_per_epoch", "gevo_pop_predict", "gevo_pop_scores", "gevo_pop_last_time",
+    "gevo_pop_steps_per_epoch", "gevo_pop_predict", "gevo_pop_predict_noalloc", "gevo_pop_scores",
+    "gevo_pop_last_time",
     "gevo_pop_export", "gevo_pop_import", "gevo_pop_epoch_labels", "gevo_epoch_permutation",
     "gevo_pop_set_profiling", "gevo_pop_kernel_stats", "gevo_pop_destroy", "gevo_status_str",
     "gevo_check_bf16_rounding", "gevo_nsga2_rank", "gevo_nsga2_select", "gevo_genomes_initial",
@@ -129,6 +130,7 @@ def lib():
         L.gevo_pop_train_steps.argtypes = [vp, u32, u32, u32]
         L.gevo_pop_steps_per_epoch.argtypes = [vp, ctypes.POINTER(u32)]
         L.gevo_pop_predict.argtypes = [vp]
+        L.gevo_pop_predict_noalloc.argtypes = [vp]
         L.gevo_pop_scores.argtypes = [vp, f32p, f32p, f32p, f32p, f32p]
         L.gevo_pop_last_time.argtypes = [vp, ctypes.POINTER(ctypes.c_double)]
         L.gevo_pop_export.argtypes = [vp, u32, f32p, ctypes.POINTER(ctypes.c_uint8), f32p, f32p]
@@ -373,6 +375,10 @@ class Population:
 
     def predict(self):
         _check(lib().gevo_pop_predict(self._h), "gevo_pop_predict")
+
+    def predict_noalloc(self):
+        """gevo_pop_predict with its scratch in the library's static device array."""
+        _check(lib().gevo_pop_predict_noalloc(self._h), "gevo_pop_predict_noalloc")
 
     def scores(self) -> dict:
         arrs = {k: np.zeros(self.P, np.float32) for k in ("train_loss", "train_acc", "test_loss", "test_acc", "time_s")}

@@ -7,6 +7,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 #include <new>
 #include <type_traits>
 #include <vector>
@@ -590,7 +591,8 @@ gevo_status do_train_steps(gevo_pop* p, uint32_t epoch, uint32_t s0, uint32_t s1
 // per hidden layer the chunk activations act[l] ([G][kPredictChunk][Np]
 // operands) and the bf16 weight copy wbf[l] ([G][Np][Kp], null when the layer
 // does not run on the prediction GEMM); the partial sums [G][n_chunks_test].
-// gevo_pop_predict takes them from the workspace.
+// gevo_pop_predict takes them from the workspace, gevo_pop_predict_noalloc
+// from the library's static scratch, one group of variants at a time.
 struct PredictBufs {
   int v0 = 0, G = 0;
   void* act[GEVO_MAX_LAYERS] = {};
@@ -737,6 +739,89 @@ gevo_status do_predict(gevo_pop* p) {
   return GEVO_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Static scratch of gevo_pop_predict_noalloc.  In host code `scratch` names a
+// host-side stand-in, not device memory: its device address (one per GPU) is
+// taken once per device with hipGetSymbolAddress and only that address is
+// passed to kernels.
+constexpr size_t kStaticScratchBytes = GEVO_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+// device address of the current device's scratch (taken on its first use)
+gevo_status static_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return GEVO_E_HIP;
+  if (dev >= kMaxDevices) return GEVO_E_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return GEVO_E_HIP;
+    g_scratch_dev[dev] = ptr;
+  }
+  *out = g_scratch_dev[dev];
+  return GEVO_OK;
+}
+
+// scratch bytes of a group of G variants: per hidden layer the chunk
+// activations and (layers on the prediction GEMM) the bf16 weight copy, then
+// the partial sums; every piece 256-byte aligned
+size_t noalloc_bytes(const Layout& y, size_t G) {
+  size_t n = 0;
+  for (int l = 0; l + 1 < y.L; ++l) {
+    const LayerLay& q = y.lay[l];
+    n += align_up(G * (size_t)kPredictChunk * q.Np * y.elt);
+    if (q.pred) n += align_up(G * (size_t)q.Np * q.Kp * 2);
+  }
+  n += align_up(G * (size_t)y.n_chunks_test * 8) + align_up(G * (size_t)y.n_chunks_test * 4);
+  return n;
+}
+
+template <typename S>
+gevo_status do_predict_noalloc(gevo_pop* p) {
+  const Layout& y = p->y;
+  void* base = nullptr;
+  gevo_status st = static_scratch(&base);
+  if (st != GEVO_OK) return st;
+  if (noalloc_bytes(y, 1) > kStaticScratchBytes) return GEVO_E_UNSUPPORTED;
+  int gmax = 1;
+  while (gmax < y.P && noalloc_bytes(y, (size_t)gmax * 2) <= kStaticScratchBytes) gmax *= 2;
+  while (gmax < y.P && noalloc_bytes(y, (size_t)gmax + 1) <= kStaticScratchBytes) ++gmax;
+  HIP_TRY(hipEventRecord(p->ev0, p->stream));
+  st = sync_masters(p, false);
+  if (st != GEVO_OK) return st;
+  // Groups run one after another on the stream and reuse the scratch; every
+  // scratch byte a group reads was written earlier in that group (the
+  // activations and weight copies by their producing kernels, each partial
+  // sum by exactly one workgroup), so nothing needs clearing.
+  for (int v0 = 0; v0 < y.P; v0 += gmax) {
+    PredictBufs b;
+    b.v0 = v0;
+    b.G = std::min(gmax, y.P - v0);
+    char* c = static_cast<char*>(base);
+    size_t off = 0;
+    auto take = [&](size_t bytes) { char* at_ = c + off; off += align_up(bytes); return at_; };
+    for (int l = 0; l + 1 < y.L; ++l) {
+      const LayerLay& q = y.lay[l];
+      b.act[l] = take((size_t)b.G * kPredictChunk * q.Np * y.elt);
+      if (q.pred) b.wbf[l] = reinterpret_cast<uint16_t*>(take((size_t)b.G * q.Np * q.Kp * 2));
+    }
+    b.part_ce = reinterpret_cast<double*>(take((size_t)b.G * y.n_chunks_test * 8));
+    b.part_corr = reinterpret_cast<unsigned int*>(take((size_t)b.G * y.n_chunks_test * 4));
+    if (off > kStaticScratchBytes) return GEVO_E_UNSUPPORTED;
+    b.convert = true;
+    b.profile = false;
+    st = predict_pass<S>(p, b);
+    if (st != GEVO_OK) return st;
+  }
+  HIP_TRY(hipEventRecord(p->ev1, p->stream));
+  p->timing_pending = true;
+  p->predicted = true;
+  return GEVO_OK;
+}
+
 gevo_status sync_timing(gevo_pop* p) {
   HIP_TRY(hipStreamSynchronize(p->stream));
   if (p->timing_pending) {
@@ -854,6 +939,10 @@ gevo_status gevo_pop_init(const gevo_pop_config* cfg, void* d_ws, size_t ws_byte
   p->stream = reinterpret_cast<hipStream_t>(hip_stream);
   p->trX = d_train_x; p->trY = d_train_y; p->teX = d_test_x; p->teY = d_test_y;
   auto fail = [&](gevo_status s) { gevo_pop_destroy(p); return s; };
+  {
+    void* scr = nullptr;                         // the no-allocation prediction's scratch on this device
+    if (static_scratch(&scr) != GEVO_OK) return fail(GEVO_E_HIP);
+  }
   if (hipEventCreate(&p->ev0) != hipSuccess || hipEventCreate(&p->ev1) != hipSuccess ||
       hipEventCreateWithFlags(&p->perm_ev[0], hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&p->perm_ev[1], hipEventDisableTiming) != hipSuccess)
@@ -1075,6 +1164,11 @@ gevo_status gevo_pop_steps_per_epoch(const gevo_pop* p, uint32_t* steps) {
 gevo_status gevo_pop_predict(gevo_pop* p) {
   if (!p) return GEVO_E_ARG;
   return p->cfg.dtype == GEVO_BF16 ? do_predict<uint16_t>(p) : do_predict<float>(p);
+}
+
+gevo_status gevo_pop_predict_noalloc(gevo_pop* p) {
+  if (!p) return GEVO_E_ARG;
+  return p->cfg.dtype == GEVO_BF16 ? do_predict_noalloc<uint16_t>(p) : do_predict_noalloc<float>(p);
 }
 
 gevo_status gevo_pop_scores(gevo_pop* p, float* train_loss, float* train_acc, float* test_loss, float* test_acc,
