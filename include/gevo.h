@@ -182,8 +182,14 @@ gevo_status gevo_pop_predict_noalloc(gevo_pop* pop);
  * stream.  Host arrays of P entries, any may be NULL: mean training CE of the
  * last trained epoch (NaN if never trained), training accuracy of that epoch,
  * mean test CE and test accuracy in [0,1] of the last predict (NaN before),
- * and time_s = wall time of the last train/predict call divided by P
- * (variants share every kernel, so time is amortised).
+ * and time_s = variant v's share of the wall time of the last
+ * train/predict call: the call's time times v's share of the device time of
+ * its workgroups (each kernel's workgroups belong to one variant and add their
+ * clock-counter time to that variant's total), so the time_s sum to the
+ * call's time.  Workgroups of unit tiles that GEVO_EDIT_WIDTH removes whole
+ * are skipped in training, so narrowed variants get a smaller share.  The
+ * small kernels that serve every variant at once (batch gathers, reductions)
+ * count toward no variant, so their time is split in the same shares.
  */
 gevo_status gevo_pop_scores(gevo_pop* pop, float* train_loss, float* train_acc, float* test_loss,
                             float* test_acc, float* time_s);

@@ -62,6 +62,7 @@ __global__ __launch_bounds__(256, 2) void k_bwd_gemm(BwdArgs<uint16_t> a) {
     v = j / gx;
     kt = j % gx;
   }
+  const uint64_t vt0 = vt_now();
   const int Kp = a.Kp, Np = a.Np, nnb = Np / 32;
   const int k0 = kt * kBK;
   const uint16_t* wt = a.Wt + (size_t)v * Kp * Np + (size_t)k0 * Np;   // rows k0.., [k][n]
@@ -155,6 +156,7 @@ __global__ __launch_bounds__(256, 2) void k_bwd_gemm(BwdArgs<uint16_t> a) {
           *reinterpret_cast<u32x2_t*>(go + (size_t)b * Kp + k0 + kw + 32 * i + 8 * q + 4 * lh) =
               u32x2_t{pk[2 * q], pk[2 * q + 1]};
     }
+  vt_add(a.vtime, v, vt0);
 }
 
 bool bwd_gemm_supported(int Kp, int Np, int Bp) {

@@ -49,6 +49,7 @@ struct Layout {
   size_t lr = 0, thresh = 0, train_ce = 0, train_corr = 0, test_ce = 0, test_corr = 0, part_ce = 0,
          part_corr = 0, xrows = 0, xcols = 0, yep = 0, xte = 0, yte = 0, perm = 0;
   size_t w1img = 0, m1blk = 0;                    // fused training: W1 register image, block-major W1 mask
+  size_t vtime = 0;                                // [P] device clock ticks of each variant's waves, last call
   size_t total = 0;
 };
 
@@ -158,6 +159,7 @@ gevo_status make_layout(const gevo_pop_config* c, Layout* o) {
   y.gscale = take(P * Bp * 32 * 4);
   y.prune_id = take(P * (size_t)kMaxGenomePrunes * 4);
   y.prune_th = take(P * (size_t)kMaxGenomePrunes * 4);
+  y.vtime = take(P * 8);
   y.train_ce = take(P * 8);
   y.train_corr = take(P * 8);
   y.test_ce = take(P * 8);
@@ -245,6 +247,7 @@ struct gevo_pop {
   bool predicted = false;
   bool has_base = false;    // initial weights come from the caller's base model
   bool gscale_on = false;   // output gradients scaled per element (gevo_pop_set_grad_scale)
+  bool ragged = false;      // some variant's hidden layer is narrowed (GEVO_EDIT_WIDTH): skip removed unit tiles
   // fused training keeps W1 in its own register image: which copy is current
   bool img_valid = false;   // the image (and the block-major mask) match the k-blocked master
   bool blk_stale = false;   // training has advanced the image past the k-blocked master
@@ -334,6 +337,8 @@ gevo_status forward_layer(gevo_pop* p, int l, const S* arows0, size_t ar0_vs, in
   a.Orows = at<S>(p, q.arows[outsel]); a.or_vs = (size_t)y.Bp * q.Np;
   a.Ocols = at<S>(p, q.acols[outsel]); a.oc_vs = (size_t)q.Np * y.Bp;
   if (q.Wt) a.Wt = at<S>(p, q.Wt);
+  a.vtime = at<unsigned long long>(p, y.vtime);
+  if (p->ragged) a.wout = at<uint32_t>(p, q.wout);
   if (a.Kp % kTile || a.Np % kTile || a.R % kTile || a.R <= 0) return GEVO_E_SHAPE;
   if constexpr (std::is_same<S, uint16_t>::value) {
     if (q.streamed) {
@@ -422,6 +427,7 @@ gevo_status train_step(gevo_pop* p, int t) {
     a.gscale = p->gscale_on ? at<float>(p, y.gscale) : nullptr;
     a.ce_acc = at<double>(p, y.train_ce);
     a.correct_acc = at<unsigned long long>(p, y.train_corr);
+    a.vtime = at<unsigned long long>(p, y.vtime);
     if (a.Kp % kTile || a.Bp % kTile) return GEVO_E_SHAPE;
     HIP_TRY(launch_out<S>(a, y.P, p->stream, prof(p, GEVO_KERNEL_OUT_TRAIN)));
   }
@@ -436,6 +442,7 @@ gevo_status train_step(gevo_pop* p, int t) {
     a.Acols = at<S>(p, h.acols[buf]); a.ac_vs = (size_t)h.Np * y.Bp;
     a.Gcols = at<S>(p, h.gcols); a.gc_vs = (size_t)h.Np * y.Bp;
     if (h.grows) { a.Grows_out = at<S>(p, h.grows); a.go_vs = (size_t)y.Bp * h.Np; }
+    a.vtime = at<unsigned long long>(p, y.vtime);
     if (a.Kp % kTile || a.Np % kTile || a.Bp % kTile || a.Kp != h.Np) return GEVO_E_SHAPE;
     if constexpr (std::is_same<S, uint16_t>::value) {
       if (bwd_gemm_supported(a.Kp, a.Np, a.Bp)) {
@@ -466,6 +473,8 @@ gevo_status train_step(gevo_pop* p, int t) {
       a.Ocols = at<S>(p, q.acols[nb]); a.oc_vs = (size_t)q.Np * y.Bp;
     }
     if (q.Wt) a.Wt = at<S>(p, q.Wt);
+    a.vtime = at<unsigned long long>(p, y.vtime);
+    if (p->ragged) a.wout = at<uint32_t>(p, q.wout);
     if (a.Kp % kTile || a.Np % kTile || a.Bp % kTile || a.Bp > kPassRows) return GEVO_E_SHAPE;
     if constexpr (std::is_same<S, uint16_t>::value) {
       if (q.streamed) {
@@ -538,6 +547,7 @@ gevo_status do_train_steps(gevo_pop* p, uint32_t epoch, uint32_t s0, uint32_t s1
   }
   HIP_TRY(hipEventRecord(p->ev0, p->stream));
   p->wbf_valid = false;                             // the masters move on
+  HIP_TRY(launch_zero_bytes(p->ws + y.vtime, (size_t)y.P * 8, p->stream, LaunchEv{}));
   {
     gevo_status sti = sync_images(p);               // before the first forward of an epoch
     if (sti != GEVO_OK) return sti;
@@ -563,6 +573,7 @@ gevo_status do_train_steps(gevo_pop* p, uint32_t epoch, uint32_t s0, uint32_t s1
     f.gscale = p->gscale_on ? at<float>(p, y.gscale) : nullptr;
     f.ce_acc = at<double>(p, y.train_ce);
     f.correct_acc = at<unsigned long long>(p, y.train_corr);
+    f.vtime = at<unsigned long long>(p, y.vtime);
     if (q2.Kp != q1.Np || q1.Kp % kTile || fused2_lds_bytes(f.Hp, f.Bp) == 0) return GEVO_E_SHAPE;
     HIP_TRY(launch_fused2(f, y.P, p->stream, prof(p, GEVO_KERNEL_FUSED_TRAIN)));
     p->blk_stale = true;
@@ -621,12 +632,14 @@ gevo_status predict_layer(gevo_pop* p, const PredictBufs& b, int l, const S* aro
   a.R = R;
   a.Arows = arows; a.ar_vs = ar_vs;
   a.Orows = static_cast<S*>(b.act[l]); a.or_vs = (size_t)kPredictChunk * q.Np;
+  a.vtime = at<unsigned long long>(p, y.vtime) + v0;
   if (a.Kp % kTile || a.Np % kTile || a.R % kTile || a.R <= 0) return GEVO_E_SHAPE;
   if constexpr (std::is_same<S, uint16_t>::value) {
     if (b.wbf[l] && pred_gemm_supported(q.Kp, q.Np, R)) {
       PredGemmArgs g{};
       g.A = arows; g.a_vs = ar_vs; g.W = b.wbf[l]; g.bias = a.bias; g.O = a.Orows; g.o_vs = a.or_vs;
       g.Kp = q.Kp; g.Np = q.Np; g.R = R; g.P = b.G;
+      g.vtime = a.vtime;
       HIP_TRY(launch_pred_gemm(g, p->stream, pev(p, b, GEVO_KERNEL_LAYER_FWD)));
       return GEVO_OK;
     }
@@ -634,6 +647,7 @@ gevo_status predict_layer(gevo_pop* p, const PredictBufs& b, int l, const S* aro
       FwdGemmArgs g{};
       g.A = arows; g.a_vs = ar_vs; g.Wm = a.Wm; g.bias = a.bias; g.O = a.Orows; g.o_vs = a.or_vs;
       g.Kp = a.Kp; g.Np = a.Np; g.R = a.R; g.P = b.G;
+      g.vtime = a.vtime;
       HIP_TRY(launch_fwd_gemm(g, p->stream, pev(p, b, GEVO_KERNEL_LAYER_FWD)));
       return GEVO_OK;
     }
@@ -678,6 +692,7 @@ gevo_status predict_pass(gevo_pop* p, const PredictBufs& b) {
           g.labels = at<int32_t>(p, y.yte) + c0;
           g.chunk0 = c0 / kOutRows; g.n_chunks_total = y.n_chunks_test;
           g.part_ce = b.part_ce; g.part_correct = b.part_corr;
+          g.vtime = at<unsigned long long>(p, y.vtime) + v0;
           HIP_TRY(launch_pred_gemm(g, p->stream, pev(p, b, GEVO_KERNEL_FWD_OUT)));
           fused = true;
           continue;
@@ -701,6 +716,7 @@ gevo_status predict_pass(gevo_pop* p, const PredictBufs& b) {
     a.n_chunks_total = y.n_chunks_test;
     a.part_ce = b.part_ce;
     a.part_correct = b.part_corr;
+    a.vtime = at<unsigned long long>(p, y.vtime) + v0;
     if (a.Kp % kTile || R % kOutRows) return GEVO_E_SHAPE;
     HIP_TRY(launch_out<S>(a, b.G, p->stream, pev(p, b, GEVO_KERNEL_OUT_PREDICT)));
   }
@@ -714,6 +730,7 @@ template <typename S>
 gevo_status do_predict(gevo_pop* p) {
   const Layout& y = p->y;
   HIP_TRY(hipEventRecord(p->ev0, p->stream));
+  HIP_TRY(launch_zero_bytes(p->ws + y.vtime, (size_t)y.P * 8, p->stream, LaunchEv{}));
   gevo_status stb = sync_masters(p);
   if (stb != GEVO_OK) return stb;
   PredictBufs b;
@@ -790,6 +807,7 @@ gevo_status do_predict_noalloc(gevo_pop* p) {
   while (gmax < y.P && noalloc_bytes(y, (size_t)gmax * 2) <= kStaticScratchBytes) gmax *= 2;
   while (gmax < y.P && noalloc_bytes(y, (size_t)gmax + 1) <= kStaticScratchBytes) ++gmax;
   HIP_TRY(hipEventRecord(p->ev0, p->stream));
+  HIP_TRY(launch_zero_bytes(p->ws + y.vtime, (size_t)y.P * 8, p->stream, LaunchEv{}));
   st = sync_masters(p, false);
   if (st != GEVO_OK) return st;
   // Groups run one after another on the stream and reuse the scratch; every
@@ -1006,7 +1024,8 @@ gevo_status gevo_pop_init(const gevo_pop_config* cfg, void* d_ws, size_t ws_byte
   g.rows = p->ws + y.xte; g.labels = reinterpret_cast<int32_t*>(p->ws + y.yte);
   hipError_t e = cfg->dtype == GEVO_BF16 ? launch_gather<uint16_t>(g, s, LaunchEv{}) : launch_gather<float>(g, s, LaunchEv{});
   if (e != hipSuccess) return fail(GEVO_E_HIP);
-  if (launch_zero_bytes(p->ws + y.train_ce, (size_t)P * 8, s, LaunchEv{}) != hipSuccess ||
+  if (launch_zero_bytes(p->ws + y.vtime, (size_t)P * 8, s, LaunchEv{}) != hipSuccess ||
+      launch_zero_bytes(p->ws + y.train_ce, (size_t)P * 8, s, LaunchEv{}) != hipSuccess ||
       launch_zero_bytes(p->ws + y.train_corr, (size_t)P * 8, s, LaunchEv{}) != hipSuccess ||
       launch_zero_bytes(p->ws + y.test_ce, (size_t)P * 8, s, LaunchEv{}) != hipSuccess ||
       launch_zero_bytes(p->ws + y.test_corr, (size_t)P * 8, s, LaunchEv{}) != hipSuccess)
@@ -1095,6 +1114,25 @@ gevo_status gevo_pop_set_genomes(gevo_pop* p, float lr_base, const uint32_t* off
   }
   const gevo_status st = init_layers(p, true);
   if (st != GEVO_OK) return st;
+  // Narrowed hidden layers: training skips the workgroups of removed unit
+  // tiles, which then never write their activation, gradient and operand-copy
+  // slots, so those buffers start from zeros.
+  bool narrowed = false;
+  for (int v = 0; v < P; ++v)
+    for (int l = 1; l < L; ++l) narrowed = narrowed || width[(size_t)v * (L + 1) + l] < (uint32_t)y.lay[l - 1].N;
+  p->ragged = narrowed;
+  if (narrowed)
+    for (int l = 0; l + 1 < L; ++l) {
+      const LayerLay& q = y.lay[l];
+      const size_t act = (size_t)P * y.Bp * q.Np * y.elt;
+      for (int bsel = 0; bsel < 2; ++bsel) {
+        HIP_TRY(launch_zero_bytes(p->ws + q.arows[bsel], act, s, LaunchEv{}));
+        HIP_TRY(launch_zero_bytes(p->ws + q.acols[bsel], act, s, LaunchEv{}));
+      }
+      HIP_TRY(launch_zero_bytes(p->ws + q.gcols, act, s, LaunchEv{}));
+      if (q.grows) HIP_TRY(launch_zero_bytes(p->ws + q.grows, act, s, LaunchEv{}));
+      if (q.Wt) HIP_TRY(launch_zero_bytes(p->ws + q.Wt, (size_t)P * q.Kp * q.Np * y.elt, s, LaunchEv{}));
+    }
   HIP_TRY(launch_zero_bytes(p->ws + y.train_ce, (size_t)P * 8, s, LaunchEv{}));
   HIP_TRY(launch_zero_bytes(p->ws + y.train_corr, (size_t)P * 8, s, LaunchEv{}));
   HIP_TRY(launch_zero_bytes(p->ws + y.test_ce, (size_t)P * 8, s, LaunchEv{}));
@@ -1184,13 +1222,19 @@ gevo_status gevo_pop_scores(gevo_pop* p, float* train_loss, float* train_acc, fl
   HIP_TRY(hipMemcpy(tc.data(), p->ws + y.train_corr, (size_t)P * 8, hipMemcpyDeviceToHost));
   HIP_TRY(hipMemcpy(sce.data(), p->ws + y.test_ce, (size_t)P * 8, hipMemcpyDeviceToHost));
   HIP_TRY(hipMemcpy(sc.data(), p->ws + y.test_corr, (size_t)P * 8, hipMemcpyDeviceToHost));
+  std::vector<unsigned long long> vt(P);
+  HIP_TRY(hipMemcpy(vt.data(), p->ws + y.vtime, (size_t)P * 8, hipMemcpyDeviceToHost));
+  double vt_sum = 0.0;
+  for (int v = 0; v < P; ++v) vt_sum += (double)vt[v];
   const bool trained = p->last_epoch >= 0 && p->rows_done > 0;
   for (int v = 0; v < P; ++v) {
     if (train_loss) train_loss[v] = trained ? (float)(tce[v] / (double)p->rows_done) : NAN;
     if (train_acc) train_acc[v] = trained ? (float)((double)tc[v] / (double)p->rows_done) : NAN;
     if (test_loss) test_loss[v] = p->predicted ? (float)(sce[v] / (double)y.n_test) : NAN;
     if (test_acc) test_acc[v] = p->predicted ? (float)((double)sc[v] / (double)y.n_test) : NAN;
-    if (time_s) time_s[v] = (float)(p->last_s / (double)P);
+    // the call's wall time split in proportion to each variant's device time
+    // (equal shares when no per-variant kernel ran)
+    if (time_s) time_s[v] = (float)(vt_sum > 0.0 ? p->last_s * ((double)vt[v] / vt_sum) : p->last_s / (double)P);
   }
   return GEVO_OK;
 }

@@ -77,6 +77,16 @@ template <> struct Op<float> {              // fp32 operands
   __device__ __forceinline__ static float to_f32(float h) { return h; }
 };
 
+// Per-variant device time (section 4.3 scores each individual by its run
+// time; here variants share launches): every wave of a kernel that works on
+// one variant adds the ticks of the constant-rate device clock from its start
+// to its end to that variant's counter (lane 0, one vector atomic per wave;
+// a null counter array records nothing).
+__device__ __forceinline__ uint64_t vt_now() { return (uint64_t)wall_clock64(); }
+__device__ __forceinline__ void vt_add(unsigned long long* acc, int v, uint64_t t0) {
+  if (acc && (threadIdx.x & 63) == 0) atomicAdd(acc + v, (unsigned long long)(vt_now() - t0));
+}
+
 __device__ __forceinline__ f32x16_t zero16() {
   f32x16_t z;
 #pragma unroll

@@ -149,6 +149,7 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, lh = lane >> 5;
   const int v = blockIdx.x;
+  const uint64_t vt0 = vt_now();
   const int Kp = a.Kp, nkb = Kp / 32;
   const int n = wave * 32 + l32;             // hidden unit of this lane's column
   float* W1 = a.W1 + (size_t)v * HP * Kp;
@@ -690,6 +691,7 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
     a.ce_acc[v] = ce_tot;
     a.correct_acc[v] = corr_tot;
   }
+  vt_add(a.vtime, v, vt0);
 }
 
 size_t fused2_lds_bytes(int hp, int bp) {

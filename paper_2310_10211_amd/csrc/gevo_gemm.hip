@@ -57,6 +57,7 @@ __global__ __launch_bounds__(512, 1) void k_fwd_gemm(FwdGemmArgs a) {
   const int p = (j / nr) * 8 + xcd, rt = j % nr;
   if (p >= a.P * nn) return;
   const int v = p / nn, n0 = (p % nn) * BN, r0 = rt * kGM;
+  const uint64_t vt0 = vt_now();
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, lh = lane >> 5;
   const int wm = wave & 3, wn = wave >> 2;          // 64-row band, BN/2-column half
@@ -164,6 +165,7 @@ __global__ __launch_bounds__(512, 1) void k_fwd_gemm(FwdGemmArgs a) {
       }
     }
   }
+  vt_add(a.vtime, v, vt0);
 }
 
 size_t fwd_gemm_lds_bytes(int bn) { return bn == 256 ? GemmLds<256>::bytes : GemmLds<128>::bytes; }

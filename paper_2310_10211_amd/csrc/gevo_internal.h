@@ -76,6 +76,12 @@ struct LayerArgs {
   // words block-major (see launch_w1_image / launch_mask_block_major)
   float* Wimg;                   // [P][Kp/32][Np/32][4][64][4]
   const uint32_t* mblk;          // [P][Kp/32][Np]
+  // structural edits: variant v keeps units n < wout[v] of this layer (null:
+  // all); a workgroup whose units are all removed does nothing (their
+  // weights and biases are +0 and stay +0; the caller keeps their activation
+  // and operand-copy slots at zero)
+  const uint32_t* wout;
+  unsigned long long* vtime;      // [P] per-variant device time in clock ticks (nullable)
 };
 
 // bf16 forward of a hidden layer over prediction rows (no update)
@@ -85,6 +91,7 @@ struct FwdGemmArgs {
   const float* bias;                // [P][Np]
   uint16_t* O; size_t o_vs;         // [v][R][Np] relu output rows
   int Kp, Np, R, P;
+  unsigned long long* vtime;      // [P] per-variant device time in clock ticks (nullable)
 };
 
 // bf16 prediction GEMM of a hidden layer (gevo_predict.hip): per variant
@@ -104,6 +111,7 @@ struct PredGemmArgs {
   int chunk0, n_chunks_total;       // partial sums at [v][chunk0 + row tile]
   double* part_ce;
   unsigned int* part_correct;
+  unsigned long long* vtime;      // [P] per-variant device time in clock ticks (nullable)
 };
 
 template <typename S>
@@ -131,6 +139,7 @@ struct OutArgs {
   unsigned int* part_correct;
   S* Gcols; size_t gc_vs;        // [v][Kp][Bp] gradient of the last hidden layer (training)
   S* Grows; size_t gr_vs;        // [v][Bp][Kp] same, row-major (nullable)
+  unsigned long long* vtime;      // [P] per-variant device time in clock ticks (nullable)
 };
 
 template <typename S>
@@ -141,6 +150,7 @@ struct BwdArgs {
   const S* Acols; size_t ac_vs;  // [v][Kp][Bp] activations of layer l-1 (for ReLU')
   S* Gcols; size_t gc_vs;        // [v][Kp][Bp] gradient at layer l-1 output
   S* Grows_out; size_t go_vs;    // [v][Bp][Kp] (nullable)
+  unsigned long long* vtime;      // [P] per-variant device time in clock ticks (nullable)
 };
 
 // Fused per-variant training of a two-layer net (bf16 operands), one
@@ -159,6 +169,7 @@ struct Fused2Args {
   double* ce_acc;
   unsigned long long* correct_acc;
   const float* gscale;           // [P][Bp][32] per-element output-gradient scale (nullable: fl32(1/b_t))
+  unsigned long long* vtime;      // [P] per-variant device time in clock ticks (nullable)
 };
 
 struct GatherArgs {

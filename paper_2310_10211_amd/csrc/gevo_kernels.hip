@@ -131,6 +131,11 @@ __global__ __launch_bounds__(256, 2) void k_layer(LayerArgs<S> a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int l32 = lane & 31, lh = lane >> 5;
   const int n0 = blockIdx.x * 32, v = blockIdx.y;
+  const uint64_t vt0 = vt_now();
+  if (a.wout && n0 >= (int)a.wout[v]) {                  // every unit of the tile removed
+    vt_add(a.vtime, v, vt0);
+    return;
+  }
   const int Kp = a.Kp, Np = a.Np, kwords = Kp / 32;
   float* Wv = a.Wm + (size_t)v * Np * Kp;                     // this variant, k-blocked
   const uint32_t* mk = a.mask + ((size_t)v * Np + n0) * kwords;
@@ -355,6 +360,7 @@ __global__ __launch_bounds__(256, 2) void k_layer(LayerArgs<S> a) {
       epilogue(row0, ntiles, acc);
     }
   }
+  vt_add(a.vtime, v, vt0);
 }
 
 // ------------------------------------------------------------ output layer
@@ -384,6 +390,7 @@ __global__ __launch_bounds__(64 * kOutWaves) void k_out(OutArgs<S> a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int l32 = lane & 31, lh = lane >> 5;
   const int v = blockIdx.y, chunk = blockIdx.x;
+  const uint64_t vt0 = vt_now();
   const int Kp = a.Kp, WS = Kp + O::PAD;
   S* wop = reinterpret_cast<S*>(smem);                  // [32][WS]  W_L as operand, [class][k]
   S* gs = wop + 32 * WS;                                // [Bp][GSTR] gradient rows (training)
@@ -494,7 +501,10 @@ __global__ __launch_bounds__(64 * kOutWaves) void k_out(OutArgs<S> a) {
       a.part_correct[(size_t)v * a.n_chunks_total + a.chunk0 + chunk] = cc;
     }
   }
-  if (!a.train) return;
+  if (!a.train) {
+    vt_add(a.vtime, v, vt0);
+    return;
+  }
 
   const float lrv = a.lr[v];
   if (threadIdx.x < 32) {
@@ -552,7 +562,10 @@ __global__ __launch_bounds__(64 * kOutWaves) void k_out(OutArgs<S> a) {
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
   }
-  if (!a.Gcols) return;
+  if (!a.Gcols) {
+    vt_add(a.vtime, v, vt0);
+    return;
+  }
   // gradient of the last hidden layer, batch-contiguous, with ReLU'
   const int tb = a.Bp / 32, ntot = (Kp / 32) * tb;
   for (int t = wave; t < ntot; t += NW) {
@@ -590,6 +603,7 @@ __global__ __launch_bounds__(64 * kOutWaves) void k_out(OutArgs<S> a) {
       }
     }
   }
+  vt_add(a.vtime, v, vt0);
 }
 
 // ------------------------------------------------------- hidden backward GEMM
@@ -602,6 +616,7 @@ __global__ __launch_bounds__(256) void k_bwd(BwdArgs<S> a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int l32 = lane & 31, lh = lane >> 5;
   const int v = blockIdx.y;
+  const uint64_t vt0 = vt_now();
   const int tb = a.Bp / 32;
   const int t = blockIdx.x * 4 + wave;
   if (t >= (a.Kp / 32) * tb) return;
@@ -620,6 +635,7 @@ __global__ __launch_bounds__(256) void k_bwd(BwdArgs<S> a) {
     a.Gcols[v * a.gc_vs + (size_t)k * a.Bp + b] = g;
     if (a.Grows_out) a.Grows_out[v * a.go_vs + (size_t)b * a.Kp + k] = g;
   }
+  vt_add(a.vtime, v, vt0);
 }
 
 // ------------------------------------------------------------- data movement

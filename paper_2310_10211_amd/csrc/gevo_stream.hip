@@ -81,6 +81,11 @@ __global__ __launch_bounds__(kST, 1) void k_stream_layer(LayerArgs<uint16_t> a) 
     v = j / gx;
     tile = j % gx;
   }
+  const uint64_t vt0 = vt_now();
+  if (a.wout && tile * kSU >= (int)a.wout[v]) {         // every unit of the tile removed
+    vt_add(a.vtime, v, vt0);
+    return;
+  }
   const int Kp = a.Kp, Np = a.Np, nkb = Kp / 32;
   // Each tile visits the k-blocks in its own rotated order, so that the
   // workgroups streaming at the same time read different lines of a shared
@@ -350,6 +355,7 @@ __global__ __launch_bounds__(kST, 1) void k_stream_layer(LayerArgs<uint16_t> a) 
           *reinterpret_cast<u32x2_t*>(ocol + (size_t)n * BP + 32 * T + 8 * q + 4 * lh) = u32x2_t{pk[2 * q], pk[2 * q + 1]};
     }
   }
+  vt_add(a.vtime, v, vt0);
 }
 
 bool stream_layer_supported(int Kp, int Np, int Bp, int R) {

@@ -10,11 +10,16 @@ struct_p per drawn edit.  Fitness (section 4.3) is minimised over two objectives
   * model error: the training-split error of the last epoch (the paper
     computes accuracy on the training split during the search and keeps the
     test split for checking the result afterwards, section 5);
-  * cost: the expected kept fraction of the weights (pruning densities times
-    the fraction the structural edits keep).  The paper's second
-    objective is run time; here every variant runs the same dense kernels, so
-    each individual's time is the same share of one launch, and the kept
-    fraction stands for the time a pruned model saves.
+  * cost (the paper's second objective is run time), one of:
+    - "kept" (default): the expected kept fraction of the weights (pruning
+      densities times the fraction the structural edits keep).  Pruned
+      weights still run in the dense kernels, so this stands for the time a
+      pruned model would save; it is deterministic.
+    - "measured": each variant's device time in the generation's training
+      and prediction calls (gevo_pop_scores' time_s, summed over the calls).
+      Workgroups of hidden-layer unit tiles that a narrowed variant has
+      removed are skipped, so narrowed variants measure faster.  Timings vary
+      from run to run, so a search on this objective is not bit-reproducible.
 Each generation keeps the n_elite best unchanged and fills the rest with the
 children of tournament winners (section 4.4).  The elites keep the fitness
 they were selected with: the whole generation is retrained as one population,
@@ -34,7 +39,7 @@ from . import Population, genomes_breed, genomes_initial, nsga2_rank, nsga2_sele
 @dataclass
 class Generation:
     genomes: list                     # edit lists [(kind, id, value), ...]
-    objectives: np.ndarray            # [P][2]: training error, expected kept fraction
+    objectives: np.ndarray            # [P][2]: training error, cost (expected kept fraction or time in s)
     test_error: np.ndarray            # [P], for checking the front afterwards
     lr: np.ndarray                    # [P] learning rates of the genomes
     rank: np.ndarray = field(default=None)
@@ -44,9 +49,12 @@ class Generation:
 class Search:
     def __init__(self, pop: Population, lr_base: float, seed: int, epochs: int = 1, rho_lo: float = 0.3,
                  n_elite: int = 16, cxpb: float = 0.8, mutpb: float = 0.5, max_edits: int = 16, n_mut: int = 3,
-                 struct_p: float = 0.0):
+                 struct_p: float = 0.0, time_objective: str = "kept"):
         if not 0 <= n_elite <= pop.P:
             raise ValueError("n_elite must be in [0, P]")
+        if time_objective not in ("kept", "measured"):
+            raise ValueError("time_objective must be 'kept' or 'measured'")
+        self.time_objective = time_objective
         self.pop, self.lr_base, self.seed, self.epochs = pop, float(lr_base), int(seed), int(epochs)
         self.rho_lo, self.n_elite, self.cxpb, self.mutpb = float(rho_lo), int(n_elite), float(cxpb), float(mutpb)
         self.max_edits, self.n_mut, self.struct_p = int(max_edits), int(n_mut), float(struct_p)
@@ -57,12 +65,16 @@ class Search:
         carried = (objectives, test errors) of the first individuals, kept as they are."""
         pop = self.pop
         lr, dens = pop.set_genomes(genomes, self.lr_base)
+        t = np.zeros(pop.P, np.float64)
         for e in range(self.epochs):
             pop.train_epoch(e)
+            if self.time_objective == "measured":
+                t += pop.scores()["time_s"]
         pop.predict()
         s = pop.scores()
         train_err = 1.0 - np.asarray(s["train_acc"], np.float64)
-        objs = np.stack([train_err, dens], axis=1)
+        cost = dens if self.time_objective == "kept" else t + np.asarray(s["time_s"], np.float64)
+        objs = np.stack([train_err, cost], axis=1)
         test_err = 1.0 - np.asarray(s["test_acc"], np.float64)
         if carried is not None:
             k = len(carried[0])

@@ -167,7 +167,8 @@ def _struct_reference(cfg, genome, lr_base):
     return lr, mask, bmask, params
 
 
-@pytest.mark.parametrize("i,dims", [(1, None), (3, None), (3, [200, 96, 64, 10])])
+@pytest.mark.parametrize("i,dims", [(1, None), (3, None), (3, [200, 96, 64, 10]),
+                                    (5, [1024, 256, 128, 10])])   # a removed 128-unit tile of the streaming kernel
 def test_structural_genomes_rebuild_and_train_like_the_oracle(i, dims):
     cfg, data = _small(i, P=4, n_train=640, n_test=256)
     if dims:
@@ -204,4 +205,49 @@ def test_structural_genomes_rebuild_and_train_like_the_oracle(i, dims):
             assert np.all(b[r_bmask[boff:boff + cfg["dims"][l]] == 0] == 0.0), (v, l)
             off += k + cfg["dims"][l]
             boff += cfg["dims"][l]
+    pop.close()
+
+
+def test_time_s_splits_the_call_time_over_the_variants():
+    cfg, data = _small(5, P=4, n_train=600, n_test=256)
+    cfg["dims"] = [1024, 256, 128, 10]
+    for k in ("x_train", "x_test"):
+        data[k] = np.ascontiguousarray(data[k][:, :1024])
+    pop = _pop(cfg, data)
+    for call in (lambda: pop.train_epoch(0), pop.predict):
+        call()
+        s = pop.scores()
+        assert np.all(s["time_s"] > 0)
+        assert abs(float(np.sum(s["time_s"], dtype=np.float64)) - pop.last_time()) <= 1e-5 * pop.last_time()
+    pop.close()
+
+
+def test_narrowed_variants_measure_less_device_time():
+    """3072-1024-512-10 in bf16: variants 4..7 keep 128 units of each hidden
+    layer, so 7 of 8 and 3 of 4 unit tiles of their streaming-kernel
+    workgroups are skipped; their share of the epoch's time is well below
+    that of the full variants 0..3, and they still train like the oracle's
+    narrowed nets (checked by the structural-genome test above)."""
+    cfg, data = _small(5, P=8, n_train=1024, n_test=256)
+    pop = _pop(cfg, data)
+    full = [(ns.LR_EDIT, 0, ns._f32_bits(1.0))]
+    narrow = full + [(ns.WIDTH_EDIT, 1, 128), (ns.WIDTH_EDIT, 2, 128)]
+    pop.set_genomes([full] * 4 + [narrow] * 4, 0.01)
+    pop.train_epoch(0)
+    t = pop.scores()["time_s"]
+    assert np.max(t[4:]) < 0.6 * np.min(t[:4]), t
+    pop.close()
+
+
+def test_search_on_measured_time_runs_and_scores_time():
+    cfg, data = _small(5, P=8, n_train=512, n_test=256)
+    cfg["dims"] = [1024, 256, 128, 10]
+    for k in ("x_train", "x_test"):
+        data[k] = np.ascontiguousarray(data[k][:, :1024])
+    pop = _pop(cfg, data)
+    from paper_2310_10211_amd.search import Search
+    search = Search(pop, 0.01, seed=7, n_elite=2, struct_p=0.5, time_objective="measured")
+    hist = search.run(2)
+    for gen in hist:
+        assert np.all(gen.objectives[:, 1] > 0) and np.all(np.isfinite(gen.objectives))
     pop.close()
