@@ -137,6 +137,12 @@ gevo_status gevo_pop_init(const gevo_pop_config* cfg, void* d_ws, size_t ws_byte
  * 0, 1, 2, ... (GEVO_E_ORDER otherwise).  Per variant the epoch's mean
  * cross-entropy (taken before each step's update) and the wall time of the
  * call (HIP events) are recorded for gevo_pop_scores.
+ * With GEVO_RESIDENT=1 in the environment when gevo_pop_init runs, two-layer
+ * bf16 nets of 784 (or 769..800) inputs, 256 hidden units, at most 16 classes
+ * and a batch of 97..128 rows train in the resident kernel (a pair of
+ * workgroups per variant, cooperative launch; slower than the default on
+ * gfx950).  That path synchronises the stream at the end of the call and
+ * returns GEVO_E_HIP if a workgroup gave up waiting for its partner.
  */
 gevo_status gevo_pop_train_epoch(gevo_pop* pop, uint32_t epoch);
 

@@ -9,7 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libgevo.so")
 SOURCES = [os.path.join(HERE, "csrc", n)
-           for n in ("gevo_kernels.hip", "gevo_fused.hip", "gevo_gemm.hip", "gevo_predict.hip", "gevo_stream.hip", "gevo_bwd.hip", "gevo_cnn.hip", "gevo_search.hip", "gevo_capi.hip")]
+           for n in ("gevo_kernels.hip", "gevo_fused.hip", "gevo_resident.hip", "gevo_gemm.hip", "gevo_predict.hip", "gevo_stream.hip", "gevo_bwd.hip", "gevo_cnn.hip", "gevo_search.hip", "gevo_capi.hip")]
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
     "-ffp-contract=off",                                   # elementwise fp32 ops round one at a time

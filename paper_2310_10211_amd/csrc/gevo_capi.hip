@@ -3,6 +3,7 @@
 // hyper-parameters and the per-epoch data order, and enqueues the kernels of
 // gevo_kernels.hip on the caller's stream.
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -39,6 +40,7 @@ struct LayerLay {
 struct Layout {
   int L = 0, P = 0, B = 0, Bp = 0, T = 0;
   bool fused = false;                              // two-layer bf16 nets train in the fused per-variant kernel
+  bool resident = false;                           // ... or, for the shapes it covers, in the resident kernel
   bool images = false;                             // some layer trains on a register-image copy of its master
   int64_t n_train = 0, n_test = 0;
   int n_test_pad = 0, n_chunks_test = 0;
@@ -49,9 +51,19 @@ struct Layout {
   size_t lr = 0, thresh = 0, train_ce = 0, train_corr = 0, test_ce = 0, test_corr = 0, part_ce = 0,
          part_corr = 0, xrows = 0, xcols = 0, yep = 0, xte = 0, yte = 0, perm = 0;
   size_t w1img = 0, m1blk = 0;                    // fused training: W1 register image, block-major W1 mask
+  size_t xbuf = 0, rerr = 0;                       // resident training: pair exchange words, error word
   size_t vtime = 0;                                // [P] device clock ticks of each variant's waves, last call
   size_t total = 0;
 };
+
+// GEVO_RESIDENT=1 in the environment trains the two-layer nets the resident
+// kernel covers in that kernel instead of the streaming fused kernel (it is
+// correct but slower on gfx950: its register-resident masters leave too few
+// registers for the rest of the step, which spills to scratch).
+bool resident_requested() {
+  const char* e = getenv("GEVO_RESIDENT");
+  return e && e[0] && e[0] != '0';
+}
 
 gevo_status validate(const gevo_pop_config* c) {
   if (!c) return GEVO_E_ARG;
@@ -111,6 +123,7 @@ gevo_status make_layout(const gevo_pop_config* c, Layout* o) {
   }
   if (out_lds(y.lay[y.L - 1].Kp, y.Bp, y.elt, pad) > kLdsBudget) return GEVO_E_UNSUPPORTED;
   y.fused = y.L == 2 && c->dtype == GEVO_BF16 && fused2_lds_bytes(y.lay[0].Np, y.Bp) > 0;
+  y.resident = y.fused && res2_supported(y.lay[0].Kp, y.lay[0].Np, y.Bp, (int)c->dims[2]) && resident_requested();
   for (int l = 0; l + 1 < y.L; ++l) {
     LayerLay& q = y.lay[l];
     q.pred = c->dtype == GEVO_BF16 && pred_gemm_supported(q.Kp, q.Np, kOutRows);
@@ -178,6 +191,10 @@ gevo_status make_layout(const gevo_pop_config* c, Layout* o) {
     const size_t Np1 = (size_t)y.lay[0].Np;
     y.w1img = take(P * Np1 * Kp1 * 4);
     y.m1blk = take(P * Np1 * (Kp1 / 32) * 4);
+  }
+  if (y.resident) {
+    y.xbuf = take((size_t)kResMaxPairs * 2 * 2 * kResXW * 8);
+    y.rerr = take(4);
   }
   y.total = off;
   return GEVO_OK;
@@ -376,10 +393,12 @@ gevo_status begin_epoch(gevo_pop* p, int e) {
   g.d0 = y.lay[0].K; g.Kp = y.lay[0].Kp; g.B = y.B; g.Bp = y.Bp; g.T = y.T;
   g.rows = p->ws + y.xrows; g.labels = at<int32_t>(p, y.yep);
   g.blocked = y.fused;                             // the fused kernel reads rows one column block at a time
+  g.res_order = y.resident;
   HIP_TRY(launch_gather<S>(g, p->stream, prof(p, GEVO_KERNEL_GATHER)));
   TransposeArgs tr{};
   tr.src = p->ws + y.xrows; tr.dst = p->ws + y.xcols; tr.Kp = y.lay[0].Kp; tr.Bp = y.Bp; tr.T = y.T;
   tr.blocked = y.fused;
+  tr.res_order = y.resident;
   HIP_TRY(launch_transpose<S>(tr, p->stream, prof(p, GEVO_KERNEL_GATHER)));
   HIP_TRY(launch_zero_bytes(p->ws + y.train_ce, (size_t)y.P * 8, p->stream, prof(p, GEVO_KERNEL_AUX)));
   HIP_TRY(launch_zero_bytes(p->ws + y.train_corr, (size_t)y.P * 8, p->stream, prof(p, GEVO_KERNEL_AUX)));
@@ -575,7 +594,25 @@ gevo_status do_train_steps(gevo_pop* p, uint32_t epoch, uint32_t s0, uint32_t s1
     f.correct_acc = at<unsigned long long>(p, y.train_corr);
     f.vtime = at<unsigned long long>(p, y.vtime);
     if (q2.Kp != q1.Np || q1.Kp % kTile || fused2_lds_bytes(f.Hp, f.Bp) == 0) return GEVO_E_SHAPE;
-    HIP_TRY(launch_fused2(f, y.P, p->stream, prof(p, GEVO_KERNEL_FUSED_TRAIN)));
+    if (y.resident) {
+      const int maxp = res2_max_pairs();
+      if (maxp < 1) return GEVO_E_UNSUPPORTED;
+      Res2Args ra{};
+      ra.f = f;
+      ra.xbuf = at<unsigned long long>(p, y.xbuf);
+      ra.err = at<unsigned int>(p, y.rerr);
+      ra.P = y.P;
+      const int pairs = y.P < maxp ? y.P : maxp;
+      HIP_TRY(launch_zero_bytes(p->ws + y.xbuf, (size_t)pairs * 2 * 2 * kResXW * 8 + 0, p->stream, LaunchEv{}));
+      HIP_TRY(launch_zero_bytes(p->ws + y.rerr, 4, p->stream, LaunchEv{}));
+      HIP_TRY(launch_res2(ra, pairs, p->stream, prof(p, GEVO_KERNEL_FUSED_TRAIN)));
+      uint32_t err = 0;
+      HIP_TRY(hipMemcpyAsync(&err, p->ws + y.rerr, 4, hipMemcpyDeviceToHost, p->stream));
+      HIP_TRY(hipStreamSynchronize(p->stream));
+      if (err) return GEVO_E_HIP;                 // a half of a pair stopped waiting for its partner
+    } else {
+      HIP_TRY(launch_fused2(f, y.P, p->stream, prof(p, GEVO_KERNEL_FUSED_TRAIN)));
+    }
     p->blk_stale = true;
     for (uint32_t t = s0; t < s1; ++t) {
       const int64_t r0 = (int64_t)t * y.B;

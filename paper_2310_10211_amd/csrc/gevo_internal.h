@@ -172,6 +172,24 @@ struct Fused2Args {
   unsigned long long* vtime;      // [P] per-variant device time in clock ticks (nullable)
 };
 
+// Resident training of two-layer nets (gevo_resident.hip): a pair of
+// workgroups per variant, exchanging their halves' logits once per step.
+constexpr int kResXW = 2048;             // exchange words per half and step parity
+constexpr int kResMaxPairs = 128;        // pairs per launch (variants beyond run in later rounds)
+struct Res2Args {
+  Fused2Args f;                          // X copies in the resident layout (perm32 within each block)
+  unsigned long long* xbuf;              // [kResMaxPairs][2 halves][2 parities][kResXW], zero before the launch
+  unsigned int* err;                     // set to 1 when a half gave up waiting for its partner
+  int P;
+};
+
+// Position of element x (0..31) of a 32-element block in the resident X
+// copies: the middle two groups of four of each 16 are swapped (an involution).
+__host__ __device__ inline int perm32(int x) {
+  const int a = (x >> 2) & 3;
+  return (x & ~12) | ((((a & 1) << 1) | (a >> 1)) << 2);
+}
+
 struct GatherArgs {
   const float* X;                // [n][d0] caller's rows
   const int32_t* y;              // [n]
@@ -179,6 +197,7 @@ struct GatherArgs {
   int64_t n;
   int d0, Kp, B, Bp, T;          // T = steps (row blocks)
   int blocked;                   // rows block-major, [T][Kp/32][Bp][32], instead of [T][Bp][Kp]
+  int res_order;                 // (blocked only) element k of a block at position perm32(k)
   void* rows;                    // [T][Bp][Kp] S
   int32_t* labels;               // [T][Bp]
 };
@@ -188,6 +207,8 @@ struct TransposeArgs {
   void* dst;                     // [T][Kp][Bp] S
   int Kp, Bp, T;
   int blocked;
+  int res_order;                 // source positions perm32(k); destination rows keep k and put row b of
+                                 // each 32 at column position perm32(b)
 };
 
 // ---------------------------------------------------------------- launchers
@@ -226,6 +247,9 @@ bool bwd_gemm_supported(int Kp, int Np, int Bp);
 hipError_t launch_bwd_gemm(const BwdArgs<uint16_t>& a, int P, hipStream_t s, const LaunchEv& ev);
 hipError_t launch_stream_layer(const LayerArgs<uint16_t>& a, int P, hipStream_t s, const LaunchEv& ev);
 size_t fused2_lds_bytes(int hp, int bp);     // 0 when the shape has no fused instantiation
+bool res2_supported(int Kp, int Hp, int Bp, int C);   // Kp 800, Hp 256, Bp 128, C <= 16
+int res2_max_pairs();                        // co-resident pairs on the current device (0: no cooperative launch)
+hipError_t launch_res2(const Res2Args& a, int pairs, hipStream_t s, const LaunchEv& ev);
 hipError_t launch_reduce_partials(const double* part_ce, const unsigned int* part_corr, int P, int n_chunks,
                                   double* ce_out, unsigned long long* corr_out, hipStream_t s, const LaunchEv& ev);
 

@@ -652,7 +652,8 @@ __global__ __launch_bounds__(256) void k_gather(GatherArgs a) {
   const float* x = a.X + src * a.d0;
   for (int k = threadIdx.x; k < a.Kp; k += blockDim.x) {
     const float xv = (valid && k < a.d0) ? x[k] : 0.0f;
-    const size_t at = a.blocked ? ((size_t)(k >> 5) * a.Bp + b) * 32 + (k & 31) : (size_t)b * a.Kp + k;
+    const int kp = a.res_order ? perm32(k & 31) : (k & 31);
+    const size_t at = a.blocked ? ((size_t)(k >> 5) * a.Bp + b) * 32 + kp : (size_t)b * a.Kp + k;
     rows[at] = O::from_f32(xv);
   }
   if (threadIdx.x == 0) a.labels[(size_t)t * a.Bp + b] = valid ? a.y[src] : -1;
@@ -671,8 +672,13 @@ __global__ __launch_bounds__(256) void k_transpose(TransposeArgs a) {
     tile[ty + 8 * i][tx] = src[a.blocked ? ((size_t)blockIdx.x * a.Bp + b) * 32 + tx : (size_t)b * a.Kp + k0 + tx];
   }
   __syncthreads();
+  // resident order: source position p holds input perm32(p); destination
+  // column position c of each 32 rows holds batch row perm32(c)
 #pragma unroll
-  for (int i = 0; i < 4; ++i) dst[(size_t)(k0 + ty + 8 * i) * a.Bp + b0 + tx] = tile[tx][ty + 8 * i];
+  for (int i = 0; i < 4; ++i) {
+    const int kk = ty + 8 * i;
+    dst[(size_t)(k0 + kk) * a.Bp + b0 + tx] = a.res_order ? tile[perm32(tx)][perm32(kk)] : tile[tx][kk];
+  }
 }
 
 // W1 master of a two-layer net between the k-blocked layout [P][Kp/32][Hp][32]

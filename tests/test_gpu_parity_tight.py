@@ -115,15 +115,33 @@ def test_streamed_net_one_step_elementwise(dims, batch, n_train, P):
     _one_step_case(cfg, data, list(range(P)))
 
 
-def test_fused_kernel_rotated_block_order_one_step_elementwise():
-    """Variant v of the fused two-layer kernel visits its column blocks from
-    block (v / 8) mod 25: variants 8 and 23 start at blocks 1 and 2."""
+# The 784-256-10 bf16 nets with a 128-row batch train in the streaming fused
+# kernel; GEVO_RESIDENT=1 selects the resident kernel (a pair of workgroups
+# per variant) for the same shapes.
+KERNELS = ["resident", "streaming"]
+
+
+def _select_kernel(monkeypatch, kernel):
+    if kernel == "resident":
+        monkeypatch.setenv("GEVO_RESIDENT", "1")
+    else:
+        monkeypatch.delenv("GEVO_RESIDENT", raising=False)
+
+
+@pytest.mark.parametrize("kernel", KERNELS)
+def test_fused_kernel_rotated_block_order_one_step_elementwise(kernel, monkeypatch):
+    """Variant v of the streaming fused kernel visits its column blocks from
+    block (v / 8) mod 25: variants 8 and 23 start at blocks 1 and 2.  In the
+    resident kernel variants 16 and 23 are the second pairs of their XCDs."""
+    _select_kernel(monkeypatch, kernel)
     cfg = synthetic.config(3, P=24, lr=(0.05, 0.2))
     data = _data(3, 256, 256, cfg["dims"])
     _one_step_case(cfg, data, [0, 8, 16, 23])
 
 
-def test_fused_kernel_rotated_block_order_epoch():
+@pytest.mark.parametrize("kernel", KERNELS)
+def test_fused_kernel_rotated_block_order_epoch(kernel, monkeypatch):
+    _select_kernel(monkeypatch, kernel)
     cfg = synthetic.config(3, P=24)
     data = _data(3, 700, 300, cfg["dims"])
     pop = _pop(cfg, data)
@@ -137,6 +155,34 @@ def test_fused_kernel_rotated_block_order_epoch():
         assert abs(float(s["train_loss"][v]) - r["train_loss"][-1]) <= 2e-2 * abs(r["train_loss"][-1]), v
         assert abs(float(s["test_loss"][v]) - r["test_loss"]) <= 2e-2 * abs(r["test_loss"]), v
         assert abs(float(s["train_acc"][v]) - r["train_acc"][-1]) <= 0.005, v
+
+
+def test_resident_and_streaming_fused_kernels_agree(monkeypatch):
+    """The two two-layer training kernels on one population (a ragged last
+    batch of 20 rows, more variants than one dispatch round of pairs would
+    need on a small grid): per-variant scores and the trained weights agree
+    to the bf16 rounding of their different fp32 summation orders."""
+    cfg = synthetic.config(3, P=20)
+    data = _data(3, 1300, 300, cfg["dims"])
+    out = {}
+    for kernel in KERNELS:
+        _select_kernel(monkeypatch, kernel)
+        pop = _pop(cfg, data)
+        pop.train_epoch(0)
+        pop.predict()
+        out[kernel] = (pop.scores(), [pop.export(v)["params"] for v in range(cfg["P"])])
+        pop.close()
+    (sa, pa), (sb, pb) = out["resident"], out["streaming"]
+    for k in ("train_loss", "test_loss"):
+        assert np.allclose(sa[k], sb[k], rtol=1e-2, atol=0), k
+    for k in ("train_acc", "test_acc"):
+        assert np.max(np.abs(sa[k] - sb[k])) <= 0.01, k
+    for v in range(cfg["P"]):
+        a, b = pa[v].astype(np.float64), pb[v].astype(np.float64)
+        assert np.array_equal(a == 0, b == 0), v           # masked weights +0 in both
+        big = np.abs(b) > 1e-2 * np.max(np.abs(b))
+        rel = np.abs(a[big] - b[big]) / np.abs(b[big])
+        assert np.median(rel) <= 1e-3 and np.max(np.abs(a - b)) <= 2e-2 * np.max(np.abs(b)), v
 
 
 # --------------------------------------------------------------- prediction
