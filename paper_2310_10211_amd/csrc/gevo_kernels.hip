@@ -27,7 +27,12 @@ namespace gevo {
 
 // ------------------------------------------------------------ population init
 // One thread per (variant, padded output row n, 32-wide word of inputs k):
-// draws the 32 mask bits and initial weights of W_l[n][k0..k0+31].
+// draws the 32 mask bits and initial weights of W_l[n][k0..k0+31].  Rows n
+// are the fastest index, so a wave writes one contiguous 8 KiB span of the
+// k-blocked master, four weights per store.
+// The base-noise draw eps = sqrt(-2 ln u1) cos(2 pi u2) uses the hardware
+// log2 and cos(2 pi x) instructions: their error moves eps by about 1e-6
+// relative, i.e. the weight w (1 + 0.01 eps) by about 1e-8.
 __global__ __launch_bounds__(256) void k_init(InitArgs a) {
   const int words = a.Kp / 32;
   const int64_t total = (int64_t)a.P * a.Np * words;
@@ -35,8 +40,8 @@ __global__ __launch_bounds__(256) void k_init(InitArgs a) {
   const float two_m24 = 5.9604644775390625e-08f;   // 2^-24
   for (int64_t it = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; it < total;
        it += (int64_t)gridDim.x * blockDim.x) {
-    const int kw = (int)(it % words);
-    const int n = (int)((it / words) % a.Np);
+    const int n = (int)(it % a.Np);
+    const int kw = (int)((it / a.Np) % words);
     const int v = (int)(it / ((int64_t)words * a.Np));
     uint32_t bits = 0;
     {
@@ -44,53 +49,64 @@ __global__ __launch_bounds__(256) void k_init(InitArgs a) {
       float* wrow = a.Wm + (size_t)v * a.Np * a.Kp + ((size_t)kw * a.Np + n) * 32;
       uint64_t blk_m = ~0ull, blk_i = ~0ull, blk_n = ~0ull;
       uint4 rm = make_uint4(0, 0, 0, 0), ri = rm, rn = rm;
-      for (int j = 0; j < 32; ++j) {
-        const int k = kw * 32 + j;
-        float w = 0.0f;
-        const bool kept_unit = !a.width_out || (n < (int)a.width_out[v] && k < (int)a.width_in[v]);
-        if (n < a.N && k < a.K) {
-          const uint64_t e = (uint64_t)n * (uint64_t)a.K + (uint64_t)k;
-          bool keep;
-          if (a.prune_off) {
-            keep = true;
-            for (uint32_t q = a.prune_off[v]; q < a.prune_off[v + 1]; ++q) {
-              const uint4 r = philox(make_uint4((uint32_t)(e >> 2), (uint32_t)a.l_index, a.prune_id[q], kStreamMask), key);
-              if ((pick(r, (uint32_t)(e & 3)) >> 8) >= a.prune_th[q]) keep = false;
+      const bool kept_row = !a.width_out || n < (int)a.width_out[v];
+      for (int q = 0; q < 8; ++q) {
+        float wq[4];
+        float4 bq = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        if (a.base_w && n < a.N) bq = *reinterpret_cast<const float4*>(a.base_w + (size_t)n * a.Kp + kw * 32 + 4 * q);
+        const float bqa[4] = {bq.x, bq.y, bq.z, bq.w};
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          const int j = 4 * q + jj, k = kw * 32 + j;
+          float w = 0.0f;
+          const bool kept_unit = kept_row && (!a.width_out || k < (int)a.width_in[v]);
+          if (n < a.N && k < a.K) {
+            const uint64_t e = (uint64_t)n * (uint64_t)a.K + (uint64_t)k;
+            bool keep;
+            if (a.prune_off) {
+              keep = true;
+              for (uint32_t pq = a.prune_off[v]; pq < a.prune_off[v + 1]; ++pq) {
+                const uint4 r = philox(make_uint4((uint32_t)(e >> 2), (uint32_t)a.l_index, a.prune_id[pq], kStreamMask), key);
+                if ((pick(r, (uint32_t)(e & 3)) >> 8) >= a.prune_th[pq]) keep = false;
+              }
+            } else {
+              if ((e >> 2) != blk_m) {
+                blk_m = e >> 2;
+                rm = philox(make_uint4((uint32_t)blk_m, (uint32_t)a.l_index, (uint32_t)v, kStreamMask), key);
+              }
+              keep = (pick(rm, (uint32_t)(e & 3)) >> 8) < th;
             }
-          } else {
-            if ((e >> 2) != blk_m) {
-              blk_m = e >> 2;
-              rm = philox(make_uint4((uint32_t)blk_m, (uint32_t)a.l_index, (uint32_t)v, kStreamMask), key);
+            if (a.base_w) {
+              w = bqa[jj];
+            } else {
+              if ((e >> 2) != blk_i) {
+                blk_i = e >> 2;
+                ri = philox(make_uint4((uint32_t)blk_i, (uint32_t)a.l_index, 0u, kStreamInit), key);
+              }
+              const float u = (float)(pick(ri, (uint32_t)(e & 3)) >> 8) * two_m24;
+              const float t = __fsub_rn(__fmul_rn(2.0f, u), 1.0f);       // exact
+              w = __fmul_rn(t, a.xavier_a);
             }
-            keep = (pick(rm, (uint32_t)(e & 3)) >> 8) < th;
+            if (a.init_kind == 1) {
+              if ((e >> 1) != blk_n) {
+                blk_n = e >> 1;
+                rn = philox(make_uint4((uint32_t)blk_n, (uint32_t)a.l_index, (uint32_t)v, kStreamNoise), key);
+              }
+              const uint32_t w0 = (uint32_t)(e & 1) * 2u;
+              const float u1 = (float)((pick(rn, w0) >> 8) + 1u) * two_m24;   // (0, 1]
+              const float u2 = (float)(pick(rn, w0 + 1) >> 8) * two_m24;      // [0, 1)
+              // -2 ln u1 = -2 ln(2) log2(u1); cos(2 pi u2) takes u2 in turns
+              const float eps = __builtin_amdgcn_sqrtf(-1.3862943611198906f * __builtin_amdgcn_logf(u1)) *
+                                __builtin_amdgcn_cosf(u2);
+              w = __fmul_rn(w, __fadd_rn(1.0f, __fmul_rn(a.noise_std, eps)));
+            }
+            keep = keep && kept_unit;
+            if (!keep) w = 0.0f;
+            bits |= (uint32_t)keep << j;
           }
-          if (a.base_w) {
-            w = a.base_w[(size_t)n * a.Kp + k];
-          } else {
-            if ((e >> 2) != blk_i) {
-              blk_i = e >> 2;
-              ri = philox(make_uint4((uint32_t)blk_i, (uint32_t)a.l_index, 0u, kStreamInit), key);
-            }
-            const float u = (float)(pick(ri, (uint32_t)(e & 3)) >> 8) * two_m24;
-            const float t = __fsub_rn(__fmul_rn(2.0f, u), 1.0f);       // exact
-            w = __fmul_rn(t, a.xavier_a);
-          }
-          if (a.init_kind == 1) {
-            if ((e >> 1) != blk_n) {
-              blk_n = e >> 1;
-              rn = philox(make_uint4((uint32_t)blk_n, (uint32_t)a.l_index, (uint32_t)v, kStreamNoise), key);
-            }
-            const uint32_t w0 = (uint32_t)(e & 1) * 2u;
-            const float u1 = (float)((pick(rn, w0) >> 8) + 1u) * two_m24;   // (0, 1]
-            const float u2 = (float)(pick(rn, w0 + 1) >> 8) * two_m24;
-            const float eps = sqrtf(-2.0f * logf(u1)) * cosf(6.28318530717958647692f * u2);
-            w = __fmul_rn(w, __fadd_rn(1.0f, __fmul_rn(a.noise_std, eps)));
-          }
-          keep = keep && kept_unit;
-          if (!keep) w = 0.0f;
-          bits |= (uint32_t)keep << j;
+          wq[jj] = w;
         }
-        wrow[j] = w;
+        *reinterpret_cast<float4*>(wrow + 4 * q) = make_float4(wq[0], wq[1], wq[2], wq[3]);
       }
       if (kw == 0) {
         const bool bk = n < a.N && (!a.width_out || (n < (int)a.width_out[v] && a.bias_keep[v]));

@@ -52,6 +52,7 @@ constexpr size_t kOutEnd = kOutRed + 8 * 8 + 8 * 4;
 // the output epilogue reuses (and extends) the operand buffers
 constexpr size_t kGemmOutLds = kOutEnd > kGemmLds ? kOutEnd : kGemmLds;
 static_assert(kGemmOutLds <= 160 * 1024, "LDS of one CU");
+static_assert((size_t)kPM * kHS * 2 <= kGemmLds, "the output tile fits in the operand buffers");
 
 __device__ __forceinline__ f32x16_t mma32(u32x4_t a, u32x4_t b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c,
@@ -152,12 +153,15 @@ __global__ __launch_bounds__(kPT, 1) void k_pred_gemm(PredGemmArgs a) {
   }
 
   if constexpr (!OUT) {
-    // bias, ReLU, bf16; lane holds unit l32 of a 32-unit tile and rows crow(r) of a 32-row tile
-    uint16_t* Out = a.O + a.o_vs * v;
+    // bias, ReLU, bf16 into an LDS copy of the tile (lane: unit l32 of a
+    // 32-unit tile, rows crow(r) of a 32-row tile), then every wave writes
+    // whole rows: two 512-byte rows per store instruction
+    __syncthreads();                                   // every wave is done with the operand buffers
+    uint16_t* Ot = reinterpret_cast<uint16_t*>(smem);  // [256 rows][kHS]
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      const int n = n0 + wn * 128 + t * 32 + l32;
-      const float bn = a.bias[(size_t)v * a.Np + n];
+      const int nl = wn * 128 + t * 32 + l32;
+      const float bn = a.bias[(size_t)v * a.Np + n0 + nl];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
         float f[16];
@@ -169,11 +173,17 @@ __global__ __launch_bounds__(kPT, 1) void k_pred_gemm(PredGemmArgs a) {
         uint32_t pk[8];
         to_bf16x2(f, pk);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = r0 + wm * 64 + i * 32 + crow(r, lane);
-          Out[(size_t)row * a.Np + n] = (uint16_t)(pk[r >> 1] >> (16 * (r & 1)));
-        }
+        for (int r = 0; r < 16; ++r)
+          Ot[(wm * 64 + i * 32 + crow(r, lane)) * kHS + nl] = (uint16_t)(pk[r >> 1] >> (16 * (r & 1)));
       }
+    }
+    __syncthreads();
+    uint16_t* Out = a.O + a.o_vs * v + (size_t)r0 * a.Np + n0;
+#pragma unroll
+    for (int it = 0; it < 16; ++it) {
+      const int row = wave * 32 + 2 * it + lh;
+      const u32x4_t val = *reinterpret_cast<const u32x4_t*>(Ot + row * kHS + 8 * l32);
+      *reinterpret_cast<u32x4_t*>(Out + (size_t)row * a.Np + 8 * l32) = val;
     }
   } else {
     // The layer is one tile wide (Np == 256): the tile holds whole rows of
