@@ -462,10 +462,11 @@ gevo_status gevo_cnn_scores(gevo_cnn* h, float* test_loss, float* test_acc, floa
  * shrinking or padding tensors.  The removed layer passes its input on,
  * repaired to the shape the next layer reads: a depthwise layer of stride 2
  * keeps the pixels (2 yo, 2 xo); a pointwise layer keeps its first
- * block_channels[i] channels or appends zero channels.  The variant's
- * master of that layer is overwritten by the layer's identity form (the
- * depthwise centre tap 1, or ones on the pointwise diagonal; every other
- * weight and every bias +0; the mask marks the ones), which computes
+ * block_channels[i] channels or appends channels of value 1 (the value
+ * section 4.1 pads with).  The variant's master of that layer is
+ * overwritten by the layer's identity form (the depthwise centre tap 1, or
+ * ones on the pointwise diagonal; every other weight +0; every bias +0
+ * except 1 for appended channels; the mask marks the ones), which computes
  * exactly that on the layer's non-negative (ReLU) inputs, so later predict
  * calls see the edit and gevo_cnn_export returns that form.  The edit
  * cannot be undone short of a new gevo_cnn_init.  Asynchronous on the
@@ -475,7 +476,8 @@ gevo_status gevo_cnn_scores(gevo_cnn* h, float* test_loss, float* test_acc, floa
 gevo_status gevo_cnn_remove_layer(gevo_cnn* h, uint32_t v, uint32_t layer);
 
 /* Variant v's parameters (canonical layout), mask (uint8 0/1 over the
- * weights, same order) and density rho_v; any output may be NULL. */
+ * weights, same order) and density rho_v (the draw of gevo_cnn_init; not
+ * updated by gevo_cnn_remove_layer); any output may be NULL. */
 gevo_status gevo_cnn_export(gevo_cnn* h, uint32_t v, float* params_out, uint8_t* mask_out, float* density_out);
 
 /* Kernel-level timing, as for gevo_pop_set_profiling: with profiling enabled

@@ -36,7 +36,8 @@ pointwise layer by their definitions; the whole forward against a
 brute-force per-pixel implementation on a tiny net; tensor_init against the
 chain initialisation of the fully connected nets; removed layers (skip plus
 repair) against the same layers with identity weights (the centre tap, or
-the truncated identity matrix, and zero biases).
+the truncated identity matrix with bias 1 on appended channels, and zero
+biases otherwise).
 """
 from __future__ import annotations
 
@@ -163,11 +164,12 @@ def removed_depthwise(a, stride):
 
 def removed_pointwise(a, c_out):
     """A removed pointwise layer: its output is its input, repaired to c_out
-    channels -- the first c_out channels kept, or zero channels appended."""
+    channels -- the first c_out channels kept (values dropped at the tensor's
+    far edge), or channels of value 1 appended (section 4.1 pads with 1)."""
     n, H, Wd, C = a.shape
     if C >= c_out:
         return a[..., :c_out]
-    return np.concatenate([a, np.zeros((n, H, Wd, c_out - C), a.dtype)], axis=3)
+    return np.concatenate([a, np.ones((n, H, Wd, c_out - C), a.dtype)], axis=3)
 
 
 def forward_logits(cfg, params, x, mode="bf16", removed=()):

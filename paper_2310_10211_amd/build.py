@@ -26,7 +26,8 @@ def hipcc() -> str:
 
 
 # kernels whose master prefetches are explicit loads with explicit waits
-PREFETCH_CHECKED = (("gevo_fused.hip", "_ZN4gevo8k_fused2"), ("gevo_stream.hip", "_ZN4gevo14k_stream_layer"))
+PREFETCH_CHECKED = (("gevo_fused.hip", "_ZN4gevo8k_fused2"), ("gevo_stream.hip", "_ZN4gevo14k_stream_layer"),
+                    ("gevo_predict.hip", "_ZN4gevo11k_pred_gemm"))
 
 
 def check_fused_prefetch() -> dict:

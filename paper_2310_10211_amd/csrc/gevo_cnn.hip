@@ -115,10 +115,11 @@ __global__ __launch_bounds__(256) void k_cnn_pack_pairs(const float* __restrict_
 // master (k-blocked [Kp/32][Np][32]), biases [Np] and mask bits ([Np][Kp/32],
 // bit k % 32 of word k / 32): W[k][n] = 1 where k == centre (a depthwise
 // layer's centre tap, for every channel) or, with centre < 0, where k == n (a
-// pointwise layer: channels passed on, zero channels appended or the first N
-// kept); every other weight, the padding and every bias +0.  Every block
-// layer reads a ReLU output, so relu(x 1 + 0) = x exactly and the layer
-// passes its input on.
+// pointwise layer: channels passed on, the first N kept); every other weight
+// and the padding +0, every bias +0 except those of the channels a widening
+// pointwise layer appends, which are 1 (the value section 4.1 pads tensors
+// with: relu(0 + 1) = 1).  Every block layer reads a ReLU output, so
+// relu(x 1 + 0) = x exactly and the layer passes its input on.
 __global__ __launch_bounds__(256) void k_cnn_identity(float* __restrict__ Wm, float* __restrict__ bias,
                                                       uint32_t* __restrict__ mask, int Kp, int Np, int K, int N,
                                                       int centre) {
@@ -134,7 +135,7 @@ __global__ __launch_bounds__(256) void k_cnn_identity(float* __restrict__ Wm, fl
     for (int b = 0; b < 32; ++b) bits |= one(32 * kw + b, n) ? 1u << b : 0u;
     mask[i] = bits;
   }
-  for (int n = t0; n < Np; n += stride) bias[n] = 0.0f;
+  for (int n = t0; n < Np; n += stride) bias[n] = (centre < 0 && n >= K && n < N) ? 1.0f : 0.0f;
 }
 
 typedef __bf16 cnn_bf16x2 __attribute__((ext_vector_type(2)));

@@ -78,21 +78,20 @@ __global__ __launch_bounds__(kPT, 1) void k_pred_gemm(PredGemmArgs a) {
   const uint16_t* W = a.W + ((size_t)v * a.Np + n0) * Kp;
 
   // two register staging sets: thread chunk c = tid + 512 u covers row
-  // (tid >> 3) + 64 u, 16 bytes tid & 7 of the block
+  // (tid >> 3) + 64 u, 16 bytes tid & 7 of the block.  The loads are explicit
+  // instructions and each set is waited for explicitly where it is staged
+  // into LDS: a load the compiler tracked into these loop-carried registers
+  // would make it wait for every outstanding load before the staging, which
+  // drains the second set in flight.
   u32x4_t sa0[4], sw0[4], sa1[4], sw1[4];
   auto load = [&](u32x4_t (&sa)[4], u32x4_t (&sw)[4], int kb) {
     const int k = kb * kPK + (tid & 7) * 8;
-    const bool in = k < Kp;
-    const int kc = in ? k : 0;
+    const int kc = k < Kp ? k : 0;                 // past the input width: an in-bounds re-read, zeroed when staged
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const size_t off = (size_t)((tid >> 3) + 64 * u) * Kp + kc;
-      sa[u] = *reinterpret_cast<const u32x4_t*>(A + off);
-      sw[u] = *reinterpret_cast<const u32x4_t*>(W + off);
-    }
-    if (!in) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) sa[u] = sw[u] = u32x4_t{0u, 0u, 0u, 0u};
+      asm volatile("global_load_dwordx4 %0, %1, off" : "=&v"(sa[u]) : "v"(A + off) : "memory");
+      asm volatile("global_load_dwordx4 %0, %1, off" : "=&v"(sw[u]) : "v"(W + off) : "memory");
     }
   };
   auto store = [&](const u32x4_t (&sa)[4], const u32x4_t (&sw)[4], int buf) {
@@ -104,6 +103,19 @@ __global__ __launch_bounds__(kPT, 1) void k_pred_gemm(PredGemmArgs a) {
       *reinterpret_cast<u32x4_t*>(as + row * kPS + q * 8) = sa[u];
       *reinterpret_cast<u32x4_t*>(ws + row * kPS + q * 8) = sw[u];
     }
+  };
+  // block kb's set into LDS buffer kb & 1 once its eight loads are done:
+  // with YOUNGER the next set's eight loads (issued after it) may stay in flight
+  auto stage = [&](auto youngerc, u32x4_t (&sa)[4], u32x4_t (&sw)[4], int kb) {
+    if constexpr (decltype(youngerc)::value) asm volatile("s_waitcnt vmcnt(8)" : : : "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" : : : "memory");
+#pragma unroll
+    for (int u = 0; u < 4; ++u) asm volatile("" : "+v"(sa[u]), "+v"(sw[u]));
+    if (kb * kPK + (tid & 7) * 8 >= Kp) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) sa[u] = sw[u] = u32x4_t{0u, 0u, 0u, 0u};
+    }
+    store(sa, sw, kb & 1);
   };
 
   f32x16_t acc[2][4];
@@ -134,23 +146,38 @@ __global__ __launch_bounds__(kPT, 1) void k_pred_gemm(PredGemmArgs a) {
   // blocks 0 and 1 in flight, block 0 staged; then at block kb: multiply,
   // stage block kb + 1 (loaded two blocks ago), barrier, load block kb + 3
   // into the set just staged
+  // Block b lives in register set b & 1.  At least three blocks
+  // (pred_gemm_supported), so every wait below is unconditional on its path.
+  const std::true_type younger{};
+  const std::false_type last{};
   load(sa0, sw0, 0);
-  if (nblk > 1) load(sa1, sw1, 1);
-  store(sa0, sw0, 0);
+  load(sa1, sw1, 1);
+  stage(younger, sa0, sw0, 0);
   __syncthreads();
-  if (nblk > 2) load(sa0, sw0, 2);
-  auto iter = [&](int kb, u32x4_t (&sa)[4], u32x4_t (&sw)[4]) {
+  load(sa0, sw0, 2);
+  // blocks 0 .. nblk-3: multiply block kb, stage block kb + 1 (block kb + 2 is
+  // in flight behind it), then load block kb + 3 into the set just staged
+  // (past the last block: an in-bounds re-read of it, never staged)
+  auto mid = [&](int kb, u32x4_t (&sa)[4], u32x4_t (&sw)[4]) {
     compute(kb & 1);
-    if (kb + 1 < nblk) {
-      store(sa, sw, (kb + 1) & 1);
-      __syncthreads();
-      if (kb + 3 < nblk) load(sa, sw, kb + 3);
-    }
+    stage(younger, sa, sw, kb + 1);
+    __syncthreads();
+    load(sa, sw, kb + 3 < nblk ? kb + 3 : nblk - 1);
   };
-  for (int kb = 0; kb < nblk; kb += 2) {
-    iter(kb, sa1, sw1);
-    if (kb + 1 < nblk) iter(kb + 1, sa0, sw0);
+  const int M = nblk - 2;
+  int kb = 0;
+  for (; kb + 1 < M; kb += 2) {
+    mid(kb, sa1, sw1);
+    mid(kb + 1, sa0, sw0);
   }
+  if (kb < M) mid(kb++, sa1, sw1);
+  // block nblk - 2, then the last block, staged after every load has landed
+  compute(kb & 1);
+  asm volatile("s_waitcnt vmcnt(0)" : : : "memory");   // every load, on both paths below
+  if ((kb + 1) & 1) stage(last, sa1, sw1, kb + 1);
+  else stage(last, sa0, sw0, kb + 1);
+  __syncthreads();
+  compute((kb + 1) & 1);
 
   if constexpr (!OUT) {
     // bias, ReLU, bf16 into an LDS copy of the tile (lane: unit l32 of a
@@ -326,7 +353,7 @@ __global__ __launch_bounds__(256) void k_wt_bf16(const float* __restrict__ Wm, u
 }
 
 bool pred_gemm_supported(int Kp, int Np, int R) {
-  return Kp % 32 == 0 && Kp > 0 && Np % kPN == 0 && R % kPM == 0 && R > 0;
+  return Kp % 32 == 0 && Kp > 2 * kPK && Np % kPN == 0 && R % kPM == 0 && R > 0;
 }
 
 hipError_t launch_wt_bf16(const float* Wm, uint16_t* Wb, int P, int Kp, int Np, hipStream_t s, const LaunchEv& ev) {

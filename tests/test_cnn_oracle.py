@@ -166,9 +166,10 @@ def test_variant_params_apply_noise_and_mask_to_the_base():
 # is the identity map plus the shape repair of section 4.1.  On non-negative
 # inputs (every block layer reads a ReLU output) that equals the same layer with
 # identity weights: the depthwise centre tap 1 (at stride 2 it reads exactly the
-# pixels (2 yo, 2 xo)), or the pointwise matrix with ones on its diagonal (zero
-# channels appended when it widens, the first channels kept when it narrows),
-# and zero biases.  These pins compare the skip code against those layers
+# pixels (2 yo, 2 xo)), or the pointwise matrix with ones on its diagonal (the
+# first channels kept when it narrows; when it widens, the appended channels
+# have no weights and bias 1, so relu(1) = 1 pads them with value 1), and zero
+# biases otherwise.  These pins compare the skip code against those layers
 # computed by the convolution code pinned above.
 REMOVAL = dict(C=3, stem=4, blocks=[(1, 3), (2, 5), (2, 2)], classes=3, seed=12, dens=(1.0, 1.0),
                noise_std=0.0)
@@ -187,6 +188,8 @@ def _with_identity(cfg, params, name):
                     W[k, k] = 1.0
             out[off:off + K * N] = W.ravel()
             out[off + K * N:off + K * N + N] = 0.0
+            if name.startswith("pw"):
+                out[off + K * N + K:off + K * N + N] = 1.0     # appended channels (none when N <= K)
             return out
         off += K * N + N
     raise KeyError(name)
@@ -215,7 +218,7 @@ def test_removed_layer_ignores_its_parameters_and_repairs_shapes():
     assert d.shape[1:3] == cnn.conv3x3_depthwise(a, np.ones((9, 3)), 2).shape[1:3]
     assert np.array_equal(cnn.removed_depthwise(a, 1), a)
     wide = cnn.removed_pointwise(a, 5)
-    assert np.array_equal(wide[..., :3], a) and not np.any(wide[..., 3:])
+    assert np.array_equal(wide[..., :3], a) and np.all(wide[..., 3:] == 1.0)
     assert np.array_equal(cnn.removed_pointwise(a, 2), a[..., :2])
     params = np.abs(rng.normal(0, 0.5, cnn.param_count(REMOVAL)))
     x = rng.random((1, 5, 7, 3)).astype(np.float32)

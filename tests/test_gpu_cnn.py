@@ -214,7 +214,7 @@ def _sizes(cfg):
 # layer, section 4.1 repairs the shapes).  Per variant the names it loses;
 # the kinds covered: a stride-1 depthwise layer on the stem output, a
 # stride-2 depthwise layer inside the fused pointwise + depthwise kernel, a
-# widening pointwise layer (32 -> 128 channels, zero channels appended), a
+# widening pointwise layer (32 -> 128 channels, channels of value 1 appended), a
 # narrowing one (256 -> 128, the first kept), a square one, and variant 0
 # left whole.
 REMOVAL_CASES = [
@@ -260,11 +260,13 @@ def test_removed_layers_match_the_oracle(over, gone):
             b = e["params"][off + K * N:off + K * N + N]
             if name in gone.get(v, ()):
                 ident = np.zeros((K, N), np.float32)
+                bias = np.zeros(N, np.float32)
                 if name.startswith("dw"):
                     ident[4, :] = 1.0
                 else:
                     ident[np.arange(min(K, N)), np.arange(min(K, N))] = 1.0
-                assert W.tobytes() == ident.tobytes() and b.tobytes() == np.zeros(N, np.float32).tobytes(), name
+                    bias[K:] = 1.0                                   # appended channels hold the value 1
+                assert W.tobytes() == ident.tobytes() and b.tobytes() == bias.tobytes(), name
                 assert np.array_equal(e["mask"][moff:moff + K * N], (ident != 0).ravel().astype(np.uint8))
             else:
                 assert np.array_equal(e["mask"][moff:moff + K * N], mask[moff:moff + K * N]), (v, name)
