@@ -26,28 +26,38 @@ def hipcc() -> str:
 
 
 # kernels whose master prefetches are explicit loads with explicit waits
-PREFETCH_CHECKED = (("gevo_fused.hip", "_ZN4gevo8k_fused2"), ("gevo_stream.hip", "_ZN4gevo14k_stream_layer"),
-                    ("gevo_predict.hip", "_ZN4gevo11k_pred_gemm"))
+PREFETCH_CHECKED = (("gevo_fused.hip", "_ZN4gevo8k_fused2"), ("gevo_stream.hip", "_ZN4gevo14k_stream_layer"))
+
+
+# kernels whose direct-to-LDS loads read scalar registers from inline assembly
+# (SGPR hazard check only; they stage no prefetch registers)
+DMA_CHECKED = (("gevo_predict.hip", "_ZN4gevo11k_pred_gemm"), ("gevo_resident.hip", "_ZN4gevo6k_res2"))
+
+
+def _device_asm(d: str, src: str) -> str:
+    out = os.path.join(d, src[:-4] + ".s")
+    cmd = [hipcc(), *[f for f in FLAGS if f not in ("-fPIC", "-shared")], "--cuda-device-only", "-S",
+           "-I", os.path.join(ROOT, "include"), "-I", os.path.join(HERE, "csrc"),
+           "-o", out, os.path.join(HERE, "csrc", src)]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError("hipcc -S failed: " + res.stderr[-2000:])
+    with open(out) as f:
+        return f.read()
 
 
 def check_fused_prefetch() -> dict:
-    """Compile the kernels with explicit prefetches to gfx950 assembly and
-    verify their prefetch register discipline (see check_prefetch.py)."""
+    """Compile the kernels with explicit prefetches or direct-to-LDS loads to
+    gfx950 assembly and verify their register discipline (check_prefetch.py)."""
     import tempfile
 
     from . import check_prefetch
     found = {}
     with tempfile.TemporaryDirectory() as d:
         for src, prefix in PREFETCH_CHECKED:
-            out = os.path.join(d, src[:-4] + ".s")
-            cmd = [hipcc(), *[f for f in FLAGS if f not in ("-fPIC", "-shared")], "--cuda-device-only", "-S",
-                   "-I", os.path.join(ROOT, "include"), "-I", os.path.join(HERE, "csrc"),
-                   "-o", out, os.path.join(HERE, "csrc", src)]
-            res = subprocess.run(cmd, capture_output=True, text=True)
-            if res.returncode != 0:
-                raise RuntimeError("hipcc -S failed: " + res.stderr[-2000:])
-            with open(out) as f:
-                found.update(check_prefetch.check_assembly(f.read(), prefix))
+            found.update(check_prefetch.check_assembly(_device_asm(d, src), prefix))
+        for src, prefix in DMA_CHECKED:
+            found.update(check_prefetch.check_scalar_operands(_device_asm(d, src), prefix))
     return found
 
 

@@ -87,6 +87,31 @@ __device__ __forceinline__ void vt_add(unsigned long long* acc, int v, uint64_t 
   if (acc && (threadIdx.x & 63) == 0) atomicAdd(acc + v, (unsigned long long)(vt_now() - t0));
 }
 
+// LDS byte address of a pointer into shared memory.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// One direct-to-LDS load (gfx950 global_load_lds_dwordx4): lane l's 16 bytes
+// at sbase + voff land at LDS address lds + 16 l.  It is an explicit
+// instruction the compiler does not track; the caller waits for it with
+// wait_vm and a barrier before any wave reads the bytes.  m0 is set here; no
+// compiler-generated code of the kernels that use this reads m0.
+__device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t lds) {
+  asm volatile(
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, %1"
+      :
+      : "v"(voff), "s"(sbase), "s"(lds)
+      : "memory");
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
 __device__ __forceinline__ f32x16_t zero16() {
   f32x16_t z;
 #pragma unroll

@@ -235,7 +235,7 @@ hipError_t launch_mask_block_major(const uint32_t* src, uint32_t* dst, int P, in
 hipError_t launch_bf16_check(unsigned long long* counts, hipStream_t s);   // counts zeroed by the caller
 bool fwd_gemm_supported(int Kp, int Np, int R);   // Kp % 32, Np % 128, R % 256
 hipError_t launch_fwd_gemm(const FwdGemmArgs& a, hipStream_t s, const LaunchEv& ev);
-bool pred_gemm_supported(int Kp, int Np, int R);  // Kp % 32, Kp > 128, Np % 256, R % 256
+bool pred_gemm_supported(int Kp, int Np, int R);  // Kp % 32, Np % 256, R % 256
 hipError_t launch_pred_gemm(const PredGemmArgs& a, hipStream_t s, const LaunchEv& ev);
 // k-blocked fp32 master [P][Kp/32][Np][32] -> bf16 [P][Np][Kp] (Np % 256 == 0)
 hipError_t launch_wt_bf16(const float* Wm, uint16_t* Wb, int P, int Kp, int Np, hipStream_t s, const LaunchEv& ev);

@@ -11,11 +11,11 @@
 // One workgroup (eight waves, two per SIMD) computes a 256-row x 256-unit
 // tile of one variant; the waves form a 4 x 2 grid of 64 x 128 tiles of
 // 32x32x16 MFMAs (eight accumulator tiles per wave).  The contraction runs
-// over 64-wide blocks (zero-filled past the input width), double-buffered in
-// LDS and loaded two blocks ahead into two register sets, so each block's
-// loads have two blocks of matrix work to arrive in.  (Four waves of 128 x
-// 128, one per SIMD with loads one block ahead, measured 14% slower: 13.6
-// against 11.8 ms per prediction of the 784 -> 512 layer of 1,024 variants.)
+// over 64-wide blocks (zero-filled past the input width) that reach LDS by
+// direct-to-LDS loads, the input rows one block and the weights two blocks
+// ahead of the multiply, so no registers stage them (two staging sets of
+// registers left the waves, at 256 registers each, no room to read operand
+// fragments ahead).
 // Input rows and weights are both stored with
 // the contraction index contiguous ([row][k] and [unit][k]), so both operand
 // tiles load and read alike.  Workgroups that share a weight tile (same
@@ -38,10 +38,11 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 constexpr int kPM = 256;                 // rows per tile
 constexpr int kPN = 256;                 // units per tile
 constexpr int kPK = 64;                  // contraction per block
-constexpr int kPS = kPK + 8;             // LDS row stride (bf16) of both operand tiles: 144 B
 constexpr int kPT = 512;                 // threads
-constexpr size_t kTileBytes = (size_t)kPM * kPS * 2;
-constexpr size_t kGemmLds = 4 * kTileBytes;            // A and W tiles, two buffers each
+// operand tile in LDS: 256 rows x 64 bf16, 128 B a row, 16-byte chunk c of
+// row r stored at chunk c ^ ((r >> 1) & 7) (conflict-free operand reads)
+constexpr size_t kTileBytes = (size_t)kPM * kPK * 2;
+constexpr size_t kGemmLds = 5 * kTileBytes;            // two A buffers, then three W buffers (160 KiB)
 // output-layer epilogue: hidden tile [256][kHS] bf16, W_L operand [32][kHS] bf16, biases
 constexpr int kHS = kPN + 8;
 constexpr size_t kOutH = 0;
@@ -49,10 +50,11 @@ constexpr size_t kOutW = kOutH + (size_t)kPM * kHS * 2;
 constexpr size_t kOutB = kOutW + (size_t)32 * kHS * 2;
 constexpr size_t kOutRed = kOutB + 32 * 4;             // [8] fp64 loss sums, [8] hit counts
 constexpr size_t kOutEnd = kOutRed + 8 * 8 + 8 * 4;
-// the output epilogue reuses (and extends) the operand buffers
+// the epilogues reuse (and extend) the operand buffers: the output tile
+// [256][kHS] bf16 without the output layer, H, W_L and the sums with it
+constexpr size_t kGemmTileLds = (size_t)kPM * kHS * 2 > kGemmLds ? (size_t)kPM * kHS * 2 : kGemmLds;
 constexpr size_t kGemmOutLds = kOutEnd > kGemmLds ? kOutEnd : kGemmLds;
-static_assert(kGemmOutLds <= 160 * 1024, "LDS of one CU");
-static_assert((size_t)kPM * kHS * 2 <= kGemmLds, "the output tile fits in the operand buffers");
+static_assert(kGemmOutLds <= 160 * 1024 && kGemmTileLds <= 160 * 1024, "LDS of one CU");
 
 __device__ __forceinline__ f32x16_t mma32(u32x4_t a, u32x4_t b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c,
@@ -77,45 +79,46 @@ __global__ __launch_bounds__(kPT, 1) void k_pred_gemm(PredGemmArgs a) {
   const uint16_t* A = a.A + a.a_vs * v + (size_t)r0 * Kp;
   const uint16_t* W = a.W + ((size_t)v * a.Np + n0) * Kp;
 
-  // two register staging sets: thread chunk c = tid + 512 u covers row
-  // (tid >> 3) + 64 u, 16 bytes tid & 7 of the block.  The loads are explicit
-  // instructions and each set is waited for explicitly where it is staged
-  // into LDS: a load the compiler tracked into these loop-carried registers
-  // would make it wait for every outstanding load before the staging, which
-  // drains the second set in flight.
-  u32x4_t sa0[4], sw0[4], sa1[4], sw1[4];
-  auto load = [&](u32x4_t (&sa)[4], u32x4_t (&sw)[4], int kb) {
-    const int k = kb * kPK + (tid & 7) * 8;
-    const int kc = k < Kp ? k : 0;                 // past the input width: an in-bounds re-read, zeroed when staged
+  // Operand blocks go straight to LDS by direct-to-LDS loads: the input rows
+  // (shared by all variants, mostly cache hits) one block ahead into two
+  // buffers, the weights (first read from memory by the row tiles of a
+  // variant) two blocks ahead into three.  Wave w fills rows 32w .. 32w+31 of
+  // a tile, eight rows per instruction: row group j = 4w + jj, lane l -> LDS
+  // chunk 64 j + l = row 8 j + l / 8, stored chunk l % 8, which holds k
+  // chunk (l % 8) ^ ((row >> 1) & 7).  Chunks past the input width are read
+  // from the row's first chunk (in bounds) and zeroed in LDS once landed.
+  const uint16_t* sA = A;
+  const uint16_t* sW = W;
+  const uint32_t lds0 = lds_addr(smem);
+  uint32_t rowoff[4], cpos[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const size_t off = (size_t)((tid >> 3) + 64 * u) * Kp + kc;
-      asm volatile("global_load_dwordx4 %0, %1, off" : "=&v"(sa[u]) : "v"(A + off) : "memory");
-      asm volatile("global_load_dwordx4 %0, %1, off" : "=&v"(sw[u]) : "v"(W + off) : "memory");
+  for (int jj = 0; jj < 4; ++jj) {
+    const int r = 32 * wave + 8 * jj + (lane >> 3);
+    rowoff[jj] = (uint32_t)r * (uint32_t)Kp * 2u;
+    cpos[jj] = (uint32_t)((lane & 7) ^ ((r >> 1) & 7));   // k chunk this lane carries
+  }
+  const int wu = __builtin_amdgcn_readfirstlane(wave);   // the wave index as a scalar (LDS base in m0)
+  auto abuf = [&](int kb) { return (size_t)(kb & 1) * kTileBytes; };
+  auto wbuf = [&](int kb) { return (size_t)(2 + kb % 3) * kTileBytes; };
+  auto issue = [&](const uint16_t* base, size_t buf, int kb) {
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      const int k = kb * kPK + 8 * (int)cpos[jj];
+      const uint32_t voff = rowoff[jj] + (k < Kp ? (uint32_t)k * 2u : 0u);
+      dma16(base, voff, lds0 + (uint32_t)buf + (uint32_t)((4 * wu + jj) * 1024));
     }
   };
-  auto store = [&](const u32x4_t (&sa)[4], const u32x4_t (&sw)[4], int buf) {
-    uint16_t* as = reinterpret_cast<uint16_t*>(smem + (size_t)buf * 2 * kTileBytes);
-    uint16_t* ws = reinterpret_cast<uint16_t*>(smem + (size_t)buf * 2 * kTileBytes + kTileBytes);
+  // after block kb's loads have landed: zero this lane's chunks past the input width
+  auto zero_tail = [&](int kb) {
+    if ((kb + 1) * kPK > Kp) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int row = (tid >> 3) + 64 * u, q = tid & 7;
-      *reinterpret_cast<u32x4_t*>(as + row * kPS + q * 8) = sa[u];
-      *reinterpret_cast<u32x4_t*>(ws + row * kPS + q * 8) = sw[u];
+      for (int jj = 0; jj < 4; ++jj)
+        if (kb * kPK + 8 * (int)cpos[jj] >= Kp) {
+          const size_t at = (size_t)((4 * wave + jj) * 64 + lane) * 16;
+          *reinterpret_cast<u32x4_t*>(smem + abuf(kb) + at) = u32x4_t{0u, 0u, 0u, 0u};
+          *reinterpret_cast<u32x4_t*>(smem + wbuf(kb) + at) = u32x4_t{0u, 0u, 0u, 0u};
+        }
     }
-  };
-  // block kb's set into LDS buffer kb & 1 once its eight loads are done:
-  // with YOUNGER the next set's eight loads (issued after it) may stay in flight
-  auto stage = [&](auto youngerc, u32x4_t (&sa)[4], u32x4_t (&sw)[4], int kb) {
-    if constexpr (decltype(youngerc)::value) asm volatile("s_waitcnt vmcnt(8)" : : : "memory");
-    else asm volatile("s_waitcnt vmcnt(0)" : : : "memory");
-#pragma unroll
-    for (int u = 0; u < 4; ++u) asm volatile("" : "+v"(sa[u]), "+v"(sw[u]));
-    if (kb * kPK + (tid & 7) * 8 >= Kp) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) sa[u] = sw[u] = u32x4_t{0u, 0u, 0u, 0u};
-    }
-    store(sa, sw, kb & 1);
   };
 
   f32x16_t acc[2][4];
@@ -124,60 +127,77 @@ __global__ __launch_bounds__(kPT, 1) void k_pred_gemm(PredGemmArgs a) {
 #pragma unroll
     for (int t = 0; t < 4; ++t) acc[i][t] = zero16();
 
-  auto compute = [&](int buf) {
-    const uint16_t* as = reinterpret_cast<const uint16_t*>(smem + (size_t)buf * 2 * kTileBytes);
-    const uint16_t* ws = reinterpret_cast<const uint16_t*>(smem + (size_t)buf * 2 * kTileBytes + kTileBytes);
+  // one block from LDS buffer buf; fragment rows wm*64 + 32i + l32 (A) and
+  // wn*128 + 32t + l32 (W) all have (row >> 1) & 7 == (l32 >> 1) & 7
+  const int swz = lh ^ ((l32 >> 1) & 7);
+  auto compute = [&](int kb) {
+    const char* as = smem + abuf(kb) + (size_t)(wm * 64 + l32) * 128;
+    const char* ws = smem + wbuf(kb) + (size_t)(wn * 128 + l32) * 128;
 #pragma unroll
     for (int s = 0; s < kPK / 16; ++s) {
+      const int co = 16 * ((2 * s) ^ swz);
       u32x4_t af[2], bf[4];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-        af[i] = *reinterpret_cast<const u32x4_t*>(as + (wm * 64 + i * 32 + l32) * kPS + 16 * s + 8 * lh);
+      for (int i = 0; i < 2; ++i) af[i] = *reinterpret_cast<const u32x4_t*>(as + i * 32 * 128 + co);
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
-        bf[t] = *reinterpret_cast<const u32x4_t*>(ws + (wn * 128 + t * 32 + l32) * kPS + 16 * s + 8 * lh);
+      for (int t = 0; t < 4; ++t) bf[t] = *reinterpret_cast<const u32x4_t*>(ws + t * 32 * 128 + co);
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int t = 0; t < 4; ++t) acc[i][t] = mma32(af[i], bf[t], acc[i][t]);
+        for (int t = 0; t < 4; ++t) acc[i][t] = mma32(bf[t], af[i], acc[i][t]);
     }
   };
-
-  // blocks 0 and 1 in flight, block 0 staged; then at block kb: multiply,
-  // stage block kb + 1 (loaded two blocks ago), barrier, load block kb + 3
-  // into the set just staged
-  // Block b lives in register set b & 1.  At least three blocks
-  // (pred_gemm_supported), so every wait below is unconditional on its path.
-  const std::true_type younger{};
-  const std::false_type last{};
-  load(sa0, sw0, 0);
-  load(sa1, sw1, 1);
-  stage(younger, sa0, sw0, 0);
-  __syncthreads();
-  load(sa0, sw0, 2);
-  // blocks 0 .. nblk-3: multiply block kb, stage block kb + 1 (block kb + 2 is
-  // in flight behind it), then load block kb + 3 into the set just staged
-  // (past the last block: an in-bounds re-read of it, never staged)
-  auto mid = [&](int kb, u32x4_t (&sa)[4], u32x4_t (&sw)[4]) {
-    compute(kb & 1);
-    stage(younger, sa, sw, kb + 1);
-    __syncthreads();
-    load(sa, sw, kb + 3 < nblk ? kb + 3 : nblk - 1);
+  // The tile is accumulated transposed (units x rows): lane l holds row
+  // wm*64 + 32i + l%32 and, in registers 4q..4q+3, the four consecutive
+  // units wn*128 + 32t + 8q + 4(l/32) + 0..3.  bias + ReLU -> bf16 into the
+  // LDS rows dst[row][unit], one 8-byte write per four units.
+  auto tile_to_lds = [&](uint16_t* dst, int stride) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int u = wn * 128 + t * 32 + 8 * q + 4 * lh;
+        const float4 bn = *reinterpret_cast<const float4*>(a.bias + (size_t)v * a.Np + n0 + u);
+        const float bv[4] = {bn.x, bn.y, bn.z, bn.w};
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          float f[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float z = acc[i][t][4 * q + e] + bv[e];
+            f[e] = z > 0.0f ? z : 0.0f;
+          }
+          uint32_t pk[2];
+          to_bf16x2(f, pk);
+          *reinterpret_cast<uint2*>(dst + (size_t)(wm * 64 + i * 32 + l32) * stride + u) = make_uint2(pk[0], pk[1]);
+        }
+      }
   };
-  const int M = nblk - 2;
-  int kb = 0;
-  for (; kb + 1 < M; kb += 2) {
-    mid(kb, sa1, sw1);
-    mid(kb + 1, sa0, sw0);
+
+  // in issue order per block: the A block, then the W block two ahead, so a
+  // wait that leaves four loads in flight covers everything but that W block
+  issue(sA, abuf(0), 0);
+  issue(sW, wbuf(0), 0);
+  if (nblk > 1) {
+    issue(sW, wbuf(1), 1);
+    wait_vm<4>();
+  } else {
+    wait_vm<0>();
   }
-  if (kb < M) mid(kb++, sa1, sw1);
-  // block nblk - 2, then the last block, staged after every load has landed
-  compute(kb & 1);
-  asm volatile("s_waitcnt vmcnt(0)" : : : "memory");   // every load, on both paths below
-  if ((kb + 1) & 1) stage(last, sa1, sw1, kb + 1);
-  else stage(last, sa0, sw0, kb + 1);
+  zero_tail(0);
   __syncthreads();
-  compute((kb + 1) & 1);
+  for (int kb = 0; kb < nblk; ++kb) {
+    // the buffers block kb - 1 used are free (every wave is past the barrier)
+    if (kb + 1 < nblk) issue(sA, abuf(kb + 1), kb + 1);
+    if (kb + 2 < nblk) issue(sW, wbuf(kb + 2), kb + 2);
+    compute(kb);
+    if (kb + 1 < nblk) {
+      if (kb + 2 < nblk) wait_vm<4>();
+      else wait_vm<0>();
+      zero_tail(kb + 1);
+      __syncthreads();
+    }
+  }
 
   if constexpr (!OUT) {
     // bias, ReLU, bf16 into an LDS copy of the tile (lane: unit l32 of a
@@ -185,25 +205,7 @@ __global__ __launch_bounds__(kPT, 1) void k_pred_gemm(PredGemmArgs a) {
     // whole rows: two 512-byte rows per store instruction
     __syncthreads();                                   // every wave is done with the operand buffers
     uint16_t* Ot = reinterpret_cast<uint16_t*>(smem);  // [256 rows][kHS]
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int nl = wn * 128 + t * 32 + l32;
-      const float bn = a.bias[(size_t)v * a.Np + n0 + nl];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        float f[16];
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float z = acc[i][t][r] + bn;
-          f[r] = z > 0.0f ? z : 0.0f;
-        }
-        uint32_t pk[8];
-        to_bf16x2(f, pk);
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          Ot[(wm * 64 + i * 32 + crow(r, lane)) * kHS + nl] = (uint16_t)(pk[r >> 1] >> (16 * (r & 1)));
-      }
-    }
+    tile_to_lds(Ot, kHS);
     __syncthreads();
     uint16_t* Out = a.O + a.o_vs * v + (size_t)r0 * a.Np + n0;
 #pragma unroll
@@ -222,25 +224,7 @@ __global__ __launch_bounds__(kPT, 1) void k_pred_gemm(PredGemmArgs a) {
     float* bL = reinterpret_cast<float*>(smem + kOutB);
     double* red_ce = reinterpret_cast<double*>(smem + kOutRed);
     unsigned int* red_hit = reinterpret_cast<unsigned int*>(smem + kOutRed + 8 * 8);
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int n = wn * 128 + t * 32 + l32;
-      const float bn = a.bias[(size_t)v * a.Np + n];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        float f[16];
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float z = acc[i][t][r] + bn;
-          f[r] = z > 0.0f ? z : 0.0f;
-        }
-        uint32_t pk[8];
-        to_bf16x2(f, pk);
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          H[(wm * 64 + i * 32 + crow(r, lane)) * kHS + n] = (uint16_t)(pk[r >> 1] >> (16 * (r & 1)));
-      }
-    }
+    tile_to_lds(H, kHS);                               // n0 == 0: the layer is this one tile
     // output layer master, k-blocked [Np/32][32 classes][32 inputs]: thread tid
     // converts class tid / 8, inputs 32 (tid % 8) .. +31
     {
@@ -353,7 +337,7 @@ __global__ __launch_bounds__(256) void k_wt_bf16(const float* __restrict__ Wm, u
 }
 
 bool pred_gemm_supported(int Kp, int Np, int R) {
-  return Kp % 32 == 0 && Kp > 2 * kPK && Np % kPN == 0 && R % kPM == 0 && R > 0;
+  return Kp % 32 == 0 && Kp > 0 && Np % kPN == 0 && R % kPM == 0 && R > 0;
 }
 
 hipError_t launch_wt_bf16(const float* Wm, uint16_t* Wb, int P, int Kp, int Np, hipStream_t s, const LaunchEv& ev) {
@@ -365,7 +349,7 @@ hipError_t launch_wt_bf16(const float* Wm, uint16_t* Wb, int P, int Kp, int Np, 
 
 template <bool OUT>
 static hipError_t launch_pg(const PredGemmArgs& a, hipStream_t s, const LaunchEv& ev) {
-  constexpr size_t lds = OUT ? kGemmOutLds : kGemmLds;
+  constexpr size_t lds = OUT ? kGemmOutLds : kGemmTileLds;
   static bool attr = false;
   if (!attr) {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pred_gemm<OUT>),

@@ -116,27 +116,6 @@ __device__ __forceinline__ f32x4_t mma16(uint4 a, uint4 b, f32x4_t c) {
                                                  0, 0, 0);
 }
 
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
-}
-
-// One direct-to-LDS load: lane l's 16 bytes at sbase + voff land at LDS
-// address lds + 16 l.  m0 is set here and read by no compiler-generated code
-// of this kernel.
-__device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t lds) {
-  asm volatile(
-      "s_mov_b32 m0, %2\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %0, %1"
-      :
-      : "v"(voff), "s"(sbase), "s"(lds)
-      : "memory");
-}
-
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
-}
 
 // An opaque copy of a value: lane-dependent indices recomputed from it cannot
 // be hoisted out of a pass, where dozens of them would stay live in registers

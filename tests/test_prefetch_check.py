@@ -135,3 +135,32 @@ def test_sgpr_hazard_through_a_loop_back_edge_is_caught():
         check_prefetch.check_assembly(bad)
     hz = check_prefetch.sgpr_hazards(bad.split("\n"))
     assert len(hz) == 1 and "s[4:5]" in hz[0][2]
+
+
+# ------------------------------------------ direct-to-LDS loads (scalar operands)
+DMA_HEAD = "_ZN4gevo11k_pred_gemmILb0EEEvNS_12PredGemmArgsE:\n"
+DMA = DMA_HEAD + """\
+\ts_add_u32 s20, s6, 0x400
+\t;;#ASMSTART
+\ts_mov_b32 m0, s20
+\ts_nop 0
+\tglobal_load_lds_dwordx4 v12, s[8:9]
+\t;;#ASMEND
+\ts_endpgm
+""" + TAIL
+
+
+def test_direct_to_lds_load_with_scalar_operands_passes():
+    assert check_prefetch.check_scalar_operands(DMA, "_ZN4gevo11k_pred_gemm") == {DMA_HEAD[:-2]: 1}
+
+
+def test_lds_address_from_a_vector_register_is_caught():
+    bad = DMA.replace("s_mov_b32 m0, s20", "s_mov_b32 m0, v140")
+    with pytest.raises(RuntimeError, match="m0 is written from a vector register"):
+        check_prefetch.check_scalar_operands(bad, "_ZN4gevo11k_pred_gemm")
+
+
+def test_direct_to_lds_base_written_by_valu_just_before_is_caught():
+    bad = DMA.replace("\ts_add_u32 s20, s6, 0x400\n", "\tv_readfirstlane_b32 s8, v3\n\tv_readfirstlane_b32 s9, v4\n")
+    with pytest.raises(RuntimeError, match="reads an SGPR fewer than 5 wait states"):
+        check_prefetch.check_scalar_operands(bad, "_ZN4gevo11k_pred_gemm")
