@@ -256,7 +256,8 @@ typedef enum {
   GEVO_EDIT_LR = 0,        /* value = bits of a binary32 learning-rate factor */
   GEVO_EDIT_PRUNE = 1,     /* id = mask draw id, value = keep threshold (<= 2^24) */
   GEVO_EDIT_WIDTH = 2,     /* id = hidden layer l (1 .. L-1), value = units kept (>= 1) */
-  GEVO_EDIT_BIAS_OFF = 3   /* id = layer l (1 .. L): its biases are removed */
+  GEVO_EDIT_BIAS_OFF = 3,  /* id = layer l (1 .. L): its biases are removed */
+  GEVO_EDIT_LAYER_OFF = 4  /* id = hidden layer l (1 .. L-1): the layer is removed */
 } gevo_edit_kind;
 typedef struct {
   uint32_t kind;    /* gevo_edit_kind */
@@ -319,12 +320,21 @@ gevo_status gevo_genomes_breed(uint32_t n, const uint32_t* offsets, const gevo_e
  * other units and their biases; GEVO_EDIT_BIAS_OFF removes the biases of
  * layer `id`.  Removed biases are +0 and stay +0 in training; a variant whose
  * units are removed computes exactly what the narrower network computes.
+ * GEVO_EDIT_LAYER_OFF removes hidden layer `id` (section 6.1 removes a layer;
+ * section 4.1 repairs the shapes): the layer takes its identity form, unit n
+ * passing kept input n on (weight 1 at k == n < min(kept inputs, kept
+ * units)), units beyond the kept inputs holding the value 1 (no weights,
+ * bias 1), every other weight and bias +0, the mask marking the ones; its
+ * pruning edits and bias removal do not apply, and it trains with learning
+ * rate 0 (so it stays the identity while its gradients are finite).  On
+ * non-negative inputs (ReLU outputs, or non-negative data for layer 1) the
+ * layer passes its input on exactly.
  * Weights are the initial weights of gevo_pop_init under the new mask,
  * biases as initialised; the next training epoch is epoch 0 again.  Writes
  * lr_out[P] and density_out[P] when not null: the product of the pruning
  * edits' keep fractions threshold / 2^24 in order, times the fraction of
- * weights the structural edits keep (sum over layers of kept inputs times
- * kept units over sum of d_{l-1} d_l), in binary64.  At most 64 pruning edits
+ * weights the structural edits keep (sum over layers that are not removed of
+ * kept inputs times kept units over sum of d_{l-1} d_l), in binary64.  At most 64 pruning edits
  * per variant.  Synchronous; GEVO_E_ARG for bad offsets, kinds, layers,
  * widths of 0, thresholds above 2^24, a non-finite or non-positive learning
  * rate or too many pruning edits, GEVO_E_ORDER during an epoch. */

@@ -100,7 +100,8 @@ def lib():
             L.or_batch_grad.argtypes = [ctypes.c_int, ctypes.c_int, u32p, f64p, f32p, i32p, ctypes.c_uint32,
                                         ctypes.c_double, f32p, f64p, f64p, f64p, f64p]
             L.or_structure_masks.argtypes = [ctypes.c_int, u32p, u32p, u8p, u8p, u8p]
-            L.or_train_steps.argtypes = [ctypes.c_int, ctypes.c_int, u32p, f64p, u8p, u8p, ctypes.c_float, f32p, i32p,
+            L.or_train_steps.argtypes = [ctypes.c_int, ctypes.c_int, u32p, f64p, u8p, u8p, ctypes.c_uint32,
+                                         ctypes.c_float, f32p, i32p,
                                          ctypes.c_uint32, u32p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
                                          f32p, f64p, u64p]
             L.or_predict.argtypes = [ctypes.c_int, ctypes.c_int, u32p, f64p, f32p, i32p, ctypes.c_uint32,
@@ -269,11 +270,30 @@ def structure_masks(dims, widths, bias_keep, mask=None):
     return m, bm
 
 
-def train_steps(mode, dims, params, mask, lr, X, y, perm, batch, t0, t1, gscale=None, bmask=None):
+def removed_layer_form(dims, widths, l):
+    """The identity form of hidden layer l removed from a net whose layers
+    keep widths[0..L] units (sections 6.1 and 4.1): (W [d_{l-1}][d_l], b
+    [d_l], mask uint8 [d_{l-1}][d_l]).  Unit n passes kept input n on
+    (W[n][n] = 1, n < min(widths[l-1], widths[l])); units widths[l-1] ..
+    widths[l]-1, when the layer is wider than its kept input, hold the value
+    1 (no weights, bias 1: the repair pads with 1); everything else is +0.
+    With ReLU on non-negative inputs the layer passes its input on exactly."""
+    d = [int(x) for x in dims]
+    K, N = d[l - 1], d[l]
+    W = np.zeros((K, N), np.float64)
+    b = np.zeros(N, np.float64)
+    m = min(int(widths[l - 1]), int(widths[l]))
+    W[np.arange(m), np.arange(m)] = 1.0
+    b[int(widths[l - 1]):int(widths[l])] = 1.0
+    return W, b, (W != 0).astype(np.uint8)
+
+
+def train_steps(mode, dims, params, mask, lr, X, y, perm, batch, t0, t1, gscale=None, bmask=None, frozen=0):
     """In-place SGD steps [t0, t1) on ``params``; returns (ce_sum, correct).
     gscale ([batch][C], optional): row i scales the output gradient of row i of
     every batch in place of fl(1/b_t).  bmask (over all biases, optional):
-    biases with 0 stay +0."""
+    biases with 0 stay +0.  frozen: bit l-1 set -> layer l updates with
+    learning rate 0 (a removed layer)."""
     d = _dims(dims)
     assert params.dtype == np.float64 and params.flags.c_contiguous
     mask = np.ascontiguousarray(mask, dtype=np.uint8)
@@ -285,7 +305,8 @@ def train_steps(mode, dims, params, mask, lr, X, y, perm, batch, t0, t1, gscale=
     gs, gsp = _gscale(gscale, batch, int(d[-1]))
     bm = None if bmask is None else np.ascontiguousarray(bmask, dtype=np.uint8)
     rc = lib().or_train_steps(_mode(mode), len(d) - 1, _p(d, ctypes.c_uint32), _p(params, ctypes.c_double),
-                              _p(mask, ctypes.c_uint8), None if bm is None else _p(bm, ctypes.c_uint8), float(lr), _p(X, ctypes.c_float), _p(y, ctypes.c_int32),
+                              _p(mask, ctypes.c_uint8), None if bm is None else _p(bm, ctypes.c_uint8), int(frozen),
+                              float(lr), _p(X, ctypes.c_float), _p(y, ctypes.c_int32),
                               y.shape[0], _p(perm, ctypes.c_uint32), batch, t0, t1, gsp,
                               ctypes.byref(ce), ctypes.byref(corr))
     assert rc == 0, rc

@@ -499,11 +499,13 @@ int or_batch_grad(int mode, int L, const uint32_t* dims, const double* params,
  * mutation).  Update (section 6.2: the mean gradient times the
  * learning rate is subtracted from weights and biases):
  *   W <- mask ? fl(W - fl(lr * dW)) : +0,   b <- bmask ? fl(b - fl(lr * db)) : +0
- * (bmask over all biases, nullable: every bias is trained).
+ * (bmask over all biases, nullable: every bias is trained).  A layer l with
+ * bit l-1 of `frozen` set (a removed layer, sections 6.1 and 4.1: replaced by
+ * the identity map) takes the update with learning rate 0.
  * The loss of step t is taken before its update; ce_sum and correct accumulate.
  */
 int or_train_steps(int mode, int L, const uint32_t* dims, double* params, const uint8_t* mask,
-                   const uint8_t* bmask, float lr, const float* X, const int32_t* y, uint32_t n,
+                   const uint8_t* bmask, uint32_t frozen, float lr, const float* X, const int32_t* y, uint32_t n,
                    const uint32_t* perm, uint32_t batch, uint32_t t0, uint32_t t1, const float* gscale,
                    double* ce_sum, uint64_t* correct) {
   if (check_dims(L, dims)) return -1;
@@ -528,9 +530,9 @@ int or_train_steps(int mode, int L, const uint32_t* dims, double* params, const 
     double scale = (mode == OR_F64) ? 1.0 / (double)b : f32(1.0 / (double)b);
     forward(mode, &w, params, b);
     backward(mode, &w, params, yb, b, scale, gscale, grads, ce_sum, correct, NULL);
-    double lrd = (double)lr;
     size_t bo = 0;
     for (int l = 1; l <= L; ++l) {
+      const double lrd = ((frozen >> (l - 1)) & 1u) ? 0.0 : (double)lr;
       uint32_t din = dims[l - 1], dout = dims[l];
       double* W = params + w_off(dims, l);
       double* dW = grads + w_off(dims, l);

@@ -60,7 +60,7 @@ import numpy as np
 from . import philox
 
 STREAM_SELECT, STREAM_CROSS, STREAM_MUT = 7, 8, 9
-LR_EDIT, PRUNE_EDIT, WIDTH_EDIT, BIAS_EDIT = 0, 1, 2, 3
+LR_EDIT, PRUNE_EDIT, WIDTH_EDIT, BIAS_EDIT, LAYER_EDIT = 0, 1, 2, 3, 4
 INF = float("inf")
 
 
@@ -166,18 +166,22 @@ def select(rank, dist, n_elite, n_select, seed, gen):
 
 def random_edit(seed, gen, i, j, edit_id, rho_lo, struct_p=0.0, dims=None):
     """The edit drawn from (j, gen, i, 9): with probability struct_p a
-    structural edit (bias removal or a hidden width), otherwise with equal
-    odds a learning-rate factor log-uniform on [1/2, 2] or pruning at a
-    density uniform on [rho_lo, 1]."""
+    structural edit (bias removal; for nets with hidden layers, with equal
+    odds bias removal, a hidden width or a removed hidden layer), otherwise
+    with equal odds a learning-rate factor log-uniform on [1/2, 2] or
+    pruning at a density uniform on [rho_lo, 1]."""
     w = _draw(seed, j, gen, i, STREAM_MUT)
     u = _u24(w[2])
     uk = _u24(w[1])
     if uk < struct_p:
         L = len(dims) - 1
-        if _u24(w[3]) < 0.5 or L < 2:
+        us = _u24(w[3])
+        if us < 1.0 / 3.0 or L < 2:
             return (BIAS_EDIT, 1 + _below(w[0], L), 0)
         layer = 1 + _below(w[0], L - 1)
-        return (WIDTH_EDIT, layer, 1 + _below(w[2], int(dims[layer])))
+        if us < 2.0 / 3.0:
+            return (WIDTH_EDIT, layer, 1 + _below(w[2], int(dims[layer])))
+        return (LAYER_EDIT, layer, 0)
     if uk < struct_p + (1.0 - struct_p) * 0.5:
         factor = _f32(math.exp(math.log(0.5) + u * math.log(4.0)))
         return (LR_EDIT, edit_id, _f32_bits(factor))
@@ -246,14 +250,31 @@ def structure(edits, dims):
         elif kind == BIAS_EDIT:
             assert 1 <= eid <= L
             keep[eid - 1] = 0
+    for kind, eid, value in edits:                # a removed layer keeps its identity-form biases
+        if kind == LAYER_EDIT:
+            keep[eid - 1] = 1
     return widths, keep
+
+
+def removed_layers(edits, dims):
+    """[L] flags: hidden layer l (1 .. L-1) removed by a LAYER_EDIT (the
+    identity map in place of the layer, frozen in training)."""
+    L = len(dims) - 1
+    gone = [0] * L
+    for kind, eid, value in edits:
+        if kind == LAYER_EDIT:
+            assert 1 <= eid <= L - 1
+            gone[eid - 1] = 1
+    return gone
 
 
 def density(edits, dims):
     """Expected kept fraction of the weights: the pruning edits' keep
-    fractions in order, times the fraction the structural edits keep."""
+    fractions in order, times the fraction the structural edits keep (a
+    removed layer keeps none of its weights)."""
     dens = apply(edits, 1.0)[3]
     widths, _ = structure(edits, dims)
-    kept = sum(widths[l - 1] * widths[l] for l in range(1, len(dims)))
+    gone = removed_layers(edits, dims)
+    kept = sum(widths[l - 1] * widths[l] for l in range(1, len(dims)) if not gone[l - 1])
     total = sum(int(dims[l - 1]) * int(dims[l]) for l in range(1, len(dims)))
     return dens * (kept / total)

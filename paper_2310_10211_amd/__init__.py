@@ -21,7 +21,7 @@ import numpy as np
 
 __all__ = ["Population", "lib", "epoch_permutation", "check_bf16_rounding", "GevoError", "config_struct",
            "workspace_bytes", "nsga2_rank", "nsga2_select", "genomes_initial", "genomes_breed", "EDIT_LR",
-           "EDIT_PRUNE", "EDIT_WIDTH", "EDIT_BIAS_OFF"]
+           "EDIT_PRUNE", "EDIT_WIDTH", "EDIT_BIAS_OFF", "EDIT_LAYER_OFF"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgevo.so")
@@ -56,7 +56,7 @@ class GevoEdit(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_uint32), ("id", ctypes.c_uint32), ("value", ctypes.c_uint32)]
 
 
-EDIT_LR, EDIT_PRUNE, EDIT_WIDTH, EDIT_BIAS_OFF = 0, 1, 2, 3
+EDIT_LR, EDIT_PRUNE, EDIT_WIDTH, EDIT_BIAS_OFF, EDIT_LAYER_OFF = 0, 1, 2, 3, 4
 
 
 class GevoCnnConfig(ctypes.Structure):

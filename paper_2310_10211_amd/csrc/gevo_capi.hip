@@ -28,6 +28,7 @@ struct LayerLay {
   size_t Wm = 0, bias = 0, mask = 0, Wt = 0, base_w = 0, base_b = 0;
   size_t bmask = 0;                                // [P][Np/32] bias-trained bits
   size_t win = 0, wout = 0, bkeep = 0;             // [P] structural edits (gevo_pop_set_genomes)
+  size_t ident = 0;                                // [P] removed layer: identity form (gevo_pop_set_genomes)
   size_t arows[2] = {0, 0}, acols[2] = {0, 0};   // training activations (hidden layers)
   size_t gcols = 0, grows = 0;                     // gradient at this layer's output (hidden)
   size_t prows = 0;                                // predict activations
@@ -48,6 +49,7 @@ struct Layout {
   LayerLay lay[GEVO_MAX_LAYERS];
   size_t prune_off = 0, prune_id = 0, prune_th = 0;   // genome pruning edits (gevo_pop_set_genomes)
   size_t gscale = 0;                               // [P][Bp][32] output-gradient scales (gevo_pop_set_grad_scale)
+  size_t lrh = 0;                                  // [L][P] learning rate of each layer (0: a removed layer)
   size_t lr = 0, thresh = 0, train_ce = 0, train_corr = 0, test_ce = 0, test_corr = 0, part_ce = 0,
          part_corr = 0, xrows = 0, xcols = 0, yep = 0, xte = 0, yte = 0, perm = 0;
   size_t w1img = 0, m1blk = 0;                    // fused training: W1 register image, block-major W1 mask
@@ -148,6 +150,7 @@ gevo_status make_layout(const gevo_pop_config* c, Layout* o) {
     q.win = take(P * 4);
     q.wout = take(P * 4);
     q.bkeep = take(P * 4);
+    q.ident = take(P * 4);
     q.base_w = take(Np * Kp * 4);
     q.base_b = take(Np * 4);
     if (l >= 1 && l < y.L - 1) q.Wt = take(P * Kp * Np * e);         // hidden layer >= 2
@@ -167,6 +170,7 @@ gevo_status make_layout(const gevo_pop_config* c, Layout* o) {
     }
   }
   y.lr = take(P * 4);
+  y.lrh = take((size_t)y.L * P * 4);
   y.thresh = take(P * 4);
   y.prune_off = take((P + 1) * 4);
   y.gscale = take(P * Bp * 32 * 4);
@@ -478,7 +482,7 @@ gevo_status train_step(gevo_pop* p, int t) {
     LayerArgs<S> a{};
     a.Kp = q.Kp; a.Np = q.Np; a.Bp = y.Bp;
     a.Wm = at<float>(p, q.Wm); a.bias = at<float>(p, q.bias); a.mask = at<uint32_t>(p, q.mask); a.bmask = at<uint32_t>(p, q.bmask);
-    a.lr = at<float>(p, y.lr);
+    a.lr = at<float>(p, y.lrh) + (size_t)l * y.P;   // 0 for the variants that removed this layer
     a.do_update = 1;
     a.Gcols = at<S>(p, q.gcols); a.g_vs = (size_t)q.Np * y.Bp;
     if (l == 0) { a.Acols = xcols_t; a.ac_vs = 0; }
@@ -588,7 +592,8 @@ gevo_status do_train_steps(gevo_pop* p, uint32_t epoch, uint32_t s0, uint32_t s1
     f.W1 = at<float>(p, y.w1img); f.b1 = at<float>(p, q1.bias); f.m1 = at<uint32_t>(p, y.m1blk);
     f.W2 = at<float>(p, q2.Wm); f.b2 = at<float>(p, q2.bias); f.m2 = at<uint32_t>(p, q2.mask);
     f.bm1 = at<uint32_t>(p, q1.bmask); f.bm2 = at<uint32_t>(p, q2.bmask);
-    f.lr = at<float>(p, y.lr);
+    f.lr = at<float>(p, y.lrh);                   // hidden layer (0 where removed)
+    f.lr2 = at<float>(p, y.lrh) + y.P;            // output layer
     f.gscale = p->gscale_on ? at<float>(p, y.gscale) : nullptr;
     f.ce_acc = at<double>(p, y.train_ce);
     f.correct_acc = at<unsigned long long>(p, y.train_corr);
@@ -962,6 +967,7 @@ static gevo_status init_layers(gevo_pop* p, bool genomes) {
       a.width_in = reinterpret_cast<const uint32_t*>(p->ws + q.win);
       a.width_out = reinterpret_cast<const uint32_t*>(p->ws + q.wout);
       a.bias_keep = reinterpret_cast<const uint32_t*>(p->ws + q.bkeep);
+      a.ident = reinterpret_cast<const uint32_t*>(p->ws + q.ident);
     }
     a.Wm = reinterpret_cast<float*>(p->ws + q.Wm);
     a.bias = reinterpret_cast<float*>(p->ws + q.bias);
@@ -1030,6 +1036,10 @@ gevo_status gevo_pop_init(const gevo_pop_config* cfg, void* d_ws, size_t ws_byte
   if (hipMemcpyAsync(p->ws + y.lr, p->lr.data(), (size_t)P * 4, hipMemcpyHostToDevice, s) != hipSuccess ||
       hipMemcpyAsync(p->ws + y.thresh, p->thresh.data(), (size_t)P * 4, hipMemcpyHostToDevice, s) != hipSuccess)
     return fail(GEVO_E_HIP);
+  for (int l = 0; l < y.L; ++l)                  // every layer trains at the variant's rate
+    if (hipMemcpyAsync(p->ws + y.lrh + (size_t)l * P * 4, p->lr.data(), (size_t)P * 4, hipMemcpyHostToDevice, s) !=
+        hipSuccess)
+      return fail(GEVO_E_HIP);
   // optional base model, padded and transposed to the device layout
   std::vector<std::vector<float>> base_w(y.L), base_b(y.L);
   if (cfg->init == GEVO_INIT_BASE_NOISE && cfg->base_params) {
@@ -1087,7 +1097,7 @@ gevo_status gevo_pop_set_genomes(gevo_pop* p, float lr_base, const uint32_t* off
   std::vector<float> lr(P);
   std::vector<double> dens(P);
   std::vector<uint32_t> off(P + 1, 0), ids, th;
-  std::vector<uint32_t> width((size_t)P * (L + 1)), bkeep((size_t)P * L, 1u);
+  std::vector<uint32_t> width((size_t)P * (L + 1)), bkeep((size_t)P * L, 1u), gone((size_t)P * L, 0u);
   double total_w = 0.0;
   for (int l = 1; l <= L; ++l) total_w += (double)y.lay[l - 1].K * (double)y.lay[l - 1].N;
   for (int v = 0; v < P; ++v) {
@@ -1114,12 +1124,18 @@ gevo_status gevo_pop_set_genomes(gevo_pop* p, float lr_base, const uint32_t* off
       } else if (e.kind == GEVO_EDIT_BIAS_OFF) {
         if (e.id < 1 || (int)e.id > L) return GEVO_E_ARG;
         bkeep[(size_t)v * L + e.id - 1] = 0u;
+      } else if (e.kind == GEVO_EDIT_LAYER_OFF) {
+        if (e.id < 1 || (int)e.id > L - 1) return GEVO_E_ARG;
+        gone[(size_t)v * L + e.id - 1] = 1u;
       } else {
         return GEVO_E_ARG;
       }
     }
     double kept_w = 0.0;
-    for (int l = 1; l <= L; ++l) kept_w += (double)wv[l - 1] * (double)wv[l];
+    for (int l = 1; l <= L; ++l)
+      if (!gone[(size_t)v * L + l - 1]) kept_w += (double)wv[l - 1] * (double)wv[l];
+    for (int l = 1; l < L; ++l)                  // a removed layer keeps its identity biases
+      if (gone[(size_t)v * L + l - 1]) bkeep[(size_t)v * L + l - 1] = 1u;
     d = d * (kept_w / total_w);
     if (!(r > 0.0f) || !std::isfinite(r)) return GEVO_E_ARG;
     lr[v] = r;
@@ -1129,18 +1145,25 @@ gevo_status gevo_pop_set_genomes(gevo_pop* p, float lr_base, const uint32_t* off
   hipStream_t s = p->stream;
   HIP_TRY(hipStreamSynchronize(s));              // nothing may still read the state being replaced
   HIP_TRY(hipMemcpy(p->ws + y.lr, lr.data(), (size_t)P * 4, hipMemcpyHostToDevice));
+  for (int l = 0; l < L; ++l) {                  // per-layer rates: 0 for a removed (frozen) layer
+    std::vector<float> lrl(P);
+    for (int v = 0; v < P; ++v) lrl[v] = gone[(size_t)v * L + l] ? 0.0f : lr[v];
+    HIP_TRY(hipMemcpy(p->ws + y.lrh + (size_t)l * P * 4, lrl.data(), (size_t)P * 4, hipMemcpyHostToDevice));
+  }
   HIP_TRY(hipMemcpy(p->ws + y.prune_off, off.data(), off.size() * 4, hipMemcpyHostToDevice));
   if (!ids.empty()) {
     HIP_TRY(hipMemcpy(p->ws + y.prune_id, ids.data(), ids.size() * 4, hipMemcpyHostToDevice));
     HIP_TRY(hipMemcpy(p->ws + y.prune_th, th.data(), th.size() * 4, hipMemcpyHostToDevice));
   }
   for (int l = 0; l < L; ++l) {                  // per-layer structural arrays of the init kernel
-    std::vector<uint32_t> win(P), wout(P), bk(P);
+    std::vector<uint32_t> win(P), wout(P), bk(P), id(P);
     for (int v = 0; v < P; ++v) {
       win[v] = width[(size_t)v * (L + 1) + l];
       wout[v] = width[(size_t)v * (L + 1) + l + 1];
       bk[v] = bkeep[(size_t)v * L + l];
+      id[v] = gone[(size_t)v * L + l];
     }
+    HIP_TRY(hipMemcpy(p->ws + y.lay[l].ident, id.data(), (size_t)P * 4, hipMemcpyHostToDevice));
     HIP_TRY(hipMemcpy(p->ws + y.lay[l].win, win.data(), (size_t)P * 4, hipMemcpyHostToDevice));
     HIP_TRY(hipMemcpy(p->ws + y.lay[l].wout, wout.data(), (size_t)P * 4, hipMemcpyHostToDevice));
     HIP_TRY(hipMemcpy(p->ws + y.lay[l].bkeep, bk.data(), (size_t)P * 4, hipMemcpyHostToDevice));

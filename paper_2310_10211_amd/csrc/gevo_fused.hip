@@ -157,6 +157,7 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
   float* W2 = a.W2 + (size_t)v * 32 * HP;
   const uint32_t* m2 = a.m2 + (size_t)v * 32 * (HP / 32);
   const float lrv = a.lr[v];
+  const float lrv2 = a.lr2 ? a.lr2[v] : lrv;   // output layer (the hidden layer's rate is 0 when removed)
   // Every pass visits the column blocks in the order rot, rot+1, ... (mod nkb).
   // All workgroups read the same shared X blocks; workgroup v runs on XCD
   // v mod 8, and staggering the start block over the workgroups of one XCD
@@ -395,7 +396,7 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
       float db = 0.0f;
 #pragma unroll
       for (int part = 0; part < Ly::NDP; ++part) db += dbp[part * 32 + tid];
-      b2s[tid] = b2k ? __fsub_rn(b2s[tid], __fmul_rn(lrv, db)) : 0.0f;
+      b2s[tid] = b2k ? __fsub_rn(b2s[tid], __fmul_rn(lrv2, db)) : 0.0f;
     }
     if (wave == NW - 1) {
       double sc = 0.0;
@@ -661,7 +662,7 @@ __global__ __launch_bounds__(2 * HP, 1) void k_fused2(Fused2Args a) {
     {
       float f[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) f[r] = ((m2bits >> r) & 1u) ? __fsub_rn(w2v[r], __fmul_rn(lrv, d2[r])) : 0.0f;
+      for (int r = 0; r < 16; ++r) f[r] = ((m2bits >> r) & 1u) ? __fsub_rn(w2v[r], __fmul_rn(lrv2, d2[r])) : 0.0f;
       uint32_t p[8];
       to_bf16x2(f, p);
 #pragma unroll

@@ -48,6 +48,10 @@ struct InitArgs {
   const uint32_t* width_in;      // [P]
   const uint32_t* width_out;     // [P]
   const uint32_t* bias_keep;     // [P]
+  // optional removed layers: variant v with ident[v] != 0 gets the identity
+  // form (W[k][k] = 1 for k < min(width_in, width_out), bias 1 for units
+  // width_in <= n < width_out, everything else +0; the mask marks the ones)
+  const uint32_t* ident;         // [P]
   float* Wm;                     // [P][Kp/32][Np][32] (k-blocked)
   float* bias;                   // [P][Np]
   uint32_t* mask;                // [P][Np][Kp/32] row words
@@ -165,7 +169,8 @@ struct Fused2Args {
   float* W1; float* b1; const uint32_t* m1;   // register image (see launch_w1_image), [P][Hp], [P][Kp/32][Hp]
   float* W2; float* b2; const uint32_t* m2;   // [P][Hp/32][32][32], [P][32], [P][32][Hp/32]
   const uint32_t* bm1; const uint32_t* bm2;   // bias masks [P][Hp/32], [P] (bit = bias trained)
-  const float* lr;
+  const float* lr;               // [P] learning rate of W1, b1 (0 for a removed hidden layer)
+  const float* lr2;              // [P] learning rate of W2, b2
   double* ce_acc;
   unsigned long long* correct_acc;
   const float* gscale;           // [P][Bp][32] per-element output-gradient scale (nullable: fl32(1/b_t))

@@ -44,7 +44,22 @@ __global__ __launch_bounds__(256) void k_init(InitArgs a) {
     const int kw = (int)((it / a.Np) % words);
     const int v = (int)(it / ((int64_t)words * a.Np));
     uint32_t bits = 0;
-    {
+    if (a.ident && a.ident[v]) {                   // a removed layer: its identity form
+      const int win = (int)a.width_in[v], wout = (int)a.width_out[v], m = win < wout ? win : wout;
+      float* wrow = a.Wm + (size_t)v * a.Np * a.Kp + ((size_t)kw * a.Np + n) * 32;
+      for (int q = 0; q < 8; ++q) {
+        float wq[4];
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          const int j = 4 * q + jj, k = kw * 32 + j;
+          const bool one = k == n && n < m;
+          wq[jj] = one ? 1.0f : 0.0f;
+          bits |= (uint32_t)one << j;
+        }
+        *reinterpret_cast<float4*>(wrow + 4 * q) = make_float4(wq[0], wq[1], wq[2], wq[3]);
+      }
+      if (kw == 0) a.bias[(size_t)v * a.Np + n] = (n >= win && n < wout) ? 1.0f : 0.0f;
+    } else {
       const uint32_t th = a.thresh[v];
       float* wrow = a.Wm + (size_t)v * a.Np * a.Kp + ((size_t)kw * a.Np + n) * 32;
       uint64_t blk_m = ~0ull, blk_i = ~0ull, blk_n = ~0ull;

@@ -212,6 +212,7 @@ __global__ __launch_bounds__(kT, 1) void k_res2(Res2Args ra) {
     float* W2 = a.W2 + (size_t)v * 32 * HP;
     const uint32_t* m2 = a.m2 + (size_t)v * 32 * NWF;
     const float lrv = a.lr[v];
+    const float lrv2 = a.lr2 ? a.lr2[v] : lrv;   // output layer (the hidden layer's rate is 0 when removed)
 
     // ---- resident state of this half (register indices are compile-time constants)
     for_each_job(
@@ -350,7 +351,7 @@ __global__ __launch_bounds__(kT, 1) void k_res2(Res2Args ra) {
         float db = 0.0f;
 #pragma unroll
         for (int part = 0; part < Lds::NDP; ++part) db += dbp[part * 16 + tid];
-        b2s[tid] = b2k ? __fsub_rn(b2s[tid], __fmul_rn(lrv, db)) : 0.0f;
+        b2s[tid] = b2k ? __fsub_rn(b2s[tid], __fmul_rn(lrv2, db)) : 0.0f;
       }
       if (wave == kW - 1) {
         double sc = 0.0;
@@ -561,7 +562,7 @@ __global__ __launch_bounds__(kT, 1) void k_res2(Res2Args ra) {
       {
         float f[8];
 #pragma unroll
-        for (int r = 0; r < 8; ++r) f[r] = ((m2bits >> r) & 1u) ? __fsub_rn(w2v[r], __fmul_rn(lrv, d2[r])) : 0.0f;
+        for (int r = 0; r < 8; ++r) f[r] = ((m2bits >> r) & 1u) ? __fsub_rn(w2v[r], __fmul_rn(lrv2, d2[r])) : 0.0f;
 #pragma unroll
         for (int r = 0; r < 8; ++r) w2[crow(r, lane) * Lds::AS + nl] = O::from_f32(f[r]);
 #pragma unroll

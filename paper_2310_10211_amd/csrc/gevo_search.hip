@@ -53,7 +53,8 @@ struct NetShape {
 };
 
 // the edit drawn from (j, gen, i, mutation stream): with probability struct_p
-// a structural edit (bias removal, or a width of a hidden layer), otherwise a
+// a structural edit (bias removal; with hidden layers, bias removal, a width
+// of a hidden layer or a removed hidden layer with equal odds), otherwise a
 // learning-rate factor log-uniform on [1/2, 2] or pruning at a density
 // uniform on [rho_lo, 1], with equal odds
 gevo_edit random_edit(uint64_t seed, uint32_t gen, uint32_t i, uint32_t j, uint32_t id, double rho_lo,
@@ -63,14 +64,19 @@ gevo_edit random_edit(uint64_t seed, uint32_t gen, uint32_t i, uint32_t j, uint3
   const double u = u24(w[2]), uk = u24(w[1]);
   gevo_edit e{};
   if (uk < struct_p) {
-    if (u24(w[3]) < 0.5 || net.L < 2) {
+    const double us = u24(w[3]);
+    if (us < 1.0 / 3.0 || net.L < 2) {
       e.kind = GEVO_EDIT_BIAS_OFF;
       e.id = 1 + below(w[0], net.L);
       e.value = 0;
-    } else {
+    } else if (us < 2.0 / 3.0) {
       e.kind = GEVO_EDIT_WIDTH;
       e.id = 1 + below(w[0], net.L - 1);
       e.value = 1 + below(w[2], net.dims[e.id]);
+    } else {
+      e.kind = GEVO_EDIT_LAYER_OFF;
+      e.id = 1 + below(w[0], net.L - 1);
+      e.value = 0;
     }
     return e;
   }

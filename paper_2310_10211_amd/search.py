@@ -4,9 +4,9 @@ GPU, then ranked, selected and bred by the library's host code.
 
 An individual is a list of edits (patch representation, section 4.2) whose
 effects are a changed learning rate (section 6.2) and pruned weights
-(abstract), optionally also removed biases (section 6.1) and narrowed
-hidden layers (the tensor-shrinking repair, section 4.1) with probability
-struct_p per drawn edit.  Fitness (section 4.3) is minimised over two objectives:
+(abstract), optionally also removed biases and removed hidden layers
+(section 6.1) and narrowed hidden layers (the tensor-shrinking repair,
+section 4.1) with probability struct_p per drawn edit.  Fitness (section 4.3) is minimised over two objectives:
   * model error: the training-split error of the last epoch (the paper
     computes accuracy on the training split during the search and keeps the
     test split for checking the result afterwards, section 5);

@@ -146,25 +146,37 @@ def _struct_genomes(P, dims, seed):
     if L > 1:
         gs[1] = [(ns.WIDTH_EDIT, 1, max(1, dims[1] // 3)), (ns.BIAS_EDIT, 1, 0)]
         gs[2] = gs[2] + [(ns.WIDTH_EDIT, 1, dims[1] - 5), (ns.WIDTH_EDIT, 1, dims[1] - 9)]
+        gs[3] = [(ns.LAYER_EDIT, L - 1, 0), (ns.PRUNE_EDIT, 77, 2 ** 23)]   # the last hidden layer removed
+        if L > 2:
+            gs[3].append((ns.WIDTH_EDIT, 1, dims[L - 1] // 2))       # its kept input narrower than its units
     return gs
 
 
 def _struct_reference(cfg, genome, lr_base):
+    """(lr, mask, bias mask, params, frozen layer bits) of a genome."""
     dims = cfg["dims"]
     lr, ids, th, _ = ns.apply(genome, lr_base)
     widths, keep = ns.structure(genome, dims)
+    gone = ns.removed_layers(genome, dims)
     mask, bmask = oracle.structure_masks(dims, widths, keep, oracle.genome_mask(cfg["seed"], dims, ids, th))
     full, _ = oracle.variant_init(cfg["seed"], 0, dims, 1 << 24)
     params = full.copy()
     off, moff, boff = 0, 0, 0
     for l in range(1, len(dims)):
         k = dims[l - 1] * dims[l]
-        params[off:off + k] *= mask[moff:moff + k]
-        params[off + k:off + k + dims[l]] *= bmask[boff:boff + dims[l]]
+        if gone[l - 1]:                                       # the identity form, frozen in training
+            W, b, m = oracle.removed_layer_form(dims, widths, l)
+            params[off:off + k] = W.ravel()
+            params[off + k:off + k + dims[l]] = b
+            mask[moff:moff + k] = m.ravel()
+        else:
+            params[off:off + k] *= mask[moff:moff + k]
+            params[off + k:off + k + dims[l]] *= bmask[boff:boff + dims[l]]
         off += k + dims[l]
         moff += k
         boff += dims[l]
-    return lr, mask, bmask, params
+    frozen = sum(1 << l for l in range(len(gone)) if gone[l])
+    return lr, mask, bmask, params, frozen
 
 
 @pytest.mark.parametrize("i,dims", [(1, None), (3, None), (3, [200, 96, 64, 10]),
@@ -183,7 +195,7 @@ def test_structural_genomes_rebuild_and_train_like_the_oracle(i, dims):
     refs = [_struct_reference(cfg, genomes[v], 0.05) for v in range(4)]
     for v in range(4):
         e = pop.export(v)
-        r_lr, r_mask, r_bmask, r_params = refs[v]
+        r_lr, r_mask, r_bmask, r_params, _ = refs[v]
         assert np.array_equal(e["mask"], r_mask), v
         assert np.array_equal(e["params"].astype(np.float64), r_params), v
         assert lr[v] == np.float32(r_lr) and dens[v] == ns.density(genomes[v], cfg["dims"])
@@ -192,12 +204,19 @@ def test_structural_genomes_rebuild_and_train_like_the_oracle(i, dims):
     n = len(data["y_train"])
     perm = oracle.permutation(cfg["seed"], 0, n)
     for v in range(4):
-        r_lr, r_mask, r_bmask, r_params = refs[v]
+        r_lr, r_mask, r_bmask, r_params, frozen = refs[v]
         params = r_params.copy()
         ce, _ = oracle.train_steps(mode, cfg["dims"], params, r_mask, float(r_lr), data["x_train"], data["y_train"],
-                                   perm, cfg["batch"], 0, -(-n // cfg["batch"]), bmask=r_bmask)
+                                   perm, cfg["batch"], 0, -(-n // cfg["batch"]), bmask=r_bmask, frozen=frozen)
         assert abs(float(s["train_loss"][v]) - ce / n) <= rtol * abs(ce / n), (v, s["train_loss"][v], ce / n)
         e = pop.export(v)
+        if frozen:                                            # a removed layer is still its identity form
+            off = 0
+            for l in range(1, len(cfg["dims"])):
+                k = cfg["dims"][l - 1] * cfg["dims"][l] + cfg["dims"][l]
+                if (frozen >> (l - 1)) & 1:
+                    assert np.array_equal(e["params"][off:off + k].astype(np.float64), r_params[off:off + k]), (v, l)
+                off += k
         off, boff = 0, 0
         for l in range(1, len(cfg["dims"])):                   # removed biases are still +0
             k = cfg["dims"][l - 1] * cfg["dims"][l]
