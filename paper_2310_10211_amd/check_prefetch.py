@@ -218,14 +218,15 @@ def check_scalar_operands(asm: str, kernel_prefix: str) -> dict:
     """Kernels whose inline-assembly loads take scalar operands (a scalar base
     address, and m0 as the LDS address of a direct-to-LDS load): every such
     operand must be an SGPR (a vector register in ``s_mov_b32 m0, ...`` would
-    not be a scalar value), and the SGPR hazard check must pass.  Returns
+    not be a scalar value; ``vcc_lo`` is an SGPR), and the SGPR hazard check
+    must pass.  Returns
     {symbol: number of direct-to-LDS loads}."""
     found = {}
     for m in re.finditer(r"^(" + re.escape(kernel_prefix) + r"\w*):", asm, re.M):
         name = m.group(1)
         end = asm.index(".Lfunc_end", m.end())
         lines = asm[m.end():end].split("\n")
-        bad = [t for t in (l.strip() for l in lines) if re.match(r"s_mov_b32\s+m0,\s*v", t)]
+        bad = [t for t in (l.strip() for l in lines) if re.match(r"s_mov_b32\s+m0,\s*v(\d|\[)", t)]
         if bad:
             raise RuntimeError(f"{name}: m0 is written from a vector register ({bad[0]!r})")
         haz = sgpr_hazards(lines)

@@ -87,6 +87,15 @@ __device__ __forceinline__ void vt_add(unsigned long long* acc, int v, uint64_t 
   if (acc && (threadIdx.x & 63) == 0) atomicAdd(acc + v, (unsigned long long)(vt_now() - t0));
 }
 
+// An opaque copy of a value: lane-dependent indices recomputed from it cannot
+// be hoisted out of a loop, where dozens of them would stay live in registers
+// (and be spilled) for the whole loop.
+__device__ __forceinline__ int opaque(int x) {
+  int y;
+  asm volatile("v_mov_b32 %0, %1" : "=v"(y) : "v"(x));
+  return y;
+}
+
 // LDS byte address of a pointer into shared memory.
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;

@@ -19,8 +19,14 @@
 // Input rows and weights are both stored with
 // the contraction index contiguous ([row][k] and [unit][k]), so both operand
 // tiles load and read alike.  Workgroups that share a weight tile (same
-// variant, all row tiles) get consecutive dispatch slots on one XCD
-// (workgroup i runs on XCD i mod 8).
+// variant, all row tiles) run at the same time on one XCD (workgroup i runs
+// on XCD i mod 8).
+// Without the output layer one workgroup per CU runs its tiles back to back:
+// the next tile's first operand blocks load while the finished tile is
+// written out, and the stores drain while the next tile computes (all CUs
+// finish their tiles together, so a tile's 32 MB of output from the whole
+// chip would otherwise be written, and the next workgroups dispatched,
+// while no CU computes).
 #include "gevo_internal.h"
 #include "gevo_device.h"
 
@@ -50,11 +56,11 @@ constexpr size_t kOutW = kOutH + (size_t)kPM * kHS * 2;
 constexpr size_t kOutB = kOutW + (size_t)32 * kHS * 2;
 constexpr size_t kOutRed = kOutB + 32 * 4;             // [8] fp64 loss sums, [8] hit counts
 constexpr size_t kOutEnd = kOutRed + 8 * 8 + 8 * 4;
-// the epilogues reuse (and extend) the operand buffers: the output tile
-// [256][kHS] bf16 without the output layer, H, W_L and the sums with it
-constexpr size_t kGemmTileLds = (size_t)kPM * kHS * 2 > kGemmLds ? (size_t)kPM * kHS * 2 : kGemmLds;
+// the output-layer epilogue reuses (and extends) the operand buffers: H, W_L
+// and the sums; without the output layer each wave stages its rows in 8 KB of
+// buffer 1 or 4
 constexpr size_t kGemmOutLds = kOutEnd > kGemmLds ? kOutEnd : kGemmLds;
-static_assert(kGemmOutLds <= 160 * 1024 && kGemmTileLds <= 160 * 1024, "LDS of one CU");
+static_assert(kGemmOutLds <= 160 * 1024 && kGemmLds <= 160 * 1024, "LDS of one CU");
 
 __device__ __forceinline__ f32x16_t mma32(u32x4_t a, u32x4_t b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c,
@@ -66,55 +72,77 @@ __device__ __forceinline__ f32x16_t mma32(u32x4_t a, u32x4_t b, f32x16_t c) {
 template <bool OUT>
 __global__ __launch_bounds__(kPT, 1) void k_pred_gemm(PredGemmArgs a) {
   extern __shared__ __align__(16) char smem[];
-  const int nr = a.R / kPM, nn = a.Np / kPN;
-  const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3;
-  const int p = (j / nr) * 8 + xcd, rt = j % nr;
-  if (p >= a.P * nn) return;
-  const int v = p / nn, n0 = (p % nn) * kPN, r0 = rt * kPM;
-  const uint64_t vt0 = vt_now();
+  // Tiles: (variant, column tile) pairs p, each split into nr row tiles.
+  // Workgroup b runs on XCD b % 8 and serves the pairs with p % 8 == b % 8,
+  // row tile fastest: its s-th tile is tm = b / 8 + s * (gridDim.x / 8) of
+  // that XCD's sequence, so the row tiles of a pair are in flight together on
+  // one XCD and read its weight tile into that L2 once.  Without the output
+  // layer a launch holds one workgroup per CU that runs its tiles back to
+  // back; with it every workgroup runs one tile.
+  const int nr = a.R / kPM, nn = a.Np / kPN, npairs = a.P * nn;
+  const int xcd = blockIdx.x & 7, nwx = (int)(gridDim.x >> 3);
+  const int cnt = xcd < npairs ? ((npairs - 1 - xcd) / 8 + 1) * nr : 0;   // tiles of this XCD
+  int tm = (int)(blockIdx.x >> 3);
+  if (tm >= cnt) return;
+  int v, n0, r0, rt;
+  auto set_tile = [&](int mm) {
+    const int p = (mm / nr) * 8 + xcd;
+    rt = mm % nr;
+    v = p / nn;
+    n0 = (p % nn) * kPN;
+    r0 = rt * kPM;
+  };
+  set_tile(tm);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, lh = lane >> 5;
   const int wm = wave & 3, wn = wave >> 2;           // 64-row band, 128-unit band
   const int Kp = a.Kp;
   const int nblk = (Kp + kPK - 1) / kPK;
-  const uint16_t* A = a.A + a.a_vs * v + (size_t)r0 * Kp;
-  const uint16_t* W = a.W + ((size_t)v * a.Np + n0) * Kp;
+  const uint16_t* sA = a.A + a.a_vs * v + (size_t)r0 * Kp;
+  const uint16_t* sW = a.W + ((size_t)v * a.Np + n0) * Kp;
 
   // Operand blocks go straight to LDS by direct-to-LDS loads: the input rows
   // (shared by all variants, mostly cache hits) one block ahead into two
   // buffers, the weights (first read from memory by the row tiles of a
-  // variant) two blocks ahead into three.  Wave w fills rows 32w .. 32w+31 of
-  // a tile, eight rows per instruction: row group j = 4w + jj, lane l -> LDS
-  // chunk 64 j + l = row 8 j + l / 8, stored chunk l % 8, which holds k
-  // chunk (l % 8) ^ ((row >> 1) & 7).  Chunks past the input width are read
-  // from the row's first chunk (in bounds) and zeroed in LDS once landed.
-  const uint16_t* sA = A;
-  const uint16_t* sW = W;
+  // variant) two blocks ahead into three.  Only waves 0-3 issue them: a
+  // direct-to-LDS load waits at issue while the CU's load path is full (it
+  // moves about 47 bytes a clock, so a block's 64 KB take ~1,400 of the
+  // block's 2,048 MFMA clocks), and a wave waiting there issues no MFMA.
+  // The matrix core of a SIMD serves its older wave first, so the younger
+  // waves 4-7, which never wait there, fill it while waves 0-3 wait.
+  // Loader wave w fills rows 64w .. 64w+63 of a tile, eight rows per
+  // instruction: row group j = 8w + jj, lane l -> LDS chunk 64 j + l = row
+  // 8 j + l / 8, stored chunk l % 8, which holds k chunk (l % 8) ^ ((row >>
+  // 1) & 7).  Chunks past the input width are read from the row's first
+  // chunk (in bounds) and zeroed in LDS once landed.
   const uint32_t lds0 = lds_addr(smem);
-  uint32_t rowoff[4], cpos[4];
+  const int wu = __builtin_amdgcn_readfirstlane(wave);   // the wave index as a scalar (LDS base in m0)
+  const bool loader = wu < 4;
+  const int lw = wave & 3;                               // loader rows (also set in waves 4-7, unused)
+  uint32_t rowoff[8], cpos[8];
 #pragma unroll
-  for (int jj = 0; jj < 4; ++jj) {
-    const int r = 32 * wave + 8 * jj + (lane >> 3);
+  for (int jj = 0; jj < 8; ++jj) {
+    const int r = 64 * lw + 8 * jj + (lane >> 3);
     rowoff[jj] = (uint32_t)r * (uint32_t)Kp * 2u;
     cpos[jj] = (uint32_t)((lane & 7) ^ ((r >> 1) & 7));   // k chunk this lane carries
   }
-  const int wu = __builtin_amdgcn_readfirstlane(wave);   // the wave index as a scalar (LDS base in m0)
   auto abuf = [&](int kb) { return (size_t)(kb & 1) * kTileBytes; };
   auto wbuf = [&](int kb) { return (size_t)(2 + kb % 3) * kTileBytes; };
-  auto issue = [&](const uint16_t* base, size_t buf, int kb) {
+  auto issue = [&](const uint16_t* base, size_t buf, int kb, int j0 = 0, int j1 = 8) {
+    if (!loader) return;
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
+    for (int jj = j0; jj < j1; ++jj) {
       const int k = kb * kPK + 8 * (int)cpos[jj];
       const uint32_t voff = rowoff[jj] + (k < Kp ? (uint32_t)k * 2u : 0u);
-      dma16(base, voff, lds0 + (uint32_t)buf + (uint32_t)((4 * wu + jj) * 1024));
+      dma16(base, voff, lds0 + (uint32_t)buf + (uint32_t)((8 * wu + jj) * 1024));
     }
   };
-  // after block kb's loads have landed: zero this lane's chunks past the input width
+  // after block kb's loads have landed: zero the loader lane's chunks past the input width
   auto zero_tail = [&](int kb) {
-    if ((kb + 1) * kPK > Kp) {
+    if (loader && (kb + 1) * kPK > Kp) {
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj)
+      for (int jj = 0; jj < 8; ++jj)
         if (kb * kPK + 8 * (int)cpos[jj] >= Kp) {
-          const size_t at = (size_t)((4 * wave + jj) * 64 + lane) * 16;
+          const size_t at = (size_t)((8 * lw + jj) * 64 + lane) * 16;
           *reinterpret_cast<u32x4_t*>(smem + abuf(kb) + at) = u32x4_t{0u, 0u, 0u, 0u};
           *reinterpret_cast<u32x4_t*>(smem + wbuf(kb) + at) = u32x4_t{0u, 0u, 0u, 0u};
         }
@@ -122,30 +150,30 @@ __global__ __launch_bounds__(kPT, 1) void k_pred_gemm(PredGemmArgs a) {
   };
 
   f32x16_t acc[2][4];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int t = 0; t < 4; ++t) acc[i][t] = zero16();
 
-  // one block from LDS buffer buf; fragment rows wm*64 + 32i + l32 (A) and
-  // wn*128 + 32t + l32 (W) all have (row >> 1) & 7 == (l32 >> 1) & 7
-  const int swz = lh ^ ((l32 >> 1) & 7);
-  auto compute = [&](int kb) {
-    const char* as = smem + abuf(kb) + (size_t)(wm * 64 + l32) * 128;
-    const char* ws = smem + wbuf(kb) + (size_t)(wn * 128 + l32) * 128;
+  // operand fragments of contraction step s (16 wide) of block kb: rows
+  // wm*64 + 32i + l32 (A) and wn*128 + 32t + l32 (W), which all have
+  // (row >> 1) & 7 == (l32 >> 1) & 7
+  struct Frag {
+    u32x4_t a[2], b[4];
+  };
+  auto rd = [&](Frag& f, int kb, int s) {
+    // lane offsets formed at each read from an opaque lane id (hoisted out of
+    // the loop they would hold a register per buffer and step)
+    const int ln = opaque(lane), r32 = ln & 31;
+    const char* as = smem + abuf(kb) + (size_t)(wm * 64 + r32) * 128;
+    const char* ws = smem + wbuf(kb) + (size_t)(wn * 128 + r32) * 128;
+    const int co = 16 * ((2 * s) ^ (ln >> 5) ^ ((r32 >> 1) & 7));
 #pragma unroll
-    for (int s = 0; s < kPK / 16; ++s) {
-      const int co = 16 * ((2 * s) ^ swz);
-      u32x4_t af[2], bf[4];
+    for (int i = 0; i < 2; ++i) f.a[i] = *reinterpret_cast<const u32x4_t*>(as + i * 32 * 128 + co);
 #pragma unroll
-      for (int i = 0; i < 2; ++i) af[i] = *reinterpret_cast<const u32x4_t*>(as + i * 32 * 128 + co);
+    for (int t = 0; t < 4; ++t) f.b[t] = *reinterpret_cast<const u32x4_t*>(ws + t * 32 * 128 + co);
+  };
+  auto mm = [&](const Frag& f) {
 #pragma unroll
-      for (int t = 0; t < 4; ++t) bf[t] = *reinterpret_cast<const u32x4_t*>(ws + t * 32 * 128 + co);
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int t = 0; t < 4; ++t) acc[i][t] = mma32(bf[t], af[i], acc[i][t]);
-    }
+      for (int t = 0; t < 4; ++t) acc[i][t] = mma32(f.b[t], f.a[i], acc[i][t]);
   };
   // The tile is accumulated transposed (units x rows): lane l holds row
   // wm*64 + 32i + l%32 and, in registers 4q..4q+3, the four consecutive
@@ -174,144 +202,290 @@ __global__ __launch_bounds__(kPT, 1) void k_pred_gemm(PredGemmArgs a) {
       }
   };
 
-  // in issue order per block: the A block, then the W block two ahead, so a
-  // wait that leaves four loads in flight covers everything but that W block
-  issue(sA, abuf(0), 0);
-  issue(sW, wbuf(0), 0);
-  if (nblk > 1) {
-    issue(sW, wbuf(1), 1);
-    wait_vm<4>();
-  } else {
-    wait_vm<0>();
-  }
+  // a tile's first loads: A block 0, then W blocks 0 and 1 (eight loads each
+  // in a loader wave), so a wait that leaves eight loads in flight covers
+  // all but W block 1
+  auto prologue = [&]() {
+    int k0 = 0;
+    asm volatile("" : "+s"(k0));                     // offsets formed here, not kept from the first tile
+    issue(sA, abuf(k0), k0);
+    issue(sW, wbuf(k0), k0);
+    if (nblk > 1) issue(sW, wbuf(k0 + 1), k0 + 1);
+  };
+  // in place of A block nblk the tile's 256 biases go to LDS (one 1 KB
+  // copy per wave, in the A buffer block nblk - 2 used)
+  auto bias_to_lds = [&]() {
+    if constexpr (!OUT)
+      dma16(a.bias + (size_t)v * a.Np + n0, (uint32_t)lane * 16u, lds0 + (uint32_t)abuf(nblk) + (uint32_t)wu * 1024u);
+  };
+  prologue();
+  if (nblk > 1) wait_vm<8>();
+  else wait_vm<0>();
   zero_tail(0);
   __syncthreads();
-  for (int kb = 0; kb < nblk; ++kb) {
-    // the buffers block kb - 1 used are free (every wave is past the barrier)
-    if (kb + 1 < nblk) issue(sA, abuf(kb + 1), kb + 1);
-    if (kb + 2 < nblk) issue(sW, wbuf(kb + 2), kb + 2);
-    compute(kb);
-    if (kb + 1 < nblk) {
-      if (kb + 2 < nblk) wait_vm<4>();
+  for (;;) {
+    const uint64_t vt0 = vt_now();
+    asm volatile("" : : "s"(vt0));    // the clock read completes here, not pending in the loop
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) acc[i][t] = zero16();
+    // Fragments are read one contraction step ahead of the MFMAs that use
+    // them, into two register sets.  Block kb's barrier sits before its last
+    // step: by then every wave has read the whole block, so block kb + 1's
+    // first fragments are read while the last step's MFMAs run.  Each step
+    // also issues two of the wave's loads, one after its second and one after
+    // its fifth MFMA: A block kb + 2 (into the A buffer block kb used) in
+    // steps 3 and 0 after block kb's barrier, W block kb + 3 (into the W
+    // buffer block kb used) in steps 1 and 2 of block kb + 1.  The last two
+    // blocks are written out of the loop; scheduling fences keep this order.
+    Frag f0, f1;
+    struct Load {
+      const uint16_t* base;
+      size_t buf;
+      int kb, j0;                                    // j0: a constant at every use
+      bool on;
+    };
+    auto load1 = [&](const Load& l) {                // two of a loader wave's eight loads of a block
+      if (l.on) issue(l.base, l.buf, l.kb, l.j0, l.j0 + 2);
+    };
+    auto mfma = [&](const Frag& f, int q) {
+      const int i = q & 1, t = q >> 1;
+      acc[i][t] = mma32(f.b[t], f.a[i], acc[i][t]);
+    };
+    auto step = [&](Frag& nxt, int kb_n, int s_n, const Frag& cur, const Load& l0, const Load& l1) {
+      rd(nxt, kb_n, s_n);
+      mfma(cur, 0);
+      mfma(cur, 1);
+      __builtin_amdgcn_sched_barrier(0);
+      load1(l0);
+      __builtin_amdgcn_sched_barrier(0);
+      mfma(cur, 2);
+      mfma(cur, 3);
+      mfma(cur, 4);
+      __builtin_amdgcn_sched_barrier(0);
+      load1(l1);
+      __builtin_amdgcn_sched_barrier(0);
+      mfma(cur, 5);
+      mfma(cur, 6);
+      mfma(cur, 7);
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    const Load none{sA, 0, 0, 0, false};
+    auto lA = [&](int j, int jj) { return Load{sA, abuf(j), j, jj, j < nblk}; };
+    auto lW = [&](int j, int jj) { return Load{sW, wbuf(j), j, jj, j < nblk}; };
+    // steps 0-2 of block kb (step 3's fragments read): the second half of
+    // A block kb + 1, then W block kb + 2
+    auto steps012 = [&](int kb) {
+      step(f1, kb, 1, f0, lA(kb + 1, 4), lA(kb + 1, 6));
+      step(f0, kb, 2, f1, lW(kb + 2, 0), lW(kb + 2, 2));
+      step(f1, kb, 3, f0, lW(kb + 2, 4), lW(kb + 2, 6));
+    };
+    // the first half of A block 1 (or the biases) at the tile's start
+    if (nblk > 1) issue(sA, abuf(1), 1, 0, 4);
+    else bias_to_lds();
+    rd(f0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    // (an opaque copy of nblk keeps the wait below in a block of its own, so
+    // the compiler cannot sink the steps' MFMAs past the barrier)
+    int nbo = nblk;
+    asm volatile("" : "+s"(nbo));
+    int kb = 0;
+    for (; kb + 2 < nblk; ++kb) {
+      steps012(kb);
+      if (kb + 2 < nbo) wait_vm<8>();                // A and W block kb + 1 have landed
       else wait_vm<0>();
+      __syncthreads();
+      __builtin_amdgcn_sched_barrier(0);
+      step(f0, kb + 1, 0, f1, lA(kb + 2, 0), lA(kb + 2, 2));
+    }
+    if (kb + 1 < nblk) {                             // block nblk - 2
+      steps012(kb);
+      wait_vm<0>();
       zero_tail(kb + 1);
+      __syncthreads();
+      __builtin_amdgcn_sched_barrier(0);
+      bias_to_lds();
+      step(f0, kb + 1, 0, f1, none, none);
+      ++kb;
+    }
+    steps012(kb);                                    // block nblk - 1
+    mm(f1);
+    __builtin_amdgcn_sched_barrier(0);
+
+    if constexpr (OUT) {
+      // The layer is one tile wide (Np == 256): the tile holds whole rows of
+      // the last hidden activation.  H = bf16(relu(Z + b)) goes to LDS as
+      // [row][unit]; the output layer's weights as the bf16 operand [class][unit].
+      __syncthreads();                                   // every wave is done with the operand buffers
+      uint16_t* H = reinterpret_cast<uint16_t*>(smem + kOutH);
+      uint16_t* WL = reinterpret_cast<uint16_t*>(smem + kOutW);
+      float* bL = reinterpret_cast<float*>(smem + kOutB);
+      double* red_ce = reinterpret_cast<double*>(smem + kOutRed);
+      unsigned int* red_hit = reinterpret_cast<unsigned int*>(smem + kOutRed + 8 * 8);
+      tile_to_lds(H, kHS);                               // n0 == 0: the layer is this one tile
+      // output layer master, k-blocked [Np/32][32 classes][32 inputs]: thread tid
+      // converts class tid / 8, inputs 32 (tid % 8) .. +31
+      {
+        const float* WLm = a.WL + (size_t)v * 32 * kPN;
+        const int c = (tid >> 3) & 31, kb = tid & 7, q0 = (tid >> 8) * 2;
+        const float* src = WLm + ((size_t)kb * 32 + c) * 32;
+  #pragma unroll
+        for (int q = q0; q < q0 + 2; ++q) {
+          const float4 f0 = *reinterpret_cast<const float4*>(src + 8 * q);
+          const float4 f1 = *reinterpret_cast<const float4*>(src + 8 * q + 4);
+          const float f[8] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w};
+          uint32_t pk[4];
+          to_bf16x2(f, pk);
+          *reinterpret_cast<u32x4_t*>(WL + c * kHS + kb * 32 + 8 * q) = u32x4_t{pk[0], pk[1], pk[2], pk[3]};
+        }
+        if (tid < 32) bL[tid] = a.bL[(size_t)v * 32 + tid];
+      }
+      __syncthreads();
+      // logits^T of 32 rows per tile: lane holds row l32 and classes crow(r) of
+      // its half; the row's other half is in lane ^ 32
+      const int C = a.C;
+      double ce_sum = 0.0;
+      unsigned int hits = 0;
+  #pragma unroll
+      for (int tt = 0; tt < 1; ++tt) {
+        const int rl = wave * 32;                      // first row of the tile (in the workgroup)
+        f32x16_t z0 = zero16(), z1 = zero16();
+  #pragma unroll
+        for (int s = 0; s < kPN / 16; s += 2) {
+          z0 = mma32(*reinterpret_cast<const u32x4_t*>(WL + l32 * kHS + 16 * s + 8 * lh),
+                     *reinterpret_cast<const u32x4_t*>(H + (rl + l32) * kHS + 16 * s + 8 * lh), z0);
+          z1 = mma32(*reinterpret_cast<const u32x4_t*>(WL + l32 * kHS + 16 * s + 16 + 8 * lh),
+                     *reinterpret_cast<const u32x4_t*>(H + (rl + l32) * kHS + 16 * s + 16 + 8 * lh), z1);
+        }
+        const int y = a.labels[r0 + rl + l32];
+        float z[16];
+        float m = -INFINITY, bv = -INFINITY;
+        int bi = 64, nanl = 0;
+  #pragma unroll
+        for (int r = 0; r < 16; ++r) {                 // r ascending = class ascending within the lane
+          const int c = crow(r, lane);
+          z[r] = (z0[r] + z1[r]) + bL[c];
+          if (c < C) {
+            m = fmaxf(m, z[r]);
+            if (z[r] != z[r]) nanl = 1;
+            else if (z[r] > bv) { bv = z[r]; bi = c; }
+          }
+        }
+        m = fmaxf(m, __shfl_xor(m, 32));
+        nanl |= __shfl_xor(nanl, 32);
+        {
+          const float ov = __shfl_xor(bv, 32);
+          const int oi = __shfl_xor(bi, 32);
+          if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+        }
+        float sl = 0.0f, zy = 0.0f;
+  #pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int c = crow(r, lane);
+          if (c < C) sl += expf(z[r] - m);
+          if (c == y) zy = z[r];
+        }
+        const float s = sl + __shfl_xor(sl, 32);
+        zy += __shfl_xor(zy, 32);                      // exactly one lane of the pair holds class y
+        float ce = (logf(s) + m) - zy;
+        if (nanl) ce = NAN;
+        if (lh == 0 && y >= 0) {
+          ce_sum += (double)ce;
+          hits += (!nanl && bi == y) ? 1u : 0u;
+        }
+      }
+  #pragma unroll
+      for (int off = 16; off >= 1; off >>= 1) {        // lanes 0..31 hold the rows; fixed order
+        ce_sum += __shfl_xor(ce_sum, off);
+        hits += __shfl_xor(hits, off);
+      }
+      if (lane == 0) { red_ce[wave] = ce_sum; red_hit[wave] = hits; }
+      __syncthreads();
+      if (tid == 0) {
+        double t = 0.0;
+        unsigned int h = 0;
+        for (int w = 0; w < 8; ++w) { t += red_ce[w]; h += red_hit[w]; }
+        a.part_ce[(size_t)v * a.n_chunks_total + a.chunk0 + rt] = t;
+        a.part_correct[(size_t)v * a.n_chunks_total + a.chunk0 + rt] = h;
+      }
+      vt_add(a.vtime, v, vt0);
+      return;
+    } else {
+      // The tile's biases (in LDS since the last block began) are added to
+      // the accumulators (lane: units wn*128 + 32t + 8q + 4(l/32) + 0..3);
+      // no load that the compiler waits on is ever in flight.
+      const size_t bslot = abuf(nblk) + (size_t)wave * 1024;
+      wait_vm<0>();
+      // lane-dependent offsets of the write-out come from an opaque lane id,
+      // formed per tile rather than held across the tile loop
+      const int ln = opaque(lane), le32 = ln & 31, leh = ln >> 5;
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 bn =
+              *reinterpret_cast<const float4*>(smem + bslot + (size_t)(wn * 128 + t * 32 + 8 * q + 4 * leh) * 4);
+          const float bv[4] = {bn.x, bn.y, bn.z, bn.w};
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[i][t][4 * q + e] = acc[i][t][4 * q + e] + bv[e];
+        }
+      __syncthreads();                                 // every wave is done with the operand buffers
+      uint16_t* Out = a.O + a.o_vs * v + (size_t)r0 * a.Np + n0;
+      const int vdone = v;
+      // The next tile's first blocks load into buffers 0, 2 and 3 while this
+      // tile is written out through buffers 1 and 4.
+      const bool more = tm + nwx < cnt;
+      if (more) {
+        tm += nwx;
+        set_tile(tm);
+        sA = a.A + a.a_vs * v + (size_t)r0 * Kp;
+        sW = a.W + ((size_t)v * a.Np + n0) * Kp;
+        prologue();
+      }
+      // ReLU -> bf16 -> global rows, per wave in two rounds of 64 rows x 64
+      // units staged in the wave's own 8 KB of LDS (16-byte chunk c of row r
+      // at c ^ (r & 7)), then read back as whole 128-byte row segments: eight
+      // rows per store instruction, sixteen store instructions per wave.
+      char* st = smem + (size_t)(wn ? 4 : 1) * kTileBytes + (size_t)wm * 8192;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+              const int row = 32 * i + le32, c = 4 * tt + q;
+              float f[4];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const float z = acc[i][2 * h + tt][4 * q + e];
+                f[e] = z > 0.0f ? z : 0.0f;
+              }
+              uint32_t pk[2];
+              to_bf16x2(f, pk);
+              *reinterpret_cast<uint2*>(st + row * 128 + ((c ^ (row & 7)) << 4) + (leh << 3)) = make_uint2(pk[0], pk[1]);
+            }
+#pragma unroll
+        for (int it = 0; it < 8; ++it) {
+          const int row = 8 * it + (ln >> 3), c = ln & 7;
+          const u32x4_t val = *reinterpret_cast<const u32x4_t*>(st + row * 128 + ((c ^ (row & 7)) << 4));
+          *reinterpret_cast<u32x4_t*>(Out + (size_t)(wm * 64 + row) * a.Np + wn * 128 + 64 * h + 8 * c) = val;
+        }
+      }
+      vt_add(a.vtime, vdone, vt0);
+      if (!more) return;
+      // every memory operation after the next tile's first weight block (its
+      // second weight block, then at least the sixteen stores) may stay in flight
+      if (nblk > 1) wait_vm<24>();
+      else wait_vm<16>();
+      zero_tail(0);
       __syncthreads();
     }
   }
-
-  if constexpr (!OUT) {
-    // bias, ReLU, bf16 into an LDS copy of the tile (lane: unit l32 of a
-    // 32-unit tile, rows crow(r) of a 32-row tile), then every wave writes
-    // whole rows: two 512-byte rows per store instruction
-    __syncthreads();                                   // every wave is done with the operand buffers
-    uint16_t* Ot = reinterpret_cast<uint16_t*>(smem);  // [256 rows][kHS]
-    tile_to_lds(Ot, kHS);
-    __syncthreads();
-    uint16_t* Out = a.O + a.o_vs * v + (size_t)r0 * a.Np + n0;
-#pragma unroll
-    for (int it = 0; it < 16; ++it) {
-      const int row = wave * 32 + 2 * it + lh;
-      const u32x4_t val = *reinterpret_cast<const u32x4_t*>(Ot + row * kHS + 8 * l32);
-      *reinterpret_cast<u32x4_t*>(Out + (size_t)row * a.Np + 8 * l32) = val;
-    }
-  } else {
-    // The layer is one tile wide (Np == 256): the tile holds whole rows of
-    // the last hidden activation.  H = bf16(relu(Z + b)) goes to LDS as
-    // [row][unit]; the output layer's weights as the bf16 operand [class][unit].
-    __syncthreads();                                   // every wave is done with the operand buffers
-    uint16_t* H = reinterpret_cast<uint16_t*>(smem + kOutH);
-    uint16_t* WL = reinterpret_cast<uint16_t*>(smem + kOutW);
-    float* bL = reinterpret_cast<float*>(smem + kOutB);
-    double* red_ce = reinterpret_cast<double*>(smem + kOutRed);
-    unsigned int* red_hit = reinterpret_cast<unsigned int*>(smem + kOutRed + 8 * 8);
-    tile_to_lds(H, kHS);                               // n0 == 0: the layer is this one tile
-    // output layer master, k-blocked [Np/32][32 classes][32 inputs]: thread tid
-    // converts class tid / 8, inputs 32 (tid % 8) .. +31
-    {
-      const float* WLm = a.WL + (size_t)v * 32 * kPN;
-      const int c = (tid >> 3) & 31, kb = tid & 7, q0 = (tid >> 8) * 2;
-      const float* src = WLm + ((size_t)kb * 32 + c) * 32;
-#pragma unroll
-      for (int q = q0; q < q0 + 2; ++q) {
-        const float4 f0 = *reinterpret_cast<const float4*>(src + 8 * q);
-        const float4 f1 = *reinterpret_cast<const float4*>(src + 8 * q + 4);
-        const float f[8] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w};
-        uint32_t pk[4];
-        to_bf16x2(f, pk);
-        *reinterpret_cast<u32x4_t*>(WL + c * kHS + kb * 32 + 8 * q) = u32x4_t{pk[0], pk[1], pk[2], pk[3]};
-      }
-      if (tid < 32) bL[tid] = a.bL[(size_t)v * 32 + tid];
-    }
-    __syncthreads();
-    // logits^T of 32 rows per tile: lane holds row l32 and classes crow(r) of
-    // its half; the row's other half is in lane ^ 32
-    const int C = a.C;
-    double ce_sum = 0.0;
-    unsigned int hits = 0;
-#pragma unroll
-    for (int tt = 0; tt < 1; ++tt) {
-      const int rl = wave * 32;                      // first row of the tile (in the workgroup)
-      f32x16_t z0 = zero16(), z1 = zero16();
-#pragma unroll
-      for (int s = 0; s < kPN / 16; s += 2) {
-        z0 = mma32(*reinterpret_cast<const u32x4_t*>(WL + l32 * kHS + 16 * s + 8 * lh),
-                   *reinterpret_cast<const u32x4_t*>(H + (rl + l32) * kHS + 16 * s + 8 * lh), z0);
-        z1 = mma32(*reinterpret_cast<const u32x4_t*>(WL + l32 * kHS + 16 * s + 16 + 8 * lh),
-                   *reinterpret_cast<const u32x4_t*>(H + (rl + l32) * kHS + 16 * s + 16 + 8 * lh), z1);
-      }
-      const int y = a.labels[r0 + rl + l32];
-      float z[16];
-      float m = -INFINITY, bv = -INFINITY;
-      int bi = 64, nanl = 0;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {                 // r ascending = class ascending within the lane
-        const int c = crow(r, lane);
-        z[r] = (z0[r] + z1[r]) + bL[c];
-        if (c < C) {
-          m = fmaxf(m, z[r]);
-          if (z[r] != z[r]) nanl = 1;
-          else if (z[r] > bv) { bv = z[r]; bi = c; }
-        }
-      }
-      m = fmaxf(m, __shfl_xor(m, 32));
-      nanl |= __shfl_xor(nanl, 32);
-      {
-        const float ov = __shfl_xor(bv, 32);
-        const int oi = __shfl_xor(bi, 32);
-        if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
-      }
-      float sl = 0.0f, zy = 0.0f;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int c = crow(r, lane);
-        if (c < C) sl += expf(z[r] - m);
-        if (c == y) zy = z[r];
-      }
-      const float s = sl + __shfl_xor(sl, 32);
-      zy += __shfl_xor(zy, 32);                      // exactly one lane of the pair holds class y
-      float ce = (logf(s) + m) - zy;
-      if (nanl) ce = NAN;
-      if (lh == 0 && y >= 0) {
-        ce_sum += (double)ce;
-        hits += (!nanl && bi == y) ? 1u : 0u;
-      }
-    }
-#pragma unroll
-    for (int off = 16; off >= 1; off >>= 1) {        // lanes 0..31 hold the rows; fixed order
-      ce_sum += __shfl_xor(ce_sum, off);
-      hits += __shfl_xor(hits, off);
-    }
-    if (lane == 0) { red_ce[wave] = ce_sum; red_hit[wave] = hits; }
-    __syncthreads();
-    if (tid == 0) {
-      double t = 0.0;
-      unsigned int h = 0;
-      for (int w = 0; w < 8; ++w) { t += red_ce[w]; h += red_hit[w]; }
-      a.part_ce[(size_t)v * a.n_chunks_total + a.chunk0 + rt] = t;
-      a.part_correct[(size_t)v * a.n_chunks_total + a.chunk0 + rt] = h;
-    }
-  }
-  vt_add(a.vtime, v, vt0);
 }
 
 // bf16 operand copy of a hidden layer's master: from the k-blocked fp32
@@ -347,9 +521,22 @@ hipError_t launch_wt_bf16(const float* Wm, uint16_t* Wb, int P, int Kp, int Np, 
   return hipGetLastError();
 }
 
+// compute units of the current device, cached per device
+static int device_cus() {
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
+
 template <bool OUT>
 static hipError_t launch_pg(const PredGemmArgs& a, hipStream_t s, const LaunchEv& ev) {
-  constexpr size_t lds = OUT ? kGemmOutLds : kGemmTileLds;
+  constexpr size_t lds = OUT ? kGemmOutLds : kGemmLds;
   static bool attr = false;
   if (!attr) {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pred_gemm<OUT>),
@@ -357,8 +544,14 @@ static hipError_t launch_pg(const PredGemmArgs& a, hipStream_t s, const LaunchEv
     attr = true;
   }
   const int64_t pairs = (int64_t)a.P * (a.Np / kPN);
-  const int64_t slots = (pairs + 7) / 8 * 8 * (a.R / kPM);
-  hipExtLaunchKernelGGL((k_pred_gemm<OUT>), dim3((unsigned)slots), dim3(kPT), lds, s, ev.start, ev.stop, 0, a);
+  int64_t per_xcd = (pairs + 7) / 8 * (a.R / kPM);      // tiles of the busiest XCD
+  if (!OUT) {                                            // one workgroup per CU, tiles back to back
+    const int cus = device_cus();
+    if (cus < 8) return hipErrorInvalidDevice;
+    if (per_xcd > cus / 8) per_xcd = cus / 8;
+  }
+  hipExtLaunchKernelGGL((k_pred_gemm<OUT>), dim3((unsigned)(8 * per_xcd)), dim3(kPT), lds, s, ev.start, ev.stop, 0,
+                        a);
   return hipGetLastError();
 }
 

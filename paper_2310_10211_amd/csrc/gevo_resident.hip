@@ -117,14 +117,6 @@ __device__ __forceinline__ f32x4_t mma16(uint4 a, uint4 b, f32x4_t c) {
 }
 
 
-// An opaque copy of a value: lane-dependent indices recomputed from it cannot
-// be hoisted out of a pass, where dozens of them would stay live in registers
-// for the whole step loop.
-__device__ __forceinline__ int opaque(int x) {
-  int y;
-  asm volatile("v_mov_b32 %0, %1" : "=v"(y) : "v"(x));
-  return y;
-}
 template <typename T>
 __device__ __forceinline__ T* opaque_s(T* p) {
   asm volatile("" : "+s"(p));

@@ -164,3 +164,12 @@ def test_direct_to_lds_base_written_by_valu_just_before_is_caught():
     bad = DMA.replace("\ts_add_u32 s20, s6, 0x400\n", "\tv_readfirstlane_b32 s8, v3\n\tv_readfirstlane_b32 s9, v4\n")
     with pytest.raises(RuntimeError, match="reads an SGPR fewer than 5 wait states"):
         check_prefetch.check_scalar_operands(bad, "_ZN4gevo11k_pred_gemm")
+
+
+def test_lds_address_from_vcc_lo_is_a_scalar_operand():
+    ok = DMA.replace("\ts_add_u32 s20, s6, 0x400\n", "\ts_add_i32 vcc_lo, s6, 0x400\n").replace(
+        "s_mov_b32 m0, s20", "s_mov_b32 m0, vcc_lo")
+    assert check_prefetch.check_scalar_operands(ok, "_ZN4gevo11k_pred_gemm") == {DMA_HEAD[:-2]: 1}
+    bad = ok.replace("s_mov_b32 m0, vcc_lo", "s_mov_b32 m0, v[12]")
+    with pytest.raises(RuntimeError, match="m0 is written from a vector register"):
+        check_prefetch.check_scalar_operands(bad, "_ZN4gevo11k_pred_gemm")
