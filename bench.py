@@ -34,7 +34,8 @@ KERNEL_SOURCES = ["gevo_device.h", "gevo_internal.h", "gevo_kernels.hip", "gevo_
                   "gevo_bwd.hip", "gevo_gemm.hip", "gevo_predict.hip"]
 # rocprofv3 kernel-name stem -> kernel kind of gevo_pop_kernel_stats (training kind, predict kind)
 KERNEL_KIND_OF = {"k_fused2": ("fused_train", None), "k_stream_layer": ("layer_train", "layer_fwd"),
-                  "k_layer": ("layer_train", "layer_fwd"), "k_out": ("out_train", "out_predict"),
+                  "k_layer": ("layer_train", "layer_fwd"), "k_out_fwd": ("out_train", None),
+                  "k_out_upd": ("out_train", None), "k_out": (None, "out_predict"),
                   "k_bwd_gemm": ("bwd", None), "k_bwd": ("bwd", None), "k_pred_gemmILb1": (None, "fwd_out"),
                   "k_pred_gemmILb0": (None, "layer_fwd"), "k_wt_bf16": (None, "weight_copy"),
                   "k_fwd_gemm": (None, "layer_fwd")}
@@ -260,7 +261,7 @@ def fold_traffic(cfg, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, comm
                 top[stem] = grid
         for (stem, grid), vals in groups.items():
             tr_kind, pr_kind = KERNEL_KIND_OF[stem]
-            kind = tr_kind if (stem == "k_fused2" or (trains and grid == top[stem])) else pr_kind
+            kind = tr_kind if (tr_kind and (stem == "k_fused2" or (trains and grid == top[stem]))) else pr_kind
             if kind is None:
                 continue
             cur = per.get(kind)

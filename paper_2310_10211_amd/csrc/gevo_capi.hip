@@ -49,6 +49,7 @@ struct Layout {
   LayerLay lay[GEVO_MAX_LAYERS];
   size_t prune_off = 0, prune_id = 0, prune_th = 0;   // genome pruning edits (gevo_pop_set_genomes)
   size_t gscale = 0;                               // [P][Bp][32] output-gradient scales (gevo_pop_set_grad_scale)
+  size_t ogrd = 0, opdb = 0, opce = 0, opcorr = 0; // training output layer, between its two passes
   size_t lrh = 0;                                  // [L][P] learning rate of each layer (0: a removed layer)
   size_t lr = 0, thresh = 0, train_ce = 0, train_corr = 0, test_ce = 0, test_corr = 0, part_ce = 0,
          part_corr = 0, xrows = 0, xcols = 0, yep = 0, xte = 0, yte = 0, perm = 0;
@@ -174,6 +175,12 @@ gevo_status make_layout(const gevo_pop_config* c, Layout* o) {
   y.thresh = take(P * 4);
   y.prune_off = take((P + 1) * 4);
   y.gscale = take(P * Bp * 32 * 4);
+  if (y.n_train > 0) {
+    y.ogrd = take(P * Bp * 32 * e);
+    y.opdb = take(P * (Bp / 32) * 32 * 4);
+    y.opce = take(P * (Bp / 32) * 8);
+    y.opcorr = take(P * (Bp / 32) * 4);
+  }
   y.prune_id = take(P * (size_t)kMaxGenomePrunes * 4);
   y.prune_th = take(P * (size_t)kMaxGenomePrunes * 4);
   y.vtime = take(P * 8);
@@ -451,6 +458,10 @@ gevo_status train_step(gevo_pop* p, int t) {
     a.ce_acc = at<double>(p, y.train_ce);
     a.correct_acc = at<unsigned long long>(p, y.train_corr);
     a.vtime = at<unsigned long long>(p, y.vtime);
+    a.ogrd = at<S>(p, y.ogrd);
+    a.opdb = at<float>(p, y.opdb);
+    a.opce = at<double>(p, y.opce);
+    a.opcorr = at<unsigned int>(p, y.opcorr);
     if (a.Kp % kTile || a.Bp % kTile) return GEVO_E_SHAPE;
     HIP_TRY(launch_out<S>(a, y.P, p->stream, prof(p, GEVO_KERNEL_OUT_TRAIN)));
   }

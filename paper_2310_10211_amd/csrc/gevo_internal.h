@@ -144,6 +144,12 @@ struct OutArgs {
   S* Gcols; size_t gc_vs;        // [v][Kp][Bp] gradient of the last hidden layer (training)
   S* Grows; size_t gr_vs;        // [v][Bp][Kp] same, row-major (nullable)
   unsigned long long* vtime;      // [P] per-variant device time in clock ticks (nullable)
+  // training, between the two passes: G rows [P][Bp][32] and, per 32-row
+  // tile, the sums of G by class [P][Bp/32][32], of CE [P][Bp/32] and hits
+  S* ogrd;
+  float* opdb;
+  double* opce;
+  unsigned int* opcorr;
 };
 
 template <typename S>

@@ -395,37 +395,30 @@ __global__ __launch_bounds__(256, 2) void k_layer(LayerArgs<S> a) {
 }
 
 // ------------------------------------------------------------ output layer
-// Workgroup = (row chunk, variant).  Logits on MFMA (classes padded to 32),
-// then per row (32 lanes hold the 32 classes of a row): max, NaN flag,
-// sum of exp, log-sum-exp, CE = lse - z_y, argmax with the lowest index on
-// ties (a NaN logit makes the row a miss), and in training the gradient
-// G = (softmax - onehot(y)) * fl(1/b) (section 6.2).  Training continues with
-//   dW_L[c][k] = sum_b G[b][c] A[k][b]  + masked SGD update of W_L, b_L
-//   G_{L-1}[k][b] = (sum_c W_L[c][k] G[b][c]) * [A[k][b] > 0]
-// using the pre-update W_L kept in LDS.
+// Prediction: workgroup = (256-row chunk, variant).  Logits on MFMA (classes
+// padded to 32), then per row (32 lanes hold the 32 classes of a row): max,
+// NaN flag, sum of exp, log-sum-exp, CE = lse - z_y, and the argmax with the
+// lowest index on ties (a NaN logit makes the row a miss); the chunk's CE
+// and hit sums go to per-chunk partials.  (Training runs in the two passes
+// below.)
 constexpr int kOutWaves = 8;
 
-template <typename S, int BPMAX>
+template <typename S>
 __global__ __launch_bounds__(64 * kOutWaves) void k_out(OutArgs<S> a) {
   using O = Op<S>;
   using F = typename O::Frag;
   constexpr int KM = O::KM, KE = O::KE;
-  constexpr int GSTR = 32 + O::PAD;
-  constexpr int NG = BPMAX / KM;
   constexpr int NW = kOutWaves;
   constexpr int NT = 64 * NW;
   extern __shared__ __align__(16) char smem[];
   __shared__ double red_ce[NW];
   __shared__ unsigned int red_corr[NW];
-  __shared__ float red_db[NW][32];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int l32 = lane & 31, lh = lane >> 5;
   const int v = blockIdx.y, chunk = blockIdx.x;
   const uint64_t vt0 = vt_now();
   const int Kp = a.Kp, WS = Kp + O::PAD;
   S* wop = reinterpret_cast<S*>(smem);                  // [32][WS]  W_L as operand, [class][k]
-  S* gs = wop + 32 * WS;                                // [Bp][GSTR] gradient rows (training)
-  float* stg = reinterpret_cast<float*>(gs + (size_t)a.Bp * GSTR);   // [NW][32][36] fp32 staging (training)
   const float* Wm = a.Wm + (size_t)v * 32 * Kp;
   {
     const int q = Kp / 4;                                // float4 per row
@@ -450,13 +443,12 @@ __global__ __launch_bounds__(64 * kOutWaves) void k_out(OutArgs<S> a) {
   const float bias_c = a.bias[(size_t)v * 32 + l32];
   __syncthreads();
 
-  const int row_base = a.train ? 0 : chunk * kOutRows;
-  const int rows = a.train ? a.Bp : min(kOutRows, a.rows - row_base);
+  const int row_base = chunk * kOutRows;
+  const int rows = min(kOutRows, a.rows - row_base);
   const int ntiles = rows / 32;
   const bool cvalid = l32 < a.C;
   double ce_sum = 0.0;
   unsigned int corr = 0;
-  float db_part = 0.0f;
   for (int tile = wave; tile < ntiles; tile += NW) {
     f32x16_t acc0 = zero16(), acc1 = zero16();
     const S* ar = a.Arows + v * a.ar_vs + (size_t)(row_base + tile * 32 + l32) * Kp + lh * KE;
@@ -477,7 +469,6 @@ __global__ __launch_bounds__(64 * kOutWaves) void k_out(OutArgs<S> a) {
     for (int r = 0; r < 16; ++r) ylab[r] = a.labels[row_base + tile * 32 + crow(r, lane)];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int rl = tile * 32 + crow(r, lane);
       const int y = ylab[r];
       const float z = (acc0[r] + acc1[r]) + bias_c;
       int isn = (cvalid && (z != z)) ? 1 : 0;
@@ -504,79 +495,275 @@ __global__ __launch_bounds__(64 * kOutWaves) void k_out(OutArgs<S> a) {
         ce_sum += (double)ce;
         corr += (!isn && bi == y) ? 1u : 0u;
       }
-      if (a.train) {
-        const float p = e / s;
-        const float sc = a.gscale ? a.gscale[((size_t)v * a.Bp + rl) * 32 + l32] : a.scale;
-        const float g = (cvalid && rvalid) ? (p - (l32 == y ? 1.0f : 0.0f)) * sc : 0.0f;
-        db_part += g;
-        gs[rl * GSTR + l32] = O::from_f32(g);
-      }
     }
   }
   // reductions in a fixed order
   ce_sum += __shfl_xor(ce_sum, 32);
   corr += __shfl_xor(corr, 32);
-  db_part += __shfl_xor(db_part, 32);
   if (lane == 0) { red_ce[wave] = ce_sum; red_corr[wave] = corr; }
-  if (lh == 0) red_db[wave][l32] = db_part;
   __syncthreads();
   if (threadIdx.x == 0) {
     double t = 0.0;
     unsigned int cc = 0;
     for (int w = 0; w < NW; ++w) { t += red_ce[w]; cc += red_corr[w]; }
-    if (a.train) {
-      a.ce_acc[v] += t;
-      a.correct_acc[v] += cc;
-    } else {
-      a.part_ce[(size_t)v * a.n_chunks_total + a.chunk0 + chunk] = t;
-      a.part_correct[(size_t)v * a.n_chunks_total + a.chunk0 + chunk] = cc;
+    a.part_ce[(size_t)v * a.n_chunks_total + a.chunk0 + chunk] = t;
+    a.part_correct[(size_t)v * a.n_chunks_total + a.chunk0 + chunk] = cc;
+  }
+  vt_add(a.vtime, v, vt0);
+}
+
+// ---------------------------------------------- output layer, training in two passes
+// The training step of the output layer (section 6.2), spread over many
+// workgroups per variant instead of k_out's one.
+// Pass 1, one workgroup per (32-row tile, variant): logits^T (classes x
+// rows: a lane holds one row's classes crow(r) of its half, the row's other
+// half in lane ^ 32; the four waves take quarters of the contraction,
+// summed in a fixed order), then, as in k_out, per row max, NaN flag,
+// log-sum-exp, CE, argmax (lowest index on ties, a NaN logit is a miss) and
+// the gradient rows G = (softmax - onehot(y)) * scale, written out with the
+// tile's sums of G by class, of CE and of hits.
+template <typename S>
+__global__ __launch_bounds__(256) void k_out_fwd(OutArgs<S> a) {
+  using O = Op<S>;
+  using F = typename O::Frag;
+  constexpr int KM = O::KM, KE = O::KE;
+  extern __shared__ __align__(16) char smem[];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int l32 = lane & 31, lh = lane >> 5;
+  const int v = blockIdx.y, tile = blockIdx.x, ntile = a.Bp / 32;
+  const uint64_t vt0 = vt_now();
+  const int Kp = a.Kp, WS = Kp + O::PAD;
+  float* red = reinterpret_cast<float*>(smem);          // [3][16][64] partial logits of waves 1-3; then G [32 rows][33]
+  S* wop = reinterpret_cast<S*>(smem + 3 * 16 * 64 * 4);   // [32][WS]  W_L as operand, [class][k]
+  const float* Wm = a.Wm + (size_t)v * 32 * Kp;
+  {
+    // sixteen float4 loads in flight per thread (the master is k-blocked [Kp/32][32][32])
+    const int q = Kp / 4;                                // float4 per row
+    for (int j0 = threadIdx.x; j0 < 32 * q; j0 += 256 * 16) {
+      float4 w4[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int j = j0 + u * 256;
+        w4[u] = j < 32 * q ? *reinterpret_cast<const float4*>(Wm + (size_t)j * 4) : make_float4(0, 0, 0, 0);
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int j = j0 + u * 256;
+        if (j < 32 * q) {
+          S* dst = wop + ((j / 8) % 32) * WS + (j / 256) * 32 + (j % 8) * 4;   // row (j/8)%32, chunk j/256
+          dst[0] = O::from_f32(w4[u].x); dst[1] = O::from_f32(w4[u].y);
+          dst[2] = O::from_f32(w4[u].z); dst[3] = O::from_f32(w4[u].w);
+        }
+      }
     }
   }
-  if (!a.train) {
-    vt_add(a.vtime, v, vt0);
-    return;
+  __syncthreads();
+  const int steps = Kp / KM, s0 = wave * steps / 4, s1 = (wave + 1) * steps / 4;
+  const S* ar = a.Arows + v * a.ar_vs + (size_t)(tile * 32 + l32) * Kp + lh * KE;
+  const S* wr = wop + l32 * WS + lh * KE;
+  f32x16_t acc0 = zero16(), acc1 = zero16();
+  int st = s0;
+  for (; st + 4 <= s1; st += 4) {
+    F x[4], w[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) { x[u] = O::load(ar + (st + u) * KM); w[u] = O::load(wr + (st + u) * KM); }
+    acc0 = O::mma(w[0], x[0], acc0);
+    acc1 = O::mma(w[1], x[1], acc1);
+    acc0 = O::mma(w[2], x[2], acc0);
+    acc1 = O::mma(w[3], x[3], acc1);
   }
-
-  const float lrv = a.lr[v];
-  if (threadIdx.x < 32) {
+  for (; st < s1; ++st) acc0 = O::mma(O::load(wr + st * KM), O::load(ar + st * KM), acc0);
+  if (wave > 0) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) red[((wave - 1) * 16 + r) * 64 + lane] = acc0[r] + acc1[r];
+  }
+  __syncthreads();
+  if (wave > 0) return;
+  // lane: row rl = tile*32 + l32, classes c(r) = crow(r, lane), ascending in r
+  const int C = a.C;
+  const int rl = tile * 32 + l32;
+  const int y = a.labels[rl];
+  const bool rvalid = y >= 0;
+  float z[16];
+  float m = -INFINITY, bv = -INFINITY;
+  int bi = 64, nanl = 0;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int c = crow(r, lane);
+    const float zp = (((acc0[r] + acc1[r]) + red[r * 64 + lane]) + red[(16 + r) * 64 + lane]) + red[(32 + r) * 64 + lane];
+    z[r] = zp + a.bias[(size_t)v * 32 + c];
+    if (c < C) {
+      m = fmaxf(m, z[r]);
+      if (z[r] != z[r]) nanl = 1;
+      else if (z[r] > bv) { bv = z[r]; bi = c; }
+    }
+  }
+  m = fmaxf(m, __shfl_xor(m, 32));
+  nanl |= __shfl_xor(nanl, 32);
+  {
+    const float ov = __shfl_xor(bv, 32);
+    const int oi = __shfl_xor(bi, 32);
+    if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+  }
+  float ex[16], sl = 0.0f, zy = 0.0f;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int c = crow(r, lane);
+    ex[r] = c < C ? expf(z[r] - m) : 0.0f;
+    sl += ex[r];
+    if (c == y) zy = z[r];
+  }
+  const float sm = sl + __shfl_xor(sl, 32);
+  zy += __shfl_xor(zy, 32);                          // exactly one lane of the pair holds class y
+  float ce = (logf(sm) + m) - zy;
+  if (nanl) ce = NAN;
+  // G of this lane's classes: 4 consecutive classes per register group q
+  float* gt = red;                                   // [32 rows][33] fp32 G for the class sums
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    float g4[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = 4 * q + j, c = crow(r, lane);
+      const float sc = a.gscale ? a.gscale[((size_t)v * a.Bp + rl) * 32 + c] : a.scale;
+      g4[j] = (c < C && rvalid) ? (ex[r] / sm - (c == y ? 1.0f : 0.0f)) * sc : 0.0f;
+      gt[l32 * 33 + c] = g4[j];
+    }
+    S* gd = a.ogrd + ((size_t)v * a.Bp + rl) * 32 + 8 * q + 4 * lh;
+    if constexpr (sizeof(S) == 2) {
+      const uint32_t lo = (uint32_t)O::from_f32(g4[0]) | (uint32_t)O::from_f32(g4[1]) << 16;
+      const uint32_t hi = (uint32_t)O::from_f32(g4[2]) | (uint32_t)O::from_f32(g4[3]) << 16;
+      *reinterpret_cast<uint2*>(gd) = make_uint2(lo, hi);
+    } else {
+      *reinterpret_cast<float4*>(gd) = make_float4(g4[0], g4[1], g4[2], g4[3]);
+    }
+  }
+  // the tile's sums: CE and hits over rows (lanes 0-31), G by class (lane c
+  // sums column c in row order)
+  double ce_sum = (lh == 0 && rvalid) ? (double)ce : 0.0;
+  unsigned int corr = (lh == 0 && rvalid && !nanl && bi == y) ? 1u : 0u;
+#pragma unroll
+  for (int off = 16; off >= 1; off >>= 1) {
+    ce_sum += __shfl_xor(ce_sum, off);
+    corr += __shfl_xor(corr, off);
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  const size_t ti = (size_t)v * ntile + tile;
+  if (lh == 0) {
     float db = 0.0f;
-    for (int w = 0; w < NW; ++w) db += red_db[w][threadIdx.x];
-    const float bo = a.bias[(size_t)v * 32 + threadIdx.x];
-    const bool bk = (a.bmask[v] >> threadIdx.x) & 1u;
-    a.bias[(size_t)v * 32 + threadIdx.x] = bk ? __fsub_rn(bo, __fmul_rn(lrv, db)) : 0.0f;
+    for (int rr = 0; rr < 32; ++rr) db += gt[rr * 33 + l32];
+    a.opdb[ti * 32 + l32] = db;
   }
-  // dW_L and the masked update of the master (old W_L stays in LDS): the dW
-  // tile is staged in LDS, then lane (row rn, 16 columns) updates with float4
-  const int nsteps = a.Bp / KM;
-  typename O::Frag ga[NG];
-#pragma unroll
-  for (int s2 = 0; s2 < NG; ++s2)
-    if (s2 < nsteps) ga[s2] = O::gather(&gs[(s2 * KM + lh * KE) * GSTR + l32], GSTR);
-  float* Wmv = a.Wm + (size_t)v * 32 * Kp;
-  const uint32_t* mk = a.mask + (size_t)v * 32 * (Kp / 32);
+  if (lane == 0) { a.opce[ti] = ce_sum; a.opcorr[ti] = corr; }
+  vt_add(a.vtime, v, vt0);
+}
+
+// Pass 2, one workgroup per (32-input column tile kt, variant): wave 0 forms
+// dW_L[c][k] = sum_b G[b][c] A[k][b] for the tile's 32 inputs and applies
+// the masked SGD update to those columns of the master; all four waves form
+// G_{L-1}[k][b] = (sum_c W_L[c][k] G[b][c]) * [A[k][b] > 0] for the same
+// inputs from the columns' pre-update values.  The kt == 0 workgroup also
+// updates the biases and adds the CE and hit sums, tiles in order.  Each
+// workgroup alone reads and writes its columns, so no other workgroup sees
+// a half-updated W_L.
+template <typename S, int BPMAX>
+__global__ __launch_bounds__(256) void k_out_upd(OutArgs<S> a) {
+  using O = Op<S>;
+  constexpr int KM = O::KM, KE = O::KE;
+  constexpr int GSTR = 32 + O::PAD, WSTR = 32 + O::PAD;
+  constexpr int NG = BPMAX / KM;
+  extern __shared__ __align__(16) char smem[];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int l32 = lane & 31, lh = lane >> 5;
+  const int v = blockIdx.y, kt = blockIdx.x, ntile = a.Bp / 32;
+  const uint64_t vt0 = vt_now();
+  const int Kp = a.Kp;
+  const int BT = a.Bp + O::PAD;
+  float* stg = reinterpret_cast<float*>(smem);                       // [32][36] dW staging (wave 0)
+  S* wold = reinterpret_cast<S*>(smem + 32 * 36 * 4);                // [32 classes][WSTR] old W_L columns
+  S* gs = wold + 32 * WSTR;                                          // [Bp][GSTR] G rows
+  S* gT = gs + (size_t)a.Bp * GSTR;                                  // [32 classes][BT] G columns
+  // wave 0's operands for dW and the update, in flight with the G loads
   const S* Acv = a.Acols + v * a.ac_vs;
-  float* dws = stg + wave * 32 * 36;
+  const int nsteps = a.Bp / KM;
   const int rn = lane >> 1, cs = (lane & 1) * 16;
-  for (int kt = wave; kt < Kp / 32; kt += NW) {
-    const int k0 = kt * 32;
-    float4 w4[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) w4[u] = *reinterpret_cast<const float4*>(Wmv + ((size_t)kt * 32 + rn) * 32 + cs + 4 * u);
-    const uint32_t mw = mk[(size_t)rn * (Kp / 32) + kt];
-    f32x16_t d = zero16();
-    const S* ap = Acv + (size_t)(k0 + l32) * a.Bp + lh * KE;
+  typename O::Frag af[NG];
+  float4 w4[4];
+  uint32_t mw = 0;
+  float* Wmv = a.Wm + (size_t)v * 32 * Kp;
+  if (wave == 0) {
+    const S* ap = Acv + (size_t)(kt * 32 + l32) * a.Bp + lh * KE;
 #pragma unroll
     for (int s2 = 0; s2 < NG; ++s2)
-      if (s2 < nsteps) d = O::mma(ga[s2], O::load(ap + s2 * KM), d);
+      if (s2 < nsteps) af[s2] = O::load(ap + s2 * KM);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) dws[crow(r, lane) * 36 + l32] = d[r];
+    for (int u = 0; u < 4; ++u) w4[u] = *reinterpret_cast<const float4*>(Wmv + ((size_t)kt * 32 + rn) * 32 + cs + 4 * u);
+    mw = a.mask[(size_t)v * 32 * (Kp / 32) + (size_t)rn * (Kp / 32) + kt];
+  }
+  {
+    // 16-byte loads, all of a thread's issued before any is stored
+    constexpr int PER = 16 / (int)sizeof(S);               // elements per 16 bytes
+    const uint4* gsrc = reinterpret_cast<const uint4*>(a.ogrd + (size_t)v * a.Bp * 32);
+    const int nvec = a.Bp * 32 / PER;                    // at most 256 * 32 / 4
+    uint4 gv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = threadIdx.x + u * 256;
+      gv[u] = i < nvec ? gsrc[i] : make_uint4(0, 0, 0, 0);
+    }
+    const float4 wv = reinterpret_cast<const float4*>(a.Wm + ((size_t)v * (Kp / 32) + kt) * 32 * 32)[threadIdx.x];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = threadIdx.x + u * 256;
+      if (i < nvec) {
+        const S* e = reinterpret_cast<const S*>(&gv[u]);
+        const int row = (i * PER) >> 5, col = (i * PER) & 31;
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+          gs[row * GSTR + col + j] = e[j];
+          gT[(col + j) * BT + row] = e[j];
+        }
+      }
+    }
+    // k-blocked master tile [c][32 k]: thread t holds class t / 8, inputs 4 (t % 8) .. +3
+    S* wd = wold + (threadIdx.x >> 3) * WSTR + (threadIdx.x & 7) * 4;
+    wd[0] = O::from_f32(wv.x); wd[1] = O::from_f32(wv.y); wd[2] = O::from_f32(wv.z); wd[3] = O::from_f32(wv.w);
+  }
+  __syncthreads();
+  if (kt == 0) {
+    const float lrv = a.lr[v];
+    if (threadIdx.x < 32) {
+      float db = 0.0f;
+      for (int t = 0; t < ntile; ++t) db += a.opdb[((size_t)v * ntile + t) * 32 + threadIdx.x];
+      const float bo = a.bias[(size_t)v * 32 + threadIdx.x];
+      const bool bk = (a.bmask[v] >> threadIdx.x) & 1u;
+      a.bias[(size_t)v * 32 + threadIdx.x] = bk ? __fsub_rn(bo, __fmul_rn(lrv, db)) : 0.0f;
+    } else if (threadIdx.x == 64) {
+      double t = 0.0;
+      unsigned int cc = 0;
+      for (int u = 0; u < ntile; ++u) { t += a.opce[(size_t)v * ntile + u]; cc += a.opcorr[(size_t)v * ntile + u]; }
+      a.ce_acc[v] += t;
+      a.correct_acc[v] += cc;
+    }
+  }
+  if (wave == 0) {
+    // dW tile staged in LDS, then lane (row rn, 16 columns) updates with float4
+    const float lrv = a.lr[v];
+    f32x16_t d = zero16();
+#pragma unroll
+    for (int s2 = 0; s2 < NG; ++s2)
+      if (s2 < nsteps) d = O::mma(O::load(&gT[l32 * BT + s2 * KM + lh * KE]), af[s2], d);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) stg[crow(r, lane) * 36 + l32] = d[r];
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
     float wn[16];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const float4 t = *reinterpret_cast<const float4*>(dws + rn * 36 + cs + 4 * u);
+      const float4 t = *reinterpret_cast<const float4*>(stg + rn * 36 + cs + 4 * u);
       const float dv[4] = {t.x, t.y, t.z, t.w};
       const float wv[4] = {w4[u].x, w4[u].y, w4[u].z, w4[u].w};
 #pragma unroll
@@ -589,47 +776,40 @@ __global__ __launch_bounds__(64 * kOutWaves) void k_out(OutArgs<S> a) {
     for (int u = 0; u < 4; ++u)
       *reinterpret_cast<float4*>(Wmv + ((size_t)kt * 32 + rn) * 32 + cs + 4 * u) =
           make_float4(wn[4 * u], wn[4 * u + 1], wn[4 * u + 2], wn[4 * u + 3]);
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
   }
-  if (!a.Gcols) {
-    vt_add(a.vtime, v, vt0);
-    return;
-  }
-  // gradient of the last hidden layer, batch-contiguous, with ReLU'
-  const int tb = a.Bp / 32, ntot = (Kp / 32) * tb;
-  for (int t = wave; t < ntot; t += NW) {
-    const int kt = t / tb, bt = t % tb;
-    float av[16];
+  if (a.Gcols) {
+    // gradient of the last hidden layer for inputs kt*32 .. +31, batch-contiguous, with ReLU'
+    for (int bt = wave - 1; wave > 0 && bt < ntile; bt += 3) {   // waves 1-3 (wave 0 has dW)
+      float av[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) av[r] = O::to_f32(Acv[(size_t)(kt * 32 + crow(r, lane)) * a.Bp + bt * 32 + l32]);
-    f32x16_t acc = zero16();
+      for (int r = 0; r < 16; ++r) av[r] = O::to_f32(Acv[(size_t)(kt * 32 + crow(r, lane)) * a.Bp + bt * 32 + l32]);
+      f32x16_t acc = zero16();
 #pragma unroll
-    for (int ks = 0; ks < 32 / KM; ++ks) {
-      const typename O::Frag af = O::gather(&wop[(ks * KM + lh * KE) * WS + kt * 32 + l32], WS);
-      const typename O::Frag bf = O::load(&gs[(bt * 32 + l32) * GSTR + ks * KM + lh * KE]);
-      acc = O::mma(af, bf, acc);
-    }
-    const int b = bt * 32 + l32;
-    S g[16];
+      for (int ks = 0; ks < 32 / KM; ++ks) {
+        const typename O::Frag wf = O::gather(&wold[(ks * KM + lh * KE) * WSTR + l32], WSTR);
+        const typename O::Frag bf = O::load(&gs[(bt * 32 + l32) * GSTR + ks * KM + lh * KE]);
+        acc = O::mma(wf, bf, acc);
+      }
+      const int b = bt * 32 + l32;
+      S g[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      g[r] = O::from_f32(av[r] > 0.0f ? acc[r] : 0.0f);
-      a.Gcols[v * a.gc_vs + (size_t)(kt * 32 + crow(r, lane)) * a.Bp + b] = g[r];
-    }
-    if (a.Grows) {
-      // rows [b][k]: accumulator rows 4q..4q+3 are the consecutive inputs
-      // kt 32 + 8q + 4 (l / 32) + 0..3, one 4-element store each
-      S* gr = a.Grows + v * a.gr_vs + (size_t)b * Kp + kt * 32 + 4 * lh;
+      for (int r = 0; r < 16; ++r) {
+        g[r] = O::from_f32(av[r] > 0.0f ? acc[r] : 0.0f);
+        a.Gcols[v * a.gc_vs + (size_t)(kt * 32 + crow(r, lane)) * a.Bp + b] = g[r];
+      }
+      if (a.Grows) {
+        // rows [b][k]: accumulator rows 4q..4q+3 are the consecutive inputs
+        // kt 32 + 8q + 4 (l / 32) + 0..3, one 4-element store each
+        S* gr = a.Grows + v * a.gr_vs + (size_t)b * Kp + kt * 32 + 4 * lh;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        if constexpr (sizeof(S) == 2) {
-          const uint32_t lo = (uint32_t)g[4 * q] | (uint32_t)g[4 * q + 1] << 16;
-          const uint32_t hi = (uint32_t)g[4 * q + 2] | (uint32_t)g[4 * q + 3] << 16;
-          *reinterpret_cast<uint2*>(gr + 8 * q) = make_uint2(lo, hi);
-        } else {
-          *reinterpret_cast<float4*>(gr + 8 * q) = make_float4(g[4 * q], g[4 * q + 1], g[4 * q + 2], g[4 * q + 3]);
+        for (int q = 0; q < 4; ++q) {
+          if constexpr (sizeof(S) == 2) {
+            const uint32_t lo = (uint32_t)g[4 * q] | (uint32_t)g[4 * q + 1] << 16;
+            const uint32_t hi = (uint32_t)g[4 * q + 2] | (uint32_t)g[4 * q + 3] << 16;
+            *reinterpret_cast<uint2*>(gr + 8 * q) = make_uint2(lo, hi);
+          } else {
+            *reinterpret_cast<float4*>(gr + 8 * q) = make_float4(g[4 * q], g[4 * q + 1], g[4 * q + 2], g[4 * q + 3]);
+          }
         }
       }
     }
@@ -818,32 +998,37 @@ hipError_t launch_layer(const LayerArgs<S>& a0, int P, hipStream_t s, const Laun
 }
 
 template <typename S>
-size_t out_lds_bytes(int Kp, int Bp, int train) {
-  return (size_t)32 * (Kp + Op<S>::PAD) * sizeof(S) +
-         (train ? (size_t)Bp * (32 + Op<S>::PAD) * sizeof(S) + (size_t)kOutWaves * 32 * 36 * 4 : 0);
-}
-
-template <typename S>
 hipError_t launch_out(const OutArgs<S>& a, int P, hipStream_t s, const LaunchEv& ev) {
-  const size_t lds = out_lds_bytes<S>(a.Kp, a.Bp, a.train);
-  const dim3 grid(a.train ? 1 : (a.rows + kOutRows - 1) / kOutRows, P);
-  if (a.Bp <= 128) {
+  if (a.train) {
+    // two passes: rows of the batch, then columns of W_L
+    if (!a.ogrd || !a.opdb || !a.opce || !a.opcorr || a.Bp > 256 || a.Bp % 32 || a.Kp % 32) return hipErrorInvalidValue;
+    const size_t lds1 = (size_t)3 * 16 * 64 * 4 + (size_t)32 * (a.Kp + Op<S>::PAD) * sizeof(S);
+    const size_t lds2 = (size_t)32 * 36 * 4 + (size_t)32 * (32 + Op<S>::PAD) * sizeof(S) +
+                        (size_t)a.Bp * (32 + Op<S>::PAD) * sizeof(S) + (size_t)32 * (a.Bp + Op<S>::PAD) * sizeof(S);
+    if (lds1 > kLdsBudget || lds2 > kLdsBudget) return hipErrorInvalidValue;
     static bool attr = false;
     if (!attr) {
-      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_out<S, 128>),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBudget);
+      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_out_fwd<S>), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)kLdsBudget);
       attr = true;
     }
-    hipExtLaunchKernelGGL((k_out<S, 128>), grid, dim3(64 * kOutWaves), lds, s, ev.start, ev.stop, 0, a);
-  } else {
-    static bool attr = false;
-    if (!attr) {
-      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_out<S, 256>),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBudget);
-      attr = true;
-    }
-    hipExtLaunchKernelGGL((k_out<S, 256>), grid, dim3(64 * kOutWaves), lds, s, ev.start, ev.stop, 0, a);
+    hipExtLaunchKernelGGL(k_out_fwd<S>, dim3(a.Bp / 32, P), dim3(256), lds1, s, ev.start, nullptr, 0, a);
+    if (a.Bp <= 128)
+      hipExtLaunchKernelGGL((k_out_upd<S, 128>), dim3(a.Kp / 32, P), dim3(256), lds2, s, nullptr, ev.stop, 0, a);
+    else
+      hipExtLaunchKernelGGL((k_out_upd<S, 256>), dim3(a.Kp / 32, P), dim3(256), lds2, s, nullptr, ev.stop, 0, a);
+    return hipGetLastError();
   }
+  const size_t lds = (size_t)32 * (a.Kp + Op<S>::PAD) * sizeof(S);
+  if (lds > kLdsBudget) return hipErrorInvalidValue;
+  const dim3 grid((a.rows + kOutRows - 1) / kOutRows, P);
+  static bool attr = false;
+  if (!attr) {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_out<S>), hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)kLdsBudget);
+    attr = true;
+  }
+  hipExtLaunchKernelGGL(k_out<S>, grid, dim3(64 * kOutWaves), lds, s, ev.start, ev.stop, 0, a);
   return hipGetLastError();
 }
 
