@@ -31,7 +31,8 @@ PREFETCH_CHECKED = (("gevo_fused.hip", "_ZN4gevo8k_fused2"), ("gevo_stream.hip",
 
 # kernels whose direct-to-LDS loads read scalar registers from inline assembly
 # (SGPR hazard check only; they stage no prefetch registers)
-DMA_CHECKED = (("gevo_predict.hip", "_ZN4gevo11k_pred_gemm"), ("gevo_resident.hip", "_ZN4gevo6k_res2"))
+DMA_CHECKED = (("gevo_predict.hip", "_ZN4gevo11k_pred_gemm"), ("gevo_resident.hip", "_ZN4gevo6k_res2"),
+               ("gevo_bwd.hip", "_ZN4gevo10k_bwd_gemm"))
 
 
 def _device_asm(d: str, src: str) -> str:

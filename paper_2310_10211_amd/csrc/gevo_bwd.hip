@@ -9,13 +9,16 @@
 // One workgroup (4 waves) computes 128 inputs k x all batch rows of one
 // variant, so every operand byte is read from global memory by one
 // workgroup of each k tile.  The contraction runs over 32-unit blocks of
-// layer l, double-buffered in LDS; wave w computes the 64 x BP/2 sub-tile
-// (k half w&1, batch half w>>1) with 32x32x16 MFMAs, accumulating the blocks
-// in increasing order.  The k tiles of one variant share an XCD (workgroup i
-// runs on XCD i % 8), so the variant's gradient rows are fetched into that
-// XCD's L2 once.  The epilogue applies ReLU' from the activations and writes
-// the gradient in columns [k][b] (and, when the layer below has a backward
-// of its own, in rows [b][k]).
+// layer l that reach LDS by direct-to-LDS loads two blocks ahead of the
+// multiply, into a ring of three stages (rows of 64 bytes, 16-byte chunk c
+// of row r stored at c ^ ((r >> 1) & 3), so fragment reads do not collide
+// in the banks); wave w computes the 64 x BP/2 sub-tile (k half w&1, batch
+// half w>>1) with 32x32x16 MFMAs, accumulating the blocks in increasing
+// order.  The k tiles of one variant share an XCD (workgroup i runs on XCD
+// i % 8), so the variant's gradient rows are fetched into that XCD's L2
+// once.  The epilogue applies ReLU' from the activations and writes the
+// gradient in columns [k][b] (and, when the layer below has a backward of
+// its own, in rows [b][k]).
 #include "gevo_internal.h"
 #include "gevo_device.h"
 
@@ -29,7 +32,7 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 constexpr int kBK = 128;                 // inputs k per workgroup
-constexpr int kBS = 32 + 8;              // LDS row stride (bf16 elements) of both operand blocks
+constexpr int kStages = 3;               // operand ring depth (loads run two blocks ahead)
 
 __device__ __forceinline__ f32x16_t mma32(u32x4_t a, u32x4_t b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c,
@@ -38,10 +41,10 @@ __device__ __forceinline__ f32x16_t mma32(u32x4_t a, u32x4_t b, f32x16_t c) {
 
 template <int BP>
 struct BwdLds {
-  static constexpr int a_elems = kBK * kBS;   // W^T block [128 k][32 n]
-  static constexpr int b_elems = BP * kBS;    // G block [BP b][32 n]
-  static constexpr int stage = a_elems + b_elems;
-  static constexpr size_t bytes = (size_t)2 * stage * 2;
+  static constexpr int a_bytes = kBK * 64;    // W^T block [128 k][32 n] bf16
+  static constexpr int b_bytes = BP * 64;     // G block [BP b][32 n]
+  static constexpr int stage = a_bytes + b_bytes;
+  static constexpr size_t bytes = (size_t)kStages * stage;
 };
 
 }  // namespace
@@ -50,9 +53,9 @@ template <int BP>
 __global__ __launch_bounds__(256, 2) void k_bwd_gemm(BwdArgs<uint16_t> a) {
   typedef BwdLds<BP> Ly;
   constexpr int BTW = BP / 64;            // 32-wide batch tiles per wave
-  constexpr int UA = kBK * 4 / 256;       // 16-byte chunks per thread of the W^T block
-  constexpr int UB = BP * 4 / 256;        // and of the G block
-  extern __shared__ __align__(16) uint16_t lds[];
+  constexpr int JA = kBK / 64;            // direct-to-LDS loads per wave per block: W^T rows
+  constexpr int JB = BP / 64;             // and G rows (16 rows of 64 bytes per load)
+  extern __shared__ __align__(16) char lds[];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, lh = lane >> 5;
   int v, kt;
@@ -68,32 +71,29 @@ __global__ __launch_bounds__(256, 2) void k_bwd_gemm(BwdArgs<uint16_t> a) {
   const uint16_t* wt = a.Wt + (size_t)v * Kp * Np + (size_t)k0 * Np;   // rows k0.., [k][n]
   const uint16_t* gr = a.Grows + a.gr_vs * v;                           // [b][n]
 
-  u32x4_t sa[UA], sb[UB];
-  auto load = [&](int nb) {
+  // Wave w loads rows 16j .. 16j+15 of each operand block for its j: load j,
+  // lane l -> LDS chunk 64 j + l = row 16 j + l / 4, stored chunk l % 4,
+  // which holds n chunk (l % 4) ^ ((row >> 1) & 3).
+  const uint32_t lds0 = lds_addr(lds);
+  const int wu = __builtin_amdgcn_readfirstlane(wave);
+  uint32_t offa[JA], offb[JB];
 #pragma unroll
-    for (int q = 0; q < UA; ++q) {
-      const int i = tid + 256 * q;
-      sa[q] = *reinterpret_cast<const u32x4_t*>(wt + (size_t)(i >> 2) * Np + nb * 32 + (i & 3) * 8);
-    }
+  for (int q = 0; q < JA; ++q) {
+    const int row = 16 * (JA * wave + q) + (lane >> 2);
+    offa[q] = (uint32_t)row * (uint32_t)Np * 2u + (uint32_t)(((lane & 3) ^ ((row >> 1) & 3)) * 16);
+  }
 #pragma unroll
-    for (int q = 0; q < UB; ++q) {
-      const int i = tid + 256 * q;
-      sb[q] = *reinterpret_cast<const u32x4_t*>(gr + (size_t)(i >> 2) * Np + nb * 32 + (i & 3) * 8);
-    }
-  };
-  auto store = [&](int buf) {
-    uint16_t* sA = lds + buf * Ly::stage;
-    uint16_t* sB = sA + Ly::a_elems;
+  for (int q = 0; q < JB; ++q) {
+    const int row = 16 * (JB * wave + q) + (lane >> 2);
+    offb[q] = (uint32_t)row * (uint32_t)Np * 2u + (uint32_t)(((lane & 3) ^ ((row >> 1) & 3)) * 16);
+  }
+  auto issue = [&](int nb) {                          // block nb into stage nb % 3: JA + JB loads
+    const uint32_t st = lds0 + (uint32_t)((nb % kStages) * Ly::stage);
 #pragma unroll
-    for (int q = 0; q < UA; ++q) {
-      const int i = tid + 256 * q;
-      *reinterpret_cast<u32x4_t*>(sA + (i >> 2) * kBS + (i & 3) * 8) = sa[q];
-    }
+    for (int q = 0; q < JA; ++q) dma16(wt, offa[q] + (uint32_t)nb * 64u, st + (uint32_t)((JA * wu + q) * 1024));
 #pragma unroll
-    for (int q = 0; q < UB; ++q) {
-      const int i = tid + 256 * q;
-      *reinterpret_cast<u32x4_t*>(sB + (i >> 2) * kBS + (i & 3) * 8) = sb[q];
-    }
+    for (int q = 0; q < JB; ++q)
+      dma16(gr, offb[q] + (uint32_t)nb * 64u, st + (uint32_t)(Ly::a_bytes + (JB * wu + q) * 1024));
   };
 
   const int kw = (wave & 1) * 64, bw = (wave >> 1) * (BP / 2);   // this wave's sub-tile
@@ -103,59 +103,111 @@ __global__ __launch_bounds__(256, 2) void k_bwd_gemm(BwdArgs<uint16_t> a) {
 #pragma unroll
     for (int jt = 0; jt < BTW; ++jt) acc[i][jt] = zero16();
 
-  load(0);
-  store(0);
+  // fragment rows kw + 32i + l32 (W^T) and bw + 32jt + l32 (G) all have
+  // (row >> 1) & 3 == (l32 >> 1) & 3
+  const int swz = (l32 >> 1) & 3;
+  issue(0);
+  if (nnb > 1) {
+    issue(1);
+    wait_vm<JA + JB>();
+  } else {
+    wait_vm<0>();
+  }
   __syncthreads();
   for (int nb = 0; nb < nnb; ++nb) {
-    const int buf = nb & 1;
-    if (nb + 1 < nnb) load(nb + 1);
-    const uint16_t* sA = lds + buf * Ly::stage + (kw + l32) * kBS + 8 * lh;
-    const uint16_t* sB = lds + buf * Ly::stage + Ly::a_elems + (bw + l32) * kBS + 8 * lh;
+    // the stage of block nb - 1 is free (every wave is past the barrier)
+    if (nb + 2 < nnb) issue(nb + 2);
+    const char* sA = lds + (nb % kStages) * Ly::stage + (size_t)(kw + l32) * 64;
+    const char* sB = lds + (nb % kStages) * Ly::stage + Ly::a_bytes + (size_t)(bw + l32) * 64;
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
+      const int co = 16 * ((2 * s + lh) ^ swz);
       u32x4_t fa[2], fb[BTW];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) fa[i] = *reinterpret_cast<const u32x4_t*>(sA + 32 * i * kBS + 16 * s);
+      for (int i = 0; i < 2; ++i) fa[i] = *reinterpret_cast<const u32x4_t*>(sA + 32 * i * 64 + co);
 #pragma unroll
-      for (int jt = 0; jt < BTW; ++jt) fb[jt] = *reinterpret_cast<const u32x4_t*>(sB + 32 * jt * kBS + 16 * s);
+      for (int jt = 0; jt < BTW; ++jt) fb[jt] = *reinterpret_cast<const u32x4_t*>(sB + 32 * jt * 64 + co);
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int jt = 0; jt < BTW; ++jt) acc[i][jt] = mma32(fa[i], fb[jt], acc[i][jt]);
     }
-    if (nb + 1 < nnb) store(buf ^ 1);                    // its old block was last read before the previous barrier
-    __syncthreads();
+    if (nb + 1 < nnb) {
+      // block nb + 1 has landed (block nb + 2 may not)
+      if (nb + 2 < nnb) wait_vm<JA + JB>();
+      else wait_vm<0>();
+      __syncthreads();
+    }
   }
 
-  // epilogue: lane l32 holds batch row bw + 32jt + l32, inputs k0 + kw + 32i + crow(r)
+  // epilogue: lane l32 holds batch row bw + 32jt + l32, inputs k0 + kw +
+  // 32i + crow(r).  The tile goes to LDS as bf16 rows [k][b] (stride BP + 8),
+  // then every thread takes 16-byte chunks of rows: ReLU' from the
+  // activations' columns [k][b] read 16 bytes at a time, and the gradient
+  // columns written 16 bytes at a time.  bf16 rounding commutes with the
+  // mask (bf16(0) = 0).
+  constexpr int ST = BP + 8;                             // staging row stride (elements)
+  static_assert((size_t)kBK * ST * 2 <= BwdLds<BP>::bytes, "staging fits the operand ring");
   const uint16_t* acv = a.Acols + a.ac_vs * v;
   uint16_t* gc = a.Gcols + a.gc_vs * v;
   uint16_t* go = a.Grows_out ? a.Grows_out + a.go_vs * v : nullptr;
+  uint16_t* stg = reinterpret_cast<uint16_t*>(lds);
+  __syncthreads();                                       // every wave is done with the operand ring
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int jt = 0; jt < BTW; ++jt) {
       const int b = bw + 32 * jt + l32;
-      float f[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int k = k0 + kw + 32 * i + crow(r, lane);
-        const float av = bf16_bits_to_f32(acv[(size_t)k * BP + b]);
-        f[r] = av > 0.0f ? acc[i][jt][r] : 0.0f;
-      }
       uint32_t pk[8];
-      to_bf16x2(f, pk);
+      {
+        float f[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int k = k0 + kw + 32 * i + crow(r, lane);
-        gc[(size_t)k * BP + b] = (uint16_t)(pk[r >> 1] >> (16 * (r & 1)));
+        for (int r = 0; r < 16; ++r) f[r] = acc[i][jt][r];
+        to_bf16x2(f, pk);
       }
-      if (go)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) stg[(kw + 32 * i + crow(r, lane)) * ST + b] = (uint16_t)(pk[r >> 1] >> (16 * (r & 1)));
+      if (go) {
+        // rows [b][k] keep the mask from the columns, two bytes per element
+        uint32_t mk[8];
+        {
+          float f[16];
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int k = k0 + kw + 32 * i + crow(r, lane);
+            f[r] = bf16_bits_to_f32(acv[(size_t)k * BP + b]) > 0.0f ? acc[i][jt][r] : 0.0f;
+          }
+          to_bf16x2(f, mk);
+        }
 #pragma unroll
         for (int q = 0; q < 4; ++q)                      // inputs 8q + 4lh + 0..3 are consecutive
           *reinterpret_cast<u32x2_t*>(go + (size_t)b * Kp + k0 + kw + 32 * i + 8 * q + 4 * lh) =
-              u32x2_t{pk[2 * q], pk[2 * q + 1]};
+              u32x2_t{mk[2 * q], mk[2 * q + 1]};
+      }
     }
+  __syncthreads();
+  constexpr int CPR = BP / 8;                            // 16-byte chunks per row
+  constexpr int NCH = kBK * CPR / 256;                   // chunks per thread
+  u32x4_t am[NCH];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int ci = tid + 256 * c, row = ci / CPR, b8 = (ci % CPR) * 8;
+    am[c] = *reinterpret_cast<const u32x4_t*>(acv + (size_t)(k0 + row) * BP + b8);
+  }
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int ci = tid + 256 * c, row = ci / CPR, b8 = (ci % CPR) * 8;
+    u32x4_t gv = *reinterpret_cast<const u32x4_t*>(stg + row * ST + b8);
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const uint32_t m = am[c][w];
+      uint32_t keep = 0;
+      if (bf16_bits_to_f32((uint16_t)(m & 0xffffu)) > 0.0f) keep |= 0xffffu;
+      if (bf16_bits_to_f32((uint16_t)(m >> 16)) > 0.0f) keep |= 0xffff0000u;
+      gv[w] &= keep;
+    }
+    *reinterpret_cast<u32x4_t*>(gc + (size_t)(k0 + row) * BP + b8) = gv;
+  }
   vt_add(a.vtime, v, vt0);
 }
 
