@@ -36,8 +36,8 @@ KERNEL_SOURCES = ["gevo_device.h", "gevo_internal.h", "gevo_kernels.hip", "gevo_
 KERNEL_KIND_OF = {"k_fused2": ("fused_train", None), "k_stream_layer": ("layer_train", "layer_fwd"),
                   "k_layer": ("layer_train", "layer_fwd"), "k_out_fwd": ("out_train", None),
                   "k_out_upd": ("out_train", None), "k_out": (None, "out_predict"),
-                  "k_bwd_gemm": ("bwd", None), "k_bwd": ("bwd", None), "k_pred_gemmILb1": (None, "fwd_out"),
-                  "k_pred_gemmILb0": (None, "layer_fwd"), "k_wt_bf16": (None, "weight_copy"),
+                  "k_bwd_gemm": ("bwd", None), "k_bwd": ("bwd", None), "k_pred_gemm<true>": (None, "fwd_out"),
+                  "k_pred_gemm<false>": (None, "layer_fwd"), "k_wt_bf16": (None, "weight_copy"),
                   "k_fwd_gemm": (None, "layer_fwd")}
 
 
@@ -246,6 +246,7 @@ def fold_traffic(cfg, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, comm
     """HBM bytes per launch of each kernel kind: FETCH_SIZE and WRITE_SIZE (KiB per
     dispatch) scaled by what the same counters read for a plain 1 GiB copy."""
     scale = copy_scales(copy_fetch_dir, copy_write_dir)
+    trains = cfg["epochs"] > 0 and not fused_workload(cfg)
     per = {}
     for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         groups = {}
@@ -253,24 +254,26 @@ def fold_traffic(cfg, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, comm
             stem = next((k for k in KERNEL_KIND_OF if k in name), None)
             if stem:
                 groups.setdefault((stem, grid), []).append(v)
-        trains = cfg["epochs"] > 0 and not fused_workload(cfg)
-        # the most frequent launch shape of a layer/output kernel is its training launch
+        # a training kernel runs every SGD step (once per hidden layer of its
+        # kind, one launch shape per layer); its prediction launches are a few
+        # per call: launch shapes with at least half the top count are training
         top = {}
         for (stem, grid), vals in groups.items():
-            if stem not in top or len(vals) > len(groups[(stem, top[stem])]):
-                top[stem] = grid
+            top[stem] = max(top.get(stem, 0), len(vals))
         for (stem, grid), vals in groups.items():
             tr_kind, pr_kind = KERNEL_KIND_OF[stem]
-            kind = tr_kind if (tr_kind and (stem == "k_fused2" or (trains and grid == top[stem]))) else pr_kind
+            is_train = tr_kind and (stem == "k_fused2" or (trains and 2 * len(vals) >= top[stem]))
+            kind = tr_kind if is_train else pr_kind
             if kind is None:
                 continue
-            cur = per.get(kind)
-            # a kernel kind launched with several grids: keep the most frequent launch shape
-            if cur is None or cur["grid"] == grid or len(vals) > cur["n"][counter]:
-                if cur is None or cur["grid"] != grid:
-                    cur = per[kind] = dict(grid=grid, n={"FETCH_SIZE": 0, "WRITE_SIZE": 0}, kib={})
-                cur["n"][counter] = len(vals)
-                cur["kib"][counter] = sum(vals) / len(vals)
+            # every launch of the kind: the average per launch, as the algorithmic bytes are
+            cur = per.setdefault(kind, dict(grids=set(), n={}, kib={}))
+            cur["grids"].add(grid)
+            cur["n"][counter] = cur["n"].get(counter, 0) + len(vals)
+            cur["kib"][counter] = cur["kib"].get(counter, 0.0) + sum(vals)
+    for r in per.values():
+        for c in r["kib"]:
+            r["kib"][c] /= r["n"][c]
     try:
         with open(TRAFFIC_FILE) as f:
             table = json.load(f)
@@ -281,7 +284,7 @@ def fold_traffic(cfg, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, comm
     for kind, r in per.items():
         if len(r["kib"]) != 2:
             continue
-        rec[kind] = dict(kernel_source_sha=sha, grid=r["grid"], dispatches=r["n"],
+        rec[kind] = dict(kernel_source_sha=sha, grids=sorted(r["grids"]), dispatches=r["n"],
                          fetch_kib_per_dispatch=round(r["kib"]["FETCH_SIZE"], 3),
                          write_kib_per_dispatch=round(r["kib"]["WRITE_SIZE"], 3),
                          fetch_scale=round(scale["FETCH_SIZE"], 4), write_scale=round(scale["WRITE_SIZE"], 4),
