@@ -662,9 +662,10 @@ __global__ __launch_bounds__(256) void k_out_fwd(OutArgs<S> a) {
 
 // Pass 2, one workgroup per (32-input column tile kt, variant): wave 0 forms
 // dW_L[c][k] = sum_b G[b][c] A[k][b] for the tile's 32 inputs and applies
-// the masked SGD update to those columns of the master; all four waves form
+// the masked SGD update to those columns of the master; waves 1-3 form
 // G_{L-1}[k][b] = (sum_c W_L[c][k] G[b][c]) * [A[k][b] > 0] for the same
-// inputs from the columns' pre-update values.  The kt == 0 workgroup also
+// inputs from the columns' pre-update values, one 32-row batch tile at a
+// time.  The kt == 0 workgroup also
 // updates the biases and adds the CE and hit sums, tiles in order.  Each
 // workgroup alone reads and writes its columns, so no other workgroup sees
 // a half-updated W_L.

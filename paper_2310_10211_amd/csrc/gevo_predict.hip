@@ -473,7 +473,8 @@ __global__ __launch_bounds__(kPT, 1) void k_pred_gemm(PredGemmArgs a) {
         for (int it = 0; it < 8; ++it) {
           const int row = 8 * it + (ln >> 3), c = ln & 7;
           const u32x4_t val = *reinterpret_cast<const u32x4_t*>(st + row * 128 + ((c ^ (row & 7)) << 4));
-          *reinterpret_cast<u32x4_t*>(Out + (size_t)(wm * 64 + row) * a.Np + wn * 128 + 64 * h + 8 * c) = val;
+          __builtin_nontemporal_store(val, reinterpret_cast<u32x4_t*>(Out + (size_t)(wm * 64 + row) * a.Np +
+                                                                      wn * 128 + 64 * h + 8 * c));
         }
       }
       vt_add(a.vtime, vdone, vt0);

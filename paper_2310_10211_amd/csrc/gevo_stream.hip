@@ -86,7 +86,7 @@ __global__ __launch_bounds__(kST, 1) void k_stream_layer(LayerArgs<uint16_t> a) 
     vt_add(a.vtime, v, vt0);
     return;
   }
-  const int Kp = a.Kp, Np = a.Np, nkb = Kp / 32;
+  const int Kp = a.Kp, Np = a.Np, nkb = Kp / 32, last = nkb - 1;
   // Each tile visits the k-blocks in its own rotated order, so that the
   // workgroups streaming at the same time read different lines of a shared
   // input rather than all the same ones (visit j is block phys(j)).
@@ -144,24 +144,24 @@ __global__ __launch_bounds__(kST, 1) void k_stream_layer(LayerArgs<uint16_t> a) 
   }
   const int grp = tile * (kSU / 32) + wave;            // this wave's 32-unit group
   const uint32_t ow = (uint32_t)((grp * 1024 + lane * 4) * 4), om = (uint32_t)(n * 4);
-  u32x4_t st[2 * XU];                                  // input staging: columns [0, XU), rows [XU, 2XU)
-  auto load_xc = [&](int j) {
-    if constexpr (UPD) {
-      const uint16_t* bc = acol + (size_t)phys(j) * 32 * BP;
-#pragma unroll
-      for (int q = 0; q < XU; ++q)
-        asm volatile("global_load_dwordx4 %0, %1, %2" : "=&v"(st[q]) : "v"(oc[q]), "s"(bc) : "memory");
+  // input staging, two register sets used alternately by even and odd
+  // visits: columns in [0, XU), rows in [XU, 2XU)
+  u32x4_t stE[2 * XU], stO[2 * XU];
+  // staging load i (0 <= i < NX: the column loads, then the row loads) of
+  // visit j: columns of visit j + 2, rows of visit j + 1 (clamped to the last
+  // visit, re-read in bounds and never used)
+  auto load_x1 = [&](int j, int i, u32x4_t (&st)[2 * XU]) {
+    const int jc = min(j + 2, last), jr = min(j + 1, last);
+    if (UPD && i < XU) {
+      const uint16_t* bc = acol + (size_t)phys(jc) * 32 * BP;
+      asm volatile("global_load_dwordx4 %0, %1, %2" : "=&v"(st[i]) : "v"(oc[i]), "s"(bc) : "memory");
+    } else if constexpr (FWD) {
+      const int q = UPD ? i - XU : i;
+      const uint16_t* br = arow + phys(jr) * 32;
+      asm volatile("global_load_dwordx4 %0, %1, %2" : "=&v"(st[XU + q]) : "v"(orr[q]), "s"(br) : "memory");
     }
   };
-  auto load_xr = [&](int j) {
-    if constexpr (FWD) {
-      const uint16_t* br = arow + phys(j) * 32;
-#pragma unroll
-      for (int q = 0; q < XU; ++q)
-        asm volatile("global_load_dwordx4 %0, %1, %2" : "=&v"(st[XU + q]) : "v"(orr[q]), "s"(br) : "memory");
-    }
-  };
-  auto store_xc = [&](int buf) {
+  auto store_xc = [&](int buf, const u32x4_t (&st)[2 * XU]) {
     if constexpr (UPD) {
 #pragma unroll
       for (int q = 0; q < XU; ++q) {
@@ -170,7 +170,7 @@ __global__ __launch_bounds__(kST, 1) void k_stream_layer(LayerArgs<uint16_t> a) 
       }
     }
   };
-  auto store_xr = [&](int buf) {
+  auto store_xr = [&](int buf, const u32x4_t (&st)[2 * XU]) {
     if constexpr (FWD) {
 #pragma unroll
       for (int q = 0; q < XU; ++q) {
@@ -215,7 +215,6 @@ __global__ __launch_bounds__(kST, 1) void k_stream_layer(LayerArgs<uint16_t> a) 
 #pragma unroll
   for (int T = 0; T < BT; ++T) z[T] = zero16();
   uint32_t pp[8];                                      // bf16 B operand of the previous visit
-  const int last = nkb - 1;
 
   // forward of the previous visit's block: rows 32T + l32 from buffer buf,
   // k = 16s2 + 4lh + {0..3, 8..11}, B operand from pp
@@ -237,19 +236,25 @@ __global__ __launch_bounds__(kST, 1) void k_stream_layer(LayerArgs<uint16_t> a) 
   };
 
   // Visit j: the weight gradient of block phys(j) (inputs in column buffer
-  // j&1), the forward of visit j-1 (rows in buffer (j-1)&1) while the update
-  // of visit j is applied, then the staged inputs (columns of j+1, rows of j)
-  // into LDS, barrier, and the staging loads (columns of j+2, rows of j+1)
-  // and master words of visit j+2 into the registers just consumed.  Vector
-  // memory operations retire in issue order: younger than visit j's master
-  // words are visit j-1's master stores (S), its staging loads (NX) and visit
-  // j+1's master words (NW); younger than the staging loads are visit j+1's
-  // master words and this visit's stores.
-  auto iter = [&](auto firstc, int j, f32x4_t (&w)[4], uint32_t& m) {
+  // j&1) with visit j's staging loads (columns of j+2, rows of j+1, into the
+  // register set of j's parity) spread between its MFMAs, the forward of
+  // visit j-1 (rows in buffer (j-1)&1) while the update of visit j is
+  // applied, the master stores of j and the master words of j+2 into the
+  // registers just consumed, then visit j-1's staged inputs (columns of j+1,
+  // rows of j) into LDS and a barrier.  Vector memory operations retire in
+  // issue order.  Younger than visit j's master words (issued by visit j-2)
+  // are visit j-1's staging loads (NX), master stores (S) and master words
+  // of j+1 (NW); younger than visit j-1's staging loads are visit j-1's
+  // stores and master words and visit j's staging loads, stores and master
+  // words.  (Younger transposed-copy stores only make a wait stricter.)
+  // For visit 0 the prologue issued the master words of 0, the staging
+  // loads of visit -1 and the master words of 1, in that order.
+  auto iter = [&](auto firstc, int j, f32x4_t (&w)[4], uint32_t& m, u32x4_t (&sx)[2 * XU],
+                  u32x4_t (&sy)[2 * XU]) {
     constexpr bool first = decltype(firstc)::value;
     asm volatile("s_waitcnt vmcnt(%5)"
                  : "+v"(w[0]), "+v"(w[1]), "+v"(w[2]), "+v"(w[3]), "+v"(m)
-                 : "n"((first ? 0 : S) + NX + NW)
+                 : "n"(first ? NX + NW : NX + S + NW)
                  : "memory");
     const int kb = phys(j);
     float wn[16];
@@ -259,8 +264,16 @@ __global__ __launch_bounds__(kST, 1) void k_stream_layer(LayerArgs<uint16_t> a) 
 #pragma unroll
       for (int s = 0; s < NBS; ++s) xa[s] = *reinterpret_cast<const u32x4_t*>(xcb + 16 * s);
       f32x16_t d = zero16();
+      // one staging load after every second MFMA (NX <= NBS / 2)
 #pragma unroll
-      for (int s = 0; s < NBS; ++s) d = mma32(xa[s], gs[s], d);
+      for (int s = 0; s < NBS; ++s) {
+        d = mma32(xa[s], gs[s], d);
+        if ((s & 1) && (s >> 1) < NX) {
+          __builtin_amdgcn_sched_barrier(0);
+          load_x1(j, s >> 1, sx);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
       if constexpr (FWD && !first) forward((j - 1) & 1);
       // masked update: a sign-extended mask bit selects the new value or +0
 #pragma unroll
@@ -274,53 +287,56 @@ __global__ __launch_bounds__(kST, 1) void k_stream_layer(LayerArgs<uint16_t> a) 
       for (int q = 0; q < 4; ++q)
         *reinterpret_cast<float4*>(wp + 256 * q) = make_float4(wn[4 * q], wn[4 * q + 1], wn[4 * q + 2], wn[4 * q + 3]);
     } else {
+#pragma unroll
+      for (int i = 0; i < NX; ++i) load_x1(j, i, sx);
       if constexpr (FWD && !first) forward((j - 1) & 1);
 #pragma unroll
       for (int r = 0; r < 16; ++r) wn[r] = w[r >> 2][r & 3];
     }
     to_bf16x2(wn, pp);
+    load_w(min(j + 2, last), w, m);                    // after the last use of this visit's words
     if (a.Wt) {                                        // transposed operand copy for the backward of the layer above
       uint16_t* wt = a.Wt + (size_t)v * Kp * Np + (size_t)(32 * kb) * Np + n;
 #pragma unroll
       for (int r = 0; r < 16; ++r)
         wt[(size_t)(8 * (r >> 2) + 4 * lh + (r & 3)) * Np] = (uint16_t)(pp[r >> 1] >> (16 * (r & 1)));
     }
-    asm volatile("s_waitcnt vmcnt(%0)" : : "n"(NW + S) : "memory");
+    asm volatile("s_waitcnt vmcnt(%0)" : : "n"(first ? NX + S + 2 * NW : NX + 2 * S + 2 * NW) : "memory");
 #pragma unroll
-    for (int q = 0; q < 2 * XU; ++q) asm volatile("" : "+v"(st[q]));
-    if (j < last) store_xc((j + 1) & 1);
-    store_xr(j & 1);
+    for (int q = 0; q < 2 * XU; ++q) asm volatile("" : "+v"(sy[q]));
+    if (j < last) store_xc((j + 1) & 1, sy);
+    store_xr(j & 1, sy);
     __syncthreads();
-    load_xc(min(j + 2, last));
-    load_xr(min(j + 1, last));
-    load_w(min(j + 2, last), w, m);
   };
 
-  // Prologue: the columns of visit 0 into LDS, then the staging loads of the
-  // first visit (columns of 1, rows of 0) and master visits 0 and 1 (past the
-  // end the last block is re-read in bounds and never used).
+  // Prologue: the columns of visit 0 into LDS, then the master words of
+  // visit 0, the staging loads of visit -1 (columns of 1, rows of 0) and the
+  // master words of visit 1 (past the end the last block is re-read in
+  // bounds and never used).
   f32x4_t wA[4], wB[4];
   uint32_t mA = 0u, mB = 0u;
-  load_xc(0);
+#pragma unroll
+  for (int i = 0; i < NX; ++i)
+    if (UPD && i < XU) load_x1(-2, i, stE);            // columns of visit 0
   load_w(0, wA, mA);
   asm volatile("s_waitcnt vmcnt(%0)" : : "n"(NW) : "memory");
 #pragma unroll
-  for (int q = 0; q < XU; ++q) asm volatile("" : "+v"(st[q]));
-  store_xc(0);
+  for (int q = 0; q < 2 * XU; ++q) asm volatile("" : "+v"(stE[q]));
+  store_xc(0, stE);
   __syncthreads();                                     // (the bias of this lane is read by this lane only)
   if (UPD && lh == 0) a.bias[(size_t)v * Np + n] = bias_n;
-  load_xc(min(1, last));
-  load_xr(0);
+#pragma unroll
+  for (int i = 0; i < NX; ++i) load_x1(-1, i, stO);   // columns of visit 1, rows of visit 0
   load_w(min(1, last), wB, mB);
   // whole pairs of visits (the block count is even): the register sets keep
   // their roles on every path, so no copy of a set in flight is ever needed
   const std::true_type first{};
   const std::false_type later{};
-  iter(first, 0, wA, mA);
-  iter(later, 1, wB, mB);
+  iter(first, 0, wA, mA, stE, stO);
+  iter(later, 1, wB, mB, stO, stE);
   for (int j = 2; j < nkb; j += 2) {
-    iter(later, j, wA, mA);
-    iter(later, j + 1, wB, mB);
+    iter(later, j, wA, mA, stE, stO);
+    iter(later, j + 1, wB, mB, stO, stE);
   }
   if constexpr (FWD) forward(last & 1);
   // the unused prefetches of the last visits land before their registers are reused
@@ -330,7 +346,7 @@ __global__ __launch_bounds__(kST, 1) void k_stream_layer(LayerArgs<uint16_t> a) 
                :
                : "memory");
 #pragma unroll
-  for (int q = 0; q < 2 * XU; ++q) asm volatile("" : "+v"(st[q]));
+  for (int q = 0; q < 2 * XU; ++q) asm volatile("" : "+v"(stE[q]), "+v"(stO[q]));
 
   if constexpr (FWD) {
     // bias, ReLU, bf16 rows [b][n] and columns [n][b]
