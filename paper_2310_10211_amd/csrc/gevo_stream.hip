@@ -54,7 +54,12 @@ struct StreamLds {                       // sizes in bf16 elements, two buffers 
   static constexpr int XC = BP + 8;      // input columns of a block [32][BP]
   static constexpr int rows = BP * XR;
   static constexpr int cols = 32 * XC;
-  static constexpr size_t bytes = (size_t)2 * (rows + cols) * 2;
+  // per wave, the block's transposed operand copy [32 k][32 n] on its way to
+  // global memory; a 40-element (80-byte) row stride puts the rows k and
+  // k + 4 that one 2-byte write instruction touches on different banks
+  static constexpr int TR = 40;
+  static constexpr int tcopy = kSW * 32 * TR;
+  static constexpr size_t bytes = ((size_t)2 * (rows + cols) + tcopy) * 2;
 };
 
 }  // namespace
@@ -73,6 +78,7 @@ __global__ __launch_bounds__(kST, 1) void k_stream_layer(LayerArgs<uint16_t> a) 
   uint16_t* xc = lds + 2 * Ly::rows;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, lh = lane >> 5;
+  uint16_t* tw = lds + 2 * (Ly::rows + Ly::cols) + wave * 32 * Ly::TR;   // this wave's transpose tile
   // the tiles of one variant share an XCD and its L2 (workgroup i runs on XCD i % 8)
   int v, tile;
   {
@@ -295,11 +301,23 @@ __global__ __launch_bounds__(kST, 1) void k_stream_layer(LayerArgs<uint16_t> a) 
     }
     to_bf16x2(wn, pp);
     load_w(min(j + 2, last), w, m);                    // after the last use of this visit's words
-    if (a.Wt) {                                        // transposed operand copy for the backward of the layer above
-      uint16_t* wt = a.Wt + (size_t)v * Kp * Np + (size_t)(32 * kb) * Np + n;
+    if (a.Wt) {
+      // transposed operand copy for the backward of the layer above: the
+      // wave's 32 inputs x 32 units go through its LDS tile [k][n], then out
+      // as 16-byte pieces of rows k (eight units each)
 #pragma unroll
       for (int r = 0; r < 16; ++r)
-        wt[(size_t)(8 * (r >> 2) + 4 * lh + (r & 3)) * Np] = (uint16_t)(pp[r >> 1] >> (16 * (r & 1)));
+        tw[(8 * (r >> 2) + 4 * lh + (r & 3)) * Ly::TR + l32] = (uint16_t)(pp[r >> 1] >> (16 * (r & 1)));
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");   // the other lanes' writes before the reads
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+      uint16_t* wt = a.Wt + (size_t)v * Kp * Np + (size_t)(32 * kb) * Np + (size_t)grp * 32 + 8 * (lane & 3);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int kk = 16 * h + (lane >> 2);
+        const u32x4_t t = *reinterpret_cast<const u32x4_t*>(tw + kk * Ly::TR + 8 * (lane & 3));
+        *reinterpret_cast<u32x4_t*>(wt + (size_t)kk * Np) = t;
+      }
     }
     asm volatile("s_waitcnt vmcnt(%0)" : : "n"(first ? NX + S + 2 * NW : NX + 2 * S + 2 * NW) : "memory");
 #pragma unroll
