@@ -21,12 +21,12 @@
 // tiles load and read alike.  Workgroups that share a weight tile (same
 // variant, all row tiles) run at the same time on one XCD (workgroup i runs
 // on XCD i mod 8).
-// Without the output layer one workgroup per CU runs its tiles back to back:
-// the next tile's first operand blocks load while the finished tile is
-// written out, and the stores drain while the next tile computes (all CUs
-// finish their tiles together, so a tile's 32 MB of output from the whole
-// chip would otherwise be written, and the next workgroups dispatched,
-// while no CU computes).
+// One workgroup per CU runs its tiles back to back: the next tile's first
+// operand blocks load while the finished tile is written out (or, with the
+// output layer, while its logits and losses are formed), and the stores
+// drain while the next tile computes (all CUs finish their tiles together,
+// so a tile's 32 MB of output from the whole chip would otherwise be
+// written, and the next workgroups dispatched, while no CU computes).
 #include "gevo_internal.h"
 #include "gevo_device.h"
 
@@ -49,18 +49,15 @@ constexpr int kPT = 512;                 // threads
 // row r stored at chunk c ^ ((r >> 1) & 7) (conflict-free operand reads)
 constexpr size_t kTileBytes = (size_t)kPM * kPK * 2;
 constexpr size_t kGemmLds = 5 * kTileBytes;            // two A buffers, then three W buffers (160 KiB)
-// output-layer epilogue: hidden tile [256][kHS] bf16, W_L operand [32][kHS] bf16, biases
+// The epilogues use buffers 1 and 4 while the next tile's first blocks load
+// into 0, 2 and 3.  Without the output layer each wave stages its rows in
+// 8 KB of buffer 1 or 4; with it, buffer 1 holds the output layer's bf16
+// operand [32 classes][kHS], its biases and the band sums, and buffer 4 the
+// partial logits of the four row bands ([2][16][64] fp32 each).
 constexpr int kHS = kPN + 8;
-constexpr size_t kOutH = 0;
-constexpr size_t kOutW = kOutH + (size_t)kPM * kHS * 2;
-constexpr size_t kOutB = kOutW + (size_t)32 * kHS * 2;
-constexpr size_t kOutRed = kOutB + 32 * 4;             // [8] fp64 loss sums, [8] hit counts
-constexpr size_t kOutEnd = kOutRed + 8 * 8 + 8 * 4;
-// the output-layer epilogue reuses (and extends) the operand buffers: H, W_L
-// and the sums; without the output layer each wave stages its rows in 8 KB of
-// buffer 1 or 4
-constexpr size_t kGemmOutLds = kOutEnd > kGemmLds ? kOutEnd : kGemmLds;
-static_assert(kGemmOutLds <= 160 * 1024 && kGemmLds <= 160 * 1024, "LDS of one CU");
+constexpr size_t kOutEnd = (size_t)32 * kHS * 2 + 32 * 4 + 4 * 8 + 4 * 4;
+static_assert(kOutEnd <= kTileBytes && 4 * 2 * 16 * 64 * 4 <= kTileBytes, "epilogue scratch fits buffers 1 and 4");
+static_assert(kGemmLds <= 160 * 1024, "LDS of one CU");
 
 __device__ __forceinline__ f32x16_t mma32(u32x4_t a, u32x4_t b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c,
@@ -76,9 +73,8 @@ __global__ __launch_bounds__(kPT, 1) void k_pred_gemm(PredGemmArgs a) {
   // Workgroup b runs on XCD b % 8 and serves the pairs with p % 8 == b % 8,
   // row tile fastest: its s-th tile is tm = b / 8 + s * (gridDim.x / 8) of
   // that XCD's sequence, so the row tiles of a pair are in flight together on
-  // one XCD and read its weight tile into that L2 once.  Without the output
-  // layer a launch holds one workgroup per CU that runs its tiles back to
-  // back; with it every workgroup runs one tile.
+  // one XCD and read its weight tile into that L2 once.  A launch holds one
+  // workgroup per CU that runs its tiles back to back.
   const int nr = a.R / kPM, nn = a.Np / kPN, npairs = a.P * nn;
   const int xcd = blockIdx.x & 7, nwx = (int)(gridDim.x >> 3);
   const int cnt = xcd < npairs ? ((npairs - 1 - xcd) / 8 + 1) * nr : 0;   // tiles of this XCD
@@ -177,30 +173,7 @@ __global__ __launch_bounds__(kPT, 1) void k_pred_gemm(PredGemmArgs a) {
   };
   // The tile is accumulated transposed (units x rows): lane l holds row
   // wm*64 + 32i + l%32 and, in registers 4q..4q+3, the four consecutive
-  // units wn*128 + 32t + 8q + 4(l/32) + 0..3.  bias + ReLU -> bf16 into the
-  // LDS rows dst[row][unit], one 8-byte write per four units.
-  auto tile_to_lds = [&](uint16_t* dst, int stride) {
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int u = wn * 128 + t * 32 + 8 * q + 4 * lh;
-        const float4 bn = *reinterpret_cast<const float4*>(a.bias + (size_t)v * a.Np + n0 + u);
-        const float bv[4] = {bn.x, bn.y, bn.z, bn.w};
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          float f[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float z = acc[i][t][4 * q + e] + bv[e];
-            f[e] = z > 0.0f ? z : 0.0f;
-          }
-          uint32_t pk[2];
-          to_bf16x2(f, pk);
-          *reinterpret_cast<uint2*>(dst + (size_t)(wm * 64 + i * 32 + l32) * stride + u) = make_uint2(pk[0], pk[1]);
-        }
-      }
-  };
+  // units wn*128 + 32t + 8q + 4(l/32) + 0..3.
 
   // a tile's first loads: A block 0, then W blocks 0 and 1 (eight loads each
   // in a loader wave), so a wait that leaves eight loads in flight covers
@@ -215,8 +188,7 @@ __global__ __launch_bounds__(kPT, 1) void k_pred_gemm(PredGemmArgs a) {
   // in place of A block nblk the tile's 256 biases go to LDS (one 1 KB
   // copy per wave, in the A buffer block nblk - 2 used)
   auto bias_to_lds = [&]() {
-    if constexpr (!OUT)
-      dma16(a.bias + (size_t)v * a.Np + n0, (uint32_t)lane * 16u, lds0 + (uint32_t)abuf(nblk) + (uint32_t)wu * 1024u);
+    dma16(a.bias + (size_t)v * a.Np + n0, (uint32_t)lane * 16u, lds0 + (uint32_t)abuf(nblk) + (uint32_t)wu * 1024u);
   };
   prologue();
   if (nblk > 1) wait_vm<8>();
@@ -315,22 +287,59 @@ __global__ __launch_bounds__(kPT, 1) void k_pred_gemm(PredGemmArgs a) {
 
     if constexpr (OUT) {
       // The layer is one tile wide (Np == 256): the tile holds whole rows of
-      // the last hidden activation.  H = bf16(relu(Z + b)) goes to LDS as
-      // [row][unit]; the output layer's weights as the bf16 operand [class][unit].
+      // the last hidden activation, and the output layer runs on it here.
+      // H = bf16(relu(Z + b)) stays in registers as the operand of the
+      // logits MFMAs: register 4q + e of accumulator (i, t) is unit
+      // wn*128 + 32t + 8q + 4(l/32) + e of row wm*64 + 32i + l%32, so
+      // registers 8s'..8s'+7 of (i, t) contract over the units
+      // 32t + 16s' + {4(l/32) + 0..3, 8 + 4(l/32) + 0..3} of the wave's band,
+      // and the output layer's bf16 weights are read from LDS in the same
+      // order.  Each wave sums the logits over its 128 units; the two waves
+      // of a row band add theirs in LDS.
+      const size_t bslot = abuf(nblk) + (size_t)wave * 1024;
+      wait_vm<0>();
+      // lane-dependent offsets come from an opaque lane id, formed per tile
+      // rather than held (and spilled) across the tile loop
+      const int ln = opaque(lane), le32 = ln & 31, leh = ln >> 5;
+      u32x4_t hf[2][4][2];
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 bn =
+              *reinterpret_cast<const float4*>(smem + bslot + (size_t)(wn * 128 + t * 32 + 8 * q + 4 * leh) * 4);
+          const float bv[4] = {bn.x, bn.y, bn.z, bn.w};
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+            float f[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float z = acc[i][t][4 * q + e] + bv[e];
+              f[e] = z > 0.0f ? z : 0.0f;
+            }
+            uint32_t pk[2];
+            to_bf16x2(f, pk);
+            hf[i][t][q >> 1][2 * (q & 1)] = pk[0];
+            hf[i][t][q >> 1][2 * (q & 1) + 1] = pk[1];
+          }
+        }
       __syncthreads();                                   // every wave is done with the operand buffers
-      uint16_t* H = reinterpret_cast<uint16_t*>(smem + kOutH);
-      uint16_t* WL = reinterpret_cast<uint16_t*>(smem + kOutW);
-      float* bL = reinterpret_cast<float*>(smem + kOutB);
-      double* red_ce = reinterpret_cast<double*>(smem + kOutRed);
-      unsigned int* red_hit = reinterpret_cast<unsigned int*>(smem + kOutRed + 8 * 8);
-      tile_to_lds(H, kHS);                               // n0 == 0: the layer is this one tile
-      // output layer master, k-blocked [Np/32][32 classes][32 inputs]: thread tid
-      // converts class tid / 8, inputs 32 (tid % 8) .. +31
+      // the output layer's operand [class][unit] (bf16) and biases into
+      // buffer 1, the row labels of this wave's band into registers: every
+      // load the compiler waits on completes before the next tile's
+      // direct-to-LDS loads go out
+      uint16_t* WL = reinterpret_cast<uint16_t*>(smem + kTileBytes);
+      float* bL = reinterpret_cast<float*>(smem + kTileBytes + (size_t)32 * kHS * 2);
+      double* red_ce = reinterpret_cast<double*>(smem + kTileBytes + (size_t)32 * kHS * 2 + 32 * 4);
+      unsigned int* red_hit = reinterpret_cast<unsigned int*>(red_ce + 4);
+      float* red = reinterpret_cast<float*>(smem + 4 * kTileBytes) + (size_t)wm * 2048;   // [2][16][64] per band
       {
+        // master k-blocked [Np/32][32 classes][32 inputs]: thread tid converts
+        // class tid / 8, inputs 32 (tid % 8) .. +31, half (tid >> 8)
         const float* WLm = a.WL + (size_t)v * 32 * kPN;
         const int c = (tid >> 3) & 31, kb = tid & 7, q0 = (tid >> 8) * 2;
         const float* src = WLm + ((size_t)kb * 32 + c) * 32;
-  #pragma unroll
+#pragma unroll
         for (int q = q0; q < q0 + 2; ++q) {
           const float4 f0 = *reinterpret_cast<const float4*>(src + 8 * q);
           const float4 f1 = *reinterpret_cast<const float4*>(src + 8 * q + 4);
@@ -341,76 +350,109 @@ __global__ __launch_bounds__(kPT, 1) void k_pred_gemm(PredGemmArgs a) {
         }
         if (tid < 32) bL[tid] = a.bL[(size_t)v * 32 + tid];
       }
+      int ylab[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) ylab[i] = a.labels[r0 + wm * 64 + 32 * i + le32];
+      asm volatile("" : "+v"(ylab[0]), "+v"(ylab[1]));     // the label loads complete here
       __syncthreads();
-      // logits^T of 32 rows per tile: lane holds row l32 and classes crow(r) of
-      // its half; the row's other half is in lane ^ 32
-      const int C = a.C;
-      double ce_sum = 0.0;
-      unsigned int hits = 0;
-  #pragma unroll
-      for (int tt = 0; tt < 1; ++tt) {
-        const int rl = wave * 32;                      // first row of the tile (in the workgroup)
-        f32x16_t z0 = zero16(), z1 = zero16();
-  #pragma unroll
-        for (int s = 0; s < kPN / 16; s += 2) {
-          z0 = mma32(*reinterpret_cast<const u32x4_t*>(WL + l32 * kHS + 16 * s + 8 * lh),
-                     *reinterpret_cast<const u32x4_t*>(H + (rl + l32) * kHS + 16 * s + 8 * lh), z0);
-          z1 = mma32(*reinterpret_cast<const u32x4_t*>(WL + l32 * kHS + 16 * s + 16 + 8 * lh),
-                     *reinterpret_cast<const u32x4_t*>(H + (rl + l32) * kHS + 16 * s + 16 + 8 * lh), z1);
-        }
-        const int y = a.labels[r0 + rl + l32];
-        float z[16];
-        float m = -INFINITY, bv = -INFINITY;
-        int bi = 64, nanl = 0;
-  #pragma unroll
-        for (int r = 0; r < 16; ++r) {                 // r ascending = class ascending within the lane
-          const int c = crow(r, lane);
-          z[r] = (z0[r] + z1[r]) + bL[c];
-          if (c < C) {
-            m = fmaxf(m, z[r]);
-            if (z[r] != z[r]) nanl = 1;
-            else if (z[r] > bv) { bv = z[r]; bi = c; }
+      const int vcur = v, rtcur = rt;
+      const bool more = tm + nwx < cnt;
+      if (more) {                                        // the next tile's first blocks into buffers 0, 2, 3
+        tm += nwx;
+        set_tile(tm);
+        sA = a.A + a.a_vs * v + (size_t)r0 * Kp;
+        sW = a.W + ((size_t)v * a.Np + n0) * Kp;
+        prologue();
+      }
+      f32x16_t lg[2] = {zero16(), zero16()};
+      {
+        const uint16_t* wrow = WL + le32 * kHS + wn * 128 + 4 * leh;
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+          for (int s2 = 0; s2 < 2; ++s2) {
+            const uint2 lo = *reinterpret_cast<const uint2*>(wrow + 32 * t + 16 * s2);
+            const uint2 hi = *reinterpret_cast<const uint2*>(wrow + 32 * t + 16 * s2 + 8);
+            const u32x4_t wf = u32x4_t{lo.x, lo.y, hi.x, hi.y};
+#pragma unroll
+            for (int i = 0; i < 2; ++i) lg[i] = mma32(wf, hf[i][t][s2], lg[i]);
+          }
+      }
+      if (wn == 1) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) red[(i * 16 + r) * 64 + ln] = lg[i][r];
+      }
+      __syncthreads();
+      if (wn == 0) {
+        // logits^T of the band's rows: lane holds row 32i + l32 and classes
+        // crow(r) of its half; the row's other half is in lane ^ 32
+        const int C = a.C;
+        double ce_sum = 0.0;
+        unsigned int hits = 0;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const int y = ylab[i];
+          float z[16];
+          float m = -INFINITY, bv = -INFINITY;
+          int bi = 64, nanl = 0;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {               // r ascending = class ascending within the lane
+            const int c = crow(r, ln);
+            z[r] = (lg[i][r] + red[(i * 16 + r) * 64 + ln]) + bL[c];
+            if (c < C) {
+              m = fmaxf(m, z[r]);
+              if (z[r] != z[r]) nanl = 1;
+              else if (z[r] > bv) { bv = z[r]; bi = c; }
+            }
+          }
+          m = fmaxf(m, __shfl_xor(m, 32));
+          nanl |= __shfl_xor(nanl, 32);
+          {
+            const float ov = __shfl_xor(bv, 32);
+            const int oi = __shfl_xor(bi, 32);
+            if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+          }
+          float sl = 0.0f, zy = 0.0f;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int c = crow(r, ln);
+            if (c < C) sl += expf(z[r] - m);
+            if (c == y) zy = z[r];
+          }
+          const float s = sl + __shfl_xor(sl, 32);
+          zy += __shfl_xor(zy, 32);                    // exactly one lane of the pair holds class y
+          float ce = (logf(s) + m) - zy;
+          if (nanl) ce = NAN;
+          if (leh == 0 && y >= 0) {
+            ce_sum += (double)ce;
+            hits += (!nanl && bi == y) ? 1u : 0u;
           }
         }
-        m = fmaxf(m, __shfl_xor(m, 32));
-        nanl |= __shfl_xor(nanl, 32);
-        {
-          const float ov = __shfl_xor(bv, 32);
-          const int oi = __shfl_xor(bi, 32);
-          if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+#pragma unroll
+        for (int off = 16; off >= 1; off >>= 1) {      // lanes 0..31 hold the rows; fixed order
+          ce_sum += __shfl_xor(ce_sum, off);
+          hits += __shfl_xor(hits, off);
         }
-        float sl = 0.0f, zy = 0.0f;
-  #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int c = crow(r, lane);
-          if (c < C) sl += expf(z[r] - m);
-          if (c == y) zy = z[r];
-        }
-        const float s = sl + __shfl_xor(sl, 32);
-        zy += __shfl_xor(zy, 32);                      // exactly one lane of the pair holds class y
-        float ce = (logf(s) + m) - zy;
-        if (nanl) ce = NAN;
-        if (lh == 0 && y >= 0) {
-          ce_sum += (double)ce;
-          hits += (!nanl && bi == y) ? 1u : 0u;
-        }
+        if (lane == 0) { red_ce[wm] = ce_sum; red_hit[wm] = hits; }
       }
-  #pragma unroll
-      for (int off = 16; off >= 1; off >>= 1) {        // lanes 0..31 hold the rows; fixed order
-        ce_sum += __shfl_xor(ce_sum, off);
-        hits += __shfl_xor(hits, off);
-      }
-      if (lane == 0) { red_ce[wave] = ce_sum; red_hit[wave] = hits; }
       __syncthreads();
       if (tid == 0) {
         double t = 0.0;
-        unsigned int h = 0;
-        for (int w = 0; w < 8; ++w) { t += red_ce[w]; h += red_hit[w]; }
-        a.part_ce[(size_t)v * a.n_chunks_total + a.chunk0 + rt] = t;
-        a.part_correct[(size_t)v * a.n_chunks_total + a.chunk0 + rt] = h;
+        unsigned int hsum = 0;
+        for (int w = 0; w < 4; ++w) { t += red_ce[w]; hsum += red_hit[w]; }
+        a.part_ce[(size_t)vcur * a.n_chunks_total + a.chunk0 + rtcur] = t;
+        a.part_correct[(size_t)vcur * a.n_chunks_total + a.chunk0 + rtcur] = hsum;
       }
-      vt_add(a.vtime, v, vt0);
-      return;
+      vt_add(a.vtime, vcur, vt0);
+      if (!more) return;
+      // the next tile's A and W block 0 have landed (W block 1 and this
+      // tile's last stores may stay in flight)
+      if (nblk > 1) wait_vm<8>();
+      else wait_vm<0>();
+      zero_tail(0);
+      __syncthreads();
     } else {
       // The tile's biases (in LDS since the last block began) are added to
       // the accumulators (lane: units wn*128 + 32t + 8q + 4(l/32) + 0..3);
@@ -537,7 +579,7 @@ static int device_cus() {
 
 template <bool OUT>
 static hipError_t launch_pg(const PredGemmArgs& a, hipStream_t s, const LaunchEv& ev) {
-  constexpr size_t lds = OUT ? kGemmOutLds : kGemmLds;
+  constexpr size_t lds = kGemmLds;
   static bool attr = false;
   if (!attr) {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pred_gemm<OUT>),
@@ -546,11 +588,9 @@ static hipError_t launch_pg(const PredGemmArgs& a, hipStream_t s, const LaunchEv
   }
   const int64_t pairs = (int64_t)a.P * (a.Np / kPN);
   int64_t per_xcd = (pairs + 7) / 8 * (a.R / kPM);      // tiles of the busiest XCD
-  if (!OUT) {                                            // one workgroup per CU, tiles back to back
-    const int cus = device_cus();
-    if (cus < 8) return hipErrorInvalidDevice;
-    if (per_xcd > cus / 8) per_xcd = cus / 8;
-  }
+  const int cus = device_cus();                          // one workgroup per CU, tiles back to back
+  if (cus < 8) return hipErrorInvalidDevice;
+  if (per_xcd > cus / 8) per_xcd = cus / 8;
   hipExtLaunchKernelGGL((k_pred_gemm<OUT>), dim3((unsigned)(8 * per_xcd)), dim3(kPT), lds, s, ev.start, ev.stop, 0,
                         a);
   return hipGetLastError();
