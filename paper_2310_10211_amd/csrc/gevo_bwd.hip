@@ -87,13 +87,15 @@ __global__ __launch_bounds__(256, 2) void k_bwd_gemm(BwdArgs<uint16_t> a) {
     const int row = 16 * (JB * wave + q) + (lane >> 2);
     offb[q] = (uint32_t)row * (uint32_t)Np * 2u + (uint32_t)(((lane & 3) ^ ((row >> 1) & 3)) * 16);
   }
-  auto issue = [&](int nb) {                          // block nb into stage nb % 3: JA + JB loads
+  // load j of block nb (j < JA: W^T rows, else G rows) into stage nb % 3
+  auto issue1 = [&](int nb, int j) {
     const uint32_t st = lds0 + (uint32_t)((nb % kStages) * Ly::stage);
+    if (j < JA) dma16(wt, offa[j] + (uint32_t)nb * 64u, st + (uint32_t)((JA * wu + j) * 1024));
+    else dma16(gr, offb[j - JA] + (uint32_t)nb * 64u, st + (uint32_t)(Ly::a_bytes + (JB * wu + j - JA) * 1024));
+  };
+  auto issue = [&](int nb) {                          // block nb into stage nb % 3: JA + JB loads
 #pragma unroll
-    for (int q = 0; q < JA; ++q) dma16(wt, offa[q] + (uint32_t)nb * 64u, st + (uint32_t)((JA * wu + q) * 1024));
-#pragma unroll
-    for (int q = 0; q < JB; ++q)
-      dma16(gr, offb[q] + (uint32_t)nb * 64u, st + (uint32_t)(Ly::a_bytes + (JB * wu + q) * 1024));
+    for (int j = 0; j < JA + JB; ++j) issue1(nb, j);
   };
 
   const int kw = (wave & 1) * 64, bw = (wave >> 1) * (BP / 2);   // this wave's sub-tile
@@ -115,8 +117,10 @@ __global__ __launch_bounds__(256, 2) void k_bwd_gemm(BwdArgs<uint16_t> a) {
   }
   __syncthreads();
   for (int nb = 0; nb < nnb; ++nb) {
-    // the stage of block nb - 1 is free (every wave is past the barrier)
-    if (nb + 2 < nnb) issue(nb + 2);
+    // Block nb + 2 goes into the stage of block nb - 1 (free: every wave is
+    // past the barrier), one load after every second MFMA rather than all
+    // at once, where the wave would wait at issue for the load path.
+    const bool ld = nb + 2 < nnb;
     const char* sA = lds + (nb % kStages) * Ly::stage + (size_t)(kw + l32) * 64;
     const char* sB = lds + (nb % kStages) * Ly::stage + Ly::a_bytes + (size_t)(bw + l32) * 64;
 #pragma unroll
@@ -130,7 +134,16 @@ __global__ __launch_bounds__(256, 2) void k_bwd_gemm(BwdArgs<uint16_t> a) {
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int jt = 0; jt < BTW; ++jt) acc[i][jt] = mma32(fa[i], fb[jt], acc[i][jt]);
+        for (int jt = 0; jt < BTW; ++jt) {
+          acc[i][jt] = mma32(fa[i], fb[jt], acc[i][jt]);
+          constexpr int kPer = 2 * BTW;                  // MFMAs per contraction step
+          const int m = s * kPer + i * BTW + jt;         // a constant after unrolling
+          if ((m & 1) && (m >> 1) < JA + JB) {
+            __builtin_amdgcn_sched_barrier(0);
+            if (ld) issue1(nb + 2, m >> 1);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        }
     }
     if (nb + 1 < nnb) {
       // block nb + 1 has landed (block nb + 2 may not)
