@@ -551,8 +551,14 @@ __global__ __launch_bounds__(256) void k_out_fwd(OutArgs<S> a) {
         const int j = j0 + u * 256;
         if (j < 32 * q) {
           S* dst = wop + ((j / 8) % 32) * WS + (j / 256) * 32 + (j % 8) * 4;   // row (j/8)%32, chunk j/256
-          dst[0] = O::from_f32(w4[u].x); dst[1] = O::from_f32(w4[u].y);
-          dst[2] = O::from_f32(w4[u].z); dst[3] = O::from_f32(w4[u].w);
+          if constexpr (sizeof(S) == 2) {                 // four bf16 in one 8-byte write (WS * 2 is a multiple of 16)
+            const uint32_t lo = (uint32_t)O::from_f32(w4[u].x) | (uint32_t)O::from_f32(w4[u].y) << 16;
+            const uint32_t hi = (uint32_t)O::from_f32(w4[u].z) | (uint32_t)O::from_f32(w4[u].w) << 16;
+            *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
+          } else {
+            dst[0] = O::from_f32(w4[u].x); dst[1] = O::from_f32(w4[u].y);
+            dst[2] = O::from_f32(w4[u].z); dst[3] = O::from_f32(w4[u].w);
+          }
         }
       }
     }
@@ -563,6 +569,16 @@ __global__ __launch_bounds__(256) void k_out_fwd(OutArgs<S> a) {
   const S* wr = wop + l32 * WS + lh * KE;
   f32x16_t acc0 = zero16(), acc1 = zero16();
   int st = s0;
+  for (; st + 8 <= s1; st += 8) {                      // eight row loads in flight
+    F x[8], w[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) { x[u] = O::load(ar + (st + u) * KM); w[u] = O::load(wr + (st + u) * KM); }
+#pragma unroll
+    for (int u = 0; u < 8; u += 2) {
+      acc0 = O::mma(w[u], x[u], acc0);
+      acc1 = O::mma(w[u + 1], x[u + 1], acc1);
+    }
+  }
   for (; st + 4 <= s1; st += 4) {
     F x[4], w[4];
 #pragma unroll
@@ -721,16 +737,25 @@ __global__ __launch_bounds__(256) void k_out_upd(OutArgs<S> a) {
       if (i < nvec) {
         const S* e = reinterpret_cast<const S*>(&gv[u]);
         const int row = (i * PER) >> 5, col = (i * PER) & 31;
+        if constexpr (sizeof(S) == 2) {
+          *reinterpret_cast<uint4*>(gs + row * GSTR + col) = gv[u];   // GSTR * 2 = 80 bytes: 16-byte aligned
+        } else {
 #pragma unroll
-        for (int j = 0; j < PER; ++j) {
-          gs[row * GSTR + col + j] = e[j];
-          gT[(col + j) * BT + row] = e[j];
+          for (int j = 0; j < PER; ++j) gs[row * GSTR + col + j] = e[j];
         }
+#pragma unroll
+        for (int j = 0; j < PER; ++j) gT[(col + j) * BT + row] = e[j];
       }
     }
     // k-blocked master tile [c][32 k]: thread t holds class t / 8, inputs 4 (t % 8) .. +3
     S* wd = wold + (threadIdx.x >> 3) * WSTR + (threadIdx.x & 7) * 4;
-    wd[0] = O::from_f32(wv.x); wd[1] = O::from_f32(wv.y); wd[2] = O::from_f32(wv.z); wd[3] = O::from_f32(wv.w);
+    if constexpr (sizeof(S) == 2) {                     // WSTR * 2 = 80 bytes: 8-byte aligned pieces
+      const uint32_t lo = (uint32_t)O::from_f32(wv.x) | (uint32_t)O::from_f32(wv.y) << 16;
+      const uint32_t hi = (uint32_t)O::from_f32(wv.z) | (uint32_t)O::from_f32(wv.w) << 16;
+      *reinterpret_cast<uint2*>(wd) = make_uint2(lo, hi);
+    } else {
+      wd[0] = O::from_f32(wv.x); wd[1] = O::from_f32(wv.y); wd[2] = O::from_f32(wv.z); wd[3] = O::from_f32(wv.w);
+    }
   }
   __syncthreads();
   if (kt == 0) {
