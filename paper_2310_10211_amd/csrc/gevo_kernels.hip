@@ -193,9 +193,17 @@ __global__ __launch_bounds__(256, 2) void k_layer(LayerArgs<S> a) {
       a.bias[(size_t)v * Np + n0 + nl] = bn;
       bias_l[nl] = bn;
     }
-    const S* gp = G + (size_t)(n0 + l32) * a.Bp + lh * KE;
+    if constexpr (sizeof(S) == 4) {
+      // fp32: contraction step s2 pairs batch rows s2 (lanes 0-31) and
+      // Bp/2 + s2 (lanes 32-63), so a lane's operands are contiguous
+      const S* gp = G + (size_t)(n0 + l32) * a.Bp + lh * (a.Bp / 2);
 #pragma unroll
-    for (int s2 = 0; s2 < NG; ++s2) gf[s2] = s2 < nsteps ? O::load(gp + s2 * KM) : F{};
+      for (int s2 = 0; s2 < NG; ++s2) gf[s2] = s2 < nsteps ? gp[s2] : F{};
+    } else {
+      const S* gp = G + (size_t)(n0 + l32) * a.Bp + lh * KE;
+#pragma unroll
+      for (int s2 = 0; s2 < NG; ++s2) gf[s2] = s2 < nsteps ? O::load(gp + s2 * KM) : F{};
+    }
   } else if (threadIdx.x < 32) {
     bias_l[threadIdx.x] = a.bias[(size_t)v * Np + n0 + threadIdx.x];
   }
@@ -231,12 +239,27 @@ __global__ __launch_bounds__(256, 2) void k_layer(LayerArgs<S> a) {
           for (int u = 0; u < 4; ++u) nx[u] = *reinterpret_cast<const float4*>(wptr(c + 4) + 4 * u);
           nmw = mrow[c + 4];
         }
-        const S* ap = acb + (size_t)c * 32 * a.Bp;
         f32x16_t d0 = zero16(), d1 = zero16();
+        if constexpr (sizeof(S) == 4) {
+          // batch rows s2 and Bp/2 + s2 as above: four steps per 16-byte load
+          const float* ap = a.Acols + v * a.ac_vs + (size_t)(kb0 + c * 32 + l32) * a.Bp + lh * (a.Bp / 2);
 #pragma unroll
-        for (int s2 = 0; s2 < NG; s2 += 2) {
-          if (s2 < nsteps) d0 = O::mma(gf[s2], O::load(ap + s2 * KM), d0);
-          if (s2 + 1 < nsteps) d1 = O::mma(gf[s2 + 1], O::load(ap + (s2 + 1) * KM), d1);
+          for (int s4 = 0; s4 < NG; s4 += 4)
+            if (s4 < nsteps) {
+              const float4 x = *reinterpret_cast<const float4*>(ap + s4);
+              d0 = O::mma(gf[s4], x.x, d0);
+              d1 = O::mma(gf[s4 + 1], x.y, d1);
+              d0 = O::mma(gf[s4 + 2], x.z, d0);
+              d1 = O::mma(gf[s4 + 3], x.w, d1);
+              if ((s4 & 15) == 12) __builtin_amdgcn_sched_barrier(0);   // at most four loads ahead
+            }
+        } else {
+          const S* ap = acb + (size_t)c * 32 * a.Bp;
+#pragma unroll
+          for (int s2 = 0; s2 < NG; s2 += 2) {
+            if (s2 < nsteps) d0 = O::mma(gf[s2], O::load(ap + s2 * KM), d0);
+            if (s2 + 1 < nsteps) d1 = O::mma(gf[s2 + 1], O::load(ap + (s2 + 1) * KM), d1);
+          }
         }
 #pragma unroll
         for (int r = 0; r < 16; ++r) dws[crow(r, lane) * DSTR + l32] = d0[r] + d1[r];
@@ -313,6 +336,22 @@ __global__ __launch_bounds__(256, 2) void k_layer(LayerArgs<S> a) {
       const S* ar = a.Arows + v * a.ar_vs + (size_t)(row0 + tile * 32 + l32) * Kp + kb0 + lh * KE;
       const S* br = wt + l32 * WS + lh * KE;
       int k = 0;
+      if constexpr (sizeof(S) == 4) {
+        // fp32: within each 16 inputs, step u pairs inputs u (lanes 0-31) and
+        // 8 + u (lanes 32-63), so a lane's row operands are two 16-byte loads
+        const float* ar8 = a.Arows + v * a.ar_vs + (size_t)(row0 + tile * 32 + l32) * Kp + kb0 + 8 * lh;
+        const float* br8 = wt + l32 * WS + 8 * lh;
+        for (; k + 16 <= kw; k += 16) {
+          const float4 x0 = *reinterpret_cast<const float4*>(ar8 + k);
+          const float4 x1 = *reinterpret_cast<const float4*>(ar8 + k + 4);
+          const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+          for (int u = 0; u < 8; u += 2) {
+            acc[ti][0] = O::mma(xs[u], br8[k + u], acc[ti][0]);
+            acc[ti][1] = O::mma(xs[u + 1], br8[k + u + 1], acc[ti][1]);
+          }
+        }
+      }
       for (; k + 4 * KM <= kw; k += 4 * KM) {
         F x[4], w[4];
 #pragma unroll
