@@ -177,8 +177,21 @@ __global__ __launch_bounds__(256, 2) void k_layer(LayerArgs<S> a) {
 
   F gf[NG];
   if (a.do_update) {
-    // bias gradient of the 32 units: 8 lanes per unit, fixed-order reduction
     const S* G = a.Gcols + v * a.g_vs;
+    // the gradient operand of dW first, so its loads are in flight with the
+    // bias gradient's (the bias store below would otherwise hold them back)
+    if constexpr (sizeof(S) == 4) {
+      // fp32: contraction step s2 pairs batch rows s2 (lanes 0-31) and
+      // Bp/2 + s2 (lanes 32-63), so a lane's operands are contiguous
+      const S* gp = G + (size_t)(n0 + l32) * a.Bp + lh * (a.Bp / 2);
+#pragma unroll
+      for (int s2 = 0; s2 < NG; ++s2) gf[s2] = s2 < nsteps ? gp[s2] : F{};
+    } else {
+      const S* gp = G + (size_t)(n0 + l32) * a.Bp + lh * KE;
+#pragma unroll
+      for (int s2 = 0; s2 < NG; ++s2) gf[s2] = s2 < nsteps ? O::load(gp + s2 * KM) : F{};
+    }
+    // bias gradient of the 32 units: 8 lanes per unit, fixed-order reduction
     const int nl = threadIdx.x >> 3, seg = threadIdx.x & 7, per = a.Bp / 8;
     const S* gr = G + (size_t)(n0 + nl) * a.Bp + seg * per;
     float s = 0.0f;
@@ -192,17 +205,6 @@ __global__ __launch_bounds__(256, 2) void k_layer(LayerArgs<S> a) {
       const float bn = bk ? __fsub_rn(bo, __fmul_rn(lrv, s)) : 0.0f;
       a.bias[(size_t)v * Np + n0 + nl] = bn;
       bias_l[nl] = bn;
-    }
-    if constexpr (sizeof(S) == 4) {
-      // fp32: contraction step s2 pairs batch rows s2 (lanes 0-31) and
-      // Bp/2 + s2 (lanes 32-63), so a lane's operands are contiguous
-      const S* gp = G + (size_t)(n0 + l32) * a.Bp + lh * (a.Bp / 2);
-#pragma unroll
-      for (int s2 = 0; s2 < NG; ++s2) gf[s2] = s2 < nsteps ? gp[s2] : F{};
-    } else {
-      const S* gp = G + (size_t)(n0 + l32) * a.Bp + lh * KE;
-#pragma unroll
-      for (int s2 = 0; s2 < NG; ++s2) gf[s2] = s2 < nsteps ? O::load(gp + s2 * KM) : F{};
     }
   } else if (threadIdx.x < 32) {
     bias_l[threadIdx.x] = a.bias[(size_t)v * Np + n0 + threadIdx.x];
