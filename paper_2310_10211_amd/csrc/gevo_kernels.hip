@@ -610,6 +610,23 @@ __global__ __launch_bounds__(256) void k_out_fwd(OutArgs<S> a) {
   const S* wr = wop + l32 * WS + lh * KE;
   f32x16_t acc0 = zero16(), acc1 = zero16();
   int st = s0;
+  if constexpr (sizeof(S) == 4) {
+    // fp32: within each 16 inputs, step u pairs inputs u (lanes 0-31) and
+    // 8 + u (lanes 32-63): a lane's row operands are two 16-byte loads
+    const float* ar8 = a.Arows + v * a.ar_vs + (size_t)(tile * 32 + l32) * Kp + 8 * lh;
+    const float* wr8 = wop + l32 * WS + 8 * lh;
+    for (; st + 8 <= s1; st += 8) {
+      const int k = st * KM;                             // a multiple of 8 (Kp is a multiple of 32)
+      const float4 x0 = *reinterpret_cast<const float4*>(ar8 + k);
+      const float4 x1 = *reinterpret_cast<const float4*>(ar8 + k + 4);
+      const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+      for (int u = 0; u < 8; u += 2) {
+        acc0 = O::mma(wr8[k + u], xs[u], acc0);
+        acc1 = O::mma(wr8[k + u + 1], xs[u + 1], acc1);
+      }
+    }
+  }
   for (; st + 8 <= s1; st += 8) {                      // eight row loads in flight
     F x[8], w[8];
 #pragma unroll
@@ -752,10 +769,22 @@ __global__ __launch_bounds__(256) void k_out_upd(OutArgs<S> a) {
   uint32_t mw = 0;
   float* Wmv = a.Wm + (size_t)v * 32 * Kp;
   if (wave == 0) {
-    const S* ap = Acv + (size_t)(kt * 32 + l32) * a.Bp + lh * KE;
+    if constexpr (sizeof(S) == 4) {
+      // fp32: step s2 pairs batch rows s2 (lanes 0-31) and Bp/2 + s2 (lanes
+      // 32-63), so a lane's operands are contiguous: four per 16-byte load
+      const float* ap = Acv + (size_t)(kt * 32 + l32) * a.Bp + lh * (a.Bp / 2);
 #pragma unroll
-    for (int s2 = 0; s2 < NG; ++s2)
-      if (s2 < nsteps) af[s2] = O::load(ap + s2 * KM);
+      for (int s4 = 0; s4 < NG; s4 += 4)
+        if (s4 < nsteps) {
+          const float4 x = *reinterpret_cast<const float4*>(ap + s4);
+          af[s4] = x.x; af[s4 + 1] = x.y; af[s4 + 2] = x.z; af[s4 + 3] = x.w;
+        }
+    } else {
+      const S* ap = Acv + (size_t)(kt * 32 + l32) * a.Bp + lh * KE;
+#pragma unroll
+      for (int s2 = 0; s2 < NG; ++s2)
+        if (s2 < nsteps) af[s2] = O::load(ap + s2 * KM);
+    }
 #pragma unroll
     for (int u = 0; u < 4; ++u) w4[u] = *reinterpret_cast<const float4*>(Wmv + ((size_t)kt * 32 + rn) * 32 + cs + 4 * u);
     mw = a.mask[(size_t)v * 32 * (Kp / 32) + (size_t)rn * (Kp / 32) + kt];
@@ -821,7 +850,10 @@ __global__ __launch_bounds__(256) void k_out_upd(OutArgs<S> a) {
     f32x16_t d = zero16();
 #pragma unroll
     for (int s2 = 0; s2 < NG; ++s2)
-      if (s2 < nsteps) d = O::mma(O::load(&gT[l32 * BT + s2 * KM + lh * KE]), af[s2], d);
+      if (s2 < nsteps) {
+        const int b = sizeof(S) == 4 ? lh * (a.Bp / 2) + s2 : s2 * KM + lh * KE;   // the pairing of af
+        d = O::mma(O::load(&gT[l32 * BT + b]), af[s2], d);
+      }
 #pragma unroll
     for (int r = 0; r < 16; ++r) stg[crow(r, lane) * 36 + l32] = d[r];
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
