@@ -271,7 +271,7 @@ def _tie_params(dims, v_bias):
 
 
 @pytest.mark.parametrize("i,dims", [
-    (3, [784, 256, 10]),            # bf16: prediction GEMM + output kernel
+    (3, [784, 256, 10]),            # bf16: prediction GEMM with the output layer fused
     (5, [1024, 256, 128, 10]),      # bf16, three layers
     (2, [784, 96, 10]),             # fp32
     (1, [256, 10]),                 # fp32, output layer only (784 fp32 inputs exceed its LDS tile)
